@@ -1,0 +1,295 @@
+"""Float64 CPU oracle of the BCMT token-mixing layer (forward and backward).
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, plainly written reference
+that the HIP implementation is checked against.  Only the test suite, the
+smoke check and the CPU-baseline leg of the benchmark may import it; the
+product path never does, and this module imports nothing from the product
+package.
+
+Every function follows "BCMT: Blockwise Causal Memory Transformer"
+(arXiv 2608.13578).  Section numbers below are the paper's.
+
+Notation (the paper overloads two letters, so they are renamed here):
+  * the memory decay, written alpha in Sec. 3.5, is ``gamma`` here;
+  * the pooling softmax weights, also written alpha in Sec. 3.4, are ``a``;
+  * ``h`` is the number of heads and ``dh = D / h`` the head width (Sec. 3.3);
+  * ``Hloc`` is the local representation H of Sec. 3.3 (the paper reuses H).
+
+Readings of points the paper leaves open (all listed in the design notes):
+  * no biases anywhere (none appear in any equation of Sec. 3.3-3.8);
+  * the causal mask of Sec. 3.3 keeps the diagonal (a token attends to itself
+    and to earlier tokens of its block, Sec. 3.6) and is applied by exclusion;
+  * the pooling softmax of Sec. 3.4 runs over all tokens of a block (the
+    one-block shift of Sec. 3.5 is what keeps the layer causal);
+  * a partial last block (Sec. 3.2) gets attention, pooling and broadcast over
+    its own tokens only;
+  * gamma = 0 uses 0**0 = 1, so the memory equals the block's own summary;
+  * the residual form Y = X + layer(X) exists only for stacking layers; the
+    paper's layer output is exactly Y = H + G * M_tokens (Sec. 3.8);
+  * the paper states no backward pass; the one here is derived by hand and
+    pinned by finite differences in the tests.
+
+Parity status: forward pinned by library attention (dense / block-diagonal
+causal), closed forms of the memory normaliser, convexity, gamma limits,
+HOnly / W_m = 0 and W_g = 0 identities, and causality; backward pinned by
+central finite differences.  End-to-end values beyond those pins have no
+printed worked example in the paper ("parity unpinned" beyond the pins).
+"""
+
+import numpy as np
+
+PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
+
+
+def n_blocks(T, L):
+    """Number of blocks, the ceiling of T / L (Sec. 3.2)."""
+    return -(-T // L)
+
+
+def block_ranges(T, L):
+    """Contiguous, non-overlapping [start, end) token ranges (Sec. 3.2)."""
+    return [(s, min(s + L, T)) for s in range(0, T, L)]
+
+
+def sigmoid(u):
+    """Logistic sigmoid (Sec. 3.8), evaluated without overflow."""
+    out = np.empty_like(u)
+    pos = u >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-u[pos]))
+    e = np.exp(u[~pos])
+    out[~pos] = e / (1.0 + e)
+    return out
+
+
+def softmax_last(z):
+    """Max-subtracted softmax over the last axis."""
+    z = z - z.max(axis=-1, keepdims=True)
+    e = np.exp(z)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def memory_weights(n, gamma):
+    """Row-normalised weights of the exponential causal memory (Sec. 3.5).
+
+    A[i, j] = gamma**(i-j) / sum_{j'<=i} gamma**(i-j') for j <= i, else 0, so
+    that M = A @ S.  Each row is a convex combination.  Indices are 0-based.
+    Also returns the unnormalised weights and their row sums.
+    """
+    i = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    lower = j <= i
+    expo = np.where(lower, i - j, 0)
+    w = np.where(lower, np.power(float(gamma), expo), 0.0)  # 0**0 == 1
+    z = w.sum(axis=1)
+    return w / z[:, None], w, z
+
+
+def exp_memory(S, gamma):
+    """M^(i) = sum_{j<=i} gamma^(i-j) S^(j) / sum_{j<=i} gamma^(i-j) (Sec. 3.5).
+
+    S: [..., N_b, D] block summaries.  Written as the literal double sum, each
+    memory vector touching only the summaries j <= i.
+    """
+    n = S.shape[-2]
+    A, _, _ = memory_weights(n, gamma)
+    M = np.empty_like(S)
+    for i in range(n):
+        M[..., i, :] = np.einsum("j,...jd->...d", A[i, :i + 1], S[..., :i + 1, :])
+    return M
+
+
+def block_causal_attention(Q, K, V, L, h):
+    """Dense causal multi-head attention confined to each block (Sec. 3.3, 3.6).
+
+    Q, K, V: [B, T, D].  Head i uses columns i*dh .. (i+1)*dh-1.  Within a
+    block, query t sees keys u of the same block with u <= t.  Returns the
+    concatenated head outputs [B, T, D] and the attention probabilities of
+    every block, list of [B, h, Lb, Lb].
+    """
+    B, T, D = Q.shape
+    dh = D // h
+    out = np.zeros_like(Q)
+    probs = []
+    for s, e in block_ranges(T, L):
+        n = e - s
+        q = Q[:, s:e].reshape(B, n, h, dh).transpose(0, 2, 1, 3)
+        k = K[:, s:e].reshape(B, n, h, dh).transpose(0, 2, 1, 3)
+        v = V[:, s:e].reshape(B, n, h, dh).transpose(0, 2, 1, 3)
+        z = q @ k.transpose(0, 1, 3, 2) / np.sqrt(dh)
+        keep = np.tril(np.ones((n, n), dtype=bool))
+        z = np.where(keep, z, -np.inf)  # excluded entries, whatever their value
+        A = softmax_last(z)
+        probs.append(A)
+        o = A @ v
+        out[:, s:e] = o.transpose(0, 2, 1, 3).reshape(B, n, D)
+    return out, probs
+
+
+def forward(X, P, L, h, gamma, residual=False):
+    """One BCMT token-mixing layer, X [B, T, D] -> Y [B, T, D] (Sec. 3.2-3.8).
+
+    P: dict of float64 weights Wq, Wk, Wv, Wo, Wm, Wg [D, D] (input-major, so
+    that y = x @ W) and wp [D].  Returns (Y, cache) with every intermediate.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    B, T, D = X.shape
+    nb = n_blocks(T, L)
+    blk = np.arange(T) // L
+
+    # Sec. 3.3: per-head projections and block-local causal attention.
+    Q = X @ P["Wq"]
+    K = X @ P["Wk"]
+    V = X @ P["Wv"]
+    Hcat, probs = block_causal_attention(Q, K, V, L, h)
+    # Sec. 3.3: head concatenation and output projection; blocks concatenated.
+    Hloc = Hcat @ P["Wo"]
+
+    # Sec. 3.4: pooling scores, per-block softmax, adaptive summaries.
+    s = Hloc @ P["wp"]                       # [B, T]
+    a = np.zeros_like(s)
+    S = np.zeros((B, nb, D))
+    for i, (b0, b1) in enumerate(block_ranges(T, L)):
+        a[:, b0:b1] = softmax_last(s[:, b0:b1])
+        S[:, i] = np.einsum("bt,btd->bd", a[:, b0:b1], Hloc[:, b0:b1])
+
+    # Sec. 3.5: normalised exponential memory, projection, one-block shift.
+    M = exp_memory(S, gamma)
+    Mproj = M @ P["Wm"]
+    Mcausal = np.zeros_like(Mproj)
+    Mcausal[:, 1:] = Mproj[:, :-1]
+
+    # Sec. 3.7: broadcast to tokens; Sec. 3.8: gate and injection.
+    Mtok = Mcausal[:, blk]                   # [B, T, D]
+    U = Hloc @ P["Wg"]
+    G = sigmoid(U)
+    Y = Hloc + G * Mtok
+    if residual:
+        Y = Y + X
+    cache = dict(X=X, P=P, L=L, h=h, gamma=float(gamma), residual=residual,
+                 Q=Q, K=K, V=V, probs=probs, Hcat=Hcat, Hloc=Hloc, s=s, a=a,
+                 S=S, M=M, Mproj=Mproj, Mcausal=Mcausal, U=U, G=G)
+    return Y, cache
+
+
+def backward(cache, dY):
+    """Gradients of sum(dY * Y) for the layer of ``forward``.
+
+    The paper gives no backward pass; this is the chain rule applied to the
+    forward steps in reverse order.  Weight gradients are summed over the
+    batch.  Returns a dict with dX, dWq, dWk, dWv, dWo, dWm, dWg, dwp, dgamma.
+    """
+    c = cache
+    P, L, h, gamma = c["P"], c["L"], c["h"], c["gamma"]
+    X, Hloc, G, Mcausal = c["X"], c["Hloc"], c["G"], c["Mcausal"]
+    dY = np.asarray(dY, dtype=np.float64)
+    B, T, D = X.shape
+    nb = n_blocks(T, L)
+    blk = np.arange(T) // L
+    ranges = block_ranges(T, L)
+
+    # Gate and injection: Y = Hloc + G * Mtok, G = sigmoid(Hloc @ Wg).
+    dH = dY.copy()
+    dG = dY * Mcausal[:, blk]
+    dU = dG * G * (1.0 - G)
+    dMtok = dY * G
+    dWg = np.einsum("btd,bte->de", Hloc, dU)
+    dH += dU @ P["Wg"].T
+    # Broadcast: each block's memory vector is summed over its tokens.
+    dMcausal = np.zeros((B, nb, D))
+    for i, (b0, b1) in enumerate(ranges):
+        dMcausal[:, i] = dMtok[:, b0:b1].sum(axis=1)
+
+    # Shift and projection: Mcausal[i] = Mproj[i-1], Mproj = M @ Wm.
+    dMproj = np.zeros_like(dMcausal)
+    dMproj[:, :-1] = dMcausal[:, 1:]
+    dWm = np.einsum("bid,bie->de", c["M"], dMproj)
+    dM = dMproj @ P["Wm"].T
+
+    # Memory M = A(gamma) @ S with A the normalised decay weights.
+    A, w, z = memory_weights(nb, gamma)
+    dS = np.einsum("ij,bid->bjd", A, dM)
+    i_idx = np.arange(nb)[:, None]
+    j_idx = np.arange(nb)[None, :]
+    dist = i_idx - j_idx
+    lower = dist >= 0
+    # d/dgamma of gamma**(i-j): (i-j) * gamma**(i-j-1), zero on the diagonal.
+    dw = np.where(dist >= 1, dist * np.power(float(gamma), np.where(dist >= 1, dist - 1, 0)), 0.0)
+    dw = np.where(lower, dw, 0.0)
+    dz = dw.sum(axis=1)
+    dA = (dw - A * dz[:, None]) / z[:, None]
+    dgamma = float(np.einsum("ij,bid,bjd->", dA, dM, c["S"]))
+
+    # Pooling: S_i = sum_t a_t Hloc[t], a = softmax(Hloc @ wp) per block.
+    dwp = np.zeros(D)
+    for i, (b0, b1) in enumerate(ranges):
+        a = c["a"][:, b0:b1]                          # [B, n]
+        Hb = Hloc[:, b0:b1]                           # [B, n, D]
+        da = np.einsum("bd,btd->bt", dS[:, i], Hb)
+        ds = a * (da - np.einsum("bt,bt->b", a, da)[:, None])
+        dH[:, b0:b1] += a[:, :, None] * dS[:, i][:, None, :] + ds[:, :, None] * P["wp"]
+        dwp += np.einsum("bt,btd->d", ds, Hb)
+
+    # Output projection: Hloc = Hcat @ Wo.
+    dWo = np.einsum("btd,bte->de", c["Hcat"], dH)
+    dHcat = dH @ P["Wo"].T
+
+    # Block-local causal attention, per block and head.
+    dh = D // h
+    dQ = np.zeros_like(X)
+    dK = np.zeros_like(X)
+    dV = np.zeros_like(X)
+    for bi, (b0, b1) in enumerate(ranges):
+        n = b1 - b0
+        Ab = c["probs"][bi]                           # [B, h, n, n]
+
+        def heads(M_):
+            return M_[:, b0:b1].reshape(B, n, h, dh).transpose(0, 2, 1, 3)
+
+        q, k, v, do = heads(c["Q"]), heads(c["K"]), heads(c["V"]), heads(dHcat)
+        dv = Ab.transpose(0, 1, 3, 2) @ do
+        dA_ = do @ v.transpose(0, 1, 3, 2)
+        dz_ = Ab * (dA_ - (dA_ * Ab).sum(axis=-1, keepdims=True))
+        dq = dz_ @ k / np.sqrt(dh)
+        dk = dz_.transpose(0, 1, 3, 2) @ q / np.sqrt(dh)
+
+        def unheads(m):
+            return m.transpose(0, 2, 1, 3).reshape(B, n, D)
+
+        dQ[:, b0:b1] = unheads(dq)
+        dK[:, b0:b1] = unheads(dk)
+        dV[:, b0:b1] = unheads(dv)
+
+    # Q/K/V projections.
+    dWq = np.einsum("btd,bte->de", X, dQ)
+    dWk = np.einsum("btd,bte->de", X, dK)
+    dWv = np.einsum("btd,bte->de", X, dV)
+    dX = dQ @ P["Wq"].T + dK @ P["Wk"].T + dV @ P["Wv"].T
+    if c["residual"]:
+        dX = dX + dY
+    return dict(dX=dX, dWq=dWq, dWk=dWk, dWv=dWv, dWo=dWo, dWm=dWm, dWg=dWg,
+                dwp=dwp, dgamma=dgamma)
+
+
+def stack_forward(X, layers, L, h, gamma, residual=True):
+    """A stack of layers, X_{l+1} = X_l + layer_l(X_l) when ``residual``."""
+    caches = []
+    for P in layers:
+        X, cache = forward(X, P, L, h, gamma, residual=residual)
+        caches.append(cache)
+    return X, caches
+
+
+def stack_backward(caches, dY):
+    """Backward through ``stack_forward``; returns dX and per-layer grads.
+
+    dgamma of each layer is reported separately (each layer has its own decay
+    input, even when all share one value).
+    """
+    grads = []
+    g = dY
+    for cache in reversed(caches):
+        gr = backward(cache, g)
+        grads.append(gr)
+        g = gr["dX"]
+    grads.reverse()
+    return g, grads
