@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Throughput of the BCMT token-mixing layer (forward + backward) on one MI355X.
+
+One step = bcmt_layer_forward + bcmt_layer_backward (input gradient and all
+weight and decay gradients) over one batch of synthetic inputs already
+resident in HBM.  The workload is the GPT-2-small-shaped layer at the paper's
+maximum context: B=8, T=1024, D=768, H=12 heads of 64, block L=128, bf16
+storage with float32 accumulation, activations N(0,1), weights N(0, 0.02^2).
+
+Prints one JSON line.  `value` is layer tokens/s = B*T / (time per step).
+`roofline` describes the stage with the largest GPU time, measured with HIP
+events around each launch in a second pass of the same steps (library stage
+tracing).  `cpu_baseline` is the float64 CPU oracle timed on a bounded sample
+of the same workload.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = dict(B=8, T=1024, D=768, H=12, L=128, gamma=0.8, dtype="bf16")
+PEAK = {"mfma_bf16_tflops": 2500.0, "mfma_f32_tflops": 157.3, "hbm_gbs": 8000.0}
+
+
+def stage_work(name, B, T, D, H, L, es):
+    """Algorithmic work of one launch of a stage: (bound, amount, unit).
+
+    Matrix stages count 2 flops per multiply-add of the defining product;
+    attention counts only the causal pairs of each block; bandwidth stages
+    count the bytes each must read and write once."""
+    nb = -(-T // L)
+    BT = B * T
+    pairs = 0
+    for s in range(0, T, L):
+        n = min(L, T - s)
+        pairs += n * (n + 1) // 2
+    pairs *= B
+    nch = -(-min(L, T) // 32)
+    gemm = {
+        "fwd.qkv_gemm": 6 * BT * D * D, "fwd.wo_gemm": 2 * BT * D * D,
+        "fwd.wm_gemm": 2 * B * nb * D * D, "fwd.gate_gemm": 2 * BT * D * D,
+        "bwd.wg_wgrad_gemm": 2 * BT * D * D, "bwd.wm_dgrad_gemm": 2 * B * nb * D * D,
+        "bwd.wm_wgrad_gemm": 2 * B * nb * D * D, "bwd.wg_dgrad_gemm": 2 * BT * D * D,
+        "bwd.wo_dgrad_gemm": 2 * BT * D * D, "bwd.wo_wgrad_gemm": 2 * BT * D * D,
+        "bwd.qkv_dgrad_gemm": 6 * BT * D * D, "bwd.qkv_wgrad_gemm": 6 * BT * D * D,
+        # QK^T and PV over causal pairs (forward); the backward recomputes
+        # QK^T twice and forms dP twice, dV, dK and dQ.
+        "fwd.attention": 4 * 64 * H * pairs,
+        "bwd.attention_dq": 6 * 64 * H * pairs,
+        "bwd.attention_dkdv": 8 * 64 * H * pairs,
+    }
+    if name in gemm:
+        return "mfma", gemm[name], "flop"
+    act = BT * D * es
+    hbm = {
+        "fwd.pool": act + BT * 4 + B * nb * nch * (D + 2) * 4,
+        "fwd.scan": B * nb * nch * (D + 2) * 4 + B * nb * D * (4 + 4 + es) + B * nb * 8,
+        "bwd.gate": 3 * act + B * nb * D * (4 + es),
+        "bwd.memory_scan": B * nb * D * 12,
+        "bwd.pool": act + BT * 12 + B * nb * D * 8,
+        "bwd.zero_grads": (6 * D * D + D + 1) * 4,
+    }
+    return "hbm", hbm.get(name, 0), "byte"
+
+
+def layer_flops(B, T, D, H, L):
+    """Algorithmic forward flops of one layer (projections + causal pairs)."""
+    nb = -(-T // L)
+    pairs = sum(min(L, T - s) * (min(L, T - s) + 1) // 2 for s in range(0, T, L)) * B
+    return 10 * B * T * D * D + 2 * B * (nb - 1) * D * D + 4 * 64 * H * pairs
+
+
+def cpu_baseline(seconds_target=12.0):
+    """The float64 oracle on a bounded sample of the workload (host cores)."""
+    import numpy as np
+    from oracle import bcmt_oracle as orc
+    from paper_2608_13578_amd.inputs import make_layer_inputs, make_upstream_grad, to_f64
+    w = WORKLOAD
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(i.get("num_threads", 0) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    cores = threads or len(os.sched_getaffinity(0))
+
+    def run(bs):
+        X, [W] = make_layer_inputs(bs, w["T"], w["D"], seed=0, bf16=True)
+        dY = make_upstream_grad(bs, w["T"], w["D"], seed=1, bf16=True)
+        t0 = time.perf_counter()
+        Y, cache = orc.forward(X.astype(np.float64), to_f64(W), w["L"], w["H"], w["gamma"])
+        orc.backward(cache, dY.astype(np.float64))
+        return time.perf_counter() - t0
+
+    t1 = run(1)
+    bs = max(1, min(w["B"], int(seconds_target / max(t1, 1e-3))))
+    t = run(bs) if bs > 1 else t1
+    return {"value": round(bs * w["T"] / t, 1), "unit": "tokens/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{bs} of the {w['B']} sequences (T={w['T']}, D={w['D']}, H={w['H']}, "
+                      f"L={w['L']}), float64 forward+backward, {t:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer's multi-GPU sharding is a design, not an implementation)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_13578_amd import bcmt as abi
+    from paper_2608_13578_amd.inputs import make_layer_inputs, make_upstream_grad
+    from paper_2608_13578_amd.layer import LayerBuffers, to_device
+
+    if not os.path.exists(abi.LIB_PATH):
+        from paper_2608_13578_amd.build import build
+        build()
+    w = WORKLOAD
+    B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
+    dt = w["dtype"]
+    torch.cuda.set_device(0)
+    X, [W] = make_layer_inputs(B, T, D, seed=0, bf16=True)
+    dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
+    lb = LayerBuffers(B, T, D, H, L, gamma=w["gamma"], dtype=dt)
+    lb.set_params(W)
+    Xd, dYd = to_device(X, dt), to_device(dY, dt)
+    Yd, dXd = lb.new_activation(), lb.new_activation()
+    grads = lb.new_grads()
+
+    def step():
+        lb.forward(Xd, Yd)
+        lb.backward(Xd, dYd, dXd, grads)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    tokens = B * T
+    value = tokens / (ms / 1e3)
+
+    # Second pass with per-launch events: per-stage GPU time.
+    abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    stages = abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(False)
+    es = 2 if dt == "bf16" else 4
+    rows = []
+    for name, calls, total in stages:
+        bound, amount, unit = stage_work(name, B, T, D, H, L, es)
+        avg_ms = total / calls
+        rate = amount / (avg_ms / 1e3)
+        rows.append((name, calls // args.steps, avg_ms, total / args.steps, bound, amount, rate))
+    traced_ms = sum(r[3] for r in rows)
+    print(f"{'stage':24s} {'launch/step':>11s} {'avg us':>9s} {'share':>6s}  achieved", file=sys.stderr)
+    for name, per, avg_ms, per_step, bound, amount, rate in rows:
+        ach = f"{rate / 1e12:8.1f} TFLOP/s" if bound == "mfma" else f"{rate / 1e9:8.1f} GB/s"
+        print(f"{name:24s} {per:11d} {avg_ms * 1e3:9.2f} {per_step / traced_ms:6.1%}  {ach}",
+              file=sys.stderr)
+    print(f"untraced step {ms * 1e3:.1f} us; traced sum of stages {traced_ms * 1e3:.1f} us",
+          file=sys.stderr)
+    dom = max(rows, key=lambda r: r[3])
+    name, per, avg_ms, per_step, bound, amount, rate = dom
+    if bound == "mfma":
+        peak = PEAK["mfma_bf16_tflops"] if dt == "bf16" else PEAK["mfma_f32_tflops"]
+        roof = {"bound": "mfma", "kernel": name, "achieved": round(rate / 1e12, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(rate / 1e12 / peak, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "kernel": name, "achieved": round(rate / 1e9, 1),
+                "peak": PEAK["hbm_gbs"], "unit": "GB/s",
+                "frac": round(rate / 1e9 / PEAK["hbm_gbs"], 4), "traffic": None}
+    roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
+    roof["work_per_launch"] = amount
+    fl = 3 * layer_flops(B, T, D, H, L)
+
+    out = {
+        "metric": "BCMT layer tokens/s (fwd+bwd) at T=1024 bf16",
+        "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": dt, "data": "synthetic",
+        "config": {"workload": "bcmt-layer fwd+bwd B=8 T=1024 D=768 H=12x64 L=128 bf16",
+                   "B": B, "T": T, "D": D, "H": H, "L": L, "gamma": w["gamma"]},
+        "layer_mfma_frac": round(fl / (ms / 1e3) / 1e12 / PEAK["mfma_bf16_tflops"], 4),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

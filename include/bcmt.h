@@ -1,0 +1,170 @@
+/*
+ * bcmt.h - C ABI of the BCMT token-mixing layer on AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the one of "BCMT: Blockwise Causal Memory Transformer"
+ * (arXiv 2608.13578), Sec. 3.2-3.8.  For an input X of B sequences, T
+ * tokens and D features it computes, per sequence:
+ *
+ *   blocks     : N_b = ceil(T / L) contiguous blocks of at most L tokens
+ *                (Sec. 3.2; the last block may be shorter);
+ *   local MHA  : Q = X Wq, K = X Wk, V = X Wv; per head (D = H * 64) and per
+ *                block, softmax(Q K^T / sqrt(64) + causal mask) V, where a
+ *                token sees itself and earlier tokens of its own block only
+ *                (Sec. 3.3, 3.6); heads concatenated, H = concat * Wo;
+ *   summaries  : s = H wp, a = softmax of s over each block's tokens,
+ *                S_i = sum_t a_t H[t] (Sec. 3.4);
+ *   memory     : M_i = sum_{j<=i} g^(i-j) S_j / sum_{j<=i} g^(i-j), with the
+ *                decay g in [0, 1) (written alpha in Sec. 3.5, fixed to 0.8
+ *                there); P_i = M_i Wm; shifted by one block, C_1 = 0 and
+ *                C_i = P_{i-1} (Sec. 3.5);
+ *   injection  : every token of block i receives C_i (Sec. 3.7);
+ *                G = sigmoid(H Wg), Y = H + G * C (Sec. 3.8).
+ * With BCMT_FLAG_RESIDUAL the output is X + Y instead (for stacking layers;
+ * the paper's layer output is Y).  There are no biases.
+ *
+ * Conventions
+ *   - All tensors are row-major and live in device memory owned by the
+ *     caller; the library allocates nothing and keeps no state between calls.
+ *   - Activations X, Y, dY, dX are [B, T, D]; weights Wq, Wk, Wv, Wo, Wm, Wg
+ *     are [D, D] input-major (y = x W; a torch Linear weight is the
+ *     transpose), wp is [D].  They all have the element type cfg->dtype.
+ *   - Weight and decay gradients are float32, with the same shapes.
+ *   - Every pointer must be 16-byte aligned.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL means the default
+ *     stream) in order; nothing synchronises the host.
+ *   - The GPU path needs a head width D / H of 64 and D <= 2048.
+ *
+ * Errors
+ *   Negative return values are bcmt_status codes.  All checks on the
+ *   arguments happen before anything is enqueued, so BCMT_ERR_INVALID,
+ *   BCMT_ERR_UNSUPPORTED and BCMT_ERR_WORKSPACE mean that nothing ran.
+ *   BCMT_ERR_HIP reports a failed kernel launch; kernels enqueued before it
+ *   may have run.
+ */
+#ifndef BCMT_H_
+#define BCMT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BCMT_OK = 0,
+  BCMT_ERR_INVALID = -1,     /* null or misaligned pointer, bad sizes, decay outside [0,1) */
+  BCMT_ERR_UNSUPPORTED = -2, /* valid layer the GPU path does not run (head width != 64, D > 2048) */
+  BCMT_ERR_WORKSPACE = -3,   /* workspace smaller than bcmt_workspace_bytes() */
+  BCMT_ERR_HIP = -4          /* a HIP launch failed */
+} bcmt_status;
+
+typedef enum { BCMT_F32 = 0, BCMT_BF16 = 1 } bcmt_dtype;
+
+enum {
+  BCMT_FLAG_RESIDUAL = 1,   /* Y = X + layer(X) */
+  BCMT_FLAG_ACCUM_WGRAD = 2 /* backward adds into the weight/decay gradients instead of overwriting */
+};
+
+/* Passes for bcmt_workspace_bytes(). */
+enum {
+  BCMT_PASS_FORWARD = 0,   /* forward writing `saved` for a later backward */
+  BCMT_PASS_INFERENCE = 1, /* forward with saved == NULL */
+  BCMT_PASS_BACKWARD = 2
+};
+
+typedef struct {
+  int32_t B;     /* sequences */
+  int32_t T;     /* tokens per sequence */
+  int32_t D;     /* features, D = H * 64 on the GPU path */
+  int32_t H;     /* attention heads */
+  int32_t L;     /* block size (L >= T gives a single block: dense causal attention) */
+  float gamma;   /* memory decay, 0 <= gamma < 1 (0**0 is taken as 1) */
+  int32_t dtype; /* bcmt_dtype: float32, or bfloat16 storage with float32 accumulation */
+  int32_t flags; /* BCMT_FLAG_* */
+} bcmt_config;
+
+typedef struct {
+  const void *Wq, *Wk, *Wv, *Wo, *Wm, *Wg; /* [D, D] input-major, dtype */
+  const void* wp;                          /* [D], dtype */
+} bcmt_params;
+
+/* Float32 gradients.  A NULL member is not computed. */
+typedef struct {
+  float *dWq, *dWk, *dWv, *dWo, *dWm, *dWg; /* [D, D] */
+  float* dwp;                               /* [D] */
+  float* dgamma;                            /* scalar */
+} bcmt_grads;
+
+/* Host-only check of a configuration; returns BCMT_OK or a negative status.
+ * Makes no HIP call. */
+int bcmt_validate(const bcmt_config* cfg);
+
+/* Bytes of the `saved` buffer that forward fills and backward reads
+ * (activations kept for the backward pass); 0 for an invalid config. */
+size_t bcmt_saved_bytes(const bcmt_config* cfg);
+
+/* Bytes of scratch workspace a pass needs (BCMT_PASS_*); 0 for an invalid
+ * config.  The inference pass includes room for the activations that
+ * `saved` would otherwise hold. */
+size_t bcmt_workspace_bytes(const bcmt_config* cfg, int pass);
+
+/* Forward pass (Sec. 3.2-3.8).
+ *   X      [B, T, D] input, read only.
+ *   params the seven weights, read only.
+ *   Y      [B, T, D] output; must not overlap X.
+ *   saved  bcmt_saved_bytes() bytes written for bcmt_layer_backward, or NULL
+ *          for inference (then the workspace must hold BCMT_PASS_INFERENCE
+ *          bytes).
+ *   ws     scratch of at least bcmt_workspace_bytes(cfg, pass) bytes; its
+ *          contents on entry are ignored and on exit are undefined. */
+int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* params, void* Y,
+                       void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward pass: gradients of sum(dY * Y) given the forward's `saved`.
+ *   X      the forward input (read).
+ *   saved  as written by bcmt_layer_forward with the same cfg, X and params.
+ *   dY     [B, T, D] upstream gradient (read).
+ *   dX     [B, T, D] input gradient (written), or NULL to skip it.
+ *   grads  float32 weight/decay gradients (overwritten, or accumulated
+ *          with BCMT_FLAG_ACCUM_WGRAD); NULL, or NULL members, skip them.
+ *   ws     at least bcmt_workspace_bytes(cfg, BCMT_PASS_BACKWARD) bytes.
+ * Weight-gradient reductions use float32 atomics, so they are not bitwise
+ * reproducible run to run (within rounding). */
+int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* params,
+                        const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* bcmt_strerror(int status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int bcmt_version(void);
+
+/* ---- Stage tracing (profiling aid) -------------------------------------
+ * While tracing is on, every kernel launch of bcmt_layer_forward and
+ * bcmt_layer_backward is bracketed by two HIP events recorded on the call's
+ * stream, so each stage's GPU time is measured in place.  The events are
+ * created by the library on first use and reused; they are the only
+ * resource the library ever creates.  Stage names are static strings such
+ * as "fwd.qkv_gemm" or "bwd.attention_dkdv". */
+typedef struct {
+  const char* name; /* static string */
+  int32_t calls;    /* launches recorded since the last read */
+  double total_ms;  /* summed GPU time of those launches */
+} bcmt_trace_entry;
+
+/* Turns tracing on (nonzero) or off; returns the previous setting. */
+int bcmt_trace_enable(int on);
+
+/* Waits for every recorded launch to finish, writes up to max_entries
+ * per-stage totals (stages with at least one launch, in pipeline order),
+ * clears them, and returns how many stages had launches (which may exceed
+ * max_entries), or a negative status. */
+int bcmt_trace_read(bcmt_trace_entry* out, int max_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BCMT_H_ */

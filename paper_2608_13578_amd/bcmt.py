@@ -1,0 +1,195 @@
+"""Python binding of libbcmt (the C ABI declared in include/bcmt.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  Tensors are passed as device pointers (``tensor.data_ptr()``); torch
+is used by callers for device memory and streams.  The functions have the
+names of the C entry points and raise ``BcmtError`` on a negative status.
+
+If the shared library has not been built this module fails loudly on first
+use; there is no fallback implementation.
+"""
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbcmt.so")
+
+BCMT_OK = 0
+BCMT_ERR_INVALID = -1
+BCMT_ERR_UNSUPPORTED = -2
+BCMT_ERR_WORKSPACE = -3
+BCMT_ERR_HIP = -4
+
+BCMT_F32 = 0
+BCMT_BF16 = 1
+
+BCMT_FLAG_RESIDUAL = 1
+BCMT_FLAG_ACCUM_WGRAD = 2
+
+BCMT_PASS_FORWARD = 0
+BCMT_PASS_INFERENCE = 1
+BCMT_PASS_BACKWARD = 2
+
+EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_layer_forward",
+            "bcmt_layer_backward", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
+            "bcmt_trace_read")
+
+PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
+GRAD_NAMES = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp", "dgamma")
+
+
+class BcmtError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {bcmt_strerror(status)} ({status})")
+
+
+class bcmt_config(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("H", ctypes.c_int32), ("L", ctypes.c_int32), ("gamma", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+
+class bcmt_params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
+
+
+class bcmt_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_NAMES]
+
+
+class bcmt_trace_entry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("calls", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded shared library (loaded once)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it first with "
+                "`python -m paper_2608_13578_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        cfgp = ctypes.POINTER(bcmt_config)
+        vp = ctypes.c_void_p
+        L.bcmt_validate.argtypes = [cfgp]
+        L.bcmt_validate.restype = ctypes.c_int
+        L.bcmt_saved_bytes.argtypes = [cfgp]
+        L.bcmt_saved_bytes.restype = ctypes.c_size_t
+        L.bcmt_workspace_bytes.argtypes = [cfgp, ctypes.c_int]
+        L.bcmt_workspace_bytes.restype = ctypes.c_size_t
+        L.bcmt_layer_forward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
+                                         ctypes.c_size_t, vp]
+        L.bcmt_layer_forward.restype = ctypes.c_int
+        L.bcmt_layer_backward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
+                                          ctypes.POINTER(bcmt_grads), vp, ctypes.c_size_t, vp]
+        L.bcmt_layer_backward.restype = ctypes.c_int
+        L.bcmt_strerror.argtypes = [ctypes.c_int]
+        L.bcmt_strerror.restype = ctypes.c_char_p
+        L.bcmt_version.argtypes = []
+        L.bcmt_version.restype = ctypes.c_int
+        L.bcmt_trace_enable.argtypes = [ctypes.c_int]
+        L.bcmt_trace_enable.restype = ctypes.c_int
+        L.bcmt_trace_read.argtypes = [ctypes.POINTER(bcmt_trace_entry), ctypes.c_int]
+        L.bcmt_trace_read.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def make_config(B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False, accumulate=False):
+    """A bcmt_config from plain values (dtype "bf16" or "f32")."""
+    flags = (BCMT_FLAG_RESIDUAL if residual else 0) | (BCMT_FLAG_ACCUM_WGRAD if accumulate else 0)
+    dt = {"bf16": BCMT_BF16, "f32": BCMT_F32}[dtype]
+    return bcmt_config(int(B), int(T), int(D), int(H), int(L), float(gamma), dt, flags)
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _params(p):
+    if isinstance(p, bcmt_params):
+        return p
+    return bcmt_params(*[_ptr(p[n]) for n in PARAM_NAMES])
+
+
+def _grads(g):
+    if g is None or isinstance(g, bcmt_grads):
+        return g
+    return bcmt_grads(*[_ptr(g.get(n)) for n in GRAD_NAMES])
+
+
+def _nbytes(x):
+    return x.numel() * x.element_size()
+
+
+def bcmt_strerror(status):
+    return lib().bcmt_strerror(int(status)).decode()
+
+
+def bcmt_version():
+    return lib().bcmt_version()
+
+
+def bcmt_validate(cfg):
+    return lib().bcmt_validate(ctypes.byref(cfg))
+
+
+def bcmt_saved_bytes(cfg):
+    return lib().bcmt_saved_bytes(ctypes.byref(cfg))
+
+
+def bcmt_workspace_bytes(cfg, pass_):
+    return lib().bcmt_workspace_bytes(ctypes.byref(cfg), int(pass_))
+
+
+def bcmt_layer_forward(cfg, X, params, Y, saved, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    st = lib().bcmt_layer_forward(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
+                                  _ptr(Y), _ptr(saved), _ptr(ws), int(ws_bytes), _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_layer_forward")
+
+
+def bcmt_layer_backward(cfg, X, params, saved, dY, dX, grads, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    g = _grads(grads)
+    st = lib().bcmt_layer_backward(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
+                                   _ptr(saved), _ptr(dY), _ptr(dX),
+                                   ctypes.byref(g) if g is not None else None, _ptr(ws),
+                                   int(ws_bytes), _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_layer_backward")
+
+
+def bcmt_trace_enable(on):
+    return lib().bcmt_trace_enable(1 if on else 0)
+
+
+def bcmt_trace_read(max_entries=64):
+    """Per-stage totals since the last read: list of (name, calls, total_ms)."""
+    buf = (bcmt_trace_entry * max_entries)()
+    n = lib().bcmt_trace_read(buf, max_entries)
+    if n < 0:
+        raise BcmtError(n, "bcmt_trace_read")
+    return [(buf[i].name.decode(), buf[i].calls, buf[i].total_ms) for i in range(min(n, max_entries))]

@@ -1,0 +1,431 @@
+// C ABI of the BCMT layer: argument checks, the buffer plan, and the ordered
+// launch sequence of the forward and backward passes.
+//
+// Forward (Sec. 3.2-3.8 of the paper), all on the caller's stream:
+//   1. [Q|K|V] = X [Wq|Wk|Wv]                      matrix cores
+//   2. block-local causal attention -> Hcat, lse   matrix cores
+//   3. H = Hcat Wo                                 matrix cores
+//   4. pooling scores and per-chunk softmax sums   bandwidth
+//   5. chunk merge + decayed scan -> S, M          bandwidth / latency
+//   6. P = M Wm                                    matrix cores (N_b rows)
+//   7. U = H Wg; G = sigmoid(U); Y = H + G * P[blk - 1]  (fused epilogue)
+// Backward runs the chain rule through the same steps in reverse.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/bcmt.h"
+#include "kernels.h"
+
+namespace bcmt {
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kDh = 64;
+constexpr int kMaxD = 2048;
+
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+  int B, T, D, H, L, nb, nch;
+  size_t es;
+  DType dt;
+  // saved (forward -> backward)
+  size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
+  // forward scratch
+  size_t part, fwd_bytes;
+  // backward scratch
+  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, bwd_bytes;
+
+  explicit Plan(const bcmt_config& c) {
+    B = c.B;
+    T = c.T;
+    D = c.D;
+    H = c.H;
+    L = c.L;
+    nb = (T + L - 1) / L;
+    nch = pool_chunks(L < T ? L : T);
+    dt = c.dtype == BCMT_BF16 ? DType::BF16 : DType::F32;
+    es = dt == DType::BF16 ? 2 : 4;
+    const size_t BT = (size_t)B * T, BTD = BT * D, BND = (size_t)B * nb * D;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+      size_t at = off;
+      off += up(bytes);
+      return at;
+    };
+    qkv = take(3 * BTD * es);
+    o = take(BTD * es);
+    lse = take((size_t)B * H * T * 4);
+    h = take(BTD * es);
+    g = take(BTD * es);
+    s = take(BT * 4);
+    stats = take((size_t)B * nb * 2 * 4);
+    S = take(BND * 4);
+    M = take(BND * 4);
+    Mt = take(BND * es);
+    P = take(BND * 4);
+    saved_bytes = off;
+
+    off = 0;
+    part = take((size_t)B * nb * nch * (D + 2) * 4);
+    fwd_bytes = off;
+
+    off = 0;
+    du = take(BTD * es);
+    pbar = take(BND * es);
+    mbar = take(BND * 4);
+    dS = take(BND * 4);
+    a = take(BT * 4);
+    ds = take(BT * 4);
+    dh = take(BTD * es);
+    dout = take(BTD * es);
+    delta = take((size_t)B * H * T * 4);
+    dqkv = take(3 * BTD * es);
+    bwd_bytes = off;
+  }
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_config(const bcmt_config* c) {
+  if (!c) return BCMT_ERR_INVALID;
+  if (c->B < 1 || c->T < 1 || c->D < 1 || c->H < 1 || c->L < 1) return BCMT_ERR_INVALID;
+  if (c->D % c->H != 0) return BCMT_ERR_INVALID;
+  if (!(c->gamma >= 0.0f && c->gamma < 1.0f)) return BCMT_ERR_INVALID;
+  if (c->dtype != BCMT_F32 && c->dtype != BCMT_BF16) return BCMT_ERR_INVALID;
+  if (c->flags & ~(BCMT_FLAG_RESIDUAL | BCMT_FLAG_ACCUM_WGRAD)) return BCMT_ERR_INVALID;
+  if (c->D / c->H != kDh || c->D > kMaxD) return BCMT_ERR_UNSUPPORTED;
+  // Grid limits: rows of the projections, blocks, batch * heads.
+  const int64_t BT = (int64_t)c->B * c->T;
+  const int64_t nb = ((int64_t)c->T + c->L - 1) / c->L;
+  if (BT > 65535LL * 128 || nb > 65535 || (int64_t)c->B * c->H > 65535 || c->B > 65535)
+    return BCMT_ERR_UNSUPPORTED;
+  return BCMT_OK;
+}
+
+bool overlaps(const void* a, const void* b, size_t n) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + n && y < x + n;
+}
+
+int split_for(int tiles, int K) {
+  int s = (512 + tiles - 1) / tiles;
+  const int kmax = K / 256;
+  if (s > kmax) s = kmax;
+  return s < 1 ? 1 : s;
+}
+
+// ------------------------------------------------------------------ tracing
+// Named stages of the two passes; each is one kernel launch.
+enum Stage {
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_WM, ST_GATE,
+  ST_ZERO, ST_GATE_BWD, ST_WG_WGRAD, ST_WM_DGRAD, ST_WM_WGRAD, ST_MEM_BWD, ST_POOL_BWD,
+  ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD,
+  ST_COUNT
+};
+const char* const kStageNames[ST_COUNT] = {
+    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.scan", "fwd.wm_gemm",
+    "fwd.gate_gemm", "bwd.zero_grads", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wm_dgrad_gemm",
+    "bwd.wm_wgrad_gemm", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm", "bwd.wo_dgrad_gemm",
+    "bwd.wo_wgrad_gemm", "bwd.attention_dq", "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm",
+    "bwd.qkv_wgrad_gemm"};
+
+struct Tracer {
+  std::atomic<bool> on{false};
+  std::mutex mu;
+  struct Rec {
+    int stage;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  double total[ST_COUNT] = {};
+  int calls[ST_COUNT] = {};
+
+  hipEvent_t take() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Tracer g_trace;
+
+// Brackets one launch with two events on the launch stream when tracing is on.
+struct TraceScope {
+  int stage;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  TraceScope(int st, hipStream_t str) : stage(st), s(str) {
+    if (!g_trace.on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_trace.mu);
+    a = g_trace.take();
+    if (a && hipEventRecord(a, s) != hipSuccess) {
+      g_trace.pool.push_back(a);
+      a = nullptr;
+    }
+  }
+  void done() {
+    if (!a) return;
+    std::lock_guard<std::mutex> lk(g_trace.mu);
+    hipEvent_t b = g_trace.take();
+    if (b && hipEventRecord(b, s) == hipSuccess) {
+      g_trace.pending.push_back({stage, a, b});
+    } else {
+      g_trace.pool.push_back(a);
+      if (b) g_trace.pool.push_back(b);
+    }
+    a = nullptr;
+  }
+};
+
+#define LAUNCH(stage, expr)                            \
+  do {                                                 \
+    TraceScope ts_(stage, s);                          \
+    if ((expr) != hipSuccess) return BCMT_ERR_HIP;     \
+    ts_.done();                                        \
+  } while (0)
+
+}  // namespace
+}  // namespace bcmt
+
+using namespace bcmt;
+
+extern "C" {
+
+int bcmt_validate(const bcmt_config* cfg) { return check_config(cfg); }
+
+size_t bcmt_saved_bytes(const bcmt_config* cfg) {
+  if (check_config(cfg) != BCMT_OK) return 0;
+  return Plan(*cfg).saved_bytes;
+}
+
+size_t bcmt_workspace_bytes(const bcmt_config* cfg, int pass) {
+  if (check_config(cfg) != BCMT_OK) return 0;
+  Plan p(*cfg);
+  switch (pass) {
+    case BCMT_PASS_FORWARD: return p.fwd_bytes;
+    case BCMT_PASS_INFERENCE: return p.fwd_bytes + p.saved_bytes;
+    case BCMT_PASS_BACKWARD: return p.bwd_bytes;
+    default: return 0;
+  }
+}
+
+const char* bcmt_strerror(int status) {
+  switch (status) {
+    case BCMT_OK: return "ok";
+    case BCMT_ERR_INVALID: return "invalid argument";
+    case BCMT_ERR_UNSUPPORTED: return "configuration not supported by the GPU path";
+    case BCMT_ERR_WORKSPACE: return "workspace too small";
+    case BCMT_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int bcmt_version(void) { return 100; }
+
+int bcmt_trace_enable(int on) { return g_trace.on.exchange(on != 0) ? 1 : 0; }
+
+int bcmt_trace_read(bcmt_trace_entry* out, int max_entries) {
+  if (max_entries < 0 || (max_entries > 0 && !out)) return BCMT_ERR_INVALID;
+  std::lock_guard<std::mutex> lk(g_trace.mu);
+  int st = BCMT_OK;
+  for (auto& r : g_trace.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
+      st = BCMT_ERR_HIP;
+    } else {
+      g_trace.total[r.stage] += ms;
+      g_trace.calls[r.stage] += 1;
+    }
+    g_trace.pool.push_back(r.a);
+    g_trace.pool.push_back(r.b);
+  }
+  g_trace.pending.clear();
+  if (st != BCMT_OK) return st;
+  int n = 0;
+  for (int k = 0; k < ST_COUNT; ++k) {
+    if (g_trace.calls[k] == 0) continue;
+    if (n < max_entries) {
+      out[n].name = kStageNames[k];
+      out[n].calls = g_trace.calls[k];
+      out[n].total_ms = g_trace.total[k];
+    }
+    ++n;
+    g_trace.calls[k] = 0;
+    g_trace.total[k] = 0.0;
+  }
+  return n;
+}
+
+int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* prm, void* Y,
+                       void* saved, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_config(cfg);
+  if (st != BCMT_OK) return st;
+  if (!X || !prm || !Y) return BCMT_ERR_INVALID;
+  const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
+  for (const void* p : w)
+    if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
+  if (!aligned16(X) || !aligned16(Y) || (saved && !aligned16(saved)) || (ws && !aligned16(ws)))
+    return BCMT_ERR_INVALID;
+  Plan p(*cfg);
+  const size_t act = (size_t)p.B * p.T * p.D * p.es;
+  if (overlaps(X, Y, act)) return BCMT_ERR_INVALID;
+  const size_t need = saved ? p.fwd_bytes : p.fwd_bytes + p.saved_bytes;
+  if (!ws) return BCMT_ERR_INVALID;
+  if (ws_bytes < need) return BCMT_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  char* W = (char*)ws;
+  char* SV = saved ? (char*)saved : W + p.fwd_bytes;
+  const int BT = p.B * p.T, D = p.D;
+  const DType dt = p.dt;
+
+  // 1. Q | K | V projections (Sec. 3.3).
+  {
+    GemmDesc g{BT, 3 * D, D, X, D, false, {prm->Wq, prm->Wk, prm->Wv}, D, true, kSegN, D, 1};
+    LAUNCH(ST_QKV, gemm_store(dt, g, SV + p.qkv, 3 * D, false, nullptr, 0, s));
+  }
+  // 2. Block-local causal attention (Sec. 3.3, 3.6).
+  LAUNCH(ST_ATTN_FWD, attn_fwd(dt, SV + p.qkv, SV + p.o, (float*)(SV + p.lse), p.B, p.T, D, p.H, p.L, s));
+  // 3. Output projection (Sec. 3.3).
+  {
+    GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    LAUNCH(ST_WO, gemm_store(dt, g, SV + p.h, D, false, nullptr, 0, s));
+  }
+  // 4-5. Adaptive summaries (Sec. 3.4) and the exponential memory (Sec. 3.5).
+  LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, prm->wp, (float*)(SV + p.s), (float*)(W + p.part), p.B, p.T, D,
+                  p.L, s));
+  LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(W + p.part), (float*)(SV + p.S), (float*)(SV + p.M),
+                  SV + p.Mt, (float*)(SV + p.stats), p.B, p.T, D, p.L, cfg->gamma, s));
+  // 6. Memory projection (Sec. 3.5); the shift is applied where P is read.
+  {
+    GemmDesc g{p.B * p.nb, D, D, SV + p.Mt, D, false, {prm->Wm, nullptr, nullptr}, D, true,
+               kSegNone, 0, 1};
+    LAUNCH(ST_WM, gemm_store(dt, g, SV + p.P, D, true, nullptr, 0, s));
+  }
+  // 7. Gate and injection (Sec. 3.7, 3.8).
+  {
+    GemmDesc g{BT, D, D, SV + p.h, D, false, {prm->Wg, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    GateEpi e{Y, SV + p.g, SV + p.h, (cfg->flags & BCMT_FLAG_RESIDUAL) ? X : nullptr,
+              (const float*)(SV + p.P), p.T, p.L, p.nb, D};
+    LAUNCH(ST_GATE, gemm_gate(dt, g, e, s));
+  }
+  return BCMT_OK;
+}
+
+int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                        const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
+                        void* ws, size_t ws_bytes, void* stream) {
+  int st = check_config(cfg);
+  if (st != BCMT_OK) return st;
+  if (!X || !prm || !saved || !dY) return BCMT_ERR_INVALID;
+  const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
+  for (const void* p : w)
+    if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
+  if (!aligned16(X) || !aligned16(saved) || !aligned16(dY) || (dX && !aligned16(dX)) ||
+      (ws && !aligned16(ws)))
+    return BCMT_ERR_INVALID;
+  bcmt_grads none;
+  memset(&none, 0, sizeof(none));
+  const bcmt_grads& gr = grads ? *grads : none;
+  const float* gp[7] = {gr.dWq, gr.dWk, gr.dWv, gr.dWo, gr.dWm, gr.dWg, gr.dwp};
+  for (const float* q : gp)
+    if (q && !aligned16(q)) return BCMT_ERR_INVALID;
+  if (gr.dgamma && ((uintptr_t)gr.dgamma & 3u)) return BCMT_ERR_INVALID;
+  Plan p(*cfg);
+  const size_t act = (size_t)p.B * p.T * p.D * p.es;
+  if (dX && (overlaps(dX, dY, act) || overlaps(dX, X, act))) return BCMT_ERR_INVALID;
+  if (!ws) return BCMT_ERR_INVALID;
+  if (ws_bytes < p.bwd_bytes) return BCMT_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  const char* SV = (const char*)saved;
+  char* W = (char*)ws;
+  const int BT = p.B * p.T, D = p.D, BN = p.B * p.nb;
+  const DType dt = p.dt;
+  const bool residual = cfg->flags & BCMT_FLAG_RESIDUAL;
+
+  if (!(cfg->flags & BCMT_FLAG_ACCUM_WGRAD)) {
+    float* mats[6] = {gr.dWq, gr.dWk, gr.dWv, gr.dWo, gr.dWm, gr.dWg};
+    for (float* m : mats)
+      if (m) LAUNCH(ST_ZERO, fill_f32(m, (int64_t)D * D, 0.f, s));
+    if (gr.dwp) LAUNCH(ST_ZERO, fill_f32(gr.dwp, D, 0.f, s));
+    if (gr.dgamma) LAUNCH(ST_ZERO, fill_f32(gr.dgamma, 1, 0.f, s));
+  }
+
+  // Gate and injection: dU, and the block sums of dY * G shifted back by one.
+  LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar, p.B, p.T, D,
+                  p.L, s));
+  if (gr.dWg) {
+    GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0,
+               split_for(((D + 127) / 128) * ((D + 127) / 128), BT)};
+    LAUNCH(ST_WG_WGRAD, gemm_atomic(dt, g, gr.dWg, nullptr, nullptr, D, D, s));
+  }
+  // Memory projection: dM = dP Wm^T and dWm = M^T dP.
+  {
+    GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
+               1};
+    LAUNCH(ST_WM_DGRAD, gemm_store(dt, g, W + p.mbar, D, true, nullptr, 0, s));
+  }
+  if (gr.dWm) {
+    GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0,
+               split_for(((D + 127) / 128) * ((D + 127) / 128), BN)};
+    LAUNCH(ST_WM_WGRAD, gemm_atomic(dt, g, gr.dWm, nullptr, nullptr, D, D, s));
+  }
+  // Decayed reverse scan: dS and the decay gradient.
+  LAUNCH(ST_MEM_BWD, mem_bwd((const float*)(W + p.mbar), (const float*)(SV + p.M), (float*)(W + p.dS),
+                 gr.dgamma, p.B, p.nb, D, cfg->gamma, s));
+  // Pooling backward: per-token a_t, ds_t and dwp.
+  LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
+                  (const float*)(SV + p.S), (const float*)(W + p.dS), prm->wp, (float*)(W + p.a),
+                  (float*)(W + p.ds), gr.dwp, p.B, p.T, D, p.L, s));
+  // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.
+  {
+    GemmDesc g{BT, D, D, W + p.du, D, false, {prm->Wg, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+    HbarEpi e{W + p.dh, dY, (const float*)(W + p.a), (const float*)(W + p.ds),
+              (const float*)(W + p.dS), prm->wp, p.T, p.L, p.nb, D};
+    LAUNCH(ST_HBAR, gemm_hbar(dt, g, e, s));
+  }
+  // Output projection backward.
+  {
+    GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+    LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
+  }
+  if (gr.dWo) {
+    GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0,
+               split_for(((D + 127) / 128) * ((D + 127) / 128), BT)};
+    LAUNCH(ST_WO_WGRAD, gemm_atomic(dt, g, gr.dWo, nullptr, nullptr, D, D, s));
+  }
+  // Block-local attention backward.
+  LAUNCH(ST_ATTN_BWD_DQ,
+         attn_bwd_dq(dt, SV + p.qkv, SV + p.o, W + p.dout, (const float*)(SV + p.lse),
+                     (float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+  LAUNCH(ST_ATTN_BWD_DKDV,
+         attn_bwd_dkdv(dt, SV + p.qkv, W + p.dout, (const float*)(SV + p.lse),
+                       (const float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+  // Q/K/V projections backward.
+  if (dX) {
+    GemmDesc g{BT, D, 3 * D, W + p.dqkv, 3 * D, false, {prm->Wq, prm->Wk, prm->Wv}, D, false,
+               kSegK, D, 1};
+    LAUNCH(ST_DX, gemm_store(dt, g, dX, D, false, residual ? dY : nullptr, D, s));
+  }
+  if (gr.dWq || gr.dWk || gr.dWv) {
+    GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone, 0,
+               split_for(((D + 127) / 128) * ((3 * D + 127) / 128), BT)};
+    LAUNCH(ST_QKV_WGRAD, gemm_atomic(dt, g, gr.dWq, gr.dWk, gr.dWv, D, D, s));
+  }
+  return BCMT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,486 @@
+// Block-local causal multi-head attention (Sec. 3.3 and 3.6 of the paper):
+// for every batch element, block and head, softmax(Q K^T / sqrt(dh) + causal
+// mask) V over the block's own tokens, the diagonal included.  No score
+// matrix ever leaves registers: the softmax is evaluated online over 64-key
+// tiles staged in LDS, and the forward keeps only a per-query log-sum-exp for
+// the backward recomputation.
+//
+// Head width is 64.  Work decomposition (one workgroup per (query or key
+// tile, block, batch * head)); each wave owns 32 queries (forward and dQ) or
+// 32 keys (dK/dV) as two 16-wide sub-tiles.
+//
+// Register layouts (see common.h): a matrix instruction returns lane l the
+// column (l % 16) and rows 4*(l/16) + r, r = 0..3.  The forward computes the
+// transposed scores S^T[u][t] = K[u] . Q[t], so that a lane holds one query t
+// = l % 16 and a set of keys.  Those probabilities are then directly the
+// second operand of O^T[d][t] = sum_u V^T[d][u] P^T[u][t]: the eight K
+// elements lane group g contributes are the keys 4g..4g+3 and 16+4g..16+4g+3
+// of a 32-key step, and the V^T operand is read from LDS with the same key
+// order.  Because every lane keeps one query throughout, the running max and
+// sum of the online softmax never move between lanes except for the final
+// reduction over the four lane groups.
+#include "common.h"
+#include "kernels.h"
+
+namespace bcmt {
+namespace {
+
+constexpr int kDh = 64;
+
+template <typename T> struct AttnLds {
+  static constexpr int VE = Vec16<T>::N;
+  static constexpr int NAT = kDh + VE;  // row of a natural [row][d] tile
+  static constexpr int TR = kDh + 4;    // row of a transposed [d][row] tile
+};
+
+// Stage rows r0 .. r0+63 (clipped at rmax) of a 64-column slice into LDS,
+// natural and/or transposed.  Rows past rmax are zero, so that no stale LDS
+// value ever meets a zero probability in a product.
+template <typename T, bool NAT, bool TRN>
+__device__ __forceinline__ void stage_tile(const T* src, int64_t rs, int r0, int rmax, T* nat,
+                                           T* trn, int tid, int nthr) {
+  constexpr int VE = Vec16<T>::N;
+  constexpr int VPR = kDh / VE;
+  typedef typename Vec16<T>::type vec;
+  for (int idx = tid; idx < 64 * VPR; idx += nthr) {
+    const int r = idx / VPR;
+    const int c = (idx % VPR) * VE;
+    const int row = r0 + r;
+    vec v = row < rmax ? load16(src + (int64_t)row * rs + c) : vec{};
+    if constexpr (NAT) store16(nat + r * AttnLds<T>::NAT + c, v);
+    if constexpr (TRN) {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) trn[(c + e) * AttnLds<T>::TR + r] = v[e];
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type frag_global(const T* p, bool ok) {
+  typedef typename Frag<T>::type F;
+  return ok ? load_frag(p) : F{};
+}
+
+// ------------------------------------------------------------------ forward
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const T* __restrict__ qkv,
+                                                       T* __restrict__ out,
+                                                       float* __restrict__ lse, int Tn, int D,
+                                                       int H, int L, float sl2) {
+  typedef typename Frag<T>::type F;
+  constexpr int NAT = AttnLds<T>::NAT, TR = AttnLds<T>::TR;
+  __shared__ __attribute__((aligned(16))) T Ks[64 * NAT];
+  __shared__ __attribute__((aligned(16))) T Vt[64 * TR];
+
+  const int nthr = blockDim.x;
+  const int QT = (nthr / 64) * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int q0 = bs + blockIdx.x * QT;
+  if (q0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const T* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const int tw0 = q0 + wave * 32;
+
+  F qf[2][2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds)
+      qf[nq][ds] = frag_global(base + (int64_t)t * rs + ds * 32 + lg * 8, t < be);
+  }
+  f32x4 o[2][4];
+  float m[2], l[2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    m[nq] = -INFINITY;
+    l[nq] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int kend = min(be, q0 + QT);
+  for (int kt = bs; kt < kend; kt += 64) {
+    __syncthreads();
+    stage_tile<T, true, false>(base + D, rs, kt, kend, Ks, nullptr, tid, nthr);
+    stage_tile<T, false, true>(base + 2 * D, rs, kt, kend, nullptr, Vt, tid, nthr);
+    __syncthreads();
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int tq = tw0 + nq * 16;
+      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+      f32x4 s[4];
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku) {
+        s[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds)
+          s[ku] = mma16(load_frag(Ks + (ku * 16 + lr) * NAT + ds * 32 + lg * 8), qf[nq][ds], s[ku]);
+      }
+      const int t_eff = min(tq + lr, be - 1);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int u = kt + ku * 16 + lg * 4 + r;
+          const float z = u <= t_eff ? s[ku][r] * sl2 : -INFINITY;
+          s[ku][r] = z;
+          mx = fmaxf(mx, z);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(m[nq], mx);
+      const float alpha = exp2f(m[nq] - mnew);
+      float ps = 0.f;
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = exp2f(s[ku][r] - mnew);
+          s[ku][r] = p;
+          ps += p;
+        }
+      l[nq] = l[nq] * alpha + ps;
+      m[nq] = mnew;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[nq][j] *= alpha;
+#pragma unroll
+      for (int us = 0; us < 2; ++us) {
+        const F pf = frag_from<T>(s[2 * us], s[2 * us + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const T* vp = Vt + (j * 16 + lr) * TR + us * 32 + lg * 4;
+          o[nq][j] = mma16(load_frag_split(vp, vp + 16), pf, o[nq][j]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    float lt = l[nq];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    const int t = tw0 + nq * 16 + lr;
+    if (t < be) {
+      const float inv = 1.0f / lt;
+      T* op = out + ((int64_t)b * Tn + t) * D + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        store4(op + j * 16, o[nq][j][0] * inv, o[nq][j][1] * inv, o[nq][j][2] * inv,
+               o[nq][j][3] * inv);
+      if (lg == 0) lse[((int64_t)b * H + h) * Tn + t] = m[nq] + log2f(lt);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ backward: dQ
+// Recomputes S^T and dP^T = V dO^T per key tile, forms dZ^T = P^T (dP^T -
+// delta) and accumulates dQ^T[d][t] = sum_u K^T[d][u] dZ^T[u][t].  Also
+// produces delta_t = dO_t . O_t, which the dK/dV pass reads.
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(
+    const T* __restrict__ qkv, const T* __restrict__ o, const T* __restrict__ dout,
+    const float* __restrict__ lse, float* __restrict__ delta, T* __restrict__ dqkv, int Tn,
+    int D, int H, int L, float sl2, float scale) {
+  typedef typename Frag<T>::type F;
+  constexpr int NAT = AttnLds<T>::NAT, TR = AttnLds<T>::TR;
+  __shared__ __attribute__((aligned(16))) T Ks[64 * NAT];
+  __shared__ __attribute__((aligned(16))) T Kt[64 * TR];
+  __shared__ __attribute__((aligned(16))) T Vs[64 * NAT];
+
+  const int nthr = blockDim.x;
+  const int QT = (nthr / 64) * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int q0 = bs + blockIdx.x * QT;
+  if (q0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const T* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const T* ob = o + (int64_t)b * Tn * D + h * kDh;
+  const T* db = dout + (int64_t)b * Tn * D + h * kDh;
+  const int64_t lrow = ((int64_t)b * H + h) * Tn;
+  const int tw0 = q0 + wave * 32;
+
+  F qf[2][2], df[2][2];
+  float dl[2], ls[2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+    const bool ok = t < be;
+    float part = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      qf[nq][ds] = frag_global(base + (int64_t)t * rs + ds * 32 + lg * 8, ok);
+      df[nq][ds] = frag_global(db + (int64_t)t * D + ds * 32 + lg * 8, ok);
+      const F of = frag_global(ob + (int64_t)t * D + ds * 32 + lg * 8, ok);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part += to_f32(df[nq][ds][e]) * to_f32(of[e]);
+    }
+    part += __shfl_xor(part, 16, 64);
+    part += __shfl_xor(part, 32, 64);
+    dl[nq] = part;
+    ls[nq] = ok ? lse[lrow + t] : 0.f;
+    if (ok && lg == 0) delta[lrow + t] = part;
+  }
+  f32x4 dq[2][4];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dq[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int kend = min(be, q0 + QT);
+  for (int kt = bs; kt < kend; kt += 64) {
+    __syncthreads();
+    stage_tile<T, true, true>(base + D, rs, kt, kend, Ks, Kt, tid, nthr);
+    stage_tile<T, true, false>(base + 2 * D, rs, kt, kend, Vs, nullptr, tid, nthr);
+    __syncthreads();
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int tq = tw0 + nq * 16;
+      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+      f32x4 s[4], dp[4];
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku) {
+        s[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dp[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          s[ku] = mma16(load_frag(Ks + (ku * 16 + lr) * NAT + ds * 32 + lg * 8), qf[nq][ds], s[ku]);
+          dp[ku] = mma16(load_frag(Vs + (ku * 16 + lr) * NAT + ds * 32 + lg * 8), df[nq][ds], dp[ku]);
+        }
+      }
+      const int t_eff = min(tq + lr, be - 1);
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int u = kt + ku * 16 + lg * 4 + r;
+          const float p = u <= t_eff ? exp2f(s[ku][r] * sl2 - ls[nq]) : 0.f;
+          s[ku][r] = p * (dp[ku][r] - dl[nq]);
+        }
+#pragma unroll
+      for (int us = 0; us < 2; ++us) {
+        const F zf = frag_from<T>(s[2 * us], s[2 * us + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const T* kp = Kt + (j * 16 + lr) * TR + us * 32 + lg * 4;
+          dq[nq][j] = mma16(load_frag_split(kp, kp + 16), zf, dq[nq][j]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+    if (t < be) {
+      T* p = dqkv + ((int64_t)b * Tn + t) * rs + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        store4(p + j * 16, dq[nq][j][0] * scale, dq[nq][j][1] * scale, dq[nq][j][2] * scale,
+               dq[nq][j][3] * scale);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ backward: dK, dV
+// Each wave keeps its 32 keys' K and V fragments in registers and walks the
+// query tiles at or after them: S[t][u] and dP[t][u] land with one key per
+// lane, and dV^T[d][u] += sum_t dO^T[d][t] P[t][u], dK^T[d][u] += sum_t
+// Q^T[d][t] dZ[t][u] take those registers directly as their second operand.
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
+    const T* __restrict__ qkv, const T* __restrict__ dout, const float* __restrict__ lse,
+    const float* __restrict__ delta, T* __restrict__ dqkv, int Tn, int D, int H, int L,
+    float sl2, float scale) {
+  typedef typename Frag<T>::type F;
+  constexpr int NAT = AttnLds<T>::NAT, TR = AttnLds<T>::TR;
+  __shared__ __attribute__((aligned(16))) T Qs[64 * NAT];
+  __shared__ __attribute__((aligned(16))) T Qt[64 * TR];
+  __shared__ __attribute__((aligned(16))) T Ds[64 * NAT];
+  __shared__ __attribute__((aligned(16))) T Dt[64 * TR];
+  __shared__ float ls_s[64];
+  __shared__ float dl_s[64];
+
+  const int nthr = blockDim.x;
+  const int KT = (nthr / 64) * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int k0 = bs + blockIdx.x * KT;
+  if (k0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const T* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const T* db = dout + (int64_t)b * Tn * D + h * kDh;
+  const int64_t lrow = ((int64_t)b * H + h) * Tn;
+  const int uw0 = k0 + wave * 32;
+
+  F kf[2][2], vf[2][2];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku) {
+    const int u = uw0 + ku * 16 + lr;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      kf[ku][ds] = frag_global(base + D + (int64_t)u * rs + ds * 32 + lg * 8, u < be);
+      vf[ku][ds] = frag_global(base + 2 * D + (int64_t)u * rs + ds * 32 + lg * 8, u < be);
+    }
+  }
+  f32x4 dk[2][4], dv[2][4];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dk[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dv[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  for (int tt = k0; tt < be; tt += 64) {
+    __syncthreads();
+    stage_tile<T, true, true>(base, rs, tt, be, Qs, Qt, tid, nthr);
+    stage_tile<T, true, true>(db, D, tt, be, Ds, Dt, tid, nthr);
+    for (int i = tid; i < 64; i += nthr) {
+      const int t = tt + i;
+      ls_s[i] = t < be ? lse[lrow + t] : 0.f;
+      dl_s[i] = t < be ? delta[lrow + t] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku) {
+      const int uw = uw0 + ku * 16;
+      if (uw >= be || tt + 63 < uw) continue;  // wave-uniform
+      const int u = uw + lr;
+      f32x4 p[4], z[4];
+#pragma unroll
+      for (int ts = 0; ts < 4; ++ts) {
+        f32x4 s = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          s = mma16(load_frag(Qs + (ts * 16 + lr) * NAT + ds * 32 + lg * 8), kf[ku][ds], s);
+          dp = mma16(load_frag(Ds + (ts * 16 + lr) * NAT + ds * 32 + lg * 8), vf[ku][ds], dp);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ti = ts * 16 + lg * 4 + r;
+          const int t = tt + ti;
+          const bool ok = t >= u && t < be && u < be;
+          const float pv = ok ? exp2f(s[r] * sl2 - ls_s[ti]) : 0.f;
+          p[ts][r] = pv;
+          z[ts][r] = pv * (dp[r] - dl_s[ti]);
+        }
+      }
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        const F pf = frag_from<T>(p[2 * tq], p[2 * tq + 1]);
+        const F zf = frag_from<T>(z[2 * tq], z[2 * tq + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const T* dp_ = Dt + (j * 16 + lr) * TR + tq * 32 + lg * 4;
+          dv[ku][j] = mma16(load_frag_split(dp_, dp_ + 16), pf, dv[ku][j]);
+          const T* qp = Qt + (j * 16 + lr) * TR + tq * 32 + lg * 4;
+          dk[ku][j] = mma16(load_frag_split(qp, qp + 16), zf, dk[ku][j]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku) {
+    const int u = uw0 + ku * 16 + lr;
+    if (u < be) {
+      T* p = dqkv + ((int64_t)b * Tn + u) * rs + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        store4(p + D + j * 16, dk[ku][j][0] * scale, dk[ku][j][1] * scale, dk[ku][j][2] * scale,
+               dk[ku][j][3] * scale);
+        store4(p + 2 * D + j * 16, dv[ku][j][0], dv[ku][j][1], dv[ku][j][2], dv[ku][j][3]);
+      }
+    }
+  }
+}
+
+int attn_waves(int L, int T) {
+  const int lb = L < T ? L : T;
+  const int w = (lb + 31) / 32;
+  return w < 4 ? w : 4;
+}
+
+template <typename E>
+hipError_t attn_fwd_t(const void* qkv, void* out, float* lse, int B, int T, int D, int H, int L,
+                      hipStream_t s) {
+  const int nw = attn_waves(L, T);
+  const int lb = L < T ? L : T;
+  const int nb = (T + L - 1) / L;
+  dim3 grid((lb + nw * 32 - 1) / (nw * 32), nb, B * H);
+  const float sl2 = 1.4426950408889634f / sqrtf((float)kDh);
+  hipLaunchKernelGGL(attn_fwd_kernel<E>, grid, dim3(nw * 64), 0, s, (const E*)qkv, (E*)out, lse,
+                     T, D, H, L, sl2);
+  return hipGetLastError();
+}
+
+template <typename E>
+hipError_t attn_bwd_dq_t(const void* qkv, const void* o, const void* dout, const float* lse,
+                         float* delta, void* dqkv, int B, int T, int D, int H, int L,
+                         hipStream_t s) {
+  const int nw = attn_waves(L, T);
+  const int lb = L < T ? L : T;
+  const int nb = (T + L - 1) / L;
+  dim3 grid((lb + nw * 32 - 1) / (nw * 32), nb, B * H);
+  const float scale = 1.0f / sqrtf((float)kDh);
+  const float sl2 = 1.4426950408889634f * scale;
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<E>, grid, dim3(nw * 64), 0, s, (const E*)qkv,
+                     (const E*)o, (const E*)dout, lse, delta, (E*)dqkv, T, D, H, L, sl2, scale);
+  return hipGetLastError();
+}
+
+template <typename E>
+hipError_t attn_bwd_dkdv_t(const void* qkv, const void* dout, const float* lse,
+                           const float* delta, void* dqkv, int B, int T, int D, int H, int L,
+                           hipStream_t s) {
+  const int nw = attn_waves(L, T);
+  const int lb = L < T ? L : T;
+  const int nb = (T + L - 1) / L;
+  dim3 grid((lb + nw * 32 - 1) / (nw * 32), nb, B * H);
+  const float scale = 1.0f / sqrtf((float)kDh);
+  const float sl2 = 1.4426950408889634f * scale;
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<E>, grid, dim3(nw * 64), 0, s, (const E*)qkv,
+                     (const E*)dout, lse, delta, (E*)dqkv, T, D, H, L, sl2, scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D, int H,
+                    int L, hipStream_t s) {
+  if (dt == DType::BF16) return attn_fwd_t<bf16>(qkv, out, lse, B, T, D, H, L, s);
+  return attn_fwd_t<float>(qkv, out, lse, B, T, D, H, L, s);
+}
+
+hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* dout,
+                       const float* lse, float* delta, void* dqkv, int B, int T, int D, int H,
+                       int L, hipStream_t s) {
+  if (dt == DType::BF16) return attn_bwd_dq_t<bf16>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
+  return attn_bwd_dq_t<float>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
+}
+
+hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
+                         const float* delta, void* dqkv, int B, int T, int D, int H, int L,
+                         hipStream_t s) {
+  if (dt == DType::BF16) return attn_bwd_dkdv_t<bf16>(qkv, dout, lse, delta, dqkv, B, T, D, H, L, s);
+  return attn_bwd_dkdv_t<float>(qkv, dout, lse, delta, dqkv, B, T, D, H, L, s);
+}
+
+}  // namespace bcmt

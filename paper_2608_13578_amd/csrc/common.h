@@ -1,0 +1,145 @@
+// Device-side building blocks shared by the BCMT kernels (gfx950 / CDNA4).
+//
+// Element types: the layer runs either in float32 end to end or with
+// bfloat16 storage and float32 accumulation.  Matrix products use the CDNA4
+// matrix cores through two instruction shapes that share one register
+// layout:
+//   bf16: v_mfma_f32_16x16x32_bf16  (one instruction per 32-wide K step)
+//   f32 : v_mfma_f32_16x16x4_f32    (eight instructions per 32-wide K step)
+// For both, lane l of a wave supplies, for row/column (l % 16), the eight
+// consecutive K elements 8*(l/16) .. 8*(l/16)+7 of a 32-wide K step.  For
+// f32 the eight instructions j = 0..7 each contract the elements j of the
+// four lane groups; together they cover the same 32 K values (the order of
+// the K summation differs, nothing else).
+// The 16x16 float32 result lands with lane l holding column (l % 16) and
+// rows 4*(l/16) .. 4*(l/16)+3.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bcmt {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+template <typename T> struct Frag;
+template <> struct Frag<bf16> { typedef bf16x8 type; };
+template <> struct Frag<float> { typedef f32x8 type; };
+
+// acc += A_frag (16 x 32) * B_frag (32 x 16), operands in the layout above.
+__device__ __forceinline__ f32x4 mma16(const bf16x8& a, const bf16x8& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma16(const f32x8& a, const f32x8& b, f32x4 c) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+  return c;
+}
+
+// Scalar conversions.
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+// 16-byte vectors: 8 bf16 or 4 float.
+template <typename T> struct Vec16;
+template <> struct Vec16<bf16> {
+  static constexpr int N = 8;
+  typedef bf16x8 type;
+};
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  typedef f32x4 type;
+};
+
+template <typename T>
+__device__ __forceinline__ typename Vec16<T>::type load16(const T* p) {
+  return *reinterpret_cast<const typename Vec16<T>::type*>(p);
+}
+template <typename T>
+__device__ __forceinline__ void store16(T* p, const typename Vec16<T>::type& v) {
+  *reinterpret_cast<typename Vec16<T>::type*>(p) = v;
+}
+
+// Store four consecutive values converted to T (8 bytes for bf16, 16 for f32).
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  f32x4 v = {a, b, c, d};
+  *reinterpret_cast<f32x4*>(p) = v;
+}
+__device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float d) {
+  bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
+  *reinterpret_cast<bf16x4*>(p) = v;
+}
+// Load four consecutive values as float.
+__device__ __forceinline__ f32x4 load4f(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ f32x4 load4f(const bf16* p) {
+  bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  f32x4 r = {(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+  return r;
+}
+
+// Wave-wide reductions over all 64 lanes.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+__device__ __forceinline__ float sigmoidf_(float u) {
+  // 1 / (1 + e^-u) for u >= 0 and e^u / (1 + e^u) for u < 0: both forms only
+  // ever exponentiate -|u|, so neither overflows nor cancels.
+  float e = __expf(-fabsf(u));
+  float r = 1.0f / (1.0f + e);
+  return u >= 0.0f ? r : e * r;
+}
+
+// Fragment loads from LDS: 8 consecutive elements (16 bytes for bf16, 32 for
+// f32; the f32 case is read as two 16-byte halves so that only 16-byte
+// alignment is needed).
+__device__ __forceinline__ bf16x8 load_frag(const bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+__device__ __forceinline__ f32x8 load_frag(const float* p) {
+  f32x4 lo = *reinterpret_cast<const f32x4*>(p);
+  f32x4 hi = *reinterpret_cast<const f32x4*>(p + 4);
+  f32x8 r = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return r;
+}
+// Fragment made of two runs of four consecutive elements (p[0..3], q[0..3]).
+__device__ __forceinline__ bf16x8 load_frag_split(const bf16* p, const bf16* q) {
+  bf16x4 a = *reinterpret_cast<const bf16x4*>(p);
+  bf16x4 b = *reinterpret_cast<const bf16x4*>(q);
+  bf16x8 r = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return r;
+}
+__device__ __forceinline__ f32x8 load_frag_split(const float* p, const float* q) {
+  f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  f32x4 b = *reinterpret_cast<const f32x4*>(q);
+  f32x8 r = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return r;
+}
+// Fragment from two f32x4 register tiles, converted to T.
+template <typename T> __device__ __forceinline__ typename Frag<T>::type frag_from(const f32x4& a, const f32x4& b);
+template <> __device__ __forceinline__ bf16x8 frag_from<bf16>(const f32x4& a, const f32x4& b) {
+  bf16x8 r = {(bf16)a[0], (bf16)a[1], (bf16)a[2], (bf16)a[3], (bf16)b[0], (bf16)b[1], (bf16)b[2], (bf16)b[3]};
+  return r;
+}
+template <> __device__ __forceinline__ f32x8 frag_from<float>(const f32x4& a, const f32x4& b) {
+  f32x8 r = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return r;
+}
+
+}  // namespace bcmt

@@ -1,0 +1,98 @@
+// Host-side launchers of the BCMT kernels (internal to the library).
+// Every launcher enqueues on the given stream and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bcmt {
+
+enum class DType { F32 = 0, BF16 = 1 };
+
+// ------------------------------------------------------------------ GEMM
+// C[m, n] = sum_k A(m, k) * B(k, n), float32 accumulation.
+//   A(m, k) = A[m * lda + k]            (a_mcontig = false)
+//           = A[k * lda + m]            (a_mcontig = true)
+//   B(k, n) = Bseg[n * ldb + k]         (b_ncontig = false)
+//           = Bseg[k * ldb + n]         (b_ncontig = true)
+// B may be split into up to three pointers along N (seg = kSegN) or along K
+// (seg = kSegK), each covering seg_len indices; the index inside a pointer is
+// the global index minus seg * seg_len.
+// Contiguous dimensions (K when an operand is K-contiguous, M or N
+// otherwise) must be multiples of 8 elements.
+enum { kSegNone = 0, kSegN = 1, kSegK = 2 };
+
+struct GemmDesc {
+  int M, N, K;
+  const void* A;
+  int64_t lda;
+  bool a_mcontig;
+  const void* B[3];
+  int64_t ldb;
+  bool b_ncontig;
+  int seg;
+  int seg_len;
+  int splits;  // split-K factor (only for the atomic epilogue)
+};
+
+// Plain store: C = acc (+ add), C in the compute type or float32.
+hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_f32,
+                      const void* add, int64_t ld_add, hipStream_t s);
+
+// Float32 atomic accumulation into up to three outputs split along N.
+hipError_t gemm_atomic(DType dt, const GemmDesc& g, float* C0, float* C1, float* C2,
+                       int64_t ldc, int seg_len_n, hipStream_t s);
+
+// Gate + injection epilogue (forward): U = acc;
+//   G = sigmoid(U); Y = H + G * Mc[blk(t)] (+ X); G is stored for backward.
+// Mc[b, i] = P[b, i - 1] for i >= 1 and 0 for i = 0 (the one-block shift).
+struct GateEpi {
+  void* Y;
+  void* G;
+  const void* H;
+  const void* X;     // nullable: residual off
+  const float* P;    // [B * nb, D] projected memory
+  int T, L, nb, D;
+};
+hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t s);
+
+// Backward of the local representation: dH = acc + dY + a_t * dS[blk] + ds_t * wp.
+struct HbarEpi {
+  void* dH;
+  const void* dY;
+  const float* a;     // [B*T] pooling weights
+  const float* ds;    // [B*T] pooling-score gradients
+  const float* dS;    // [B * nb, D] summary gradients
+  const void* wp;     // [D]
+  int T, L, nb, D;
+};
+hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t s);
+
+// ------------------------------------------------------------------ attention
+// qkv: [B, T, 3D] (Q | K | V), head h at columns h*64 .. h*64+63 of each.
+hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D,
+                    int H, int L, hipStream_t s);
+// Backward in two passes: dQ (also writes delta_t = dO_t . O_t), then dK/dV.
+hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* dout,
+                       const float* lse, float* delta, void* dqkv, int B, int T, int D, int H,
+                       int L, hipStream_t s);
+hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
+                         const float* delta, void* dqkv, int B, int T, int D, int H, int L,
+                         hipStream_t s);
+
+// ------------------------------------------------------------------ memory path
+int pool_chunks(int L);
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* part,
+                    int B, int T, int D, int L, hipStream_t s);
+hipError_t scan_fwd(DType dt, const float* part, float* S, float* M, void* Mt, float* stats,
+                    int B, int T, int D, int L, float gamma, hipStream_t s);
+hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
+                    void* Pbar, int B, int T, int D, int L, hipStream_t s);
+hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,
+                   int D, float gamma, hipStream_t s);
+hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
+                    const float* S, const float* dS, const void* wp, float* a_out,
+                    float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s);
+hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
+
+}  // namespace bcmt

@@ -1,0 +1,527 @@
+// The memory path of the layer: adaptive block summaries (Sec. 3.4), the
+// normalised exponential causal memory (Sec. 3.5) and the bandwidth-bound
+// parts of the backward pass.
+//
+// All of these stream [B, T, D] activations once and keep block-level
+// quantities ([B, N_b, D], float32) tiny, so they are written for coalesced
+// 16-byte row accesses and wave-level reductions, not for the matrix cores.
+//
+// Decay recurrences.  With Z_i = sum_{j<=i} g^(i-j) and N_i = sum_{j<=i}
+// g^(i-j) S_j (0-based blocks), the memory is M_i = N_i / Z_i and
+//   N_i = g N_{i-1} + S_i,  Z_i = g Z_{i-1} + 1.
+// One workgroup owns 32 feature columns of one batch element over all blocks:
+// eight segments of consecutive blocks are folded locally, the segment
+// carries are combined in LDS, and each segment is replayed with its carry.
+// No workgroup ever waits on another.
+#include "common.h"
+#include "kernels.h"
+
+namespace bcmt {
+namespace {
+
+constexpr int kPoolTok = 32;  // tokens per pooling workgroup
+
+__device__ __forceinline__ float block_reduce_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float s = 0.f;
+  const int nw = blockDim.x >> 6;
+  for (int w = 0; w < nw; ++w) s += red[w];
+  return s;
+}
+
+// ------------------------------------------------------------------ pooling (forward)
+// Workgroup = (32-token chunk, block, batch).  Each wave takes every fourth
+// token: score s_t = H[t] . w_p (wave reduction), then an online softmax
+// accumulation of sum_t e^(s_t - m) H[t].  The four waves are merged in LDS
+// and the chunk's (m, l, partial sum) is written for the scan to combine.
+template <typename T, int NVJ>
+__global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
+                                                       const T* __restrict__ wp,
+                                                       float* __restrict__ s_out,
+                                                       float* __restrict__ part, int Tn, int D,
+                                                       int L, int nb, int nch) {
+  constexpr int VE = Vec16<T>::N;
+  typedef typename Vec16<T>::type vec;
+  extern __shared__ float red[];  // [4][D] partial sums, then [4][2] stats
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+  const int bs = i * L;
+  const int be = min(bs + L, Tn);
+  const int t0 = bs + c * kPoolTok;
+  const int t1 = min(t0 + kPoolTok, be);
+  const int Dv = D / VE;
+
+  float w[NVJ][VE], acc[NVJ][VE];
+#pragma unroll
+  for (int j = 0; j < NVJ; ++j) {
+    const int v = lane + 64 * j;
+    vec wv = v < Dv ? load16(wp + v * VE) : vec{};
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      w[j][e] = to_f32(wv[e]);
+      acc[j][e] = 0.f;
+    }
+  }
+  float mw = -INFINITY, lw = 0.f;
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const T* row = H + ((int64_t)b * Tn + t) * D;
+    float hv[NVJ][VE];
+    float dot = 0.f;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j) {
+      const int v = lane + 64 * j;
+      vec x = v < Dv ? load16(row + v * VE) : vec{};
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        hv[j][e] = to_f32(x[e]);
+        dot += w[j][e] * hv[j][e];
+      }
+    }
+    dot = wave_sum(dot);
+    if (lane == 0) s_out[(int64_t)b * Tn + t] = dot;
+    const float mnew = fmaxf(mw, dot);
+    const float sc = __expf(mw - mnew);
+    const float p = __expf(dot - mnew);
+    lw = lw * sc + p;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[j][e] = acc[j][e] * sc + p * hv[j][e];
+    mw = mnew;
+  }
+  float* stat = red + 4 * D;
+#pragma unroll
+  for (int j = 0; j < NVJ; ++j) {
+    const int v = lane + 64 * j;
+    if (v < Dv) {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) red[wave * D + v * VE + e] = acc[j][e];
+    }
+  }
+  if (lane == 0) {
+    stat[wave * 2] = mw;
+    stat[wave * 2 + 1] = lw;
+  }
+  __syncthreads();
+  float mm = -INFINITY;
+  for (int k = 0; k < 4; ++k) mm = fmaxf(mm, stat[k * 2]);
+  float sc[4];
+  float lsum = 0.f;
+  for (int k = 0; k < 4; ++k) {
+    sc[k] = stat[k * 2] == -INFINITY ? 0.f : __expf(stat[k * 2] - mm);
+    lsum += sc[k] * stat[k * 2 + 1];
+  }
+  float* out = part + ((int64_t)(b * nb + i) * nch + c) * (D + 2);
+  for (int col = tid; col < D; col += blockDim.x) {
+    float s = 0.f;
+    for (int k = 0; k < 4; ++k) s += sc[k] * red[k * D + col];
+    out[2 + col] = s;
+  }
+  if (tid == 0) {
+    out[0] = mm;
+    out[1] = lsum;
+  }
+}
+
+// ------------------------------------------------------------------ chunk merge + decayed scan
+template <typename T>
+__global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__ part, int nch,
+                                                       float* __restrict__ S,
+                                                       float* __restrict__ M, T* __restrict__ Mt,
+                                                       float* __restrict__ stats, int nb, int D,
+                                                       float gamma) {
+  __shared__ float cN[8][32];
+  __shared__ float cZ[8], cG[8];
+  const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
+  const int col = blockIdx.x * 32 + cl;
+  const int b = blockIdx.y;
+  const bool act = col < D;
+  const int SL = (nb + 7) / 8;
+  const int i0 = seg * SL;
+  const int i1 = min(nb, i0 + SL);
+  const int64_t pstride = D + 2;
+
+  float N = 0.f, Z = 0.f, g = 1.f;
+  for (int i = i0; i < i1; ++i) {
+    const float* pb = part + (int64_t)(b * nb + i) * nch * pstride;
+    float mm = -INFINITY;
+    for (int c = 0; c < nch; ++c) mm = fmaxf(mm, pb[c * pstride]);
+    float l = 0.f, s = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const float mc = pb[c * pstride];
+      const float w = mc == -INFINITY ? 0.f : __expf(mc - mm);
+      l += w * pb[c * pstride + 1];
+      if (act) s += w * pb[c * pstride + 2 + col];
+    }
+    s = s / l;
+    if (act) S[(int64_t)(b * nb + i) * D + col] = s;
+    if (blockIdx.x == 0 && cl == 0) {
+      stats[(int64_t)(b * nb + i) * 2] = mm;
+      stats[(int64_t)(b * nb + i) * 2 + 1] = l;
+    }
+    N = gamma * N + s;
+    Z = gamma * Z + 1.f;
+    g *= gamma;
+  }
+  cN[seg][cl] = N;
+  if (cl == 0) {
+    cZ[seg] = Z;
+    cG[seg] = g;
+  }
+  __syncthreads();
+  float Nin = 0.f, Zin = 0.f;
+  for (int k = 0; k < seg; ++k) {
+    Nin = cG[k] * Nin + cN[k][cl];
+    Zin = cG[k] * Zin + cZ[k];
+  }
+  if (!act) return;
+  N = Nin;
+  Z = Zin;
+  for (int i = i0; i < i1; ++i) {
+    const int64_t off = (int64_t)(b * nb + i) * D + col;
+    N = gamma * N + S[off];
+    Z = gamma * Z + 1.f;
+    const float m = N / Z;
+    M[off] = m;
+    Mt[off] = from_f32<T>(m);
+  }
+}
+
+// ------------------------------------------------------------------ gate backward
+// dU = dY * Mc * G (1 - G) per element, and the block sum of dY * G, which is
+// the gradient of the shifted memory.  Workgroup = (64 column vectors, block,
+// batch); four token groups reduce through LDS.  The block sums are written
+// already shifted back by one block (row i-1 holds block i's sum; the last
+// row of each batch element is zero), in the compute type, as the left
+// operand of the W_m backward products.
+template <typename T>
+__global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
+                                                       const T* __restrict__ G,
+                                                       const float* __restrict__ P,
+                                                       T* __restrict__ dU, T* __restrict__ Pbar,
+                                                       int Tn, int D, int L, int nb) {
+  constexpr int VE = Vec16<T>::N;
+  typedef typename Vec16<T>::type vec;
+  __shared__ float red[4][64 * VE];
+  const int tid = threadIdx.x, lane = tid & 63, tg = tid >> 6;
+  const int vi = blockIdx.x * 64 + lane;
+  const int i = blockIdx.y, b = blockIdx.z;
+  const int Dv = D / VE;
+  const bool act = vi < Dv;
+  const int col = vi * VE;
+  const int bs = i * L;
+  const int be = min(bs + L, Tn);
+  float c[VE], acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    c[e] = 0.f;
+    acc[e] = 0.f;
+  }
+  if (act && i > 0) {
+    const float* pp = P + (int64_t)(b * nb + i - 1) * D + col;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) c[e] = pp[e];
+  }
+  if (act) {
+    for (int t = bs + tg; t < be; t += 4) {
+      const int64_t off = ((int64_t)b * Tn + t) * D + col;
+      const vec dy = load16(dY + off);
+      const vec g = load16(G + off);
+      vec du;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        const float y = to_f32(dy[e]), gg = to_f32(g[e]);
+        du[e] = from_f32<T>(y * c[e] * gg * (1.f - gg));
+        acc[e] += y * gg;
+      }
+      store16(dU + off, du);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VE; ++e) red[tg][lane * VE + e] = acc[e];
+  __syncthreads();
+  if (tg == 0 && act) {
+    vec o;
+#pragma unroll
+    for (int e = 0; e < VE; ++e)
+      o[e] = from_f32<T>(red[0][lane * VE + e] + red[1][lane * VE + e] + red[2][lane * VE + e] +
+                         red[3][lane * VE + e]);
+    if (i > 0) store16(Pbar + (int64_t)(b * nb + i - 1) * D + col, o);
+    else store16(Pbar + (int64_t)(b * nb + nb - 1) * D + col, vec{});
+  }
+}
+
+// ------------------------------------------------------------------ memory backward
+// Given dM (the gradient of the normalised memory, last block zero):
+//   dS_i = sum_{k>=i} g^(k-i) dM_k / Z_k                       (reverse scan)
+//   dg   = sum_{i>=1} dN_i . N_{i-1} + dZ_i Z_{i-1},  with
+//   dN_i = dS_i and dZ_i = sum_{k>=i} g^(k-i) (-dM_k . M_k / Z_k).
+// The per-column part of dZ is scanned like dS; its dot over the columns is
+// taken with the final reduction.
+__device__ __forceinline__ float zsum(int i, float gamma) {
+  // Z_i = 1 + g + ... + g^i (0-based i).
+  if (gamma == 0.f) return 1.f;
+  return (1.f - powf(gamma, (float)(i + 1))) / (1.f - gamma);
+}
+
+__global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ Mbar,
+                                                      const float* __restrict__ M,
+                                                      float* __restrict__ dS,
+                                                      float* __restrict__ dgamma, int nb, int D,
+                                                      float gamma) {
+  __shared__ float cQ[8][32], cE[8][32];
+  __shared__ float cG[8];
+  __shared__ float red[4];
+  const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
+  const int col = blockIdx.x * 32 + cl;
+  const int b = blockIdx.y;
+  const bool act = col < D;
+  const int SL = (nb + 7) / 8;
+  const int i0 = seg * SL;
+  const int i1 = min(nb, i0 + SL);
+
+  float Q = 0.f, E = 0.f, g = 1.f;
+  for (int i = i1 - 1; i >= i0; --i) {
+    const int64_t off = (int64_t)(b * nb + i) * D + col;
+    const float mb = act ? Mbar[off] : 0.f;
+    const float m = act ? M[off] : 0.f;
+    const float z = zsum(i, gamma);
+    Q = mb / z + gamma * Q;
+    E = -mb * m / z + gamma * E;
+    g *= gamma;
+  }
+  cQ[seg][cl] = Q;
+  cE[seg][cl] = E;
+  if (cl == 0) cG[seg] = g;
+  __syncthreads();
+  float Qin = 0.f, Ein = 0.f;
+  for (int k = 7; k > seg; --k) {
+    Qin = cG[k] * Qin + cQ[k][cl];
+    Ein = cG[k] * Ein + cE[k][cl];
+  }
+  Q = Qin;
+  E = Ein;
+  float acc = 0.f;
+  if (act) {
+    for (int i = i1 - 1; i >= i0; --i) {
+      const int64_t off = (int64_t)(b * nb + i) * D + col;
+      const float mb = Mbar[off];
+      const float z = zsum(i, gamma);
+      Q = mb / z + gamma * Q;
+      E = -mb * M[off] / z + gamma * E;
+      dS[off] = Q;
+      if (i >= 1) {
+        const float zp = zsum(i - 1, gamma);
+        acc += Q * (M[off - D] * zp) + E * zp;
+      }
+    }
+  }
+  const float tot = block_reduce_sum(acc, red);
+  if (threadIdx.x == 0 && dgamma) unsafeAtomicAdd(dgamma, tot);
+}
+
+// ------------------------------------------------------------------ pooling backward
+// With a_t the block softmax weights and dS_i the summary gradient:
+//   ds_t = a_t (dS_i . H[t] - dS_i . S_i),  dw_p = sum_t ds_t H[t].
+// The per-token a_t and ds_t feed the dH epilogue of the W_g backward product.
+template <typename T, int NVJ>
+__global__ __launch_bounds__(256) void pool_bwd_kernel(
+    const T* __restrict__ H, const float* __restrict__ s_in, const float* __restrict__ stats,
+    const float* __restrict__ S, const float* __restrict__ dS, float* __restrict__ a_out,
+    float* __restrict__ ds_out, float* __restrict__ dwp, int Tn, int D, int L, int nb) {
+  constexpr int VE = Vec16<T>::N;
+  typedef typename Vec16<T>::type vec;
+  extern __shared__ float red[];  // [4][D]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+  const int bs = i * L;
+  const int be = min(bs + L, Tn);
+  const int t0 = bs + c * kPoolTok;
+  const int t1 = min(t0 + kPoolTok, be);
+  const int Dv = D / VE;
+  const int64_t brow = (int64_t)(b * nb + i) * D;
+
+  float g[NVJ][VE], acc[NVJ][VE];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NVJ; ++j) {
+    const int v = lane + 64 * j;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const bool ok = v < Dv;
+      g[j][e] = ok ? dS[brow + v * VE + e] : 0.f;
+      ss += ok ? g[j][e] * S[brow + v * VE + e] : 0.f;
+      acc[j][e] = 0.f;
+    }
+  }
+  ss = wave_sum(ss);
+  const float mi = stats[(int64_t)(b * nb + i) * 2];
+  const float li = stats[(int64_t)(b * nb + i) * 2 + 1];
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const T* row = H + ((int64_t)b * Tn + t) * D;
+    float hv[NVJ][VE];
+    float dot = 0.f;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j) {
+      const int v = lane + 64 * j;
+      vec x = v < Dv ? load16(row + v * VE) : vec{};
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        hv[j][e] = to_f32(x[e]);
+        dot += g[j][e] * hv[j][e];
+      }
+    }
+    dot = wave_sum(dot);
+    const int64_t ti = (int64_t)b * Tn + t;
+    const float a = __expf(s_in[ti] - mi) / li;
+    const float dst = a * (dot - ss);
+    if (lane == 0) {
+      a_out[ti] = a;
+      ds_out[ti] = dst;
+    }
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[j][e] += dst * hv[j][e];
+  }
+#pragma unroll
+  for (int j = 0; j < NVJ; ++j) {
+    const int v = lane + 64 * j;
+    if (v < Dv) {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) red[wave * D + v * VE + e] = acc[j][e];
+    }
+  }
+  __syncthreads();
+  if (dwp) {
+    for (int col = tid; col < D; col += blockDim.x) {
+      const float s = red[col] + red[D + col] + red[2 * D + col] + red[3 * D + col];
+      if (s != 0.f) unsafeAtomicAdd(dwp + col, s);
+    }
+  }
+}
+
+__global__ void fill_kernel(float* p, int64_t n, float v) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (int64_t)gridDim.x * blockDim.x)
+    p[k] = v;
+}
+
+int nvj_for(int Dv) {
+  const int n = (Dv + 63) / 64;
+  return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
+}
+
+template <typename E>
+hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* part, int B, int T,
+                      int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int nch = pool_chunks(L < T ? L : T);
+  dim3 grid(nch, nb, B);
+  const size_t lds = (4 * (size_t)D + 8) * sizeof(float);
+  const int nvj = nvj_for(D / Vec16<E>::N);
+#define POOL_FWD(NV)                                                                         \
+  hipLaunchKernelGGL((pool_fwd_kernel<E, NV>), grid, dim3(256), lds, s, (const E*)H,       \
+                     (const E*)wp, s_out, part, T, D, L, nb, nch)
+  switch (nvj) {
+    case 1: POOL_FWD(1); break;
+    case 2: POOL_FWD(2); break;
+    case 4: POOL_FWD(4); break;
+    case 8: POOL_FWD(8); break;
+    default: POOL_FWD(16); break;
+  }
+#undef POOL_FWD
+  return hipGetLastError();
+}
+
+template <typename E>
+hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, const float* S,
+                      const float* dS, float* a_out, float* ds_out, float* dwp, int B, int T,
+                      int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int nch = pool_chunks(L < T ? L : T);
+  dim3 grid(nch, nb, B);
+  const size_t lds = 4 * (size_t)D * sizeof(float);
+  const int nvj = nvj_for(D / Vec16<E>::N);
+#define POOL_BWD(NV)                                                                          \
+  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), grid, dim3(256), lds, s, (const E*)H, s_in,  \
+                     stats, S, dS, a_out, ds_out, dwp, T, D, L, nb)
+  switch (nvj) {
+    case 1: POOL_BWD(1); break;
+    case 2: POOL_BWD(2); break;
+    case 4: POOL_BWD(4); break;
+    case 8: POOL_BWD(8); break;
+    default: POOL_BWD(16); break;
+  }
+#undef POOL_BWD
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int pool_chunks(int L) { return (L + kPoolTok - 1) / kPoolTok; }
+
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* part, int B,
+                    int T, int D, int L, hipStream_t s) {
+  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, part, B, T, D, L, s);
+  return pool_fwd_t<float>(H, wp, s_out, part, B, T, D, L, s);
+}
+
+hipError_t scan_fwd(DType dt, const float* part, float* S, float* M, void* Mt, float* stats,
+                    int B, int T, int D, int L, float gamma, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int nch = pool_chunks(L < T ? L : T);
+  dim3 grid((D + 31) / 32, B);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, part, nch, S, M, (bf16*)Mt,
+                       stats, nb, D, gamma);
+  else
+    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, part, nch, S, M,
+                       (float*)Mt, stats, nb, D, gamma);
+  return hipGetLastError();
+}
+
+hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
+                    void* Pbar, int B, int T, int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  if (dt == DType::BF16) {
+    dim3 grid((D / 8 + 63) / 64, nb, B);
+    hipLaunchKernelGGL(gate_bwd_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)dY,
+                       (const bf16*)G, P, (bf16*)dU, (bf16*)Pbar, T, D, L, nb);
+  } else {
+    dim3 grid((D / 4 + 63) / 64, nb, B);
+    hipLaunchKernelGGL(gate_bwd_kernel<float>, grid, dim3(256), 0, s, (const float*)dY,
+                       (const float*)G, P, (float*)dU, (float*)Pbar, T, D, L, nb);
+  }
+  return hipGetLastError();
+}
+
+hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,
+                   int D, float gamma, hipStream_t s) {
+  dim3 grid((D + 31) / 32, B);
+  hipLaunchKernelGGL(mem_bwd_kernel, grid, dim3(256), 0, s, Mbar, M, dS, dgamma, nb, D, gamma);
+  return hipGetLastError();
+}
+
+hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
+                    const float* S, const float* dS, const void* wp, float* a_out,
+                    float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s) {
+  (void)wp;
+  if (dt == DType::BF16)
+    return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+  return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+}
+
+hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+}  // namespace bcmt

@@ -1,0 +1,67 @@
+"""Device buffers around one BCMT layer, for callers that hold torch tensors.
+
+Allocates the `saved` activations and the two workspaces through torch's
+allocator (plumbing only) and forwards to the C ABI in ``bcmt``.  The layer's
+arithmetic runs entirely in the library's HIP kernels.
+"""
+
+import numpy as np
+import torch
+
+from . import bcmt as abi
+
+TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def to_device(arr, dtype, device="cuda"):
+    """numpy float32 values -> device tensor of the compute type (exact when
+    the values are already representable, as the seeded inputs are)."""
+    t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(device)
+    return t.to(TORCH_DTYPE[dtype]).contiguous()
+
+
+def to_host64(t):
+    """Device tensor -> float64 numpy array."""
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+class LayerBuffers:
+    """Holds a config, device weights and the scratch buffers of one layer."""
+
+    def __init__(self, B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False,
+                 accumulate=False, device="cuda"):
+        self.dtype = dtype
+        self.device = device
+        self.cfg = abi.make_config(B, T, D, H, L, gamma, dtype, residual, accumulate)
+        st = abi.bcmt_validate(self.cfg)
+        if st != abi.BCMT_OK:
+            raise abi.BcmtError(st, "bcmt_validate")
+        self.shape = (B, T, D)
+        u8 = dict(dtype=torch.uint8, device=device)
+        self.saved = torch.empty(abi.bcmt_saved_bytes(self.cfg), **u8)
+        self.ws_fwd = torch.empty(max(256, abi.bcmt_workspace_bytes(self.cfg, abi.BCMT_PASS_FORWARD)), **u8)
+        self.ws_bwd = torch.empty(max(256, abi.bcmt_workspace_bytes(self.cfg, abi.BCMT_PASS_BACKWARD)), **u8)
+        self.params = None
+
+    def set_params(self, weights):
+        """weights: dict of numpy float32 arrays (input-major [D, D], wp [D])."""
+        self.params = {k: to_device(weights[k], self.dtype, self.device) for k in abi.PARAM_NAMES}
+        return self.params
+
+    def new_activation(self):
+        return torch.empty(self.shape, dtype=TORCH_DTYPE[self.dtype], device=self.device)
+
+    def new_grads(self):
+        D = self.shape[2]
+        f = dict(dtype=torch.float32, device=self.device)
+        g = {n: torch.zeros((D, D), **f) for n in ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg")}
+        g["dwp"] = torch.zeros((D,), **f)
+        g["dgamma"] = torch.zeros((4,), **f)  # 16 bytes, value in element 0
+        return g
+
+    def forward(self, X, Y, stream=None):
+        abi.bcmt_layer_forward(self.cfg, X, self.params, Y, self.saved, self.ws_fwd, stream=stream)
+
+    def backward(self, X, dY, dX, grads, stream=None):
+        abi.bcmt_layer_backward(self.cfg, X, self.params, self.saved, dY, dX, grads, self.ws_bwd,
+                                stream=stream)

@@ -1,0 +1,164 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before any HIP call (no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_13578_amd import bcmt as abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bcmt.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(abi.LIB_PATH):
+        from paper_2608_13578_amd.build import build
+        build()
+    return abi.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bcmt_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_abi():
+    names = declared_functions()
+    assert set(names) == set(abi.EXPORTED), names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = os.popen(f"nm -D --defined-only {abi.LIB_PATH}").read()
+    for name in declared_functions():
+        assert re.search(rf"\bT {name}$", out, flags=re.M), name
+
+
+def test_version_and_strerror(lib):
+    assert abi.bcmt_version() >= 100
+    for code in (0, -1, -2, -3, -4):
+        assert isinstance(abi.bcmt_strerror(code), str) and abi.bcmt_strerror(code)
+    assert abi.bcmt_strerror(-99) == "unknown status"
+
+
+def good(**kw):
+    base = dict(B=2, T=256, D=128, H=2, L=64, gamma=0.8, dtype="bf16")
+    base.update(kw)
+    return abi.make_config(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), abi.BCMT_OK),
+    (dict(dtype="f32"), abi.BCMT_OK),
+    (dict(L=10000), abi.BCMT_OK),           # one block
+    (dict(T=1000, L=128), abi.BCMT_OK),     # ragged last block
+    (dict(gamma=0.0), abi.BCMT_OK),
+    (dict(B=0), abi.BCMT_ERR_INVALID),
+    (dict(T=0), abi.BCMT_ERR_INVALID),
+    (dict(L=0), abi.BCMT_ERR_INVALID),
+    (dict(H=3), abi.BCMT_ERR_INVALID),      # D % H != 0
+    (dict(gamma=1.0), abi.BCMT_ERR_INVALID),
+    (dict(gamma=-0.1), abi.BCMT_ERR_INVALID),
+    (dict(gamma=float("nan")), abi.BCMT_ERR_INVALID),
+    (dict(D=256, H=2), abi.BCMT_ERR_UNSUPPORTED),  # head width 128
+    (dict(D=4096, H=64), abi.BCMT_ERR_UNSUPPORTED),
+])
+def test_validate(lib, kw, code):
+    assert abi.bcmt_validate(good(**kw)) == code
+
+
+def test_validate_rejects_bad_dtype_and_flags(lib):
+    c = good()
+    c.dtype = 7
+    assert abi.bcmt_validate(c) == abi.BCMT_ERR_INVALID
+    c = good()
+    c.flags = 8
+    assert abi.bcmt_validate(c) == abi.BCMT_ERR_INVALID
+    assert lib.bcmt_validate(None) == abi.BCMT_ERR_INVALID
+
+
+def test_sizes(lib):
+    c = good()
+    saved = abi.bcmt_saved_bytes(c)
+    B, T, D = 2, 256, 128
+    assert saved >= (3 + 3) * B * T * D * 2          # qkv, o, h, g in bf16
+    assert abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_INFERENCE) == \
+        abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_FORWARD) + saved
+    assert abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_BACKWARD) > 0
+    assert abi.bcmt_workspace_bytes(c, 9) == 0
+    f32 = good(dtype="f32")
+    assert abi.bcmt_saved_bytes(f32) > saved
+    bad = good(B=0)
+    assert abi.bcmt_saved_bytes(bad) == 0 and abi.bcmt_workspace_bytes(bad, 0) == 0
+
+
+# Fake, aligned device addresses: every call below must fail its argument
+# checks before touching them.
+A = 1 << 40
+
+
+def _params(**override):
+    p = {n: A + 0x100000 * (i + 1) for i, n in enumerate(abi.PARAM_NAMES)}
+    p.update(override)
+    return abi.bcmt_params(*[p[n] for n in abi.PARAM_NAMES])
+
+
+def _fwd(cfg, X=A, params=None, Y=A + 0x10000000, saved=A + 0x20000000, ws=A + 0x40000000,
+         ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = abi.bcmt_workspace_bytes(cfg, abi.BCMT_PASS_FORWARD)
+    return abi.lib().bcmt_layer_forward(ctypes.byref(cfg), X, ctypes.byref(params or _params()),
+                                        Y, saved, ws, ws_bytes, None)
+
+
+def test_forward_argument_errors(lib):
+    c = good()
+    assert _fwd(good(B=0)) == abi.BCMT_ERR_INVALID
+    assert _fwd(good(D=256, H=2)) == abi.BCMT_ERR_UNSUPPORTED
+    assert _fwd(c, X=None) == abi.BCMT_ERR_INVALID
+    assert _fwd(c, Y=None) == abi.BCMT_ERR_INVALID
+    assert _fwd(c, params=_params(Wm=None)) == abi.BCMT_ERR_INVALID
+    assert _fwd(c, params=_params(wp=A + 8)) == abi.BCMT_ERR_INVALID      # misaligned
+    assert _fwd(c, X=A + 4) == abi.BCMT_ERR_INVALID
+    assert _fwd(c, Y=A) == abi.BCMT_ERR_INVALID                            # Y aliases X
+    assert _fwd(c, Y=A + 1024) == abi.BCMT_ERR_INVALID                     # Y overlaps X
+    assert _fwd(c, ws=None) == abi.BCMT_ERR_INVALID
+    need = abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_FORWARD)
+    assert _fwd(c, ws_bytes=need - 1) == abi.BCMT_ERR_WORKSPACE
+    # inference (no saved) needs the larger workspace
+    assert _fwd(c, saved=None, ws_bytes=need) == abi.BCMT_ERR_WORKSPACE
+    assert lib.bcmt_layer_forward(None, A, ctypes.byref(_params()), A + 0x10000000, None,
+                                  A + 0x40000000, 1 << 30, None) == abi.BCMT_ERR_INVALID
+
+
+def _bwd(cfg, X=A, saved=A + 0x20000000, dY=A + 0x30000000, dX=A + 0x38000000, grads=None,
+         ws=A + 0x40000000, ws_bytes=None, params=None):
+    if ws_bytes is None:
+        ws_bytes = abi.bcmt_workspace_bytes(cfg, abi.BCMT_PASS_BACKWARD)
+    g = grads
+    return abi.lib().bcmt_layer_backward(ctypes.byref(cfg), X, ctypes.byref(params or _params()),
+                                         saved, dY, dX, ctypes.byref(g) if g else None, ws,
+                                         ws_bytes, None)
+
+
+def test_backward_argument_errors(lib):
+    c = good()
+    assert _bwd(good(T=0)) == abi.BCMT_ERR_INVALID
+    assert _bwd(c, saved=None) == abi.BCMT_ERR_INVALID
+    assert _bwd(c, dY=None) == abi.BCMT_ERR_INVALID
+    assert _bwd(c, X=None) == abi.BCMT_ERR_INVALID
+    assert _bwd(c, dX=A + 0x30000000) == abi.BCMT_ERR_INVALID             # dX aliases dY
+    assert _bwd(c, dX=A + 2) == abi.BCMT_ERR_INVALID
+    assert _bwd(c, ws=None) == abi.BCMT_ERR_INVALID
+    need = abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_BACKWARD)
+    assert _bwd(c, ws_bytes=need - 256) == abi.BCMT_ERR_WORKSPACE
+    g = abi.bcmt_grads(*([A + 0x50000000 + 0x1000000 * i for i in range(7)] + [A + 0x60000002]))
+    assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dgamma misaligned
+    g = abi.bcmt_grads(*([A + 0x50000008] + [None] * 7))
+    assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dWq misaligned
