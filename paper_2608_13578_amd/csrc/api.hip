@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -40,7 +41,7 @@ struct Plan {
   // forward scratch
   size_t part, fwd_bytes;
   // backward scratch
-  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, bwd_bytes;
+  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, wpart, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -87,6 +88,13 @@ struct Plan {
     dout = take(BTD * es);
     delta = take((size_t)B * H * T * 4);
     dqkv = take(3 * BTD * es);
+    {
+      const int BTi = B * T, BNi = B * nb;
+      size_t w = gemm_wgrad_partial_bytes(D, 3 * D, BTi);
+      w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
+      w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
+      wpart = take(w);
+    }
     bwd_bytes = off;
   }
 };
@@ -114,12 +122,6 @@ bool overlaps(const void* a, const void* b, size_t n) {
   return x < y + n && y < x + n;
 }
 
-int split_for(int tiles, int K) {
-  int s = (512 + tiles - 1) / tiles;
-  const int kmax = K / 256;
-  if (s > kmax) s = kmax;
-  return s < 1 ? 1 : s;
-}
 
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
@@ -356,21 +358,19 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   const DType dt = p.dt;
   const bool residual = cfg->flags & BCMT_FLAG_RESIDUAL;
 
-  if (!(cfg->flags & BCMT_FLAG_ACCUM_WGRAD)) {
-    float* mats[6] = {gr.dWq, gr.dWk, gr.dWv, gr.dWo, gr.dWm, gr.dWg};
-    for (float* m : mats)
-      if (m) LAUNCH(ST_ZERO, fill_f32(m, (int64_t)D * D, 0.f, s));
-    if (gr.dwp) LAUNCH(ST_ZERO, fill_f32(gr.dwp, D, 0.f, s));
-    if (gr.dgamma) LAUNCH(ST_ZERO, fill_f32(gr.dgamma, 1, 0.f, s));
-  }
+  const bool accum = cfg->flags & BCMT_FLAG_ACCUM_WGRAD;
+  float* wpart = (float*)(W + p.wpart);
+  // dwp and dgamma are reduced with atomics; the weight matrices are written
+  // (or accumulated) by the split-K reductions.
+  if (!accum && (gr.dwp || gr.dgamma))
+    LAUNCH(ST_ZERO, zero_two(gr.dwp, D, gr.dgamma, 1, s));
 
   // Gate and injection: dU, and the block sums of dY * G shifted back by one.
   LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar, p.B, p.T, D,
                   p.L, s));
   if (gr.dWg) {
-    GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0,
-               split_for(((D + 127) / 128) * ((D + 127) / 128), BT)};
-    LAUNCH(ST_WG_WGRAD, gemm_atomic(dt, g, gr.dWg, nullptr, nullptr, D, D, s));
+    GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    LAUNCH(ST_WG_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWg, nullptr, nullptr, D, D, accum, s));
   }
   // Memory projection: dM = dP Wm^T and dWm = M^T dP.
   {
@@ -379,9 +379,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     LAUNCH(ST_WM_DGRAD, gemm_store(dt, g, W + p.mbar, D, true, nullptr, 0, s));
   }
   if (gr.dWm) {
-    GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0,
-               split_for(((D + 127) / 128) * ((D + 127) / 128), BN)};
-    LAUNCH(ST_WM_WGRAD, gemm_atomic(dt, g, gr.dWm, nullptr, nullptr, D, D, s));
+    GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    LAUNCH(ST_WM_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWm, nullptr, nullptr, D, D, accum, s));
   }
   // Decayed reverse scan: dS and the decay gradient.
   LAUNCH(ST_MEM_BWD, mem_bwd((const float*)(W + p.mbar), (const float*)(SV + p.M), (float*)(W + p.dS),
@@ -403,9 +402,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
   }
   if (gr.dWo) {
-    GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0,
-               split_for(((D + 127) / 128) * ((D + 127) / 128), BT)};
-    LAUNCH(ST_WO_WGRAD, gemm_atomic(dt, g, gr.dWo, nullptr, nullptr, D, D, s));
+    GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    LAUNCH(ST_WO_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWo, nullptr, nullptr, D, D, accum, s));
   }
   // Block-local attention backward.
   LAUNCH(ST_ATTN_BWD_DQ,
@@ -421,9 +419,9 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     LAUNCH(ST_DX, gemm_store(dt, g, dX, D, false, residual ? dY : nullptr, D, s));
   }
   if (gr.dWq || gr.dWk || gr.dWv) {
-    GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone, 0,
-               split_for(((D + 127) / 128) * ((3 * D + 127) / 128), BT)};
-    LAUNCH(ST_QKV_WGRAD, gemm_atomic(dt, g, gr.dWq, gr.dWk, gr.dWv, D, D, s));
+    GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone, 0, 1};
+    LAUNCH(ST_QKV_WGRAD,
+           gemm_wgrad(dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D, accum, s));
   }
   return BCMT_OK;
 }

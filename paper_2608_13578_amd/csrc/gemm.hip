@@ -210,19 +210,38 @@ struct EpiStore {
   }
 };
 
-struct EpiAtomic {
-  float* C[3];
-  int64_t ldc;
-  int seg;
+// Split-K partial tile: split z of an M x N product goes to P + z * M * N.
+struct EpiPartial {
+  float* P;
+  int64_t ld;
+  int64_t split_stride;
   __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
-    const int s = n / seg;
-    float* base = C[s];
-    if (!base) return;
-    float* p = base + (int64_t)m * ldc + (n - s * seg);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) unsafeAtomicAdd(p + r, v[r]);
+    store4(P + blockIdx.z * split_stride + (int64_t)m * ld + n, v[0], v[1], v[2], v[3]);
   }
 };
+
+// Sums the split-K partials (4 consecutive columns per thread) and writes or
+// accumulates into the output segment that holds column n.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, int splits,
+                                                           int M, int N, float* C0, float* C1,
+                                                           float* C2, int64_t ldc, int seg,
+                                                           int accumulate) {
+  const int64_t total = (int64_t)M * N / 4;
+  const int64_t stride = (int64_t)M * N;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    f32x4 acc = *reinterpret_cast<const f32x4*>(P + i * 4);
+    for (int z = 1; z < splits; ++z) acc += *reinterpret_cast<const f32x4*>(P + z * stride + i * 4);
+    const int64_t e = i * 4;
+    const int m = (int)(e / N), n = (int)(e - (int64_t)m * N);
+    const int sg = n / seg;
+    float* base = sg == 0 ? C0 : sg == 1 ? C1 : C2;
+    if (!base) continue;
+    f32x4* dst = reinterpret_cast<f32x4*>(base + (int64_t)m * ldc + (n - sg * seg));
+    if (accumulate) acc += *dst;
+    *dst = acc;
+  }
+}
 
 template <typename T>
 struct EpiGate {
@@ -267,6 +286,209 @@ struct EpiHbar {
   }
 };
 
+// ------------------------------------------------------------------ pipelined bf16 kernel
+// The bf16 path streams K slabs of 64 through a ring of STAGES LDS buffers
+// with direct global->LDS loads (each 16-byte load lands at base + 16*lane
+// of its instruction's 1 KB LDS window), so no register holds operand data
+// on its way in and the loads for slab k + STAGES - 1 are in flight while
+// slab k is multiplied.
+//
+// LDS keeps every operand in its global orientation:
+//   K-contiguous operand: [rows][64] with the 16-byte chunk c of row r
+//     holding global chunk c ^ ((r / 2) % 8); a fragment is one 16-byte read.
+//   M/N-contiguous operand: [64][rows] with chunk c of k-row kr holding
+//     global chunk c ^ (kr % 16); a fragment is two ds_read_b64_tr_b16
+//     reads.  That instruction hands lane i of each 16-lane group element
+//     (i % 4) of the 4-element rows read by lanes 4j + i/4, j = 0..3; with
+//     lane q addressing k-row k0 + q/4 at column c0 + 4 (q % 4), lane i
+//     receives the four k values k0..k0+3 of column c0 + i, which is the
+//     matrix instruction's operand layout.
+// The XOR swizzles spread the 16 rows (or k-rows) a fragment read touches
+// over distinct LDS banks.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+template <int R, bool RCONTIG, int SEG>
+struct PipeOperand {
+  static constexpr int BK = 64;
+  static constexpr int ELEMS = R * BK;
+  static constexpr int INSTR = ELEMS / 512;  // 1 KB per wave-wide load
+
+  // Issue this wave's share of the direct loads of one slab.
+  template <int NW>
+  __device__ __forceinline__ static void issue(const Operand<bf16, RCONTIG, SEG>& op, bf16* dst,
+                                               int r0, int rmax, int k0, int wave, int lane) {
+    static_assert(INSTR % NW == 0, "loads per wave");
+#pragma unroll
+    for (int i = 0; i < INSTR / NW; ++i) {
+      const int gi = wave * (INSTR / NW) + i;
+      const bf16* src;
+      if constexpr (!RCONTIG) {
+        const int row = gi * 8 + (lane >> 3);
+        const int cg = (lane & 7) ^ ((row >> 1) & 7);
+        const int gr = min(r0 + row, rmax - 1);
+        src = op.at(gr, k0 + cg * 8);
+      } else {
+        constexpr int CPR = R / 8;        // 16-byte chunks per k-row
+        constexpr int RPI = 64 / CPR;     // k-rows per instruction
+        static_assert(CPR >= 16 && 64 % CPR == 0, "row width");
+        const int kr = gi * RPI + lane / CPR;
+        const int cg = (lane % CPR) ^ (kr & 15);
+        const int gc = min(r0 + cg * 8, rmax - 8);
+        src = op.at(gc, k0 + kr);
+      }
+      __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(dst + gi * 512), 16, 0, 0);
+    }
+  }
+
+  // Fragment for rows/columns base .. base+15 of the tile, 32-wide K step ks.
+  __device__ __forceinline__ static bf16x8 frag(const bf16* s, int base, int ks, int lane) {
+    const int lr = lane & 15, lg = lane >> 4;
+    if constexpr (!RCONTIG) {
+      const int r = base + lr;
+      const int c = (ks * 4 + lg) ^ ((r >> 1) & 7);
+      return *reinterpret_cast<const bf16x8*>(s + r * BK + c * 8);
+    } else {
+      const int col = base + (lr & 3) * 4;
+      bf16x4 h[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int kr = ks * 32 + lg * 8 + hh * 4 + (lr >> 2);
+        const int c = (col >> 3) ^ (kr & 15);
+        h[hh] = lds_read_tr(s + kr * R + c * 8 + (col & 7));
+      }
+      bf16x8 r = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
+      return r;
+    }
+  }
+};
+
+// Tile order.  Workgroups are dealt to the chip's 8 XCDs round-robin in
+// launch order, and each XCD has its own L2.  The launch-order index is
+// mapped so that every XCD works through one contiguous run of the tile
+// sequence, and the sequence walks groups of kGroupM tile rows column by
+// column: the ~32 tiles an XCD holds at once then share a few A row panels
+// and B column panels in that XCD's L2.
+constexpr int kXcds = 8;
+constexpr int kGroupM = 4;
+
+__device__ __forceinline__ void xcd_tile_order(int bx, int by, int nx, int ny, int& tm, int& tn) {
+  const int ntiles = nx * ny;
+  const int bid = by * nx + bx;
+  const int xcd = bid % kXcds, pos = bid / kXcds;
+  const int q = ntiles / kXcds, r = ntiles % kXcds;
+  const int t = xcd < r ? xcd * (q + 1) + pos : r * (q + 1) + (xcd - r) * q + pos;
+  const int group = kGroupM * nx;
+  const int first = (t / group) * kGroupM;
+  const int gm = min(ny - first, kGroupM);
+  const int in = t % group;
+  tm = first + in % gm;
+  tn = in / gm;
+}
+
+template <int BM, int BN, int STAGES, int WGM, int WGN, bool A_MC, bool B_NC, int BSEG, class Epi>
+__global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, int K,
+                                                                Operand<bf16, A_MC, kSegNone> A,
+                                                                Operand<bf16, B_NC, BSEG> B,
+                                                                int kchunk, Epi epi) {
+  constexpr int BK = 64;
+  constexpr int NW = WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  typedef PipeOperand<BM, A_MC, kSegNone> PA;
+  typedef PipeOperand<BN, B_NC, BSEG> PB;
+  constexpr int STAGE = PA::ELEMS + PB::ELEMS;
+  constexpr int NI = (PA::INSTR + PB::INSTR) / NW;  // loads per wave per slab
+  __shared__ __attribute__((aligned(1024))) bf16 lds[STAGES * STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  int tm, tn;
+  xcd_tile_order(blockIdx.x, blockIdx.y, gridDim.x, gridDim.y, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = blockIdx.z * kchunk;
+  const int kend = min(K, kbeg + kchunk);
+  const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st) {
+    if (st < nk) {
+      bf16* sa = lds + st * STAGE;
+      PA::template issue<NW>(A, sa, m0, M, kbeg + st * BK, wave, lane);
+      PB::template issue<NW>(B, sa + PA::ELEMS, n0, N, kbeg + st * BK, wave, lane);
+    }
+  }
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // Slab kt must have landed; slabs kt+1 .. may stay in flight.
+    const int after = min(nk - 1, kt + STAGES - 2) - kt;
+    if constexpr (STAGES >= 4) {
+      if (after >= 2) wait_vmcnt<2 * NI>();
+      else if (after == 1) wait_vmcnt<NI>();
+      else wait_vmcnt<0>();
+    } else if constexpr (STAGES == 3) {
+      if (after >= 1) wait_vmcnt<NI>();
+      else wait_vmcnt<0>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    // Every wave has waited for its own loads of slab kt; the barrier makes
+    // all of them visible and retires all reads of the buffer reloaded next.
+    // (A plain s_barrier: __syncthreads would also drain the later slabs.)
+    __builtin_amdgcn_s_barrier();
+    const int nxt = kt + STAGES - 1;
+    if (nxt < nk) {
+      bf16* sa = lds + (nxt % STAGES) * STAGE;
+      PA::template issue<NW>(A, sa, m0, M, kbeg + nxt * BK, wave, lane);
+      PB::template issue<NW>(B, sa + PA::ELEMS, n0, N, kbeg + nxt * BK, wave, lane);
+    }
+    const bf16* sa = lds + (kt % STAGES) * STAGE;
+    const bf16* sb = sa + PA::ELEMS;
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8 fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) fa[i] = PA::frag(sa, wm * WTM + i * 16, ks, lane);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[j] = PB::frag(sb, wn * WTN + j * 16, ks, lane);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mma16(fb[j], fa[i], acc[i][j]);
+    }
+  }
+
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = m0 + wm * WTM + i * 16 + lr;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WTN + j * 16 + lg * 4;
+      if (m < M && n < N) epi(m, n, acc[i][j]);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ launch
 
 template <typename T, bool AMC, bool BNC, int SEG, class Epi>
@@ -279,6 +501,7 @@ hipError_t launch(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   int kchunk = (g.K + splits - 1) / splits;
   kchunk = (kchunk + BK - 1) / BK * BK;
   if (kchunk < BK) kchunk = BK;
+  if (g.kchunk > 0) kchunk = g.kchunk;
   splits = (g.K + kchunk - 1) / kchunk;
   if (splits < 1) splits = 1;
   dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, splits);
@@ -287,12 +510,41 @@ hipError_t launch(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Pipelined bf16 launch: 128 x 128 tiles, 2 x 2 waves, two 32 KB slabs in
+// flight, so that two workgroups share a CU (measured faster on these shapes
+// than a deeper ring with one workgroup per CU).  Needs the K range of every
+// split to be a whole number of 64-wide slabs.
+template <bool AMC, bool BNC, int SEG, class Epi>
+hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  constexpr int PBM = 128, PBN = 128, ST = 2, WGM = 2, WGN = 2;
+  Operand<bf16, AMC, kSegNone> A{{(const bf16*)g.A, nullptr, nullptr}, g.lda, 0};
+  Operand<bf16, BNC, SEG> B{{(const bf16*)g.B[0], (const bf16*)g.B[1], (const bf16*)g.B[2]}, g.ldb,
+                            g.seg_len};
+  int splits = g.splits < 1 ? 1 : g.splits;
+  int kchunk = (g.K + splits - 1) / splits;
+  kchunk = (kchunk + 63) / 64 * 64;
+  if (g.kchunk > 0) kchunk = g.kchunk;
+  splits = (g.K + kchunk - 1) / kchunk;
+  dim3 grid((g.N + PBN - 1) / PBN, (g.M + PBM - 1) / PBM, splits);
+  hipLaunchKernelGGL((gemm_pipe_kernel<PBM, PBN, ST, WGM, WGN, AMC, BNC, SEG, Epi>), grid,
+                     dim3(WGM * WGN * 64), 0, s, g.M, g.N, g.K, A, B, kchunk, epi);
+  return hipGetLastError();
+}
+
+template <typename T, bool AMC, bool BNC, int SEG, class Epi>
+hipError_t launch_any(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (g.K % 64 == 0) return launch_pipe<AMC, BNC, SEG>(g, epi, s);
+  }
+  return launch<T, AMC, BNC, SEG>(g, epi, s);
+}
+
 template <typename T, class Epi>
 hipError_t dispatch_store(const GemmDesc& g, const Epi& epi, hipStream_t s) {
-  if (!g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch<T, false, true, kSegNone>(g, epi, s);
-  if (!g.a_mcontig && g.b_ncontig && g.seg == kSegN) return launch<T, false, true, kSegN>(g, epi, s);
-  if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegNone) return launch<T, false, false, kSegNone>(g, epi, s);
-  if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegK) return launch<T, false, false, kSegK>(g, epi, s);
+  if (!g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, true, kSegNone>(g, epi, s);
+  if (!g.a_mcontig && g.b_ncontig && g.seg == kSegN) return launch_any<T, false, true, kSegN>(g, epi, s);
+  if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, false, kSegNone>(g, epi, s);
+  if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegK) return launch_any<T, false, false, kSegK>(g, epi, s);
   return hipErrorInvalidValue;
 }
 
@@ -308,26 +560,60 @@ hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_
   return dispatch_store<float>(g, EpiStore<float, float>{(float*)C, ldc, (const float*)add, ld_add}, s);
 }
 
-hipError_t gemm_atomic(DType dt, const GemmDesc& g, float* C0, float* C1, float* C2, int64_t ldc,
-                       int seg_len_n, hipStream_t s) {
-  if (g.M <= 0 || g.N <= 0 || g.K <= 0) return hipSuccess;
-  if (!(g.a_mcontig && g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
-  EpiAtomic e{{C0, C1, C2}, ldc, seg_len_n};
-  if (dt == DType::BF16) return launch<bf16, true, true, kSegNone>(g, e, s);
-  return launch<float, true, true, kSegNone>(g, e, s);
+// Split count for the weight-gradient products: about two workgroups per CU
+// of 128 x 128 tiles, each split at least 512 deep in K (a multiple of 64).
+static int wgrad_splits(int M, int N, int K, int* kchunk) {
+  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int sp = (512 + tiles - 1) / tiles;
+  const int kmax = K / 512;
+  if (sp > kmax) sp = kmax;
+  if (sp < 1) sp = 1;
+  int kc = (K + sp - 1) / sp;
+  kc = (kc + 63) / 64 * 64;
+  *kchunk = kc;
+  return (K + kc - 1) / kc;
+}
+
+size_t gemm_wgrad_partial_bytes(int M, int N, int K) {
+  int kc;
+  const int sp = wgrad_splits(M, N, K, &kc);
+  return (size_t)sp * M * N * sizeof(float);
+}
+
+hipError_t gemm_wgrad(DType dt, const GemmDesc& g0, float* partial, float* C0, float* C1,
+                      float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s) {
+  if (g0.M <= 0 || g0.N <= 0) return hipSuccess;
+  if (!(g0.a_mcontig && g0.b_ncontig && g0.seg == kSegNone)) return hipErrorInvalidValue;
+  if (g0.N % 4 != 0 || seg_len_n % 4 != 0) return hipErrorInvalidValue;
+  GemmDesc g = g0;
+  int kc;
+  g.splits = wgrad_splits(g.M, g.N, g.K, &kc);
+  g.kchunk = kc;  // exactly g.splits slices of `partial` get written
+  EpiPartial e{partial, g.N, (int64_t)g.M * g.N};
+  hipError_t err = dt == DType::BF16 ? launch_any<bf16, true, true, kSegNone>(g, e, s)
+                                     : launch<float, true, true, kSegNone>(g, e, s);
+  if (err != hipSuccess) return err;
+  // Splits whose K range is empty (K == 0) wrote zeros through the epilogue.
+  const int64_t total = (int64_t)g.M * g.N / 4;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, partial,
+                     g.splits, g.M, g.N, C0, C1, C2, ldc, seg_len_n, accumulate ? 1 : 0);
+  return hipGetLastError();
 }
 
 hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (!(!g.a_mcontig && g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
-  if (dt == DType::BF16) return launch<bf16, false, true, kSegNone>(g, EpiGate<bf16>{e}, s);
+  if (dt == DType::BF16) return launch_any<bf16, false, true, kSegNone>(g, EpiGate<bf16>{e}, s);
   return launch<float, false, true, kSegNone>(g, EpiGate<float>{e}, s);
 }
 
 hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (!(!g.a_mcontig && !g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
-  if (dt == DType::BF16) return launch<bf16, false, false, kSegNone>(g, EpiHbar<bf16>{e}, s);
+  if (dt == DType::BF16) return launch_any<bf16, false, false, kSegNone>(g, EpiHbar<bf16>{e}, s);
   return launch<float, false, false, kSegNone>(g, EpiHbar<float>{e}, s);
 }
 

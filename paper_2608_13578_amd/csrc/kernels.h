@@ -32,16 +32,22 @@ struct GemmDesc {
   bool b_ncontig;
   int seg;
   int seg_len;
-  int splits;  // split-K factor (only for the atomic epilogue)
+  int splits;  // split-K factor
+  int kchunk;  // if > 0: K range per split (a multiple of 64), overriding splits
 };
 
 // Plain store: C = acc (+ add), C in the compute type or float32.
 hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_f32,
                       const void* add, int64_t ld_add, hipStream_t s);
 
-// Float32 atomic accumulation into up to three outputs split along N.
-hipError_t gemm_atomic(DType dt, const GemmDesc& g, float* C0, float* C1, float* C2,
-                       int64_t ldc, int seg_len_n, hipStream_t s);
+// Weight-gradient product (large K): split-K partial tiles written to
+// `partial` (float32), then a reduction over the splits that writes, or
+// with `accumulate` adds into, up to three outputs split along N (a null
+// output is skipped).  The split count is chosen here; g.splits is ignored.
+// Deterministic: no atomics.
+size_t gemm_wgrad_partial_bytes(int M, int N, int K);
+hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
+                      float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s);
 
 // Gate + injection epilogue (forward): U = acc;
 //   G = sigmoid(U); Y = H + G * Mc[blk(t)] (+ X); G is stored for backward.
@@ -94,5 +100,7 @@ hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* sta
                     const float* S, const float* dS, const void* wp, float* a_out,
                     float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s);
 hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
+// Zeroes two small float32 buffers in one launch (either may be null).
+hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);
 
 }  // namespace bcmt

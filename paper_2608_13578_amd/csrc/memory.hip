@@ -405,6 +405,17 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(
   }
 }
 
+__global__ void zero_two_kernel(float* a, int64_t na, float* b, int64_t nb) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < na + nb;
+       k += (int64_t)gridDim.x * blockDim.x) {
+    if (k < na) {
+      if (a) a[k] = 0.f;
+    } else if (b) {
+      b[k - na] = 0.f;
+    }
+  }
+}
+
 __global__ void fill_kernel(float* p, int64_t n, float v) {
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (int64_t)gridDim.x * blockDim.x)
@@ -514,6 +525,15 @@ hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* sta
   if (dt == DType::BF16)
     return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
   return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+}
+
+hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {
+  const int64_t n = na + nb;
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(zero_two_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, na, b, nb);
+  return hipGetLastError();
 }
 
 hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s) {
