@@ -33,13 +33,13 @@ constexpr int kMaxD = 2048;
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
-  int B, T, D, H, L, nb, nch;
+  int B, T, D, H, L, nb;
   size_t es;
   DType dt;
   // saved (forward -> backward)
   size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
   // forward scratch
-  size_t part, fwd_bytes;
+  size_t mpart, fwd_bytes;
   // backward scratch
   size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, wpart, bwd_bytes;
 
@@ -50,7 +50,6 @@ struct Plan {
     H = c.H;
     L = c.L;
     nb = (T + L - 1) / L;
-    nch = pool_chunks(L < T ? L : T);
     dt = c.dtype == BCMT_BF16 ? DType::BF16 : DType::F32;
     es = dt == DType::BF16 ? 2 : 4;
     const size_t BT = (size_t)B * T, BTD = BT * D, BND = (size_t)B * nb * D;
@@ -74,7 +73,7 @@ struct Plan {
     saved_bytes = off;
 
     off = 0;
-    part = take((size_t)B * nb * nch * (D + 2) * 4);
+    mpart = take(gemm_splitk_partial_bytes(B * nb, D, D, 64));
     fwd_bytes = off;
 
     off = 0;
@@ -93,6 +92,7 @@ struct Plan {
       size_t w = gemm_wgrad_partial_bytes(D, 3 * D, BTi);
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
+      w = std::max(w, gemm_splitk_partial_bytes(BNi, D, D, 64));
       wpart = take(w);
     }
     bwd_bytes = off;
@@ -306,15 +306,17 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
     LAUNCH(ST_WO, gemm_store(dt, g, SV + p.h, D, false, nullptr, 0, s));
   }
   // 4-5. Adaptive summaries (Sec. 3.4) and the exponential memory (Sec. 3.5).
-  LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, prm->wp, (float*)(SV + p.s), (float*)(W + p.part), p.B, p.T, D,
-                  p.L, s));
-  LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(W + p.part), (float*)(SV + p.S), (float*)(SV + p.M),
-                  SV + p.Mt, (float*)(SV + p.stats), p.B, p.T, D, p.L, cfg->gamma, s));
+  LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, prm->wp, (float*)(SV + p.s), (float*)(SV + p.S),
+                               (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
+  LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(SV + p.S), (float*)(SV + p.M), SV + p.Mt, p.B,
+                               p.T, D, p.L, cfg->gamma, s));
   // 6. Memory projection (Sec. 3.5); the shift is applied where P is read.
   {
+    // Only B * N_b rows: split K so that every workgroup has one or two slabs.
     GemmDesc g{p.B * p.nb, D, D, SV + p.Mt, D, false, {prm->Wm, nullptr, nullptr}, D, true,
                kSegNone, 0, 1};
-    LAUNCH(ST_WM, gemm_store(dt, g, SV + p.P, D, true, nullptr, 0, s));
+    LAUNCH(ST_WM, gemm_splitk(dt, g, (float*)(W + p.mpart), (float*)(SV + p.P), nullptr, nullptr,
+                              D, D, false, 64, s));
   }
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
@@ -376,7 +378,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   {
     GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
                1};
-    LAUNCH(ST_WM_DGRAD, gemm_store(dt, g, W + p.mbar, D, true, nullptr, 0, s));
+    LAUNCH(ST_WM_DGRAD, gemm_splitk(dt, g, wpart, (float*)(W + p.mbar), nullptr, nullptr, D, D,
+                                    false, 64, s));
   }
   if (gr.dWm) {
     GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0, 1};

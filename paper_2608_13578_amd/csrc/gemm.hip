@@ -560,12 +560,15 @@ hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_
   return dispatch_store<float>(g, EpiStore<float, float>{(float*)C, ldc, (const float*)add, ld_add}, s);
 }
 
-// Split count for the weight-gradient products: about two workgroups per CU
-// of 128 x 128 tiles, each split at least 512 deep in K (a multiple of 64).
-static int wgrad_splits(int M, int N, int K, int* kchunk) {
+namespace {
+
+// Split-K plan: about two workgroups per CU of 128 x 128 tiles, every split
+// at least min_k deep in K (rounded to a multiple of 64).  Returns the number
+// of splits; *kchunk is the K range of each.
+static int splitk_plan(int M, int N, int K, int min_k, int* kchunk) {
   const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int sp = (512 + tiles - 1) / tiles;
-  const int kmax = K / 512;
+  const int kmax = K / min_k;
   if (sp > kmax) sp = kmax;
   if (sp < 1) sp = 1;
   int kc = (K + sp - 1) / sp;
@@ -574,26 +577,58 @@ static int wgrad_splits(int M, int N, int K, int* kchunk) {
   return (K + kc - 1) / kc;
 }
 
-size_t gemm_wgrad_partial_bytes(int M, int N, int K) {
-  int kc;
-  const int sp = wgrad_splits(M, N, K, &kc);
-  return (size_t)sp * M * N * sizeof(float);
+// Writes (or accumulates into) up to three float32 outputs split along N.
+struct EpiSegOut {
+  float* C[3];
+  int64_t ldc;
+  int seg;
+  int accumulate;
+  __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
+    const int sg = n / seg;
+    float* base = C[sg];
+    if (!base) return;
+    f32x4* dst = reinterpret_cast<f32x4*>(base + (int64_t)m * ldc + (n - sg * seg));
+    if (accumulate) v += *dst;
+    *dst = v;
+  }
+};
+
+template <typename T, class Epi>
+hipError_t dispatch_any(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  if (g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch_any<T, true, true, kSegNone>(g, epi, s);
+  if (!g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, true, kSegNone>(g, epi, s);
+  if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, false, kSegNone>(g, epi, s);
+  return hipErrorInvalidValue;
 }
 
-hipError_t gemm_wgrad(DType dt, const GemmDesc& g0, float* partial, float* C0, float* C1,
-                      float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s) {
+}  // namespace
+
+size_t gemm_splitk_partial_bytes(int M, int N, int K, int min_k) {
+  int kc;
+  const int sp = splitk_plan(M, N, K, min_k, &kc);
+  return sp > 1 ? (size_t)sp * M * N * sizeof(float) : 0;
+}
+
+size_t gemm_wgrad_partial_bytes(int M, int N, int K) {
+  return gemm_splitk_partial_bytes(M, N, K, 512);
+}
+
+hipError_t gemm_splitk(DType dt, const GemmDesc& g0, float* partial, float* C0, float* C1,
+                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
+                       hipStream_t s) {
   if (g0.M <= 0 || g0.N <= 0) return hipSuccess;
-  if (!(g0.a_mcontig && g0.b_ncontig && g0.seg == kSegNone)) return hipErrorInvalidValue;
-  if (g0.N % 4 != 0 || seg_len_n % 4 != 0) return hipErrorInvalidValue;
+  if (g0.N % 4 != 0 || seg_len_n % 4 != 0 || g0.seg != kSegNone) return hipErrorInvalidValue;
   GemmDesc g = g0;
   int kc;
-  g.splits = wgrad_splits(g.M, g.N, g.K, &kc);
+  g.splits = splitk_plan(g.M, g.N, g.K, min_k, &kc);
   g.kchunk = kc;  // exactly g.splits slices of `partial` get written
+  if (g.splits == 1) {
+    EpiSegOut e{{C0, C1, C2}, ldc, seg_len_n, accumulate ? 1 : 0};
+    return dt == DType::BF16 ? dispatch_any<bf16>(g, e, s) : dispatch_any<float>(g, e, s);
+  }
   EpiPartial e{partial, g.N, (int64_t)g.M * g.N};
-  hipError_t err = dt == DType::BF16 ? launch_any<bf16, true, true, kSegNone>(g, e, s)
-                                     : launch<float, true, true, kSegNone>(g, e, s);
+  hipError_t err = dt == DType::BF16 ? dispatch_any<bf16>(g, e, s) : dispatch_any<float>(g, e, s);
   if (err != hipSuccess) return err;
-  // Splits whose K range is empty (K == 0) wrote zeros through the epilogue.
   const int64_t total = (int64_t)g.M * g.N / 4;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 2048) blocks = 2048;
@@ -601,6 +636,12 @@ hipError_t gemm_wgrad(DType dt, const GemmDesc& g0, float* partial, float* C0, f
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, partial,
                      g.splits, g.M, g.N, C0, C1, C2, ldc, seg_len_n, accumulate ? 1 : 0);
   return hipGetLastError();
+}
+
+hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
+                      float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s) {
+  if (!(g.a_mcontig && g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
+  return gemm_splitk(dt, g, partial, C0, C1, C2, ldc, seg_len_n, accumulate, 512, s);
 }
 
 hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t s) {

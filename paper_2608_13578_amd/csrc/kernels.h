@@ -46,6 +46,13 @@ hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_
 // output is skipped).  The split count is chosen here; g.splits is ignored.
 // Deterministic: no atomics.
 size_t gemm_wgrad_partial_bytes(int M, int N, int K);
+// General split-K product into float32 outputs (any layout without B
+// segments), every split at least min_k deep; with a single split the
+// outputs are written directly and `partial` is unused.
+size_t gemm_splitk_partial_bytes(int M, int N, int K, int min_k);
+hipError_t gemm_splitk(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
+                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
+                       hipStream_t s);
 hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s);
 
@@ -87,11 +94,13 @@ hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const floa
                          hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
-int pool_chunks(int L);
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* part,
+// Pooling: scores s [B*T], summaries S [B*nb, D] and per-block softmax
+// statistics (max, normaliser) [B*nb, 2].
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, float* stats,
                     int B, int T, int D, int L, hipStream_t s);
-hipError_t scan_fwd(DType dt, const float* part, float* S, float* M, void* Mt, float* stats,
-                    int B, int T, int D, int L, float gamma, hipStream_t s);
+// Decayed scan of the summaries: M (float32) and its compute-type copy Mt.
+hipError_t scan_fwd(DType dt, const float* S, float* M, void* Mt, int B, int T, int D, int L,
+                    float gamma, hipStream_t s);
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, int B, int T, int D, int L, hipStream_t s);
 hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,

@@ -19,7 +19,13 @@
 namespace bcmt {
 namespace {
 
-constexpr int kPoolTok = 32;  // tokens per pooling workgroup
+// Pooling and gate kernels use one workgroup per (block, batch element):
+// up to 16 waves, each wave taking TB tokens at a time (their rows are loaded
+// together, then reduced together), so that enough loads are in flight per
+// CU; the block-level reductions finish in LDS without a second pass.
+
+// Tokens a wave loads at once for rows of NVJ 16-byte vectors per lane.
+template <int NVJ> struct TokBatch { static constexpr int TB = NVJ >= 4 ? 2 : (NVJ == 2 ? 4 : 8); };
 
 __device__ __forceinline__ float block_reduce_sum(float v, float* red) {
   v = wave_sum(v);
@@ -34,25 +40,26 @@ __device__ __forceinline__ float block_reduce_sum(float v, float* red) {
 }
 
 // ------------------------------------------------------------------ pooling (forward)
-// Workgroup = (32-token chunk, block, batch).  Each wave takes every fourth
-// token: score s_t = H[t] . w_p (wave reduction), then an online softmax
-// accumulation of sum_t e^(s_t - m) H[t].  The four waves are merged in LDS
-// and the chunk's (m, l, partial sum) is written for the scan to combine.
+// s_t = H[t] . w_p; a = softmax of s over the block; S_i = sum_t a_t H[t].
+// Each wave keeps a running (max, sum, weighted row sum) over its tokens; the
+// waves are merged in LDS.  Writes s (for the backward), S_i and the block's
+// softmax statistics (max, normaliser).
 template <typename T, int NVJ>
-__global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
-                                                       const T* __restrict__ wp,
-                                                       float* __restrict__ s_out,
-                                                       float* __restrict__ part, int Tn, int D,
-                                                       int L, int nb, int nch) {
+__global__ __launch_bounds__(1024) void pool_fwd_kernel(const T* __restrict__ H,
+                                                        const T* __restrict__ wp,
+                                                        float* __restrict__ s_out,
+                                                        float* __restrict__ S,
+                                                        float* __restrict__ stats, int Tn, int D,
+                                                        int L, int nb) {
   constexpr int VE = Vec16<T>::N;
+  constexpr int TB = TokBatch<NVJ>::TB;
   typedef typename Vec16<T>::type vec;
-  extern __shared__ float red[];  // [4][D] partial sums, then [4][2] stats
+  extern __shared__ float red[];  // [nw][D] partial sums, then [nw][2] stats
+  const int nw = blockDim.x >> 6;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+  const int i = blockIdx.x, b = blockIdx.y;
   const int bs = i * L;
   const int be = min(bs + L, Tn);
-  const int t0 = bs + c * kPoolTok;
-  const int t1 = min(t0 + kPoolTok, be);
   const int Dv = D / VE;
 
   float w[NVJ][VE], acc[NVJ][VE];
@@ -67,33 +74,49 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
     }
   }
   float mw = -INFINITY, lw = 0.f;
-  for (int t = t0 + wave; t < t1; t += 4) {
-    const T* row = H + ((int64_t)b * Tn + t) * D;
-    float hv[NVJ][VE];
-    float dot = 0.f;
+  for (int t0 = bs + wave * TB; t0 < be; t0 += nw * TB) {
+    vec x[TB][NVJ];
 #pragma unroll
-    for (int j = 0; j < NVJ; ++j) {
-      const int v = lane + 64 * j;
-      vec x = v < Dv ? load16(row + v * VE) : vec{};
+    for (int k = 0; k < TB; ++k)
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        hv[j][e] = to_f32(x[e]);
-        dot += w[j][e] * hv[j][e];
+      for (int j = 0; j < NVJ; ++j) {
+        const int v = lane + 64 * j;
+        x[k][j] = (t0 + k < be && v < Dv) ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE)
+                                          : vec{};
+      }
+    float sc[TB];
+    float mx = mw;
+#pragma unroll
+    for (int k = 0; k < TB; ++k) {
+      float d = 0.f;
+#pragma unroll
+      for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) d += w[j][e] * to_f32(x[k][j][e]);
+      sc[k] = wave_sum(d);
+      if (t0 + k < be) {
+        if (lane == 0) s_out[(int64_t)b * Tn + t0 + k] = sc[k];
+        mx = fmaxf(mx, sc[k]);
       }
     }
-    dot = wave_sum(dot);
-    if (lane == 0) s_out[(int64_t)b * Tn + t] = dot;
-    const float mnew = fmaxf(mw, dot);
-    const float sc = __expf(mw - mnew);
-    const float p = __expf(dot - mnew);
-    lw = lw * sc + p;
+    const float f = __expf(mw - mx);
+    lw *= f;
 #pragma unroll
     for (int j = 0; j < NVJ; ++j)
 #pragma unroll
-      for (int e = 0; e < VE; ++e) acc[j][e] = acc[j][e] * sc + p * hv[j][e];
-    mw = mnew;
+      for (int e = 0; e < VE; ++e) acc[j][e] *= f;
+#pragma unroll
+    for (int k = 0; k < TB; ++k) {
+      const float pk = t0 + k < be ? __expf(sc[k] - mx) : 0.f;
+      lw += pk;
+#pragma unroll
+      for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc[j][e] += pk * to_f32(x[k][j][e]);
+    }
+    mw = mx;
   }
-  float* stat = red + 4 * D;
+  float* stat = red + nw * D;
 #pragma unroll
   for (int j = 0; j < NVJ; ++j) {
     const int v = lane + 64 * j;
@@ -108,32 +131,28 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
   }
   __syncthreads();
   float mm = -INFINITY;
-  for (int k = 0; k < 4; ++k) mm = fmaxf(mm, stat[k * 2]);
-  float sc[4];
+  for (int k = 0; k < nw; ++k) mm = fmaxf(mm, stat[k * 2]);
   float lsum = 0.f;
-  for (int k = 0; k < 4; ++k) {
-    sc[k] = stat[k * 2] == -INFINITY ? 0.f : __expf(stat[k * 2] - mm);
-    lsum += sc[k] * stat[k * 2 + 1];
-  }
-  float* out = part + ((int64_t)(b * nb + i) * nch + c) * (D + 2);
+  for (int k = 0; k < nw; ++k)
+    if (stat[k * 2] != -INFINITY) lsum += __expf(stat[k * 2] - mm) * stat[k * 2 + 1];
+  const float inv = 1.0f / lsum;
   for (int col = tid; col < D; col += blockDim.x) {
-    float s = 0.f;
-    for (int k = 0; k < 4; ++k) s += sc[k] * red[k * D + col];
-    out[2 + col] = s;
+    float sum = 0.f;
+    for (int k = 0; k < nw; ++k)
+      if (stat[k * 2] != -INFINITY) sum += __expf(stat[k * 2] - mm) * red[k * D + col];
+    S[(int64_t)(b * nb + i) * D + col] = sum * inv;
   }
   if (tid == 0) {
-    out[0] = mm;
-    out[1] = lsum;
+    stats[(int64_t)(b * nb + i) * 2] = mm;
+    stats[(int64_t)(b * nb + i) * 2 + 1] = lsum;
   }
 }
 
-// ------------------------------------------------------------------ chunk merge + decayed scan
+// ------------------------------------------------------------------ decayed scan
 template <typename T>
-__global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__ part, int nch,
-                                                       float* __restrict__ S,
+__global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__ S,
                                                        float* __restrict__ M, T* __restrict__ Mt,
-                                                       float* __restrict__ stats, int nb, int D,
-                                                       float gamma) {
+                                                       int nb, int D, float gamma) {
   __shared__ float cN[8][32];
   __shared__ float cZ[8], cG[8];
   const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
@@ -143,27 +162,11 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__
   const int SL = (nb + 7) / 8;
   const int i0 = seg * SL;
   const int i1 = min(nb, i0 + SL);
-  const int64_t pstride = D + 2;
 
   float N = 0.f, Z = 0.f, g = 1.f;
   for (int i = i0; i < i1; ++i) {
-    const float* pb = part + (int64_t)(b * nb + i) * nch * pstride;
-    float mm = -INFINITY;
-    for (int c = 0; c < nch; ++c) mm = fmaxf(mm, pb[c * pstride]);
-    float l = 0.f, s = 0.f;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = pb[c * pstride];
-      const float w = mc == -INFINITY ? 0.f : __expf(mc - mm);
-      l += w * pb[c * pstride + 1];
-      if (act) s += w * pb[c * pstride + 2 + col];
-    }
-    s = s / l;
-    if (act) S[(int64_t)(b * nb + i) * D + col] = s;
-    if (blockIdx.x == 0 && cl == 0) {
-      stats[(int64_t)(b * nb + i) * 2] = mm;
-      stats[(int64_t)(b * nb + i) * 2 + 1] = l;
-    }
-    N = gamma * N + s;
+    const float sv = act ? S[(int64_t)(b * nb + i) * D + col] : 0.f;
+    N = gamma * N + sv;
     Z = gamma * Z + 1.f;
     g *= gamma;
   }
@@ -193,26 +196,29 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__
 
 // ------------------------------------------------------------------ gate backward
 // dU = dY * Mc * G (1 - G) per element, and the block sum of dY * G, which is
-// the gradient of the shifted memory.  Workgroup = (64 column vectors, block,
-// batch); four token groups reduce through LDS.  The block sums are written
+// the gradient of the shifted memory.  Workgroup = (block, batch): thread
+// (token group tg, column vector v) walks every TG-th token of the block four
+// at a time; the TG partial sums meet in LDS.  The block sums are written
 // already shifted back by one block (row i-1 holds block i's sum; the last
 // row of each batch element is zero), in the compute type, as the left
 // operand of the W_m backward products.
 template <typename T>
-__global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
-                                                       const T* __restrict__ G,
-                                                       const float* __restrict__ P,
-                                                       T* __restrict__ dU, T* __restrict__ Pbar,
-                                                       int Tn, int D, int L, int nb) {
+__global__ __launch_bounds__(1024) void gate_bwd_kernel(const T* __restrict__ dY,
+                                                        const T* __restrict__ G,
+                                                        const float* __restrict__ P,
+                                                        T* __restrict__ dU, T* __restrict__ Pbar,
+                                                        int Tn, int D, int L, int nb) {
   constexpr int VE = Vec16<T>::N;
+  constexpr int U = 4;
   typedef typename Vec16<T>::type vec;
-  __shared__ float red[4][64 * VE];
-  const int tid = threadIdx.x, lane = tid & 63, tg = tid >> 6;
-  const int vi = blockIdx.x * 64 + lane;
-  const int i = blockIdx.y, b = blockIdx.z;
+  extern __shared__ float red[];  // [TG][D]
   const int Dv = D / VE;
-  const bool act = vi < Dv;
-  const int col = vi * VE;
+  const int TG = blockDim.x / Dv;
+  const int tid = threadIdx.x;
+  const int v = tid % Dv, tg = tid / Dv;
+  const bool act = tg < TG;
+  const int i = blockIdx.x, b = blockIdx.y;
+  const int col = v * VE;
   const int bs = i * L;
   const int be = min(bs + L, Tn);
   float c[VE], acc[VE];
@@ -227,29 +233,40 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     for (int e = 0; e < VE; ++e) c[e] = pp[e];
   }
   if (act) {
-    for (int t = bs + tg; t < be; t += 4) {
-      const int64_t off = ((int64_t)b * Tn + t) * D + col;
-      const vec dy = load16(dY + off);
-      const vec g = load16(G + off);
-      vec du;
+    for (int t0 = bs + tg; t0 < be; t0 += U * TG) {
+      vec dy[U], g[U];
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        const float y = to_f32(dy[e]), gg = to_f32(g[e]);
-        du[e] = from_f32<T>(y * c[e] * gg * (1.f - gg));
-        acc[e] += y * gg;
+      for (int u = 0; u < U; ++u) {
+        const int t = t0 + u * TG;
+        const int64_t off = ((int64_t)b * Tn + t) * D + col;
+        dy[u] = t < be ? load16(dY + off) : vec{};
+        g[u] = t < be ? load16(G + off) : vec{};
       }
-      store16(dU + off, du);
-    }
-  }
 #pragma unroll
-  for (int e = 0; e < VE; ++e) red[tg][lane * VE + e] = acc[e];
+      for (int u = 0; u < U; ++u) {
+        const int t = t0 + u * TG;
+        vec du;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float y = to_f32(dy[u][e]), gg = to_f32(g[u][e]);
+          du[e] = from_f32<T>(y * c[e] * gg * (1.f - gg));
+          acc[e] += y * gg;
+        }
+        if (t < be) store16(dU + ((int64_t)b * Tn + t) * D + col, du);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < VE; ++e) red[tg * D + col + e] = acc[e];
+  }
   __syncthreads();
-  if (tg == 0 && act) {
+  if (act && tg == 0) {
     vec o;
 #pragma unroll
-    for (int e = 0; e < VE; ++e)
-      o[e] = from_f32<T>(red[0][lane * VE + e] + red[1][lane * VE + e] + red[2][lane * VE + e] +
-                         red[3][lane * VE + e]);
+    for (int e = 0; e < VE; ++e) {
+      float sum = 0.f;
+      for (int k = 0; k < TG; ++k) sum += red[k * D + col + e];
+      o[e] = from_f32<T>(sum);
+    }
     if (i > 0) store16(Pbar + (int64_t)(b * nb + i - 1) * D + col, o);
     else store16(Pbar + (int64_t)(b * nb + nb - 1) * D + col, vec{});
   }
@@ -329,19 +346,19 @@ __global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ 
 //   ds_t = a_t (dS_i . H[t] - dS_i . S_i),  dw_p = sum_t ds_t H[t].
 // The per-token a_t and ds_t feed the dH epilogue of the W_g backward product.
 template <typename T, int NVJ>
-__global__ __launch_bounds__(256) void pool_bwd_kernel(
+__global__ __launch_bounds__(1024) void pool_bwd_kernel(
     const T* __restrict__ H, const float* __restrict__ s_in, const float* __restrict__ stats,
     const float* __restrict__ S, const float* __restrict__ dS, float* __restrict__ a_out,
     float* __restrict__ ds_out, float* __restrict__ dwp, int Tn, int D, int L, int nb) {
   constexpr int VE = Vec16<T>::N;
+  constexpr int TB = TokBatch<NVJ>::TB;
   typedef typename Vec16<T>::type vec;
-  extern __shared__ float red[];  // [4][D]
+  extern __shared__ float red[];  // [nw][D]
+  const int nw = blockDim.x >> 6;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+  const int i = blockIdx.x, b = blockIdx.y;
   const int bs = i * L;
   const int be = min(bs + L, Tn);
-  const int t0 = bs + c * kPoolTok;
-  const int t1 = min(t0 + kPoolTok, be);
   const int Dv = D / VE;
   const int64_t brow = (int64_t)(b * nb + i) * D;
 
@@ -361,32 +378,40 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(
   ss = wave_sum(ss);
   const float mi = stats[(int64_t)(b * nb + i) * 2];
   const float li = stats[(int64_t)(b * nb + i) * 2 + 1];
-  for (int t = t0 + wave; t < t1; t += 4) {
-    const T* row = H + ((int64_t)b * Tn + t) * D;
-    float hv[NVJ][VE];
-    float dot = 0.f;
+  for (int t0 = bs + wave * TB; t0 < be; t0 += nw * TB) {
+    vec x[TB][NVJ];
 #pragma unroll
-    for (int j = 0; j < NVJ; ++j) {
-      const int v = lane + 64 * j;
-      vec x = v < Dv ? load16(row + v * VE) : vec{};
+    for (int k = 0; k < TB; ++k)
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        hv[j][e] = to_f32(x[e]);
-        dot += g[j][e] * hv[j][e];
+      for (int j = 0; j < NVJ; ++j) {
+        const int v = lane + 64 * j;
+        x[k][j] = (t0 + k < be && v < Dv) ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE)
+                                          : vec{};
       }
-    }
-    dot = wave_sum(dot);
-    const int64_t ti = (int64_t)b * Tn + t;
-    const float a = __expf(s_in[ti] - mi) / li;
-    const float dst = a * (dot - ss);
-    if (lane == 0) {
-      a_out[ti] = a;
-      ds_out[ti] = dst;
-    }
 #pragma unroll
-    for (int j = 0; j < NVJ; ++j)
+    for (int k = 0; k < TB; ++k) {
+      float d = 0.f;
 #pragma unroll
-      for (int e = 0; e < VE; ++e) acc[j][e] += dst * hv[j][e];
+      for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) d += g[j][e] * to_f32(x[k][j][e]);
+      d = wave_sum(d);
+      const int t = t0 + k;
+      float dst = 0.f;
+      if (t < be) {
+        const int64_t ti = (int64_t)b * Tn + t;
+        const float a = __expf(s_in[ti] - mi) / li;
+        dst = a * (d - ss);
+        if (lane == 0) {
+          a_out[ti] = a;
+          ds_out[ti] = dst;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc[j][e] += dst * to_f32(x[k][j][e]);
+    }
   }
 #pragma unroll
   for (int j = 0; j < NVJ; ++j) {
@@ -399,8 +424,9 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(
   __syncthreads();
   if (dwp) {
     for (int col = tid; col < D; col += blockDim.x) {
-      const float s = red[col] + red[D + col] + red[2 * D + col] + red[3 * D + col];
-      if (s != 0.f) unsafeAtomicAdd(dwp + col, s);
+      float sum = 0.f;
+      for (int k = 0; k < nw; ++k) sum += red[k * D + col];
+      if (sum != 0.f) unsafeAtomicAdd(dwp + col, sum);
     }
   }
 }
@@ -424,28 +450,52 @@ __global__ void fill_kernel(float* p, int64_t n, float v) {
 
 int nvj_for(int Dv) {
   const int n = (Dv + 63) / 64;
-  return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
+  return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : 8;
+}
+
+// Waves per pooling workgroup: enough to give every wave one token batch,
+// at most 16, and few enough that the per-wave row sums fit in 64 KB of LDS.
+template <int NVJ>
+int pool_waves(int L, int T, int D) {
+  const int lb = L < T ? L : T;
+  const int tb = TokBatch<NVJ>::TB;
+  int w = (lb + tb - 1) / tb;
+  const int wmax = (65536 - 256) / (4 * D + 8);
+  if (w > wmax) w = wmax;
+  return w < 1 ? 1 : (w > 16 ? 16 : w);
+}
+
+template <typename E, int NV>
+hipError_t pool_fwd_nv(const void* H, const void* wp, float* s_out, float* S, float* stats, int B,
+                       int T, int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int nw = pool_waves<NV>(L, T, D);
+  const size_t lds = ((size_t)nw * D + 2 * nw) * sizeof(float);
+  hipLaunchKernelGGL((pool_fwd_kernel<E, NV>), dim3(nb, B), dim3(nw * 64), lds, s, (const E*)H,
+                     (const E*)wp, s_out, S, stats, T, D, L, nb);
+  return hipGetLastError();
 }
 
 template <typename E>
-hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* part, int B, int T,
-                      int D, int L, hipStream_t s) {
-  const int nb = (T + L - 1) / L;
-  const int nch = pool_chunks(L < T ? L : T);
-  dim3 grid(nch, nb, B);
-  const size_t lds = (4 * (size_t)D + 8) * sizeof(float);
-  const int nvj = nvj_for(D / Vec16<E>::N);
-#define POOL_FWD(NV)                                                                         \
-  hipLaunchKernelGGL((pool_fwd_kernel<E, NV>), grid, dim3(256), lds, s, (const E*)H,       \
-                     (const E*)wp, s_out, part, T, D, L, nb, nch)
-  switch (nvj) {
-    case 1: POOL_FWD(1); break;
-    case 2: POOL_FWD(2); break;
-    case 4: POOL_FWD(4); break;
-    case 8: POOL_FWD(8); break;
-    default: POOL_FWD(16); break;
+hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* S, float* stats, int B,
+                      int T, int D, int L, hipStream_t s) {
+  switch (nvj_for(D / Vec16<E>::N)) {
+    case 1: return pool_fwd_nv<E, 1>(H, wp, s_out, S, stats, B, T, D, L, s);
+    case 2: return pool_fwd_nv<E, 2>(H, wp, s_out, S, stats, B, T, D, L, s);
+    case 4: return pool_fwd_nv<E, 4>(H, wp, s_out, S, stats, B, T, D, L, s);
+    default: return pool_fwd_nv<E, 8>(H, wp, s_out, S, stats, B, T, D, L, s);
   }
-#undef POOL_FWD
+}
+
+template <typename E, int NV>
+hipError_t pool_bwd_nv(const void* H, const float* s_in, const float* stats, const float* S,
+                       const float* dS, float* a_out, float* ds_out, float* dwp, int B, int T,
+                       int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int nw = pool_waves<NV>(L, T, D);
+  const size_t lds = (size_t)nw * D * sizeof(float);
+  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb, B), dim3(nw * 64), lds, s, (const E*)H,
+                     s_in, stats, S, dS, a_out, ds_out, dwp, T, D, L, nb);
   return hipGetLastError();
 }
 
@@ -453,62 +503,53 @@ template <typename E>
 hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, const float* S,
                       const float* dS, float* a_out, float* ds_out, float* dwp, int B, int T,
                       int D, int L, hipStream_t s) {
-  const int nb = (T + L - 1) / L;
-  const int nch = pool_chunks(L < T ? L : T);
-  dim3 grid(nch, nb, B);
-  const size_t lds = 4 * (size_t)D * sizeof(float);
-  const int nvj = nvj_for(D / Vec16<E>::N);
-#define POOL_BWD(NV)                                                                          \
-  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), grid, dim3(256), lds, s, (const E*)H, s_in,  \
-                     stats, S, dS, a_out, ds_out, dwp, T, D, L, nb)
-  switch (nvj) {
-    case 1: POOL_BWD(1); break;
-    case 2: POOL_BWD(2); break;
-    case 4: POOL_BWD(4); break;
-    case 8: POOL_BWD(8); break;
-    default: POOL_BWD(16); break;
+  switch (nvj_for(D / Vec16<E>::N)) {
+    case 1: return pool_bwd_nv<E, 1>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+    case 2: return pool_bwd_nv<E, 2>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+    case 4: return pool_bwd_nv<E, 4>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+    default: return pool_bwd_nv<E, 8>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
   }
-#undef POOL_BWD
+}
+
+template <typename E>
+hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, void* Pbar, int B,
+                      int T, int D, int L, hipStream_t s) {
+  const int nb = (T + L - 1) / L;
+  const int Dv = D / Vec16<E>::N;
+  int tg = 1024 / Dv;
+  const int lb = L < T ? L : T;
+  if (tg > lb) tg = lb;
+  if (tg < 1) tg = 1;
+  const size_t lds = (size_t)tg * D * sizeof(float);
+  hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B), dim3(tg * Dv), lds, s, (const E*)dY,
+                     (const E*)G, P, (E*)dU, (E*)Pbar, T, D, L, nb);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int pool_chunks(int L) { return (L + kPoolTok - 1) / kPoolTok; }
-
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* part, int B,
-                    int T, int D, int L, hipStream_t s) {
-  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, part, B, T, D, L, s);
-  return pool_fwd_t<float>(H, wp, s_out, part, B, T, D, L, s);
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, float* stats,
+                    int B, int T, int D, int L, hipStream_t s) {
+  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, S, stats, B, T, D, L, s);
+  return pool_fwd_t<float>(H, wp, s_out, S, stats, B, T, D, L, s);
 }
 
-hipError_t scan_fwd(DType dt, const float* part, float* S, float* M, void* Mt, float* stats,
-                    int B, int T, int D, int L, float gamma, hipStream_t s) {
+hipError_t scan_fwd(DType dt, const float* S, float* M, void* Mt, int B, int T, int D, int L,
+                    float gamma, hipStream_t s) {
   const int nb = (T + L - 1) / L;
-  const int nch = pool_chunks(L < T ? L : T);
   dim3 grid((D + 31) / 32, B);
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, part, nch, S, M, (bf16*)Mt,
-                       stats, nb, D, gamma);
+    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, S, M, (bf16*)Mt, nb, D, gamma);
   else
-    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, part, nch, S, M,
-                       (float*)Mt, stats, nb, D, gamma);
+    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, S, M, (float*)Mt, nb, D,
+                       gamma);
   return hipGetLastError();
 }
 
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, int B, int T, int D, int L, hipStream_t s) {
-  const int nb = (T + L - 1) / L;
-  if (dt == DType::BF16) {
-    dim3 grid((D / 8 + 63) / 64, nb, B);
-    hipLaunchKernelGGL(gate_bwd_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)dY,
-                       (const bf16*)G, P, (bf16*)dU, (bf16*)Pbar, T, D, L, nb);
-  } else {
-    dim3 grid((D / 4 + 63) / 64, nb, B);
-    hipLaunchKernelGGL(gate_bwd_kernel<float>, grid, dim3(256), 0, s, (const float*)dY,
-                       (const float*)G, P, (float*)dU, (float*)Pbar, T, D, L, nb);
-  }
-  return hipGetLastError();
+  if (dt == DType::BF16) return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, B, T, D, L, s);
+  return gate_bwd_t<float>(dY, G, P, dU, Pbar, B, T, D, L, s);
 }
 
 hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,
