@@ -126,17 +126,19 @@ bool overlaps(const void* a, const void* b, size_t n) {
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
 enum Stage {
-  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_WM, ST_GATE,
-  ST_ZERO, ST_GATE_BWD, ST_WG_WGRAD, ST_WM_DGRAD, ST_WM_WGRAD, ST_MEM_BWD, ST_POOL_BWD,
-  ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD,
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_WM, ST_WM_RED, ST_GATE,
+  ST_ZERO, ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_DGRAD_RED, ST_WM_WGRAD,
+  ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
+  ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.scan", "fwd.wm_gemm",
-    "fwd.gate_gemm", "bwd.zero_grads", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wm_dgrad_gemm",
-    "bwd.wm_wgrad_gemm", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm", "bwd.wo_dgrad_gemm",
-    "bwd.wo_wgrad_gemm", "bwd.attention_dq", "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm",
-    "bwd.qkv_wgrad_gemm"};
+    "fwd.wm_reduce", "fwd.gate_gemm", "bwd.zero_grads", "bwd.gate", "bwd.wg_wgrad_gemm",
+    "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm", "bwd.wm_dgrad_reduce", "bwd.wm_wgrad_gemm",
+    "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm",
+    "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_dq",
+    "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
 
 struct Tracer {
   std::atomic<bool> on{false};
@@ -190,6 +192,15 @@ struct TraceScope {
     a = nullptr;
   }
 };
+
+// A split-K product and its reduction as two traced stages.
+#define LAUNCH_SPLITK(stage, stage_red, dt, g, part, C0, C1, C2, ldc, seg, acc, min_k)           \
+  do {                                                                                        \
+    int sp_ = 0;                                                                              \
+    LAUNCH(stage, gemm_splitk_product(dt, g, part, C0, C1, C2, ldc, seg, acc, min_k, &sp_, s)); \
+    if (sp_ > 1)                                                                              \
+      LAUNCH(stage_red, gemm_splitk_reduce(part, sp_, (g).M, (g).N, C0, C1, C2, ldc, seg, acc, s)); \
+  } while (0)
 
 #define LAUNCH(stage, expr)                            \
   do {                                                 \
@@ -315,8 +326,8 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
     // Only B * N_b rows: split K so that every workgroup has one or two slabs.
     GemmDesc g{p.B * p.nb, D, D, SV + p.Mt, D, false, {prm->Wm, nullptr, nullptr}, D, true,
                kSegNone, 0, 1};
-    LAUNCH(ST_WM, gemm_splitk(dt, g, (float*)(W + p.mpart), (float*)(SV + p.P), nullptr, nullptr,
-                              D, D, false, 64, s));
+    LAUNCH_SPLITK(ST_WM, ST_WM_RED, dt, g, (float*)(W + p.mpart), (float*)(SV + p.P), nullptr,
+                  nullptr, D, D, false, 64);
   }
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
@@ -372,18 +383,20 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
                   p.L, s));
   if (gr.dWg) {
     GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH(ST_WG_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWg, nullptr, nullptr, D, D, accum, s));
+    LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
+                  accum, 512);
   }
   // Memory projection: dM = dP Wm^T and dWm = M^T dP.
   {
     GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
                1};
-    LAUNCH(ST_WM_DGRAD, gemm_splitk(dt, g, wpart, (float*)(W + p.mbar), nullptr, nullptr, D, D,
-                                    false, 64, s));
+    LAUNCH_SPLITK(ST_WM_DGRAD, ST_WM_DGRAD_RED, dt, g, wpart, (float*)(W + p.mbar), nullptr,
+                  nullptr, D, D, false, 64);
   }
   if (gr.dWm) {
     GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH(ST_WM_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWm, nullptr, nullptr, D, D, accum, s));
+    LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
+                  accum, 512);
   }
   // Decayed reverse scan: dS and the decay gradient.
   LAUNCH(ST_MEM_BWD, mem_bwd((const float*)(W + p.mbar), (const float*)(SV + p.M), (float*)(W + p.dS),
@@ -406,7 +419,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   }
   if (gr.dWo) {
     GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH(ST_WO_WGRAD, gemm_wgrad(dt, g, wpart, gr.dWo, nullptr, nullptr, D, D, accum, s));
+    LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
+                  accum, 512);
   }
   // Block-local attention backward.
   LAUNCH(ST_ATTN_BWD_DQ,
@@ -423,8 +437,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   }
   if (gr.dWq || gr.dWk || gr.dWv) {
     GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone, 0, 1};
-    LAUNCH(ST_QKV_WGRAD,
-           gemm_wgrad(dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D, accum, s));
+    LAUNCH_SPLITK(ST_QKV_WGRAD, ST_QKV_WGRAD_RED, dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D,
+                  accum, 512);
   }
   return BCMT_OK;
 }

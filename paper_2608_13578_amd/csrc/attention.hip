@@ -412,10 +412,458 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
   }
 }
 
+// ------------------------------------------------------------------ bf16 kernels
+// The bf16 path stages every 64 x 64 tile in its natural [row][d] layout
+// with direct global->LDS loads (double buffered), and reads the transposed
+// operands (V^T for P V, K^T for dQ, Q^T and dO^T for dK and dV) from the
+// same tiles with ds_read_b64_tr_b16: within each 16-lane group, lane i gets
+// element (i % 4) of the 4-element rows addressed by lanes 4j + i/4; with
+// lane q addressing row k0 + q/4 at column c0 + 4 (q % 4), lane i receives
+// rows k0..k0+3 of column c0 + i.  Tile element (r, c) lives at
+// r*64 + 8*((c/8) ^ ((r/2) % 8)) + c % 8: the XOR swizzle of 16-byte chunks
+// spreads a fragment's rows over distinct banks.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+__device__ __forceinline__ int toff(int r, int c) {
+  return r * 64 + (((c >> 3) ^ ((r >> 1) & 7)) << 3) + (c & 7);
+}
+__device__ __forceinline__ bf16x8 trow8(const bf16* t, int r, int c0) {
+  return *reinterpret_cast<const bf16x8*>(t + toff(r, c0));
+}
+__device__ __forceinline__ bf16x4 tcol4(const bf16* t, int k0, int c0, int lane) {
+  const int i = lane & 15;
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4_t*)(t + toff(k0 + (i >> 2), c0 + ((i & 3) << 2))));
+  return __builtin_bit_cast(bf16x4, v);
+}
+// Operand over d (rows dsub*16 + lane%16) and the 32 keys/queries
+// {b0 + 4g .. +3} u {b0 + 16 + 4g .. +3} of lane group g: the order in which
+// a transposed-score tile holds its probabilities.
+__device__ __forceinline__ bf16x8 tcol8p(const bf16* t, int b0, int dsub, int lane) {
+  const int g = lane >> 4;
+  const bf16x4 a = tcol4(t, b0 + 4 * g, dsub * 16, lane);
+  const bf16x4 b = tcol4(t, b0 + 16 + 4 * g, dsub * 16, lane);
+  bf16x8 r = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return r;
+}
+
+// This wave's direct loads of a 64 x 64 tile: rows r0 .. r0+63 of `src`
+// (row stride rs), clamped to rlast (clamped rows are never used unmasked).
+template <int NW>
+__device__ __forceinline__ void tile_issue(const bf16* src, int64_t rs, int r0, int rlast,
+                                           bf16* t, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < 8 / NW; ++i) {
+    const int gi = wave * (8 / NW) + i;
+    const int row = gi * 8 + (lane >> 3);
+    const int cg = (lane & 7) ^ ((row >> 1) & 7);
+    const int grow = min(r0 + row, rlast);
+    __builtin_amdgcn_global_load_lds(src + (int64_t)grow * rs + cg * 8, (lds_void_t*)(t + gi * 512),
+                                     16, 0, 0);
+  }
+}
+// 64 floats (one per lane of wave 0), indices clamped to last.
+__device__ __forceinline__ void vec_issue(const float* src, int i0, int last, float* dst, int lane) {
+  __builtin_amdgcn_global_load_lds(src + min(i0 + lane, last), (lds_void_t*)dst, 4, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void sync_lds() {
+  __builtin_amdgcn_s_barrier();
+}
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __restrict__ qkv,
+                                                               bf16* __restrict__ out,
+                                                               float* __restrict__ lse, int Tn,
+                                                               int D, int H, int L, float sl2) {
+  constexpr int QT = NW * 32;
+  constexpr int NI = 16 / NW;  // direct loads per wave per key tile (K and V)
+  __shared__ __attribute__((aligned(1024))) bf16 lds[2][2][64 * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int q0 = bs + blockIdx.x * QT;
+  if (q0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const bf16* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const int tw0 = q0 + wave * 32;
+  const int kend = min(be, q0 + QT);
+  const int nt = (kend - bs + 63) / 64;
+
+  bf16x8 qf[2][2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds)
+      qf[nq][ds] = t < be ? *reinterpret_cast<const bf16x8*>(base + (int64_t)t * rs + ds * 32 + lg * 8)
+                          : bf16x8{};
+  }
+  f32x4 o[2][4];
+  float m[2], l[2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    m[nq] = -INFINITY;
+    l[nq] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  tile_issue<NW>(base + D, rs, bs, kend - 1, lds[0][0], wave, lane);
+  tile_issue<NW>(base + 2 * D, rs, bs, kend - 1, lds[0][1], wave, lane);
+  if (nt > 1) {
+    tile_issue<NW>(base + D, rs, bs + 64, kend - 1, lds[1][0], wave, lane);
+    tile_issue<NW>(base + 2 * D, rs, bs + 64, kend - 1, lds[1][1], wave, lane);
+  }
+  for (int it = 0; it < nt; ++it) {
+    if (it + 1 < nt) vm_wait<NI>();
+    else vm_wait<0>();
+    sync_lds();
+    const int kt = bs + it * 64;
+    const bf16* Kt = lds[it & 1][0];
+    const bf16* Vt = lds[it & 1][1];
+    bf16x8 kf[4][2], vf[4][2];
+#pragma unroll
+    for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) vf[j][us] = tcol8p(Vt, us * 32, j, lane);
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int tq = tw0 + nq * 16;
+      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+      f32x4 s[4];
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku) {
+        s[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) s[ku] = mma16(kf[ku][ds], qf[nq][ds], s[ku]);
+      }
+      const int t_eff = min(tq + lr, be - 1);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int u = kt + ku * 16 + lg * 4 + r;
+          const float z = u <= t_eff ? s[ku][r] * sl2 : -INFINITY;
+          s[ku][r] = z;
+          mx = fmaxf(mx, z);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(m[nq], mx);
+      const float alpha = exp2f(m[nq] - mnew);
+      float ps = 0.f;
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float pv = exp2f(s[ku][r] - mnew);
+          s[ku][r] = pv;
+          ps += pv;
+        }
+      l[nq] = l[nq] * alpha + ps;
+      m[nq] = mnew;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[nq][j] *= alpha;
+#pragma unroll
+      for (int us = 0; us < 2; ++us) {
+        const bf16x8 pf = frag_from<bf16>(s[2 * us], s[2 * us + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[nq][j] = mma16(vf[j][us], pf, o[nq][j]);
+      }
+    }
+    if (it + 2 < nt) {
+      sync_lds();  // every wave is done with this buffer
+      tile_issue<NW>(base + D, rs, kt + 128, kend - 1, lds[it & 1][0], wave, lane);
+      tile_issue<NW>(base + 2 * D, rs, kt + 128, kend - 1, lds[it & 1][1], wave, lane);
+    }
+  }
+
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    float lt = l[nq];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    const int t = tw0 + nq * 16 + lr;
+    if (t < be) {
+      const float inv = 1.0f / lt;
+      bf16* op = out + ((int64_t)b * Tn + t) * D + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        store4(op + j * 16, o[nq][j][0] * inv, o[nq][j][1] * inv, o[nq][j][2] * inv,
+               o[nq][j][3] * inv);
+      if (lg == 0) lse[((int64_t)b * H + h) * Tn + t] = m[nq] + log2f(lt);
+    }
+  }
+}
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bwd_dq_bf16_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ o, const bf16* __restrict__ dout,
+    const float* __restrict__ lse, float* __restrict__ delta, bf16* __restrict__ dqkv, int Tn,
+    int D, int H, int L, float sl2, float scale) {
+  constexpr int QT = NW * 32;
+  constexpr int NI = 16 / NW;
+  __shared__ __attribute__((aligned(1024))) bf16 lds[2][2][64 * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int q0 = bs + blockIdx.x * QT;
+  if (q0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const bf16* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const bf16* ob = o + (int64_t)b * Tn * D + h * kDh;
+  const bf16* db = dout + (int64_t)b * Tn * D + h * kDh;
+  const int64_t lrow = ((int64_t)b * H + h) * Tn;
+  const int tw0 = q0 + wave * 32;
+  const int kend = min(be, q0 + QT);
+  const int nt = (kend - bs + 63) / 64;
+
+  bf16x8 qf[2][2], df[2][2];
+  float dl[2], ls[2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+    const bool ok = t < be;
+    float part = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      qf[nq][ds] = ok ? *reinterpret_cast<const bf16x8*>(base + (int64_t)t * rs + ds * 32 + lg * 8) : bf16x8{};
+      df[nq][ds] = ok ? *reinterpret_cast<const bf16x8*>(db + (int64_t)t * D + ds * 32 + lg * 8) : bf16x8{};
+      const bf16x8 of = ok ? *reinterpret_cast<const bf16x8*>(ob + (int64_t)t * D + ds * 32 + lg * 8) : bf16x8{};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part += (float)df[nq][ds][e] * (float)of[e];
+    }
+    part += __shfl_xor(part, 16, 64);
+    part += __shfl_xor(part, 32, 64);
+    dl[nq] = part;
+    ls[nq] = ok ? lse[lrow + t] : 0.f;
+    if (ok && lg == 0) delta[lrow + t] = part;
+  }
+  f32x4 dq[2][4];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dq[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  tile_issue<NW>(base + D, rs, bs, kend - 1, lds[0][0], wave, lane);
+  tile_issue<NW>(base + 2 * D, rs, bs, kend - 1, lds[0][1], wave, lane);
+  if (nt > 1) {
+    tile_issue<NW>(base + D, rs, bs + 64, kend - 1, lds[1][0], wave, lane);
+    tile_issue<NW>(base + 2 * D, rs, bs + 64, kend - 1, lds[1][1], wave, lane);
+  }
+  for (int it = 0; it < nt; ++it) {
+    if (it + 1 < nt) vm_wait<NI>();
+    else vm_wait<0>();
+    sync_lds();
+    const int kt = bs + it * 64;
+    const bf16* Kt = lds[it & 1][0];
+    const bf16* Vt = lds[it & 1][1];
+    bf16x8 kf[4][2], vf[4][2], ktf[4][2];
+#pragma unroll
+    for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
+        vf[ku][ds] = trow8(Vt, ku * 16 + lr, ds * 32 + lg * 8);
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) ktf[j][us] = tcol8p(Kt, us * 32, j, lane);
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int tq = tw0 + nq * 16;
+      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+      f32x4 s[4], dp[4];
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku) {
+        s[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dp[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          s[ku] = mma16(kf[ku][ds], qf[nq][ds], s[ku]);
+          dp[ku] = mma16(vf[ku][ds], df[nq][ds], dp[ku]);
+        }
+      }
+      const int t_eff = min(tq + lr, be - 1);
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int u = kt + ku * 16 + lg * 4 + r;
+          const float pv = u <= t_eff ? exp2f(s[ku][r] * sl2 - ls[nq]) : 0.f;
+          s[ku][r] = pv * (dp[ku][r] - dl[nq]);
+        }
+#pragma unroll
+      for (int us = 0; us < 2; ++us) {
+        const bf16x8 zf = frag_from<bf16>(s[2 * us], s[2 * us + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dq[nq][j] = mma16(ktf[j][us], zf, dq[nq][j]);
+      }
+    }
+    if (it + 2 < nt) {
+      sync_lds();
+      tile_issue<NW>(base + D, rs, kt + 128, kend - 1, lds[it & 1][0], wave, lane);
+      tile_issue<NW>(base + 2 * D, rs, kt + 128, kend - 1, lds[it & 1][1], wave, lane);
+    }
+  }
+
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+    if (t < be) {
+      bf16* p = dqkv + ((int64_t)b * Tn + t) * rs + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        store4(p + j * 16, dq[nq][j][0] * scale, dq[nq][j][1] * scale, dq[nq][j][2] * scale,
+               dq[nq][j][3] * scale);
+    }
+  }
+}
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ dout, const float* __restrict__ lse,
+    const float* __restrict__ delta, bf16* __restrict__ dqkv, int Tn, int D, int H, int L,
+    float sl2, float scale) {
+  constexpr int KT = NW * 32;
+  constexpr int NI = 16 / NW;
+  __shared__ __attribute__((aligned(1024))) bf16 lds[2][2][64 * 64];
+  __shared__ float vec_s[2][2][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int k0 = bs + blockIdx.x * KT;
+  if (k0 >= be) return;
+  const int64_t rs = 3LL * D;
+  const bf16* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const bf16* db = dout + (int64_t)b * Tn * D + h * kDh;
+  const int64_t lrow = ((int64_t)b * H + h) * Tn;
+  const int uw0 = k0 + wave * 32;
+  const int nt = (be - k0 + 63) / 64;
+
+  bf16x8 kf[2][2], vf[2][2];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku) {
+    const int u = uw0 + ku * 16 + lr;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      kf[ku][ds] = u < be ? *reinterpret_cast<const bf16x8*>(base + D + (int64_t)u * rs + ds * 32 + lg * 8) : bf16x8{};
+      vf[ku][ds] = u < be ? *reinterpret_cast<const bf16x8*>(base + 2 * D + (int64_t)u * rs + ds * 32 + lg * 8) : bf16x8{};
+    }
+  }
+  f32x4 dk[2][4], dv[2][4];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dk[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dv[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  auto issue = [&](int tt, int buf) {
+    tile_issue<NW>(base, rs, tt, be - 1, lds[buf][0], wave, lane);
+    tile_issue<NW>(db, D, tt, be - 1, lds[buf][1], wave, lane);
+    if (wave == 0) {
+      vec_issue(lse + lrow, tt, be - 1, vec_s[buf][0], lane);
+      vec_issue(delta + lrow, tt, be - 1, vec_s[buf][1], lane);
+    }
+  };
+  issue(k0, 0);
+  if (nt > 1) issue(k0 + 64, 1);
+  for (int it = 0; it < nt; ++it) {
+    if (it + 1 < nt) {
+      if (wave == 0) vm_wait<NI + 2>();
+      else vm_wait<NI>();
+    } else {
+      vm_wait<0>();
+    }
+    sync_lds();
+    const int tt = k0 + it * 64;
+    const bf16* Qt = lds[it & 1][0];
+    const bf16* Dt = lds[it & 1][1];
+    const float* ls_s = vec_s[it & 1][0];
+    const float* dl_s = vec_s[it & 1][1];
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku) {
+      const int uw = uw0 + ku * 16;
+      if (uw >= be || tt + 63 < uw) continue;  // wave-uniform
+      const int u = uw + lr;
+      f32x4 p[4], z[4];
+#pragma unroll
+      for (int ts = 0; ts < 4; ++ts) {
+        f32x4 s = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          s = mma16(trow8(Qt, ts * 16 + lr, ds * 32 + lg * 8), kf[ku][ds], s);
+          dp = mma16(trow8(Dt, ts * 16 + lr, ds * 32 + lg * 8), vf[ku][ds], dp);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ti = ts * 16 + lg * 4 + r;
+          const int t = tt + ti;
+          const bool ok = t >= u && t < be && u < be;
+          const float pv = ok ? exp2f(s[r] * sl2 - ls_s[ti]) : 0.f;
+          p[ts][r] = pv;
+          z[ts][r] = pv * (dp[r] - dl_s[ti]);
+        }
+      }
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        const bf16x8 pf = frag_from<bf16>(p[2 * tq], p[2 * tq + 1]);
+        const bf16x8 zf = frag_from<bf16>(z[2 * tq], z[2 * tq + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          dv[ku][j] = mma16(tcol8p(Dt, tq * 32, j, lane), pf, dv[ku][j]);
+          dk[ku][j] = mma16(tcol8p(Qt, tq * 32, j, lane), zf, dk[ku][j]);
+        }
+      }
+    }
+    if (it + 2 < nt) {
+      sync_lds();
+      issue(tt + 128, it & 1);
+    }
+  }
+
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku) {
+    const int u = uw0 + ku * 16 + lr;
+    if (u < be) {
+      bf16* p = dqkv + ((int64_t)b * Tn + u) * rs + h * kDh + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        store4(p + D + j * 16, dk[ku][j][0] * scale, dk[ku][j][1] * scale, dk[ku][j][2] * scale,
+               dk[ku][j][3] * scale);
+        store4(p + 2 * D + j * 16, dv[ku][j][0], dv[ku][j][1], dv[ku][j][2], dv[ku][j][3]);
+      }
+    }
+  }
+}
+
+// Waves per attention workgroup (1, 2 or 4), each owning 32 queries or keys.
 int attn_waves(int L, int T) {
   const int lb = L < T ? L : T;
   const int w = (lb + 31) / 32;
-  return w < 4 ? w : 4;
+  return w <= 1 ? 1 : (w == 2 ? 2 : 4);
 }
 
 template <typename E>
@@ -465,21 +913,50 @@ hipError_t attn_bwd_dkdv_t(const void* qkv, const void* dout, const float* lse,
 
 hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D, int H,
                     int L, hipStream_t s) {
-  if (dt == DType::BF16) return attn_fwd_t<bf16>(qkv, out, lse, B, T, D, H, L, s);
+  if (dt == DType::BF16) {
+    const int nw = attn_waves(L, T);
+    const int lb = L < T ? L : T;
+    dim3 grid((lb + nw * 32 - 1) / (nw * 32), (T + L - 1) / L, B * H);
+    const float sl2 = 1.4426950408889634f / sqrtf((float)kDh);
+#define FWD(NW) hipLaunchKernelGGL(attn_fwd_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (bf16*)out, lse, T, D, H, L, sl2)
+    if (nw == 1) FWD(1); else if (nw == 2) FWD(2); else FWD(4);
+#undef FWD
+    return hipGetLastError();
+  }
   return attn_fwd_t<float>(qkv, out, lse, B, T, D, H, L, s);
 }
 
 hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* dout,
                        const float* lse, float* delta, void* dqkv, int B, int T, int D, int H,
                        int L, hipStream_t s) {
-  if (dt == DType::BF16) return attn_bwd_dq_t<bf16>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
+  if (dt == DType::BF16) {
+    const int nw = attn_waves(L, T);
+    const int lb = L < T ? L : T;
+    dim3 grid((lb + nw * 32 - 1) / (nw * 32), (T + L - 1) / L, B * H);
+    const float scale = 1.0f / sqrtf((float)kDh);
+    const float sl2 = 1.4426950408889634f * scale;
+#define DQ(NW) hipLaunchKernelGGL(attn_bwd_dq_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (const bf16*)out, (const bf16*)dout, lse, delta, (bf16*)dqkv, T, D, H, L, sl2, scale)
+    if (nw == 1) DQ(1); else if (nw == 2) DQ(2); else DQ(4);
+#undef DQ
+    return hipGetLastError();
+  }
   return attn_bwd_dq_t<float>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
 }
 
 hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
                          const float* delta, void* dqkv, int B, int T, int D, int H, int L,
                          hipStream_t s) {
-  if (dt == DType::BF16) return attn_bwd_dkdv_t<bf16>(qkv, dout, lse, delta, dqkv, B, T, D, H, L, s);
+  if (dt == DType::BF16) {
+    const int nw = attn_waves(L, T);
+    const int lb = L < T ? L : T;
+    dim3 grid((lb + nw * 32 - 1) / (nw * 32), (T + L - 1) / L, B * H);
+    const float scale = 1.0f / sqrtf((float)kDh);
+    const float sl2 = 1.4426950408889634f * scale;
+#define DKDV(NW) hipLaunchKernelGGL(attn_bwd_dkdv_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (const bf16*)dout, lse, (const float*)delta, (bf16*)dqkv, T, D, H, L, sl2, scale)
+    if (nw == 1) DKDV(1); else if (nw == 2) DKDV(2); else DKDV(4);
+#undef DKDV
+    return hipGetLastError();
+  }
   return attn_bwd_dkdv_t<float>(qkv, dout, lse, delta, dqkv, B, T, D, H, L, s);
 }
 

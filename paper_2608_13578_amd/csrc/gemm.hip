@@ -1,19 +1,19 @@
-// Tiled matrix product on the CDNA4 matrix cores, with fused epilogues.
+// Tiled matrix products on the CDNA4 matrix cores, with fused epilogues.
 //
 // Serves every dense projection of the layer (Sec. 3.3 Q/K/V and W_O,
 // Sec. 3.5 W_m, Sec. 3.8 W_g) and their backward products.
 //
-// Workgroup tile 128 x 128, four waves in a 2 x 2 grid, each wave 64 x 64 as
-// 4 x 4 sub-tiles of 16 x 16.  The K loop stages one BK-wide slab of both
-// operands in LDS, double buffered: the next slab's global loads are issued
-// before the current slab's matrix instructions and written to the other LDS
-// buffer afterwards, so one barrier per slab suffices.
-//
-// LDS holds both operands "K-contiguous" (row = m or n, 8 consecutive k per
-// 16-byte read), which is what a lane feeds the matrix instruction.  An
-// operand stored with M/N contiguous in memory is transposed on the way in:
-// a thread loads an 8 x 8 (bf16) or 4 x 4 (f32) sub-block as 16-byte rows and
-// writes it back transposed, 16 bytes per row.
+// Two kernels:
+//  * gemm_pipe_kernel (bf16): 128 x 128 tiles, four waves of 64 x 64, K
+//    streamed in 64-deep slabs through a two-slab LDS ring filled by direct
+//    global->LDS loads; operands stay in their global orientation in LDS and
+//    M/N-major ones are read with the transposing LDS instruction.  Two
+//    workgroups share a CU.  Tiles are ordered per XCD (see xcd_tile_order).
+//  * gemm_kernel (float32, and bf16 shapes whose K is not a multiple of 64):
+//    the same tiling with register staging; M/N-major operands are
+//    transposed in registers on their way into LDS.
+// Weight gradients (K = B*T) use split-K partial tiles and a deterministic
+// reduction kernel instead of atomics.
 //
 // The matrix instruction is issued with the B tile as its first operand, so
 // a lane ends up holding four consecutive output columns of one output row:
@@ -320,11 +320,17 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
-template <int R, bool RCONTIG, int SEG>
+template <int R, int BK, bool RCONTIG, int SEG>
 struct PipeOperand {
-  static constexpr int BK = 64;
+  static_assert(BK == 32 || BK == 64, "slab depth");
   static constexpr int ELEMS = R * BK;
   static constexpr int INSTR = ELEMS / 512;  // 1 KB per wave-wide load
+  static constexpr int KCH = BK / 8;         // 16-byte chunks per K-contiguous row
+  // XOR swizzle of a K-contiguous row's chunks: spreads the 16 rows of a
+  // fragment read over all banks (rows are 64 or 128 bytes apart).
+  __device__ __forceinline__ static int kswz(int r) {
+    return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+  }
 
   // Issue this wave's share of the direct loads of one slab.
   template <int NW>
@@ -336,8 +342,9 @@ struct PipeOperand {
       const int gi = wave * (INSTR / NW) + i;
       const bf16* src;
       if constexpr (!RCONTIG) {
-        const int row = gi * 8 + (lane >> 3);
-        const int cg = (lane & 7) ^ ((row >> 1) & 7);
+        constexpr int RPI = 64 / KCH;   // rows per instruction
+        const int row = gi * RPI + lane / KCH;
+        const int cg = (lane % KCH) ^ kswz(row);
         const int gr = min(r0 + row, rmax - 1);
         src = op.at(gr, k0 + cg * 8);
       } else {
@@ -358,7 +365,7 @@ struct PipeOperand {
     const int lr = lane & 15, lg = lane >> 4;
     if constexpr (!RCONTIG) {
       const int r = base + lr;
-      const int c = (ks * 4 + lg) ^ ((r >> 1) & 7);
+      const int c = (ks * 4 + lg) ^ kswz(r);
       return *reinterpret_cast<const bf16x8*>(s + r * BK + c * 8);
     } else {
       const int col = base + (lr & 3) * 4;
@@ -379,8 +386,8 @@ struct PipeOperand {
 // launch order, and each XCD has its own L2.  The launch-order index is
 // mapped so that every XCD works through one contiguous run of the tile
 // sequence, and the sequence walks groups of kGroupM tile rows column by
-// column: the ~32 tiles an XCD holds at once then share a few A row panels
-// and B column panels in that XCD's L2.
+// column: the tiles an XCD holds at once then share a few A row panels and
+// B column panels in that XCD's L2.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 4;
 
@@ -398,17 +405,18 @@ __device__ __forceinline__ void xcd_tile_order(int bx, int by, int nx, int ny, i
   tn = in / gm;
 }
 
-template <int BM, int BN, int STAGES, int WGM, int WGN, bool A_MC, bool B_NC, int BSEG, class Epi>
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool A_MC, bool B_NC, int BSEG,
+          class Epi>
 __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, int K,
                                                                 Operand<bf16, A_MC, kSegNone> A,
                                                                 Operand<bf16, B_NC, BSEG> B,
                                                                 int kchunk, Epi epi) {
-  constexpr int BK = 64;
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
-  typedef PipeOperand<BM, A_MC, kSegNone> PA;
-  typedef PipeOperand<BN, B_NC, BSEG> PB;
+  typedef PipeOperand<BM, BK, A_MC, kSegNone> PA;
+  typedef PipeOperand<BN, BK, B_NC, BSEG> PB;
   constexpr int STAGE = PA::ELEMS + PB::ELEMS;
   constexpr int NI = (PA::INSTR + PB::INSTR) / NW;  // loads per wave per slab
   __shared__ __attribute__((aligned(1024))) bf16 lds[STAGES * STAGE];
@@ -442,7 +450,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
     // Slab kt must have landed; slabs kt+1 .. may stay in flight.
     const int after = min(nk - 1, kt + STAGES - 2) - kt;
     if constexpr (STAGES >= 4) {
-      if (after >= 2) wait_vmcnt<2 * NI>();
+      if (after >= 3 && STAGES >= 5) wait_vmcnt<3 * NI>();
+      else if (after >= 2) wait_vmcnt<2 * NI>();
       else if (after == 1) wait_vmcnt<NI>();
       else wait_vmcnt<0>();
     } else if constexpr (STAGES == 3) {
@@ -516,7 +525,7 @@ hipError_t launch(const GemmDesc& g, const Epi& epi, hipStream_t s) {
 // split to be a whole number of 64-wide slabs.
 template <bool AMC, bool BNC, int SEG, class Epi>
 hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
-  constexpr int PBM = 128, PBN = 128, ST = 2, WGM = 2, WGN = 2;
+  constexpr int PBM = 128, PBN = 128, PBK = 64, ST = 2, WGM = 2, WGN = 2;
   Operand<bf16, AMC, kSegNone> A{{(const bf16*)g.A, nullptr, nullptr}, g.lda, 0};
   Operand<bf16, BNC, SEG> B{{(const bf16*)g.B[0], (const bf16*)g.B[1], (const bf16*)g.B[2]}, g.ldb,
                             g.seg_len};
@@ -526,7 +535,7 @@ hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   if (g.kchunk > 0) kchunk = g.kchunk;
   splits = (g.K + kchunk - 1) / kchunk;
   dim3 grid((g.N + PBN - 1) / PBN, (g.M + PBM - 1) / PBM, splits);
-  hipLaunchKernelGGL((gemm_pipe_kernel<PBM, PBN, ST, WGM, WGN, AMC, BNC, SEG, Epi>), grid,
+  hipLaunchKernelGGL((gemm_pipe_kernel<PBM, PBN, PBK, ST, WGM, WGN, AMC, BNC, SEG, Epi>), grid,
                      dim3(WGM * WGN * 64), 0, s, g.M, g.N, g.K, A, B, kchunk, epi);
   return hipGetLastError();
 }
@@ -613,29 +622,46 @@ size_t gemm_wgrad_partial_bytes(int M, int N, int K) {
   return gemm_splitk_partial_bytes(M, N, K, 512);
 }
 
-hipError_t gemm_splitk(DType dt, const GemmDesc& g0, float* partial, float* C0, float* C1,
-                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
-                       hipStream_t s) {
+hipError_t gemm_splitk_product(DType dt, const GemmDesc& g0, float* partial, float* C0, float* C1,
+                               float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
+                               int* splits, hipStream_t s) {
+  *splits = 0;
   if (g0.M <= 0 || g0.N <= 0) return hipSuccess;
   if (g0.N % 4 != 0 || seg_len_n % 4 != 0 || g0.seg != kSegNone) return hipErrorInvalidValue;
   GemmDesc g = g0;
   int kc;
   g.splits = splitk_plan(g.M, g.N, g.K, min_k, &kc);
   g.kchunk = kc;  // exactly g.splits slices of `partial` get written
+  *splits = g.splits;
   if (g.splits == 1) {
     EpiSegOut e{{C0, C1, C2}, ldc, seg_len_n, accumulate ? 1 : 0};
     return dt == DType::BF16 ? dispatch_any<bf16>(g, e, s) : dispatch_any<float>(g, e, s);
   }
   EpiPartial e{partial, g.N, (int64_t)g.M * g.N};
-  hipError_t err = dt == DType::BF16 ? dispatch_any<bf16>(g, e, s) : dispatch_any<float>(g, e, s);
-  if (err != hipSuccess) return err;
-  const int64_t total = (int64_t)g.M * g.N / 4;
+  return dt == DType::BF16 ? dispatch_any<bf16>(g, e, s) : dispatch_any<float>(g, e, s);
+}
+
+hipError_t gemm_splitk_reduce(const float* partial, int splits, int M, int N, float* C0, float* C1,
+                              float* C2, int64_t ldc, int seg_len_n, bool accumulate,
+                              hipStream_t s) {
+  if (splits <= 1 || M <= 0 || N <= 0) return hipSuccess;
+  const int64_t total = (int64_t)M * N / 4;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, partial,
-                     g.splits, g.M, g.N, C0, C1, C2, ldc, seg_len_n, accumulate ? 1 : 0);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, partial, splits,
+                     M, N, C0, C1, C2, ldc, seg_len_n, accumulate ? 1 : 0);
   return hipGetLastError();
+}
+
+hipError_t gemm_splitk(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
+                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
+                       hipStream_t s) {
+  int sp = 0;
+  hipError_t e = gemm_splitk_product(dt, g, partial, C0, C1, C2, ldc, seg_len_n, accumulate, min_k,
+                                     &sp, s);
+  if (e != hipSuccess) return e;
+  return gemm_splitk_reduce(partial, sp, g.M, g.N, C0, C1, C2, ldc, seg_len_n, accumulate, s);
 }
 
 hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,

@@ -53,6 +53,15 @@ size_t gemm_splitk_partial_bytes(int M, int N, int K, int min_k);
 hipError_t gemm_splitk(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
                        float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
                        hipStream_t s);
+// The two launches of gemm_splitk separately: the product (which writes the
+// outputs itself when the plan has one split) and, when *splits > 1, the
+// reduction of the partial tiles.
+hipError_t gemm_splitk_product(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
+                               float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
+                               int* splits, hipStream_t s);
+hipError_t gemm_splitk_reduce(const float* partial, int splits, int M, int N, float* C0, float* C1,
+                              float* C2, int64_t ldc, int seg_len_n, bool accumulate,
+                              hipStream_t s);
 hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s);
 
