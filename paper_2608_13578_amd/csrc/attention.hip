@@ -423,10 +423,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
 // r*64 + 8*((c/8) ^ ((r/2) % 8)) + c % 8: the XOR swizzle of 16-byte chunks
 // spreads a fragment's rows over distinct banks.
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
-
 __device__ __forceinline__ int toff(int r, int c) {
   return r * 64 + (((c >> 3) ^ ((r >> 1) & 7)) << 3) + (c & 7);
 }
@@ -435,9 +431,7 @@ __device__ __forceinline__ bf16x8 trow8(const bf16* t, int r, int c0) {
 }
 __device__ __forceinline__ bf16x4 tcol4(const bf16* t, int k0, int c0, int lane) {
   const int i = lane & 15;
-  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_s16x4_t*)(t + toff(k0 + (i >> 2), c0 + ((i & 3) << 2))));
-  return __builtin_bit_cast(bf16x4, v);
+  return lds_read_tr(t + toff(k0 + (i >> 2), c0 + ((i & 3) << 2)));
 }
 // Operand over d (rows dsub*16 + lane%16) and the 32 keys/queries
 // {b0 + 4g .. +3} u {b0 + 16 + 4g .. +3} of lane group g: the order in which
@@ -540,6 +534,11 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __re
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int us = 0; us < 2; ++us) vf[j][us] = tcol8p(Vt, us * 32, j, lane);
+    lds_tr_wait();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) lds_tr_bind(vf[j][us]);
 #pragma unroll
     for (int nq = 0; nq < 2; ++nq) {
       const int tq = tw0 + nq * 16;
@@ -687,6 +686,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_bf16_kernel(
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int us = 0; us < 2; ++us) ktf[j][us] = tcol8p(Kt, us * 32, j, lane);
+    lds_tr_wait();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) lds_tr_bind(ktf[j][us]);
 #pragma unroll
     for (int nq = 0; nq < 2; ++nq) {
       const int tq = tw0 + nq * 16;
@@ -746,7 +750,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
   constexpr int KT = NW * 32;
   constexpr int NI = 16 / NW;
   __shared__ __attribute__((aligned(1024))) bf16 lds[2][2][64 * 64];
-  __shared__ float vec_s[2][2][64];
+  __shared__ __attribute__((aligned(16))) float vec_s[2][2][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int b = blockIdx.z / H, h = blockIdx.z % H;
@@ -801,8 +805,19 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
     const int tt = k0 + it * 64;
     const bf16* Qt = lds[it & 1][0];
     const bf16* Dt = lds[it & 1][1];
-    const float* ls_s = vec_s[it & 1][0];
-    const float* dl_s = vec_s[it & 1][1];
+    // This lane's 16 queries of the tile: ts * 16 + lg * 4 + r.
+    f32x4 lsv[4], dlv[4];
+#pragma unroll
+    for (int ts = 0; ts < 4; ++ts) {
+      lsv[ts] = lds_read_f32x4(&vec_s[it & 1][0][ts * 16 + lg * 4]);
+      dlv[ts] = lds_read_f32x4(&vec_s[it & 1][1][ts * 16 + lg * 4]);
+    }
+    lds_tr_wait();
+#pragma unroll
+    for (int ts = 0; ts < 4; ++ts) {
+      lds_tr_bind(lsv[ts]);
+      lds_tr_bind(dlv[ts]);
+    }
 #pragma unroll
     for (int ku = 0; ku < 2; ++ku) {
       const int uw = uw0 + ku * 16;
@@ -822,19 +837,31 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
           const int ti = ts * 16 + lg * 4 + r;
           const int t = tt + ti;
           const bool ok = t >= u && t < be && u < be;
-          const float pv = ok ? exp2f(s[r] * sl2 - ls_s[ti]) : 0.f;
+          const float pv = ok ? exp2f(s[r] * sl2 - lsv[ts][r]) : 0.f;
           p[ts][r] = pv;
-          z[ts][r] = pv * (dp[r] - dl_s[ti]);
+          z[ts][r] = pv * (dp[r] - dlv[ts][r]);
         }
       }
 #pragma unroll
       for (int tq = 0; tq < 2; ++tq) {
         const bf16x8 pf = frag_from<bf16>(p[2 * tq], p[2 * tq + 1]);
         const bf16x8 zf = frag_from<bf16>(z[2 * tq], z[2 * tq + 1]);
+        bf16x8 dtf[4], qtf[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          dv[ku][j] = mma16(tcol8p(Dt, tq * 32, j, lane), pf, dv[ku][j]);
-          dk[ku][j] = mma16(tcol8p(Qt, tq * 32, j, lane), zf, dk[ku][j]);
+          dtf[j] = tcol8p(Dt, tq * 32, j, lane);
+          qtf[j] = tcol8p(Qt, tq * 32, j, lane);
+        }
+        lds_tr_wait();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          lds_tr_bind(dtf[j]);
+          lds_tr_bind(qtf[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          dv[ku][j] = mma16(dtf[j], pf, dv[ku][j]);
+          dk[ku][j] = mma16(qtf[j], zf, dk[ku][j]);
         }
       }
     }

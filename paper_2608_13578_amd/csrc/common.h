@@ -142,4 +142,40 @@ template <> __device__ __forceinline__ f32x8 frag_from<float>(const f32x4& a, co
   return r;
 }
 
+// ------------------------------------------------------------------ LDS helpers
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+// ds_read_b64_tr_b16 through inline assembly.  The compiler's wait insertion
+// assumes that the builtin form may read LDS still being written by any
+// direct global->LDS load in flight and drains all of them first
+// (s_waitcnt vmcnt(0)), which would also wait for the tiles being
+// prefetched.  Callers order these reads after their own vmcnt wait and
+// barrier for the tile they read, and pass every result through
+// lds_tr_fence() before using it: the compiler does not count these reads
+// in its LDS wait bookkeeping.
+__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
+  s16x4 v;
+  const unsigned a = (unsigned)(uintptr_t)((lds_s16x4_t*)(p));
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a));
+  return __builtin_bit_cast(bf16x4, v);
+}
+// 16-byte LDS read in inline assembly, for data written by direct
+// global->LDS loads; same contract as lds_read_tr().
+__device__ __forceinline__ f32x4 lds_read_f32x4(const float* p) {
+  f32x4 v;
+  const unsigned a = (unsigned)(uintptr_t)((__attribute__((address_space(3))) float*)(p));
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+// Waits for every outstanding LDS read of this wave.
+__device__ __forceinline__ void lds_tr_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Ties a value to the preceding lds_tr_wait(), so that no use of it is
+// scheduled before the wait.
+template <class V>
+__device__ __forceinline__ void lds_tr_bind(V& v) {
+  asm volatile("" : "+v"(v));
+}
+
 }  // namespace bcmt

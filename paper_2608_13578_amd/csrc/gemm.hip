@@ -306,18 +306,9 @@ struct EpiHbar {
 // The XOR swizzles spread the 16 rows (or k-rows) a fragment read touches
 // over distinct LDS banks.
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
-
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
-  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
-  return __builtin_bit_cast(bf16x4, v);
 }
 
 template <int R, int BK, bool RCONTIG, int SEG>
@@ -479,6 +470,13 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
       for (int i = 0; i < FM; ++i) fa[i] = PA::frag(sa, wm * WTM + i * 16, ks, lane);
 #pragma unroll
       for (int j = 0; j < FN; ++j) fb[j] = PB::frag(sb, wn * WTN + j * 16, ks, lane);
+      if constexpr (A_MC || B_NC) {  // transposing reads went through inline assembly
+        lds_tr_wait();
+#pragma unroll
+        for (int i = 0; i < FM; ++i) lds_tr_bind(fa[i]);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) lds_tr_bind(fb[j]);
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
