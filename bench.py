@@ -150,7 +150,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-run", action="store_true",
-                    help="for rocprofv3: a 256 MiB calibration copy, then untraced steps only")
+                    help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
+                         "library's stage tracing on (every stage serialised on one stream, "
+                         "as in the per-stage pass of the normal run)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
@@ -193,9 +195,12 @@ def main():
         src.fill_(1)
         dst.copy_(src)
         torch.cuda.synchronize()
+        abi.bcmt_trace_enable(True)
         for _ in range(args.steps):
             step()
         torch.cuda.synchronize()
+        abi.bcmt_trace_read()
+        abi.bcmt_trace_enable(False)
         print(json.dumps({"profile_run": True, "steps": args.steps, "calibration_copy_bytes": 256 << 20}))
         return
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -208,7 +213,9 @@ def main():
     tokens = B * T
     value = tokens / (ms / 1e3)
 
-    # Second pass with per-launch events: per-stage GPU time.
+    # Second pass with per-launch events: per-stage GPU time, each stage
+    # alone (tracing keeps the backward's side-stream products on the
+    # caller's stream).
     abi.bcmt_trace_read()
     abi.bcmt_trace_enable(True)
     for _ in range(args.steps):

@@ -24,14 +24,23 @@
  *
  * Conventions
  *   - All tensors are row-major and live in device memory owned by the
- *     caller; the library allocates nothing and keeps no state between calls.
+ *     caller; the library allocates no tensor memory.  The only state it
+ *     keeps is one non-blocking stream (default priority) and a few events
+ *     per device, created by the first backward call on that device and
+ *     kept until the process ends.
  *   - Activations X, Y, dY, dX are [B, T, D]; weights Wq, Wk, Wv, Wo, Wm, Wg
  *     are [D, D] input-major (y = x W; a torch Linear weight is the
  *     transpose), wp is [D].  They all have the element type cfg->dtype.
  *   - Weight and decay gradients are float32, with the same shapes.
  *   - Every pointer must be 16-byte aligned.
- *   - Work is enqueued on `stream` (a hipStream_t; NULL means the default
- *     stream) in order; nothing synchronises the host.
+ *   - Work is enqueued on `stream` (a hipStream_t of the calling thread's
+ *     current device; NULL means the default stream); nothing synchronises
+ *     the host.  The backward pass runs its weight-gradient products on the
+ *     library's stream, ordered after their inputs on `stream` with events,
+ *     and makes `stream` wait for them before it returns: work enqueued on
+ *     `stream` afterwards sees every output, exactly as if all of it had run
+ *     on `stream`.  Calls on one device from several host threads are
+ *     serialised while they enqueue.
  *   - The GPU path needs a head width D / H of 64 and D <= 2048.
  *
  * Errors
@@ -145,10 +154,12 @@ int bcmt_version(void);
 /* ---- Stage tracing (profiling aid) -------------------------------------
  * While tracing is on, every kernel launch of bcmt_layer_forward and
  * bcmt_layer_backward is bracketed by two HIP events recorded on the call's
- * stream, so each stage's GPU time is measured in place.  The events are
- * created by the library on first use and reused; they are the only
- * resource the library ever creates.  Stage names are static strings such
- * as "fwd.qkv_gemm" or "bwd.attention_dkdv". */
+ * stream, so each stage's GPU time is measured in place.  While tracing is
+ * on, the backward pass also keeps its weight-gradient products on the
+ * call's stream instead of the library's stream, so that every stage is
+ * timed alone.  The timing events are created by the library on first use
+ * and reused.  Stage names are static strings such as "fwd.qkv_gemm" or
+ * "bwd.attention_dkdv". */
 typedef struct {
   const char* name; /* static string */
   int32_t calls;    /* launches recorded since the last read */

@@ -9,7 +9,11 @@
 //   5. chunk merge + decayed scan -> S, M          bandwidth / latency
 //   6. P = M Wm                                    matrix cores (N_b rows)
 //   7. U = H Wg; G = sigmoid(U); Y = H + G * P[blk - 1]  (fused epilogue)
-// Backward runs the chain rule through the same steps in reverse.
+// Backward runs the chain rule through the same steps in reverse.  Its
+// critical path (gate -> memory -> pooling -> dH -> attention -> dX) stays on
+// the caller's stream; the weight-gradient products, which nothing later in
+// the pass reads, run on a library-owned side stream that forks from the
+// caller's stream after their inputs exist and joins it before the pass ends.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -17,6 +21,7 @@
 #include <cstdint>
 #include <cstring>
 #include <algorithm>
+#include <map>
 #include <mutex>
 #include <vector>
 
@@ -41,7 +46,7 @@ struct Plan {
   // forward scratch
   size_t mpart, fwd_bytes;
   // backward scratch
-  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, wpart, bwd_bytes;
+  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, wpart, mpart_b, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -92,8 +97,8 @@ struct Plan {
       size_t w = gemm_wgrad_partial_bytes(D, 3 * D, BTi);
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
-      w = std::max(w, gemm_splitk_partial_bytes(BNi, D, D, 64));
-      wpart = take(w);
+      wpart = take(w);  // weight gradients (side stream, one after another)
+      mpart_b = take(gemm_splitk_partial_bytes(BNi, D, D, 64));  // dM (caller's stream)
     }
     bwd_bytes = off;
   }
@@ -192,6 +197,47 @@ struct TraceScope {
     a = nullptr;
   }
 };
+
+// ------------------------------------------------------------------ side stream
+// One non-blocking side stream per device (default priority) and the events
+// that order it against the caller's stream.  Created on first use and kept
+// until the process ends; a pass holds its device's lock while it enqueues,
+// so that two host threads never interleave their uses of the events.
+struct SideDev {
+  std::mutex mu;
+  hipStream_t side = nullptr;
+  hipEvent_t ev[8] = {};
+  bool ready = false;
+};
+std::mutex g_side_mu;
+std::map<int, SideDev*> g_side;
+
+SideDev* side_for_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  SideDev* d;
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    auto it = g_side.find(dev);
+    if (it == g_side.end()) it = g_side.emplace(dev, new SideDev).first;
+    d = it->second;
+  }
+  std::lock_guard<std::mutex> lk(d->mu);
+  if (!d->ready) {
+    if (hipStreamCreateWithFlags(&d->side, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    for (auto& e : d->ev)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+    d->ready = true;
+  }
+  return d;
+}
+
+// Makes `to` wait for everything enqueued so far on `from`.
+hipError_t order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
+  hipError_t r = hipEventRecord(e, from);
+  if (r != hipSuccess) return r;
+  return hipStreamWaitEvent(to, e, 0);
+}
 
 // A split-K product and its reduction as two traced stages.
 #define LAUNCH_SPLITK(stage, stage_red, dt, g, part, C0, C1, C2, ldc, seg, acc, min_k)           \
@@ -364,7 +410,14 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   if (!ws) return BCMT_ERR_INVALID;
   if (ws_bytes < p.bwd_bytes) return BCMT_ERR_WORKSPACE;
 
-  hipStream_t s = (hipStream_t)stream;
+  SideDev* sd = side_for_current_device();
+  if (!sd) return BCMT_ERR_HIP;
+  std::lock_guard<std::mutex> side_lock(sd->mu);
+  // With per-stage tracing on, everything runs on the caller's stream so
+  // that each stage is timed alone.
+  const bool fork = !g_trace.on.load(std::memory_order_relaxed);
+  const hipStream_t main_s = (hipStream_t)stream, side_s = fork ? sd->side : main_s;
+  hipStream_t s = main_s;  // the stream LAUNCH enqueues on
   const char* SV = (const char*)saved;
   char* W = (char*)ws;
   const int BT = p.B * p.T, D = p.D, BN = p.B * p.nb;
@@ -373,6 +426,15 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
 
   const bool accum = cfg->flags & BCMT_FLAG_ACCUM_WGRAD;
   float* wpart = (float*)(W + p.wpart);
+  int nev = 0;
+  // Work between SIDE_BEGIN and SIDE_END runs on the side stream, after
+  // everything enqueued so far on the caller's stream.
+#define SIDE_BEGIN()                                                                   \
+  do {                                                                                 \
+    if (fork && order_after(side_s, main_s, sd->ev[nev++]) != hipSuccess) return BCMT_ERR_HIP; \
+    s = side_s;                                                                        \
+  } while (0)
+#define SIDE_END() (s = main_s)
   // dwp and dgamma are reduced with atomics; the weight matrices are written
   // (or accumulated) by the split-K reductions.
   if (!accum && (gr.dwp || gr.dgamma))
@@ -381,22 +443,30 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   // Gate and injection: dU, and the block sums of dY * G shifted back by one.
   LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar, p.B, p.T, D,
                   p.L, s));
-  if (gr.dWg) {
-    GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
-                  accum, 512);
+  // dWg = H^T dU and dWm = M^T dP on the side stream.
+  if (gr.dWg || gr.dWm) {
+    SIDE_BEGIN();
+    {
+      if (gr.dWg) {
+        GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+        LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
+                      accum, 512);
+      }
+      if (gr.dWm) {
+        GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
+                   0, 1};
+        LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
+                      accum, 512);
+      }
+    }
+    SIDE_END();
   }
-  // Memory projection: dM = dP Wm^T and dWm = M^T dP.
+  // Memory projection: dM = dP Wm^T.
   {
     GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
                1};
-    LAUNCH_SPLITK(ST_WM_DGRAD, ST_WM_DGRAD_RED, dt, g, wpart, (float*)(W + p.mbar), nullptr,
-                  nullptr, D, D, false, 64);
-  }
-  if (gr.dWm) {
-    GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
-                  accum, 512);
+    LAUNCH_SPLITK(ST_WM_DGRAD, ST_WM_DGRAD_RED, dt, g, (float*)(W + p.mpart_b),
+                  (float*)(W + p.mbar), nullptr, nullptr, D, D, false, 64);
   }
   // Decayed reverse scan: dS and the decay gradient.
   LAUNCH(ST_MEM_BWD, mem_bwd((const float*)(W + p.mbar), (const float*)(SV + p.M), (float*)(W + p.dS),
@@ -412,15 +482,19 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
               (const float*)(W + p.dS), prm->wp, p.T, p.L, p.nb, D};
     LAUNCH(ST_HBAR, gemm_hbar(dt, g, e, s));
   }
-  // Output projection backward.
+  // Output projection backward: dWo on the side stream, dHcat here.
+  if (gr.dWo) {
+    SIDE_BEGIN();
+    {
+      GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+      LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
+                    accum, 512);
+    }
+    SIDE_END();
+  }
   {
     GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
-  }
-  if (gr.dWo) {
-    GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
-                  accum, 512);
   }
   // Block-local attention backward.
   LAUNCH(ST_ATTN_BWD_DQ,
@@ -429,17 +503,26 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   LAUNCH(ST_ATTN_BWD_DKDV,
          attn_bwd_dkdv(dt, SV + p.qkv, W + p.dout, (const float*)(SV + p.lse),
                        (const float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
-  // Q/K/V projections backward.
+  // Q/K/V projections backward: dW{q,k,v} on the side stream, dX here.
+  if (gr.dWq || gr.dWk || gr.dWv) {
+    SIDE_BEGIN();
+    {
+      GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone,
+                 0, 1};
+      LAUNCH_SPLITK(ST_QKV_WGRAD, ST_QKV_WGRAD_RED, dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D,
+                    accum, 512);
+    }
+    SIDE_END();
+  }
   if (dX) {
     GemmDesc g{BT, D, 3 * D, W + p.dqkv, 3 * D, false, {prm->Wq, prm->Wk, prm->Wv}, D, false,
                kSegK, D, 1};
     LAUNCH(ST_DX, gemm_store(dt, g, dX, D, false, residual ? dY : nullptr, D, s));
   }
-  if (gr.dWq || gr.dWk || gr.dWv) {
-    GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone, 0, 1};
-    LAUNCH_SPLITK(ST_QKV_WGRAD, ST_QKV_WGRAD_RED, dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D,
-                  accum, 512);
-  }
+  // Join: later work on the caller's stream sees every side-stream result.
+  if (nev > 0 && order_after(main_s, side_s, sd->ev[nev++]) != hipSuccess) return BCMT_ERR_HIP;
+#undef SIDE_BEGIN
+#undef SIDE_END
   return BCMT_OK;
 }
 
