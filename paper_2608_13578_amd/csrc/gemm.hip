@@ -311,7 +311,7 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int R, int BK, bool RCONTIG, int SEG>
+template <int R, int BK, bool RCONTIG>
 struct PipeOperand {
   static_assert(BK == 32 || BK == 64, "slab depth");
   static constexpr int ELEMS = R * BK;
@@ -322,33 +322,75 @@ struct PipeOperand {
   __device__ __forceinline__ static int kswz(int r) {
     return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
   }
+};
 
-  // Issue this wave's share of the direct loads of one slab.
-  template <int NW>
-  __device__ __forceinline__ static void issue(const Operand<bf16, RCONTIG, SEG>& op, bf16* dst,
-                                               int r0, int rmax, int k0, int wave, int lane) {
-    static_assert(INSTR % NW == 0, "loads per wave");
+// The direct loads of one operand of one workgroup.  A slab is addressed by
+// a wave-uniform base pointer (scalar registers) plus a per-lane byte offset
+// that does not change from slab to slab, so issuing a load costs no vector
+// arithmetic.  Rows beyond the operand's last one are clamped to it (their
+// products are never stored), so every address lies inside the operand; the
+// buffer descriptor's size is the extent the slab may touch, so a stray
+// offset would read zeros rather than leave it.
+//   K-contiguous (RCONTIG false): row r of the tile, 16-byte chunk c of the
+//     slab; base = P + r0 * ld + k.
+//   row-contiguous (RCONTIG true): k-row kr of the slab, 16-byte chunk c of
+//     the tile's rows; base = P + k * ld + c0 with c0 = min(r0, rmax - 8).
+template <int R, int BK, bool RCONTIG, int NW>
+struct PipeLoad {
+  typedef PipeOperand<R, BK, RCONTIG> Op;
+  static constexpr int PER = Op::INSTR / NW;  // loads per wave per slab
+  static_assert(Op::INSTR % NW == 0, "loads per wave");
+  uint32_t voff[PER];
+  uint32_t extent;  // bytes a slab may touch from its base
+  int r0, c0;
+
+  __device__ __forceinline__ void setup(int row0, int rmax, int64_t ld, int wave, int lane) {
+    r0 = row0;
+    if constexpr (!RCONTIG) {
+      constexpr int RPI = 64 / Op::KCH;  // rows per load instruction
+      const int nrows = min(R, rmax - row0);
 #pragma unroll
-    for (int i = 0; i < INSTR / NW; ++i) {
-      const int gi = wave * (INSTR / NW) + i;
-      const bf16* src;
-      if constexpr (!RCONTIG) {
-        constexpr int RPI = 64 / KCH;   // rows per instruction
-        const int row = gi * RPI + lane / KCH;
-        const int cg = (lane % KCH) ^ kswz(row);
-        const int gr = min(r0 + row, rmax - 1);
-        src = op.at(gr, k0 + cg * 8);
-      } else {
-        constexpr int CPR = R / 8;        // 16-byte chunks per k-row
-        constexpr int RPI = 64 / CPR;     // k-rows per instruction
-        static_assert(CPR >= 16 && 64 % CPR == 0, "row width");
-        const int kr = gi * RPI + lane / CPR;
-        const int cg = (lane % CPR) ^ (kr & 15);
-        const int gc = min(r0 + cg * 8, rmax - 8);
-        src = op.at(gc, k0 + kr);
+      for (int i = 0; i < PER; ++i) {
+        const int row = (wave * PER + i) * RPI + lane / Op::KCH;
+        const int cg = (lane % Op::KCH) ^ Op::kswz(row);
+        const int rr = min(row, nrows - 1);
+        voff[i] = (uint32_t)(((int64_t)rr * ld + cg * 8) * 2);
       }
-      __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(dst + gi * 512), 16, 0, 0);
+      extent = (uint32_t)(((int64_t)(nrows - 1) * ld + BK) * 2);
+    } else {
+      constexpr int CPR = R / 8;     // 16-byte chunks per k-row
+      constexpr int RPI = 64 / CPR;  // k-rows per load instruction
+      static_assert(CPR >= 16 && 64 % CPR == 0, "row width");
+      c0 = min(row0, rmax - 8);
+      const int cend = min(row0 + R, rmax);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int kr = (wave * PER + i) * RPI + lane / CPR;
+        const int cg = (lane % CPR) ^ (kr & 15);
+        const int gc = min(row0 + cg * 8, rmax - 8);
+        voff[i] = (uint32_t)(((int64_t)kr * ld + (gc - c0)) * 2);
+      }
+      extent = (uint32_t)(((int64_t)(BK - 1) * ld + (cend - c0)) * 2);
     }
+  }
+
+  // Base of the slab starting at k (relative to pointer P).
+  __device__ __forceinline__ const bf16* slab(const bf16* P, int64_t ld, int k) const {
+    if constexpr (!RCONTIG) return P + (int64_t)r0 * ld + k;
+    else return P + (int64_t)k * ld + c0;
+  }
+
+  // This wave's loads of one slab into dst (the operand's LDS region).
+  // (The buffer-descriptor type exists only in the device compilation pass.)
+  __device__ __forceinline__ void issue(const bf16* base, bf16* dst, int wave) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)extent, 0x00020000);
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + (wave * PER + i) * 512), 16,
+                                               voff[i], 0, 0, 0);
+#endif
   }
 
   // Fragment for rows/columns base .. base+15 of the tile, 32-wide K step ks.
@@ -356,7 +398,7 @@ struct PipeOperand {
     const int lr = lane & 15, lg = lane >> 4;
     if constexpr (!RCONTIG) {
       const int r = base + lr;
-      const int c = (ks * 4 + lg) ^ kswz(r);
+      const int c = (ks * 4 + lg) ^ Op::kswz(r);
       return *reinterpret_cast<const bf16x8*>(s + r * BK + c * 8);
     } else {
       const int col = base + (lr & 3) * 4;
@@ -406,14 +448,16 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
-  typedef PipeOperand<BM, BK, A_MC, kSegNone> PA;
-  typedef PipeOperand<BN, BK, B_NC, BSEG> PB;
-  constexpr int STAGE = PA::ELEMS + PB::ELEMS;
-  constexpr int NI = (PA::INSTR + PB::INSTR) / NW;  // loads per wave per slab
+  typedef PipeLoad<BM, BK, A_MC, NW> LA;
+  typedef PipeLoad<BN, BK, B_NC, NW> LB;
+  constexpr int AEL = LA::Op::ELEMS;
+  constexpr int STAGE = AEL + LB::Op::ELEMS;
+  constexpr int NI = LA::PER + LB::PER;  // loads per wave per slab
   __shared__ __attribute__((aligned(1024))) bf16 lds[STAGES * STAGE];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
   int tm, tn;
   xcd_tile_order(blockIdx.x, blockIdx.y, gridDim.x, gridDim.y, tm, tn);
@@ -421,6 +465,31 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
   const int kbeg = blockIdx.z * kchunk;
   const int kend = min(K, kbeg + kchunk);
   const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+
+  // B split along N: the tile lies inside one part (the launcher checks that
+  // the part width is a multiple of BN).
+  const bf16* bptr = B.p[0];
+  int bn0 = n0, bnmax = N;
+  if constexpr (BSEG == kSegN) {
+    const int sg = n0 / B.seg_len;
+    bptr = B.p[sg];
+    bn0 = n0 - sg * B.seg_len;
+    bnmax = B.seg_len;
+  }
+  LA la;
+  LB lb;
+  la.setup(m0, M, A.ld, wave, lane);
+  lb.setup(bn0, bnmax, B.ld, wave, lane);
+  // Slab base of B at global k (B split along K: each slab lies inside one
+  // part; the launcher checks that the part length is a multiple of BK).
+  auto bslab = [&](int k) {
+    if constexpr (BSEG == kSegK) {
+      const int sg = k / B.seg_len;
+      return lb.slab(B.p[sg], B.ld, k - sg * B.seg_len);
+    } else {
+      return lb.slab(bptr, B.ld, k);
+    }
+  };
 
   f32x4 acc[FM][FN];
 #pragma unroll
@@ -432,8 +501,9 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
   for (int st = 0; st < STAGES - 1; ++st) {
     if (st < nk) {
       bf16* sa = lds + st * STAGE;
-      PA::template issue<NW>(A, sa, m0, M, kbeg + st * BK, wave, lane);
-      PB::template issue<NW>(B, sa + PA::ELEMS, n0, N, kbeg + st * BK, wave, lane);
+      const int k = kbeg + st * BK;
+      la.issue(la.slab(A.p[0], A.ld, k), sa, wave);
+      lb.issue(bslab(k), sa + AEL, wave);
     }
   }
 
@@ -458,18 +528,19 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
     const int nxt = kt + STAGES - 1;
     if (nxt < nk) {
       bf16* sa = lds + (nxt % STAGES) * STAGE;
-      PA::template issue<NW>(A, sa, m0, M, kbeg + nxt * BK, wave, lane);
-      PB::template issue<NW>(B, sa + PA::ELEMS, n0, N, kbeg + nxt * BK, wave, lane);
+      const int k = kbeg + nxt * BK;
+      la.issue(la.slab(A.p[0], A.ld, k), sa, wave);
+      lb.issue(bslab(k), sa + AEL, wave);
     }
     const bf16* sa = lds + (kt % STAGES) * STAGE;
-    const bf16* sb = sa + PA::ELEMS;
+    const bf16* sb = sa + AEL;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       bf16x8 fa[FM], fb[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) fa[i] = PA::frag(sa, wm * WTM + i * 16, ks, lane);
+      for (int i = 0; i < FM; ++i) fa[i] = LA::frag(sa, wm * WTM + i * 16, ks, lane);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) fb[j] = PB::frag(sb, wn * WTN + j * 16, ks, lane);
+      for (int j = 0; j < FN; ++j) fb[j] = LB::frag(sb, wn * WTN + j * 16, ks, lane);
       if constexpr (A_MC || B_NC) {  // transposing reads went through inline assembly
         lds_tr_wait();
 #pragma unroll
@@ -541,7 +612,12 @@ hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
 template <typename T, bool AMC, bool BNC, int SEG, class Epi>
 hipError_t launch_any(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
-    if (g.K % 64 == 0) return launch_pipe<AMC, BNC, SEG>(g, epi, s);
+    // The pipelined kernel needs whole 64-deep slabs, operands of at least
+    // 8 rows, and B parts that never split a tile (N) or a slab (K).
+    bool ok = g.K % 64 == 0 && g.M >= 8 && g.N >= 8;
+    if (SEG == kSegN) ok = ok && g.seg_len % 128 == 0;
+    if (SEG == kSegK) ok = ok && g.seg_len % 64 == 0;
+    if (ok) return launch_pipe<AMC, BNC, SEG>(g, epi, s);
   }
   return launch<T, AMC, BNC, SEG>(g, epi, s);
 }
