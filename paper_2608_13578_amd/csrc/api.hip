@@ -5,9 +5,9 @@
 //   1. [Q|K|V] = X [Wq|Wk|Wv]                      matrix cores
 //   2. block-local causal attention -> Hcat, lse   matrix cores
 //   3. H = Hcat Wo                                 matrix cores
-//   4. pooling scores and per-chunk softmax sums   bandwidth
-//   5. chunk merge + decayed scan -> S, M          bandwidth / latency
-//   6. P = M Wm                                    matrix cores (N_b rows)
+//   4. pooling scores, block softmax -> S          bandwidth
+//   5. Q = S Wm (split-K partials)                 matrix cores (N_b rows)
+//   6. decayed scans of S and Q -> M, P = M Wm     latency
 //   7. U = H Wg; G = sigmoid(U); Y = H + G * P[blk - 1]  (fused epilogue)
 // Backward runs the chain rule through the same steps in reverse.  Its
 // critical path (gate -> memory -> pooling -> dH -> attention -> dX) stays on
@@ -44,9 +44,9 @@ struct Plan {
   // saved (forward -> backward)
   size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
   // forward scratch
-  size_t mpart, fwd_bytes;
+  size_t St, mpart, fwd_bytes;
   // backward scratch
-  size_t du, pbar, mbar, dS, a, ds, dh, dout, delta, dqkv, wpart, mpart_b, bwd_bytes;
+  size_t du, pbar, dS, a, ds, dh, dout, delta, dqkv, wpart, mpart_b, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -78,13 +78,15 @@ struct Plan {
     saved_bytes = off;
 
     off = 0;
-    mpart = take(gemm_splitk_partial_bytes(B * nb, D, D, 64));
+    St = take(BND * es);
+    // split-K partials of the memory projection (at least one slice: the
+    // scan reads them even when the product has a single split)
+    mpart = take(std::max(gemm_splitk_partial_bytes(B * nb, D, D, 64), BND * 4));
     fwd_bytes = off;
 
     off = 0;
     du = take(BTD * es);
     pbar = take(BND * es);
-    mbar = take(BND * 4);
     dS = take(BND * 4);
     a = take(BT * 4);
     ds = take(BT * 4);
@@ -98,7 +100,8 @@ struct Plan {
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
       wpart = take(w);  // weight gradients (side stream, one after another)
-      mpart_b = take(gemm_splitk_partial_bytes(BNi, D, D, 64));  // dM (caller's stream)
+      // dM as split-K partials, read by the reverse scan (caller's stream)
+      mpart_b = take(std::max(gemm_splitk_partial_bytes(BNi, D, D, 64), BND * 4));
     }
     bwd_bytes = off;
   }
@@ -131,17 +134,16 @@ bool overlaps(const void* a, const void* b, size_t n) {
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
 enum Stage {
-  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_WM, ST_WM_RED, ST_GATE,
-  ST_ZERO, ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_DGRAD_RED, ST_WM_WGRAD,
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_WM, ST_SCAN_FWD, ST_GATE,
+  ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_WGRAD,
   ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
-    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.scan", "fwd.wm_gemm",
-    "fwd.wm_reduce", "fwd.gate_gemm", "bwd.zero_grads", "bwd.gate", "bwd.wg_wgrad_gemm",
-    "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm", "bwd.wm_dgrad_reduce", "bwd.wm_wgrad_gemm",
-    "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm",
+    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.wm_gemm", "fwd.scan",
+    "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm",
+    "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
 
@@ -362,18 +364,22 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
     GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
     LAUNCH(ST_WO, gemm_store(dt, g, SV + p.h, D, false, nullptr, 0, s));
   }
-  // 4-5. Adaptive summaries (Sec. 3.4) and the exponential memory (Sec. 3.5).
+  // 4. Adaptive summaries (Sec. 3.4).
   LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, prm->wp, (float*)(SV + p.s), (float*)(SV + p.S),
-                               (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
-  LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(SV + p.S), (float*)(SV + p.M), SV + p.Mt, p.B,
-                               p.T, D, p.L, cfg->gamma, s));
-  // 6. Memory projection (Sec. 3.5); the shift is applied where P is read.
+                               W + p.St, (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
+  // 5-6. Exponential memory and its projection (Sec. 3.5).  The projection
+  // is linear and so is the normalised decayed sum, so the summaries are
+  // projected first (Q = S Wm, as split-K partial products over only
+  // B * N_b rows) and one scan then yields both M and P = M Wm; the shift is
+  // applied where P is read.
+  int qs = 0;
   {
-    // Only B * N_b rows: split K so that every workgroup has one or two slabs.
-    GemmDesc g{p.B * p.nb, D, D, SV + p.Mt, D, false, {prm->Wm, nullptr, nullptr}, D, true,
+    float* Q = (float*)(W + p.mpart);
+    GemmDesc g{p.B * p.nb, D, D, W + p.St, D, false, {prm->Wm, nullptr, nullptr}, D, true,
                kSegNone, 0, 1};
-    LAUNCH_SPLITK(ST_WM, ST_WM_RED, dt, g, (float*)(W + p.mpart), (float*)(SV + p.P), nullptr,
-                  nullptr, D, D, false, 64);
+    LAUNCH(ST_WM, gemm_splitk_product(dt, g, Q, Q, nullptr, nullptr, D, D, false, 64, &qs, s));
+    LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(SV + p.S), Q, qs, (float*)(SV + p.M),
+                                 SV + p.Mt, (float*)(SV + p.P), p.B, p.T, D, p.L, cfg->gamma, s));
   }
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
@@ -435,14 +441,13 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     s = side_s;                                                                        \
   } while (0)
 #define SIDE_END() (s = main_s)
-  // dwp and dgamma are reduced with atomics; the weight matrices are written
-  // (or accumulated) by the split-K reductions.
-  if (!accum && (gr.dwp || gr.dgamma))
-    LAUNCH(ST_ZERO, zero_two(gr.dwp, D, gr.dgamma, 1, s));
-
   // Gate and injection: dU, and the block sums of dY * G shifted back by one.
-  LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar, p.B, p.T, D,
-                  p.L, s));
+  // dwp and dgamma are reduced with atomics later in the pass; this kernel
+  // clears them first unless the gradients accumulate.  The weight matrices
+  // are written (or accumulated) by the split-K reductions.
+  LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
+                               accum ? nullptr : gr.dwp, D, accum ? nullptr : gr.dgamma, p.B,
+                               p.T, D, p.L, s));
   // dWg = H^T dU and dWm = M^T dP on the side stream.
   if (gr.dWg || gr.dWm) {
     SIDE_BEGIN();
@@ -461,16 +466,17 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     }
     SIDE_END();
   }
-  // Memory projection: dM = dP Wm^T.
+  // Memory projection: dM = dP Wm^T as split-K partials, summed by the
+  // decayed reverse scan that follows (dS and the decay gradient).
   {
+    int ms = 0;
+    float* Mp = (float*)(W + p.mpart_b);
     GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
                1};
-    LAUNCH_SPLITK(ST_WM_DGRAD, ST_WM_DGRAD_RED, dt, g, (float*)(W + p.mpart_b),
-                  (float*)(W + p.mbar), nullptr, nullptr, D, D, false, 64);
+    LAUNCH(ST_WM_DGRAD, gemm_splitk_product(dt, g, Mp, Mp, nullptr, nullptr, D, D, false, 64, &ms, s));
+    LAUNCH(ST_MEM_BWD, mem_bwd(Mp, ms, (const float*)(SV + p.M), (float*)(W + p.dS), gr.dgamma,
+                               p.B, p.nb, D, cfg->gamma, s));
   }
-  // Decayed reverse scan: dS and the decay gradient.
-  LAUNCH(ST_MEM_BWD, mem_bwd((const float*)(W + p.mbar), (const float*)(SV + p.M), (float*)(W + p.dS),
-                 gr.dgamma, p.B, p.nb, D, cfg->gamma, s));
   // Pooling backward: per-token a_t, ds_t and dwp.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
                   (const float*)(SV + p.S), (const float*)(W + p.dS), prm->wp, (float*)(W + p.a),

@@ -103,17 +103,22 @@ hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const floa
                          hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
-// Pooling: scores s [B*T], summaries S [B*nb, D] and per-block softmax
-// statistics (max, normaliser) [B*nb, 2].
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, float* stats,
-                    int B, int T, int D, int L, hipStream_t s);
-// Decayed scan of the summaries: M (float32) and its compute-type copy Mt.
-hipError_t scan_fwd(DType dt, const float* S, float* M, void* Mt, int B, int T, int D, int L,
-                    float gamma, hipStream_t s);
+// Pooling: scores s [B*T], summaries S [B*nb, D] (float32, and St in the
+// compute type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, void* St,
+                    float* stats, int B, int T, int D, int L, hipStream_t s);
+// Decayed scan: M (float32) and its compute-type copy Mt from the summaries
+// S, and P from the projected summaries, given as qs split-K partial
+// products Q (each [B*nb, D], consecutive).
+hipError_t scan_fwd(DType dt, const float* S, const float* Q, int qs, float* M, void* Mt, float* P,
+                    int B, int T, int D, int L, float gamma, hipStream_t s);
+// Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
-                    void* Pbar, int B, int T, int D, int L, hipStream_t s);
-hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,
-                   int D, float gamma, hipStream_t s);
+                    void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
+                    hipStream_t s);
+// Reverse decayed scan; dM is given as ms split-K partial products.
+hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float* dgamma, int B,
+                   int nb, int D, float gamma, hipStream_t s);
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
                     const float* S, const float* dS, const void* wp, float* a_out,
                     float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s);

@@ -48,7 +48,7 @@ template <typename T, int NVJ>
 __global__ __launch_bounds__(1024) void pool_fwd_kernel(const T* __restrict__ H,
                                                         const T* __restrict__ wp,
                                                         float* __restrict__ s_out,
-                                                        float* __restrict__ S,
+                                                        float* __restrict__ S, T* __restrict__ St,
                                                         float* __restrict__ stats, int Tn, int D,
                                                         int L, int nb) {
   constexpr int VE = Vec16<T>::N;
@@ -141,6 +141,7 @@ __global__ __launch_bounds__(1024) void pool_fwd_kernel(const T* __restrict__ H,
     for (int k = 0; k < nw; ++k)
       if (stat[k * 2] != -INFINITY) sum += __expf(stat[k * 2] - mm) * red[k * D + col];
     S[(int64_t)(b * nb + i) * D + col] = sum * inv;
+    St[(int64_t)(b * nb + i) * D + col] = from_f32<T>(sum * inv);
   }
   if (tid == 0) {
     stats[(int64_t)(b * nb + i) * 2] = mm;
@@ -149,11 +150,17 @@ __global__ __launch_bounds__(1024) void pool_fwd_kernel(const T* __restrict__ H,
 }
 
 // ------------------------------------------------------------------ decayed scan
+// The same recurrence runs over two inputs: the summaries S (giving M, kept
+// for the backward) and their projections Q_i = S_i W_m, given as the sum of
+// the qs split-K partial products (giving P_i = M_i W_m, since the
+// normalised decayed sum is linear in its input).
 template <typename T>
 __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__ S,
-                                                       float* __restrict__ M, T* __restrict__ Mt,
+                                                       const float* __restrict__ Q, int qs,
+                                                       int64_t qstride, float* __restrict__ M,
+                                                       T* __restrict__ Mt, float* __restrict__ P,
                                                        int nb, int D, float gamma) {
-  __shared__ float cN[8][32];
+  __shared__ float cN[8][32], cP[8][32];
   __shared__ float cZ[8], cG[8];
   const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
   const int col = blockIdx.x * 32 + cl;
@@ -162,35 +169,47 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__
   const int SL = (nb + 7) / 8;
   const int i0 = seg * SL;
   const int i1 = min(nb, i0 + SL);
+  auto qsum = [&](int64_t off) {
+    float v = 0.f;
+    for (int z = 0; z < qs; ++z) v += Q[z * qstride + off];
+    return v;
+  };
 
-  float N = 0.f, Z = 0.f, g = 1.f;
+  float N = 0.f, NP = 0.f, Z = 0.f, g = 1.f;
   for (int i = i0; i < i1; ++i) {
-    const float sv = act ? S[(int64_t)(b * nb + i) * D + col] : 0.f;
-    N = gamma * N + sv;
+    const int64_t off = (int64_t)(b * nb + i) * D + col;
+    N = gamma * N + (act ? S[off] : 0.f);
+    NP = gamma * NP + (act ? qsum(off) : 0.f);
     Z = gamma * Z + 1.f;
     g *= gamma;
   }
   cN[seg][cl] = N;
+  cP[seg][cl] = NP;
   if (cl == 0) {
     cZ[seg] = Z;
     cG[seg] = g;
   }
   __syncthreads();
-  float Nin = 0.f, Zin = 0.f;
+  float Nin = 0.f, Pin = 0.f, Zin = 0.f;
   for (int k = 0; k < seg; ++k) {
     Nin = cG[k] * Nin + cN[k][cl];
+    Pin = cG[k] * Pin + cP[k][cl];
     Zin = cG[k] * Zin + cZ[k];
   }
   if (!act) return;
   N = Nin;
+  NP = Pin;
   Z = Zin;
   for (int i = i0; i < i1; ++i) {
     const int64_t off = (int64_t)(b * nb + i) * D + col;
     N = gamma * N + S[off];
+    NP = gamma * NP + qsum(off);
     Z = gamma * Z + 1.f;
-    const float m = N / Z;
+    const float rz = 1.f / Z;
+    const float m = N * rz;
     M[off] = m;
     Mt[off] = from_f32<T>(m);
+    P[off] = NP * rz;
   }
 }
 
@@ -202,12 +221,21 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__
 // already shifted back by one block (row i-1 holds block i's sum; the last
 // row of each batch element is zero), in the compute type, as the left
 // operand of the W_m backward products.
+// The first workgroup also clears dwp and dgamma (when given), which later
+// kernels of the pass accumulate into with atomics.
 template <typename T>
 __global__ __launch_bounds__(1024) void gate_bwd_kernel(const T* __restrict__ dY,
                                                         const T* __restrict__ G,
                                                         const float* __restrict__ P,
                                                         T* __restrict__ dU, T* __restrict__ Pbar,
-                                                        int Tn, int D, int L, int nb) {
+                                                        float* __restrict__ zero_a, int na,
+                                                        float* __restrict__ zero_b, int Tn, int D,
+                                                        int L, int nb) {
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    for (int k = threadIdx.x; k < na; k += blockDim.x)
+      if (zero_a) zero_a[k] = 0.f;
+    if (threadIdx.x == 0 && zero_b) *zero_b = 0.f;
+  }
   constexpr int VE = Vec16<T>::N;
   constexpr int U = 4;
   typedef typename Vec16<T>::type vec;
@@ -285,11 +313,17 @@ __device__ __forceinline__ float zsum(int i, float gamma) {
   return (1.f - powf(gamma, (float)(i + 1))) / (1.f - gamma);
 }
 
-__global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ Mbar,
-                                                      const float* __restrict__ M,
+// dM arrives as the sum of ms split-K partial products (stride mstride).
+__global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ Mpart, int ms,
+                                                      int64_t mstride, const float* __restrict__ M,
                                                       float* __restrict__ dS,
                                                       float* __restrict__ dgamma, int nb, int D,
                                                       float gamma) {
+  auto mbar = [&](int64_t off) {
+    float v = 0.f;
+    for (int z = 0; z < ms; ++z) v += Mpart[z * mstride + off];
+    return v;
+  };
   __shared__ float cQ[8][32], cE[8][32];
   __shared__ float cG[8];
   __shared__ float red[4];
@@ -304,7 +338,7 @@ __global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ 
   float Q = 0.f, E = 0.f, g = 1.f;
   for (int i = i1 - 1; i >= i0; --i) {
     const int64_t off = (int64_t)(b * nb + i) * D + col;
-    const float mb = act ? Mbar[off] : 0.f;
+    const float mb = act ? mbar(off) : 0.f;
     const float m = act ? M[off] : 0.f;
     const float z = zsum(i, gamma);
     Q = mb / z + gamma * Q;
@@ -326,7 +360,7 @@ __global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ 
   if (act) {
     for (int i = i1 - 1; i >= i0; --i) {
       const int64_t off = (int64_t)(b * nb + i) * D + col;
-      const float mb = Mbar[off];
+      const float mb = mbar(off);
       const float z = zsum(i, gamma);
       Q = mb / z + gamma * Q;
       E = -mb * M[off] / z + gamma * E;
@@ -466,24 +500,24 @@ int pool_waves(int L, int T, int D) {
 }
 
 template <typename E, int NV>
-hipError_t pool_fwd_nv(const void* H, const void* wp, float* s_out, float* S, float* stats, int B,
-                       int T, int D, int L, hipStream_t s) {
+hipError_t pool_fwd_nv(const void* H, const void* wp, float* s_out, float* S, void* St,
+                       float* stats, int B, int T, int D, int L, hipStream_t s) {
   const int nb = (T + L - 1) / L;
   const int nw = pool_waves<NV>(L, T, D);
   const size_t lds = ((size_t)nw * D + 2 * nw) * sizeof(float);
   hipLaunchKernelGGL((pool_fwd_kernel<E, NV>), dim3(nb, B), dim3(nw * 64), lds, s, (const E*)H,
-                     (const E*)wp, s_out, S, stats, T, D, L, nb);
+                     (const E*)wp, s_out, S, (E*)St, stats, T, D, L, nb);
   return hipGetLastError();
 }
 
 template <typename E>
-hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* S, float* stats, int B,
-                      int T, int D, int L, hipStream_t s) {
+hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* S, void* St,
+                      float* stats, int B, int T, int D, int L, hipStream_t s) {
   switch (nvj_for(D / Vec16<E>::N)) {
-    case 1: return pool_fwd_nv<E, 1>(H, wp, s_out, S, stats, B, T, D, L, s);
-    case 2: return pool_fwd_nv<E, 2>(H, wp, s_out, S, stats, B, T, D, L, s);
-    case 4: return pool_fwd_nv<E, 4>(H, wp, s_out, S, stats, B, T, D, L, s);
-    default: return pool_fwd_nv<E, 8>(H, wp, s_out, S, stats, B, T, D, L, s);
+    case 1: return pool_fwd_nv<E, 1>(H, wp, s_out, S, St, stats, B, T, D, L, s);
+    case 2: return pool_fwd_nv<E, 2>(H, wp, s_out, S, St, stats, B, T, D, L, s);
+    case 4: return pool_fwd_nv<E, 4>(H, wp, s_out, S, St, stats, B, T, D, L, s);
+    default: return pool_fwd_nv<E, 8>(H, wp, s_out, S, St, stats, B, T, D, L, s);
   }
 }
 
@@ -512,8 +546,9 @@ hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, cons
 }
 
 template <typename E>
-hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, void* Pbar, int B,
-                      int T, int D, int L, hipStream_t s) {
+hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, void* Pbar,
+                      float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
+                      hipStream_t s) {
   const int nb = (T + L - 1) / L;
   const int Dv = D / Vec16<E>::N;
   int tg = 1024 / Dv;
@@ -522,40 +557,46 @@ hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, v
   if (tg < 1) tg = 1;
   const size_t lds = (size_t)tg * D * sizeof(float);
   hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B), dim3(tg * Dv), lds, s, (const E*)dY,
-                     (const E*)G, P, (E*)dU, (E*)Pbar, T, D, L, nb);
+                     (const E*)G, P, (E*)dU, (E*)Pbar, zero_a, na, zero_b, T, D, L, nb);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, float* stats,
-                    int B, int T, int D, int L, hipStream_t s) {
-  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, S, stats, B, T, D, L, s);
-  return pool_fwd_t<float>(H, wp, s_out, S, stats, B, T, D, L, s);
+hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, void* St,
+                    float* stats, int B, int T, int D, int L, hipStream_t s) {
+  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, S, St, stats, B, T, D, L, s);
+  return pool_fwd_t<float>(H, wp, s_out, S, St, stats, B, T, D, L, s);
 }
 
-hipError_t scan_fwd(DType dt, const float* S, float* M, void* Mt, int B, int T, int D, int L,
-                    float gamma, hipStream_t s) {
+hipError_t scan_fwd(DType dt, const float* S, const float* Q, int qs, float* M, void* Mt, float* P,
+                    int B, int T, int D, int L, float gamma, hipStream_t s) {
   const int nb = (T + L - 1) / L;
+  const int64_t qstride = (int64_t)B * nb * D;
   dim3 grid((D + 31) / 32, B);
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, S, M, (bf16*)Mt, nb, D, gamma);
+    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, S, Q, qs, qstride, M,
+                       (bf16*)Mt, P, nb, D, gamma);
   else
-    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, S, M, (float*)Mt, nb, D,
-                       gamma);
+    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, S, Q, qs, qstride, M,
+                       (float*)Mt, P, nb, D, gamma);
   return hipGetLastError();
 }
 
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
-                    void* Pbar, int B, int T, int D, int L, hipStream_t s) {
-  if (dt == DType::BF16) return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, B, T, D, L, s);
-  return gate_bwd_t<float>(dY, G, P, dU, Pbar, B, T, D, L, s);
+                    void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
+                    hipStream_t s) {
+  if (dt == DType::BF16)
+    return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, s);
+  return gate_bwd_t<float>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, s);
 }
 
-hipError_t mem_bwd(const float* Mbar, const float* M, float* dS, float* dgamma, int B, int nb,
-                   int D, float gamma, hipStream_t s) {
+hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float* dgamma, int B,
+                   int nb, int D, float gamma, hipStream_t s) {
   dim3 grid((D + 31) / 32, B);
-  hipLaunchKernelGGL(mem_bwd_kernel, grid, dim3(256), 0, s, Mbar, M, dS, dgamma, nb, D, gamma);
+  const int64_t mstride = (int64_t)B * nb * D;
+  hipLaunchKernelGGL(mem_bwd_kernel, grid, dim3(256), 0, s, Mpart, ms, mstride, M, dS, dgamma, nb,
+                     D, gamma);
   return hipGetLastError();
 }
 
