@@ -44,7 +44,7 @@ struct Plan {
   // saved (forward -> backward)
   size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
   // forward scratch
-  size_t St, mpart, fwd_bytes;
+  size_t sp, St, mpart, fwd_bytes;
   // backward scratch
   size_t du, pbar, dS, a, ds, dh, dout, delta, dqkv, wpart, mpart_b, bwd_bytes;
 
@@ -78,6 +78,7 @@ struct Plan {
     saved_bytes = off;
 
     off = 0;
+    sp = take(BT * (D / kDh) * 4);  // partial pooling scores, D / 64 per token
     St = take(BND * es);
     // split-K partials of the memory projection (at least one slice: the
     // scan reads them even when the product has a single split)
@@ -136,14 +137,14 @@ bool overlaps(const void* a, const void* b, size_t n) {
 enum Stage {
   ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_WM, ST_SCAN_FWD, ST_GATE,
   ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_WGRAD,
-  ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
+  ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_DWP, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.wm_gemm", "fwd.scan",
     "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm",
-    "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.wg_dgrad_gemm",
+    "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.pool_dwp", "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
 
@@ -359,14 +360,15 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
   }
   // 2. Block-local causal attention (Sec. 3.3, 3.6).
   LAUNCH(ST_ATTN_FWD, attn_fwd(dt, SV + p.qkv, SV + p.o, (float*)(SV + p.lse), p.B, p.T, D, p.H, p.L, s));
-  // 3. Output projection (Sec. 3.3).
+  // 3. Output projection (Sec. 3.3), also writing partial pooling scores.
   {
     GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    LAUNCH(ST_WO, gemm_store(dt, g, SV + p.h, D, false, nullptr, 0, s));
+    LAUNCH(ST_WO, gemm_score(dt, g, SV + p.h, prm->wp, (float*)(W + p.sp), s));
   }
   // 4. Adaptive summaries (Sec. 3.4).
-  LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, prm->wp, (float*)(SV + p.s), (float*)(SV + p.S),
-                               W + p.St, (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
+  LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, (const float*)(W + p.sp), D / kDh,
+                               (float*)(SV + p.s), (float*)(SV + p.S), W + p.St,
+                               (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
   // 5-6. Exponential memory and its projection (Sec. 3.5).  The projection
   // is linear and so is the normalised decayed sum, so the summaries are
   // projected first (Q = S Wm, as split-K partial products over only
@@ -477,10 +479,16 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     LAUNCH(ST_MEM_BWD, mem_bwd(Mp, ms, (const float*)(SV + p.M), (float*)(W + p.dS), gr.dgamma,
                                p.B, p.nb, D, cfg->gamma, s));
   }
-  // Pooling backward: per-token a_t, ds_t and dwp.
+  // Pooling backward: per-token a_t and ds_t; dwp = sum_t ds_t H[t] on the
+  // side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
-                  (const float*)(SV + p.S), (const float*)(W + p.dS), prm->wp, (float*)(W + p.a),
-                  (float*)(W + p.ds), gr.dwp, p.B, p.T, D, p.L, s));
+                               (const float*)(SV + p.S), (const float*)(W + p.dS),
+                               (float*)(W + p.a), (float*)(W + p.ds), p.B, p.T, D, p.L, s));
+  if (gr.dwp) {
+    SIDE_BEGIN();
+    LAUNCH(ST_DWP, pool_dwp(dt, SV + p.h, (const float*)(W + p.ds), gr.dwp, (int64_t)BT, D, s));
+    SIDE_END();
+  }
   // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.
   {
     GemmDesc g{BT, D, D, W + p.du, D, false, {prm->Wg, nullptr, nullptr}, D, false, kSegNone, 0, 1};

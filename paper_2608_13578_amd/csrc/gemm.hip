@@ -185,13 +185,43 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(int M, int N, int K,
     __syncthreads();
   }
 
+  run_epilogue<4, 4>(epi, acc, m0 + wm * 64, n0 + wn * 64, M, N, lane);
+}
+
+// ------------------------------------------------------------------ epilogue driver
+// Hands every fragment of a wave's tile to the epilogue.  An epilogue with
+// kRowDot also folds each fragment into a per-row value (rowdot) that is
+// summed over the wave's columns and handed to row() once per row, by the
+// lane group holding the row's first four columns.
+template <class Epi, class = void>
+struct HasRowDot {
+  static constexpr bool value = false;
+};
+template <class Epi>
+struct HasRowDot<Epi, decltype((void)Epi::kRowDot)> {
+  static constexpr bool value = Epi::kRowDot;
+};
+
+template <int FM, int FN, class Epi>
+__device__ __forceinline__ void run_epilogue(const Epi& epi, const f32x4 (&acc)[FM][FN], int mb,
+                                             int nb, int M, int N, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + wm * 64 + i * 16 + lr;
+  for (int i = 0; i < FM; ++i) {
+    const int m = mb + i * 16 + lr;
+    float rs = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + wn * 64 + j * 16 + lg * 4;
-      if (m < M && n < N) epi(m, n, acc[i][j]);
+    for (int j = 0; j < FN; ++j) {
+      const int n = nb + j * 16 + lg * 4;
+      if (m < M && n < N) {
+        epi(m, n, acc[i][j]);
+        if constexpr (HasRowDot<Epi>::value) rs += epi.rowdot(n, acc[i][j]);
+      }
+    }
+    if constexpr (HasRowDot<Epi>::value) {
+      rs += __shfl_xor(rs, 16);
+      rs += __shfl_xor(rs, 32);
+      if (lg == 0 && m < M && nb < N) epi.row(m, nb, rs);
     }
   }
 }
@@ -207,6 +237,33 @@ struct EpiStore {
   __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
     if (add) v += load4f(add + (int64_t)m * ld_add + n);
     store4(C + (int64_t)m * ldc + n, v[0], v[1], v[2], v[3]);
+  }
+};
+
+// Output projection (Sec. 3.3) with the pooling scores of Sec. 3.4 folded
+// in: stores H and, for every row, the partial score over this wave's 64
+// columns, sum_n H[m, n] wp[n] (from the stored, rounded H), to
+// sp[m * (N / 64) + n0 / 64]; the pooling kernel adds the N / 64 parts.
+template <typename T>
+struct EpiScore {
+  T* C;
+  int64_t ldc;
+  const T* wp;
+  float* sp;
+  int nparts;
+  static constexpr bool kRowDot = true;
+  __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
+    store4(C + (int64_t)m * ldc + n, v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ float rowdot(int n, f32x4 v) const {
+    const f32x4 w = load4f(wp + n);
+    float d = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) d += to_f32(from_f32<T>(v[r])) * w[r];
+    return d;
+  }
+  __device__ __forceinline__ void row(int m, int n0, float v) const {
+    sp[(int64_t)m * nparts + n0 / 64] = v;
   }
 };
 
@@ -555,16 +612,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
     }
   }
 
-  const int lr = lane & 15, lg = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * WTM + i * 16 + lr;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * WTN + j * 16 + lg * 4;
-      if (m < M && n < N) epi(m, n, acc[i][j]);
-    }
-  }
+  run_epilogue<FM, FN>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N, lane);
 }
 
 // ------------------------------------------------------------------ launch
@@ -742,6 +790,18 @@ hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, fl
                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s) {
   if (!(g.a_mcontig && g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
   return gemm_splitk(dt, g, partial, C0, C1, C2, ldc, seg_len_n, accumulate, 512, s);
+}
+
+hipError_t gemm_score(DType dt, const GemmDesc& g, void* C, const void* wp, float* sp,
+                      hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.N % 64 != 0 || !(!g.a_mcontig && g.b_ncontig && g.seg == kSegNone))
+    return hipErrorInvalidValue;
+  if (dt == DType::BF16)
+    return launch_any<bf16, false, true, kSegNone>(
+        g, EpiScore<bf16>{(bf16*)C, g.N, (const bf16*)wp, sp, g.N / 64}, s);
+  return launch<float, false, true, kSegNone>(
+      g, EpiScore<float>{(float*)C, g.N, (const float*)wp, sp, g.N / 64}, s);
 }
 
 hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t s) {

@@ -65,6 +65,12 @@ hipError_t gemm_splitk_reduce(const float* partial, int splits, int M, int N, fl
 hipError_t gemm_wgrad(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
                       float* C2, int64_t ldc, int seg_len_n, bool accumulate, hipStream_t s);
 
+// Output projection with the pooling scores: C = acc ([M, N], row stride N)
+// and sp[m * (N / 64) + q] = sum over columns 64q .. 64q+63 of C[m, n] wp[n]
+// (N a multiple of 64; A K-contiguous, B N-contiguous).
+hipError_t gemm_score(DType dt, const GemmDesc& g, void* C, const void* wp, float* sp,
+                      hipStream_t s);
+
 // Gate + injection epilogue (forward): U = acc;
 //   G = sigmoid(U); Y = H + G * Mc[blk(t)] (+ X); G is stored for backward.
 // Mc[b, i] = P[b, i - 1] for i >= 1 and 0 for i = 0 (the one-block shift).
@@ -103,10 +109,11 @@ hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const floa
                          hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
-// Pooling: scores s [B*T], summaries S [B*nb, D] (float32, and St in the
-// compute type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, void* St,
-                    float* stats, int B, int T, int D, int L, hipStream_t s);
+// Pooling, from the np partial scores per token written by gemm_score:
+// scores s [B*T], summaries S [B*nb, D] (float32, and St in the compute
+// type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
+hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
+                    void* St, float* stats, int B, int T, int D, int L, hipStream_t s);
 // Decayed scan: M (float32) and its compute-type copy Mt from the summaries
 // S, and P from the projected summaries, given as qs split-K partial
 // products Q (each [B*nb, D], consecutive).
@@ -119,9 +126,13 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
 // Reverse decayed scan; dM is given as ms split-K partial products.
 hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float* dgamma, int B,
                    int nb, int D, float gamma, hipStream_t s);
+// Pooling backward: per-token softmax weights a_t and score gradients ds_t.
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
-                    const float* S, const float* dS, const void* wp, float* a_out,
-                    float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s);
+                    const float* S, const float* dS, float* a_out, float* ds_out, int B, int T,
+                    int D, int L, hipStream_t s);
+// dwp += sum over the ntok rows t of ds_t H[t] (atomic adds; dwp may be null).
+hipError_t pool_dwp(DType dt, const void* H, const float* ds, float* dwp, int64_t ntok, int D,
+                    hipStream_t s);
 hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // Zeroes two small float32 buffers in one launch (either may be null).
 hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);

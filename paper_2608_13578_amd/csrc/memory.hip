@@ -19,10 +19,10 @@
 namespace bcmt {
 namespace {
 
-// Pooling and gate kernels use one workgroup per (block, batch element):
-// up to 16 waves, each wave taking TB tokens at a time (their rows are loaded
-// together, then reduced together), so that enough loads are in flight per
-// CU; the block-level reductions finish in LDS without a second pass.
+// The pooling backward uses one workgroup per chunk of a block's tokens: up
+// to 16 waves, each wave taking TB whole rows at a time (their rows are
+// loaded together, then reduced together), so that enough loads are in
+// flight per CU.
 
 // Tokens a wave loads at once for rows of NVJ 16-byte vectors per lane.
 template <int NVJ> struct TokBatch { static constexpr int TB = NVJ >= 4 ? 2 : (NVJ == 2 ? 4 : 8); };
@@ -39,113 +39,121 @@ __device__ __forceinline__ float block_reduce_sum(float v, float* red) {
   return s;
 }
 
+// ------------------------------------------------------------------ column-chunk layout
+// Pooling (forward) and the gate backward walk a block's tokens over a chunk
+// of columns: workgroup = (block, batch element, chunk of 16 vectors of
+// 16 bytes), thread = (vector v, token group tg) with 16 of each; thread
+// (v, tg) visits tokens bs + tg, bs + tg + 16, ... and the 16 token groups
+// are merged in LDS.  No reduction crosses workgroups, and a launch has
+// N_b * B * ceil(D / chunk) workgroups.
+constexpr int kVec = 16, kTg = 16;
+
 // ------------------------------------------------------------------ pooling (forward)
-// s_t = H[t] . w_p; a = softmax of s over the block; S_i = sum_t a_t H[t].
-// Each wave keeps a running (max, sum, weighted row sum) over its tokens; the
-// waves are merged in LDS.  Writes s (for the backward), S_i and the block's
-// softmax statistics (max, normaliser).
-template <typename T, int NVJ>
-__global__ __launch_bounds__(1024) void pool_fwd_kernel(const T* __restrict__ H,
-                                                        const T* __restrict__ wp,
-                                                        float* __restrict__ s_out,
-                                                        float* __restrict__ S, T* __restrict__ St,
-                                                        float* __restrict__ stats, int Tn, int D,
-                                                        int L, int nb) {
+// s_t = H[t] . w_p arrives as np partial sums per token (written by the
+// output projection's epilogue); a = softmax of s over the block;
+// S_i = sum_t a_t H[t].  The block's tokens are taken 256 at a time: their
+// scores go to LDS (one token per thread) with the tile's max and
+// exponential sum, then every thread adds its tokens' weighted rows with the
+// loads of four tokens in flight; the running max is the same for the whole
+// workgroup, so only the token groups' sums remain to be added at the end.
+// Chunk 0 of each block also writes s (for the backward) and the block's
+// softmax statistics (max, normaliser); S_i is written in float32 and in
+// the compute type (the operand of the memory projection).
+__device__ __forceinline__ float block_max256(float v, float* red) {
+  v = wave_max(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  const float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  return r;
+}
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  const float r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
+                                                       const float* __restrict__ sp, int np,
+                                                       float* __restrict__ s_out,
+                                                       float* __restrict__ S, T* __restrict__ St,
+                                                       float* __restrict__ stats, int Tn, int D,
+                                                       int L, int nb) {
   constexpr int VE = Vec16<T>::N;
-  constexpr int TB = TokBatch<NVJ>::TB;
+  constexpr int U = 4;
   typedef typename Vec16<T>::type vec;
-  extern __shared__ float red[];  // [nw][D] partial sums, then [nw][2] stats
-  const int nw = blockDim.x >> 6;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ float racc[kTg][kVec * VE];
+  __shared__ float sc[256];
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  const int v = tid % kVec, tg = tid / kVec;
   const int i = blockIdx.x, b = blockIdx.y;
+  const int c0 = blockIdx.z * kVec * VE;
+  const int col = c0 + v * VE;
+  const bool act = col < D;
   const int bs = i * L;
   const int be = min(bs + L, Tn);
-  const int Dv = D / VE;
+  const bool first = blockIdx.z == 0;
+  const T* hb = H + (int64_t)b * Tn * D + col;
 
-  float w[NVJ][VE], acc[NVJ][VE];
+  float m = -INFINITY, l = 0.f, acc[VE];
 #pragma unroll
-  for (int j = 0; j < NVJ; ++j) {
-    const int v = lane + 64 * j;
-    vec wv = v < Dv ? load16(wp + v * VE) : vec{};
-#pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      w[j][e] = to_f32(wv[e]);
-      acc[j][e] = 0.f;
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  for (int t0 = bs; t0 < be; t0 += 256) {
+    const int n = min(256, be - t0);
+    float x = -INFINITY;
+    if (tid < n) {
+      const int64_t row = (int64_t)b * Tn + t0 + tid;
+      x = 0.f;
+      for (int q = 0; q < np; ++q) x += sp[row * np + q];
+      if (first) s_out[row] = x;
     }
-  }
-  float mw = -INFINITY, lw = 0.f;
-  for (int t0 = bs + wave * TB; t0 < be; t0 += nw * TB) {
-    vec x[TB][NVJ];
+    sc[tid] = x;
+    const float mn = fmaxf(m, block_max256(x, red));  // also publishes sc[]
+    const float f = __expf(m - mn);
+    l = l * f + block_sum256(tid < n ? __expf(x - mn) : 0.f, red);
 #pragma unroll
-    for (int k = 0; k < TB; ++k)
+    for (int e = 0; e < VE; ++e) acc[e] *= f;
+    m = mn;
+    if (act) {
+      for (int k0 = tg; k0 < n; k0 += U * kTg) {
+        vec h[U];
 #pragma unroll
-      for (int j = 0; j < NVJ; ++j) {
-        const int v = lane + 64 * j;
-        x[k][j] = (t0 + k < be && v < Dv) ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE)
-                                          : vec{};
+        for (int u = 0; u < U; ++u) {
+          const int k = k0 + u * kTg;
+          h[u] = k < n ? load16(hb + (int64_t)(t0 + k) * D) : vec{};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = k0 + u * kTg;
+          const float w = k < n ? __expf(sc[k] - mn) : 0.f;
+#pragma unroll
+          for (int e = 0; e < VE; ++e) acc[e] += w * to_f32(h[u][e]);
+        }
       }
-    float sc[TB];
-    float mx = mw;
-#pragma unroll
-    for (int k = 0; k < TB; ++k) {
-      float d = 0.f;
-#pragma unroll
-      for (int j = 0; j < NVJ; ++j)
-#pragma unroll
-        for (int e = 0; e < VE; ++e) d += w[j][e] * to_f32(x[k][j][e]);
-      sc[k] = wave_sum(d);
-      if (t0 + k < be) {
-        if (lane == 0) s_out[(int64_t)b * Tn + t0 + k] = sc[k];
-        mx = fmaxf(mx, sc[k]);
-      }
     }
-    const float f = __expf(mw - mx);
-    lw *= f;
-#pragma unroll
-    for (int j = 0; j < NVJ; ++j)
-#pragma unroll
-      for (int e = 0; e < VE; ++e) acc[j][e] *= f;
-#pragma unroll
-    for (int k = 0; k < TB; ++k) {
-      const float pk = t0 + k < be ? __expf(sc[k] - mx) : 0.f;
-      lw += pk;
-#pragma unroll
-      for (int j = 0; j < NVJ; ++j)
-#pragma unroll
-        for (int e = 0; e < VE; ++e) acc[j][e] += pk * to_f32(x[k][j][e]);
-    }
-    mw = mx;
+    __syncthreads();  // sc[] is rewritten by the next tile
   }
-  float* stat = red + nw * D;
 #pragma unroll
-  for (int j = 0; j < NVJ; ++j) {
-    const int v = lane + 64 * j;
-    if (v < Dv) {
-#pragma unroll
-      for (int e = 0; e < VE; ++e) red[wave * D + v * VE + e] = acc[j][e];
-    }
-  }
-  if (lane == 0) {
-    stat[wave * 2] = mw;
-    stat[wave * 2 + 1] = lw;
-  }
+  for (int e = 0; e < VE; ++e) racc[tg][v * VE + e] = acc[e];
   __syncthreads();
-  float mm = -INFINITY;
-  for (int k = 0; k < nw; ++k) mm = fmaxf(mm, stat[k * 2]);
-  float lsum = 0.f;
-  for (int k = 0; k < nw; ++k)
-    if (stat[k * 2] != -INFINITY) lsum += __expf(stat[k * 2] - mm) * stat[k * 2 + 1];
-  const float inv = 1.0f / lsum;
-  for (int col = tid; col < D; col += blockDim.x) {
+  const float inv = 1.0f / l;
+  const int64_t brow = (int64_t)(b * nb + i);
+  if (tid < kVec * VE && c0 + tid < D) {
     float sum = 0.f;
-    for (int k = 0; k < nw; ++k)
-      if (stat[k * 2] != -INFINITY) sum += __expf(stat[k * 2] - mm) * red[k * D + col];
-    S[(int64_t)(b * nb + i) * D + col] = sum * inv;
-    St[(int64_t)(b * nb + i) * D + col] = from_f32<T>(sum * inv);
+    for (int k = 0; k < kTg; ++k) sum += racc[k][tid];
+    S[brow * D + c0 + tid] = sum * inv;
+    St[brow * D + c0 + tid] = from_f32<T>(sum * inv);
   }
-  if (tid == 0) {
-    stats[(int64_t)(b * nb + i) * 2] = mm;
-    stats[(int64_t)(b * nb + i) * 2 + 1] = lsum;
+  if (first && tid == 0) {
+    stats[brow * 2] = m;
+    stats[brow * 2 + 1] = l;
   }
 }
 
@@ -215,38 +223,33 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__
 
 // ------------------------------------------------------------------ gate backward
 // dU = dY * Mc * G (1 - G) per element, and the block sum of dY * G, which is
-// the gradient of the shifted memory.  Workgroup = (block, batch): thread
-// (token group tg, column vector v) walks every TG-th token of the block four
-// at a time; the TG partial sums meet in LDS.  The block sums are written
-// already shifted back by one block (row i-1 holds block i's sum; the last
-// row of each batch element is zero), in the compute type, as the left
-// operand of the W_m backward products.
-// The first workgroup also clears dwp and dgamma (when given), which later
-// kernels of the pass accumulate into with atomics.
+// the gradient of the shifted memory, in the column-chunk layout.  The block
+// sums are written already shifted back by one block (row i-1 holds block
+// i's sum; the last row of each batch element is zero), in the compute type,
+// as the left operand of the W_m backward products.  The first workgroup
+// also clears dwp and dgamma (when given), which later kernels of the pass
+// accumulate into with atomics.
 template <typename T>
-__global__ __launch_bounds__(1024) void gate_bwd_kernel(const T* __restrict__ dY,
-                                                        const T* __restrict__ G,
-                                                        const float* __restrict__ P,
-                                                        T* __restrict__ dU, T* __restrict__ Pbar,
-                                                        float* __restrict__ zero_a, int na,
-                                                        float* __restrict__ zero_b, int Tn, int D,
-                                                        int L, int nb) {
-  if (blockIdx.x == 0 && blockIdx.y == 0) {
+__global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
+                                                       const T* __restrict__ G,
+                                                       const float* __restrict__ P,
+                                                       T* __restrict__ dU, T* __restrict__ Pbar,
+                                                       float* __restrict__ zero_a, int na,
+                                                       float* __restrict__ zero_b, int Tn, int D,
+                                                       int L, int nb) {
+  constexpr int VE = Vec16<T>::N;
+  typedef typename Vec16<T>::type vec;
+  __shared__ float racc[kTg][kVec * VE];
+  if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
     for (int k = threadIdx.x; k < na; k += blockDim.x)
       if (zero_a) zero_a[k] = 0.f;
     if (threadIdx.x == 0 && zero_b) *zero_b = 0.f;
   }
-  constexpr int VE = Vec16<T>::N;
-  constexpr int U = 4;
-  typedef typename Vec16<T>::type vec;
-  extern __shared__ float red[];  // [TG][D]
-  const int Dv = D / VE;
-  const int TG = blockDim.x / Dv;
-  const int tid = threadIdx.x;
-  const int v = tid % Dv, tg = tid / Dv;
-  const bool act = tg < TG;
+  const int v = threadIdx.x % kVec, tg = threadIdx.x / kVec;
   const int i = blockIdx.x, b = blockIdx.y;
-  const int col = v * VE;
+  const int c0 = blockIdx.z * kVec * VE;
+  const int col = c0 + v * VE;
+  const bool act = col < D;
   const int bs = i * L;
   const int be = min(bs + L, Tn);
   float c[VE], acc[VE];
@@ -256,23 +259,28 @@ __global__ __launch_bounds__(1024) void gate_bwd_kernel(const T* __restrict__ dY
     acc[e] = 0.f;
   }
   if (act && i > 0) {
-    const float* pp = P + (int64_t)(b * nb + i - 1) * D + col;
+    const f32x4* pp = reinterpret_cast<const f32x4*>(P + (int64_t)(b * nb + i - 1) * D + col);
 #pragma unroll
-    for (int e = 0; e < VE; ++e) c[e] = pp[e];
+    for (int q = 0; q < VE / 4; ++q) {
+      const f32x4 w = pp[q];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) c[q * 4 + r] = w[r];
+    }
   }
   if (act) {
-    for (int t0 = bs + tg; t0 < be; t0 += U * TG) {
+    constexpr int U = 2;
+    for (int t0 = bs + tg; t0 < be; t0 += U * kTg) {
       vec dy[U], g[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int t = t0 + u * TG;
+        const int t = t0 + u * kTg;
         const int64_t off = ((int64_t)b * Tn + t) * D + col;
         dy[u] = t < be ? load16(dY + off) : vec{};
         g[u] = t < be ? load16(G + off) : vec{};
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int t = t0 + u * TG;
+        const int t = t0 + u * kTg;
         vec du;
 #pragma unroll
         for (int e = 0; e < VE; ++e) {
@@ -283,20 +291,16 @@ __global__ __launch_bounds__(1024) void gate_bwd_kernel(const T* __restrict__ dY
         if (t < be) store16(dU + ((int64_t)b * Tn + t) * D + col, du);
       }
     }
-#pragma unroll
-    for (int e = 0; e < VE; ++e) red[tg * D + col + e] = acc[e];
   }
-  __syncthreads();
-  if (act && tg == 0) {
-    vec o;
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      float sum = 0.f;
-      for (int k = 0; k < TG; ++k) sum += red[k * D + col + e];
-      o[e] = from_f32<T>(sum);
-    }
-    if (i > 0) store16(Pbar + (int64_t)(b * nb + i - 1) * D + col, o);
-    else store16(Pbar + (int64_t)(b * nb + nb - 1) * D + col, vec{});
+  for (int e = 0; e < VE; ++e) racc[tg][v * VE + e] = acc[e];
+  __syncthreads();
+  if (threadIdx.x < kVec * VE && c0 + (int)threadIdx.x < D) {
+    const int cc = threadIdx.x;
+    float sum = 0.f;
+    for (int k = 0; k < kTg; ++k) sum += racc[k][cc];
+    const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * D + c0 + cc;
+    Pbar[dst] = from_f32<T>(i > 0 ? sum : 0.f);
   }
 }
 
@@ -378,25 +382,26 @@ __global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ 
 // ------------------------------------------------------------------ pooling backward
 // With a_t the block softmax weights and dS_i the summary gradient:
 //   ds_t = a_t (dS_i . H[t] - dS_i . S_i),  dw_p = sum_t ds_t H[t].
-// The per-token a_t and ds_t feed the dH epilogue of the W_g backward product.
+// pool_bwd_kernel writes the per-token a_t and ds_t (they feed the dH
+// epilogue of the W_g backward product); dwp_kernel then forms dw_p off the
+// critical path.  Workgroup = (chunk of tc tokens of block i, batch element).
 template <typename T, int NVJ>
 __global__ __launch_bounds__(1024) void pool_bwd_kernel(
     const T* __restrict__ H, const float* __restrict__ s_in, const float* __restrict__ stats,
     const float* __restrict__ S, const float* __restrict__ dS, float* __restrict__ a_out,
-    float* __restrict__ ds_out, float* __restrict__ dwp, int Tn, int D, int L, int nb) {
+    float* __restrict__ ds_out, int Tn, int D, int L, int nb, int tc, int nch) {
   constexpr int VE = Vec16<T>::N;
   constexpr int TB = TokBatch<NVJ>::TB;
   typedef typename Vec16<T>::type vec;
-  extern __shared__ float red[];  // [nw][D]
   const int nw = blockDim.x >> 6;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i = blockIdx.x, b = blockIdx.y;
-  const int bs = i * L;
-  const int be = min(bs + L, Tn);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x / nch, b = blockIdx.y;
+  const int bs = i * L + (blockIdx.x % nch) * tc;
+  const int be = min(min(i * L + L, Tn), bs + tc);
   const int Dv = D / VE;
   const int64_t brow = (int64_t)(b * nb + i) * D;
 
-  float g[NVJ][VE], acc[NVJ][VE];
+  float g[NVJ][VE];
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < NVJ; ++j) {
@@ -406,7 +411,6 @@ __global__ __launch_bounds__(1024) void pool_bwd_kernel(
       const bool ok = v < Dv;
       g[j][e] = ok ? dS[brow + v * VE + e] : 0.f;
       ss += ok ? g[j][e] * S[brow + v * VE + e] : 0.f;
-      acc[j][e] = 0.f;
     }
   }
   ss = wave_sum(ss);
@@ -431,37 +435,59 @@ __global__ __launch_bounds__(1024) void pool_bwd_kernel(
         for (int e = 0; e < VE; ++e) d += g[j][e] * to_f32(x[k][j][e]);
       d = wave_sum(d);
       const int t = t0 + k;
-      float dst = 0.f;
-      if (t < be) {
+      if (t < be && lane == 0) {
         const int64_t ti = (int64_t)b * Tn + t;
         const float a = __expf(s_in[ti] - mi) / li;
-        dst = a * (d - ss);
-        if (lane == 0) {
-          a_out[ti] = a;
-          ds_out[ti] = dst;
-        }
+        a_out[ti] = a;
+        ds_out[ti] = a * (d - ss);
+      }
+    }
+  }
+}
+
+// dw_p += sum_t ds_t H[t] over a range of tokens, in the column-chunk layout
+// (workgroup = (column chunk, token range)); one atomic add per column.
+template <typename T>
+__global__ __launch_bounds__(256) void dwp_kernel(const T* __restrict__ H,
+                                                  const float* __restrict__ ds,
+                                                  float* __restrict__ dwp, int64_t ntok, int D,
+                                                  int64_t per) {
+  constexpr int VE = Vec16<T>::N;
+  constexpr int U = 4;
+  typedef typename Vec16<T>::type vec;
+  __shared__ float racc[kTg][kVec * VE];
+  const int tid = threadIdx.x;
+  const int v = tid % kVec, tg = tid / kVec;
+  const int c0 = blockIdx.x * kVec * VE;
+  const int col = c0 + v * VE;
+  const int64_t t_beg = (int64_t)blockIdx.y * per;
+  const int64_t t_end = t_beg + per < ntok ? t_beg + per : ntok;
+  float acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  if (col < D) {
+    for (int64_t t0 = t_beg + tg; t0 < t_end; t0 += U * kTg) {
+      vec h[U];
+      float w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t t = t0 + u * kTg;
+        h[u] = t < t_end ? load16(H + t * D + col) : vec{};
+        w[u] = t < t_end ? ds[t] : 0.f;
       }
 #pragma unroll
-      for (int j = 0; j < NVJ; ++j)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int e = 0; e < VE; ++e) acc[j][e] += dst * to_f32(x[k][j][e]);
+        for (int e = 0; e < VE; ++e) acc[e] += w[u] * to_f32(h[u][e]);
     }
   }
 #pragma unroll
-  for (int j = 0; j < NVJ; ++j) {
-    const int v = lane + 64 * j;
-    if (v < Dv) {
-#pragma unroll
-      for (int e = 0; e < VE; ++e) red[wave * D + v * VE + e] = acc[j][e];
-    }
-  }
+  for (int e = 0; e < VE; ++e) racc[tg][v * VE + e] = acc[e];
   __syncthreads();
-  if (dwp) {
-    for (int col = tid; col < D; col += blockDim.x) {
-      float sum = 0.f;
-      for (int k = 0; k < nw; ++k) sum += red[k * D + col];
-      if (sum != 0.f) unsafeAtomicAdd(dwp + col, sum);
-    }
+  if (tid < kVec * VE && c0 + tid < D) {
+    float sum = 0.f;
+    for (int k = 0; k < kTg; ++k) sum += racc[k][tid];
+    unsafeAtomicAdd(dwp + c0 + tid, sum);
   }
 }
 
@@ -487,62 +513,65 @@ int nvj_for(int Dv) {
   return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : 8;
 }
 
-// Waves per pooling workgroup: enough to give every wave one token batch,
-// at most 16, and few enough that the per-wave row sums fit in 64 KB of LDS.
+// Waves per pooling-backward workgroup: enough to give every wave one token
+// batch of the chunk, at most 16, and few enough that the per-wave row sums
+// fit in 64 KB of LDS.
 template <int NVJ>
-int pool_waves(int L, int T, int D) {
-  const int lb = L < T ? L : T;
+int pool_waves(int tc, int D) {
   const int tb = TokBatch<NVJ>::TB;
-  int w = (lb + tb - 1) / tb;
+  int w = (tc + tb - 1) / tb;
   const int wmax = (65536 - 256) / (4 * D + 8);
   if (w > wmax) w = wmax;
   return w < 1 ? 1 : (w > 16 ? 16 : w);
 }
 
-template <typename E, int NV>
-hipError_t pool_fwd_nv(const void* H, const void* wp, float* s_out, float* S, void* St,
-                       float* stats, int B, int T, int D, int L, hipStream_t s) {
-  const int nb = (T + L - 1) / L;
-  const int nw = pool_waves<NV>(L, T, D);
-  const size_t lds = ((size_t)nw * D + 2 * nw) * sizeof(float);
-  hipLaunchKernelGGL((pool_fwd_kernel<E, NV>), dim3(nb, B), dim3(nw * 64), lds, s, (const E*)H,
-                     (const E*)wp, s_out, S, (E*)St, stats, T, D, L, nb);
-  return hipGetLastError();
-}
-
 template <typename E>
-hipError_t pool_fwd_t(const void* H, const void* wp, float* s_out, float* S, void* St,
+hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, float* S, void* St,
                       float* stats, int B, int T, int D, int L, hipStream_t s) {
-  switch (nvj_for(D / Vec16<E>::N)) {
-    case 1: return pool_fwd_nv<E, 1>(H, wp, s_out, S, St, stats, B, T, D, L, s);
-    case 2: return pool_fwd_nv<E, 2>(H, wp, s_out, S, St, stats, B, T, D, L, s);
-    case 4: return pool_fwd_nv<E, 4>(H, wp, s_out, S, St, stats, B, T, D, L, s);
-    default: return pool_fwd_nv<E, 8>(H, wp, s_out, S, St, stats, B, T, D, L, s);
-  }
+  const int nb = (T + L - 1) / L;
+  const int cw = kVec * Vec16<E>::N;
+  hipLaunchKernelGGL(pool_fwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
+                     (const E*)H, sp, np, s_out, S, (E*)St, stats, T, D, L, nb);
+  return hipGetLastError();
 }
 
 template <typename E, int NV>
 hipError_t pool_bwd_nv(const void* H, const float* s_in, const float* stats, const float* S,
-                       const float* dS, float* a_out, float* ds_out, float* dwp, int B, int T,
-                       int D, int L, hipStream_t s) {
+                       const float* dS, float* a_out, float* ds_out, int B, int T, int D, int L,
+                       hipStream_t s) {
   const int nb = (T + L - 1) / L;
-  const int nw = pool_waves<NV>(L, T, D);
-  const size_t lds = (size_t)nw * D * sizeof(float);
-  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb, B), dim3(nw * 64), lds, s, (const E*)H,
-                     s_in, stats, S, dS, a_out, ds_out, dwp, T, D, L, nb);
+  const int lb = L < T ? L : T;
+  const int tc = lb < 32 ? lb : 32;  // tokens per workgroup
+  const int nch = (lb + tc - 1) / tc;
+  const int nw = pool_waves<NV>(tc, D);
+  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb * nch, B), dim3(nw * 64), 0, s,
+                     (const E*)H, s_in, stats, S, dS, a_out, ds_out, T, D, L, nb, tc, nch);
   return hipGetLastError();
 }
 
 template <typename E>
 hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, const float* S,
-                      const float* dS, float* a_out, float* ds_out, float* dwp, int B, int T,
-                      int D, int L, hipStream_t s) {
+                      const float* dS, float* a_out, float* ds_out, int B, int T, int D, int L,
+                      hipStream_t s) {
   switch (nvj_for(D / Vec16<E>::N)) {
-    case 1: return pool_bwd_nv<E, 1>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
-    case 2: return pool_bwd_nv<E, 2>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
-    case 4: return pool_bwd_nv<E, 4>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
-    default: return pool_bwd_nv<E, 8>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+    case 1: return pool_bwd_nv<E, 1>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+    case 2: return pool_bwd_nv<E, 2>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+    case 4: return pool_bwd_nv<E, 4>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+    default: return pool_bwd_nv<E, 8>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
   }
+}
+
+template <typename E>
+hipError_t dwp_t(const void* H, const float* ds, float* dwp, int64_t ntok, int D, hipStream_t s) {
+  const int cw = kVec * Vec16<E>::N;
+  // about 128 tokens per workgroup, at most 256 token ranges
+  int64_t ranges = (ntok + 127) / 128;
+  if (ranges > 256) ranges = 256;
+  if (ranges < 1) ranges = 1;
+  const int64_t per = (ntok + ranges - 1) / ranges;
+  hipLaunchKernelGGL(dwp_kernel<E>, dim3((D + cw - 1) / cw, (unsigned)ranges), dim3(kVec * kTg), 0,
+                     s, (const E*)H, ds, dwp, ntok, D, per);
+  return hipGetLastError();
 }
 
 template <typename E>
@@ -550,23 +579,19 @@ hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, v
                       float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
                       hipStream_t s) {
   const int nb = (T + L - 1) / L;
-  const int Dv = D / Vec16<E>::N;
-  int tg = 1024 / Dv;
-  const int lb = L < T ? L : T;
-  if (tg > lb) tg = lb;
-  if (tg < 1) tg = 1;
-  const size_t lds = (size_t)tg * D * sizeof(float);
-  hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B), dim3(tg * Dv), lds, s, (const E*)dY,
-                     (const E*)G, P, (E*)dU, (E*)Pbar, zero_a, na, zero_b, T, D, L, nb);
+  const int cw = kVec * Vec16<E>::N;
+  hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
+                     (const E*)dY, (const E*)G, P, (E*)dU, (E*)Pbar, zero_a, na, zero_b, T, D, L,
+                     nb);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t pool_fwd(DType dt, const void* H, const void* wp, float* s_out, float* S, void* St,
-                    float* stats, int B, int T, int D, int L, hipStream_t s) {
-  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, wp, s_out, S, St, stats, B, T, D, L, s);
-  return pool_fwd_t<float>(H, wp, s_out, S, St, stats, B, T, D, L, s);
+hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
+                    void* St, float* stats, int B, int T, int D, int L, hipStream_t s) {
+  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
+  return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
 }
 
 hipError_t scan_fwd(DType dt, const float* S, const float* Q, int qs, float* M, void* Mt, float* P,
@@ -601,12 +626,18 @@ hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float*
 }
 
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
-                    const float* S, const float* dS, const void* wp, float* a_out,
-                    float* ds_out, float* dwp, int B, int T, int D, int L, hipStream_t s) {
-  (void)wp;
+                    const float* S, const float* dS, float* a_out, float* ds_out, int B, int T,
+                    int D, int L, hipStream_t s) {
   if (dt == DType::BF16)
-    return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
-  return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, dwp, B, T, D, L, s);
+    return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+  return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+}
+
+hipError_t pool_dwp(DType dt, const void* H, const float* ds, float* dwp, int64_t ntok, int D,
+                    hipStream_t s) {
+  if (!dwp || ntok <= 0) return hipSuccess;
+  if (dt == DType::BF16) return dwp_t<bf16>(H, ds, dwp, ntok, D, s);
+  return dwp_t<float>(H, ds, dwp, ntok, D, s);
 }
 
 hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {
