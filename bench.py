@@ -53,6 +53,9 @@ def stage_work(name, B, T, D, H, L, es):
         "fwd.attention": 4 * 64 * H * pairs,
         "bwd.attention_dq": 6 * 64 * H * pairs,
         "bwd.attention_dkdv": 8 * 64 * H * pairs,
+        # fused backward: dV, dP, dQ and dK over the causal pairs (the
+        # recomputed scores are not credited)
+        "bwd.attention_block": 8 * 64 * H * pairs,
     }
     if name in gemm:
         return "mfma", gemm[name], "flop"

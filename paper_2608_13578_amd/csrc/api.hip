@@ -138,14 +138,14 @@ enum Stage {
   ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_WM, ST_SCAN_FWD, ST_GATE,
   ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_WGRAD,
   ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_DWP, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
-  ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
+  ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.wm_gemm", "fwd.scan",
     "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm",
     "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.pool_dwp", "bwd.wg_dgrad_gemm",
-    "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_dq",
+    "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
 
 struct Tracer {
@@ -510,13 +510,20 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
   }
-  // Block-local attention backward.
-  LAUNCH(ST_ATTN_BWD_DQ,
-         attn_bwd_dq(dt, SV + p.qkv, SV + p.o, W + p.dout, (const float*)(SV + p.lse),
-                     (float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
-  LAUNCH(ST_ATTN_BWD_DKDV,
-         attn_bwd_dkdv(dt, SV + p.qkv, W + p.dout, (const float*)(SV + p.lse),
-                       (const float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+  // Block-local attention backward: one fused kernel when a block fits one
+  // workgroup, else dQ (with delta) and then dK / dV.
+  if (attn_bwd_fused(dt, p.T, p.L)) {
+    LAUNCH(ST_ATTN_BWD_BLOCK,
+           attn_bwd_block(dt, SV + p.qkv, SV + p.o, W + p.dout, (const float*)(SV + p.lse),
+                          W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+  } else {
+    LAUNCH(ST_ATTN_BWD_DQ,
+           attn_bwd_dq(dt, SV + p.qkv, SV + p.o, W + p.dout, (const float*)(SV + p.lse),
+                       (float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+    LAUNCH(ST_ATTN_BWD_DKDV,
+           attn_bwd_dkdv(dt, SV + p.qkv, W + p.dout, (const float*)(SV + p.lse),
+                         (const float*)(W + p.delta), W + p.dqkv, p.B, p.T, D, p.H, p.L, s));
+  }
   // Q/K/V projections backward: dW{q,k,v} on the side stream, dX here.
   if (gr.dWq || gr.dWk || gr.dWv) {
     SIDE_BEGIN();

@@ -886,6 +886,248 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
   }
 }
 
+// Fused backward of one block for blocks of at most NW * 32 tokens:
+// workgroup = (block, batch * head).  Q, K, V and dO of the whole block are
+// loaded into LDS once (direct loads); each wave first forms delta_t =
+// dO_t . O_t for its 32 queries, then owns 32 keys for dK and dV (scores
+// held transposed, as in attn_bwd_dkdv_bf16_kernel) and finally its 32
+// queries for dQ (as in attn_bwd_dq_bf16_kernel), recomputing the
+// probabilities from lse instead of keeping them.
+template <int NW>
+__global__ __launch_bounds__(NW * 64, 2) void attn_bwd_block_bf16_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ o, const bf16* __restrict__ dout,
+    const float* __restrict__ lse, bf16* __restrict__ dqkv, int Tn, int D, int H, int L,
+    float sl2, float scale) {
+  constexpr int NT = (NW * 32 + 63) / 64;  // 64-row tiles per matrix
+  __shared__ __attribute__((aligned(1024))) bf16 lds[4][NT][64 * 64];  // Q, K, V, dO
+  __shared__ float ls_s[NT * 64], dl_s[NT * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z / H, h = blockIdx.z % H;
+  const int bs = blockIdx.y * L;
+  const int be = min(bs + L, Tn);
+  const int ntile = (be - bs + 63) / 64;
+  const int64_t rs = 3LL * D;
+  const bf16* base = qkv + (int64_t)b * Tn * rs + h * kDh;
+  const bf16* ob = o + (int64_t)b * Tn * D + h * kDh;
+  const bf16* db = dout + (int64_t)b * Tn * D + h * kDh;
+  const int64_t lrow = ((int64_t)b * H + h) * Tn;
+  const int w0 = wave * 32;  // this wave's 32 queries (dQ) and keys (dK, dV), block-relative
+
+  for (int it = 0; it < ntile; ++it) {
+    const int r0 = bs + it * 64;
+    tile_issue<NW>(base, rs, r0, be - 1, lds[0][it], wave, lane);
+    tile_issue<NW>(base + D, rs, r0, be - 1, lds[1][it], wave, lane);
+    tile_issue<NW>(base + 2 * D, rs, r0, be - 1, lds[2][it], wave, lane);
+    tile_issue<NW>(db, D, r0, be - 1, lds[3][it], wave, lane);
+  }
+  // delta and lse of this wave's queries, while the tiles land.
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int tl = w0 + nq * 16 + lr;
+    const int t = bs + tl;
+    const bool ok = t < be;
+    float part = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      const bf16x8 dfv = ok ? *reinterpret_cast<const bf16x8*>(db + (int64_t)t * D + ds * 32 + lg * 8) : bf16x8{};
+      const bf16x8 ofv = ok ? *reinterpret_cast<const bf16x8*>(ob + (int64_t)t * D + ds * 32 + lg * 8) : bf16x8{};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part += (float)dfv[e] * (float)ofv[e];
+    }
+    part += __shfl_xor(part, 16, 64);
+    part += __shfl_xor(part, 32, 64);
+    if (lg == 0 && tl < NT * 64) {
+      dl_s[tl] = part;
+      ls_s[tl] = ok ? lse[lrow + t] : 0.f;
+    }
+  }
+  vm_wait<0>();
+  __syncthreads();
+
+  // ---- dK, dV for keys bs + w0 .. +31
+  if (bs + w0 < be) {
+    const int kt0 = w0 / 64, kr0 = w0 % 64;
+    bf16x8 kf[2][2], vf[2][2];
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        kf[ku][ds] = trow8(lds[1][kt0], kr0 + ku * 16 + lr, ds * 32 + lg * 8);
+        vf[ku][ds] = trow8(lds[2][kt0], kr0 + ku * 16 + lr, ds * 32 + lg * 8);
+      }
+    f32x4 dk[2][4], dv[2][4];
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        dk[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dv[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    // Both 16-key groups share every fragment read of the query tile; key
+    // rows past the block end are masked to zero probability.
+    for (int it = kt0; it < ntile; ++it) {
+      const int tt = bs + it * 64;
+      const bf16* Qt = lds[0][it];
+      const bf16* Dt = lds[3][it];
+      f32x4 p[2][4], z[2][4];
+#pragma unroll
+      for (int ts = 0; ts < 4; ++ts) {
+        bf16x8 qr[2], dr[2];
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          qr[ds] = trow8(Qt, ts * 16 + lr, ds * 32 + lg * 8);
+          dr[ds] = trow8(Dt, ts * 16 + lr, ds * 32 + lg * 8);
+        }
+#pragma unroll
+        for (int ku = 0; ku < 2; ++ku) {
+          const int u = bs + w0 + ku * 16 + lr;
+          f32x4 sc = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ds = 0; ds < 2; ++ds) {
+            sc = mma16(qr[ds], kf[ku][ds], sc);
+            dp = mma16(dr[ds], vf[ku][ds], dp);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ti = ts * 16 + lg * 4 + r;
+            const int t = tt + ti;
+            const bool ok = t >= u && t < be && u < be;
+            const float pv = ok ? exp2f(sc[r] * sl2 - ls_s[it * 64 + ti]) : 0.f;
+            p[ku][ts][r] = pv;
+            z[ku][ts][r] = pv * (dp[r] - dl_s[it * 64 + ti]);
+          }
+        }
+      }
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        bf16x8 dtf[4], qtf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          dtf[j] = tcol8p(Dt, tq * 32, j, lane);
+          qtf[j] = tcol8p(Qt, tq * 32, j, lane);
+        }
+        lds_tr_wait();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          lds_tr_bind(dtf[j]);
+          lds_tr_bind(qtf[j]);
+        }
+#pragma unroll
+        for (int ku = 0; ku < 2; ++ku) {
+          const bf16x8 pf = frag_from<bf16>(p[ku][2 * tq], p[ku][2 * tq + 1]);
+          const bf16x8 zf = frag_from<bf16>(z[ku][2 * tq], z[ku][2 * tq + 1]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            dv[ku][j] = mma16(dtf[j], pf, dv[ku][j]);
+            dk[ku][j] = mma16(qtf[j], zf, dk[ku][j]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku) {
+      const int u = bs + w0 + ku * 16 + lr;
+      if (u < be) {
+        bf16* pp = dqkv + ((int64_t)b * Tn + u) * rs + h * kDh + lg * 4;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          store4(pp + D + j * 16, dk[ku][j][0] * scale, dk[ku][j][1] * scale,
+                 dk[ku][j][2] * scale, dk[ku][j][3] * scale);
+          store4(pp + 2 * D + j * 16, dv[ku][j][0], dv[ku][j][1], dv[ku][j][2], dv[ku][j][3]);
+        }
+      }
+    }
+  }
+
+  // ---- dQ for queries bs + w0 .. +31
+  if (bs + w0 < be) {
+    const int qt0 = w0 / 64, qr0 = w0 % 64;
+    bf16x8 qf[2][2], df[2][2];
+    float dl[2], ls[2];
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        qf[nq][ds] = trow8(lds[0][qt0], qr0 + nq * 16 + lr, ds * 32 + lg * 8);
+        df[nq][ds] = trow8(lds[3][qt0], qr0 + nq * 16 + lr, ds * 32 + lg * 8);
+      }
+      dl[nq] = dl_s[w0 + nq * 16 + lr];
+      ls[nq] = ls_s[w0 + nq * 16 + lr];
+    }
+    f32x4 dq[2][4];
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dq[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int tw0 = bs + w0;
+    for (int it = 0; it <= qt0; ++it) {
+      const int kt = bs + it * 64;
+      const bf16* Kt = lds[1][it];
+      const bf16* Vt = lds[2][it];
+      bf16x8 kf[4][2], vf[4][2], ktf[4][2];
+#pragma unroll
+      for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
+          vf[ku][ds] = trow8(Vt, ku * 16 + lr, ds * 32 + lg * 8);
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int us = 0; us < 2; ++us) ktf[j][us] = tcol8p(Kt, us * 32, j, lane);
+      lds_tr_wait();
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int us = 0; us < 2; ++us) lds_tr_bind(ktf[j][us]);
+#pragma unroll
+      for (int nq = 0; nq < 2; ++nq) {
+        const int tq = tw0 + nq * 16;
+        if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+        f32x4 sc[4], dp[4];
+#pragma unroll
+        for (int ku = 0; ku < 4; ++ku) {
+          sc[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+          dp[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ds = 0; ds < 2; ++ds) {
+            sc[ku] = mma16(kf[ku][ds], qf[nq][ds], sc[ku]);
+            dp[ku] = mma16(vf[ku][ds], df[nq][ds], dp[ku]);
+          }
+        }
+        const int t_eff = min(tq + lr, be - 1);
+#pragma unroll
+        for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int u = kt + ku * 16 + lg * 4 + r;
+            const float pv = u <= t_eff ? exp2f(sc[ku][r] * sl2 - ls[nq]) : 0.f;
+            sc[ku][r] = pv * (dp[ku][r] - dl[nq]);
+          }
+#pragma unroll
+        for (int us = 0; us < 2; ++us) {
+          const bf16x8 zf = frag_from<bf16>(sc[2 * us], sc[2 * us + 1]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dq[nq][j] = mma16(ktf[j][us], zf, dq[nq][j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int t = tw0 + nq * 16 + lr;
+      if (t < be) {
+        bf16* pp = dqkv + ((int64_t)b * Tn + t) * rs + h * kDh + lg * 4;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          store4(pp + j * 16, dq[nq][j][0] * scale, dq[nq][j][1] * scale, dq[nq][j][2] * scale,
+                 dq[nq][j][3] * scale);
+      }
+    }
+  }
+}
+
 // Waves per attention workgroup (1, 2 or 4), each owning 32 queries or keys.
 int attn_waves(int L, int T) {
   const int lb = L < T ? L : T;
@@ -968,6 +1210,25 @@ hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* d
     return hipGetLastError();
   }
   return attn_bwd_dq_t<float>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
+}
+
+bool attn_bwd_fused(DType dt, int T, int L) {
+  const int lb = L < T ? L : T;
+  return dt == DType::BF16 && lb <= 128;
+}
+
+hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void* dout,
+                          const float* lse, void* dqkv, int B, int T, int D, int H, int L,
+                          hipStream_t s) {
+  if (!attn_bwd_fused(dt, T, L)) return hipErrorInvalidValue;
+  const int nw = attn_waves(L, T);
+  dim3 grid(1, (T + L - 1) / L, B * H);
+  const float scale = 1.0f / sqrtf((float)kDh);
+  const float sl2 = 1.4426950408889634f * scale;
+#define BLK(NW) hipLaunchKernelGGL(attn_bwd_block_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (const bf16*)out, (const bf16*)dout, lse, (bf16*)dqkv, T, D, H, L, sl2, scale)
+  if (nw == 1) BLK(1); else if (nw == 2) BLK(2); else BLK(4);
+#undef BLK
+  return hipGetLastError();
 }
 
 hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,

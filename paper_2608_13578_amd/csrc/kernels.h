@@ -107,6 +107,13 @@ hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* d
 hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
                          const float* delta, void* dqkv, int B, int T, int D, int H, int L,
                          hipStream_t s);
+// Whether attn_bwd_block serves this layer (bf16, blocks of at most 128
+// tokens), and the fused backward of each block in one workgroup (dQ, dK,
+// dV; delta is formed internally and not written).
+bool attn_bwd_fused(DType dt, int T, int L);
+hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void* dout,
+                          const float* lse, void* dqkv, int B, int T, int D, int H, int L,
+                          hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
 // Pooling, from the np partial scores per token written by gemm_score:
