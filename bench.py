@@ -133,13 +133,13 @@ def cpu_baseline(seconds_target=12.0):
 
     t1 = run(1)
     bs = max(1, min(w["B"], int(seconds_target / max(t1, 1e-3))))
-    # Whole batches repeated until about seconds_target of CPU work.
-    reps = 1
-    if bs == w["B"]:
-        reps = max(1, int(seconds_target / max(t1 * w["B"], 1e-3)))
-    t = 0.0
-    for _ in range(reps):
-        t += run(bs) if (bs > 1 or reps > 1) else t1
+    # Repeated until at least seconds_target of CPU work (capped at 4x that
+    # many repetitions of the estimate, so a slow host stays bounded).
+    reps, t = 0, 0.0
+    max_reps = max(1, int(4 * seconds_target / max(t1 * bs, 1e-3)))
+    while t < seconds_target and reps < max_reps:
+        t += run(bs)
+        reps += 1
     return {"value": round(reps * bs * w["T"] / t, 1), "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{reps} x {bs} of the {w['B']} sequences (T={w['T']}, D={w['D']}, "
