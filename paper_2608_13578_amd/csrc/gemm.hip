@@ -226,6 +226,70 @@ __device__ __forceinline__ void run_epilogue(const Epi& epi, const f32x4 (&acc)[
   }
 }
 
+// 8 consecutive elements to / from float (16 bytes of bf16, 32 of float).
+__device__ __forceinline__ void ld8(const bf16* p, float (&o)[8]) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (float)v[e];
+}
+__device__ __forceinline__ void ld8(const float* p, float (&o)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o[e] = a[e];
+    o[4 + e] = b[e];
+  }
+}
+__device__ __forceinline__ void st8(bf16* p, const float (&v)[8]) {
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
+  *reinterpret_cast<bf16x8*>(p) = o;
+}
+__device__ __forceinline__ void st8(float* p, const float (&v)[8]) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+  *reinterpret_cast<f32x4*>(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+}
+
+// Staged epilogue of the pipelined kernel.  The accumulator tile goes to
+// LDS (float32, rows of BN, 16-byte chunks XOR-swizzled by row so that the
+// 16 rows a fragment spans fall on distinct banks), then every thread hands
+// 8 consecutive columns of a row at a time to the epilogue's apply8: the
+// 16 lanes of a row write one contiguous 256-byte (bf16) segment, where the
+// fragment layout would write 32-byte pieces of 16 rows.  Every lane calls
+// apply8 the same number of times (with ok = false outside the matrix), so
+// an epilogue may reduce across lanes.
+template <int BM, int BN, int FM, int FN, int WTM, int WTN, int NTH, class Epi>
+__device__ __forceinline__ void staged_epilogue(const Epi& epi, const f32x4 (&acc)[FM][FN],
+                                                float* cs, int m0, int n0, int wm, int wn, int M,
+                                                int N, int tid) {
+  constexpr int CH = BN / 4;  // 16-byte chunks per row
+  static_assert((CH & (CH - 1)) == 0, "power-of-two row chunks");
+  const int lane = tid & 63, lr = lane & 15, lg = lane >> 4;
+  __syncthreads();  // every wave is done reading the operand slabs
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int r = wm * WTM + i * 16 + lr;
+      const int c4 = (wn * WTN + j * 16 + lg * 4) / 4;
+      *reinterpret_cast<f32x4*>(cs + r * BN + ((c4 ^ (r & (CH - 1))) * 4)) = acc[i][j];
+    }
+  __syncthreads();
+  constexpr int CPR = BN / 8;  // 8-column items per row
+  static_assert((BM * CPR) % NTH == 0, "items per thread");
+#pragma unroll 2
+  for (int it = tid; it < BM * CPR; it += NTH) {
+    const int r = it / CPR, c8 = it % CPR;
+    const float* row = cs + r * BN;
+    const f32x4 a = *reinterpret_cast<const f32x4*>(row + (((2 * c8) ^ (r & (CH - 1))) * 4));
+    const f32x4 b = *reinterpret_cast<const f32x4*>(row + (((2 * c8 + 1) ^ (r & (CH - 1))) * 4));
+    const float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    const int m = m0 + r, n = n0 + c8 * 8;
+    epi.apply8(m, n, v, m < M && n < N);
+  }
+}
+
 // ------------------------------------------------------------------ epilogues
 
 template <typename TO, typename TA>
@@ -237,6 +301,19 @@ struct EpiStore {
   __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
     if (add) v += load4f(add + (int64_t)m * ld_add + n);
     store4(C + (int64_t)m * ldc + n, v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = v[e];
+    if (add) {
+      float a[8];
+      ld8(add + (int64_t)m * ld_add + n, a);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] += a[e];
+    }
+    st8(C + (int64_t)m * ldc + n, o);
   }
 };
 
@@ -265,6 +342,24 @@ struct EpiScore {
   __device__ __forceinline__ void row(int m, int n0, float v) const {
     sp[(int64_t)m * nparts + n0 / 64] = v;
   }
+  // The 8 lanes holding one row's 64-column group (n0 a multiple of 64) are
+  // consecutive and aligned, so the group's dot is a reduction over them.
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    float d = 0.f;
+    if (ok) {
+      float o[8], w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = to_f32(from_f32<T>(v[e]));
+      ld8(wp + n, w);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d += o[e] * w[e];
+      st8(C + (int64_t)m * ldc + n, o);
+    }
+    d += __shfl_xor(d, 1);
+    d += __shfl_xor(d, 2);
+    d += __shfl_xor(d, 4);
+    if (ok && (n & 63) == 0) sp[(int64_t)m * nparts + n / 64] = d;
+  }
 };
 
 // Split-K partial tile: split z of an M x N product goes to P + z * M * N.
@@ -274,6 +369,9 @@ struct EpiPartial {
   int64_t split_stride;
   __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
     store4(P + blockIdx.z * split_stride + (int64_t)m * ld + n, v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (ok) st8(P + blockIdx.z * split_stride + (int64_t)m * ld + n, v);
   }
 };
 
@@ -322,6 +420,34 @@ struct EpiGate {
     store4(reinterpret_cast<T*>(e.Y) + off, y[0], y[1], y[2], y[3]);
     store4(reinterpret_cast<T*>(e.G) + off, g[0], g[1], g[2], g[3]);
   }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&u)[8], bool ok) const {
+    if (!ok) return;
+    const int b = m / e.T;
+    const int t = m - b * e.T;
+    const int blk = t / e.L;
+    const int64_t off = (int64_t)m * e.D + n;
+    float h[8], c[8], g[8], y[8];
+    ld8(reinterpret_cast<const T*>(e.H) + off, h);
+    if (blk > 0) {
+      ld8(e.P + (int64_t)(b * e.nb + blk - 1) * e.D + n, c);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) c[k] = 0.f;
+    }
+    if (e.X) {
+      float x[8];
+      ld8(reinterpret_cast<const T*>(e.X) + off, x);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) h[k] += x[k];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      g[k] = sigmoidf_(u[k]);
+      y[k] = h[k] + g[k] * c[k];
+    }
+    st8(reinterpret_cast<T*>(e.Y) + off, y);
+    st8(reinterpret_cast<T*>(e.G) + off, g);
+  }
 };
 
 template <typename T>
@@ -340,6 +466,21 @@ struct EpiHbar {
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[r] = v[r] + dy[r] + a * dS[r] + ds * w[r];
     store4(reinterpret_cast<T*>(e.dH) + off, o[0], o[1], o[2], o[3]);
+  }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    const int b = m / e.T;
+    const int t = m - b * e.T;
+    const int blk = t / e.L;
+    const int64_t off = (int64_t)m * e.D + n;
+    float dy[8], dS[8], w[8], o[8];
+    ld8(reinterpret_cast<const T*>(e.dY) + off, dy);
+    ld8(e.dS + (int64_t)(b * e.nb + blk) * e.D + n, dS);
+    ld8(reinterpret_cast<const T*>(e.wp) + n, w);
+    const float a = e.a[m], ds = e.ds[m];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = v[k] + dy[k] + a * dS[k] + ds * w[k];
+    st8(reinterpret_cast<T*>(e.dH) + off, o);
   }
 };
 
@@ -612,7 +753,9 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
     }
   }
 
-  run_epilogue<FM, FN>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N, lane);
+  static_assert(STAGES * STAGE * 2 >= BM * BN * 4, "staging tile fits the LDS ring");
+  staged_epilogue<BM, BN, FM, FN, WTM, WTN, NW * 64>(epi, acc, reinterpret_cast<float*>(lds), m0,
+                                                      n0, wm, wn, M, N, tid);
 }
 
 // ------------------------------------------------------------------ launch
@@ -722,6 +865,25 @@ struct EpiSegOut {
     if (accumulate) v += *dst;
     *dst = v;
   }
+  // (Output segments are multiples of 8 columns wide, so 8 columns never
+  // straddle two of them.)
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    const int sg = n / seg;
+    float* base = C[sg];
+    if (!base) return;
+    float* dst = base + (int64_t)m * ldc + (n - sg * seg);
+    float o[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = v[k];
+    if (accumulate) {
+      float a[8];
+      ld8(dst, a);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) o[k] += a[k];
+    }
+    st8(dst, o);
+  }
 };
 
 template <typename T, class Epi>
@@ -749,7 +911,7 @@ hipError_t gemm_splitk_product(DType dt, const GemmDesc& g0, float* partial, flo
                                int* splits, hipStream_t s) {
   *splits = 0;
   if (g0.M <= 0 || g0.N <= 0) return hipSuccess;
-  if (g0.N % 4 != 0 || seg_len_n % 4 != 0 || g0.seg != kSegNone) return hipErrorInvalidValue;
+  if (g0.N % 8 != 0 || seg_len_n % 8 != 0 || g0.seg != kSegNone) return hipErrorInvalidValue;
   GemmDesc g = g0;
   int kc;
   g.splits = splitk_plan(g.M, g.N, g.K, min_k, &kc);
