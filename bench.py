@@ -43,8 +43,8 @@ def stage_work(name, B, T, D, H, L, es):
     pairs *= B
     gemm = {
         "fwd.qkv_gemm": 6 * BT * D * D, "fwd.wo_gemm": 2 * BT * D * D,
-        "fwd.wm_gemm": 2 * B * nb * D * D, "fwd.gate_gemm": 2 * BT * D * D,
-        "bwd.wg_wgrad_gemm": 2 * BT * D * D, "bwd.wm_dgrad_gemm": 2 * B * nb * D * D,
+        "fwd.gate_gemm": 2 * BT * D * D,
+        "bwd.wg_wgrad_gemm": 2 * BT * D * D,
         "bwd.wm_wgrad_gemm": 2 * B * nb * D * D, "bwd.wg_dgrad_gemm": 2 * BT * D * D,
         "bwd.wo_dgrad_gemm": 2 * BT * D * D, "bwd.wo_wgrad_gemm": 2 * BT * D * D,
         "bwd.qkv_dgrad_gemm": 6 * BT * D * D, "bwd.qkv_wgrad_gemm": 6 * BT * D * D,
@@ -64,9 +64,12 @@ def stage_work(name, B, T, D, H, L, es):
     act = BT * D * es
     hbm = {
         "fwd.pool": act + BT * 4 + B * nb * D * 4 + B * nb * 8,
-        "fwd.scan": B * nb * D * (4 + 4 + 4 + es),
+        # memory projection + scan: read S (float32 and compute type) and W_m,
+        # write M (both types) and P
+        "fwd.memory_scan": B * nb * D * (4 + es + 4 + es + 4) + D * D * es,
         "bwd.gate": 3 * act + B * nb * D * (4 + es),
-        "bwd.memory_scan": B * nb * D * 12,
+        # read dP (compute type), W_m and M, write dS
+        "bwd.memory_scan": B * nb * D * (es + 4 + 4) + D * D * es,
         "bwd.pool": act + BT * 12 + B * nb * D * 8,
         "bwd.zero_grads": (D + 1) * 4,
     }

@@ -44,9 +44,9 @@ struct Plan {
   // saved (forward -> backward)
   size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
   // forward scratch
-  size_t sp, St, mpart, fwd_bytes;
+  size_t sp, St, fwd_bytes;
   // backward scratch
-  size_t du, pbar, dS, a, ds, dh, dout, delta, dqkv, wpart, mpart_b, bwd_bytes;
+  size_t du, pbar, dS, a, ds, dh, dout, delta, dqkv, wpart, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -80,9 +80,6 @@ struct Plan {
     off = 0;
     sp = take(BT * (D / kDh) * 4);  // partial pooling scores, D / 64 per token
     St = take(BND * es);
-    // split-K partials of the memory projection (at least one slice: the
-    // scan reads them even when the product has a single split)
-    mpart = take(std::max(gemm_splitk_partial_bytes(B * nb, D, D, 64), BND * 4));
     fwd_bytes = off;
 
     off = 0;
@@ -101,8 +98,6 @@ struct Plan {
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
       wpart = take(w);  // weight gradients (side stream, one after another)
-      // dM as split-K partials, read by the reverse scan (caller's stream)
-      mpart_b = take(std::max(gemm_splitk_partial_bytes(BNi, D, D, 64), BND * 4));
     }
     bwd_bytes = off;
   }
@@ -135,15 +130,15 @@ bool overlaps(const void* a, const void* b, size_t n) {
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
 enum Stage {
-  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_WM, ST_SCAN_FWD, ST_GATE,
-  ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_DGRAD, ST_WM_WGRAD,
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_GATE,
+  ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_WGRAD,
   ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_DWP, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
-    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.wm_gemm", "fwd.scan",
-    "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce", "bwd.wm_dgrad_gemm",
+    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.memory_scan",
+    "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce",
     "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.pool_dwp", "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
@@ -369,20 +364,12 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
   LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, (const float*)(W + p.sp), D / kDh,
                                (float*)(SV + p.s), (float*)(SV + p.S), W + p.St,
                                (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
-  // 5-6. Exponential memory and its projection (Sec. 3.5).  The projection
-  // is linear and so is the normalised decayed sum, so the summaries are
-  // projected first (Q = S Wm, as split-K partial products over only
-  // B * N_b rows) and one scan then yields both M and P = M Wm; the shift is
-  // applied where P is read.
-  int qs = 0;
-  {
-    float* Q = (float*)(W + p.mpart);
-    GemmDesc g{p.B * p.nb, D, D, W + p.St, D, false, {prm->Wm, nullptr, nullptr}, D, true,
-               kSegNone, 0, 1};
-    LAUNCH(ST_WM, gemm_splitk_product(dt, g, Q, Q, nullptr, nullptr, D, D, false, 64, &qs, s));
-    LAUNCH(ST_SCAN_FWD, scan_fwd(dt, (const float*)(SV + p.S), Q, qs, (float*)(SV + p.M),
-                                 SV + p.Mt, (float*)(SV + p.P), p.B, p.T, D, p.L, cfg->gamma, s));
-  }
+  // 5-6. Exponential memory and its projection (Sec. 3.5): one kernel
+  // projects the summaries (Q = S Wm, over only B * N_b rows) and scans S
+  // and Q, which yields M and P = M Wm (the decayed sum is linear); the
+  // shift is applied where P is read.
+  LAUNCH(ST_SCAN_FWD, mem_fwd(dt, W + p.St, prm->Wm, (const float*)(SV + p.S), (float*)(SV + p.M),
+                              SV + p.Mt, (float*)(SV + p.P), p.B, p.nb, D, cfg->gamma, s));
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
     GemmDesc g{BT, D, D, SV + p.h, D, false, {prm->Wg, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -468,17 +455,10 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
     }
     SIDE_END();
   }
-  // Memory projection: dM = dP Wm^T as split-K partials, summed by the
-  // decayed reverse scan that follows (dS and the decay gradient).
-  {
-    int ms = 0;
-    float* Mp = (float*)(W + p.mpart_b);
-    GemmDesc g{BN, D, D, W + p.pbar, D, false, {prm->Wm, nullptr, nullptr}, D, false, kSegNone, 0,
-               1};
-    LAUNCH(ST_WM_DGRAD, gemm_splitk_product(dt, g, Mp, Mp, nullptr, nullptr, D, D, false, 64, &ms, s));
-    LAUNCH(ST_MEM_BWD, mem_bwd(Mp, ms, (const float*)(SV + p.M), (float*)(W + p.dS), gr.dgamma,
-                               p.B, p.nb, D, cfg->gamma, s));
-  }
+  // Memory projection and decayed reverse scan: dM = dP Wm^T, dS and the
+  // decay gradient, in one kernel.
+  LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
+                             gr.dgamma, p.B, p.nb, D, cfg->gamma, s));
   // Pooling backward: per-token a_t and ds_t; dwp = sum_t ds_t H[t] on the
   // side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),

@@ -121,18 +121,18 @@ hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void
 // type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
 hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
                     void* St, float* stats, int B, int T, int D, int L, hipStream_t s);
-// Decayed scan: M (float32) and its compute-type copy Mt from the summaries
-// S, and P from the projected summaries, given as qs split-K partial
-// products Q (each [B*nb, D], consecutive).
-hipError_t scan_fwd(DType dt, const float* S, const float* Q, int qs, float* M, void* Mt, float* P,
-                    int B, int T, int D, int L, float gamma, hipStream_t s);
+// Memory forward: Q = St Wm (St = S in the compute type, [B*nb, D]) and the
+// decayed scans of S and Q: M (float32), Mt (compute type) and P = M Wm.
+hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
+                   float* P, int B, int nb, int D, float gamma, hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
                     hipStream_t s);
-// Reverse decayed scan; dM is given as ms split-K partial products.
-hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float* dgamma, int B,
-                   int nb, int D, float gamma, hipStream_t s);
+// Memory backward: dM = Pbar Wm^T, then the reverse decayed scan: dS and
+// the decay gradient (atomically added to *dgamma when given).
+hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
+                   float* dgamma, int B, int nb, int D, float gamma, hipStream_t s);
 // Pooling backward: per-token softmax weights a_t and score gradients ds_t.
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
                     const float* S, const float* dS, float* a_out, float* ds_out, int B, int T,

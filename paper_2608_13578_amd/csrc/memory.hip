@@ -9,10 +9,8 @@
 // Decay recurrences.  With Z_i = sum_{j<=i} g^(i-j) and N_i = sum_{j<=i}
 // g^(i-j) S_j (0-based blocks), the memory is M_i = N_i / Z_i and
 //   N_i = g N_{i-1} + S_i,  Z_i = g Z_{i-1} + 1.
-// One workgroup owns 32 feature columns of one batch element over all blocks:
-// eight segments of consecutive blocks are folded locally, the segment
-// carries are combined in LDS, and each segment is replayed with its carry.
-// No workgroup ever waits on another.
+// One workgroup owns 32 feature columns of one batch element over all
+// blocks, so no workgroup ever waits on another.
 #include "common.h"
 #include "kernels.h"
 
@@ -157,67 +155,149 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
   }
 }
 
-// ------------------------------------------------------------------ decayed scan
-// The same recurrence runs over two inputs: the summaries S (giving M, kept
-// for the backward) and their projections Q_i = S_i W_m, given as the sum of
-// the qs split-K partial products (giving P_i = M_i W_m, since the
-// normalised decayed sum is linear in its input).
-template <typename T>
-__global__ __launch_bounds__(256) void scan_fwd_kernel(const float* __restrict__ S,
-                                                       const float* __restrict__ Q, int qs,
-                                                       int64_t qstride, float* __restrict__ M,
-                                                       T* __restrict__ Mt, float* __restrict__ P,
-                                                       int nb, int D, float gamma) {
-  __shared__ float cN[8][32], cP[8][32];
-  __shared__ float cZ[8], cG[8];
-  const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
-  const int col = blockIdx.x * 32 + cl;
-  const int b = blockIdx.y;
-  const bool act = col < D;
-  const int SL = (nb + 7) / 8;
-  const int i0 = seg * SL;
-  const int i1 = min(nb, i0 + SL);
-  auto qsum = [&](int64_t off) {
-    float v = 0.f;
-    for (int z = 0; z < qs; ++z) v += Q[z * qstride + off];
-    return v;
-  };
+// ------------------------------------------------------------------ memory projection + scan
+// Each workgroup owns 32 columns of one sequence and walks its N_b blocks in
+// row tiles of 16: a small matrix product gives the tile's 16 x 32 outputs
+// (the four waves take alternate 32-deep k steps and meet in LDS), then 32
+// threads carry the decayed recurrence of their column through the tile.
+//   forward:  Q = S W_m (A = S in the compute type, B = W_m [D, D] read
+//             through LDS), and with Z_i = g Z_{i-1} + 1 the recurrences
+//             N_i = g N_{i-1} + S_i and NP_i = g NP_{i-1} + Q_i give
+//             M = N / Z (float32 and compute type) and P = M W_m = NP / Z
+//             (the normalised decayed sum is linear, so scanning the
+//             projections equals projecting the scan);
+//   backward: dM = dP W_m^T (A = dP, B(k, n) = W_m[n, k], read directly),
+//             then, from the last block down,
+//               Qs_i = dM_i / Z_i + g Qs_{i+1}      (= dS_i = dN_i)
+//               E_i  = -dM_i . M_i / Z_i + g E_{i+1} (= dZ_i, per column)
+//             and dg = sum_{i>=1} Qs_i N_{i-1} + E_i Z_{i-1} with
+//             N_{i-1} = M_{i-1} Z_{i-1}.
+// Z_i = 1 + g + ... + g^i (0-based i), with lg2 = log2(g) (g > 0).
+__device__ __forceinline__ float zsum(int i, float gamma, float lg2) {
+  if (gamma == 0.f) return 1.f;
+  return (1.f - exp2f(lg2 * (float)(i + 1))) / (1.f - gamma);
+}
 
-  float N = 0.f, NP = 0.f, Z = 0.f, g = 1.f;
-  for (int i = i0; i < i1; ++i) {
-    const int64_t off = (int64_t)(b * nb + i) * D + col;
-    N = gamma * N + (act ? S[off] : 0.f);
-    NP = gamma * NP + (act ? qsum(off) : 0.f);
-    Z = gamma * Z + 1.f;
-    g *= gamma;
+constexpr int kMsCols = 32, kMsRows = 16, kMsWaves = 8, kMsGroup = 4;
+
+// Forward: W_m columns c0 .. c0+31 for rows kc .. kc+kn-1 are staged in LDS
+// (dynamic, kc chunks of at most 64 KB); the k steps of a row tile are
+// dealt to the eight waves round-robin and each wave loads kMsGroup steps'
+// fragments before multiplying them, so that the loads overlap.
+template <typename T, bool FWD>
+__global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
+    const T* __restrict__ A, const T* __restrict__ Wm, const float* __restrict__ S,
+    float* __restrict__ M, T* __restrict__ Mt, float* __restrict__ P, const float* __restrict__ Min,
+    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, int kcr) {
+  typedef typename Frag<T>::type F;
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  T* Bs = reinterpret_cast<T*>(dyn);  // [kcr][kMsCols] (forward only)
+  __shared__ float part[kMsWaves][kMsRows][kMsCols];
+  __shared__ float red[kMsWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int c0 = blockIdx.x * kMsCols, b = blockIdx.y;
+  const int nt = (nb + kMsRows - 1) / kMsRows;
+  const int col = c0 + tid;
+  const bool scol = tid < kMsCols && col < D;
+  float N = 0.f, NP = 0.f, Z = 0.f, Qs = 0.f, E = 0.f, dg = 0.f;
+  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+
+  for (int q = 0; q < nt; ++q) {
+    const int rt = FWD ? q : nt - 1 - q;
+    const int i0 = rt * kMsRows;
+    const int arow = i0 + lr;
+    const T* ap = A + ((int64_t)b * nb + (arow < nb ? arow : 0)) * D;
+    f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    for (int kc = 0; kc < D; kc += (FWD ? kcr : D)) {
+      const int kn = FWD ? min(kcr, D - kc) : D;
+      if constexpr (FWD) {
+        __syncthreads();
+        constexpr int VE = Vec16<T>::N;
+        constexpr int VPR = kMsCols / VE;  // 16-byte vectors per staged row
+        for (int e = tid; e < kn * VPR; e += blockDim.x) {
+          const int kr = e / VPR, cv = (e % VPR) * VE;
+          const bool ok = c0 + cv < D;
+          store16(Bs + kr * kMsCols + cv,
+                  ok ? load16(Wm + (int64_t)(kc + kr) * D + c0 + cv) : typename Vec16<T>::type{});
+        }
+        __syncthreads();
+      }
+      const int nks = kn / 32;
+      for (int g0 = wave; g0 < nks; g0 += kMsWaves * kMsGroup) {
+        F af[kMsGroup], bfr[kMsGroup][2];
+#pragma unroll
+        for (int u = 0; u < kMsGroup; ++u) {
+          const int ks = g0 + u * kMsWaves;
+          const bool on = ks < nks;
+          const int kl = ks * 32 + lg * 8;  // within the chunk
+          af[u] = (on && arow < nb) ? load_frag(ap + kc + kl) : F{};
+#pragma unroll
+          for (int ntl = 0; ntl < 2; ++ntl) {
+            const int n = c0 + ntl * 16 + lr;
+            if constexpr (FWD) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                bfr[u][ntl][e] = on ? Bs[(kl + e) * kMsCols + ntl * 16 + lr] : from_f32<T>(0.f);
+            } else {
+              bfr[u][ntl] = (on && n < D) ? load_frag(Wm + (int64_t)n * D + kc + kl) : F{};
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kMsGroup; ++u)
+#pragma unroll
+          for (int ntl = 0; ntl < 2; ++ntl) acc[ntl] = mma16(bfr[u][ntl], af[u], acc[ntl]);
+      }
+    }
+    // lane holds row i0 + lr, columns 16 ntl + 4 lg + r of this wave's sum
+#pragma unroll
+    for (int ntl = 0; ntl < 2; ++ntl)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) part[wave][lr][ntl * 16 + lg * 4 + r] = acc[ntl][r];
+    __syncthreads();
+    if (scol) {
+      for (int k = 0; k < kMsRows; ++k) {
+        const int ii = FWD ? k : kMsRows - 1 - k;
+        const int i = i0 + ii;
+        if (i >= nb) continue;
+        float g = 0.f;
+#pragma unroll
+        for (int w = 0; w < kMsWaves; ++w) g += part[w][ii][tid];
+        const int64_t off = ((int64_t)b * nb + i) * D + col;
+        if constexpr (FWD) {
+          N = gamma * N + S[off];
+          NP = gamma * NP + g;
+          Z = gamma * Z + 1.f;
+          const float rz = 1.f / Z;
+          const float m = N * rz;
+          M[off] = m;
+          Mt[off] = from_f32<T>(m);
+          P[off] = NP * rz;
+        } else {
+          const float z = zsum(i, gamma, lg2);
+          const float m = Min[off];
+          Qs = g / z + gamma * Qs;
+          E = -g * m / z + gamma * E;
+          dS[off] = Qs;
+          if (i >= 1) {
+            const float zp = zsum(i - 1, gamma, lg2);
+            dg += Qs * (Min[off - D] * zp) + E * zp;
+          }
+        }
+      }
+    }
+    __syncthreads();  // part[] is rewritten by the next row tile
   }
-  cN[seg][cl] = N;
-  cP[seg][cl] = NP;
-  if (cl == 0) {
-    cZ[seg] = Z;
-    cG[seg] = g;
-  }
-  __syncthreads();
-  float Nin = 0.f, Pin = 0.f, Zin = 0.f;
-  for (int k = 0; k < seg; ++k) {
-    Nin = cG[k] * Nin + cN[k][cl];
-    Pin = cG[k] * Pin + cP[k][cl];
-    Zin = cG[k] * Zin + cZ[k];
-  }
-  if (!act) return;
-  N = Nin;
-  NP = Pin;
-  Z = Zin;
-  for (int i = i0; i < i1; ++i) {
-    const int64_t off = (int64_t)(b * nb + i) * D + col;
-    N = gamma * N + S[off];
-    NP = gamma * NP + qsum(off);
-    Z = gamma * Z + 1.f;
-    const float rz = 1.f / Z;
-    const float m = N * rz;
-    M[off] = m;
-    Mt[off] = from_f32<T>(m);
-    P[off] = NP * rz;
+  if constexpr (!FWD) {
+    const float v = wave_sum(dg);
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    if (tid == 0 && dgamma) {
+      float t = 0.f;
+      for (int w = 0; w < kMsWaves; ++w) t += red[w];
+      unsafeAtomicAdd(dgamma, t);
+    }
   }
 }
 
@@ -302,81 +382,6 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * D + c0 + cc;
     Pbar[dst] = from_f32<T>(i > 0 ? sum : 0.f);
   }
-}
-
-// ------------------------------------------------------------------ memory backward
-// Given dM (the gradient of the normalised memory, last block zero):
-//   dS_i = sum_{k>=i} g^(k-i) dM_k / Z_k                       (reverse scan)
-//   dg   = sum_{i>=1} dN_i . N_{i-1} + dZ_i Z_{i-1},  with
-//   dN_i = dS_i and dZ_i = sum_{k>=i} g^(k-i) (-dM_k . M_k / Z_k).
-// The per-column part of dZ is scanned like dS; its dot over the columns is
-// taken with the final reduction.
-__device__ __forceinline__ float zsum(int i, float gamma) {
-  // Z_i = 1 + g + ... + g^i (0-based i).
-  if (gamma == 0.f) return 1.f;
-  return (1.f - powf(gamma, (float)(i + 1))) / (1.f - gamma);
-}
-
-// dM arrives as the sum of ms split-K partial products (stride mstride).
-__global__ __launch_bounds__(256) void mem_bwd_kernel(const float* __restrict__ Mpart, int ms,
-                                                      int64_t mstride, const float* __restrict__ M,
-                                                      float* __restrict__ dS,
-                                                      float* __restrict__ dgamma, int nb, int D,
-                                                      float gamma) {
-  auto mbar = [&](int64_t off) {
-    float v = 0.f;
-    for (int z = 0; z < ms; ++z) v += Mpart[z * mstride + off];
-    return v;
-  };
-  __shared__ float cQ[8][32], cE[8][32];
-  __shared__ float cG[8];
-  __shared__ float red[4];
-  const int cl = threadIdx.x & 31, seg = threadIdx.x >> 5;
-  const int col = blockIdx.x * 32 + cl;
-  const int b = blockIdx.y;
-  const bool act = col < D;
-  const int SL = (nb + 7) / 8;
-  const int i0 = seg * SL;
-  const int i1 = min(nb, i0 + SL);
-
-  float Q = 0.f, E = 0.f, g = 1.f;
-  for (int i = i1 - 1; i >= i0; --i) {
-    const int64_t off = (int64_t)(b * nb + i) * D + col;
-    const float mb = act ? mbar(off) : 0.f;
-    const float m = act ? M[off] : 0.f;
-    const float z = zsum(i, gamma);
-    Q = mb / z + gamma * Q;
-    E = -mb * m / z + gamma * E;
-    g *= gamma;
-  }
-  cQ[seg][cl] = Q;
-  cE[seg][cl] = E;
-  if (cl == 0) cG[seg] = g;
-  __syncthreads();
-  float Qin = 0.f, Ein = 0.f;
-  for (int k = 7; k > seg; --k) {
-    Qin = cG[k] * Qin + cQ[k][cl];
-    Ein = cG[k] * Ein + cE[k][cl];
-  }
-  Q = Qin;
-  E = Ein;
-  float acc = 0.f;
-  if (act) {
-    for (int i = i1 - 1; i >= i0; --i) {
-      const int64_t off = (int64_t)(b * nb + i) * D + col;
-      const float mb = mbar(off);
-      const float z = zsum(i, gamma);
-      Q = mb / z + gamma * Q;
-      E = -mb * M[off] / z + gamma * E;
-      dS[off] = Q;
-      if (i >= 1) {
-        const float zp = zsum(i - 1, gamma);
-        acc += Q * (M[off - D] * zp) + E * zp;
-      }
-    }
-  }
-  const float tot = block_reduce_sum(acc, red);
-  if (threadIdx.x == 0 && dgamma) unsafeAtomicAdd(dgamma, tot);
 }
 
 // ------------------------------------------------------------------ pooling backward
@@ -594,17 +599,21 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
   return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
 }
 
-hipError_t scan_fwd(DType dt, const float* S, const float* Q, int qs, float* M, void* Mt, float* P,
-                    int B, int T, int D, int L, float gamma, hipStream_t s) {
-  const int nb = (T + L - 1) / L;
-  const int64_t qstride = (int64_t)B * nb * D;
-  dim3 grid((D + 31) / 32, B);
+hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
+                   float* P, int B, int nb, int D, float gamma, hipStream_t s) {
+  dim3 grid((D + kMsCols - 1) / kMsCols, B);
+  const int es = dt == DType::BF16 ? 2 : 4;
+  int kcr = (64 * 1024) / (kMsCols * es);  // staged W_m rows per chunk (64 KB)
+  if (kcr > D) kcr = D;
+  const size_t lds = (size_t)kcr * kMsCols * es;
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(256), 0, s, S, Q, qs, qstride, M,
-                       (bf16*)Mt, P, nb, D, gamma);
+    hipLaunchKernelGGL((memscan_kernel<bf16, true>), grid, dim3(kMsWaves * 64), lds, s,
+                       (const bf16*)St, (const bf16*)Wm, S, M, (bf16*)Mt, P, nullptr, nullptr,
+                       nullptr, nb, D, gamma, kcr);
   else
-    hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(256), 0, s, S, Q, qs, qstride, M,
-                       (float*)Mt, P, nb, D, gamma);
+    hipLaunchKernelGGL((memscan_kernel<float, true>), grid, dim3(kMsWaves * 64), lds, s,
+                       (const float*)St, (const float*)Wm, S, M, (float*)Mt, P, nullptr, nullptr,
+                       nullptr, nb, D, gamma, kcr);
   return hipGetLastError();
 }
 
@@ -616,12 +625,17 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
   return gate_bwd_t<float>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, s);
 }
 
-hipError_t mem_bwd(const float* Mpart, int ms, const float* M, float* dS, float* dgamma, int B,
-                   int nb, int D, float gamma, hipStream_t s) {
-  dim3 grid((D + 31) / 32, B);
-  const int64_t mstride = (int64_t)B * nb * D;
-  hipLaunchKernelGGL(mem_bwd_kernel, grid, dim3(256), 0, s, Mpart, ms, mstride, M, dS, dgamma, nb,
-                     D, gamma);
+hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
+                   float* dgamma, int B, int nb, int D, float gamma, hipStream_t s) {
+  dim3 grid((D + kMsCols - 1) / kMsCols, B);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
+                       (const bf16*)Pbar, (const bf16*)Wm, nullptr, nullptr, nullptr, nullptr, M,
+                       dS, dgamma, nb, D, gamma, 0);
+  else
+    hipLaunchKernelGGL((memscan_kernel<float, false>), grid, dim3(kMsWaves * 64), 0, s,
+                       (const float*)Pbar, (const float*)Wm, nullptr, nullptr, nullptr, nullptr, M,
+                       dS, dgamma, nb, D, gamma, 0);
   return hipGetLastError();
 }
 
