@@ -169,8 +169,23 @@ __device__ __forceinline__ f32x4 lds_read_f32x4(const float* p) {
   asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
   return v;
 }
+// 16-byte bf16 LDS read in inline assembly; same contract as lds_read_tr().
+__device__ __forceinline__ bf16x8 lds_read_b128(const bf16* p) {
+  bf16x8 v;
+  const unsigned a = (unsigned)(uintptr_t)((__attribute__((address_space(3))) bf16*)(p));
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
 // Waits for every outstanding LDS read of this wave.
 __device__ __forceinline__ void lds_tr_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Waits until at most N of this wave's LDS reads are outstanding (they
+// complete in issue order).  Only for stretches of code whose LDS and scalar
+// memory traffic is all issued through the inline-assembly reads above.
+template <int N>
+__device__ __forceinline__ void lds_wait() {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
 // Ties a value to the preceding lds_tr_wait(), so that no use of it is
 // scheduled before the wait.
 template <class V>

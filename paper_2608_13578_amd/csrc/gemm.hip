@@ -18,6 +18,8 @@
 // The matrix instruction is issued with the B tile as its first operand, so
 // a lane ends up holding four consecutive output columns of one output row:
 // the epilogue stores 8 (bf16) or 16 (f32) contiguous bytes per lane.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -122,7 +124,7 @@ template <typename T, bool A_MC, bool B_NC, int BSEG, class Epi>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(int M, int N, int K,
                                                         Operand<T, A_MC, kSegNone> A,
                                                         Operand<T, B_NC, BSEG> B, int kchunk,
-                                                        Epi epi) {
+                                                        Epi epi0) {
   constexpr int BK = KSlab<T>::BK;
   constexpr int VE = Vec16<T>::N;
   constexpr int LDS_ROW = BK + VE;
@@ -135,6 +137,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(int M, int N, int K,
   const int lr = lane & 15, lg = lane >> 4;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int kbeg = blockIdx.z * kchunk;
+  Epi epi = epi0;
+  bind_split(epi, blockIdx.z);
   const int kend = min(K, kbeg + kchunk);
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
@@ -362,18 +366,20 @@ struct EpiScore {
   }
 };
 
-// Split-K partial tile: split z of an M x N product goes to P + z * M * N.
+// Split-K partial tile: split z of an M x N product goes to P + z * M * N
+// (the kernel moves P to its split's slice through bind_split).
 struct EpiPartial {
   float* P;
   int64_t ld;
   int64_t split_stride;
   __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
-    store4(P + blockIdx.z * split_stride + (int64_t)m * ld + n, v[0], v[1], v[2], v[3]);
+    store4(P + (int64_t)m * ld + n, v[0], v[1], v[2], v[3]);
   }
   __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
-    if (ok) st8(P + blockIdx.z * split_stride + (int64_t)m * ld + n, v);
+    if (ok) st8(P + (int64_t)m * ld + n, v);
   }
 };
+__device__ __forceinline__ void bind_split(EpiPartial& e, int z) { e.P += z * e.split_stride; }
 
 // Sums the split-K partials (4 consecutive columns per thread) and writes or
 // accumulates into the output segment that holds column n.
@@ -488,8 +494,8 @@ struct EpiHbar {
 // The bf16 path streams K slabs of 64 through a ring of STAGES LDS buffers
 // with direct global->LDS loads (each 16-byte load lands at base + 16*lane
 // of its instruction's 1 KB LDS window), so no register holds operand data
-// on its way in and the loads for slab k + STAGES - 1 are in flight while
-// slab k is multiplied.
+// on its way in and the loads of the next slabs are in flight while one is
+// multiplied.
 //
 // LDS keeps every operand in its global orientation:
 //   K-contiguous operand: [rows][64] with the 16-byte chunk c of row r
@@ -597,7 +603,7 @@ struct PipeLoad {
     if constexpr (!RCONTIG) {
       const int r = base + lr;
       const int c = (ks * 4 + lg) ^ Op::kswz(r);
-      return *reinterpret_cast<const bf16x8*>(s + r * BK + c * 8);
+      return lds_read_b128(s + r * BK + c * 8);
     } else {
       const int col = base + (lr & 3) * 4;
       bf16x4 h[2];
@@ -614,35 +620,42 @@ struct PipeLoad {
 };
 
 // Tile order.  Workgroups are dealt to the chip's 8 XCDs round-robin in
-// launch order, and each XCD has its own L2.  The launch-order index is
-// mapped so that every XCD works through one contiguous run of the tile
-// sequence, and the sequence walks groups of kGroupM tile rows column by
-// column: the tiles an XCD holds at once then share a few A row panels and
-// B column panels in that XCD's L2.
+// launch order (x fastest, then y, then the split index z), and each XCD has
+// its own L2.  The launch-order index is mapped so that every XCD works
+// through one contiguous run of the (split, tile) sequence; within a split
+// the sequence walks groups of `group` tile rows column by column.  The
+// launcher picks the group height that keeps the A row panels plus B column
+// panels each XCD touches smallest (xcd_group_rows), so that they are read
+// from HBM once per XCD and then served from its L2.
 constexpr int kXcds = 8;
-constexpr int kGroupM = 4;
 
-__device__ __forceinline__ void xcd_tile_order(int bx, int by, int nx, int ny, int& tm, int& tn) {
+__device__ __forceinline__ void xcd_tile_order(int group, int& tm, int& tn, int& z) {
+  const int nx = gridDim.x, ny = gridDim.y;
   const int ntiles = nx * ny;
-  const int bid = by * nx + bx;
+  const int total = ntiles * gridDim.z;
+  const int bid = (blockIdx.z * ny + blockIdx.y) * nx + blockIdx.x;
   const int xcd = bid % kXcds, pos = bid / kXcds;
-  const int q = ntiles / kXcds, r = ntiles % kXcds;
-  const int t = xcd < r ? xcd * (q + 1) + pos : r * (q + 1) + (xcd - r) * q + pos;
-  const int group = kGroupM * nx;
-  const int first = (t / group) * kGroupM;
-  const int gm = min(ny - first, kGroupM);
-  const int in = t % group;
+  const int q = total / kXcds, r = total % kXcds;
+  int t = xcd < r ? xcd * (q + 1) + pos : r * (q + 1) + (xcd - r) * q + pos;
+  z = t / ntiles;
+  t -= z * ntiles;
+  const int first = (t / (group * nx)) * group;
+  const int gm = min(ny - first, group);
+  const int in = t - first * nx;
   tm = first + in % gm;
   tn = in / gm;
 }
 
+// Split-K partial epilogues write the slice of their split; others ignore it.
+template <class E>
+__device__ __forceinline__ void bind_split(E&, int) {}
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool A_MC, bool B_NC, int BSEG,
           class Epi>
 __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, int K,
                                                                 Operand<bf16, A_MC, kSegNone> A,
                                                                 Operand<bf16, B_NC, BSEG> B,
-                                                                int kchunk, Epi epi) {
+                                                                int kchunk, int group, Epi epi0) {
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
@@ -657,10 +670,12 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
-  int tm, tn;
-  xcd_tile_order(blockIdx.x, blockIdx.y, gridDim.x, gridDim.y, tm, tn);
+  int tm, tn, z;
+  xcd_tile_order(group, tm, tn, z);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int kbeg = blockIdx.z * kchunk;
+  const int kbeg = z * kchunk;
+  Epi epi = epi0;
+  bind_split(epi, z);
   const int kend = min(K, kbeg + kchunk);
   const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
 
@@ -695,8 +710,54 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Software pipeline: the fragments of the next 32-wide K step are read
+  // from LDS while the matrix instructions of the current one run; the
+  // first step of slab kt + 1 is read during the last step of slab kt,
+  // right after the barrier that publishes slab kt + 1 and releases slab
+  // kt's buffer for slab kt + STAGES.  Every LDS access of the loop goes
+  // through inline assembly, so the waits below count all of them.
+  constexpr int NKS = BK / 32;  // K steps per slab
+  static_assert(NKS == 1 || NKS == 2, "slab depth");
+  constexpr int UNR = NKS == 1 ? 2 : 1;  // slabs per trip, so that fragment sets alternate
+  constexpr int NR = FM * (A_MC ? 2 : 1) + FN * (B_NC ? 2 : 1);  // LDS reads per K step
+  constexpr int NRW = NR < 15 ? NR : 15;
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto read_step = [&](const bf16* s, int ks, bf16x8(&a)[FM], bf16x8(&b)[FN]) {
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st) {
+    for (int i = 0; i < FM; ++i) a[i] = LA::frag(s, wm * WTM + i * 16, ks, lane);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) b[j] = LB::frag(s + AEL, wn * WTN + j * 16, ks, lane);
+  };
+  // The matrix instructions are inline assembly too, so that they stay
+  // between the reads and waits that feed them (the accumulators stay put in
+  // AGPRs).  The compiler's hazard tracking does not see them: s_nop 2
+  // covers a vector write of an operand just before, and the loop's end
+  // waits out their passes before anything reads the accumulators.
+  auto mma_step = [&](bf16x8(&a)[FM], bf16x8(&b)[FN]) {
+    asm volatile("s_nop 2");
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                     : "+a"(acc[i][j])
+                     : "v"(b[j]), "v"(a[i]));
+  };
+  // Waits until slab `need` has landed, given that slabs up to `last` were
+  // issued (each wave's own loads; the barrier that follows covers the rest).
+  auto wait_slab = [&](int need, int last) {
+    const int after = last - need;
+    if (after >= 4 && STAGES >= 5) wait_vmcnt<4 * NI>();
+    else if (after >= 3 && STAGES >= 4) wait_vmcnt<3 * NI>();
+    else if (after >= 2 && STAGES >= 3) wait_vmcnt<2 * NI>();
+    else if (after >= 1) wait_vmcnt<NI>();
+    else wait_vmcnt<0>();
+  };
+  auto buf = [&](int kt) { return lds + (kt % STAGES) * STAGE; };
+
+  // Prologue: every buffer of the ring receives its slab.
+#pragma unroll
+  for (int st = 0; st < STAGES; ++st) {
     if (st < nk) {
       bf16* sa = lds + st * STAGE;
       const int k = kbeg + st * BK;
@@ -704,54 +765,45 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
       lb.issue(bslab(k), sa + AEL, wave);
     }
   }
-
-  for (int kt = 0; kt < nk; ++kt) {
-    // Slab kt must have landed; slabs kt+1 .. may stay in flight.
-    const int after = min(nk - 1, kt + STAGES - 2) - kt;
-    if constexpr (STAGES >= 4) {
-      if (after >= 3 && STAGES >= 5) wait_vmcnt<3 * NI>();
-      else if (after >= 2) wait_vmcnt<2 * NI>();
-      else if (after == 1) wait_vmcnt<NI>();
-      else wait_vmcnt<0>();
-    } else if constexpr (STAGES == 3) {
-      if (after >= 1) wait_vmcnt<NI>();
-      else wait_vmcnt<0>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    // Every wave has waited for its own loads of slab kt; the barrier makes
-    // all of them visible and retires all reads of the buffer reloaded next.
-    // (A plain s_barrier: __syncthreads would also drain the later slabs.)
+  if (nk > 0) {
+    wait_slab(0, min(nk, STAGES) - 1);
     __builtin_amdgcn_s_barrier();
-    const int nxt = kt + STAGES - 1;
-    if (nxt < nk) {
-      bf16* sa = lds + (nxt % STAGES) * STAGE;
-      const int k = kbeg + nxt * BK;
-      la.issue(la.slab(A.p[0], A.ld, k), sa, wave);
-      lb.issue(bslab(k), sa + AEL, wave);
-    }
-    const bf16* sa = lds + (kt % STAGES) * STAGE;
-    const bf16* sb = sa + AEL;
+    read_step(lds, 0, fa[0], fb[0]);
+  }
+
+  for (int kt0 = 0; kt0 < nk; kt0 += UNR) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 fa[FM], fb[FN];
+    for (int uu = 0; uu < UNR; ++uu) {
+      const int kt = kt0 + uu;
+      if (UNR > 1 && kt >= nk) break;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) fa[i] = LA::frag(sa, wm * WTM + i * 16, ks, lane);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) fb[j] = LB::frag(sb, wn * WTN + j * 16, ks, lane);
-      if constexpr (A_MC || B_NC) {  // transposing reads went through inline assembly
-        lds_tr_wait();
-#pragma unroll
-        for (int i = 0; i < FM; ++i) lds_tr_bind(fa[i]);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) lds_tr_bind(fb[j]);
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int c = (uu * NKS + ks) & 1;  // fragment set of this step
+        if (ks + 1 < NKS) {
+          read_step(buf(kt), ks + 1, fa[c ^ 1], fb[c ^ 1]);
+          lds_wait<NRW>();  // this step's fragments have landed
+        } else {
+          lds_wait<0>();  // this step's too, and this wave is done reading slab kt
+          if (kt + 1 < nk) {
+            wait_slab(kt + 1, min(nk, kt + STAGES) - 1);
+            // Slab kt + 1 is visible to all waves, and no wave reads slab kt
+            // any more: its buffer takes slab kt + STAGES.
+            __builtin_amdgcn_s_barrier();
+            const int nxt = kt + STAGES;
+            if (nxt < nk) {
+              bf16* sn = buf(kt);
+              const int k = kbeg + nxt * BK;
+              la.issue(la.slab(A.p[0], A.ld, k), sn, wave);
+              lb.issue(bslab(k), sn + AEL, wave);
+            }
+            read_step(buf(kt + 1), 0, fa[c ^ 1], fb[c ^ 1]);
+          }
+        }
+        mma_step(fa[c], fb[c]);
       }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mma16(fb[j], fa[i], acc[i][j]);
     }
   }
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
 
   static_assert(STAGES * STAGE * 2 >= BM * BN * 4, "staging tile fits the LDS ring");
   staged_epilogue<BM, BN, FM, FN, WTM, WTN, NW * 64>(epi, acc, reinterpret_cast<float*>(lds), m0,
@@ -759,6 +811,72 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
 }
 
 // ------------------------------------------------------------------ launch
+
+// Tile rows plus tile columns (counted per split, whose K ranges differ)
+// that the tiles [a, b) of the (split, tile) sequence touch with group
+// height g.
+int64_t panels_touched(int64_t a, int64_t b, int g, int nx, int ny) {
+  const int64_t ntiles = (int64_t)nx * ny;
+  int64_t cost = 0;
+  while (a < b) {  // one split at a time
+    const int64_t z = a / ntiles, ts = a - z * ntiles;
+    const int64_t te = std::min(b, (z + 1) * ntiles) - z * ntiles;
+    int64_t cols = 0;
+    for (int64_t gi = ts / ((int64_t)g * nx); gi * g * nx < te; ++gi) {
+      const int64_t first = gi * g, hg = std::min<int64_t>(g, ny - first);
+      const int64_t gs = first * nx;
+      const int64_t la = std::max(ts, gs) - gs, lb = std::min(te, gs + hg * nx) - gs;
+      if (lb <= la) continue;
+      cost += std::min(hg, lb - la);
+      cols += (lb - 1) / hg - la / hg + 1;
+    }
+    cost += std::min<int64_t>(cols, nx);
+    a = (z + 1) * ntiles;
+  }
+  return cost;
+}
+
+// Group height for xcd_tile_order.  A candidate costs, for the worst XCD,
+// the panels its whole run touches (each read from HBM into that XCD's L2
+// once) plus the panels its first 64 tiles touch (roughly what it holds at
+// once: two workgroups on each of its 32 CUs), which must fit its L2
+// together with the output being written.  The cheapest candidate wins,
+// the smallest on ties.
+int xcd_group_rows_search(int nx, int ny, int nz) {
+  const int64_t total = (int64_t)nx * ny * nz;
+  const int64_t q = total / kXcds, r = total % kXcds;
+  int best = 1;
+  int64_t best_cost = -1;
+  for (int g = 1; g <= ny && g <= 256; ++g) {
+    int64_t worst = 0;
+    for (int x = 0; x < kXcds; ++x) {
+      const int64_t a = x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q;
+      const int64_t b = a + q + (x < r ? 1 : 0);
+      const int64_t cost = panels_touched(a, b, g, nx, ny) +
+                           panels_touched(a, std::min<int64_t>(b, a + 64), g, nx, ny);
+      worst = std::max(worst, cost);
+    }
+    if (best_cost < 0 || worst < best_cost) {
+      best_cost = worst;
+      best = g;
+    }
+  }
+  return best;
+}
+
+// The search above, remembered per grid shape (a layer launches the same
+// few shapes over and over; one small table per host thread).
+int xcd_group_rows(int nx, int ny, int nz) {
+  struct Entry { int nx, ny, nz, g; };
+  thread_local Entry cache[16];
+  thread_local int used = 0;
+  for (int i = 0; i < used && i < 16; ++i)
+    if (cache[i].nx == nx && cache[i].ny == ny && cache[i].nz == nz) return cache[i].g;
+  const int g = xcd_group_rows_search(nx, ny, nz);
+  cache[used % 16] = Entry{nx, ny, nz, g};
+  ++used;
+  return g;
+}
 
 template <typename T, bool AMC, bool BNC, int SEG, class Epi>
 hipError_t launch(const GemmDesc& g, const Epi& epi, hipStream_t s) {
@@ -795,8 +913,9 @@ hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   if (g.kchunk > 0) kchunk = g.kchunk;
   splits = (g.K + kchunk - 1) / kchunk;
   dim3 grid((g.N + PBN - 1) / PBN, (g.M + PBM - 1) / PBM, splits);
+  const int group = xcd_group_rows((int)grid.x, (int)grid.y, (int)grid.z);
   hipLaunchKernelGGL((gemm_pipe_kernel<PBM, PBN, PBK, ST, WGM, WGN, AMC, BNC, SEG, Epi>), grid,
-                     dim3(WGM * WGN * 64), 0, s, g.M, g.N, g.K, A, B, kchunk, epi);
+                     dim3(WGM * WGN * 64), 0, s, g.M, g.N, g.K, A, B, kchunk, group, epi);
   return hipGetLastError();
 }
 
@@ -836,12 +955,13 @@ hipError_t gemm_store(DType dt, const GemmDesc& g, void* C, int64_t ldc, bool c_
 
 namespace {
 
-// Split-K plan: about two workgroups per CU of 128 x 128 tiles, every split
+// Split-K plan: at most two workgroups per CU of 128 x 128 tiles (two fit in
+// LDS at once), so that the whole grid is resident in one round; every split
 // at least min_k deep in K (rounded to a multiple of 64).  Returns the number
 // of splits; *kchunk is the K range of each.
 static int splitk_plan(int M, int N, int K, int min_k, int* kchunk) {
   const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
-  int sp = (512 + tiles - 1) / tiles;
+  int sp = 512 / tiles;
   const int kmax = K / min_k;
   if (sp > kmax) sp = kmax;
   if (sp < 1) sp = 1;
