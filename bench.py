@@ -62,6 +62,9 @@ def stage_work(name, B, T, D, H, L, es):
     if name.endswith("_reduce"):
         return "hbm", 0, "byte"  # split-K reductions: size depends on the split plan
     act = BT * D * es
+    # dw_p partial rows: one per 8 * (16 / nvj) tokens of each block
+    nvj = next(n for n in (1, 2, 4, 8) if n * 64 >= D // (16 // es) or n == 8)
+    pool_rows = B * nb * -(-min(L, T) // (8 * (16 // nvj)))
     hbm = {
         "fwd.pool": act + BT * 4 + B * nb * D * 4 + B * nb * 8,
         # memory projection + scan: read S (float32 and compute type) and W_m,
@@ -70,7 +73,9 @@ def stage_work(name, B, T, D, H, L, es):
         "bwd.gate": 3 * act + B * nb * D * (4 + es),
         # read dP (compute type), W_m and M, write dS
         "bwd.memory_scan": B * nb * D * (es + 4 + 4) + D * D * es,
-        "bwd.pool": act + BT * 12 + B * nb * D * 8,
+        # read H, s, dS and S; write a, ds and the dw_p partial rows
+        "bwd.pool": act + BT * 12 + B * nb * D * 8 + pool_rows * D * 4,
+        "bwd.pool_dwp": pool_rows * D * 4,
         "bwd.zero_grads": (D + 1) * 4,
     }
     return "hbm", hbm.get(name, 0), "byte"

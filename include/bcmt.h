@@ -138,9 +138,9 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
  *   grads  float32 weight/decay gradients (overwritten, or accumulated
  *          with BCMT_FLAG_ACCUM_WGRAD); NULL, or NULL members, skip them.
  *   ws     at least bcmt_workspace_bytes(cfg, BCMT_PASS_BACKWARD) bytes.
- * The weight-matrix gradients are reduced deterministically; dwp and dgamma
- * are summed with float32 atomics, so those two may differ run to run in the
- * last bits. */
+ * The weight-matrix gradients and dwp are reduced in a fixed order
+ * (deterministic); dgamma is summed with float32 atomics, so it may differ
+ * run to run in the last bits. */
 int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* params,
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
                         void* ws, size_t ws_bytes, void* stream);

@@ -46,7 +46,7 @@ struct Plan {
   // forward scratch
   size_t sp, St, fwd_bytes;
   // backward scratch
-  size_t du, pbar, dS, a, ds, dh, dout, delta, dqkv, wpart, bwd_bytes;
+  size_t du, pbar, dS, a, ds, dwpp, dh, dout, delta, dqkv, wpart, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -88,6 +88,7 @@ struct Plan {
     dS = take(BND * 4);
     a = take(BT * 4);
     ds = take(BT * 4);
+    dwpp = take((size_t)pool_bwd_partial_rows(dt, B, T, D, L) * D * 4);
     dh = take(BTD * es);
     dout = take(BTD * es);
     delta = take((size_t)B * H * T * 4);
@@ -431,12 +432,11 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   } while (0)
 #define SIDE_END() (s = main_s)
   // Gate and injection: dU, and the block sums of dY * G shifted back by one.
-  // dwp and dgamma are reduced with atomics later in the pass; this kernel
-  // clears them first unless the gradients accumulate.  The weight matrices
-  // are written (or accumulated) by the split-K reductions.
+  // dgamma is reduced with atomics later in the pass; this kernel clears it
+  // first unless the gradients accumulate.  The weight matrices and dwp are
+  // written (or accumulated) by fixed-order reductions.
   LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                               accum ? nullptr : gr.dwp, D, accum ? nullptr : gr.dgamma, p.B,
-                               p.T, D, p.L, s));
+                               nullptr, 0, accum ? nullptr : gr.dgamma, p.B, p.T, D, p.L, s));
   // dWg = H^T dU and dWm = M^T dP on the side stream.
   if (gr.dWg || gr.dWm) {
     SIDE_BEGIN();
@@ -459,14 +459,15 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   // decay gradient, in one kernel.
   LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
                              gr.dgamma, p.B, p.nb, D, cfg->gamma, s));
-  // Pooling backward: per-token a_t and ds_t; dwp = sum_t ds_t H[t] on the
-  // side stream.
+  // Pooling backward: per-token a_t and ds_t, and partial sums of
+  // ds_t H[t]; dwp = their sum on the side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
                                (const float*)(SV + p.S), (const float*)(W + p.dS),
-                               (float*)(W + p.a), (float*)(W + p.ds), p.B, p.T, D, p.L, s));
+                               (float*)(W + p.a), (float*)(W + p.ds),
+                               gr.dwp ? (float*)(W + p.dwpp) : nullptr, p.B, p.T, D, p.L, s));
   if (gr.dwp) {
     SIDE_BEGIN();
-    LAUNCH(ST_DWP, pool_dwp(dt, SV + p.h, (const float*)(W + p.ds), gr.dwp, (int64_t)BT, D, s));
+    LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
     SIDE_END();
   }
   // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.

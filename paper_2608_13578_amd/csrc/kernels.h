@@ -133,13 +133,18 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
 // the decay gradient (atomically added to *dgamma when given).
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
                    float* dgamma, int B, int nb, int D, float gamma, hipStream_t s);
-// Pooling backward: per-token softmax weights a_t and score gradients ds_t.
+// Pooling backward: per-token softmax weights a_t and score gradients ds_t,
+// and (when dwp_part is not null) partial sums of ds_t H[t] over chunks of
+// tokens, one row of D floats per chunk.
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
-                    const float* S, const float* dS, float* a_out, float* ds_out, int B, int T,
-                    int D, int L, hipStream_t s);
-// dwp += sum over the ntok rows t of ds_t H[t] (atomic adds; dwp may be null).
-hipError_t pool_dwp(DType dt, const void* H, const float* ds, float* dwp, int64_t ntok, int D,
-                    hipStream_t s);
+                    const float* S, const float* dS, float* a_out, float* ds_out,
+                    float* dwp_part, int B, int T, int D, int L, hipStream_t s);
+// Rows of D floats the dwp_part workspace needs (partial sums and the
+// reduction's intermediate rows).
+int64_t pool_bwd_partial_rows(DType dt, int B, int T, int D, int L);
+// dwp = (or +=) the sum of the partial rows, in a fixed order.
+hipError_t pool_dwp(float* dwp_part, DType dt, int B, int T, int D, int L, float* dwp,
+                    bool accumulate, hipStream_t s);
 hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // Zeroes two small float32 buffers in one launch (either may be null).
 hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);

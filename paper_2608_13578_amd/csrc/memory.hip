@@ -387,112 +387,167 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
 // ------------------------------------------------------------------ pooling backward
 // With a_t the block softmax weights and dS_i the summary gradient:
 //   ds_t = a_t (dS_i . H[t] - dS_i . S_i),  dw_p = sum_t ds_t H[t].
-// pool_bwd_kernel writes the per-token a_t and ds_t (they feed the dH
-// epilogue of the W_g backward product); dwp_kernel then forms dw_p off the
-// critical path.  Workgroup = (chunk of tc tokens of block i, batch element).
+// Workgroup = (chunk of 8 * TB tokens of block i, batch element), 8 waves;
+// each wave requests its TB rows (NVJ 16-byte vectors per lane) at once,
+// forms their dot products with dS_i, writes a_t and ds_t (they feed the dH
+// epilogue of the W_g backward product) and keeps sum ds_t H[t] over its
+// rows in registers.  The waves' sums meet in LDS in a fixed order and the
+// chunk's sum becomes one row of dwp_part; colsum_kernel adds the rows, so
+// dw_p needs no atomics and comes out the same on every run.
+template <int NVJ> struct PoolRows { static constexpr int TB = 16 / NVJ; };
+constexpr int kPoolWaves = 8;
+
 template <typename T, int NVJ>
-__global__ __launch_bounds__(1024) void pool_bwd_kernel(
+__global__ __launch_bounds__(kPoolWaves * 64) void pool_bwd_kernel(
     const T* __restrict__ H, const float* __restrict__ s_in, const float* __restrict__ stats,
     const float* __restrict__ S, const float* __restrict__ dS, float* __restrict__ a_out,
-    float* __restrict__ ds_out, int Tn, int D, int L, int nb, int tc, int nch) {
+    float* __restrict__ ds_out, float* __restrict__ dwp_part, int Tn, int D, int L, int nb,
+    int nch) {
   constexpr int VE = Vec16<T>::N;
-  constexpr int TB = TokBatch<NVJ>::TB;
+  constexpr int TB = PoolRows<NVJ>::TB;
+  constexpr int ROW = NVJ * 64 * VE;  // columns one wave covers
   typedef typename Vec16<T>::type vec;
-  const int nw = blockDim.x >> 6;
+  __shared__ float red[kPoolWaves / 2][ROW];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = blockIdx.x / nch, b = blockIdx.y;
-  const int bs = i * L + (blockIdx.x % nch) * tc;
-  const int be = min(min(i * L + L, Tn), bs + tc);
+  const int i = blockIdx.x / nch, ch = blockIdx.x % nch, b = blockIdx.y;
+  const int bend = min(i * L + L, Tn);
+  const int t0 = i * L + ch * (kPoolWaves * TB) + wave * TB;  // this wave's first row
   const int Dv = D / VE;
   const int64_t brow = (int64_t)(b * nb + i) * D;
 
+  // This wave's rows first: nothing else decides their addresses.
+  vec x[TB][NVJ];
+  float sv[TB];
+#pragma unroll
+  for (int k = 0; k < TB; ++k) {
+    const bool tok = t0 + k < bend;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j) {
+      const int v = lane + 64 * j;
+      x[k][j] = tok && v < Dv ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE) : vec{};
+    }
+    sv[k] = tok ? s_in[(int64_t)b * Tn + t0 + k] : 0.f;
+  }
   float g[NVJ][VE];
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < NVJ; ++j) {
     const int v = lane + 64 * j;
+    if (v < Dv) {
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      const bool ok = v < Dv;
-      g[j][e] = ok ? dS[brow + v * VE + e] : 0.f;
-      ss += ok ? g[j][e] * S[brow + v * VE + e] : 0.f;
+      for (int q = 0; q < VE / 4; ++q) {
+        const f32x4 dv = *reinterpret_cast<const f32x4*>(dS + brow + v * VE + q * 4);
+        const f32x4 sw = *reinterpret_cast<const f32x4*>(S + brow + v * VE + q * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          g[j][q * 4 + r] = dv[r];
+          ss += dv[r] * sw[r];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) g[j][e] = 0.f;
     }
   }
   ss = wave_sum(ss);
   const float mi = stats[(int64_t)(b * nb + i) * 2];
   const float li = stats[(int64_t)(b * nb + i) * 2 + 1];
-  for (int t0 = bs + wave * TB; t0 < be; t0 += nw * TB) {
-    vec x[TB][NVJ];
+
+  float pw[NVJ][VE];
 #pragma unroll
-    for (int k = 0; k < TB; ++k)
+  for (int j = 0; j < NVJ; ++j)
 #pragma unroll
-      for (int j = 0; j < NVJ; ++j) {
-        const int v = lane + 64 * j;
-        x[k][j] = (t0 + k < be && v < Dv) ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE)
-                                          : vec{};
-      }
+    for (int e = 0; e < VE; ++e) pw[j][e] = 0.f;
 #pragma unroll
-    for (int k = 0; k < TB; ++k) {
-      float d = 0.f;
+  for (int k = 0; k < TB; ++k) {
+    float d = 0.f;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) d += g[j][e] * to_f32(x[k][j][e]);
+    d = wave_sum(d);
+    const int t = t0 + k;
+    const float a = __expf(sv[k] - mi) / li;
+    const float ds = t < bend ? a * (d - ss) : 0.f;
+    if (t < bend && lane == 0) {
+      const int64_t ti = (int64_t)b * Tn + t;
+      a_out[ti] = a;
+      ds_out[ti] = ds;
+    }
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) pw[j][e] += ds * to_f32(x[k][j][e]);
+  }
+  if (!dwp_part) return;  // (uniform over the workgroup)
+
+  // Pairwise tree over the waves: w += w + half, half = 4, 2, 1.
+#pragma unroll
+  for (int half = kPoolWaves / 2; half >= 1; half >>= 1) {
+    if (wave >= half && wave < 2 * half) {
 #pragma unroll
       for (int j = 0; j < NVJ; ++j)
 #pragma unroll
-        for (int e = 0; e < VE; ++e) d += g[j][e] * to_f32(x[k][j][e]);
-      d = wave_sum(d);
-      const int t = t0 + k;
-      if (t < be && lane == 0) {
-        const int64_t ti = (int64_t)b * Tn + t;
-        const float a = __expf(s_in[ti] - mi) / li;
-        a_out[ti] = a;
-        ds_out[ti] = a * (d - ss);
+        for (int e = 0; e < VE; ++e) red[wave - half][(lane + 64 * j) * VE + e] = pw[j][e];
+    }
+    __syncthreads();
+    if (wave < half) {
+#pragma unroll
+      for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) pw[j][e] += red[wave][(lane + 64 * j) * VE + e];
+    }
+    __syncthreads();
+  }
+  if (wave == 0) {
+    float* row = dwp_part + ((int64_t)(b * nb + i) * nch + ch) * D;
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j) {
+      const int v = lane + 64 * j;
+      if (v < Dv) {
+#pragma unroll
+        for (int q = 0; q < VE / 4; ++q)
+          *reinterpret_cast<f32x4*>(row + v * VE + q * 4) =
+              f32x4{pw[j][q * 4], pw[j][q * 4 + 1], pw[j][q * 4 + 2], pw[j][q * 4 + 3]};
       }
     }
   }
 }
 
-// dw_p += sum_t ds_t H[t] over a range of tokens, in the column-chunk layout
-// (workgroup = (column chunk, token range)); one atomic add per column.
-template <typename T>
-__global__ __launch_bounds__(256) void dwp_kernel(const T* __restrict__ H,
-                                                  const float* __restrict__ ds,
-                                                  float* __restrict__ dwp, int64_t ntok, int D,
-                                                  int64_t per) {
-  constexpr int VE = Vec16<T>::N;
-  constexpr int U = 4;
-  typedef typename Vec16<T>::type vec;
-  __shared__ float racc[kTg][kVec * VE];
-  const int tid = threadIdx.x;
-  const int v = tid % kVec, tg = tid / kVec;
-  const int c0 = blockIdx.x * kVec * VE;
-  const int col = c0 + v * VE;
-  const int64_t t_beg = (int64_t)blockIdx.y * per;
-  const int64_t t_end = t_beg + per < ntok ? t_beg + per : ntok;
-  float acc[VE];
-#pragma unroll
-  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
-  if (col < D) {
-    for (int64_t t0 = t_beg + tg; t0 < t_end; t0 += U * kTg) {
-      vec h[U];
-      float w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t t = t0 + u * kTg;
-        h[u] = t < t_end ? load16(H + t * D + col) : vec{};
-        w[u] = t < t_end ? ds[t] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int e = 0; e < VE; ++e) acc[e] += w[u] * to_f32(h[u][e]);
+// out[c] = sum over rows r < R of P[r][c] for 64 columns per workgroup and
+// up to kColRows rows per workgroup (blockIdx.y): thread (vector v, row
+// group rg) adds rows rg, rg + 16, ... of its four columns, and the 16 row
+// groups meet in LDS in a fixed order.  With more than one row range
+// (gridDim.y > 1) each range writes its own row of `out` (stride N), which a
+// second pass adds up.
+constexpr int kColRows = 256;
+__global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ P, int64_t R, int N,
+                                                     float* __restrict__ out, int accumulate) {
+  __shared__ f32x4 red[16][16];
+  const int v = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int c = blockIdx.x * 64 + v * 4;
+  const int64_t r0 = (int64_t)blockIdx.y * kColRows;
+  const int64_t r1 = r0 + kColRows < R ? r0 + kColRows : R;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (c < N) {
+    int64_t r = r0 + rg;
+    for (; r + 48 < r1; r += 64) {
+      const f32x4 a0 = *reinterpret_cast<const f32x4*>(P + r * N + c);
+      const f32x4 a1 = *reinterpret_cast<const f32x4*>(P + (r + 16) * N + c);
+      const f32x4 a2 = *reinterpret_cast<const f32x4*>(P + (r + 32) * N + c);
+      const f32x4 a3 = *reinterpret_cast<const f32x4*>(P + (r + 48) * N + c);
+      acc += (a0 + a1) + (a2 + a3);
     }
+    for (; r < r1; r += 16) acc += *reinterpret_cast<const f32x4*>(P + r * N + c);
   }
-#pragma unroll
-  for (int e = 0; e < VE; ++e) racc[tg][v * VE + e] = acc[e];
+  red[rg][v] = acc;
   __syncthreads();
-  if (tid < kVec * VE && c0 + tid < D) {
-    float sum = 0.f;
-    for (int k = 0; k < kTg; ++k) sum += racc[k][tid];
-    unsafeAtomicAdd(dwp + c0 + tid, sum);
+  if (rg == 0 && c < N) {
+    f32x4 sum = red[0][v];
+    for (int k = 1; k < 16; ++k) sum += red[k][v];
+    f32x4* dst = reinterpret_cast<f32x4*>(out + (int64_t)blockIdx.y * N + c);
+    if (accumulate) sum += *dst;
+    *dst = sum;
   }
 }
 
@@ -518,18 +573,6 @@ int nvj_for(int Dv) {
   return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : 8;
 }
 
-// Waves per pooling-backward workgroup: enough to give every wave one token
-// batch of the chunk, at most 16, and few enough that the per-wave row sums
-// fit in 64 KB of LDS.
-template <int NVJ>
-int pool_waves(int tc, int D) {
-  const int tb = TokBatch<NVJ>::TB;
-  int w = (tc + tb - 1) / tb;
-  const int wmax = (65536 - 256) / (4 * D + 8);
-  if (w > wmax) w = wmax;
-  return w < 1 ? 1 : (w > 16 ? 16 : w);
-}
-
 template <typename E>
 hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, float* S, void* St,
                       float* stats, int B, int T, int D, int L, hipStream_t s) {
@@ -540,43 +583,37 @@ hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, floa
   return hipGetLastError();
 }
 
+// Tokens per pooling-backward workgroup and workgroups per block.
+template <typename E>
+void pool_bwd_shape(int D, int L, int T, int* tc, int* nch) {
+  const int nv = nvj_for(D / Vec16<E>::N);
+  *tc = kPoolWaves * (16 / nv);
+  const int lb = L < T ? L : T;
+  *nch = (lb + *tc - 1) / *tc;
+}
+
 template <typename E, int NV>
 hipError_t pool_bwd_nv(const void* H, const float* s_in, const float* stats, const float* S,
-                       const float* dS, float* a_out, float* ds_out, int B, int T, int D, int L,
-                       hipStream_t s) {
+                       const float* dS, float* a_out, float* ds_out, float* dwp_part, int B,
+                       int T, int D, int L, hipStream_t s) {
   const int nb = (T + L - 1) / L;
-  const int lb = L < T ? L : T;
-  const int tc = lb < 32 ? lb : 32;  // tokens per workgroup
-  const int nch = (lb + tc - 1) / tc;
-  const int nw = pool_waves<NV>(tc, D);
-  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb * nch, B), dim3(nw * 64), 0, s,
-                     (const E*)H, s_in, stats, S, dS, a_out, ds_out, T, D, L, nb, tc, nch);
+  int tc, nch;
+  pool_bwd_shape<E>(D, L, T, &tc, &nch);
+  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb * nch, B), dim3(kPoolWaves * 64), 0, s,
+                     (const E*)H, s_in, stats, S, dS, a_out, ds_out, dwp_part, T, D, L, nb, nch);
   return hipGetLastError();
 }
 
 template <typename E>
 hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, const float* S,
-                      const float* dS, float* a_out, float* ds_out, int B, int T, int D, int L,
-                      hipStream_t s) {
+                      const float* dS, float* a_out, float* ds_out, float* dwp_part, int B, int T,
+                      int D, int L, hipStream_t s) {
   switch (nvj_for(D / Vec16<E>::N)) {
-    case 1: return pool_bwd_nv<E, 1>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
-    case 2: return pool_bwd_nv<E, 2>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
-    case 4: return pool_bwd_nv<E, 4>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
-    default: return pool_bwd_nv<E, 8>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+    case 1: return pool_bwd_nv<E, 1>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
+    case 2: return pool_bwd_nv<E, 2>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
+    case 4: return pool_bwd_nv<E, 4>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
+    default: return pool_bwd_nv<E, 8>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
   }
-}
-
-template <typename E>
-hipError_t dwp_t(const void* H, const float* ds, float* dwp, int64_t ntok, int D, hipStream_t s) {
-  const int cw = kVec * Vec16<E>::N;
-  // about 128 tokens per workgroup, at most 256 token ranges
-  int64_t ranges = (ntok + 127) / 128;
-  if (ranges > 256) ranges = 256;
-  if (ranges < 1) ranges = 1;
-  const int64_t per = (ntok + ranges - 1) / ranges;
-  hipLaunchKernelGGL(dwp_kernel<E>, dim3((D + cw - 1) / cw, (unsigned)ranges), dim3(kVec * kTg), 0,
-                     s, (const E*)H, ds, dwp, ntok, D, per);
-  return hipGetLastError();
 }
 
 template <typename E>
@@ -640,18 +677,48 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, f
 }
 
 hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* stats,
-                    const float* S, const float* dS, float* a_out, float* ds_out, int B, int T,
-                    int D, int L, hipStream_t s) {
+                    const float* S, const float* dS, float* a_out, float* ds_out,
+                    float* dwp_part, int B, int T, int D, int L, hipStream_t s) {
   if (dt == DType::BF16)
-    return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
-  return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, B, T, D, L, s);
+    return pool_bwd_t<bf16>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
+  return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
 }
 
-hipError_t pool_dwp(DType dt, const void* H, const float* ds, float* dwp, int64_t ntok, int D,
-                    hipStream_t s) {
-  if (!dwp || ntok <= 0) return hipSuccess;
-  if (dt == DType::BF16) return dwp_t<bf16>(H, ds, dwp, ntok, D, s);
-  return dwp_t<float>(H, ds, dwp, ntok, D, s);
+// Rows of dw_p partial sums the pooling backward writes.
+int64_t pool_rows(DType dt, int B, int T, int D, int L) {
+  int tc, nch;
+  if (dt == DType::BF16) pool_bwd_shape<bf16>(D, L, T, &tc, &nch);
+  else pool_bwd_shape<float>(D, L, T, &tc, &nch);
+  return (int64_t)B * ((T + L - 1) / L) * nch;
+}
+
+int64_t pool_bwd_partial_rows(DType dt, int B, int T, int D, int L) {
+  int64_t r = pool_rows(dt, B, T, D, L), all = r;
+  while (r > 1) {  // the reduction's intermediate rows
+    r = (r + kColRows - 1) / kColRows;
+    all += r;
+  }
+  return all;
+}
+
+hipError_t pool_dwp(float* dwp_part, DType dt, int B, int T, int D, int L, float* dwp,
+                    bool accumulate, hipStream_t s) {
+  if (!dwp) return hipSuccess;
+  int64_t R = pool_rows(dt, B, T, D, L);
+  float* in = dwp_part;
+  // Each pass folds kColRows rows into one, in a fixed order.
+  while (R > kColRows) {
+    const int64_t ranges = (R + kColRows - 1) / kColRows;
+    if (ranges > 65535) return hipErrorInvalidValue;
+    float* out = in + R * D;
+    hipLaunchKernelGGL(colsum_kernel, dim3((D + 63) / 64, (unsigned)ranges), dim3(256), 0, s,
+                       (const float*)in, R, D, out, 0);
+    in = out;
+    R = ranges;
+  }
+  hipLaunchKernelGGL(colsum_kernel, dim3((D + 63) / 64, 1), dim3(256), 0, s, (const float*)in, R,
+                     D, dwp, accumulate ? 1 : 0);
+  return hipGetLastError();
 }
 
 hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {

@@ -111,6 +111,8 @@ CASES = [
     ("bf16-ragged-T1000", 1, 1000, 256, 4, 128, "bf16", 1.0, 2 / np.sqrt(256), 0.8, False),
     ("bf16-L1024-dense", 1, 1024, 256, 4, 1024, "bf16", 1.0, 0.02, 0.8, False),
     ("bf16-L256", 2, 1024, 256, 4, 256, "bf16", 1.0, 0.02, 0.8, True),
+    # 1024 blocks: the w_p gradient's partial rows take two reduction passes
+    ("f32-many-blocks-L8", 2, 4096, 128, 2, 8, "f32", 1.0, 0.05, 0.8, False),
 ]
 
 
