@@ -473,7 +473,7 @@ __device__ __forceinline__ void sync_lds() {
 }
 
 template <int NW>
-__global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __restrict__ qkv,
+__global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* __restrict__ qkv,
                                                                bf16* __restrict__ out,
                                                                float* __restrict__ lse, int Tn,
                                                                int D, int H, int L, float sl2) {
@@ -525,31 +525,36 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __re
     const int kt = bs + it * 64;
     const bf16* Kt = lds[it & 1][0];
     const bf16* Vt = lds[it & 1][1];
-    bf16x8 kf[4][2], vf[4][2];
-#pragma unroll
-    for (int ku = 0; ku < 4; ++ku)
-#pragma unroll
-      for (int ds = 0; ds < 2; ++ds) kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int us = 0; us < 2; ++us) vf[j][us] = tcol8p(Vt, us * 32, j, lane);
-    lds_tr_wait();
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int us = 0; us < 2; ++us) lds_tr_bind(vf[j][us]);
+    // Scores of both query groups first (the key fragments are dead after
+    // that), then the softmax update, then the value fragments and P V: at
+    // most one of the two fragment sets is live at a time.  (Every wave
+    // still reaches the barriers below.)
+    bool live[2];
 #pragma unroll
     for (int nq = 0; nq < 2; ++nq) {
       const int tq = tw0 + nq * 16;
-      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
-      f32x4 s[4];
+      live[nq] = !(tq >= be || tq + 15 < kt);  // wave-uniform
+    }
+    f32x4 s[2][4];
+    if (live[0] || live[1]) {
+      bf16x8 kf[4][2];
 #pragma unroll
-      for (int ku = 0; ku < 4; ++ku) {
-        s[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
-        for (int ds = 0; ds < 2; ++ds) s[ku] = mma16(kf[ku][ds], qf[nq][ds], s[ku]);
-      }
+        for (int ds = 0; ds < 2; ++ds) kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
+#pragma unroll
+      for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+        for (int ku = 0; ku < 4; ++ku) {
+          s[nq][ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ds = 0; ds < 2; ++ds) s[nq][ku] = mma16(kf[ku][ds], qf[nq][ds], s[nq][ku]);
+        }
+    }
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      if (!live[nq]) continue;
+      const int tq = tw0 + nq * 16;
       const int t_eff = min(tq + lr, be - 1);
       float mx = -INFINITY;
 #pragma unroll
@@ -557,8 +562,8 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __re
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int u = kt + ku * 16 + lg * 4 + r;
-          const float z = u <= t_eff ? s[ku][r] * sl2 : -INFINITY;
-          s[ku][r] = z;
+          const float z = u <= t_eff ? s[nq][ku][r] * sl2 : -INFINITY;
+          s[nq][ku][r] = z;
           mx = fmaxf(mx, z);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
@@ -570,19 +575,35 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_bf16_kernel(const bf16* __re
       for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float pv = exp2f(s[ku][r] - mnew);
-          s[ku][r] = pv;
+          const float pv = exp2f(s[nq][ku][r] - mnew);
+          s[nq][ku][r] = pv;
           ps += pv;
         }
       l[nq] = l[nq] * alpha + ps;
       m[nq] = mnew;
 #pragma unroll
       for (int j = 0; j < 4; ++j) o[nq][j] *= alpha;
+    }
+    if (live[0] || live[1]) {
+      bf16x8 vf[4][2];
 #pragma unroll
-      for (int us = 0; us < 2; ++us) {
-        const bf16x8 pf = frag_from<bf16>(s[2 * us], s[2 * us + 1]);
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[nq][j] = mma16(vf[j][us], pf, o[nq][j]);
+        for (int us = 0; us < 2; ++us) vf[j][us] = tcol8p(Vt, us * 32, j, lane);
+      lds_tr_wait();
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int us = 0; us < 2; ++us) lds_tr_bind(vf[j][us]);
+#pragma unroll
+      for (int nq = 0; nq < 2; ++nq) {
+        if (!live[nq]) continue;
+#pragma unroll
+        for (int us = 0; us < 2; ++us) {
+          const bf16x8 pf = frag_from<bf16>(s[nq][2 * us], s[nq][2 * us + 1]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[nq][j] = mma16(vf[j][us], pf, o[nq][j]);
+        }
       }
     }
     if (it + 2 < nt) {
