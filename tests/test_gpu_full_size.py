@@ -1,0 +1,131 @@
+"""Parity at the full sizes of the measured workloads, on sampled outputs.
+
+Sequences are independent and the layer is causal (Sec. 3.6), so the
+outputs of a token prefix of chosen sequences depend on that region of the
+input alone.  The HIP path runs the full-size launch (the configuration the
+benchmark times, or the larger long-context and block-size ones); the
+upstream gradient is zero outside the sampled region; the float64 oracle runs
+the region alone.  Then Y and dX agree on the region, dX is exactly zero
+outside it, and every weight, w_p and decay gradient equals the region's.
+Tolerances as in test_gpu_parity: max-abs-rel <= 2e-2 in bf16.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+
+from conftest import maxabs_rel
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-2
+# The 12-layer stack stores every layer's output and input gradient in bf16.
+# A float64 model of the stack that rounds only those tensors to bf16 (CPU,
+# same inputs) already misses the exact stack by up to 2.1e-2 on dw_p over
+# two blocks and 1.3e-2 over a whole sequence: dw_p is a covariance of s̄_t
+# and H[t] over the block, so it cancels heavily.  dw_p of the stack gets
+# 5e-2; everything else keeps 2e-2.
+TOL_STACK_DWP = 5e-2
+GRADS = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp")
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "no GPU visible"
+    from paper_2608_13578_amd import bcmt as abi
+    abi.lib()
+    return torch
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def sampled_case(torch, label, B, T, D, H, L, rows, P, n_layers=1, residual=False, gamma=0.8):
+    from oracle import bcmt_oracle as orc
+    from paper_2608_13578_amd.inputs import make_layer_inputs, make_upstream_grad, to_f64
+    from paper_2608_13578_amd.layer import LayerBuffers, to_device, to_host64
+    say(f"case {label}: B={B} T={T} D={D} H={H} L={L} layers={n_layers} "
+        f"sampled sequences {rows}, tokens < {P}")
+    X, Ws = make_layer_inputs(B, T, D, seed=0, x_std=1.0, w_std=0.02, bf16=True,
+                              n_layers=n_layers)
+    dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
+    keep = np.zeros((B, T, 1), dtype=np.float32)
+    keep[rows, :P] = 1.0
+    dY = dY * keep
+
+    # full-size launch on the GPU: forward through the stack, then backward
+    layers = []
+    xs = [to_device(X, "bf16")]
+    for W in Ws:
+        lb = LayerBuffers(B, T, D, H, L, gamma=gamma, dtype="bf16", residual=residual)
+        lb.set_params(W)
+        y = lb.new_activation()
+        lb.forward(xs[-1], y)
+        layers.append(lb)
+        xs.append(y)
+    g = to_device(dY, "bf16")
+    grads = [None] * n_layers
+    for li in reversed(range(n_layers)):
+        lb = layers[li]
+        dx = lb.new_activation()
+        gr = lb.new_grads()
+        lb.backward(xs[li], g, dx, gr)
+        grads[li] = gr
+        g = dx
+    torch.cuda.synchronize()
+    Y = to_host64(xs[-1])
+    dX = to_host64(g)
+    say(f"[{label}] GPU pass done")
+
+    # the oracle on the sampled region alone
+    Xr = X[rows, :P].astype(np.float64)
+    dYr = dY[rows, :P].astype(np.float64)
+    Wr = [to_f64(W) for W in Ws]
+    if n_layers == 1:
+        Yr, cache = orc.forward(Xr, Wr[0], L, H, gamma, residual)
+        gr_ref = [orc.backward(cache, dYr)]
+        dXr = gr_ref[0]["dX"]
+    else:
+        Yr, caches = orc.stack_forward(Xr, Wr, L, H, gamma, residual)
+        dXr, gr_ref = orc.stack_backward(caches, dYr)
+
+    errs = {"Y": maxabs_rel(Y[rows, :P], Yr), "dX": maxabs_rel(dX[rows, :P], dXr)}
+    outside = dX.copy()
+    outside[rows, :P] = 0.0
+    assert not np.any(outside), f"{label}: dX nonzero outside the sampled region"
+    for li in range(n_layers):
+        for k in GRADS:
+            errs[f"{k}[{li}]"] = maxabs_rel(to_host64(grads[li][k]), gr_ref[li][k])
+        dg = float(grads[li]["dgamma"][0].item())
+        ref = gr_ref[li]["dgamma"]
+        errs[f"dgamma[{li}]"] = abs(dg - ref) / max(abs(ref), 1e-30)
+    worst = max(errs, key=errs.get)
+    say(f"[{label}] worst {worst}={errs[worst]:.2e}; Y={errs['Y']:.2e} dX={errs['dX']:.2e}")
+    def tol(k):
+        return TOL_STACK_DWP if (n_layers > 1 and k.startswith("dwp")) else TOL_BF16
+    bad = {k: e for k, e in errs.items() if not (e <= tol(k))}
+    assert not bad, f"{label}: above tolerance: {bad}"
+
+
+@pytest.mark.parametrize("L", [32, 64, 128, 256, 1024])
+def test_block_size_sweep(torch_cuda, L):
+    """B=16, T=1024, D=768, H=12, bf16; sequences 0 and 15 checked whole."""
+    sampled_case(torch_cuda, f"sweep-L{L}", 16, 1024, 768, 12, L, rows=[0, 15], P=1024)
+
+
+@pytest.mark.parametrize("T,rows,P", [(4096, [0], 4096), (16384, [0, 1], 1024),
+                                      (65536, [0, 1], 1024)])
+def test_long_context(torch_cuda, T, rows, P):
+    """B=2, D=1024, H=16, L=256, bf16, T up to 65536 (256 blocks)."""
+    sampled_case(torch_cuda, f"long-T{T}", 2, T, 1024, 16, 256, rows=rows, P=P)
+
+
+def test_twelve_layer_stack(torch_cuda):
+    """Forward + backward of 12 residual layers at B=8, T=1024, D=768, H=12,
+    L=128, bf16; sequence 3 checked whole."""
+    sampled_case(torch_cuda, "stack-12", 8, 1024, 768, 12, 128, rows=[3], P=1024, n_layers=12,
+                 residual=True)
