@@ -154,12 +154,69 @@ def cpu_baseline(seconds_target=12.0):
                       f"H={w['H']}, L={w['L']}), float64 forward+backward, {t:.1f} s"}
 
 
+# Long-context shape for the bandwidth-bound kernels: at the measured layer
+# they move 13-40 MB per launch, too little for a bandwidth figure to mean
+# much beside launch latency; here each moves 16x more.
+LONG = {"B": 2, "T": 65536, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}
+
+
+def long_context(make_step, torch, abi, dt, steps=10, warmup=3):
+    """Layer throughput at the long-context shape and, per bandwidth-bound
+    stage (and the attention kernels), bytes moved / stage time against the
+    HBM peak.  Stage times come from the library's per-stage tracer (every
+    stage alone on one stream)."""
+    g = LONG
+    B, T, D, H, L = g["B"], g["T"], g["D"], g["H"], g["L"]
+    es = 2 if dt == "bf16" else 4
+    step, keep = make_step(B, T, D, H, L, g["gamma"])
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    stages = abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(False)
+    act = B * T * D * es
+    # attention: Q, K, V read and O written (forward); the fused backward
+    # reads Q, K, V, O, dO and writes dQ, dK, dV; the two-kernel backward
+    # (blocks over 128 tokens) reads Q, K, V, O, dO and writes dQ, then reads
+    # Q, K, V, dO and writes dK, dV
+    attn_bytes = {"fwd.attention": 4 * act, "bwd.attention_block": 8 * act,
+                  "bwd.attention_dq": 6 * act, "bwd.attention_dkdv": 6 * act}
+    res = {}
+    for name, calls, total in stages:
+        bound, amount, unit = stage_work(name, B, T, D, H, L, es)
+        if name in attn_bytes:
+            amount, bound = attn_bytes[name], "hbm"
+        if bound != "hbm" or amount <= 0:
+            continue
+        avg_s = total / calls / 1e3
+        gbs = amount / avg_s / 1e9
+        res[name] = {"us": round(avg_s * 1e6, 1), "bytes": amount, "GB/s": round(gbs, 1),
+                     "frac": round(gbs / PEAK["hbm_gbs"], 3)}
+    return {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} {dt}",
+            "tokens_per_s": round(B * T / (ms / 1e3), 1), "ms_per_step": round(ms, 3),
+            "hbm_stages": res}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-long-context", action="store_true",
+                    help="skip the long-context pass (bandwidth kernels at T=65536)")
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
                          "library's stage tracing on (every stage serialised on one stream, "
@@ -183,18 +240,23 @@ def main():
     B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
     dt = w["dtype"]
     torch.cuda.set_device(0)
-    X, [W] = make_layer_inputs(B, T, D, seed=0, bf16=True)
-    dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
-    lb = LayerBuffers(B, T, D, H, L, gamma=w["gamma"], dtype=dt)
-    lb.set_params(W)
-    Xd, dYd = to_device(X, dt), to_device(dY, dt)
-    Yd, dXd = lb.new_activation(), lb.new_activation()
-    grads = lb.new_grads()
 
-    def step():
-        lb.forward(Xd, Yd)
-        lb.backward(Xd, dYd, dXd, grads)
+    def make_step(B, T, D, H, L, gamma):
+        X, [W] = make_layer_inputs(B, T, D, seed=0, bf16=True)
+        dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
+        lb = LayerBuffers(B, T, D, H, L, gamma=gamma, dtype=dt)
+        lb.set_params(W)
+        Xd, dYd = to_device(X, dt), to_device(dY, dt)
+        del X, dY
+        Yd, dXd = lb.new_activation(), lb.new_activation()
+        grads = lb.new_grads()
 
+        def step():
+            lb.forward(Xd, Yd)
+            lb.backward(Xd, dYd, dXd, grads)
+        return step, (lb, Xd, dYd, Yd, dXd, grads)
+
+    step, keep = make_step(B, T, D, H, L, w["gamma"])
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -274,6 +336,10 @@ def main():
         "layer_mfma_frac": round(fl / (ms / 1e3) / 1e12 / PEAK["mfma_bf16_tflops"], 4),
         "roofline": roof,
     }
+    if not args.no_long_context:
+        del keep, step
+        torch.cuda.empty_cache()
+        out["long_context"] = long_context(make_step, torch, abi, dt)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)
