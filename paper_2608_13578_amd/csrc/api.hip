@@ -44,9 +44,9 @@ struct Plan {
   // saved (forward -> backward)
   size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
   // forward scratch
-  size_t sp, St, fwd_bytes;
+  size_t sp, St, mpart, fwd_bytes;
   // backward scratch
-  size_t du, pbar, dS, a, ds, dwpp, dh, dout, delta, dqkv, wpart, bwd_bytes;
+  size_t du, pbar, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart, bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -80,12 +80,15 @@ struct Plan {
     off = 0;
     sp = take(BT * (D / kDh) * 4);  // partial pooling scores, D / 64 per token
     St = take(BND * es);
+    mpart = take(mem_part_bytes(B, nb, D));  // W_m product partials (long sequences)
     fwd_bytes = off;
 
     off = 0;
     du = take(BTD * es);
     pbar = take(BND * es);
     dS = take(BND * 4);
+    dM = take(mem_fused(nb) ? 0 : BND * 4);
+    mpart_b = take(mem_part_bytes(B, nb, D));
     a = take(BT * 4);
     ds = take(BT * 4);
     dwpp = take((size_t)pool_bwd_partial_rows(dt, B, T, D, L) * D * 4);
@@ -370,7 +373,8 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
   // and Q, which yields M and P = M Wm (the decayed sum is linear); the
   // shift is applied where P is read.
   LAUNCH(ST_SCAN_FWD, mem_fwd(dt, W + p.St, prm->Wm, (const float*)(SV + p.S), (float*)(SV + p.M),
-                              SV + p.Mt, (float*)(SV + p.P), p.B, p.nb, D, cfg->gamma, s));
+                              SV + p.Mt, (float*)(SV + p.P), (float*)(W + p.mpart), p.B, p.nb, D,
+                              cfg->gamma, s));
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
     GemmDesc g{BT, D, D, SV + p.h, D, false, {prm->Wg, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -458,7 +462,8 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   // Memory projection and decayed reverse scan: dM = dP Wm^T, dS and the
   // decay gradient, in one kernel.
   LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
-                             gr.dgamma, p.B, p.nb, D, cfg->gamma, s));
+                             gr.dgamma, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
+                             cfg->gamma, s));
   // Pooling backward: per-token a_t and ds_t, and partial sums of
   // ds_t H[t]; dwp = their sum on the side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),

@@ -121,18 +121,26 @@ hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void
 // type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
 hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
                     void* St, float* stats, int B, int T, int D, int L, hipStream_t s);
-// Memory forward: Q = St Wm (St = S in the compute type, [B*nb, D]) and the
-// decayed scans of S and Q: M (float32), Mt (compute type) and P = M Wm.
+// Memory forward: M (float32), Mt (compute type) and P = M Wm from S.  Up
+// to a few dozen blocks per sequence one kernel does it all (Q = St Wm with
+// St = S in the compute type, [B*nb, D], and the decayed scans of S and Q);
+// for longer sequences a parallel scan gives M and a split-K product P,
+// using `part` (mem_part_bytes bytes; may be null when that is 0).
+bool mem_fused(int nb);
+size_t mem_part_bytes(int B, int nb, int D);
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
-                   float* P, int B, int nb, int D, float gamma, hipStream_t s);
+                   float* P, float* part, int B, int nb, int D, float gamma, hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
                     hipStream_t s);
 // Memory backward: dM = Pbar Wm^T, then the reverse decayed scan: dS and
-// the decay gradient (atomically added to *dgamma when given).
+// the decay gradient (atomically added to *dgamma when given).  For long
+// sequences (see mem_fwd) dM goes through `dM` ([B*nb, D] float32) and a
+// split-K product using `part`; both may be null for short ones.
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
-                   float* dgamma, int B, int nb, int D, float gamma, hipStream_t s);
+                   float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
+                   hipStream_t s);
 // Pooling backward: per-token softmax weights a_t and score gradients ds_t,
 // and (when dwp_part is not null) partial sums of ds_t H[t] over chunks of
 // tokens, one row of D floats per chunk.

@@ -301,6 +301,161 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
   }
 }
 
+// ------------------------------------------------------------------ long scans
+// For many blocks the memory path runs as two pieces: the decayed scans
+// below (parallel over blocks) and the W_m products as ordinary matrix
+// products (memscan_kernel walks all blocks of a sequence inside one
+// workgroup, which serialises a long sequence).
+//
+// Workgroup = (16 columns, sequence), thread = (column, chunk of 16
+// blocks), 16 chunks per pass of 256 blocks.  Each thread scans its chunk
+// with a zero carry, the chunk ends meet in LDS, each thread folds the
+// chunks before (after, for the reverse scan) into its carry, and applies
+// it: with the recurrence x_i = g x_{i-1} + y_i, the true value is the local
+// one plus g^(distance) times the carry.  A pass hands its end carry to the
+// next one.
+constexpr int kScCols = 16, kScChunks = 16, kScRows = 16;
+// Up to this many blocks per sequence the fused kernel runs; beyond it, the
+// scans above plus split-K matrix products (each split at least kMemMinK deep).
+constexpr int kMemFusedMaxBlocks = 32, kMemMinK = 256;
+
+__device__ __forceinline__ float pow16(float g) {
+  float g2 = g * g, g4 = g2 * g2, g8 = g4 * g4;
+  return g8 * g8;
+}
+
+// M = N / Z with N_i = g N_{i-1} + S_i (float32 and compute type).
+template <typename T>
+__global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
+    const float* __restrict__ S, float* __restrict__ M, T* __restrict__ Mt, int nb, int D,
+    float gamma) {
+  __shared__ float agg[kScChunks][kScCols];
+  const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
+  const int col = blockIdx.x * kScCols + c;
+  const bool on = col < D;
+  const int b = blockIdx.y;
+  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+  const float g16 = pow16(gamma);
+  float carry = 0.f;  // N just before this pass
+  for (int p0 = 0; p0 < nb; p0 += kScChunks * kScRows) {
+    const int a = p0 + k * kScRows;
+    float v[kScRows];
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) {
+      const int i = a + r;
+      v[r] = on && i < nb ? S[((int64_t)b * nb + i) * D + col] : 0.f;
+    }
+    float n = 0.f;
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) {
+      n = gamma * n + v[r];
+      v[r] = n;
+    }
+    agg[k][c] = n;
+    __syncthreads();
+    float cin = carry, cout = carry;
+    for (int j = 0; j < kScChunks; ++j) {
+      if (j == k) cin = cout;
+      cout = g16 * cout + agg[j][c];
+    }
+    float f = gamma;
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) {
+      const int i = a + r;
+      if (on && i < nb) {
+        const float m = (v[r] + f * cin) / zsum(i, gamma, lg2);
+        const int64_t off = ((int64_t)b * nb + i) * D + col;
+        M[off] = m;
+        Mt[off] = from_f32<T>(m);
+      }
+      f *= gamma;
+    }
+    carry = cout;
+    __syncthreads();  // agg[] is rewritten by the next pass
+  }
+}
+
+// Reverse scans of the memory backward from dM (float32), M:
+//   Qs_i = dM_i / Z_i + g Qs_{i+1} (= dS_i),  E_i = -dM_i . M_i / Z_i + g E_{i+1},
+//   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one atomic add per workgroup).
+template <typename T>
+__global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
+    const float* __restrict__ dM, const float* __restrict__ M, float* __restrict__ dS,
+    float* __restrict__ dgamma, int nb, int D, float gamma) {
+  __shared__ float aq[kScChunks][kScCols], ae[kScChunks][kScCols];
+  __shared__ float red[kScCols * kScChunks / 64];
+  const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
+  const int col = blockIdx.x * kScCols + c;
+  const bool on = col < D;
+  const int b = blockIdx.y;
+  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+  const float g16 = pow16(gamma);
+  constexpr int PASS = kScChunks * kScRows;
+  float cq = 0.f, ce = 0.f;  // Qs and E just after this pass
+  float dg = 0.f;
+  for (int p0 = (nb - 1) / PASS * PASS; p0 >= 0; p0 -= PASS) {
+    const int a = p0 + k * kScRows;
+    float x[kScRows], y[kScRows], mprev[kScRows];
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) {
+      const int i = a + r;
+      const bool ok = on && i < nb;
+      const int64_t off = ((int64_t)b * nb + i) * D + col;
+      const float dm = ok ? dM[off] : 0.f;
+      const float m = ok ? M[off] : 0.f;
+      const float z = zsum(i, gamma, lg2);
+      x[r] = dm / z;
+      y[r] = -dm * m / z;
+      mprev[r] = ok && i >= 1 ? M[off - D] : 0.f;
+    }
+    float q = 0.f, e = 0.f;
+#pragma unroll
+    for (int r = kScRows - 1; r >= 0; --r) {
+      q = x[r] + gamma * q;
+      e = y[r] + gamma * e;
+      x[r] = q;
+      y[r] = e;
+    }
+    aq[k][c] = q;
+    ae[k][c] = e;
+    __syncthreads();
+    float iq = cq, ie = ce, oq = cq, oe = ce;
+    for (int j = kScChunks - 1; j >= 0; --j) {
+      if (j == k) {
+        iq = oq;
+        ie = oe;
+      }
+      oq = aq[j][c] + g16 * oq;
+      oe = ae[j][c] + g16 * oe;
+    }
+    float f = gamma;
+#pragma unroll
+    for (int r = kScRows - 1; r >= 0; --r) {
+      const int i = a + r;
+      const float qs = x[r] + f * iq, es = y[r] + f * ie;
+      f *= gamma;
+      if (on && i < nb) {
+        dS[((int64_t)b * nb + i) * D + col] = qs;
+        if (i >= 1) {
+          const float zp = zsum(i - 1, gamma, lg2);
+          dg += qs * (mprev[r] * zp) + es * zp;
+        }
+      }
+    }
+    cq = oq;
+    ce = oe;
+    __syncthreads();  // aq[] / ae[] are rewritten by the next pass
+  }
+  const float v = wave_sum(dg);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0 && dgamma) {
+    float t = 0.f;
+    for (int w = 0; w < kScCols * kScChunks / 64; ++w) t += red[w];
+    unsafeAtomicAdd(dgamma, t);
+  }
+}
+
 // ------------------------------------------------------------------ gate backward
 // dU = dY * Mc * G (1 - G) per element, and the block sum of dY * G, which is
 // the gradient of the shifted memory, in the column-chunk layout.  The block
@@ -636,8 +791,28 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
   return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
 }
 
+bool mem_fused(int nb) { return nb <= kMemFusedMaxBlocks; }
+
+size_t mem_part_bytes(int B, int nb, int D) {
+  return mem_fused(nb) ? 0 : gemm_splitk_partial_bytes(B * nb, D, D, kMemMinK);
+}
+
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
-                   float* P, int B, int nb, int D, float gamma, hipStream_t s) {
+                   float* P, float* part, int B, int nb, int D, float gamma, hipStream_t s) {
+  if (!mem_fused(nb)) {
+    // M from the scan, then P = M W_m as a matrix product.
+    const dim3 grid((D + kScCols - 1) / kScCols, B);
+    if (dt == DType::BF16)
+      hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
+                         (bf16*)Mt, nb, D, gamma);
+    else
+      hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
+                         (float*)Mt, nb, D, gamma);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    GemmDesc g{B * nb, D, D, Mt, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    return gemm_splitk(dt, g, part, P, nullptr, nullptr, D, D, false, kMemMinK, s);
+  }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   const int es = dt == DType::BF16 ? 2 : 4;
   int kcr = (64 * 1024) / (kMsCols * es);  // staged W_m rows per chunk (64 KB)
@@ -663,7 +838,22 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
 }
 
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
-                   float* dgamma, int B, int nb, int D, float gamma, hipStream_t s) {
+                   float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
+                   hipStream_t s) {
+  if (!mem_fused(nb)) {
+    // dM = dP W_m^T as a matrix product, then the reverse scans.
+    GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+    hipError_t e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, false, kMemMinK, s);
+    if (e != hipSuccess) return e;
+    const dim3 grid((D + kScCols - 1) / kScCols, B);
+    if (dt == DType::BF16)
+      hipLaunchKernelGGL(scan_bwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, dM, M, dS,
+                         dgamma, nb, D, gamma);
+    else
+      hipLaunchKernelGGL(scan_bwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, dM, M,
+                         dS, dgamma, nb, D, gamma);
+    return hipGetLastError();
+  }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
