@@ -915,7 +915,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
 // queries for dQ (as in attn_bwd_dq_bf16_kernel), recomputing the
 // probabilities from lse instead of keeping them.
 template <int NW>
-__global__ __launch_bounds__(NW * 64, 2) void attn_bwd_block_bf16_kernel(
+__global__ __launch_bounds__(NW * 64, NW >= 8 ? 1 : 2) void attn_bwd_block_bf16_kernel(
     const bf16* __restrict__ qkv, const bf16* __restrict__ o, const bf16* __restrict__ dout,
     const float* __restrict__ lse, bf16* __restrict__ dqkv, int Tn, int D, int H, int L,
     float sl2, float scale) {
@@ -1235,19 +1235,20 @@ hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* d
 
 bool attn_bwd_fused(DType dt, int T, int L) {
   const int lb = L < T ? L : T;
-  return dt == DType::BF16 && lb <= 128;
+  return dt == DType::BF16 && lb <= 256;
 }
 
 hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void* dout,
                           const float* lse, void* dqkv, int B, int T, int D, int H, int L,
                           hipStream_t s) {
   if (!attn_bwd_fused(dt, T, L)) return hipErrorInvalidValue;
-  const int nw = attn_waves(L, T);
+  const int lb = L < T ? L : T;
+  const int nw = lb <= 128 ? attn_waves(L, T) : 8;  // one wave per 32 tokens of the block
   dim3 grid(1, (T + L - 1) / L, B * H);
   const float scale = 1.0f / sqrtf((float)kDh);
   const float sl2 = 1.4426950408889634f * scale;
 #define BLK(NW) hipLaunchKernelGGL(attn_bwd_block_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (const bf16*)out, (const bf16*)dout, lse, (bf16*)dqkv, T, D, H, L, sl2, scale)
-  if (nw == 1) BLK(1); else if (nw == 2) BLK(2); else BLK(4);
+  if (nw == 1) BLK(1); else if (nw == 2) BLK(2); else if (nw == 4) BLK(4); else BLK(8);
 #undef BLK
   return hipGetLastError();
 }
