@@ -186,6 +186,9 @@ def long_context(make_step, torch, abi, dt, steps=10, warmup=3):
     torch.cuda.synchronize()
     stages = abi.bcmt_trace_read()
     abi.bcmt_trace_enable(False)
+    print(f"long context B={B} T={T} D={D} H={H} L={L}: {ms * 1e3:.1f} us per step", file=sys.stderr)
+    for name, calls, total in stages:
+        print(f"  {name:24s} {total / calls * 1e3:10.1f} us", file=sys.stderr)
     act = B * T * D * es
     # attention: Q, K, V read and O written (forward); the fused backward
     # reads Q, K, V, O, dO and writes dQ, dK, dV; the two-kernel backward
