@@ -29,11 +29,20 @@ Readings of points the paper leaves open (all listed in the design notes):
   * the paper states no backward pass; the one here is derived by hand and
     pinned by finite differences in the tests.
 
+Chunked execution: a sequence cut at block boundaries into consecutive
+chunks gives the same layer when each chunk starts the recurrence of Sec. 3.5
+from the state the previous chunk ended with.  That state (the "carry") is
+N = sum_j gamma^(k-j) S_j and Z = sum_j gamma^(k-j) over all earlier blocks j
+(k the last of them); the first block of a chunk receives M = N / Z projected
+by W_m, and Z = 0 stands for an empty history (the start of a sequence).
+
 Parity status: forward pinned by library attention (dense / block-diagonal
 causal), closed forms of the memory normaliser, convexity, gamma limits,
 HOnly / W_m = 0 and W_g = 0 identities, and causality; backward pinned by
-central finite differences.  End-to-end values beyond those pins have no
-printed worked example in the paper ("parity unpinned" beyond the pins).
+central finite differences; the carry pinned by chunked runs equal to the
+whole sequence's (values and gradients) and by finite differences.
+End-to-end values beyond those pins have no printed worked example in the
+paper ("parity unpinned" beyond the pins).
 """
 
 import numpy as np
@@ -98,6 +107,37 @@ def exp_memory(S, gamma):
     return M
 
 
+def exp_memory_carry(S, gamma, N_in, Z_in):
+    """The memory of Sec. 3.5 for blocks that follow earlier ones.
+
+    S: [B, n, D] summaries of this chunk's blocks; N_in [B, D] and Z_in [B]
+    aggregate the earlier blocks (N_in = sum_j gamma^(-1-j) S_j and
+    Z_in = sum_j gamma^(-1-j) over blocks j < 0).  Block i of the chunk then
+    has the double sums of Sec. 3.5 over every block up to it:
+      N_i = sum_{0<=j<=i} gamma^(i-j) S_j + gamma^(i+1) N_in,
+      Z_i = sum_{0<=j<=i} gamma^(i-j)     + gamma^(i+1) Z_in,
+    and M_i = N_i / Z_i.  Returns M [B, n, D], N [B, n, D], Z [B, n].
+    """
+    B, n, D = S.shape
+    g = float(gamma)
+    N = np.zeros((B, n, D))
+    Z = np.zeros((B, n))
+    for i in range(n):
+        for j in range(i + 1):
+            N[:, i] += g ** (i - j) * S[:, j]
+            Z[:, i] += g ** (i - j)
+        N[:, i] += g ** (i + 1) * N_in
+        Z[:, i] += g ** (i + 1) * Z_in
+    return N / Z[:, :, None], N, Z
+
+
+def carry_memory(N_in, Z_in):
+    """M = N / Z of the earlier blocks, or 0 for an empty history (Z = 0)."""
+    Z = np.asarray(Z_in, dtype=np.float64)
+    safe = np.where(Z > 0, Z, 1.0)
+    return np.where((Z > 0)[:, None], np.asarray(N_in, dtype=np.float64) / safe[:, None], 0.0)
+
+
 def block_causal_attention(Q, K, V, L, h):
     """Dense causal multi-head attention confined to each block (Sec. 3.3, 3.6).
 
@@ -125,11 +165,15 @@ def block_causal_attention(Q, K, V, L, h):
     return out, probs
 
 
-def forward(X, P, L, h, gamma, residual=False):
+def forward(X, P, L, h, gamma, residual=False, carry=None):
     """One BCMT token-mixing layer, X [B, T, D] -> Y [B, T, D] (Sec. 3.2-3.8).
 
     P: dict of float64 weights Wq, Wk, Wv, Wo, Wm, Wg [D, D] (input-major, so
     that y = x @ W) and wp [D].  Returns (Y, cache) with every intermediate.
+
+    ``carry`` = (N_in [B, D], Z_in [B]) makes X a chunk that follows earlier
+    blocks of the same sequences (see exp_memory_carry); the state after the
+    chunk's last block is then cache["carry_out"] = (N_out, Z_out).
     """
     X = np.asarray(X, dtype=np.float64)
     B, T, D = X.shape
@@ -153,10 +197,22 @@ def forward(X, P, L, h, gamma, residual=False):
         S[:, i] = np.einsum("bt,btd->bd", a[:, b0:b1], Hloc[:, b0:b1])
 
     # Sec. 3.5: normalised exponential memory, projection, one-block shift.
-    M = exp_memory(S, gamma)
-    Mproj = M @ P["Wm"]
-    Mcausal = np.zeros_like(Mproj)
-    Mcausal[:, 1:] = Mproj[:, :-1]
+    if carry is None:
+        M = exp_memory(S, gamma)
+        Mproj = M @ P["Wm"]
+        Mcausal = np.zeros_like(Mproj)
+        Mcausal[:, 1:] = Mproj[:, :-1]
+        extra = {}
+    else:
+        N_in = np.asarray(carry[0], dtype=np.float64)
+        Z_in = np.asarray(carry[1], dtype=np.float64)
+        M, Nacc, Zacc = exp_memory_carry(S, gamma, N_in, Z_in)
+        # The earlier blocks' memory precedes this chunk's first block.
+        Mext = np.concatenate([carry_memory(N_in, Z_in)[:, None], M], axis=1)
+        Mproj = Mext @ P["Wm"]
+        Mcausal = Mproj[:, :-1].copy()
+        extra = dict(N_in=N_in, Z_in=Z_in, Mext=Mext, Nacc=Nacc, Zacc=Zacc,
+                     carry_out=(Nacc[:, -1].copy(), Zacc[:, -1].copy()))
 
     # Sec. 3.7: broadcast to tokens; Sec. 3.8: gate and injection.
     Mtok = Mcausal[:, blk]                   # [B, T, D]
@@ -167,16 +223,21 @@ def forward(X, P, L, h, gamma, residual=False):
         Y = Y + X
     cache = dict(X=X, P=P, L=L, h=h, gamma=float(gamma), residual=residual,
                  Q=Q, K=K, V=V, probs=probs, Hcat=Hcat, Hloc=Hloc, s=s, a=a,
-                 S=S, M=M, Mproj=Mproj, Mcausal=Mcausal, U=U, G=G)
+                 S=S, M=M, Mproj=Mproj, Mcausal=Mcausal, U=U, G=G, **extra)
     return Y, cache
 
 
-def backward(cache, dY):
+def backward(cache, dY, dcarry=None):
     """Gradients of sum(dY * Y) for the layer of ``forward``.
 
     The paper gives no backward pass; this is the chain rule applied to the
     forward steps in reverse order.  Weight gradients are summed over the
     batch.  Returns a dict with dX, dWq, dWk, dWv, dWo, dWm, dWg, dwp, dgamma.
+
+    For a chunk (``forward`` with a carry) the loss also holds
+    sum(dN_out * N_out) + sum(dZ_out * Z_out) with ``dcarry`` = (dN_out,
+    dZ_out) (None: zero), and the result adds dN_in and dZ_in, the gradients
+    of the incoming state.
     """
     c = cache
     P, L, h, gamma = c["P"], c["L"], c["h"], c["gamma"]
@@ -199,25 +260,29 @@ def backward(cache, dY):
     for i, (b0, b1) in enumerate(ranges):
         dMcausal[:, i] = dMtok[:, b0:b1].sum(axis=1)
 
-    # Shift and projection: Mcausal[i] = Mproj[i-1], Mproj = M @ Wm.
-    dMproj = np.zeros_like(dMcausal)
-    dMproj[:, :-1] = dMcausal[:, 1:]
-    dWm = np.einsum("bid,bie->de", c["M"], dMproj)
-    dM = dMproj @ P["Wm"].T
+    extra = {}
+    if "carry_out" not in c:
+        # Shift and projection: Mcausal[i] = Mproj[i-1], Mproj = M @ Wm.
+        dMproj = np.zeros_like(dMcausal)
+        dMproj[:, :-1] = dMcausal[:, 1:]
+        dWm = np.einsum("bid,bie->de", c["M"], dMproj)
+        dM = dMproj @ P["Wm"].T
 
-    # Memory M = A(gamma) @ S with A the normalised decay weights.
-    A, w, z = memory_weights(nb, gamma)
-    dS = np.einsum("ij,bid->bjd", A, dM)
-    i_idx = np.arange(nb)[:, None]
-    j_idx = np.arange(nb)[None, :]
-    dist = i_idx - j_idx
-    lower = dist >= 0
-    # d/dgamma of gamma**(i-j): (i-j) * gamma**(i-j-1), zero on the diagonal.
-    dw = np.where(dist >= 1, dist * np.power(float(gamma), np.where(dist >= 1, dist - 1, 0)), 0.0)
-    dw = np.where(lower, dw, 0.0)
-    dz = dw.sum(axis=1)
-    dA = (dw - A * dz[:, None]) / z[:, None]
-    dgamma = float(np.einsum("ij,bid,bjd->", dA, dM, c["S"]))
+        # Memory M = A(gamma) @ S with A the normalised decay weights.
+        A, w, z = memory_weights(nb, gamma)
+        dS = np.einsum("ij,bid->bjd", A, dM)
+        i_idx = np.arange(nb)[:, None]
+        j_idx = np.arange(nb)[None, :]
+        dist = i_idx - j_idx
+        lower = dist >= 0
+        # d/dgamma of gamma**(i-j): (i-j) * gamma**(i-j-1), zero on the diagonal.
+        dw = np.where(dist >= 1, dist * np.power(float(gamma), np.where(dist >= 1, dist - 1, 0)), 0.0)
+        dw = np.where(lower, dw, 0.0)
+        dz = dw.sum(axis=1)
+        dA = (dw - A * dz[:, None]) / z[:, None]
+        dgamma = float(np.einsum("ij,bid,bjd->", dA, dM, c["S"]))
+    else:
+        dS, dWm, dgamma, extra = _memory_carry_backward(c, dMcausal, dcarry)
 
     # Pooling: S_i = sum_t a_t Hloc[t], a = softmax(Hloc @ wp) per block.
     dwp = np.zeros(D)
@@ -267,7 +332,61 @@ def backward(cache, dY):
     if c["residual"]:
         dX = dX + dY
     return dict(dX=dX, dWq=dWq, dWk=dWk, dWv=dWv, dWo=dWo, dWm=dWm, dWg=dWg,
-                dwp=dwp, dgamma=dgamma)
+                dwp=dwp, dgamma=dgamma, **extra)
+
+
+def _memory_carry_backward(c, dMcausal, dcarry):
+    """Chain rule through exp_memory_carry and the projection of a chunk.
+
+    Differentiates the double sums of exp_memory_carry directly: with
+    dN_i = dM_i / Z_i (+ dN_out at the last block) and
+    dZ_i = -(dM_i . M_i) / Z_i (+ dZ_out at the last block),
+      dS_j    = sum_{i>=j} gamma^(i-j) dN_i,
+      dN_in   = sum_i gamma^(i+1) dN_i + dM_prev / Z_in,
+      dZ_in   = sum_i gamma^(i+1) dZ_i - (dM_prev . M_prev) / Z_in,
+      dgamma  = sum_i sum_{j<i} (i-j) gamma^(i-j-1) (dN_i . S_j + dZ_i)
+              + sum_i (i+1) gamma^i (dN_i . N_in + dZ_i Z_in),
+    where M_prev = N_in / Z_in is the earlier blocks' memory (its terms are
+    absent when Z_in = 0).  Returns dS, dWm, dgamma and {dN_in, dZ_in}.
+    """
+    P, g = c["P"], c["gamma"]
+    S, Mext, Nacc, Zacc = c["S"], c["Mext"], c["Nacc"], c["Zacc"]
+    N_in, Z_in = c["N_in"], c["Z_in"]
+    B, n, D = S.shape
+    # Mcausal[i] = Mproj[i] with Mproj = Mext @ Wm; Mproj's last row is unused.
+    dMproj = np.zeros((B, n + 1, D))
+    dMproj[:, :n] = dMcausal
+    dWm = np.einsum("bid,bie->de", Mext, dMproj)
+    dMext = dMproj @ P["Wm"].T
+    dM_prev, dM = dMext[:, 0], dMext[:, 1:]
+    M = Mext[:, 1:]
+
+    dN = dM / Zacc[:, :, None]
+    dZ = -np.einsum("bid,bid->bi", dM, M) / Zacc
+    if dcarry is not None:
+        dN[:, -1] += np.asarray(dcarry[0], dtype=np.float64)
+        dZ[:, -1] += np.asarray(dcarry[1], dtype=np.float64)
+
+    dS = np.zeros_like(S)
+    dN_in = np.zeros((B, D))
+    dZ_in = np.zeros(B)
+    dgamma = 0.0
+    for i in range(n):
+        for j in range(i + 1):
+            dS[:, j] += g ** (i - j) * dN[:, i]
+            if j < i:
+                dgamma += (i - j) * g ** (i - j - 1) * (
+                    np.sum(dN[:, i] * S[:, j]) + np.sum(dZ[:, i]))
+        dN_in += g ** (i + 1) * dN[:, i]
+        dZ_in += g ** (i + 1) * dZ[:, i]
+        dgamma += (i + 1) * (g ** i if i > 0 else 1.0) * (
+            np.sum(dN[:, i] * N_in) + np.sum(dZ[:, i] * Z_in))
+    has = Z_in > 0
+    safe = np.where(has, Z_in, 1.0)
+    M_prev = carry_memory(N_in, Z_in)
+    dN_in += np.where(has[:, None], dM_prev / safe[:, None], 0.0)
+    dZ_in -= np.where(has, np.einsum("bd,bd->b", dM_prev, M_prev) / safe, 0.0)
+    return dS, dWm, float(dgamma), dict(dN_in=dN_in, dZ_in=dZ_in)
 
 
 def stack_forward(X, layers, L, h, gamma, residual=True):
