@@ -145,6 +145,58 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
                         void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Chunked execution ---------------------------------------------------
+ * Only the memory of Sec. 3.5 crosses block boundaries, through the decayed
+ * recurrence over blocks; attention, pooling and the gate stay inside a
+ * block.  A sequence cut at block boundaries into consecutive chunks can
+ * therefore run chunk by chunk, each call continuing the recurrence from the
+ * state left by the blocks before it:
+ *   N = sum_j g^(k-j) S_j,   Z = sum_j g^(k-j)   (j <= k, k the last block),
+ * float32 in device memory.  The chunk's first block receives the memory
+ * N / Z of the earlier blocks, projected by Wm, exactly as if the previous
+ * chunk's last block preceded it in one call.  Z = 0 stands for an empty
+ * history (the start of the sequences): the first block then receives 0,
+ * and N must be 0.  Chaining chunks gives the whole-sequence layer when
+ * every chunk except the last holds a multiple of L tokens (otherwise a
+ * block would be cut in two).  Sequences of the batch may be at different
+ * positions: Z is per sequence. */
+typedef struct {
+  float* N; /* [B, D] */
+  float* Z; /* [B] */
+} bcmt_carry;
+
+/* Forward pass of one chunk.
+ *   carry_in   state after the earlier blocks (read), or NULL for an empty
+ *              history.
+ *   carry_out  receives the state after the chunk's last block, or NULL.
+ *              It may use the same buffers as carry_in (the incoming state
+ *              is copied into `saved` before anything is written).
+ * A carry given must have both members, N 16-byte and Z 4-byte aligned.
+ * The other arguments are those of bcmt_layer_forward, with the same
+ * workspace and `saved` sizes; `saved` written here is for
+ * bcmt_layer_backward_chunk (bcmt_layer_backward would drop the incoming
+ * state's contribution). */
+int bcmt_layer_forward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* params,
+                             const bcmt_carry* carry_in, void* Y, const bcmt_carry* carry_out,
+                             void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward pass of one chunk, given the `saved` of bcmt_layer_forward_chunk:
+ * gradients of sum(dY * Y) + sum(dN * N_out) + sum(dZ * Z_out), where
+ * (N_out, Z_out) is the chunk's outgoing state and (dN, dZ) = *dcarry_out.
+ *   dcarry_out  gradient arriving for the outgoing state (read), or NULL
+ *               for none (the last chunk).
+ *   dcarry_in   receives the gradient of the incoming state, or NULL.  It
+ *               may use the same buffers as dcarry_out.
+ * grads->dgamma includes the decay's effect through the incoming state's
+ * first block.  Running the chunks' backward passes from the last to the
+ * first, each given the dcarry_in of the chunk after it, with
+ * BCMT_FLAG_ACCUM_WGRAD from the second call on, yields the gradients of
+ * the whole sequence. */
+int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* params,
+                              const void* saved, const void* dY, const bcmt_carry* dcarry_out,
+                              void* dX, const bcmt_carry* dcarry_in, const bcmt_grads* grads,
+                              void* ws, size_t ws_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* bcmt_strerror(int status);
 

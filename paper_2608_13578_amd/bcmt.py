@@ -32,8 +32,8 @@ BCMT_PASS_INFERENCE = 1
 BCMT_PASS_BACKWARD = 2
 
 EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_layer_forward",
-            "bcmt_layer_backward", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
-            "bcmt_trace_read")
+            "bcmt_layer_backward", "bcmt_layer_forward_chunk", "bcmt_layer_backward_chunk",
+            "bcmt_strerror", "bcmt_version", "bcmt_trace_enable", "bcmt_trace_read")
 
 PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
 GRAD_NAMES = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp", "dgamma")
@@ -57,6 +57,11 @@ class bcmt_params(ctypes.Structure):
 
 class bcmt_grads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in GRAD_NAMES]
+
+
+class bcmt_carry(ctypes.Structure):
+    """Memory state between chunks: N [B, D] and Z [B], float32 device pointers."""
+    _fields_ = [("N", ctypes.c_void_p), ("Z", ctypes.c_void_p)]
 
 
 class bcmt_trace_entry(ctypes.Structure):
@@ -89,6 +94,14 @@ def lib():
         L.bcmt_layer_backward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
                                           ctypes.POINTER(bcmt_grads), vp, ctypes.c_size_t, vp]
         L.bcmt_layer_backward.restype = ctypes.c_int
+        carryp = ctypes.POINTER(bcmt_carry)
+        L.bcmt_layer_forward_chunk.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), carryp, vp,
+                                               carryp, vp, vp, ctypes.c_size_t, vp]
+        L.bcmt_layer_forward_chunk.restype = ctypes.c_int
+        L.bcmt_layer_backward_chunk.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp,
+                                                carryp, vp, carryp, ctypes.POINTER(bcmt_grads),
+                                                vp, ctypes.c_size_t, vp]
+        L.bcmt_layer_backward_chunk.restype = ctypes.c_int
         L.bcmt_strerror.argtypes = [ctypes.c_int]
         L.bcmt_strerror.restype = ctypes.c_char_p
         L.bcmt_version.argtypes = []
@@ -137,6 +150,17 @@ def _grads(g):
     return bcmt_grads(*[_ptr(g.get(n)) for n in GRAD_NAMES])
 
 
+def _carry(c):
+    """None, a bcmt_carry, or an (N, Z) pair of tensors / pointers."""
+    if c is None or isinstance(c, bcmt_carry):
+        return c
+    return bcmt_carry(_ptr(c[0]), _ptr(c[1]))
+
+
+def _ref(x):
+    return ctypes.byref(x) if x is not None else None
+
+
 def _nbytes(x):
     return x.numel() * x.element_size()
 
@@ -180,6 +204,30 @@ def bcmt_layer_backward(cfg, X, params, saved, dY, dX, grads, ws, ws_bytes=None,
                                    int(ws_bytes), _stream(stream))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_layer_backward")
+
+
+def bcmt_layer_forward_chunk(cfg, X, params, carry_in, Y, carry_out, saved, ws, ws_bytes=None,
+                             stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    st = lib().bcmt_layer_forward_chunk(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
+                                        _ref(_carry(carry_in)), _ptr(Y), _ref(_carry(carry_out)),
+                                        _ptr(saved), _ptr(ws), int(ws_bytes), _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_layer_forward_chunk")
+
+
+def bcmt_layer_backward_chunk(cfg, X, params, saved, dY, dcarry_out, dX, dcarry_in, grads, ws,
+                              ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    g = _grads(grads)
+    st = lib().bcmt_layer_backward_chunk(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
+                                         _ptr(saved), _ptr(dY), _ref(_carry(dcarry_out)), _ptr(dX),
+                                         _ref(_carry(dcarry_in)), _ref(g), _ptr(ws), int(ws_bytes),
+                                         _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_layer_backward_chunk")
 
 
 def bcmt_trace_enable(on):

@@ -9,6 +9,11 @@
 //   5. Q = S Wm (split-K partials)                 matrix cores (N_b rows)
 //   6. decayed scans of S and Q -> M, P = M Wm     latency
 //   7. U = H Wg; G = sigmoid(U); Y = H + G * P[blk - 1]  (fused epilogue)
+// A chunk of a longer sequence (the *_chunk entry points) also takes the
+// memory state left by the earlier blocks: before step 5 it is copied into
+// `saved` with its memory in the compute type, which is projected by Wm for
+// the chunk's first block; the scans start from it and write the state after
+// the last block.
 // Backward runs the chain rule through the same steps in reverse.  Its
 // critical path (gate -> memory -> pooling -> dH -> attention -> dX) stays on
 // the caller's stream; the weight-gradient products, which nothing later in
@@ -42,11 +47,15 @@ struct Plan {
   size_t es;
   DType dt;
   // saved (forward -> backward)
-  size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P, saved_bytes;
+  size_t qkv, o, lse, h, g, s, stats, S, M, Mt, P;
+  size_t cN, cZ, cMt, cP;  // incoming chunk state: N, Z, N / Z (compute type), (N / Z) Wm
+  size_t saved_bytes;
   // forward scratch
-  size_t sp, St, mpart, fwd_bytes;
+  size_t sp, St, mpart, cpart, fwd_bytes;
   // backward scratch
-  size_t du, pbar, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart, bwd_bytes;
+  size_t du, pbar, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart;
+  size_t cpbar, cdm, ce0, cpart_b;  // chunk state gradients
+  size_t bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
     B = c.B;
@@ -75,12 +84,18 @@ struct Plan {
     M = take(BND * 4);
     Mt = take(BND * es);
     P = take(BND * 4);
+    const size_t BD = (size_t)B * D;
+    cN = take(BD * 4);
+    cZ = take((size_t)B * 4);
+    cMt = take(BD * es);
+    cP = take(BD * 4);
     saved_bytes = off;
 
     off = 0;
     sp = take(BT * (D / kDh) * 4);  // partial pooling scores, D / 64 per token
     St = take(BND * es);
     mpart = take(mem_part_bytes(B, nb, D));  // W_m product partials (long sequences)
+    cpart = take(carry_part_bytes(B, D));
     fwd_bytes = off;
 
     off = 0;
@@ -103,6 +118,10 @@ struct Plan {
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
       wpart = take(w);  // weight gradients (side stream, one after another)
     }
+    cpbar = take(BD * es);
+    cdm = take(BD * 4);
+    ce0 = take(BD * 4);
+    cpart_b = take(carry_part_bytes(B, D));
     bwd_bytes = off;
   }
 };
@@ -130,20 +149,30 @@ bool overlaps(const void* a, const void* b, size_t n) {
   return x < y + n && y < x + n;
 }
 
+// A chunk state, when given, needs both members: N 16-byte and Z 4-byte aligned.
+bool carry_ok(const bcmt_carry* c) {
+  if (!c) return true;
+  return c->N && c->Z && aligned16(c->N) && ((uintptr_t)c->Z & 3u) == 0;
+}
+
 
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
 enum Stage {
-  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_SCAN_FWD, ST_GATE,
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_CARRY_IN, ST_CARRY_PROJ, ST_SCAN_FWD, ST_GATE,
   ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_WGRAD,
-  ST_WM_WGRAD_RED, ST_MEM_BWD, ST_POOL_BWD, ST_DWP, ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
+  ST_WM_WGRAD_RED, ST_CARRY_WGRAD, ST_CARRY_DGRAD, ST_MEM_BWD, ST_CARRY_BWD, ST_POOL_BWD, ST_DWP,
+  ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
-    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.memory_scan",
+    "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.carry_in",
+    "fwd.carry_proj_gemm", "fwd.memory_scan",
     "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce",
-    "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.memory_scan", "bwd.pool", "bwd.pool_dwp", "bwd.wg_dgrad_gemm",
+    "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.carry_wm_wgrad_gemm",
+    "bwd.carry_dgrad_gemm", "bwd.memory_scan", "bwd.carry_in", "bwd.pool", "bwd.pool_dwp",
+    "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
 
@@ -329,11 +358,17 @@ int bcmt_trace_read(bcmt_trace_entry* out, int max_entries) {
   return n;
 }
 
-int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* prm, void* Y,
-                       void* saved, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+// The forward and backward passes; `chunk` selects the chunked form, with an
+// incoming and an outgoing memory state.
+static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* prm, void* Y,
+                         void* saved, void* ws, size_t ws_bytes, void* stream, bool chunk,
+                         const bcmt_carry* cin, const bcmt_carry* cout) {
   int st = check_config(cfg);
   if (st != BCMT_OK) return st;
   if (!X || !prm || !Y) return BCMT_ERR_INVALID;
+  if (!carry_ok(cin) || !carry_ok(cout)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* p : w)
     if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
@@ -371,26 +406,45 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
   // 5-6. Exponential memory and its projection (Sec. 3.5): one kernel
   // projects the summaries (Q = S Wm, over only B * N_b rows) and scans S
   // and Q, which yields M and P = M Wm (the decayed sum is linear); the
-  // shift is applied where P is read.
+  // shift is applied where P is read.  A chunk first takes the state of the
+  // earlier blocks (a copy, so that carry_out may overwrite carry_in) and
+  // projects its memory for the first block.
+  Carry cr;
+  if (chunk) {
+    LAUNCH(ST_CARRY_IN, carry_prep(dt, cin ? cin->N : nullptr, cin ? cin->Z : nullptr,
+                                   (float*)(SV + p.cN), (float*)(SV + p.cZ), SV + p.cMt,
+                                   cin ? nullptr : (float*)(SV + p.cP), p.B, D, s));
+    if (cin)
+      LAUNCH(ST_CARRY_PROJ, carry_proj(dt, SV + p.cMt, prm->Wm, (float*)(SV + p.cP),
+                                       (float*)(W + p.cpart), false, p.B, D, s));
+    cr.Nin = (const float*)(SV + p.cN);
+    cr.Zin = (const float*)(SV + p.cZ);
+    cr.Pc = (const float*)(SV + p.cP);
+    cr.Nout = cout ? cout->N : nullptr;
+    cr.Zout = cout ? cout->Z : nullptr;
+  }
   LAUNCH(ST_SCAN_FWD, mem_fwd(dt, W + p.St, prm->Wm, (const float*)(SV + p.S), (float*)(SV + p.M),
                               SV + p.Mt, (float*)(SV + p.P), (float*)(W + p.mpart), p.B, p.nb, D,
-                              cfg->gamma, s));
+                              cfg->gamma, cr, s));
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
     GemmDesc g{BT, D, D, SV + p.h, D, false, {prm->Wg, nullptr, nullptr}, D, true, kSegNone, 0, 1};
     GateEpi e{Y, SV + p.g, SV + p.h, (cfg->flags & BCMT_FLAG_RESIDUAL) ? X : nullptr,
-              (const float*)(SV + p.P), p.T, p.L, p.nb, D};
+              (const float*)(SV + p.P), p.T, p.L, p.nb, D,
+              chunk ? (const float*)(SV + p.cP) : nullptr};
     LAUNCH(ST_GATE, gemm_gate(dt, g, e, s));
   }
   return BCMT_OK;
 }
 
-int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
-                        const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
-                        void* ws, size_t ws_bytes, void* stream) {
+static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                          const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
+                          void* ws, size_t ws_bytes, void* stream, bool chunk,
+                          const bcmt_carry* dcout, const bcmt_carry* dcin) {
   int st = check_config(cfg);
   if (st != BCMT_OK) return st;
   if (!X || !prm || !saved || !dY) return BCMT_ERR_INVALID;
+  if (!carry_ok(dcout) || !carry_ok(dcin)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* p : w)
     if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
@@ -440,7 +494,9 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
   // first unless the gradients accumulate.  The weight matrices and dwp are
   // written (or accumulated) by fixed-order reductions.
   LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                               nullptr, 0, accum ? nullptr : gr.dgamma, p.B, p.T, D, p.L, s));
+                               nullptr, 0, accum ? nullptr : gr.dgamma, p.B, p.T, D, p.L,
+                               chunk ? (const float*)(SV + p.cP) : nullptr,
+                               chunk ? W + p.cpbar : nullptr, s));
   // dWg = H^T dU and dWm = M^T dP on the side stream.
   if (gr.dWg || gr.dWm) {
     SIDE_BEGIN();
@@ -455,15 +511,38 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
                    0, 1};
         LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
                       accum, 512);
+        if (chunk) {
+          // The earlier blocks' memory fed the first block: dWm += Mc^T dPc.
+          GemmDesc gc{D, D, p.B, SV + p.cMt, D, true, {W + p.cpbar, nullptr, nullptr}, D, true,
+                      kSegNone, 0, 1};
+          LAUNCH_SPLITK(ST_CARRY_WGRAD, ST_CARRY_WGRAD, dt, gc, wpart, gr.dWm, nullptr, nullptr,
+                        D, D, true, 512);
+        }
       }
     }
     SIDE_END();
   }
   // Memory projection and decayed reverse scan: dM = dP Wm^T, dS and the
-  // decay gradient, in one kernel.
+  // decay gradient, in one kernel.  A chunk also feeds in the gradient of
+  // the state it passed on and forms the gradient of the state it took.
+  Carry cr;
+  if (chunk) {
+    LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar, prm->Wm, (float*)(W + p.cdm),
+                                      (float*)(W + p.cpart_b), true, p.B, D, s));
+    cr.Zin = (const float*)(SV + p.cZ);
+    cr.dNout = dcout ? dcout->N : nullptr;
+    cr.dZout = dcout ? dcout->Z : nullptr;
+    cr.e0 = (float*)(W + p.ce0);
+  }
   LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
                              gr.dgamma, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
-                             cfg->gamma, s));
+                             cfg->gamma, cr, s));
+  if (chunk)
+    LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
+                                      (const float*)(W + p.cdm), (const float*)(W + p.dS),
+                                      (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
+                                      dcin ? dcin->Z : nullptr, gr.dgamma, p.B, p.nb, D,
+                                      cfg->gamma, s));
   // Pooling backward: per-token a_t and ds_t, and partial sums of
   // ds_t H[t]; dwp = their sum on the side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
@@ -531,6 +610,34 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
 #undef SIDE_BEGIN
 #undef SIDE_END
   return BCMT_OK;
+}
+
+extern "C" {
+
+int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* prm, void* Y,
+                       void* saved, void* ws, size_t ws_bytes, void* stream) {
+  return layer_forward(cfg, X, prm, Y, saved, ws, ws_bytes, stream, false, nullptr, nullptr);
+}
+
+int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                        const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
+                        void* ws, size_t ws_bytes, void* stream) {
+  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, false, nullptr,
+                        nullptr);
+}
+
+int bcmt_layer_forward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                             const bcmt_carry* carry_in, void* Y, const bcmt_carry* carry_out,
+                             void* saved, void* ws, size_t ws_bytes, void* stream) {
+  return layer_forward(cfg, X, prm, Y, saved, ws, ws_bytes, stream, true, carry_in, carry_out);
+}
+
+int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                              const void* saved, const void* dY, const bcmt_carry* dcarry_out,
+                              void* dX, const bcmt_carry* dcarry_in, const bcmt_grads* grads,
+                              void* ws, size_t ws_bytes, void* stream) {
+  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, true, dcarry_out,
+                        dcarry_in);
 }
 
 }  // extern "C"

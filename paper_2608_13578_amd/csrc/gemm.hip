@@ -415,6 +415,7 @@ struct EpiGate {
     const f32x4 h = load4f(reinterpret_cast<const T*>(e.H) + off);
     f32x4 c = {0.f, 0.f, 0.f, 0.f};
     if (blk > 0) c = load4f(e.P + (int64_t)(b * e.nb + blk - 1) * e.D + n);
+    else if (e.Pc) c = load4f(e.Pc + (int64_t)b * e.D + n);
     f32x4 x = {0.f, 0.f, 0.f, 0.f};
     if (e.X) x = load4f(reinterpret_cast<const T*>(e.X) + off);
     f32x4 g, y;
@@ -436,6 +437,8 @@ struct EpiGate {
     ld8(reinterpret_cast<const T*>(e.H) + off, h);
     if (blk > 0) {
       ld8(e.P + (int64_t)(b * e.nb + blk - 1) * e.D + n, c);
+    } else if (e.Pc) {
+      ld8(e.Pc + (int64_t)b * e.D + n, c);
     } else {
 #pragma unroll
       for (int k = 0; k < 8; ++k) c[k] = 0.f;

@@ -74,6 +74,8 @@ hipError_t gemm_score(DType dt, const GemmDesc& g, void* C, const void* wp, floa
 // Gate + injection epilogue (forward): U = acc;
 //   G = sigmoid(U); Y = H + G * Mc[blk(t)] (+ X); G is stored for backward.
 // Mc[b, i] = P[b, i - 1] for i >= 1 and 0 for i = 0 (the one-block shift).
+// A chunk that follows earlier blocks (Pc not null) gives its block 0
+// Mc = Pc[b] instead.
 struct GateEpi {
   void* Y;
   void* G;
@@ -81,6 +83,7 @@ struct GateEpi {
   const void* X;     // nullable: residual off
   const float* P;    // [B * nb, D] projected memory
   int T, L, nb, D;
+  const float* Pc;   // nullable: [B, D] projected memory of the earlier blocks
 };
 hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t s);
 
@@ -116,6 +119,23 @@ hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void
                           hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
+// State of the decayed memory recurrence shared by consecutive chunks of the
+// same sequences (float32).  Forward: N and Z before the chunk's first block
+// (Nin [B, D], Zin [B]; null: empty history), Pc = (Nin / Zin) Wm [B, D]
+// (read by the fused scan), and where to write N and Z after the last block
+// (Nout, Zout; nullable).  Backward: the gradients arriving for that final
+// state (dNout, dZout; nullable) and the per-column gradient of Z at the
+// first block (e0 [B, D]; nullable).  All members null: a whole sequence.
+struct Carry {
+  const float* Nin = nullptr;
+  const float* Zin = nullptr;
+  const float* Pc = nullptr;
+  float* Nout = nullptr;
+  float* Zout = nullptr;
+  const float* dNout = nullptr;
+  const float* dZout = nullptr;
+  float* e0 = nullptr;
+};
 // Pooling, from the np partial scores per token written by gemm_score:
 // scores s [B*T], summaries S [B*nb, D] (float32, and St in the compute
 // type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
@@ -129,18 +149,39 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
 bool mem_fused(int nb);
 size_t mem_part_bytes(int B, int nb, int D);
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
-                   float* P, float* part, int B, int nb, int D, float gamma, hipStream_t s);
+                   float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
+                   hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
+// With Pc (a chunk after earlier blocks) block 0 uses Mc = Pc[b] and its
+// sum of dY * G goes to Pbar_c [B, D] (compute type).
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                    hipStream_t s);
+                    const float* Pc, void* Pbar_c, hipStream_t s);
 // Memory backward: dM = Pbar Wm^T, then the reverse decayed scan: dS and
 // the decay gradient (atomically added to *dgamma when given).  For long
 // sequences (see mem_fwd) dM goes through `dM` ([B*nb, D] float32) and a
 // split-K product using `part`; both may be null for short ones.
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
                    float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
-                   hipStream_t s);
+                   const Carry& c, hipStream_t s);
+// Chunked execution.  carry_prep copies the incoming state (Nu [B, D],
+// Zu [B]; both null: empty history) to Nin / Zin and writes its memory
+// Mct = Nin / Zin (0 where Zin = 0) in the compute type; with no incoming
+// state it also zeroes Pc.  carry_proj: Pc = Mct Wm, or with `transposed`
+// dMc = Pbar_c Wm^T, both [B, D] float32, using `part`
+// (carry_part_bytes bytes).  carry_finish forms the incoming state's
+// gradients from dMc, dS of block 0 and e0:
+//   dNin = dMc / Zin + g dS_0,  dZin = sum_cols (g e0 - dMc . M_in / Zin),
+// and adds the first block's decay term sum_cols dS_0 Nin + e0 Zin to
+// *dgamma (atomic); null outputs are skipped.
+hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, float* Zin,
+                      void* Mct, float* Pc, int B, int D, hipStream_t s);
+size_t carry_part_bytes(int B, int D);
+hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
+                      bool transposed, int B, int D, hipStream_t s);
+hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
+                        const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
+                        int D, float gamma, hipStream_t s);
 // Pooling backward: per-token softmax weights a_t and score gradients ds_t,
 // and (when dwp_part is not null) partial sums of ds_t H[t] over chunks of
 // tokens, one row of D floats per chunk.

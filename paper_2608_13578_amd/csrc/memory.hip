@@ -172,10 +172,18 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
 //               E_i  = -dM_i . M_i / Z_i + g E_{i+1} (= dZ_i, per column)
 //             and dg = sum_{i>=1} Qs_i N_{i-1} + E_i Z_{i-1} with
 //             N_{i-1} = M_{i-1} Z_{i-1}.
-// Z_i = 1 + g + ... + g^i (0-based i), with lg2 = log2(g) (g > 0).
-__device__ __forceinline__ float zsum(int i, float gamma, float lg2) {
+// A chunk that follows earlier blocks starts from their state (N, Z, and
+// NP = Pc Z); the state after the last block goes to c.Nout / c.Zout, the
+// gradients of that state enter the reverse scans at the last block, and
+// E of the first block goes to c.e0.
+// Z_i = 1 + g + ... + g^i + g^(i+1) zin (0-based i), where zin is the
+// normaliser of the blocks before the first one (0 for none), with
+// lg2 = log2(g) (g > 0).  The power underflows to 0 for long sequences,
+// where Z_i has converged to 1 / (1 - g).
+__device__ __forceinline__ float zsum(int i, float gamma, float lg2, float zin) {
   if (gamma == 0.f) return 1.f;
-  return (1.f - exp2f(lg2 * (float)(i + 1))) / (1.f - gamma);
+  const float gi = exp2f(lg2 * (float)(i + 1));
+  return (1.f - gi) / (1.f - gamma) + gi * zin;
 }
 
 constexpr int kMsCols = 32, kMsRows = 16, kMsWaves = 8, kMsGroup = 4;
@@ -188,7 +196,8 @@ template <typename T, bool FWD>
 __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     const T* __restrict__ A, const T* __restrict__ Wm, const float* __restrict__ S,
     float* __restrict__ M, T* __restrict__ Mt, float* __restrict__ P, const float* __restrict__ Min,
-    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, int kcr) {
+    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, int kcr,
+    Carry cr) {
   typedef typename Frag<T>::type F;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
   T* Bs = reinterpret_cast<T*>(dyn);  // [kcr][kMsCols] (forward only)
@@ -202,6 +211,14 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
   const bool scol = tid < kMsCols && col < D;
   float N = 0.f, NP = 0.f, Z = 0.f, Qs = 0.f, E = 0.f, dg = 0.f;
   const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
+  if constexpr (FWD) {
+    Z = zin;
+    if (scol && cr.Nin) {
+      N = cr.Nin[(int64_t)b * D + col];
+      NP = cr.Pc[(int64_t)b * D + col] * zin;
+    }
+  }
 
   for (int q = 0; q < nt; ++q) {
     const int rt = FWD ? q : nt - 1 - q;
@@ -274,15 +291,25 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
           M[off] = m;
           Mt[off] = from_f32<T>(m);
           P[off] = NP * rz;
+          if (i == nb - 1) {
+            if (cr.Nout) cr.Nout[(int64_t)b * D + col] = N;
+            if (cr.Zout && tid == 0 && blockIdx.x == 0) cr.Zout[b] = Z;
+          }
         } else {
-          const float z = zsum(i, gamma, lg2);
+          const float z = zsum(i, gamma, lg2, zin);
           const float m = Min[off];
           Qs = g / z + gamma * Qs;
           E = -g * m / z + gamma * E;
+          if (i == nb - 1) {
+            if (cr.dNout) Qs += cr.dNout[(int64_t)b * D + col];
+            if (cr.dZout && col == 0) E += cr.dZout[b];
+          }
           dS[off] = Qs;
           if (i >= 1) {
-            const float zp = zsum(i - 1, gamma, lg2);
+            const float zp = zsum(i - 1, gamma, lg2, zin);
             dg += Qs * (Min[off - D] * zp) + E * zp;
+          } else if (cr.e0) {
+            cr.e0[(int64_t)b * D + col] = E;
           }
         }
       }
@@ -313,7 +340,8 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
 // chunks before (after, for the reverse scan) into its carry, and applies
 // it: with the recurrence x_i = g x_{i-1} + y_i, the true value is the local
 // one plus g^(distance) times the carry.  A pass hands its end carry to the
-// next one.
+// next one; the first pass starts from the state of the earlier blocks
+// (zero for a whole sequence).
 constexpr int kScCols = 16, kScChunks = 16, kScRows = 16;
 // Up to this many blocks per sequence the fused kernel runs; beyond it, the
 // scans above plus split-K matrix products (each split at least kMemMinK deep).
@@ -328,7 +356,7 @@ __device__ __forceinline__ float pow16(float g) {
 template <typename T>
 __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
     const float* __restrict__ S, float* __restrict__ M, T* __restrict__ Mt, int nb, int D,
-    float gamma) {
+    float gamma, Carry cr) {
   __shared__ float agg[kScChunks][kScCols];
   const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
   const int col = blockIdx.x * kScCols + c;
@@ -336,7 +364,8 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
   const int b = blockIdx.y;
   const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
   const float g16 = pow16(gamma);
-  float carry = 0.f;  // N just before this pass
+  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
+  float carry = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;  // N just before this pass
   for (int p0 = 0; p0 < nb; p0 += kScChunks * kScRows) {
     const int a = p0 + k * kScRows;
     float v[kScRows];
@@ -363,25 +392,30 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
     for (int r = 0; r < kScRows; ++r) {
       const int i = a + r;
       if (on && i < nb) {
-        const float m = (v[r] + f * cin) / zsum(i, gamma, lg2);
+        const float n = v[r] + f * cin;
+        const float m = n / zsum(i, gamma, lg2, zin);
         const int64_t off = ((int64_t)b * nb + i) * D + col;
         M[off] = m;
         Mt[off] = from_f32<T>(m);
+        if (i == nb - 1 && cr.Nout) cr.Nout[(int64_t)b * D + col] = n;
       }
       f *= gamma;
     }
     carry = cout;
     __syncthreads();  // agg[] is rewritten by the next pass
   }
+  if (cr.Zout && blockIdx.x == 0 && threadIdx.x == 0) cr.Zout[b] = zsum(nb - 1, gamma, lg2, zin);
 }
 
 // Reverse scans of the memory backward from dM (float32), M:
 //   Qs_i = dM_i / Z_i + g Qs_{i+1} (= dS_i),  E_i = -dM_i . M_i / Z_i + g E_{i+1},
 //   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one atomic add per workgroup).
+// The gradients of a chunk's final state enter at the last block; E of the
+// first block goes to cr.e0.
 template <typename T>
 __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
     const float* __restrict__ dM, const float* __restrict__ M, float* __restrict__ dS,
-    float* __restrict__ dgamma, int nb, int D, float gamma) {
+    float* __restrict__ dgamma, int nb, int D, float gamma, Carry cr) {
   __shared__ float aq[kScChunks][kScCols], ae[kScChunks][kScCols];
   __shared__ float red[kScCols * kScChunks / 64];
   const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
@@ -391,6 +425,7 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
   const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
   const float g16 = pow16(gamma);
   constexpr int PASS = kScChunks * kScRows;
+  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
   float cq = 0.f, ce = 0.f;  // Qs and E just after this pass
   float dg = 0.f;
   for (int p0 = (nb - 1) / PASS * PASS; p0 >= 0; p0 -= PASS) {
@@ -403,9 +438,13 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
       const int64_t off = ((int64_t)b * nb + i) * D + col;
       const float dm = ok ? dM[off] : 0.f;
       const float m = ok ? M[off] : 0.f;
-      const float z = zsum(i, gamma, lg2);
+      const float z = zsum(i, gamma, lg2, zin);
       x[r] = dm / z;
       y[r] = -dm * m / z;
+      if (ok && i == nb - 1) {
+        if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
+        if (cr.dZout && col == 0) y[r] += cr.dZout[b];
+      }
       mprev[r] = ok && i >= 1 ? M[off - D] : 0.f;
     }
     float q = 0.f, e = 0.f;
@@ -437,8 +476,10 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
       if (on && i < nb) {
         dS[((int64_t)b * nb + i) * D + col] = qs;
         if (i >= 1) {
-          const float zp = zsum(i - 1, gamma, lg2);
+          const float zp = zsum(i - 1, gamma, lg2, zin);
           dg += qs * (mprev[r] * zp) + es * zp;
+        } else if (cr.e0) {
+          cr.e0[(int64_t)b * D + col] = es;
         }
       }
     }
@@ -463,7 +504,9 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
 // i's sum; the last row of each batch element is zero), in the compute type,
 // as the left operand of the W_m backward products.  The first workgroup
 // also clears dwp and dgamma (when given), which later kernels of the pass
-// accumulate into with atomics.
+// accumulate into with atomics.  In a chunk that follows earlier blocks
+// (Pc not null) block 0 was injected with Pc[b], and its sum goes to
+// Pbar_c[b].
 template <typename T>
 __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
                                                        const T* __restrict__ G,
@@ -471,7 +514,9 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
                                                        T* __restrict__ dU, T* __restrict__ Pbar,
                                                        float* __restrict__ zero_a, int na,
                                                        float* __restrict__ zero_b, int Tn, int D,
-                                                       int L, int nb) {
+                                                       int L, int nb,
+                                                       const float* __restrict__ Pc,
+                                                       T* __restrict__ Pbar_c) {
   constexpr int VE = Vec16<T>::N;
   typedef typename Vec16<T>::type vec;
   __shared__ float racc[kTg][kVec * VE];
@@ -493,8 +538,9 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     c[e] = 0.f;
     acc[e] = 0.f;
   }
-  if (act && i > 0) {
-    const f32x4* pp = reinterpret_cast<const f32x4*>(P + (int64_t)(b * nb + i - 1) * D + col);
+  if (act && (i > 0 || Pc)) {
+    const f32x4* pp = reinterpret_cast<const f32x4*>(
+        i > 0 ? P + (int64_t)(b * nb + i - 1) * D + col : Pc + (int64_t)b * D + col);
 #pragma unroll
     for (int q = 0; q < VE / 4; ++q) {
       const f32x4 w = pp[q];
@@ -536,6 +582,69 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     for (int k = 0; k < kTg; ++k) sum += racc[k][cc];
     const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * D + c0 + cc;
     Pbar[dst] = from_f32<T>(i > 0 ? sum : 0.f);
+    if (i == 0 && Pbar_c) Pbar_c[(int64_t)b * D + c0 + cc] = from_f32<T>(sum);
+  }
+}
+
+// ------------------------------------------------------------------ chunk state
+// One workgroup per sequence.  carry_prep: copy of the incoming state and its
+// memory Nin / Zin in the compute type (the operand of the W_m product that
+// feeds the chunk's first block); zero when there is no incoming state.
+template <typename T>
+__global__ __launch_bounds__(256) void carry_prep_kernel(const float* __restrict__ Nu,
+                                                         const float* __restrict__ Zu,
+                                                         float* __restrict__ Nin,
+                                                         float* __restrict__ Zin,
+                                                         T* __restrict__ Mct,
+                                                         float* __restrict__ Pc, int D) {
+  const int b = blockIdx.x;
+  const float z = Zu ? Zu[b] : 0.f;
+  for (int c = threadIdx.x; c < D; c += blockDim.x) {
+    const int64_t o = (int64_t)b * D + c;
+    const float n = Nu ? Nu[o] : 0.f;
+    Nin[o] = n;
+    Mct[o] = from_f32<T>(z > 0.f ? n / z : 0.f);
+    if (Pc) Pc[o] = 0.f;
+  }
+  if (threadIdx.x == 0) Zin[b] = z;
+}
+
+// carry_finish: gradients of the incoming state.  With M_in = Nin / Zin and
+// dMc = dPc Wm^T its gradient through the first block's context,
+//   N_0 = g Nin + S_0 and Z_0 = g Zin + 1 give
+//   dNin = dMc / Zin + g dS_0,
+//   dZin = sum_cols (g E_0 - dMc . M_in / Zin),
+//   dgamma += sum_cols (dS_0 Nin + E_0 Zin)
+// (the dMc terms vanish for an empty history, Zin = 0).
+__global__ __launch_bounds__(256) void carry_finish_kernel(
+    const float* __restrict__ Nin, const float* __restrict__ Zin, const float* __restrict__ dMc,
+    const float* __restrict__ dS, const float* __restrict__ e0, float* __restrict__ dNin,
+    float* __restrict__ dZin, float* __restrict__ dgamma, int nb, int D, float gamma) {
+  __shared__ float red[2][4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const float z = Zin[b];
+  float ez = 0.f, dg = 0.f;
+  for (int c = tid; c < D; c += blockDim.x) {
+    const int64_t o = (int64_t)b * D + c;
+    const float n = Nin[o], dm = dMc[o], e = e0[o];
+    const float q = dS[(int64_t)b * nb * D + c];
+    const float dmz = z > 0.f ? dm / z : 0.f;
+    if (dNin) dNin[o] = dmz + gamma * q;
+    ez += gamma * e - (z > 0.f ? dmz * (n / z) : 0.f);
+    dg += q * n + e * z;
+  }
+  ez = wave_sum(ez);
+  dg = wave_sum(dg);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = ez;
+    red[1][tid >> 6] = dg;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float tz = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const float tg = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    if (dZin) dZin[b] = tz;
+    if (dgamma) unsafeAtomicAdd(dgamma, tg);
   }
 }
 
@@ -774,12 +883,12 @@ hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, cons
 template <typename E>
 hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, void* Pbar,
                       float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                      hipStream_t s) {
+                      const float* Pc, void* Pbar_c, hipStream_t s) {
   const int nb = (T + L - 1) / L;
   const int cw = kVec * Vec16<E>::N;
   hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
                      (const E*)dY, (const E*)G, P, (E*)dU, (E*)Pbar, zero_a, na, zero_b, T, D, L,
-                     nb);
+                     nb, Pc, (E*)Pbar_c);
   return hipGetLastError();
 }
 
@@ -798,16 +907,17 @@ size_t mem_part_bytes(int B, int nb, int D) {
 }
 
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
-                   float* P, float* part, int B, int nb, int D, float gamma, hipStream_t s) {
+                   float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
+                   hipStream_t s) {
   if (!mem_fused(nb)) {
     // M from the scan, then P = M W_m as a matrix product.
     const dim3 grid((D + kScCols - 1) / kScCols, B);
     if (dt == DType::BF16)
       hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
-                         (bf16*)Mt, nb, D, gamma);
+                         (bf16*)Mt, nb, D, gamma, c);
     else
       hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
-                         (float*)Mt, nb, D, gamma);
+                         (float*)Mt, nb, D, gamma, c);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     GemmDesc g{B * nb, D, D, Mt, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -821,25 +931,25 @@ hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, flo
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, true>), grid, dim3(kMsWaves * 64), lds, s,
                        (const bf16*)St, (const bf16*)Wm, S, M, (bf16*)Mt, P, nullptr, nullptr,
-                       nullptr, nb, D, gamma, kcr);
+                       nullptr, nb, D, gamma, kcr, c);
   else
     hipLaunchKernelGGL((memscan_kernel<float, true>), grid, dim3(kMsWaves * 64), lds, s,
                        (const float*)St, (const float*)Wm, S, M, (float*)Mt, P, nullptr, nullptr,
-                       nullptr, nb, D, gamma, kcr);
+                       nullptr, nb, D, gamma, kcr, c);
   return hipGetLastError();
 }
 
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                    hipStream_t s) {
+                    const float* Pc, void* Pbar_c, hipStream_t s) {
   if (dt == DType::BF16)
-    return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, s);
-  return gate_bwd_t<float>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, s);
+    return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, Pc, Pbar_c, s);
+  return gate_bwd_t<float>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, Pc, Pbar_c, s);
 }
 
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
                    float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
-                   hipStream_t s) {
+                   const Carry& c, hipStream_t s) {
   if (!mem_fused(nb)) {
     // dM = dP W_m^T as a matrix product, then the reverse scans.
     GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
@@ -848,21 +958,50 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, f
     const dim3 grid((D + kScCols - 1) / kScCols, B);
     if (dt == DType::BF16)
       hipLaunchKernelGGL(scan_bwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, dM, M, dS,
-                         dgamma, nb, D, gamma);
+                         dgamma, nb, D, gamma, c);
     else
       hipLaunchKernelGGL(scan_bwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, dM, M,
-                         dS, dgamma, nb, D, gamma);
+                         dS, dgamma, nb, D, gamma, c);
     return hipGetLastError();
   }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
                        (const bf16*)Pbar, (const bf16*)Wm, nullptr, nullptr, nullptr, nullptr, M,
-                       dS, dgamma, nb, D, gamma, 0);
+                       dS, dgamma, nb, D, gamma, 0, c);
   else
     hipLaunchKernelGGL((memscan_kernel<float, false>), grid, dim3(kMsWaves * 64), 0, s,
                        (const float*)Pbar, (const float*)Wm, nullptr, nullptr, nullptr, nullptr, M,
-                       dS, dgamma, nb, D, gamma, 0);
+                       dS, dgamma, nb, D, gamma, 0, c);
+  return hipGetLastError();
+}
+
+hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, float* Zin,
+                      void* Mct, float* Pc, int B, int D, hipStream_t s) {
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(carry_prep_kernel<bf16>, dim3(B), dim3(256), 0, s, Nu, Zu, Nin, Zin,
+                       (bf16*)Mct, Pc, D);
+  else
+    hipLaunchKernelGGL(carry_prep_kernel<float>, dim3(B), dim3(256), 0, s, Nu, Zu, Nin, Zin,
+                       (float*)Mct, Pc, D);
+  return hipGetLastError();
+}
+
+size_t carry_part_bytes(int B, int D) { return gemm_splitk_partial_bytes(B, D, D, kMemMinK); }
+
+hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
+                      bool transposed, int B, int D, hipStream_t s) {
+  // B(k, n) = Wm[k, n] (Pc = Mct Wm) or Wm[n, k] (dMc = Pbar_c Wm^T).
+  GemmDesc g{B, D, D, A, D, false, {Wm, nullptr, nullptr}, D, !transposed, kSegNone, 0, 1};
+  return gemm_splitk(dt, g, part, out, nullptr, nullptr, D, D, false, kMemMinK, s);
+}
+
+hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
+                        const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
+                        int D, float gamma, hipStream_t s) {
+  if (!dNin && !dZin && !dgamma) return hipSuccess;
+  hipLaunchKernelGGL(carry_finish_kernel, dim3(B), dim3(256), 0, s, Nin, Zin, dMc, dS, e0, dNin,
+                     dZin, dgamma, nb, D, gamma);
   return hipGetLastError();
 }
 

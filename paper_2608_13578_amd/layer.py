@@ -65,3 +65,17 @@ class LayerBuffers:
     def backward(self, X, dY, dX, grads, stream=None):
         abi.bcmt_layer_backward(self.cfg, X, self.params, self.saved, dY, dX, grads, self.ws_bwd,
                                 stream=stream)
+
+    def new_carry(self):
+        """A zeroed memory state (N [B, D], Z [B], float32): an empty history."""
+        B, _, D = self.shape
+        f = dict(dtype=torch.float32, device=self.device)
+        return torch.zeros((B, D), **f), torch.zeros((B,), **f)
+
+    def forward_chunk(self, X, Y, carry_in, carry_out, stream=None):
+        abi.bcmt_layer_forward_chunk(self.cfg, X, self.params, carry_in, Y, carry_out, self.saved,
+                                     self.ws_fwd, stream=stream)
+
+    def backward_chunk(self, X, dY, dcarry_out, dX, dcarry_in, grads, stream=None):
+        abi.bcmt_layer_backward_chunk(self.cfg, X, self.params, self.saved, dY, dcarry_out, dX,
+                                      dcarry_in, grads, self.ws_bwd, stream=stream)

@@ -162,3 +162,41 @@ def test_backward_argument_errors(lib):
     assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dgamma misaligned
     g = abi.bcmt_grads(*([A + 0x50000008] + [None] * 7))
     assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dWq misaligned
+
+
+def _carry(N, Z):
+    return abi.bcmt_carry(N, Z)
+
+
+def test_chunk_argument_errors(lib):
+    """The chunked entry points check their states before anything runs."""
+    c = good()
+    p = _params()
+    ws_f = abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_FORWARD)
+    ws_b = abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_BACKWARD)
+    ok = _carry(A + 0x70000000, A + 0x71000000)
+
+    def fwd(cin, cout, X=A):
+        return lib.bcmt_layer_forward_chunk(
+            ctypes.byref(c), X, ctypes.byref(p), ctypes.byref(cin) if cin else None,
+            A + 0x10000000, ctypes.byref(cout) if cout else None, A + 0x20000000,
+            A + 0x40000000, ws_f, None)
+
+    def bwd(dout, din, saved=A + 0x20000000):
+        return lib.bcmt_layer_backward_chunk(
+            ctypes.byref(c), A, ctypes.byref(p), saved, A + 0x30000000,
+            ctypes.byref(dout) if dout else None, A + 0x38000000,
+            ctypes.byref(din) if din else None, None, A + 0x40000000, ws_b, None)
+
+    for bad in (_carry(None, A + 0x71000000), _carry(A + 0x70000000, None),
+                _carry(A + 0x70000008, A + 0x71000000), _carry(A + 0x70000000, A + 0x71000002)):
+        assert fwd(bad, None) == abi.BCMT_ERR_INVALID
+        assert fwd(ok, bad) == abi.BCMT_ERR_INVALID
+        assert bwd(bad, None) == abi.BCMT_ERR_INVALID
+        assert bwd(ok, bad) == abi.BCMT_ERR_INVALID
+    assert fwd(ok, ok, X=None) == abi.BCMT_ERR_INVALID
+    assert bwd(ok, ok, saved=None) == abi.BCMT_ERR_INVALID
+    # the chunked passes use the same workspace sizes
+    assert lib.bcmt_layer_forward_chunk(ctypes.byref(c), A, ctypes.byref(p), None, A + 0x10000000,
+                                        None, A + 0x20000000, A + 0x40000000, ws_f - 1,
+                                        None) == abi.BCMT_ERR_WORKSPACE

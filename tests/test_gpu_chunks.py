@@ -1,0 +1,223 @@
+"""Parity of the chunked entry points (a memory state carried across calls).
+
+A sequence cut at block boundaries runs as consecutive chunks, each continuing
+the decayed memory recurrence of Sec. 3.5 from the state the previous chunk
+left; the backward runs the chunks in reverse, each handing the gradient of
+its incoming state to the chunk before it.  Every case compares, tensor by
+tensor with max|gpu - ref| / max|ref|, the GPU chunks with the oracle's
+chunks on the same inputs: each chunk's output and outgoing state, the
+input gradients, the weight and decay gradients summed over the chunks, and
+each chunk's incoming-state gradient.  Bounds: 2e-2 for bf16, 1e-4 for
+float32.
+"""
+
+import numpy as np
+import pytest
+
+from test_gpu_parity import GRADS, TOL, compare, inputs, say, torch_cuda  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+
+def _to_dev(torch, a):
+    return None if a is None else torch.tensor(np.asarray(a, dtype=np.float32), device="cuda")
+
+
+def _host(t):
+    return t.detach().double().cpu().numpy()
+
+
+def gpu_chunks(torch, B, cuts, D, H, L, dtype, X, W, dY, gamma=0.8, residual=False,
+               carry0=None, dcarry_last=None, inplace=False):
+    """Chained forward over the chunks, then the backward in reverse."""
+    from paper_2608_13578_amd.layer import LayerBuffers, to_device, to_host64
+    cin = None if carry0 is None else tuple(_to_dev(torch, a) for a in carry0)
+    runs, ys, carries = [], [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        lb = LayerBuffers(B, b - a, D, H, L, gamma=gamma, dtype=dtype, residual=residual,
+                          accumulate=True)
+        lb.set_params(W)
+        Xd = to_device(X[:, a:b], dtype)
+        Yd = lb.new_activation()
+        cout = cin if (inplace and cin is not None) else lb.new_carry()
+        lb.forward_chunk(Xd, Yd, cin, cout)
+        torch.cuda.synchronize()
+        ys.append(to_host64(Yd))
+        carries.append((_host(cout[0]), _host(cout[1])))
+        runs.append((lb, Xd, a, b))
+        cin = cout
+    out = {"Y": np.concatenate(ys, axis=1), "carries": carries}
+    if dY is None:
+        return out
+    grads = runs[0][0].new_grads()
+    dcarry = None if dcarry_last is None else tuple(_to_dev(torch, a) for a in dcarry_last)
+    dxs, dins = [], []
+    for lb, Xd, a, b in reversed(runs):
+        dYd = to_device(dY[:, a:b], dtype)
+        dXd = lb.new_activation()
+        din = dcarry if (inplace and dcarry is not None) else lb.new_carry()
+        lb.backward_chunk(Xd, dYd, dcarry, dXd, din, grads)
+        torch.cuda.synchronize()
+        dxs.append(to_host64(dXd))
+        dins.append((_host(din[0]), _host(din[1])))
+        dcarry = din
+    out["dX"] = np.concatenate(dxs[::-1], axis=1)
+    for k in GRADS:
+        out[k] = _host(grads[k])
+    out["dgamma"] = float(grads["dgamma"][0].item())
+    out["dcarries"] = dins[::-1]
+    return out
+
+
+def oracle_chunks(B, cuts, D, H, L, X, W, dY, gamma=0.8, residual=False, carry0=None,
+                  dcarry_last=None):
+    from oracle import bcmt_oracle as orc
+    from paper_2608_13578_amd.inputs import to_f64
+    P = to_f64(W)
+    carry = (np.zeros((B, D)), np.zeros(B)) if carry0 is None else \
+        tuple(np.asarray(a, dtype=np.float64) for a in carry0)
+    ys, caches, carries = [], [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        Y, c = orc.forward(X[:, a:b].astype(np.float64), P, L, H, gamma, residual, carry=carry)
+        ys.append(Y)
+        caches.append((c, a, b))
+        carry = c["carry_out"]
+        carries.append(carry)
+    out = {"Y": np.concatenate(ys, axis=1), "carries": carries}
+    if dY is None:
+        return out
+    dcarry = None if dcarry_last is None else tuple(np.asarray(a, np.float64) for a in dcarry_last)
+    dxs, dins, grads = [], [], []
+    for c, a, b in reversed(caches):
+        g = orc.backward(c, dY[:, a:b].astype(np.float64), dcarry=dcarry)
+        dxs.append(g["dX"])
+        grads.append(g)
+        dcarry = (g["dN_in"], g["dZ_in"])
+        dins.append(dcarry)
+    out["dX"] = np.concatenate(dxs[::-1], axis=1)
+    for k in GRADS + ("dgamma",):
+        out[k] = sum(g[k] for g in grads)
+    out["dcarries"] = dins[::-1]
+    return out
+
+
+def compare_chunks(gpu, ref, dtype, label, tol=None):
+    """Tensors, plus each chunk's outgoing state and incoming-state gradient."""
+    flat_g = {k: v for k, v in gpu.items() if k not in ("carries", "dcarries")}
+    flat_r = {k: v for k, v in ref.items() if k not in ("carries", "dcarries")}
+    for n, (cg, cr) in enumerate(zip(gpu["carries"], ref["carries"])):
+        flat_g[f"N_out{n}"], flat_g[f"Z_out{n}"] = cg
+        flat_r[f"N_out{n}"], flat_r[f"Z_out{n}"] = cr
+    for n, (cg, cr) in enumerate(zip(gpu.get("dcarries", []), ref.get("dcarries", []))):
+        flat_g[f"dN_in{n}"], flat_g[f"dZ_in{n}"] = cg
+        flat_r[f"dN_in{n}"], flat_r[f"dZ_in{n}"] = cr
+    compare(flat_g, flat_r, dtype, label, tol)
+
+
+def _state(rng, B, D, Z):
+    """An arbitrary incoming state: N = Z * m with m ~ N(0, 0.5^2) columns, so
+    that the memory N / Z is of the size of a summary."""
+    Z = np.asarray(Z, dtype=np.float32)
+    N = (rng.standard_normal((B, D)).astype(np.float32) * 0.5) * Z[:, None]
+    return N, Z
+
+
+CHAINS = [
+    # name, B, cuts, D, H, L, dtype, w_std, gamma, residual
+    # at most 32 blocks per chunk: the single-kernel memory path; the last
+    # chunk ends with a partial block
+    ("bf16-fused-ragged", 2, [0, 256, 640, 1000], 256, 4, 128, "bf16", 0.02, 0.8, False),
+    # 50 blocks per chunk: the parallel scans and the W_m matrix products
+    ("f32-long-scans", 2, [0, 800, 1600], 128, 2, 16, "f32", 0.05, 0.9, False),
+    ("f32-fused-residual-gamma0", 1, [0, 96, 160, 320], 192, 3, 32, "f32", 0.05, 0.0, True),
+]
+
+
+@pytest.mark.parametrize("case", CHAINS, ids=[c[0] for c in CHAINS])
+def test_chained_chunks(torch_cuda, case):
+    name, B, cuts, D, H, L, dtype, ws, gamma, res = case
+    say(f"chunks {name}: B={B} cuts={cuts} D={D} H={H} L={L} {dtype}")
+    X, W, dY = inputs(B, cuts[-1], D, dtype, w_std=ws)
+    gpu = gpu_chunks(torch_cuda, B, cuts, D, H, L, dtype, X, W, dY, gamma, res)
+    ref = oracle_chunks(B, cuts, D, H, L, X, W, dY, gamma, res)
+    compare_chunks(gpu, ref, dtype, name)
+
+
+STATES = [
+    # name, B, T, D, H, L, dtype, w_std, gamma, Z_in (0: empty history)
+    ("f32-fused-state", 2, 256, 128, 2, 64, "f32", 0.05, 0.8, [0.0, 2.7]),
+    ("bf16-long-state", 2, 2560, 256, 4, 32, "bf16", 0.02, 0.8, [3.1, 4.6]),
+    ("f32-long-state-gamma0", 2, 1200, 128, 2, 16, "f32", 0.05, 0.0, [1.0, 0.0]),
+]
+
+
+@pytest.mark.parametrize("case", STATES, ids=[c[0] for c in STATES])
+def test_chunk_with_arbitrary_state(torch_cuda, case):
+    """One chunk after an arbitrary history, with a gradient arriving for its
+    outgoing state."""
+    name, B, T, D, H, L, dtype, ws, gamma, Z = case
+    say(f"state {name}: B={B} T={T} D={D} H={H} L={L} {dtype} Z_in={Z}")
+    X, W, dY = inputs(B, T, D, dtype, w_std=ws)
+    rng = np.random.default_rng(7)
+    N0, Z0 = _state(rng, B, D, Z)
+    N0[np.asarray(Z) == 0] = 0.0
+    dN = rng.standard_normal((B, D)).astype(np.float32)
+    dZ = rng.standard_normal(B).astype(np.float32)
+    cuts = [0, T]
+    gpu = gpu_chunks(torch_cuda, B, cuts, D, H, L, dtype, X, W, dY, gamma, carry0=(N0, Z0),
+                     dcarry_last=(dN, dZ))
+    ref = oracle_chunks(B, cuts, D, H, L, X, W, dY, gamma, carry0=(N0, Z0), dcarry_last=(dN, dZ))
+    compare_chunks(gpu, ref, dtype, name)
+
+
+def test_state_buffers_in_place(torch_cuda):
+    """carry_out may be carry_in and dcarry_in may be dcarry_out: the results
+    equal those of separate buffers bit for bit."""
+    torch = torch_cuda
+    B, cuts, D, H, L = 2, [0, 512, 1024], 256, 4, 64
+    X, W, dY = inputs(B, cuts[-1], D, "bf16")
+    rng = np.random.default_rng(3)
+    c0 = _state(rng, B, D, [1.5, 2.0])
+    d0 = (rng.standard_normal((B, D)).astype(np.float32), rng.standard_normal(B).astype(np.float32))
+    a = gpu_chunks(torch, B, cuts, D, H, L, "bf16", X, W, dY, carry0=c0, dcarry_last=d0)
+    b = gpu_chunks(torch, B, cuts, D, H, L, "bf16", X, W, dY, carry0=c0, dcarry_last=d0,
+                   inplace=True)
+    for k in ("Y", "dX") + GRADS:
+        assert np.array_equal(a[k], b[k]), k
+    for x, y in zip(a["carries"] + a["dcarries"], b["carries"] + b["dcarries"]):
+        assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+    assert abs(a["dgamma"] - b["dgamma"]) <= 1e-5 * abs(a["dgamma"])
+
+
+@pytest.mark.parametrize("dtype,T,D,H,L", [("bf16", 512, 256, 4, 64), ("f32", 2048, 128, 2, 32)])
+def test_empty_history_is_the_plain_layer(torch_cuda, dtype, T, D, H, L):
+    """A chunk with no incoming state computes what the plain entry points
+    compute: identical outputs and gradients (dgamma to its atomics'
+    rounding)."""
+    torch = torch_cuda
+    from test_gpu_parity import run_gpu
+    B = 2
+    X, W, dY = inputs(B, T, D, dtype, w_std=0.05)
+    plain = run_gpu(torch, B, T, D, H, L, dtype, X, W, dY)
+    ch = gpu_chunks(torch, B, [0, T], D, H, L, dtype, X, W, dY)
+    for k in ("Y", "dX") + GRADS:
+        assert np.array_equal(plain[k], ch[k]), k
+    assert abs(plain["dgamma"] - ch["dgamma"]) <= 1e-5 * abs(plain["dgamma"])
+
+
+def test_long_context_chunks_match_whole_sequence(torch_cuda):
+    """B=2, T=16384, D=1024, H=16, L=256 (64 blocks) as four chunks of 4096
+    tokens against the whole sequence in one call, both on the GPU: the two
+    differ only in where bf16 rounding happens, so every tensor agrees to the
+    bf16 bound; the outgoing state's memory equals the last block's memory."""
+    torch = torch_cuda
+    from test_gpu_parity import run_gpu
+    B, T, D, H, L = 2, 16384, 1024, 16, 256
+    X, W, dY = inputs(B, T, D, "bf16")
+    whole = run_gpu(torch, B, T, D, H, L, "bf16", X, W, dY)
+    ch = gpu_chunks(torch, B, [0, 4096, 8192, 12288, 16384], D, H, L, "bf16", X, W, dY)
+    flat = {k: ch[k] for k in ("Y", "dX", "dgamma") + GRADS}
+    compare(flat, {k: whole[k] for k in flat}, "bf16", "long-context-chunks")
+    N, Z = ch["carries"][-1]
+    z64 = (1 - 0.8 ** (T // L)) / (1 - 0.8)
+    assert np.allclose(Z, z64, rtol=1e-5)
