@@ -160,11 +160,13 @@ def cpu_baseline(seconds_target=12.0):
 LONG = {"B": 2, "T": 65536, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}
 
 
-def long_context(make_step, torch, abi, dt, steps=10, warmup=3):
+def long_context(make_step, torch, abi, dt, steps=10, warmup=3, make_chunked=None, chunks=4):
     """Layer throughput at the long-context shape and, per bandwidth-bound
     stage (and the attention kernels), bytes moved / stage time against the
     HBM peak.  Stage times come from the library's per-stage tracer (every
-    stage alone on one stream)."""
+    stage alone on one stream).  With make_chunked, the same sequence also
+    runs as `chunks` consecutive calls of the chunked entry points (the
+    memory state handed from chunk to chunk, the backward in reverse)."""
     g = LONG
     B, T, D, H, L = g["B"], g["T"], g["D"], g["H"], g["L"]
     es = 2 if dt == "bf16" else 4
@@ -207,9 +209,30 @@ def long_context(make_step, torch, abi, dt, steps=10, warmup=3):
         gbs = amount / avg_s / 1e9
         res[name] = {"us": round(avg_s * 1e6, 1), "bytes": amount, "GB/s": round(gbs, 1),
                      "frac": round(gbs / PEAK["hbm_gbs"], 3)}
-    return {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} {dt}",
-            "tokens_per_s": round(B * T / (ms / 1e3), 1), "ms_per_step": round(ms, 3),
-            "hbm_stages": res}
+    out = {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} {dt}",
+           "tokens_per_s": round(B * T / (ms / 1e3), 1), "ms_per_step": round(ms, 3),
+           "hbm_stages": res}
+    if make_chunked is not None:
+        del step, keep
+        torch.cuda.empty_cache()
+        cstep, ckeep = make_chunked(B, T, D, H, L, g["gamma"], chunks)
+        for _ in range(warmup):
+            cstep()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            cstep()
+        e1.record()
+        torch.cuda.synchronize()
+        cms = e0.elapsed_time(e1) / steps
+        print(f"  as {chunks} chunks of {T // chunks} tokens: {cms * 1e3:.1f} us per step",
+              file=sys.stderr)
+        out["chunked"] = {"chunks": chunks, "tokens_per_chunk": T // chunks,
+                          "tokens_per_s": round(B * T / (cms / 1e3), 1),
+                          "ms_per_step": round(cms, 3),
+                          "time_vs_one_call": round(cms / ms, 3)}
+        del cstep, ckeep
+    return out
 
 
 def main():
@@ -258,6 +281,37 @@ def main():
             lb.forward(Xd, Yd)
             lb.backward(Xd, dYd, dXd, grads)
         return step, (lb, Xd, dYd, Yd, dXd, grads)
+
+    def make_chunked(B, T, D, H, L, gamma, n):
+        """Forward over n consecutive chunks (state handed on), then the
+        backward from the last chunk to the first (state gradient handed
+        back), weight gradients accumulated."""
+        X, [W] = make_layer_inputs(B, T, D, seed=0, bf16=True)
+        dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
+        tc = T // n
+        runs = []
+        grads = None
+        for k in range(n):
+            lb = LayerBuffers(B, tc, D, H, L, gamma=gamma, dtype=dt, accumulate=True)
+            lb.set_params(W)
+            Xd = to_device(X[:, k * tc:(k + 1) * tc], dt)
+            dYd = to_device(dY[:, k * tc:(k + 1) * tc], dt)
+            if grads is None:
+                grads = lb.new_grads()
+            runs.append((lb, Xd, dYd, lb.new_activation(), lb.new_activation(), lb.new_carry(),
+                         lb.new_carry()))
+        del X, dY
+
+        def step():
+            cin = None
+            for lb, Xd, dYd, Yd, dXd, cout, dcin in runs:
+                lb.forward_chunk(Xd, Yd, cin, cout)
+                cin = cout
+            dcout = None
+            for lb, Xd, dYd, Yd, dXd, cout, dcin in reversed(runs):
+                lb.backward_chunk(Xd, dYd, dcout, dXd, dcin, grads)
+                dcout = dcin
+        return step, (runs, grads)
 
     step, keep = make_step(B, T, D, H, L, w["gamma"])
     for _ in range(args.warmup):
@@ -342,7 +396,7 @@ def main():
     if not args.no_long_context:
         del keep, step
         torch.cuda.empty_cache()
-        out["long_context"] = long_context(make_step, torch, abi, dt)
+        out["long_context"] = long_context(make_step, torch, abi, dt, make_chunked=make_chunked)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)
