@@ -197,6 +197,46 @@ int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_
                               void* dX, const bcmt_carry* dcarry_in, const bcmt_grads* grads,
                               void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Incremental decoding ------------------------------------------------
+ * The layer is causal (Sec. 3.6): the output of token t of block i depends
+ * on the tokens of block i up to t (Sec. 3.3) and on the context C_i, which
+ * the earlier blocks fix (Sec. 3.5, 3.7).  The decoder produces the layer's
+ * output one token at a time for B sequences in step, from a decode state
+ * that holds, per sequence, the current block's keys, values and local
+ * outputs H (compute type), their pooling scores, the memory state (N, Z)
+ * and the current block's context C (float32).  When a block's last token
+ * has been decoded, the block's summary enters the memory and the next
+ * block's context is formed, as in the layer.  Token by token, the outputs
+ * equal those of bcmt_layer_forward over the whole sequence.
+ *
+ * cfg gives B, D, H, L, gamma, dtype and the residual flag (T is not used);
+ * the decoder also needs L <= 4096 and B <= 64 (else BCMT_ERR_UNSUPPORTED).
+ * The state and the workspace are caller-owned device buffers of the sizes
+ * below (0 for an unsupported config); the workspace is scratch. */
+size_t bcmt_decode_state_bytes(const bcmt_config* cfg);
+size_t bcmt_decode_workspace_bytes(const bcmt_config* cfg);
+
+/* Starts decoding at a block boundary.  carry_in: the memory state after the
+ * blocks already processed (for example the carry_out of
+ * bcmt_layer_forward_chunk over a prompt of whole blocks), or NULL to start
+ * a sequence.  Reads params->Wm only (the context (N / Z) Wm of the first
+ * block); the other params members may be NULL. */
+int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* params,
+                      const bcmt_carry* carry_in, void* state, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* Decodes one token per sequence.
+ *   t  index of the token counted from the last reset (0, 1, 2, ...); the
+ *      caller passes consecutive values, each once.  Token t sits at
+ *      position t mod L of its block; t mod L == L - 1 completes the block.
+ *   x  [B, D] the new token's layer input (dtype), read.
+ *   y  [B, D] its layer output (dtype), written; must not overlap x.
+ * The enqueued work allocates nothing and has a fixed launch sequence for a
+ * given t mod L (suitable for capture in a HIP graph per position). */
+int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* params, int64_t t,
+                     const void* x, void* y, void* state, void* ws, size_t ws_bytes,
+                     void* stream);
+
 /* Static description of a status code. */
 const char* bcmt_strerror(int status);
 

@@ -33,7 +33,9 @@ BCMT_PASS_BACKWARD = 2
 
 EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_layer_forward",
             "bcmt_layer_backward", "bcmt_layer_forward_chunk", "bcmt_layer_backward_chunk",
-            "bcmt_strerror", "bcmt_version", "bcmt_trace_enable", "bcmt_trace_read")
+            "bcmt_decode_state_bytes", "bcmt_decode_workspace_bytes", "bcmt_decode_reset",
+            "bcmt_decode_step", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
+            "bcmt_trace_read")
 
 PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
 GRAD_NAMES = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp", "dgamma")
@@ -102,6 +104,16 @@ def lib():
                                                 carryp, vp, carryp, ctypes.POINTER(bcmt_grads),
                                                 vp, ctypes.c_size_t, vp]
         L.bcmt_layer_backward_chunk.restype = ctypes.c_int
+        L.bcmt_decode_state_bytes.argtypes = [cfgp]
+        L.bcmt_decode_state_bytes.restype = ctypes.c_size_t
+        L.bcmt_decode_workspace_bytes.argtypes = [cfgp]
+        L.bcmt_decode_workspace_bytes.restype = ctypes.c_size_t
+        L.bcmt_decode_reset.argtypes = [cfgp, ctypes.POINTER(bcmt_params), carryp, vp, vp,
+                                        ctypes.c_size_t, vp]
+        L.bcmt_decode_reset.restype = ctypes.c_int
+        L.bcmt_decode_step.argtypes = [cfgp, ctypes.POINTER(bcmt_params), ctypes.c_int64, vp, vp,
+                                       vp, vp, ctypes.c_size_t, vp]
+        L.bcmt_decode_step.restype = ctypes.c_int
         L.bcmt_strerror.argtypes = [ctypes.c_int]
         L.bcmt_strerror.restype = ctypes.c_char_p
         L.bcmt_version.argtypes = []
@@ -142,6 +154,13 @@ def _params(p):
     if isinstance(p, bcmt_params):
         return p
     return bcmt_params(*[_ptr(p[n]) for n in PARAM_NAMES])
+
+
+def _params_partial(p):
+    """Like _params, but members missing from a dict are NULL."""
+    if isinstance(p, bcmt_params):
+        return p
+    return bcmt_params(*[_ptr(p.get(n)) for n in PARAM_NAMES])
 
 
 def _grads(g):
@@ -228,6 +247,33 @@ def bcmt_layer_backward_chunk(cfg, X, params, saved, dY, dcarry_out, dX, dcarry_
                                          _stream(stream))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_layer_backward_chunk")
+
+
+def bcmt_decode_state_bytes(cfg):
+    return lib().bcmt_decode_state_bytes(ctypes.byref(cfg))
+
+
+def bcmt_decode_workspace_bytes(cfg):
+    return lib().bcmt_decode_workspace_bytes(ctypes.byref(cfg))
+
+
+def bcmt_decode_reset(cfg, params, carry_in, state, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    st = lib().bcmt_decode_reset(ctypes.byref(cfg), ctypes.byref(_params_partial(params)),
+                                 _ref(_carry(carry_in)), _ptr(state), _ptr(ws), int(ws_bytes),
+                                 _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_decode_reset")
+
+
+def bcmt_decode_step(cfg, params, t, x, y, state, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    st = lib().bcmt_decode_step(ctypes.byref(cfg), ctypes.byref(_params(params)), int(t), _ptr(x),
+                                _ptr(y), _ptr(state), _ptr(ws), int(ws_bytes), _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_decode_step")
 
 
 def bcmt_trace_enable(on):

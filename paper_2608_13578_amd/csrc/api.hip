@@ -126,6 +126,48 @@ struct Plan {
   }
 };
 
+// Decode state (the current block's caches and the memory state) and the
+// scratch of one decode step.
+struct DecPlan {
+  int B, D, H, L;
+  DType dt;
+  size_t es;
+  size_t Kc, Vc, Hc, spc, N, Z, C, tickets, state_bytes;
+  size_t q, o, Mt, part, cpart, ws_bytes;
+
+  explicit DecPlan(const bcmt_config& c) {
+    B = c.B;
+    D = c.D;
+    H = c.H;
+    L = c.L;
+    dt = c.dtype == BCMT_BF16 ? DType::BF16 : DType::F32;
+    es = dt == DType::BF16 ? 2 : 4;
+    const size_t BLD = (size_t)B * L * D, BD = (size_t)B * D;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+      size_t at = off;
+      off += up(bytes);
+      return at;
+    };
+    Kc = take(BLD * es);
+    Vc = take(BLD * es);
+    Hc = take(BLD * es);
+    spc = take((size_t)B * L * dec_score_parts(dt, D) * 4);
+    N = take(BD * 4);
+    Z = take((size_t)B * 4);
+    C = take(BD * 4);
+    tickets = take((size_t)kDecTickets * 4);
+    state_bytes = off;
+    off = 0;
+    q = take(BD * es);
+    o = take(BD * es);
+    Mt = take(BD * es);
+    part = take(dec_part_bytes(dt, B, D));
+    cpart = take(carry_part_bytes(B, D));
+    ws_bytes = off;
+  }
+};
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_config(const bcmt_config* c) {
@@ -149,6 +191,13 @@ bool overlaps(const void* a, const void* b, size_t n) {
   return x < y + n && y < x + n;
 }
 
+int check_decode(const bcmt_config* c) {
+  const int st = check_config(c);
+  if (st != BCMT_OK) return st;
+  if (c->L > dec_max_blocklen() || c->B > dec_max_batch()) return BCMT_ERR_UNSUPPORTED;
+  return BCMT_OK;
+}
+
 // A chunk state, when given, needs both members: N 16-byte and Z 4-byte aligned.
 bool carry_ok(const bcmt_carry* c) {
   if (!c) return true;
@@ -164,6 +213,7 @@ enum Stage {
   ST_WM_WGRAD_RED, ST_CARRY_WGRAD, ST_CARRY_DGRAD, ST_MEM_BWD, ST_CARRY_BWD, ST_POOL_BWD, ST_DWP,
   ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
+  ST_DEC_RESET, ST_DEC_QKV, ST_DEC_ATTN, ST_DEC_WO, ST_DEC_GATE, ST_DEC_POOL, ST_DEC_MEM,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
@@ -174,7 +224,9 @@ const char* const kStageNames[ST_COUNT] = {
     "bwd.carry_dgrad_gemm", "bwd.memory_scan", "bwd.carry_in", "bwd.pool", "bwd.pool_dwp",
     "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
-    "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce"};
+    "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce",
+    "dec.reset", "dec.qkv_gemv", "dec.attention", "dec.wo_gemv", "dec.gate_gemv", "dec.pool",
+    "dec.wm_gemv"};
 
 struct Tracer {
   std::atomic<bool> on{false};
@@ -638,6 +690,78 @@ int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_
                               void* ws, size_t ws_bytes, void* stream) {
   return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, true, dcarry_out,
                         dcarry_in);
+}
+
+size_t bcmt_decode_state_bytes(const bcmt_config* cfg) {
+  if (check_decode(cfg) != BCMT_OK) return 0;
+  return DecPlan(*cfg).state_bytes;
+}
+
+size_t bcmt_decode_workspace_bytes(const bcmt_config* cfg) {
+  if (check_decode(cfg) != BCMT_OK) return 0;
+  return DecPlan(*cfg).ws_bytes;
+}
+
+int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* prm, const bcmt_carry* carry_in,
+                      void* state, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_decode(cfg);
+  if (st != BCMT_OK) return st;
+  if (!prm || !prm->Wm || !aligned16(prm->Wm) || !carry_ok(carry_in)) return BCMT_ERR_INVALID;
+  if (!state || !aligned16(state) || !ws || !aligned16(ws)) return BCMT_ERR_INVALID;
+  DecPlan p(*cfg);
+  if (ws_bytes < p.ws_bytes) return BCMT_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  char* S = (char*)state;
+  char* W = (char*)ws;
+  // The memory state and the first block's context (N / Z) Wm, or zeros.
+  LAUNCH(ST_DEC_RESET, carry_prep(p.dt, carry_in ? carry_in->N : nullptr,
+                                  carry_in ? carry_in->Z : nullptr, (float*)(S + p.N),
+                                  (float*)(S + p.Z), W + p.Mt,
+                                  carry_in ? nullptr : (float*)(S + p.C), p.B, p.D, s));
+  if (carry_in)
+    LAUNCH(ST_DEC_RESET, carry_proj(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C),
+                                    (float*)(W + p.cpart), false, p.B, p.D, s));
+  LAUNCH(ST_DEC_RESET, fill_f32((float*)(S + p.tickets), kDecTickets, 0.f, s));
+  return BCMT_OK;
+}
+
+int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* prm, int64_t t, const void* x,
+                     void* y, void* state, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_decode(cfg);
+  if (st != BCMT_OK) return st;
+  if (t < 0 || !x || !y || !prm || !state || !ws) return BCMT_ERR_INVALID;
+  const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
+  for (const void* q : w)
+    if (!q || !aligned16(q)) return BCMT_ERR_INVALID;
+  if (!aligned16(x) || !aligned16(y) || !aligned16(state) || !aligned16(ws))
+    return BCMT_ERR_INVALID;
+  DecPlan p(*cfg);
+  if (overlaps(x, y, (size_t)p.B * p.D * p.es)) return BCMT_ERR_INVALID;
+  if (ws_bytes < p.ws_bytes) return BCMT_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  char* S = (char*)state;
+  char* W = (char*)ws;
+  const int off = (int)(t % p.L);
+  float* part = (float*)(W + p.part);
+  unsigned* tk = (unsigned*)(S + p.tickets);
+  LAUNCH(ST_DEC_QKV, dec_qkv(p.dt, x, prm->Wq, prm->Wk, prm->Wv, W + p.q, S + p.Kc, S + p.Vc, p.B,
+                             p.D, p.L, off, part, tk, s));
+  LAUNCH(ST_DEC_ATTN, dec_attn(p.dt, W + p.q, S + p.Kc, S + p.Vc, W + p.o, p.B, p.D, p.H, p.L,
+                               off, s));
+  LAUNCH(ST_DEC_WO, dec_wo(p.dt, W + p.o, prm->Wo, prm->wp, S + p.Hc, (float*)(S + p.spc), p.B,
+                           p.D, p.L, off, part, tk, s));
+  LAUNCH(ST_DEC_GATE, dec_gate(p.dt, prm->Wg, S + p.Hc, (const float*)(S + p.C),
+                               (cfg->flags & BCMT_FLAG_RESIDUAL) ? x : nullptr, y, p.B, p.D, p.L,
+                               off, part, tk, s));
+  if (off == p.L - 1) {
+    // The block is complete: its summary enters the memory, which gives the
+    // next block's context.
+    LAUNCH(ST_DEC_POOL, dec_pool(p.dt, S + p.Hc, (const float*)(S + p.spc), (float*)(S + p.N),
+                                 (const float*)(S + p.Z), W + p.Mt, p.B, p.D, p.L, cfg->gamma, s));
+    LAUNCH(ST_DEC_MEM, dec_mem(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C), (float*)(S + p.Z), p.B,
+                               p.D, cfg->gamma, part, tk, s));
+  }
+  return BCMT_OK;
 }
 
 }  // extern "C"

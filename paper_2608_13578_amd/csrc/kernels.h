@@ -195,6 +195,36 @@ int64_t pool_bwd_partial_rows(DType dt, int B, int T, int D, int L);
 hipError_t pool_dwp(float* dwp_part, DType dt, int B, int T, int D, int L, float* dwp,
                     bool accumulate, hipStream_t s);
 hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
+
+// ------------------------------------------------------------------ decoding
+// One more token per sequence (decode.hip).  The block caches hold, per
+// sequence, L rows of D: keys Kc, values Vc and local outputs Hc (compute
+// type), and the score parts spc [B, L, dec_score_parts] (float32); N, Z
+// and C are the memory state and the current block's context (float32).
+// The matrix-vector products share `part` (dec_part_bytes) and `tickets`
+// (kDecTickets counters, zero between products; each product leaves them
+// zero).  `off` is the new token's slot in its block.
+constexpr int kDecTickets = 2048;
+int dec_max_blocklen();
+int dec_max_batch();
+int dec_score_parts(DType dt, int D);
+size_t dec_part_bytes(DType dt, int B, int D);
+hipError_t dec_qkv(DType dt, const void* x, const void* Wq, const void* Wk, const void* Wv,
+                   void* q, void* Kc, void* Vc, int B, int D, int L, int off, float* part,
+                   unsigned* tickets, hipStream_t s);
+hipError_t dec_attn(DType dt, const void* q, const void* Kc, const void* Vc, void* o, int B,
+                    int D, int H, int L, int off, hipStream_t s);
+hipError_t dec_wo(DType dt, const void* o, const void* Wo, const void* wp, void* Hc, float* spc,
+                  int B, int D, int L, int off, float* part, unsigned* tickets, hipStream_t s);
+hipError_t dec_gate(DType dt, const void* Wg, const void* Hc, const float* C, const void* x,
+                    void* y, int B, int D, int L, int off, float* part, unsigned* tickets,
+                    hipStream_t s);
+// After the block's last token: pooling, N = g N + S, Mt = N / (g Z + 1).
+hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const float* Z, void* Mt,
+                    int B, int D, int L, float gamma, hipStream_t s);
+// C = Mt Wm, Z = g Z + 1.
+hipError_t dec_mem(DType dt, const void* Mt, const void* Wm, float* C, float* Z, int B, int D,
+                   float gamma, float* part, unsigned* tickets, hipStream_t s);
 // Zeroes two small float32 buffers in one launch (either may be null).
 hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);
 

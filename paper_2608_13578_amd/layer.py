@@ -79,3 +79,30 @@ class LayerBuffers:
     def backward_chunk(self, X, dY, dcarry_out, dX, dcarry_in, grads, stream=None):
         abi.bcmt_layer_backward_chunk(self.cfg, X, self.params, self.saved, dY, dcarry_out, dX,
                                       dcarry_in, grads, self.ws_bwd, stream=stream)
+
+
+class DecodeBuffers:
+    """Decode state and workspace for B sequences decoded in step."""
+
+    def __init__(self, B, D, H, L, gamma=0.8, dtype="bf16", residual=False, device="cuda"):
+        self.dtype = dtype
+        self.device = device
+        self.cfg = abi.make_config(B, 1, D, H, L, gamma, dtype, residual)
+        u8 = dict(dtype=torch.uint8, device=device)
+        n = abi.bcmt_decode_state_bytes(self.cfg)
+        if n == 0:
+            raise abi.BcmtError(abi.BCMT_ERR_UNSUPPORTED, "bcmt_decode_state_bytes")
+        self.state = torch.empty(n, **u8)
+        self.ws = torch.empty(max(256, abi.bcmt_decode_workspace_bytes(self.cfg)), **u8)
+        self.shape = (B, D)
+        self.params = None
+
+    def set_params(self, weights):
+        self.params = {k: to_device(weights[k], self.dtype, self.device) for k in abi.PARAM_NAMES}
+        return self.params
+
+    def reset(self, carry_in=None, stream=None):
+        abi.bcmt_decode_reset(self.cfg, self.params, carry_in, self.state, self.ws, stream=stream)
+
+    def step(self, t, x, y, stream=None):
+        abi.bcmt_decode_step(self.cfg, self.params, t, x, y, self.state, self.ws, stream=stream)

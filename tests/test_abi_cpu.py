@@ -200,3 +200,39 @@ def test_chunk_argument_errors(lib):
     assert lib.bcmt_layer_forward_chunk(ctypes.byref(c), A, ctypes.byref(p), None, A + 0x10000000,
                                         None, A + 0x20000000, A + 0x40000000, ws_f - 1,
                                         None) == abi.BCMT_ERR_WORKSPACE
+
+
+def test_decode_sizes_and_argument_errors(lib):
+    """Decode sizes follow the config; bad arguments fail before any launch."""
+    c = good()
+    sb = abi.bcmt_decode_state_bytes(c)
+    wb = abi.bcmt_decode_workspace_bytes(c)
+    assert sb > 0 and wb > 0
+    assert abi.bcmt_decode_state_bytes(good(L=128)) > sb      # caches grow with L
+    assert abi.bcmt_decode_state_bytes(good(L=5000)) == 0     # block too long to decode
+    assert abi.bcmt_decode_state_bytes(good(B=65)) == 0       # batch too large to decode
+    assert abi.bcmt_decode_state_bytes(good(B=0)) == 0
+    p = _params()
+    st, ws = A + 0x20000000, A + 0x40000000
+
+    def step(t=0, x=A, y=A + 0x10000000, state=st, w=ws, n=wb, cfg=c):
+        return lib.bcmt_decode_step(ctypes.byref(cfg), ctypes.byref(p), t, x, y, state, w, n, None)
+
+    assert step(t=-1) == abi.BCMT_ERR_INVALID
+    assert step(x=None) == abi.BCMT_ERR_INVALID
+    assert step(y=A) == abi.BCMT_ERR_INVALID                 # y aliases x
+    assert step(y=A + 8) == abi.BCMT_ERR_INVALID             # misaligned
+    assert step(state=None) == abi.BCMT_ERR_INVALID
+    assert step(n=wb - 1) == abi.BCMT_ERR_WORKSPACE
+    assert step(cfg=good(L=5000)) == abi.BCMT_ERR_UNSUPPORTED
+    assert lib.bcmt_decode_step(ctypes.byref(c), ctypes.byref(_params(Wg=None)), 0, A,
+                                A + 0x10000000, st, ws, wb, None) == abi.BCMT_ERR_INVALID
+    # reset reads only Wm
+    none = abi.bcmt_params(*([None] * 7))
+    assert lib.bcmt_decode_reset(ctypes.byref(c), ctypes.byref(none), None, st, ws, wb,
+                                 None) == abi.BCMT_ERR_INVALID
+    bad = abi.bcmt_carry(A + 0x70000000, None)
+    assert lib.bcmt_decode_reset(ctypes.byref(c), ctypes.byref(p), ctypes.byref(bad), st, ws, wb,
+                                 None) == abi.BCMT_ERR_INVALID
+    assert lib.bcmt_decode_reset(ctypes.byref(c), ctypes.byref(p), None, st, ws, wb - 1,
+                                 None) == abi.BCMT_ERR_WORKSPACE
