@@ -235,6 +235,60 @@ def long_context(make_step, torch, abi, dt, steps=10, warmup=3, make_chunked=Non
     return out
 
 
+DECODE = [{"B": 8, "D": 768, "H": 12, "L": 128, "gamma": 0.8},
+          {"B": 2, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}]
+
+
+def decode_bench(torch, abi, dt, g, blocks=2, warmup_blocks=1):
+    """Incremental decoding: time per decode step (one token for each of B
+    sequences) over `blocks` whole blocks, and the per-stage times.  The
+    weights a step must read (Wq, Wk, Wv, Wo, Wg; Wm once per block) set its
+    bandwidth floor."""
+    from paper_2608_13578_amd.inputs import make_layer_inputs
+    from paper_2608_13578_amd.layer import DecodeBuffers, to_device
+    B, D, H, L = g["B"], g["D"], g["H"], g["L"]
+    es = 2 if dt == "bf16" else 4
+    X, [W] = make_layer_inputs(B, L, D, seed=0, bf16=True)
+    db = DecodeBuffers(B, D, H, L, gamma=g["gamma"], dtype=dt)
+    db.set_params(W)
+    xs = [to_device(X[:, t], dt) for t in range(L)]
+    y = torch.empty((B, D), dtype=xs[0].dtype, device="cuda")
+    db.reset()
+    t = 0
+    for _ in range(warmup_blocks * L):
+        db.step(t, xs[t % L], y)
+        t += 1
+    torch.cuda.synchronize()
+    n = blocks * L
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n):
+        db.step(t, xs[t % L], y)
+        t += 1
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / n
+    abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(True)
+    for _ in range(n):
+        db.step(t, xs[t % L], y)
+        t += 1
+    torch.cuda.synchronize()
+    stages = abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(False)
+    wbytes = (5 * D * D + D * D / L) * es
+    print(f"decode B={B} D={D} H={H} L={L}: {us:.1f} us per step", file=sys.stderr)
+    per = {}
+    for name, calls, total in stages:
+        per[name] = round(total / calls * 1e3, 2)
+        print(f"  {name:24s} {total / calls * 1e3:10.2f} us  x{calls / n:.3f} per step",
+              file=sys.stderr)
+    return {"workload": f"bcmt-layer decode B={B} D={D} H={H}x64 L={L} {dt}",
+            "us_per_step": round(us, 2), "tokens_per_s": round(B / (us * 1e-6), 1),
+            "weight_bytes_per_step": int(wbytes),
+            "weight_GB/s": round(wbytes / (us * 1e-6) / 1e9, 1), "stage_us": per}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -243,6 +297,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the long-context pass (bandwidth kernels at T=65536)")
+    ap.add_argument("--no-decode", action="store_true", help="skip the incremental decoding pass")
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
                          "library's stage tracing on (every stage serialised on one stream, "
@@ -397,6 +452,8 @@ def main():
         del keep, step
         torch.cuda.empty_cache()
         out["long_context"] = long_context(make_step, torch, abi, dt, make_chunked=make_chunked)
+    if not args.no_decode:
+        out["decode"] = [decode_bench(torch, abi, dt, g) for g in DECODE]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)

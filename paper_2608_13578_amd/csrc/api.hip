@@ -132,8 +132,8 @@ struct DecPlan {
   int B, D, H, L;
   DType dt;
   size_t es;
-  size_t Kc, Vc, Hc, spc, N, Z, C, tickets, state_bytes;
-  size_t q, o, Mt, part, cpart, ws_bytes;
+  size_t Kc, Vc, Hc, spc, N, Z, C, state_bytes;
+  size_t o, Mt, part, cpart, ws_bytes;
 
   explicit DecPlan(const bcmt_config& c) {
     B = c.B;
@@ -152,14 +152,12 @@ struct DecPlan {
     Kc = take(BLD * es);
     Vc = take(BLD * es);
     Hc = take(BLD * es);
-    spc = take((size_t)B * L * dec_score_parts(dt, D) * 4);
+    spc = take((size_t)B * L * dec_score_parts(D) * 4);
     N = take(BD * 4);
     Z = take((size_t)B * 4);
     C = take(BD * 4);
-    tickets = take((size_t)kDecTickets * 4);
     state_bytes = off;
     off = 0;
-    q = take(BD * es);
     o = take(BD * es);
     Mt = take(BD * es);
     part = take(dec_part_bytes(dt, B, D));
@@ -213,7 +211,8 @@ enum Stage {
   ST_WM_WGRAD_RED, ST_CARRY_WGRAD, ST_CARRY_DGRAD, ST_MEM_BWD, ST_CARRY_BWD, ST_POOL_BWD, ST_DWP,
   ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
-  ST_DEC_RESET, ST_DEC_QKV, ST_DEC_ATTN, ST_DEC_WO, ST_DEC_GATE, ST_DEC_POOL, ST_DEC_MEM,
+  ST_DEC_RESET, ST_DEC_QKV, ST_DEC_ATTN, ST_DEC_WO, ST_DEC_WO_FIN, ST_DEC_GATE, ST_DEC_GATE_FIN,
+  ST_DEC_POOL, ST_DEC_MEM, ST_DEC_MEM_FIN,
   ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
@@ -225,8 +224,8 @@ const char* const kStageNames[ST_COUNT] = {
     "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce",
-    "dec.reset", "dec.qkv_gemv", "dec.attention", "dec.wo_gemv", "dec.gate_gemv", "dec.pool",
-    "dec.wm_gemv"};
+    "dec.reset", "dec.qkv_gemv", "dec.attention", "dec.wo_gemv", "dec.wo_finish",
+    "dec.gate_gemv", "dec.gate_finish", "dec.pool", "dec.wm_gemv", "dec.wm_finish"};
 
 struct Tracer {
   std::atomic<bool> on{false};
@@ -721,7 +720,6 @@ int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* prm, const bcmt
   if (carry_in)
     LAUNCH(ST_DEC_RESET, carry_proj(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C),
                                     (float*)(W + p.cpart), false, p.B, p.D, s));
-  LAUNCH(ST_DEC_RESET, fill_f32((float*)(S + p.tickets), kDecTickets, 0.f, s));
   return BCMT_OK;
 }
 
@@ -743,23 +741,32 @@ int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* prm, int64_t t, 
   char* W = (char*)ws;
   const int off = (int)(t % p.L);
   float* part = (float*)(W + p.part);
-  unsigned* tk = (unsigned*)(S + p.tickets);
-  LAUNCH(ST_DEC_QKV, dec_qkv(p.dt, x, prm->Wq, prm->Wk, prm->Wv, W + p.q, S + p.Kc, S + p.Vc, p.B,
-                             p.D, p.L, off, part, tk, s));
-  LAUNCH(ST_DEC_ATTN, dec_attn(p.dt, W + p.q, S + p.Kc, S + p.Vc, W + p.o, p.B, p.D, p.H, p.L,
+  const int D = p.D;
+  const int ks3 = dec_splits(p.dt, D, 3 * D, p.B), ks1 = dec_splits(p.dt, D, D, p.B);
+  // [q k v] = x [Wq Wk Wv] (K-split partial sums), then attention over the
+  // block's cache, which first adds them up and appends k and v.
+  LAUNCH(ST_DEC_QKV, dec_product(p.dt, x, D, prm->Wq, prm->Wk, prm->Wv, p.B, D, 3 * D, part, s));
+  LAUNCH(ST_DEC_ATTN, dec_attn(p.dt, part, ks3, S + p.Kc, S + p.Vc, W + p.o, p.B, D, p.H, p.L,
                                off, s));
-  LAUNCH(ST_DEC_WO, dec_wo(p.dt, W + p.o, prm->Wo, prm->wp, S + p.Hc, (float*)(S + p.spc), p.B,
-                           p.D, p.L, off, part, tk, s));
-  LAUNCH(ST_DEC_GATE, dec_gate(p.dt, prm->Wg, S + p.Hc, (const float*)(S + p.C),
-                               (cfg->flags & BCMT_FLAG_RESIDUAL) ? x : nullptr, y, p.B, p.D, p.L,
-                               off, part, tk, s));
+  // h = o Wo (cached, with its pooling score), then the gate and injection.
+  LAUNCH(ST_DEC_WO, dec_product(p.dt, W + p.o, D, prm->Wo, nullptr, nullptr, p.B, D, D, part, s));
+  LAUNCH(ST_DEC_WO_FIN, dec_wo_finish(p.dt, part, ks1, prm->wp, S + p.Hc, (float*)(S + p.spc),
+                                      p.B, D, p.L, off, s));
+  char* hrow = S + p.Hc + (size_t)off * D * p.es;
+  LAUNCH(ST_DEC_GATE, dec_product(p.dt, hrow, (int64_t)p.L * D, prm->Wg, nullptr, nullptr, p.B, D,
+                                  D, part, s));
+  LAUNCH(ST_DEC_GATE_FIN, dec_gate_finish(p.dt, part, ks1, S + p.Hc, (const float*)(S + p.C),
+                                          (cfg->flags & BCMT_FLAG_RESIDUAL) ? x : nullptr, y, p.B,
+                                          D, p.L, off, s));
   if (off == p.L - 1) {
     // The block is complete: its summary enters the memory, which gives the
     // next block's context.
     LAUNCH(ST_DEC_POOL, dec_pool(p.dt, S + p.Hc, (const float*)(S + p.spc), (float*)(S + p.N),
-                                 (const float*)(S + p.Z), W + p.Mt, p.B, p.D, p.L, cfg->gamma, s));
-    LAUNCH(ST_DEC_MEM, dec_mem(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C), (float*)(S + p.Z), p.B,
-                               p.D, cfg->gamma, part, tk, s));
+                                 (const float*)(S + p.Z), W + p.Mt, p.B, D, p.L, cfg->gamma, s));
+    LAUNCH(ST_DEC_MEM, dec_product(p.dt, W + p.Mt, D, prm->Wm, nullptr, nullptr, p.B, D, D, part,
+                                   s));
+    LAUNCH(ST_DEC_MEM_FIN, dec_mem_finish(part, ks1, (float*)(S + p.C), (float*)(S + p.Z), p.B, D,
+                                          cfg->gamma, s));
   }
   return BCMT_OK;
 }

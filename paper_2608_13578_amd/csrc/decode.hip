@@ -14,13 +14,14 @@
 // block's context C = (N / Z) Wm.
 //
 // The products have a handful of rows (the sequences) against a [D, N]
-// weight, so they are weight-streaming matrix-vector products: a workgroup
-// reads a 32-row by 64-column (bf16) tile of the weight per round, lanes
-// owning 16-byte column vectors, and keeps every sequence's partial sums.
-// K is split over workgroups; the last workgroup to finish a column tile
-// (an atomic ticket per tile, reset by that workgroup) adds the K partials
-// in a fixed order and applies the step's epilogue, so each product is one
-// launch and its result is the same on every run.
+// weight: they are weight-streaming matrix-vector products, and what bounds
+// them is how many loads are in flight per CU.  So each product is split
+// into 250-400 workgroups of a few KB of weights each (64 columns x 32-128
+// rows, one round of 16-byte loads per lane), writing partial sums per K
+// split; a second small kernel adds the splits in a fixed order and applies
+// the step's epilogue (for the QKV product the attention kernel does it).
+// The kernel boundary makes the partials visible across the chip's L2s, so
+// nothing synchronises inside a kernel, and every run gives the same result.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -32,12 +33,10 @@ namespace bcmt {
 namespace {
 
 constexpr int kDvB = 8;                     // sequences per workgroup
-constexpr int kDvWaves = 4;
 constexpr int kDvLanesPerRow = 8;           // a row of the column tile: 8 lanes x 16 bytes
 constexpr int kDvRowsPerWave = 64 / kDvLanesPerRow;
-constexpr int kDvRowStep = kDvWaves * kDvRowsPerWave;  // rows per round (32)
-constexpr int kDvMaxKc = 256;               // K rows per workgroup at most
-constexpr int kDvUnroll = 4;                // rounds whose loads are issued together
+constexpr int kDvRowStep = 4 * kDvRowsPerWave;  // rows per round of the 4 waves (32)
+constexpr int kDvMaxKc = 128;               // K rows per workgroup at most (4 rounds)
 constexpr int kDecMaxBatch = 64;
 
 template <typename T>
@@ -55,45 +54,55 @@ struct DvW {
   }
 };
 
-template <typename T, class Epi>
-__global__ __launch_bounds__(kDvWaves * 64) void dec_gemv_kernel(
-    const T* __restrict__ x, int64_t ldx, int B, DvW<T> w, int K, int N, int kc,
-    float* __restrict__ part, unsigned* __restrict__ tickets, Epi epi) {
+// part[ky][b][n] = sum over the rows k of split ky of x[b, k] W[k, n], for a
+// column tile of CT columns, kc rows (a multiple of 32) and up to kDvB
+// sequences per workgroup.  Lane (column vector cg, row lane rl) of wave w
+// takes rows w*8 + rl + 32u; the row lanes meet by shuffles, the waves in
+// LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void dec_gemv_part_kernel(const T* __restrict__ x, int64_t ldx,
+                                                            int B, DvW<T> w, int K, int N, int kc,
+                                                            float* __restrict__ part) {
   constexpr int VE = Vec16<T>::N, CT = dv_cols<T>();
   __shared__ float xs[kDvB][kDvMaxKc];
-  __shared__ float red[kDvWaves][kDvB][CT];
-  __shared__ float vals[kDvB][CT];
-  __shared__ int last;
+  __shared__ float red[4][kDvB][CT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n0 = blockIdx.x * CT;
   const int k0 = blockIdx.y * kc;
   const int b0 = blockIdx.z * kDvB;
   const int nbt = min(kDvB, B - b0);
   const int kn = min(kc, K - k0);
-  // Every entry is written (zeros past the rows and sequences present), so
-  // the rounds past kn multiply zero weights by zeros.
-  for (int e = tid; e < kDvB * kDvMaxKc; e += blockDim.x) {
-    const int b = e / kDvMaxKc, k = e % kDvMaxKc;
-    xs[b][k] = (b < nbt && k < kn) ? to_f32(x[(int64_t)(b0 + b) * ldx + k0 + k]) : 0.f;
+  // The weight tile's loads go out first; x (tiny) is staged meanwhile.
+  const int cg = lane % kDvLanesPerRow, rl = lane / kDvLanesPerRow;
+  const T* wcol = w.col(n0 + cg * VE) + (int64_t)k0 * w.ld;
+  constexpr int U = kDvMaxKc / kDvRowStep;
+  typename Vec16<T>::type wv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int r = wave * kDvRowsPerWave + rl + u * kDvRowStep;
+    wv[u] = r < kn ? load16(wcol + (int64_t)r * w.ld) : typename Vec16<T>::type{};
+  }
+  // x[b0.., k0..k0+kc) as 16-byte vectors (kc and K are multiples of 32).
+  {
+    const int kv = kc / VE;
+    for (int e = tid; e < kDvB * kv; e += blockDim.x) {
+      const int b = e / kv, k = (e - b * kv) * VE;
+      const auto v = (b < nbt && k < kn) ? load16(x + (int64_t)(b0 + b) * ldx + k0 + k)
+                                         : typename Vec16<T>::type{};
+#pragma unroll
+      for (int q = 0; q < VE; ++q) xs[b][k + q] = to_f32(v[q]);
+    }
   }
   __syncthreads();
-  const int cg = lane % kDvLanesPerRow, rl = lane / kDvLanesPerRow;
-  const T* wcol = w.col(n0 + cg * VE);
   float acc[kDvB][VE];
 #pragma unroll
   for (int b = 0; b < kDvB; ++b)
 #pragma unroll
     for (int e = 0; e < VE; ++e) acc[b][e] = 0.f;
-  for (int r0 = wave * kDvRowsPerWave + rl; r0 < kn; r0 += kDvUnroll * kDvRowStep) {
-    typename Vec16<T>::type wv[kDvUnroll];
 #pragma unroll
-    for (int u = 0; u < kDvUnroll; ++u) {
-      const int r = r0 + u * kDvRowStep;
-      wv[u] = r < kn ? load16(wcol + (int64_t)(k0 + r) * w.ld) : typename Vec16<T>::type{};
-    }
-#pragma unroll
-    for (int u = 0; u < kDvUnroll; ++u) {
-      const int r = min(r0 + u * kDvRowStep, kDvMaxKc - 1);  // zero weights past kn
+  for (int u = 0; u < U; ++u) {
+    const int r = wave * kDvRowsPerWave + rl + u * kDvRowStep;
+    if (r < kn) {
 #pragma unroll
       for (int b = 0; b < kDvB; ++b) {
         const float xb = xs[b][r];
@@ -102,148 +111,173 @@ __global__ __launch_bounds__(kDvWaves * 64) void dec_gemv_kernel(
       }
     }
   }
-  // Lanes of one column vector (same cg) hold different rows: add them up.
+  // The 8 row lanes of a column vector (lane bits 3-5) reduce-scatter their
+  // sums over the 8 sequences: at each step a lane keeps the half of its
+  // sequences whose bit matches its own row-lane bit and receives the
+  // partner's sums for them, so that row lane r ends with sequence r's sums
+  // (56 shuffles per lane instead of 192, each step's shuffles independent).
+  float h4[4][VE], h2[2][VE], h1[VE];
+  {
+    const bool p = rl & 1;
+    float snd[4][VE];
 #pragma unroll
-  for (int b = 0; b < kDvB; ++b)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      float v = acc[b][e];
-      v += __shfl_xor(v, 8);
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      if (rl == 0) red[wave][b][cg * VE + e] = v;
-    }
-  __syncthreads();
-  for (int e = tid; e < kDvB * CT; e += blockDim.x) {
-    const int b = e / CT, c = e % CT;
-    const float v = (red[0][b][c] + red[1][b][c]) + (red[2][b][c] + red[3][b][c]);
-    if (b < nbt && n0 + c < N) part[((int64_t)blockIdx.y * B + b0 + b) * N + n0 + c] = v;
+      for (int e = 0; e < VE; ++e) snd[i][e] = p ? acc[2 * i][e] : acc[2 * i + 1][e];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) snd[i][e] = __shfl_xor(snd[i][e], 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) h4[i][e] = (p ? acc[2 * i + 1][e] : acc[2 * i][e]) + snd[i][e];
   }
-  // Publish the partials, then take a ticket; the last of the K splits of
-  // this tile finishes it.
-  __threadfence();
-  __syncthreads();
-  unsigned* tk = tickets + blockIdx.z * gridDim.x + blockIdx.x;
-  if (tid == 0) last = atomicAdd(tk, 1u) == gridDim.y - 1;
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  for (int e = tid; e < kDvB * CT; e += blockDim.x) {
-    const int b = e / CT, c = e % CT;
-    float v = 0.f;
-    if (b < nbt && n0 + c < N)
-      for (int s = 0; s < (int)gridDim.y; ++s) v += part[((int64_t)s * B + b0 + b) * N + n0 + c];
-    vals[b][c] = v;
+  {  // h4[i] holds sequence 2i + (rl & 1)
+    const bool p = (rl >> 1) & 1;
+    float snd[2][VE];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) snd[i][e] = p ? h4[2 * i][e] : h4[2 * i + 1][e];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) snd[i][e] = __shfl_xor(snd[i][e], 16);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) h2[i][e] = (p ? h4[2 * i + 1][e] : h4[2 * i][e]) + snd[i][e];
   }
-  if (tid == 0) *tk = 0u;  // ready for the next product
+  {  // h2[i] holds sequence 4i + (rl & 3)
+    const bool p = (rl >> 2) & 1;
+    float snd[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) snd[e] = p ? h2[0][e] : h2[1][e];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) snd[e] = __shfl_xor(snd[e], 32);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) h1[e] = (p ? h2[1][e] : h2[0][e]) + snd[e];
+  }
+  // h1 holds sequence rl's sums for this lane's column vector
+#pragma unroll
+  for (int e = 0; e < VE; ++e) red[wave][rl][cg * VE + e] = h1[e];
   __syncthreads();
-  epi.finish(b0, nbt, n0, vals, tid);
+  for (int e = tid; e < nbt * CT; e += blockDim.x) {
+    const int b = e / CT, c = e % CT;
+    part[((int64_t)blockIdx.y * B + b0 + b) * N + n0 + c] =
+        (red[0][b][c] + red[1][b][c]) + (red[2][b][c] + red[3][b][c]);
+  }
 }
 
-// [q k v]: q to its buffer, k and v to the block caches at slot `off`.
+// Sum of the K splits of output (b, n), in split order; eight splits' loads
+// are issued before they are added.
+__device__ __forceinline__ float dv_sum(const float* __restrict__ part, int ks, int B, int N, int b,
+                                        int n) {
+  const int64_t stride = (int64_t)B * N;
+  const float* p = part + (int64_t)b * N + n;
+  float v = 0.f;
+  int s = 0;
+  for (; s + 8 <= ks; s += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = p[(s + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += t[u];
+  }
+  for (; s < ks; ++s) v += p[s * stride];
+  return v;
+}
+
+// h = o Wo into the block cache at slot off, and per 64 columns the part of
+// the pooling score h . wp.  Thread = column n of sequence blockIdx.y.
 template <typename T>
-struct EpiDecQkv {
-  T* q;
-  T* Kc;
-  T* Vc;
-  int D, L, off;
-  template <int CT>
-  __device__ void finish(int b0, int nbt, int n0, const float (&v)[kDvB][CT], int tid) const {
-    for (int e = tid; e < nbt * CT; e += blockDim.x) {
-      const int b = e / CT, c = e % CT, n = n0 + c;
-      const int sg = n / D, col = n - sg * D;
-      const T val = from_f32<T>(v[b][c]);
-      if (sg == 0) q[(int64_t)(b0 + b) * D + col] = val;
-      else (sg == 1 ? Kc : Vc)[((int64_t)(b0 + b) * L + off) * D + col] = val;
-    }
-  }
-};
+__global__ __launch_bounds__(256) void dec_wo_finish_kernel(const float* __restrict__ part, int ks,
+                                                            int B, int D, const T* __restrict__ wp,
+                                                            T* __restrict__ Hc,
+                                                            float* __restrict__ spc, int L,
+                                                            int off) {
+  const int b = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool on = n < D;
+  const float v = on ? dv_sum(part, ks, B, D, b, n) : 0.f;
+  if (on) Hc[((int64_t)b * L + off) * D + n] = from_f32<T>(v);
+  const float sc = wave_sum(on ? v * to_f32(wp[n]) : 0.f);
+  if ((threadIdx.x & 63) == 0 && on) spc[((int64_t)b * L + off) * (D / 64) + n / 64] = sc;
+}
 
-// h = o Wo to the block cache, and this tile's part of the score h . wp.
+// y = h + sigmoid(u) C (+ x), u = h Wg.
 template <typename T>
-struct EpiDecWo {
-  T* Hc;
-  float* spc;  // [B, L, np]
-  const T* wp;
-  int D, L, off, np;
-  template <int CT>
-  __device__ void finish(int b0, int nbt, int n0, const float (&v)[kDvB][CT], int tid) const {
-    for (int e = tid; e < nbt * CT; e += blockDim.x) {
-      const int b = e / CT, c = e % CT;
-      Hc[((int64_t)(b0 + b) * L + off) * D + n0 + c] = from_f32<T>(v[b][c]);
-    }
-    if (tid < nbt) {
-      float sc = 0.f;
-      for (int c = 0; c < CT; ++c) sc += v[tid][c] * to_f32(wp[n0 + c]);
-      spc[((int64_t)(b0 + tid) * L + off) * np + n0 / CT] = sc;
-    }
-  }
-};
+__global__ __launch_bounds__(256) void dec_gate_finish_kernel(const float* __restrict__ part,
+                                                              int ks, int B, int D,
+                                                              const T* __restrict__ Hc,
+                                                              const float* __restrict__ C,
+                                                              const T* __restrict__ x,
+                                                              T* __restrict__ y, int L, int off) {
+  const int b = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= D) return;
+  const float u = dv_sum(part, ks, B, D, b, n);
+  const int64_t row = (int64_t)b * D + n;
+  float out = to_f32(Hc[((int64_t)b * L + off) * D + n]) + sigmoidf_(u) * C[row];
+  if (x) out += to_f32(x[row]);
+  y[row] = from_f32<T>(out);
+}
 
-// y = h + sigmoid(u) * C (+ x), u = h Wg.
-template <typename T>
-struct EpiDecGate {
-  T* y;
-  const T* Hc;
-  const float* C;
-  const T* x;  // nullable
-  int D, L, off;
-  template <int CT>
-  __device__ void finish(int b0, int nbt, int n0, const float (&v)[kDvB][CT], int tid) const {
-    for (int e = tid; e < nbt * CT; e += blockDim.x) {
-      const int b = e / CT, c = e % CT, n = n0 + c;
-      const int64_t row = (int64_t)(b0 + b) * D + n;
-      float out = to_f32(Hc[((int64_t)(b0 + b) * L + off) * D + n]) + sigmoidf_(v[b][c]) * C[row];
-      if (x) out += to_f32(x[row]);
-      y[row] = from_f32<T>(out);
-    }
-  }
-};
+// C = Mt Wm for the next block, Z = g Z + 1.
+__global__ __launch_bounds__(256) void dec_mem_finish_kernel(const float* __restrict__ part,
+                                                             int ks, int B, int D,
+                                                             float* __restrict__ C,
+                                                             float* __restrict__ Z, float gamma) {
+  const int b = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= D) return;
+  C[(int64_t)b * D + n] = dv_sum(part, ks, B, D, b, n);
+  if (n == 0) Z[b] = gamma * Z[b] + 1.f;
+}
 
-// C = Mt Wm for the next block; the first column tile also advances Z.
-struct EpiDecMem {
-  float* C;
-  float* Z;
-  int D;
-  float gamma;
-  template <int CT>
-  __device__ void finish(int b0, int nbt, int n0, const float (&v)[kDvB][CT], int tid) const {
-    for (int e = tid; e < nbt * CT; e += blockDim.x) {
-      const int b = e / CT, c = e % CT;
-      C[(int64_t)(b0 + b) * D + n0 + c] = v[b][c];
-    }
-    if (n0 == 0 && tid < nbt) Z[b0 + tid] = gamma * Z[b0 + tid] + 1.f;
-  }
-};
-
-// Attention of the new token over the block's cached tokens 0..off, one
-// workgroup per (head, sequence): scores one key per thread, then thread
-// (dim d, key group g) adds p_j V[j, d] over the keys j = g mod 4.
+// Attention of the new token over the block's tokens 0..off, one workgroup
+// per (head, sequence).  First the QKV product's K splits are added for
+// this head: q, and the new token's k and v, which go to the block cache at
+// slot off and are also kept in LDS for this token's own score and value.
+// Scores: one cached key per thread (its 64 dims as 16-byte loads issued
+// together).  Output: thread (16-byte vector v of the head's dims, key
+// group g) adds p_j V[j] over the cached keys j = g mod G with four keys'
+// loads in flight; the groups meet in LDS.
 constexpr int kDecMaxL = 4096;
 
 template <typename T>
-__global__ __launch_bounds__(256) void dec_attn_kernel(const T* __restrict__ q,
-                                                       const T* __restrict__ Kc,
-                                                       const T* __restrict__ Vc,
-                                                       T* __restrict__ o, int D, int L, int off) {
-  constexpr int VE = Vec16<T>::N;
-  __shared__ float qs[64];
+__global__ __launch_bounds__(256) void dec_attn_kernel(const float* __restrict__ part, int ks,
+                                                       int B, T* __restrict__ Kc,
+                                                       T* __restrict__ Vc, T* __restrict__ o,
+                                                       int D, int L, int off) {
+  constexpr int VE = Vec16<T>::N, NV = 64 / VE;  // 16-byte vectors per head row
+  constexpr int G = 256 / NV;                     // key groups
+  __shared__ float qkv[3][64];                    // q (scaled by 1/8), k, v of the new token
   __shared__ float sc[kDecMaxL];
-  __shared__ float red[4][64];
+  __shared__ float red[G][64];
   __shared__ float wr[4];
   const int tid = threadIdx.x, h = blockIdx.x, b = blockIdx.y;
-  const int n = off + 1;
-  if (tid < 64) qs[tid] = to_f32(q[(int64_t)b * D + h * 64 + tid]) * 0.125f;
+  if (tid < 192) {
+    const int which = tid / 64, d = tid % 64;
+    const float v = dv_sum(part, ks, B, 3 * D, b, which * D + h * 64 + d);
+    const T vt = from_f32<T>(v);  // Q, K and V are stored in the compute type
+    qkv[which][d] = to_f32(vt) * (which == 0 ? 0.125f : 1.f);
+    if (which > 0) (which == 1 ? Kc : Vc)[((int64_t)b * L + off) * D + h * 64 + d] = vt;
+  }
   __syncthreads();
+  const int n = off + 1;
   float mx = -INFINITY;
   for (int j = tid; j < n; j += blockDim.x) {
-    const T* kr = Kc + ((int64_t)b * L + j) * D + h * 64;
     float d = 0.f;
+    if (j == off) {
+      for (int e = 0; e < 64; ++e) d += qkv[0][e] * qkv[1][e];
+    } else {
+      const T* kr = Kc + ((int64_t)b * L + j) * D + h * 64;
+      typename Vec16<T>::type kv[NV];
 #pragma unroll
-    for (int v = 0; v < 64 / VE; ++v) {
-      const auto kv = load16(kr + v * VE);
+      for (int v = 0; v < NV; ++v) kv[v] = load16(kr + v * VE);
 #pragma unroll
-      for (int e = 0; e < VE; ++e) d += qs[v * VE + e] * to_f32(kv[e]);
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < VE; ++e) d += qkv[0][v * VE + e] * to_f32(kv[v][e]);
     }
     sc[j] = d;
     mx = fmaxf(mx, d);
@@ -263,19 +297,45 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const T* __restrict__ q,
   if ((tid & 63) == 0) wr[tid >> 6] = sum;
   __syncthreads();
   const float total = (wr[0] + wr[1]) + (wr[2] + wr[3]);
-  const int d = tid & 63, g = tid >> 6;
-  float acc = 0.f;
-  for (int j = g; j < n; j += 4) acc += sc[j] * to_f32(Vc[((int64_t)b * L + j) * D + h * 64 + d]);
-  red[g][d] = acc;
+  const int vi = tid % NV, g = tid / NV;
+  float acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  const T* vb = Vc + (int64_t)b * L * D + h * 64 + vi * VE;
+  constexpr int U = 4;
+  for (int j0 = g; j0 < off; j0 += U * G) {  // the cached tokens before this one
+    typename Vec16<T>::type vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * G;
+      vv[u] = j < off ? load16(vb + (int64_t)j * D) : typename Vec16<T>::type{};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * G;
+      const float p = j < off ? sc[j] : 0.f;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] += p * to_f32(vv[u][e]);
+    }
+  }
+  if (g == off % G)  // the new token itself
+#pragma unroll
+    for (int e = 0; e < VE; ++e) acc[e] += sc[off] * qkv[2][vi * VE + e];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) red[g][vi * VE + e] = acc[e];
   __syncthreads();
-  if (tid < 64)
-    o[(int64_t)b * D + h * 64 + tid] =
-        from_f32<T>(((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid])) / total);
+  if (tid < 64) {
+    float t = 0.f;
+    for (int k = 0; k < G; ++k) t += red[k][tid];
+    o[(int64_t)b * D + h * 64 + tid] = from_f32<T>(t / total);
+  }
 }
 
 // After a block's last token: a = softmax of the block's scores, S = sum_t
 // a_t H[t] for 64 columns per workgroup, N = g N + S, and the new memory
 // N / (g Z + 1) in the compute type (Z itself advances in the W_m product).
+// Thread (16-byte vector v of the 64 columns, token group g) adds its
+// tokens t = g mod G with four tokens' loads in flight.
 template <typename T>
 __global__ __launch_bounds__(256) void dec_pool_kernel(const T* __restrict__ Hc,
                                                        const float* __restrict__ spc, int np,
@@ -283,8 +343,9 @@ __global__ __launch_bounds__(256) void dec_pool_kernel(const T* __restrict__ Hc,
                                                        const float* __restrict__ Z,
                                                        T* __restrict__ Mt, int D, int L,
                                                        float gamma) {
+  constexpr int VE = Vec16<T>::N, NV = 64 / VE, G = 256 / NV;
   __shared__ float a[kDecMaxL];
-  __shared__ float red[4][64];
+  __shared__ float red[G][64];
   __shared__ float wr[4];
   const int tid = threadIdx.x, b = blockIdx.y, c0 = blockIdx.x * 64;
   float mx = -INFINITY;
@@ -310,121 +371,135 @@ __global__ __launch_bounds__(256) void dec_pool_kernel(const T* __restrict__ Hc,
   if ((tid & 63) == 0) wr[tid >> 6] = sum;
   __syncthreads();
   const float total = (wr[0] + wr[1]) + (wr[2] + wr[3]);
-  const int d = tid & 63, g = tid >> 6;
-  float acc = 0.f;
-  for (int t = g; t < L; t += 4) acc += a[t] * to_f32(Hc[((int64_t)b * L + t) * D + c0 + d]);
-  red[g][d] = acc;
+  const int vi = tid % NV, g = tid / NV;
+  float acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  const T* hb = Hc + (int64_t)b * L * D + c0 + vi * VE;
+  constexpr int U = 4;
+  for (int t0 = g; t0 < L; t0 += U * G) {
+    typename Vec16<T>::type hv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u * G;
+      hv[u] = t < L ? load16(hb + (int64_t)t * D) : typename Vec16<T>::type{};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u * G;
+      const float w = t < L ? a[t] : 0.f;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] += w * to_f32(hv[u][e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VE; ++e) red[g][vi * VE + e] = acc[e];
   __syncthreads();
   if (tid < 64) {
+    float S = 0.f;
+    for (int k = 0; k < G; ++k) S += red[k][tid];
+    S /= total;
     const int64_t o = (int64_t)b * D + c0 + tid;
-    const float S = ((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid])) / total;
     const float nn = gamma * N[o] + S;
     N[o] = nn;
     Mt[o] = from_f32<T>(nn / (gamma * Z[b] + 1.f));
   }
 }
 
-// Split of K over workgroups: enough workgroups to cover the chip, each
-// taking a multiple of 32 rows and at most kDvMaxKc.
+// K split: enough workgroups to cover the chip (about 256), each taking a
+// multiple of 32 rows and at most kDvMaxKc.
 int dv_plan(int K, int N, int B, int cols, int* kc) {
   const int tiles = ((N + cols - 1) / cols) * ((B + kDvB - 1) / kDvB);
-  int ks = (256 + tiles - 1) / tiles;
-  if (ks > K / kDvRowStep) ks = K / kDvRowStep;
-  if (ks < 1) ks = 1;
-  int c = (K + ks - 1) / ks;
-  c = (c + kDvRowStep - 1) / kDvRowStep * kDvRowStep;
+  const int target = (256 + tiles - 1) / tiles;
+  int c = K / target / kDvRowStep * kDvRowStep;
+  if (c < kDvRowStep) c = kDvRowStep;
   if (c > kDvMaxKc) c = kDvMaxKc;
   *kc = c;
   return (K + c - 1) / c;
-}
-
-template <typename T, class Epi>
-hipError_t dv_launch(const T* x, int64_t ldx, int B, DvW<T> w, int K, int N, float* part,
-                     unsigned* tickets, const Epi& epi, hipStream_t s) {
-  constexpr int CT = dv_cols<T>();
-  int kc;
-  const int ks = dv_plan(K, N, B, CT, &kc);
-  dim3 grid((N + CT - 1) / CT, ks, (B + kDvB - 1) / kDvB);
-  hipLaunchKernelGGL((dec_gemv_kernel<T, Epi>), grid, dim3(kDvWaves * 64), 0, s, x, ldx, B, w, K,
-                     N, kc, part, tickets, epi);
-  return hipGetLastError();
-}
-
-template <typename T>
-DvW<T> dv_w(const void* a, const void* b, const void* c, int seg, int64_t ld) {
-  return DvW<T>{{(const T*)a, (const T*)(b ? b : a), (const T*)(c ? c : a)}, seg, ld};
 }
 
 }  // namespace
 
 int dec_max_blocklen() { return kDecMaxL; }
 int dec_max_batch() { return kDecMaxBatch; }
+int dec_score_parts(int D) { return D / 64; }
 
-int dec_score_parts(DType dt, int D) {
-  return D / (dt == DType::BF16 ? dv_cols<bf16>() : dv_cols<float>());
+int dec_splits(DType dt, int K, int N, int B) {
+  int kc;
+  return dv_plan(K, N, B, dt == DType::BF16 ? dv_cols<bf16>() : dv_cols<float>(), &kc);
 }
 
 size_t dec_part_bytes(DType dt, int B, int D) {
-  const int cols = dt == DType::BF16 ? dv_cols<bf16>() : dv_cols<float>();
-  int kc;
-  const size_t a = (size_t)dv_plan(D, 3 * D, B, cols, &kc) * B * 3 * D;
-  const size_t b = (size_t)dv_plan(D, D, B, cols, &kc) * B * D;
+  const size_t a = (size_t)dec_splits(dt, D, 3 * D, B) * B * 3 * D;
+  const size_t b = (size_t)dec_splits(dt, D, D, B) * B * D;
   return (a > b ? a : b) * sizeof(float);
 }
 
-hipError_t dec_qkv(DType dt, const void* x, const void* Wq, const void* Wk, const void* Wv,
-                   void* q, void* Kc, void* Vc, int B, int D, int L, int off, float* part,
-                   unsigned* tickets, hipStream_t s) {
-  if (dt == DType::BF16)
-    return dv_launch<bf16>((const bf16*)x, D, B, dv_w<bf16>(Wq, Wk, Wv, D, D), D, 3 * D, part,
-                           tickets, EpiDecQkv<bf16>{(bf16*)q, (bf16*)Kc, (bf16*)Vc, D, L, off}, s);
-  return dv_launch<float>((const float*)x, D, B, dv_w<float>(Wq, Wk, Wv, D, D), D, 3 * D, part,
-                          tickets, EpiDecQkv<float>{(float*)q, (float*)Kc, (float*)Vc, D, L, off},
-                          s);
-}
-
-hipError_t dec_attn(DType dt, const void* q, const void* Kc, const void* Vc, void* o, int B,
-                    int D, int H, int L, int off, hipStream_t s) {
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(dec_attn_kernel<bf16>, dim3(H, B), dim3(256), 0, s, (const bf16*)q,
-                       (const bf16*)Kc, (const bf16*)Vc, (bf16*)o, D, L, off);
-  else
-    hipLaunchKernelGGL(dec_attn_kernel<float>, dim3(H, B), dim3(256), 0, s, (const float*)q,
-                       (const float*)Kc, (const float*)Vc, (float*)o, D, L, off);
+hipError_t dec_product(DType dt, const void* x, int64_t ldx, const void* W0, const void* W1,
+                       const void* W2, int B, int D, int N, float* part, hipStream_t s) {
+  int kc;
+  if (dt == DType::BF16) {
+    const int ks = dv_plan(D, N, B, dv_cols<bf16>(), &kc);
+    const DvW<bf16> w{{(const bf16*)W0, (const bf16*)(W1 ? W1 : W0), (const bf16*)(W2 ? W2 : W0)},
+                      D, D};
+    hipLaunchKernelGGL(dec_gemv_part_kernel<bf16>, dim3(N / dv_cols<bf16>(), ks, (B + kDvB - 1) / kDvB),
+                       dim3(256), 0, s, (const bf16*)x, ldx, B, w, D, N, kc, part);
+  } else {
+    const int ks = dv_plan(D, N, B, dv_cols<float>(), &kc);
+    const DvW<float> w{
+        {(const float*)W0, (const float*)(W1 ? W1 : W0), (const float*)(W2 ? W2 : W0)}, D, D};
+    hipLaunchKernelGGL(dec_gemv_part_kernel<float>,
+                       dim3(N / dv_cols<float>(), ks, (B + kDvB - 1) / kDvB), dim3(256), 0, s,
+                       (const float*)x, ldx, B, w, D, N, kc, part);
+  }
   return hipGetLastError();
 }
 
-hipError_t dec_wo(DType dt, const void* o, const void* Wo, const void* wp, void* Hc, float* spc,
-                  int B, int D, int L, int off, float* part, unsigned* tickets, hipStream_t s) {
-  const int np = dec_score_parts(dt, D);
+hipError_t dec_attn(DType dt, const float* part, int ks, void* Kc, void* Vc, void* o, int B, int D,
+                    int H, int L, int off, hipStream_t s) {
   if (dt == DType::BF16)
-    return dv_launch<bf16>((const bf16*)o, D, B, dv_w<bf16>(Wo, nullptr, nullptr, D, D), D, D,
-                           part, tickets,
-                           EpiDecWo<bf16>{(bf16*)Hc, spc, (const bf16*)wp, D, L, off, np}, s);
-  return dv_launch<float>((const float*)o, D, B, dv_w<float>(Wo, nullptr, nullptr, D, D), D, D,
-                          part, tickets,
-                          EpiDecWo<float>{(float*)Hc, spc, (const float*)wp, D, L, off, np}, s);
+    hipLaunchKernelGGL(dec_attn_kernel<bf16>, dim3(H, B), dim3(256), 0, s, part, ks, B,
+                       (bf16*)Kc, (bf16*)Vc, (bf16*)o, D, L, off);
+  else
+    hipLaunchKernelGGL(dec_attn_kernel<float>, dim3(H, B), dim3(256), 0, s, part, ks, B,
+                       (float*)Kc, (float*)Vc, (float*)o, D, L, off);
+  return hipGetLastError();
 }
 
-hipError_t dec_gate(DType dt, const void* Wg, const void* Hc, const float* C, const void* x,
-                    void* y, int B, int D, int L, int off, float* part, unsigned* tickets,
-                    hipStream_t s) {
-  const int64_t ldh = (int64_t)L * D;
-  if (dt == DType::BF16) {
-    const bf16* h = (const bf16*)Hc + (int64_t)off * D;
-    return dv_launch<bf16>(h, ldh, B, dv_w<bf16>(Wg, nullptr, nullptr, D, D), D, D, part, tickets,
-                           EpiDecGate<bf16>{(bf16*)y, (const bf16*)Hc, C, (const bf16*)x, D, L,
-                                            off}, s);
-  }
-  const float* h = (const float*)Hc + (int64_t)off * D;
-  return dv_launch<float>(h, ldh, B, dv_w<float>(Wg, nullptr, nullptr, D, D), D, D, part, tickets,
-                          EpiDecGate<float>{(float*)y, (const float*)Hc, C, (const float*)x, D, L,
-                                            off}, s);
+hipError_t dec_wo_finish(DType dt, const float* part, int ks, const void* wp, void* Hc, float* spc,
+                         int B, int D, int L, int off, hipStream_t s) {
+  const dim3 grid((D + 255) / 256, B);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(dec_wo_finish_kernel<bf16>, grid, dim3(256), 0, s, part, ks, B, D,
+                       (const bf16*)wp, (bf16*)Hc, spc, L, off);
+  else
+    hipLaunchKernelGGL(dec_wo_finish_kernel<float>, grid, dim3(256), 0, s, part, ks, B, D,
+                       (const float*)wp, (float*)Hc, spc, L, off);
+  return hipGetLastError();
+}
+
+hipError_t dec_gate_finish(DType dt, const float* part, int ks, const void* Hc, const float* C,
+                           const void* x, void* y, int B, int D, int L, int off, hipStream_t s) {
+  const dim3 grid((D + 255) / 256, B);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(dec_gate_finish_kernel<bf16>, grid, dim3(256), 0, s, part, ks, B, D,
+                       (const bf16*)Hc, C, (const bf16*)x, (bf16*)y, L, off);
+  else
+    hipLaunchKernelGGL(dec_gate_finish_kernel<float>, grid, dim3(256), 0, s, part, ks, B, D,
+                       (const float*)Hc, C, (const float*)x, (float*)y, L, off);
+  return hipGetLastError();
+}
+
+hipError_t dec_mem_finish(const float* part, int ks, float* C, float* Z, int B, int D, float gamma,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(dec_mem_finish_kernel, dim3((D + 255) / 256, B), dim3(256), 0, s, part, ks,
+                     B, D, C, Z, gamma);
+  return hipGetLastError();
 }
 
 hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const float* Z, void* Mt,
                     int B, int D, int L, float gamma, hipStream_t s) {
-  const int np = dec_score_parts(dt, D);
+  const int np = dec_score_parts(D);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(dec_pool_kernel<bf16>, dim3(D / 64, B), dim3(256), 0, s, (const bf16*)Hc,
                        spc, np, N, Z, (bf16*)Mt, D, L, gamma);
@@ -432,15 +507,6 @@ hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const 
     hipLaunchKernelGGL(dec_pool_kernel<float>, dim3(D / 64, B), dim3(256), 0, s, (const float*)Hc,
                        spc, np, N, Z, (float*)Mt, D, L, gamma);
   return hipGetLastError();
-}
-
-hipError_t dec_mem(DType dt, const void* Mt, const void* Wm, float* C, float* Z, int B, int D,
-                   float gamma, float* part, unsigned* tickets, hipStream_t s) {
-  if (dt == DType::BF16)
-    return dv_launch<bf16>((const bf16*)Mt, D, B, dv_w<bf16>(Wm, nullptr, nullptr, D, D), D, D,
-                           part, tickets, EpiDecMem{C, Z, D, gamma}, s);
-  return dv_launch<float>((const float*)Mt, D, B, dv_w<float>(Wm, nullptr, nullptr, D, D), D, D,
-                          part, tickets, EpiDecMem{C, Z, D, gamma}, s);
 }
 
 }  // namespace bcmt

@@ -199,33 +199,33 @@ hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // ------------------------------------------------------------------ decoding
 // One more token per sequence (decode.hip).  The block caches hold, per
 // sequence, L rows of D: keys Kc, values Vc and local outputs Hc (compute
-// type), and the score parts spc [B, L, dec_score_parts] (float32); N, Z
-// and C are the memory state and the current block's context (float32).
-// The matrix-vector products share `part` (dec_part_bytes) and `tickets`
-// (kDecTickets counters, zero between products; each product leaves them
-// zero).  `off` is the new token's slot in its block.
-constexpr int kDecTickets = 2048;
+// type), and the score parts spc [B, L, D / 64] (float32); N, Z and C are
+// the memory state and the current block's context (float32).  `off` is
+// the new token's slot in its block.  A product x [B, D] (row stride ldx)
+// times [D, N] (W0 | W1 | W2, D columns each, or W0 alone with N = D)
+// writes dec_splits() K-split partial sums to `part` (dec_part_bytes), which
+// the next kernel adds up.
 int dec_max_blocklen();
 int dec_max_batch();
-int dec_score_parts(DType dt, int D);
+int dec_score_parts(int D);
+int dec_splits(DType dt, int K, int N, int B);
 size_t dec_part_bytes(DType dt, int B, int D);
-hipError_t dec_qkv(DType dt, const void* x, const void* Wq, const void* Wk, const void* Wv,
-                   void* q, void* Kc, void* Vc, int B, int D, int L, int off, float* part,
-                   unsigned* tickets, hipStream_t s);
-hipError_t dec_attn(DType dt, const void* q, const void* Kc, const void* Vc, void* o, int B,
-                    int D, int H, int L, int off, hipStream_t s);
-hipError_t dec_wo(DType dt, const void* o, const void* Wo, const void* wp, void* Hc, float* spc,
-                  int B, int D, int L, int off, float* part, unsigned* tickets, hipStream_t s);
-hipError_t dec_gate(DType dt, const void* Wg, const void* Hc, const float* C, const void* x,
-                    void* y, int B, int D, int L, int off, float* part, unsigned* tickets,
-                    hipStream_t s);
+hipError_t dec_product(DType dt, const void* x, int64_t ldx, const void* W0, const void* W1,
+                       const void* W2, int B, int D, int N, float* part, hipStream_t s);
+// Adds the QKV splits (k and v to the caches at off), then attention -> o.
+hipError_t dec_attn(DType dt, const float* part, int ks, void* Kc, void* Vc, void* o, int B, int D,
+                    int H, int L, int off, hipStream_t s);
+// h = sum of the splits -> Hc at off, with its score parts -> spc.
+hipError_t dec_wo_finish(DType dt, const float* part, int ks, const void* wp, void* Hc, float* spc,
+                         int B, int D, int L, int off, hipStream_t s);
+// y = h + sigmoid(u) C (+ x), u = sum of the splits.
+hipError_t dec_gate_finish(DType dt, const float* part, int ks, const void* Hc, const float* C,
+                           const void* x, void* y, int B, int D, int L, int off, hipStream_t s);
 // After the block's last token: pooling, N = g N + S, Mt = N / (g Z + 1).
 hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const float* Z, void* Mt,
                     int B, int D, int L, float gamma, hipStream_t s);
-// C = Mt Wm, Z = g Z + 1.
-hipError_t dec_mem(DType dt, const void* Mt, const void* Wm, float* C, float* Z, int B, int D,
-                   float gamma, float* part, unsigned* tickets, hipStream_t s);
-// Zeroes two small float32 buffers in one launch (either may be null).
-hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);
+// C = sum of the splits of Mt Wm, Z = g Z + 1.
+hipError_t dec_mem_finish(const float* part, int ks, float* C, float* Z, int B, int D, float gamma,
+                          hipStream_t s);
 
 }  // namespace bcmt
