@@ -7,8 +7,8 @@
  *
  *   blocks     : N_b = ceil(T / L) contiguous blocks of at most L tokens
  *                (Sec. 3.2; the last block may be shorter);
- *   local MHA  : Q = X Wq, K = X Wk, V = X Wv; per head (D = H * 64) and per
- *                block, softmax(Q K^T / sqrt(64) + causal mask) V, where a
+ *   local MHA  : Q = X Wq, K = X Wk, V = X Wv; per head (width dh = D / H)
+ *                and per block, softmax(Q K^T / sqrt(dh) + causal mask) V, where a
  *                token sees itself and earlier tokens of its own block only
  *                (Sec. 3.3, 3.6); heads concatenated, H = concat * Wo;
  *   summaries  : s = H wp, a = softmax of s over each block's tokens,
@@ -41,7 +41,8 @@
  *     `stream` afterwards sees every output, exactly as if all of it had run
  *     on `stream`.  Calls on one device from several host threads are
  *     serialised while they enqueue.
- *   - The GPU path needs a head width D / H of 64 and D <= 2048.
+ *   - The GPU path needs a head width D / H of 64, 32 or 16 (the paper's
+ *     model uses 16), D a multiple of 64 and D <= 2048.
  *
  * Errors
  *   Negative return values are bcmt_status codes.  All checks on the
@@ -63,7 +64,7 @@ extern "C" {
 typedef enum {
   BCMT_OK = 0,
   BCMT_ERR_INVALID = -1,     /* null or misaligned pointer, bad sizes, decay outside [0,1) */
-  BCMT_ERR_UNSUPPORTED = -2, /* valid layer the GPU path does not run (head width != 64, D > 2048) */
+  BCMT_ERR_UNSUPPORTED = -2, /* valid layer the GPU path does not run (head width not 16/32/64, D % 64, D > 2048) */
   BCMT_ERR_WORKSPACE = -3,   /* workspace smaller than bcmt_workspace_bytes() */
   BCMT_ERR_HIP = -4          /* a HIP launch failed */
 } bcmt_status;
@@ -85,7 +86,7 @@ enum {
 typedef struct {
   int32_t B;     /* sequences */
   int32_t T;     /* tokens per sequence */
-  int32_t D;     /* features, D = H * 64 on the GPU path */
+  int32_t D;     /* features; on the GPU path D = H * dh with dh in {16, 32, 64} */
   int32_t H;     /* attention heads */
   int32_t L;     /* block size (L >= T gives a single block: dense causal attention) */
   float gamma;   /* memory decay, 0 <= gamma < 1 (0**0 is taken as 1) */
@@ -210,7 +211,8 @@ int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_
  * equal those of bcmt_layer_forward over the whole sequence.
  *
  * cfg gives B, D, H, L, gamma, dtype and the residual flag (T is not used);
- * the decoder also needs L <= 4096 and B <= 64 (else BCMT_ERR_UNSUPPORTED).
+ * the decoder also needs L <= 4096, B <= 64 and heads of 64 dimensions
+ * (else BCMT_ERR_UNSUPPORTED).
  * The state and the workspace are caller-owned device buffers of the sizes
  * below (0 for an unsupported config); the workspace is scratch. */
 size_t bcmt_decode_state_bytes(const bcmt_config* cfg);

@@ -175,7 +175,11 @@ int check_config(const bcmt_config* c) {
   if (!(c->gamma >= 0.0f && c->gamma < 1.0f)) return BCMT_ERR_INVALID;
   if (c->dtype != BCMT_F32 && c->dtype != BCMT_BF16) return BCMT_ERR_INVALID;
   if (c->flags & ~(BCMT_FLAG_RESIDUAL | BCMT_FLAG_ACCUM_WGRAD)) return BCMT_ERR_INVALID;
-  if (c->D / c->H != kDh || c->D > kMaxD) return BCMT_ERR_UNSUPPORTED;
+  // Heads of 64 dimensions (matrix-core attention) or of 16 / 32 (the
+  // paper's model width); D a multiple of 64 for the 64-column score parts.
+  const int dh = c->D / c->H;
+  if ((dh != kDh && dh != 16 && dh != 32) || c->D % 64 != 0 || c->D > kMaxD)
+    return BCMT_ERR_UNSUPPORTED;
   // Grid limits: rows of the projections, blocks, batch * heads.
   const int64_t BT = (int64_t)c->B * c->T;
   const int64_t nb = ((int64_t)c->T + c->L - 1) / c->L;
@@ -192,7 +196,8 @@ bool overlaps(const void* a, const void* b, size_t n) {
 int check_decode(const bcmt_config* c) {
   const int st = check_config(c);
   if (st != BCMT_OK) return st;
-  if (c->L > dec_max_blocklen() || c->B > dec_max_batch()) return BCMT_ERR_UNSUPPORTED;
+  if (c->L > dec_max_blocklen() || c->B > dec_max_batch() || c->D / c->H != kDh)
+    return BCMT_ERR_UNSUPPORTED;
   return BCMT_OK;
 }
 
@@ -628,7 +633,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   }
   // Block-local attention backward: one fused kernel when a block fits one
   // workgroup, else dQ (with delta) and then dK / dV.
-  if (attn_bwd_fused(dt, p.T, p.L)) {
+  if (attn_bwd_fused(dt, p.T, D, p.H, p.L)) {
     LAUNCH(ST_ATTN_BWD_BLOCK,
            attn_bwd_block(dt, SV + p.qkv, SV + p.o, W + p.dout, (const float*)(SV + p.lse),
                           W + p.dqkv, p.B, p.T, D, p.H, p.L, s));

@@ -1203,6 +1203,7 @@ hipError_t attn_bwd_dkdv_t(const void* qkv, const void* dout, const float* lse,
 
 hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D, int H,
                     int L, hipStream_t s) {
+  if (attn_small_heads(D, H)) return attn_small_fwd(dt, qkv, out, lse, B, T, D, H, L, s);
   if (dt == DType::BF16) {
     const int nw = attn_waves(L, T);
     const int lb = L < T ? L : T;
@@ -1219,6 +1220,8 @@ hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int
 hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* dout,
                        const float* lse, float* delta, void* dqkv, int B, int T, int D, int H,
                        int L, hipStream_t s) {
+  if (attn_small_heads(D, H))
+    return attn_small_dq(dt, qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
   if (dt == DType::BF16) {
     const int nw = attn_waves(L, T);
     const int lb = L < T ? L : T;
@@ -1233,15 +1236,15 @@ hipError_t attn_bwd_dq(DType dt, const void* qkv, const void* out, const void* d
   return attn_bwd_dq_t<float>(qkv, out, dout, lse, delta, dqkv, B, T, D, H, L, s);
 }
 
-bool attn_bwd_fused(DType dt, int T, int L) {
+bool attn_bwd_fused(DType dt, int T, int D, int H, int L) {
   const int lb = L < T ? L : T;
-  return dt == DType::BF16 && lb <= 256;
+  return dt == DType::BF16 && lb <= 256 && !attn_small_heads(D, H);
 }
 
 hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void* dout,
                           const float* lse, void* dqkv, int B, int T, int D, int H, int L,
                           hipStream_t s) {
-  if (!attn_bwd_fused(dt, T, L)) return hipErrorInvalidValue;
+  if (!attn_bwd_fused(dt, T, D, H, L)) return hipErrorInvalidValue;
   const int lb = L < T ? L : T;
   const int nw = lb <= 128 ? attn_waves(L, T) : 8;  // one wave per 32 tokens of the block
   dim3 grid(1, (T + L - 1) / L, B * H);
@@ -1256,6 +1259,8 @@ hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void
 hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
                          const float* delta, void* dqkv, int B, int T, int D, int H, int L,
                          hipStream_t s) {
+  if (attn_small_heads(D, H))
+    return attn_small_dkdv(dt, qkv, dout, lse, delta, dqkv, B, T, D, H, L, s);
   if (dt == DType::BF16) {
     const int nw = attn_waves(L, T);
     const int lb = L < T ? L : T;

@@ -113,10 +113,23 @@ hipError_t attn_bwd_dkdv(DType dt, const void* qkv, const void* dout, const floa
 // Whether attn_bwd_block serves this layer (bf16, blocks of at most 128
 // tokens), and the fused backward of each block in one workgroup (dQ, dK,
 // dV; delta is formed internally and not written).
-bool attn_bwd_fused(DType dt, int T, int L);
+bool attn_bwd_fused(DType dt, int T, int D, int H, int L);
 hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void* dout,
                           const float* lse, void* dqkv, int B, int T, int D, int H, int L,
                           hipStream_t s);
+
+// Heads of 16 or 32 dimensions (attention_small.hip): the same three
+// passes (forward, dQ with delta, dK / dV) in float32 vector arithmetic;
+// attn_fwd / attn_bwd_dq / attn_bwd_dkdv route such layers there.
+bool attn_small_heads(int D, int H);
+hipError_t attn_small_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D,
+                          int H, int L, hipStream_t s);
+hipError_t attn_small_dq(DType dt, const void* qkv, const void* o, const void* dout,
+                         const float* lse, float* delta, void* dqkv, int B, int T, int D, int H,
+                         int L, hipStream_t s);
+hipError_t attn_small_dkdv(DType dt, const void* qkv, const void* dout, const float* lse,
+                           const float* delta, void* dqkv, int B, int T, int D, int H, int L,
+                           hipStream_t s);
 
 // ------------------------------------------------------------------ memory path
 // State of the decayed memory recurrence shared by consecutive chunks of the

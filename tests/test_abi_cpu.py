@@ -66,6 +66,10 @@ def good(**kw):
     (dict(gamma=1.0), abi.BCMT_ERR_INVALID),
     (dict(gamma=-0.1), abi.BCMT_ERR_INVALID),
     (dict(gamma=float("nan")), abi.BCMT_ERR_INVALID),
+    (dict(D=128, H=8), abi.BCMT_OK),               # head width 16 (the paper's model)
+    (dict(D=128, H=4), abi.BCMT_OK),               # head width 32
+    (dict(D=96, H=3), abi.BCMT_ERR_UNSUPPORTED),   # D not a multiple of 64
+    (dict(D=64, H=8), abi.BCMT_ERR_UNSUPPORTED),   # head width 8
     (dict(D=256, H=2), abi.BCMT_ERR_UNSUPPORTED),  # head width 128
     (dict(D=4096, H=64), abi.BCMT_ERR_UNSUPPORTED),
 ])
@@ -212,6 +216,7 @@ def test_decode_sizes_and_argument_errors(lib):
     assert abi.bcmt_decode_state_bytes(good(L=5000)) == 0     # block too long to decode
     assert abi.bcmt_decode_state_bytes(good(B=65)) == 0       # batch too large to decode
     assert abi.bcmt_decode_state_bytes(good(B=0)) == 0
+    assert abi.bcmt_decode_state_bytes(good(D=128, H=8)) == 0   # decoding needs 64-wide heads
     p = _params()
     st, ws = A + 0x20000000, A + 0x40000000
 

@@ -117,6 +117,19 @@ def test_block_size_sweep(torch_cuda, L):
     sampled_case(torch_cuda, f"sweep-L{L}", 16, 1024, 768, 12, L, rows=[0, 15], P=1024)
 
 
+@pytest.mark.parametrize("L", [64, 128, 256, 512, 1024])
+def test_paper_model_shape(torch_cuda, L):
+    """The paper's model width: B=16, T=1024, D=128 with 8 heads of 16
+    dimensions, bf16, the block sizes it sweeps and the dense limit L = T.
+    All 16 sequences are checked whole: the decay gradient of a couple of
+    sequences alone is a small, heavily cancelling sum (two sequences at
+    L = 128 give a scalar the bf16 path misses by 5e-2, while the float32
+    path matches it to 1e-6 and all 16 sequences give 8.6e-3).  The dense
+    limit (no memory, dgamma = 0) checks sequences 0 and 15."""
+    rows = [0, 15] if L >= 1024 else list(range(16))
+    sampled_case(torch_cuda, f"paper-shape-L{L}", 16, 1024, 128, 8, L, rows=rows, P=1024)
+
+
 @pytest.mark.parametrize("T,rows,P", [(4096, [0], 4096), (16384, [0, 1], 1024),
                                       (65536, [0, 1], 1024)])
 def test_long_context(torch_cuda, T, rows, P):

@@ -119,6 +119,13 @@ CASES = [
     # 0.588, and the bf16 path misses it by 3.1e-2 through the single-kernel
     # memory path and the chunked one alike, which agree to 5e-6.)
     ("bf16-many-blocks-L16", 2, 2550, 256, 4, 16, "bf16", 1.0, 0.02, 0.8, False),
+    # heads of 16 and 32 dimensions (the paper's model uses 16): ragged
+    # blocks, a stress distribution, one long block staged in many chunks
+    ("f32-dh16-ragged-L48", 2, 200, 128, 8, 48, "f32", 1.0, 0.05, 0.8, False),
+    ("f32-dh32-stress-residual", 1, 256, 128, 4, 64, "f32", 1.0, 2 / np.sqrt(128), 0.8, True),
+    ("f32-dh16-one-block-T300", 1, 300, 64, 4, 512, "f32", 1.0, 0.05, 0.8, False),
+    ("bf16-dh16-L128", 2, 512, 128, 8, 128, "bf16", 1.0, 0.02, 0.8, False),
+    ("bf16-dh32-L1000", 1, 1000, 128, 4, 1000, "bf16", 1.0, 0.02, 0.8, False),
 ]
 
 
