@@ -235,6 +235,47 @@ def long_context(make_step, torch, abi, dt, steps=10, warmup=3, make_chunked=Non
     return out
 
 
+PAPER_SHAPE = {"B": 16, "T": 1024, "D": 128, "H": 8, "Ls": [64, 128, 256, 512, 1024],
+               "gamma": 0.8}
+
+
+def paper_shape(make_step, torch, abi, steps=30, warmup=5):
+    """The layer at the paper's model width (d_model 128, 8 heads of 16
+    dimensions) over the block sizes it sweeps; L = T is the dense limit
+    (one block: plain causal attention, no memory).  Reports fwd+bwd
+    tokens/s per L, its ratio to the dense limit, and the layer's device
+    buffers (saved activations + the larger workspace)."""
+    g = PAPER_SHAPE
+    B, T, D, H = g["B"], g["T"], g["D"], g["H"]
+    out = {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x{D // H} bf16", "by_L": {}}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for L in g["Ls"]:
+        step, keep = make_step(B, T, D, H, L, g["gamma"])
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        cfg = keep[0].cfg
+        mem = abi.bcmt_saved_bytes(cfg) + max(abi.bcmt_workspace_bytes(cfg, abi.BCMT_PASS_FORWARD),
+                                              abi.bcmt_workspace_bytes(cfg, abi.BCMT_PASS_BACKWARD))
+        out["by_L"][str(L)] = {"us_per_step": round(ms * 1e3, 1),
+                               "tokens_per_s": round(B * T / (ms / 1e3), 1),
+                               "device_bytes": int(mem)}
+        del step, keep
+    dense = out["by_L"][str(T)]["tokens_per_s"]
+    for L, r in out["by_L"].items():
+        r["vs_dense"] = round(r["tokens_per_s"] / dense, 3)
+        print(f"paper shape L={L:>5s}: {r['us_per_step']:8.1f} us per step, "
+              f"{r['tokens_per_s'] / 1e6:7.2f} M tokens/s, x{r['vs_dense']:.2f} of dense",
+              file=sys.stderr)
+    return out
+
+
 DECODE = [{"B": 8, "D": 768, "H": 12, "L": 128, "gamma": 0.8},
           {"B": 2, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}]
 
@@ -298,6 +339,8 @@ def main():
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the long-context pass (bandwidth kernels at T=65536)")
     ap.add_argument("--no-decode", action="store_true", help="skip the incremental decoding pass")
+    ap.add_argument("--no-paper-shape", action="store_true",
+                    help="skip the pass at the paper's model width (D=128, 16-dim heads)")
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
                          "library's stage tracing on (every stage serialised on one stream, "
@@ -454,6 +497,8 @@ def main():
         out["long_context"] = long_context(make_step, torch, abi, dt, make_chunked=make_chunked)
     if not args.no_decode:
         out["decode"] = [decode_bench(torch, abi, dt, g) for g in DECODE]
+    if not args.no_paper_shape:
+        out["paper_shape"] = paper_shape(make_step, torch, abi)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)
