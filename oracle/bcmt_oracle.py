@@ -29,6 +29,11 @@ Readings of points the paper leaves open (all listed in the design notes):
   * the paper states no backward pass; the one here is derived by hand and
     pinned by finite differences in the tests.
 
+Per-channel decay: ``gamma`` may also be one decay per feature channel
+([D]); each channel then has its own recurrence of Sec. 3.5 (and its own
+normaliser Z), and the decay gradient is per channel.  This generalises the
+paper's single decay (its suggested extension); a scalar is the paper's.
+
 Chunked execution: a sequence cut at block boundaries into consecutive
 chunks gives the same layer when each chunk starts the recurrence of Sec. 3.5
 from the state the previous chunk ended with.  That state (the "carry") is
@@ -107,35 +112,51 @@ def exp_memory(S, gamma):
     return M
 
 
+def _per_channel(gamma, D):
+    """The decay as one value per channel [D] (a scalar repeated)."""
+    return np.broadcast_to(np.asarray(gamma, dtype=np.float64), (D,))
+
+
+def _z_channels(Z, D):
+    """A normaliser shared by the channels ([B]) or per channel ([B, D]),
+    as [B, D]."""
+    Z = np.asarray(Z, dtype=np.float64)
+    return np.repeat(Z[:, None], D, axis=1) if Z.ndim == 1 else Z
+
+
 def exp_memory_carry(S, gamma, N_in, Z_in):
     """The memory of Sec. 3.5 for blocks that follow earlier ones.
 
-    S: [B, n, D] summaries of this chunk's blocks; N_in [B, D] and Z_in [B]
-    aggregate the earlier blocks (N_in = sum_j gamma^(-1-j) S_j and
-    Z_in = sum_j gamma^(-1-j) over blocks j < 0).  Block i of the chunk then
-    has the double sums of Sec. 3.5 over every block up to it:
+    S: [B, n, D] summaries of this chunk's blocks; N_in [B, D] and Z_in
+    ([B], or [B, D] per channel) aggregate the earlier blocks
+    (N_in = sum_j gamma^(-1-j) S_j and Z_in = sum_j gamma^(-1-j) over blocks
+    j < 0).  gamma is a scalar or one decay per channel [D].  Block i of the
+    chunk then has the double sums of Sec. 3.5 over every block up to it,
+    channel by channel:
       N_i = sum_{0<=j<=i} gamma^(i-j) S_j + gamma^(i+1) N_in,
       Z_i = sum_{0<=j<=i} gamma^(i-j)     + gamma^(i+1) Z_in,
-    and M_i = N_i / Z_i.  Returns M [B, n, D], N [B, n, D], Z [B, n].
+    and M_i = N_i / Z_i.  Returns M, N and Z, all [B, n, D].
     """
     B, n, D = S.shape
-    g = float(gamma)
+    g = _per_channel(gamma, D)
+    Zc = _z_channels(Z_in, D)
     N = np.zeros((B, n, D))
-    Z = np.zeros((B, n))
+    Z = np.zeros((B, n, D))
     for i in range(n):
         for j in range(i + 1):
             N[:, i] += g ** (i - j) * S[:, j]
             Z[:, i] += g ** (i - j)
         N[:, i] += g ** (i + 1) * N_in
-        Z[:, i] += g ** (i + 1) * Z_in
-    return N / Z[:, :, None], N, Z
+        Z[:, i] += g ** (i + 1) * Zc
+    return N / Z, N, Z
 
 
 def carry_memory(N_in, Z_in):
     """M = N / Z of the earlier blocks, or 0 for an empty history (Z = 0)."""
-    Z = np.asarray(Z_in, dtype=np.float64)
+    N_in = np.asarray(N_in, dtype=np.float64)
+    Z = _z_channels(Z_in, N_in.shape[1])
     safe = np.where(Z > 0, Z, 1.0)
-    return np.where((Z > 0)[:, None], np.asarray(N_in, dtype=np.float64) / safe[:, None], 0.0)
+    return np.where(Z > 0, N_in / safe, 0.0)
 
 
 def block_causal_attention(Q, K, V, L, h):
@@ -173,7 +194,9 @@ def forward(X, P, L, h, gamma, residual=False, carry=None):
 
     ``carry`` = (N_in [B, D], Z_in [B]) makes X a chunk that follows earlier
     blocks of the same sequences (see exp_memory_carry); the state after the
-    chunk's last block is then cache["carry_out"] = (N_out, Z_out).
+    chunk's last block is then cache["carry_out"] = (N_out, Z_out).  With a
+    per-channel ``gamma`` [D] the normalisers are per channel: Z_in and
+    Z_out are [B, D].
     """
     X = np.asarray(X, dtype=np.float64)
     B, T, D = X.shape
@@ -197,6 +220,9 @@ def forward(X, P, L, h, gamma, residual=False, carry=None):
         S[:, i] = np.einsum("bt,btd->bd", a[:, b0:b1], Hloc[:, b0:b1])
 
     # Sec. 3.5: normalised exponential memory, projection, one-block shift.
+    per_channel = np.ndim(gamma) > 0
+    if per_channel and carry is None:
+        carry = (np.zeros((B, D)), np.zeros((B, D)))
     if carry is None:
         M = exp_memory(S, gamma)
         Mproj = M @ P["Wm"]
@@ -211,8 +237,9 @@ def forward(X, P, L, h, gamma, residual=False, carry=None):
         Mext = np.concatenate([carry_memory(N_in, Z_in)[:, None], M], axis=1)
         Mproj = Mext @ P["Wm"]
         Mcausal = Mproj[:, :-1].copy()
+        Z_out = Zacc[:, -1].copy() if per_channel else Zacc[:, -1, 0].copy()
         extra = dict(N_in=N_in, Z_in=Z_in, Mext=Mext, Nacc=Nacc, Zacc=Zacc,
-                     carry_out=(Nacc[:, -1].copy(), Zacc[:, -1].copy()))
+                     per_channel=per_channel, carry_out=(Nacc[:, -1].copy(), Z_out))
 
     # Sec. 3.7: broadcast to tokens; Sec. 3.8: gate and injection.
     Mtok = Mcausal[:, blk]                   # [B, T, D]
@@ -221,7 +248,9 @@ def forward(X, P, L, h, gamma, residual=False, carry=None):
     Y = Hloc + G * Mtok
     if residual:
         Y = Y + X
-    cache = dict(X=X, P=P, L=L, h=h, gamma=float(gamma), residual=residual,
+    cache = dict(X=X, P=P, L=L, h=h,
+                 gamma=np.asarray(gamma, dtype=np.float64) if per_channel else float(gamma),
+                 residual=residual,
                  Q=Q, K=K, V=V, probs=probs, Hcat=Hcat, Hloc=Hloc, s=s, a=a,
                  S=S, M=M, Mproj=Mproj, Mcausal=Mcausal, U=U, G=G, **extra)
     return Y, cache
@@ -338,21 +367,26 @@ def backward(cache, dY, dcarry=None):
 def _memory_carry_backward(c, dMcausal, dcarry):
     """Chain rule through exp_memory_carry and the projection of a chunk.
 
-    Differentiates the double sums of exp_memory_carry directly: with
-    dN_i = dM_i / Z_i (+ dN_out at the last block) and
-    dZ_i = -(dM_i . M_i) / Z_i (+ dZ_out at the last block),
+    Differentiates the double sums of exp_memory_carry directly, channel by
+    channel: with dN_i = dM_i / Z_i (+ dN_out at the last block) and
+    dZ_i = -dM_i M_i / Z_i (+ dZ_out at the last block),
       dS_j    = sum_{i>=j} gamma^(i-j) dN_i,
       dN_in   = sum_i gamma^(i+1) dN_i + dM_prev / Z_in,
-      dZ_in   = sum_i gamma^(i+1) dZ_i - (dM_prev . M_prev) / Z_in,
-      dgamma  = sum_i sum_{j<i} (i-j) gamma^(i-j-1) (dN_i . S_j + dZ_i)
-              + sum_i (i+1) gamma^i (dN_i . N_in + dZ_i Z_in),
-    where M_prev = N_in / Z_in is the earlier blocks' memory (its terms are
-    absent when Z_in = 0).  Returns dS, dWm, dgamma and {dN_in, dZ_in}.
+      dZ_in   = sum_i gamma^(i+1) dZ_i - dM_prev M_prev / Z_in,
+      dgamma  = sum_i sum_{j<i} (i-j) gamma^(i-j-1) (dN_i S_j + dZ_i)
+              + sum_i (i+1) gamma^i (dN_i N_in + dZ_i Z_in),
+    summed over the sequences, where M_prev = N_in / Z_in is the earlier
+    blocks' memory (its terms are absent where Z_in = 0).  With a single
+    decay (and one normaliser shared by the channels) dgamma and dZ_in are
+    the sums of these over the channels.  Returns dS, dWm, dgamma and
+    {dN_in, dZ_in}.
     """
-    P, g = c["P"], c["gamma"]
+    P = c["P"]
     S, Mext, Nacc, Zacc = c["S"], c["Mext"], c["Nacc"], c["Zacc"]
-    N_in, Z_in = c["N_in"], c["Z_in"]
+    N_in = c["N_in"]
     B, n, D = S.shape
+    g = _per_channel(c["gamma"], D)
+    Zc_in = _z_channels(c["Z_in"], D)
     # Mcausal[i] = Mproj[i] with Mproj = Mext @ Wm; Mproj's last row is unused.
     dMproj = np.zeros((B, n + 1, D))
     dMproj[:, :n] = dMcausal
@@ -361,32 +395,38 @@ def _memory_carry_backward(c, dMcausal, dcarry):
     dM_prev, dM = dMext[:, 0], dMext[:, 1:]
     M = Mext[:, 1:]
 
-    dN = dM / Zacc[:, :, None]
-    dZ = -np.einsum("bid,bid->bi", dM, M) / Zacc
+    dN = dM / Zacc
+    dZ = -dM * M / Zacc                      # per channel
     if dcarry is not None:
         dN[:, -1] += np.asarray(dcarry[0], dtype=np.float64)
-        dZ[:, -1] += np.asarray(dcarry[1], dtype=np.float64)
+        dZo = np.asarray(dcarry[1], dtype=np.float64)
+        if c["per_channel"]:
+            dZ[:, -1] += dZo
+        else:  # the shared normaliser: its gradient enters once
+            dZ[:, -1, 0] += dZo
 
     dS = np.zeros_like(S)
     dN_in = np.zeros((B, D))
-    dZ_in = np.zeros(B)
-    dgamma = 0.0
+    dZ_in = np.zeros((B, D))
+    dgamma = np.zeros(D)
     for i in range(n):
         for j in range(i + 1):
             dS[:, j] += g ** (i - j) * dN[:, i]
             if j < i:
                 dgamma += (i - j) * g ** (i - j - 1) * (
-                    np.sum(dN[:, i] * S[:, j]) + np.sum(dZ[:, i]))
+                    np.sum(dN[:, i] * S[:, j], axis=0) + np.sum(dZ[:, i], axis=0))
         dN_in += g ** (i + 1) * dN[:, i]
         dZ_in += g ** (i + 1) * dZ[:, i]
-        dgamma += (i + 1) * (g ** i if i > 0 else 1.0) * (
-            np.sum(dN[:, i] * N_in) + np.sum(dZ[:, i] * Z_in))
-    has = Z_in > 0
-    safe = np.where(has, Z_in, 1.0)
-    M_prev = carry_memory(N_in, Z_in)
-    dN_in += np.where(has[:, None], dM_prev / safe[:, None], 0.0)
-    dZ_in -= np.where(has, np.einsum("bd,bd->b", dM_prev, M_prev) / safe, 0.0)
-    return dS, dWm, float(dgamma), dict(dN_in=dN_in, dZ_in=dZ_in)
+        dgamma += (i + 1) * (g ** i if i > 0 else np.ones(D)) * (
+            np.sum(dN[:, i] * N_in, axis=0) + np.sum(dZ[:, i] * Zc_in, axis=0))
+    has = Zc_in > 0
+    safe = np.where(has, Zc_in, 1.0)
+    M_prev = carry_memory(N_in, c["Z_in"])
+    dN_in += np.where(has, dM_prev / safe, 0.0)
+    dZ_in -= np.where(has, dM_prev * M_prev / safe, 0.0)
+    if not c["per_channel"]:
+        return dS, dWm, float(dgamma.sum()), dict(dN_in=dN_in, dZ_in=dZ_in.sum(axis=1))
+    return dS, dWm, dgamma, dict(dN_in=dN_in, dZ_in=dZ_in)
 
 
 def stack_forward(X, layers, L, h, gamma, residual=True):

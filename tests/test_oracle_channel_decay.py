@@ -1,0 +1,157 @@
+"""Pins of the oracle's per-channel decay (one decay per feature channel).
+
+Each channel then runs the recurrence of Sec. 3.5 with its own decay; these
+tests compare it with the single-decay layer (itself pinned elsewhere), with
+closed forms, with channel independence, with chunked runs, and with finite
+differences.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import bcmt_oracle as orc
+from paper_2608_13578_amd.inputs import make_layer_inputs, make_upstream_grad, to_f64
+
+B, D, h, L = 2, 32, 2, 16
+
+
+def _setup(T, w_std=0.3, seed=0):
+    X, [W] = make_layer_inputs(B, T, D, seed=seed, x_std=1.0, w_std=w_std)
+    dY = make_upstream_grad(B, T, D, seed=1).astype(np.float64)
+    return X.astype(np.float64), to_f64(W), dY
+
+
+def _rel(a, b):
+    return float(np.abs(a - b).max() / max(np.abs(b).max(), 1e-300))
+
+
+def _decays(seed=4, lo=0.3, hi=0.95):
+    return np.random.default_rng(seed).uniform(lo, hi, D)
+
+
+def test_equal_channels_are_the_single_decay():
+    """gamma = 0.8 in every channel gives the layer with the scalar 0.8; the
+    per-channel decay gradients add up to the scalar one."""
+    X, W, dY = _setup(80)
+    Y0, c0 = orc.forward(X, W, L, h, 0.8)
+    g0 = orc.backward(c0, dY)
+    Y1, c1 = orc.forward(X, W, L, h, np.full(D, 0.8))
+    g1 = orc.backward(c1, dY)
+    assert _rel(Y1, Y0) < 1e-13
+    for k in ("dX", "dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp"):
+        assert _rel(g1[k], g0[k]) < 1e-11, k
+    assert np.shape(g1["dgamma"]) == (D,)
+    assert abs(g1["dgamma"].sum() - g0["dgamma"]) <= 1e-11 * abs(g0["dgamma"])
+
+
+def test_zero_decay_channel_keeps_its_summary():
+    """A channel with decay 0 has M_i = S_i (0**0 = 1), whatever the other
+    channels' decays."""
+    X, W, _ = _setup(80)
+    g = _decays()
+    g[5] = 0.0
+    _, c = orc.forward(X, W, L, h, g)
+    assert _rel(c["M"][:, :, 5], c["S"][:, :, 5]) < 1e-14
+
+
+def test_per_channel_normaliser_closed_form():
+    """After k blocks channel d's normaliser is (1 - g_d^k) / (1 - g_d)."""
+    X, W, _ = _setup(96)
+    g = _decays()
+    _, c = orc.forward(X, W, L, h, g)
+    k = 96 // L
+    N, Z = c["carry_out"]
+    assert Z.shape == (B, D)
+    assert np.allclose(Z, (1 - g ** k) / (1 - g), rtol=1e-13, atol=0)
+    assert _rel(N / Z, c["M"][:, -1]) < 1e-13
+
+
+def test_channels_are_independent():
+    """Changing one channel's decay changes that channel's memory only."""
+    X, W, _ = _setup(64)
+    g = _decays()
+    _, c0 = orc.forward(X, W, L, h, g)
+    g2 = g.copy()
+    g2[7] = 0.5 if g[7] != 0.5 else 0.6
+    _, c1 = orc.forward(X, W, L, h, g2)
+    diff = np.abs(c1["M"] - c0["M"]).max(axis=(0, 1))
+    assert diff[7] > 0 and np.all(np.delete(diff, 7) == 0.0)
+
+
+@pytest.mark.parametrize("T,cuts", [(96, [0, 32, 48, 96]), (90, [0, 16, 64, 90])])
+def test_chunks_equal_whole_sequence(T, cuts):
+    """Chunks with a per-channel state ([B, D] normalisers) reproduce the
+    whole sequence's values and gradients."""
+    X, W, dY = _setup(T)
+    g = _decays()
+    Yw, cw = orc.forward(X, W, L, h, g)
+    gw = orc.backward(cw, dY)
+    carry = (np.zeros((B, D)), np.zeros((B, D)))
+    ys, caches = [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        Y, c = orc.forward(X[:, a:b], W, L, h, g, carry=carry)
+        ys.append(Y)
+        caches.append((c, a, b))
+        carry = c["carry_out"]
+    assert _rel(np.concatenate(ys, axis=1), Yw) < 1e-12
+    dcarry, dxs, grads = None, [], []
+    for c, a, b in reversed(caches):
+        gr = orc.backward(c, dY[:, a:b], dcarry=dcarry)
+        dxs.append(gr["dX"])
+        grads.append(gr)
+        dcarry = (gr["dN_in"], gr["dZ_in"])
+    assert _rel(np.concatenate(dxs[::-1], axis=1), gw["dX"]) < 1e-11
+    for k in ("dWq", "dWm", "dWg", "dwp"):
+        assert _rel(sum(gr[k] for gr in grads), gw[k]) < 1e-11, k
+    assert _rel(sum(gr["dgamma"] for gr in grads), gw["dgamma"]) < 1e-11
+
+
+@pytest.mark.parametrize("with_state", [False, True])
+def test_channel_decay_gradients_finite_differences(with_state):
+    """Central differences of sum(dY * Y) (+ dN_out . N_out + dZ_out . Z_out
+    with an incoming state) in every channel's decay, and in the state."""
+    T = 64
+    X, W, dY = _setup(T)
+    g = _decays(lo=0.2, hi=0.9)
+    rng = np.random.default_rng(31)
+    if with_state:
+        Z_in = rng.uniform(1.0, 4.0, (B, D))
+        N_in = rng.standard_normal((B, D)) * Z_in * 0.5
+        carry = (N_in, Z_in)
+        dN_out = rng.standard_normal((B, D))
+        dZ_out = rng.standard_normal((B, D))
+        dcarry = (dN_out, dZ_out)
+    else:
+        carry, dcarry = None, None
+    _, c = orc.forward(X, W, L, h, g, carry=carry)
+    gr = orc.backward(c, dY, dcarry=dcarry)
+
+    def outputs(g_=g, N_=None, Z_=None):
+        cy = carry if carry is None else (carry[0] if N_ is None else N_,
+                                          carry[1] if Z_ is None else Z_)
+        Y, cc = orc.forward(X, W, L, h, g_, carry=cy)
+        return (Y,) + (tuple(cc["carry_out"]) if carry is not None else ())
+
+    weights = (dY,) + (tuple(dcarry) if dcarry is not None else ())
+
+    def directional(f, eps):
+        outs = [f(k * eps) for k in (1, -1, 2, -2)]
+        tot = 0.0
+        for part, w in enumerate(weights):
+            p1, m1, p2, m2 = (o[part] for o in outs)
+            tot += float(((8 * (p1 - m1) - (p2 - m2)) * w).sum())
+        return tot / (12 * eps)
+
+    v = rng.standard_normal(D)
+    ana = float((gr["dgamma"] * v).sum())
+    fd = directional(lambda e: outputs(g_=g + e * v), 1e-4)
+    assert abs(fd - ana) <= 1e-6 * np.linalg.norm(gr["dgamma"]) * np.linalg.norm(v), (fd, ana)
+    if with_state:
+        vz = rng.standard_normal((B, D))
+        ana = float((gr["dZ_in"] * vz).sum())
+        fd = directional(lambda e: outputs(Z_=carry[1] + e * vz), 1e-3)
+        assert abs(fd - ana) <= 1e-6 * np.linalg.norm(gr["dZ_in"]) * np.linalg.norm(vz)
+        vn = rng.standard_normal((B, D))
+        ana = float((gr["dN_in"] * vn).sum())
+        fd = directional(lambda e: outputs(N_=carry[0] + e * vn), 1e-3)
+        assert abs(fd - ana) <= 1e-6 * np.linalg.norm(gr["dN_in"]) * np.linalg.norm(vn)
