@@ -72,8 +72,9 @@ typedef enum {
 typedef enum { BCMT_F32 = 0, BCMT_BF16 = 1 } bcmt_dtype;
 
 enum {
-  BCMT_FLAG_RESIDUAL = 1,   /* Y = X + layer(X) */
-  BCMT_FLAG_ACCUM_WGRAD = 2 /* backward adds into the weight/decay gradients instead of overwriting */
+  BCMT_FLAG_RESIDUAL = 1,     /* Y = X + layer(X) */
+  BCMT_FLAG_ACCUM_WGRAD = 2,  /* backward adds into the weight/decay gradients instead of overwriting */
+  BCMT_FLAG_CHANNEL_DECAY = 4 /* one decay per feature channel: params->gamma_ch (see below) */
 };
 
 /* Passes for bcmt_workspace_bytes(). */
@@ -94,9 +95,17 @@ typedef struct {
   int32_t flags; /* BCMT_FLAG_* */
 } bcmt_config;
 
+/* Per-channel decay (BCMT_FLAG_CHANNEL_DECAY): channel d of the memory runs
+ * the recurrence of Sec. 3.5 with its own decay gamma_ch[d] in [0, 1) (the
+ * paper uses one decay for all channels; cfg->gamma is then unused), and has
+ * its own normaliser Z.  The backward writes the per-channel gradient to
+ * dgamma_ch [D] (dgamma is not written); chunk states and their gradients
+ * carry Z as [B, D].  The last member of each struct is read only with the
+ * flag, so callers that never set it may use structs without it. */
 typedef struct {
   const void *Wq, *Wk, *Wv, *Wo, *Wm, *Wg; /* [D, D] input-major, dtype */
   const void* wp;                          /* [D], dtype */
+  const float* gamma_ch;                   /* [D] float32, with BCMT_FLAG_CHANNEL_DECAY */
 } bcmt_params;
 
 /* Float32 gradients.  A NULL member is not computed. */
@@ -104,6 +113,7 @@ typedef struct {
   float *dWq, *dWk, *dWv, *dWo, *dWm, *dWg; /* [D, D] */
   float* dwp;                               /* [D] */
   float* dgamma;                            /* scalar */
+  float* dgamma_ch;                         /* [D], with BCMT_FLAG_CHANNEL_DECAY */
 } bcmt_grads;
 
 /* Host-only check of a configuration; returns BCMT_OK or a negative status.
@@ -163,7 +173,7 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
  * positions: Z is per sequence. */
 typedef struct {
   float* N; /* [B, D] */
-  float* Z; /* [B] */
+  float* Z; /* [B], or [B, D] with BCMT_FLAG_CHANNEL_DECAY */
 } bcmt_carry;
 
 /* Forward pass of one chunk.

@@ -26,6 +26,7 @@ BCMT_BF16 = 1
 
 BCMT_FLAG_RESIDUAL = 1
 BCMT_FLAG_ACCUM_WGRAD = 2
+BCMT_FLAG_CHANNEL_DECAY = 4
 
 BCMT_PASS_FORWARD = 0
 BCMT_PASS_INFERENCE = 1
@@ -39,6 +40,9 @@ EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_l
 
 PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
 GRAD_NAMES = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp", "dgamma")
+# the per-channel decay and its gradient (read with BCMT_FLAG_CHANNEL_DECAY)
+PARAM_FIELDS = PARAM_NAMES + ("gamma_ch",)
+GRAD_FIELDS = GRAD_NAMES + ("dgamma_ch",)
 
 
 class BcmtError(RuntimeError):
@@ -54,11 +58,11 @@ class bcmt_config(ctypes.Structure):
 
 
 class bcmt_params(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
 
 
 class bcmt_grads(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_NAMES]
+    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_FIELDS]
 
 
 class bcmt_carry(ctypes.Structure):
@@ -126,9 +130,11 @@ def lib():
     return _lib
 
 
-def make_config(B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False, accumulate=False):
+def make_config(B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False, accumulate=False,
+                channel_decay=False):
     """A bcmt_config from plain values (dtype "bf16" or "f32")."""
-    flags = (BCMT_FLAG_RESIDUAL if residual else 0) | (BCMT_FLAG_ACCUM_WGRAD if accumulate else 0)
+    flags = ((BCMT_FLAG_RESIDUAL if residual else 0) | (BCMT_FLAG_ACCUM_WGRAD if accumulate else 0)
+             | (BCMT_FLAG_CHANNEL_DECAY if channel_decay else 0))
     dt = {"bf16": BCMT_BF16, "f32": BCMT_F32}[dtype]
     return bcmt_config(int(B), int(T), int(D), int(H), int(L), float(gamma), dt, flags)
 
@@ -153,20 +159,20 @@ def _stream(stream):
 def _params(p):
     if isinstance(p, bcmt_params):
         return p
-    return bcmt_params(*[_ptr(p[n]) for n in PARAM_NAMES])
+    return bcmt_params(*[_ptr(p[n]) for n in PARAM_NAMES], _ptr(p.get("gamma_ch")))
 
 
 def _params_partial(p):
     """Like _params, but members missing from a dict are NULL."""
     if isinstance(p, bcmt_params):
         return p
-    return bcmt_params(*[_ptr(p.get(n)) for n in PARAM_NAMES])
+    return bcmt_params(*[_ptr(p.get(n)) for n in PARAM_FIELDS])
 
 
 def _grads(g):
     if g is None or isinstance(g, bcmt_grads):
         return g
-    return bcmt_grads(*[_ptr(g.get(n)) for n in GRAD_NAMES])
+    return bcmt_grads(*[_ptr(g.get(n)) for n in GRAD_FIELDS])
 
 
 def _carry(c):

@@ -86,7 +86,7 @@ struct Plan {
     P = take(BND * 4);
     const size_t BD = (size_t)B * D;
     cN = take(BD * 4);
-    cZ = take((size_t)B * 4);
+    cZ = take(BD * 4);  // one normaliser per sequence, or per channel
     cMt = take(BD * es);
     cP = take(BD * 4);
     saved_bytes = off;
@@ -94,7 +94,8 @@ struct Plan {
     off = 0;
     sp = take(BT * (D / kDh) * 4);  // partial pooling scores, D / 64 per token
     St = take(BND * es);
-    mpart = take(mem_part_bytes(B, nb, D));  // W_m product partials (long sequences)
+    const bool pc = c.flags & BCMT_FLAG_CHANNEL_DECAY;
+    mpart = take(mem_part_bytes(B, nb, D, pc));  // W_m product partials (scan + product path)
     cpart = take(carry_part_bytes(B, D));
     fwd_bytes = off;
 
@@ -102,8 +103,8 @@ struct Plan {
     du = take(BTD * es);
     pbar = take(BND * es);
     dS = take(BND * 4);
-    dM = take(mem_fused(nb) ? 0 : BND * 4);
-    mpart_b = take(mem_part_bytes(B, nb, D));
+    dM = take(mem_fused(nb, pc) ? 0 : BND * 4);
+    mpart_b = take(mem_part_bytes(B, nb, D, pc));
     a = take(BT * 4);
     ds = take(BT * 4);
     dwpp = take((size_t)pool_bwd_partial_rows(dt, B, T, D, L) * D * 4);
@@ -154,7 +155,7 @@ struct DecPlan {
     Hc = take(BLD * es);
     spc = take((size_t)B * L * dec_score_parts(D) * 4);
     N = take(BD * 4);
-    Z = take((size_t)B * 4);
+    Z = take(BD * 4);  // one normaliser per sequence, or per channel
     C = take(BD * 4);
     state_bytes = off;
     off = 0;
@@ -174,7 +175,8 @@ int check_config(const bcmt_config* c) {
   if (c->D % c->H != 0) return BCMT_ERR_INVALID;
   if (!(c->gamma >= 0.0f && c->gamma < 1.0f)) return BCMT_ERR_INVALID;
   if (c->dtype != BCMT_F32 && c->dtype != BCMT_BF16) return BCMT_ERR_INVALID;
-  if (c->flags & ~(BCMT_FLAG_RESIDUAL | BCMT_FLAG_ACCUM_WGRAD)) return BCMT_ERR_INVALID;
+  if (c->flags & ~(BCMT_FLAG_RESIDUAL | BCMT_FLAG_ACCUM_WGRAD | BCMT_FLAG_CHANNEL_DECAY))
+    return BCMT_ERR_INVALID;
   // Heads of 64 dimensions (matrix-core attention) or of 16 / 32 (the
   // paper's model width); D a multiple of 64 for the 64-column score parts.
   const int dh = c->D / c->H;
@@ -199,6 +201,16 @@ int check_decode(const bcmt_config* c) {
   if (c->L > dec_max_blocklen() || c->B > dec_max_batch() || c->D / c->H != kDh)
     return BCMT_ERR_UNSUPPORTED;
   return BCMT_OK;
+}
+
+// The per-channel decay of a config with BCMT_FLAG_CHANNEL_DECAY (null
+// otherwise); such a config needs it, 4-byte aligned.
+const float* channel_decay(const bcmt_config* c, const bcmt_params* prm) {
+  return (c->flags & BCMT_FLAG_CHANNEL_DECAY) ? prm->gamma_ch : nullptr;
+}
+bool decay_ok(const bcmt_config* c, const bcmt_params* prm) {
+  if (!(c->flags & BCMT_FLAG_CHANNEL_DECAY)) return true;
+  return prm->gamma_ch && ((uintptr_t)prm->gamma_ch & 3u) == 0;
 }
 
 // A chunk state, when given, needs both members: N 16-byte and Z 4-byte aligned.
@@ -424,7 +436,7 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
   int st = check_config(cfg);
   if (st != BCMT_OK) return st;
   if (!X || !prm || !Y) return BCMT_ERR_INVALID;
-  if (!carry_ok(cin) || !carry_ok(cout)) return BCMT_ERR_INVALID;
+  if (!carry_ok(cin) || !carry_ok(cout) || !decay_ok(cfg, prm)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* p : w)
     if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
@@ -466,10 +478,12 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
   // earlier blocks (a copy, so that carry_out may overwrite carry_in) and
   // projects its memory for the first block.
   Carry cr;
+  cr.gvec = channel_decay(cfg, prm);
+  cr.zcol = cr.gvec != nullptr;
   if (chunk) {
     LAUNCH(ST_CARRY_IN, carry_prep(dt, cin ? cin->N : nullptr, cin ? cin->Z : nullptr,
                                    (float*)(SV + p.cN), (float*)(SV + p.cZ), SV + p.cMt,
-                                   cin ? nullptr : (float*)(SV + p.cP), p.B, D, s));
+                                   cin ? nullptr : (float*)(SV + p.cP), p.B, D, cr.zcol, s));
     if (cin)
       LAUNCH(ST_CARRY_PROJ, carry_proj(dt, SV + p.cMt, prm->Wm, (float*)(SV + p.cP),
                                        (float*)(W + p.cpart), false, p.B, D, s));
@@ -500,7 +514,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   int st = check_config(cfg);
   if (st != BCMT_OK) return st;
   if (!X || !prm || !saved || !dY) return BCMT_ERR_INVALID;
-  if (!carry_ok(dcout) || !carry_ok(dcin)) return BCMT_ERR_INVALID;
+  if (!carry_ok(dcout) || !carry_ok(dcin) || !decay_ok(cfg, prm)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* p : w)
     if (!p || !aligned16(p)) return BCMT_ERR_INVALID;
@@ -514,6 +528,10 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   for (const float* q : gp)
     if (q && !aligned16(q)) return BCMT_ERR_INVALID;
   if (gr.dgamma && ((uintptr_t)gr.dgamma & 3u)) return BCMT_ERR_INVALID;
+  const float* gvec = channel_decay(cfg, prm);
+  if (gvec && gr.dgamma_ch && ((uintptr_t)gr.dgamma_ch & 3u)) return BCMT_ERR_INVALID;
+  // the decay gradient: one scalar, or one value per channel
+  float* dgam = gvec ? gr.dgamma_ch : gr.dgamma;
   Plan p(*cfg);
   const size_t act = (size_t)p.B * p.T * p.D * p.es;
   if (dX && (overlaps(dX, dY, act) || overlaps(dX, X, act))) return BCMT_ERR_INVALID;
@@ -550,7 +568,8 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   // first unless the gradients accumulate.  The weight matrices and dwp are
   // written (or accumulated) by fixed-order reductions.
   LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                               nullptr, 0, accum ? nullptr : gr.dgamma, p.B, p.T, D, p.L,
+                               (accum || !gvec) ? nullptr : dgam, gvec ? D : 0,
+                               (accum || gvec) ? nullptr : dgam, p.B, p.T, D, p.L,
                                chunk ? (const float*)(SV + p.cP) : nullptr,
                                chunk ? W + p.cpbar : nullptr, s));
   // dWg = H^T dU and dWm = M^T dP on the side stream.
@@ -582,6 +601,8 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   // decay gradient, in one kernel.  A chunk also feeds in the gradient of
   // the state it passed on and forms the gradient of the state it took.
   Carry cr;
+  cr.gvec = gvec;
+  cr.zcol = gvec != nullptr;
   if (chunk) {
     LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar, prm->Wm, (float*)(W + p.cdm),
                                       (float*)(W + p.cpart_b), true, p.B, D, s));
@@ -591,14 +612,14 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     cr.e0 = (float*)(W + p.ce0);
   }
   LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
-                             gr.dgamma, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
+                             dgam, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
                              cfg->gamma, cr, s));
   if (chunk)
     LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
                                       (const float*)(W + p.cdm), (const float*)(W + p.dS),
                                       (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
-                                      dcin ? dcin->Z : nullptr, gr.dgamma, p.B, p.nb, D,
-                                      cfg->gamma, s));
+                                      dcin ? dcin->Z : nullptr, dgam, p.B, p.nb, D,
+                                      cfg->gamma, gvec, gvec != nullptr, s));
   // Pooling backward: per-token a_t and ds_t, and partial sums of
   // ds_t H[t]; dwp = their sum on the side stream.
   LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
@@ -710,7 +731,8 @@ int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* prm, const bcmt
                       void* state, void* ws, size_t ws_bytes, void* stream) {
   int st = check_decode(cfg);
   if (st != BCMT_OK) return st;
-  if (!prm || !prm->Wm || !aligned16(prm->Wm) || !carry_ok(carry_in)) return BCMT_ERR_INVALID;
+  if (!prm || !prm->Wm || !aligned16(prm->Wm) || !carry_ok(carry_in) || !decay_ok(cfg, prm))
+    return BCMT_ERR_INVALID;
   if (!state || !aligned16(state) || !ws || !aligned16(ws)) return BCMT_ERR_INVALID;
   DecPlan p(*cfg);
   if (ws_bytes < p.ws_bytes) return BCMT_ERR_WORKSPACE;
@@ -721,7 +743,8 @@ int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* prm, const bcmt
   LAUNCH(ST_DEC_RESET, carry_prep(p.dt, carry_in ? carry_in->N : nullptr,
                                   carry_in ? carry_in->Z : nullptr, (float*)(S + p.N),
                                   (float*)(S + p.Z), W + p.Mt,
-                                  carry_in ? nullptr : (float*)(S + p.C), p.B, p.D, s));
+                                  carry_in ? nullptr : (float*)(S + p.C), p.B, p.D,
+                                  channel_decay(cfg, prm) != nullptr, s));
   if (carry_in)
     LAUNCH(ST_DEC_RESET, carry_proj(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C),
                                     (float*)(W + p.cpart), false, p.B, p.D, s));
@@ -732,7 +755,7 @@ int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* prm, int64_t t, 
                      void* y, void* state, void* ws, size_t ws_bytes, void* stream) {
   int st = check_decode(cfg);
   if (st != BCMT_OK) return st;
-  if (t < 0 || !x || !y || !prm || !state || !ws) return BCMT_ERR_INVALID;
+  if (t < 0 || !x || !y || !prm || !state || !ws || !decay_ok(cfg, prm)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* q : w)
     if (!q || !aligned16(q)) return BCMT_ERR_INVALID;
@@ -767,11 +790,12 @@ int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* prm, int64_t t, 
     // The block is complete: its summary enters the memory, which gives the
     // next block's context.
     LAUNCH(ST_DEC_POOL, dec_pool(p.dt, S + p.Hc, (const float*)(S + p.spc), (float*)(S + p.N),
-                                 (const float*)(S + p.Z), W + p.Mt, p.B, D, p.L, cfg->gamma, s));
+                                 (const float*)(S + p.Z), W + p.Mt, p.B, D, p.L, cfg->gamma,
+                                 channel_decay(cfg, prm), s));
     LAUNCH(ST_DEC_MEM, dec_product(p.dt, W + p.Mt, D, prm->Wm, nullptr, nullptr, p.B, D, D, part,
                                    s));
     LAUNCH(ST_DEC_MEM_FIN, dec_mem_finish(part, ks1, (float*)(S + p.C), (float*)(S + p.Z), p.B, D,
-                                          cfg->gamma, s));
+                                          cfg->gamma, channel_decay(cfg, prm), s));
   }
   return BCMT_OK;
 }

@@ -222,15 +222,18 @@ __global__ __launch_bounds__(256) void dec_gate_finish_kernel(const float* __res
   y[row] = from_f32<T>(out);
 }
 
-// C = Mt Wm for the next block, Z = g Z + 1.
+// C = Mt Wm for the next block, Z = g Z + 1 (per channel with gvec).
 __global__ __launch_bounds__(256) void dec_mem_finish_kernel(const float* __restrict__ part,
                                                              int ks, int B, int D,
                                                              float* __restrict__ C,
-                                                             float* __restrict__ Z, float gamma) {
+                                                             float* __restrict__ Z, float gamma,
+                                                             const float* __restrict__ gvec) {
   const int b = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= D) return;
-  C[(int64_t)b * D + n] = dv_sum(part, ks, B, D, b, n);
-  if (n == 0) Z[b] = gamma * Z[b] + 1.f;
+  const int64_t o = (int64_t)b * D + n;
+  C[o] = dv_sum(part, ks, B, D, b, n);
+  if (gvec) Z[o] = gvec[n] * Z[o] + 1.f;
+  else if (n == 0) Z[b] = gamma * Z[b] + 1.f;
 }
 
 // Attention of the new token over the block's tokens 0..off, one workgroup
@@ -342,7 +345,8 @@ __global__ __launch_bounds__(256) void dec_pool_kernel(const T* __restrict__ Hc,
                                                        float* __restrict__ N,
                                                        const float* __restrict__ Z,
                                                        T* __restrict__ Mt, int D, int L,
-                                                       float gamma) {
+                                                       float gamma,
+                                                       const float* __restrict__ gvec) {
   constexpr int VE = Vec16<T>::N, NV = 64 / VE, G = 256 / NV;
   __shared__ float a[kDecMaxL];
   __shared__ float red[G][64];
@@ -400,9 +404,10 @@ __global__ __launch_bounds__(256) void dec_pool_kernel(const T* __restrict__ Hc,
     for (int k = 0; k < G; ++k) S += red[k][tid];
     S /= total;
     const int64_t o = (int64_t)b * D + c0 + tid;
-    const float nn = gamma * N[o] + S;
+    const float gam = gvec ? gvec[c0 + tid] : gamma;
+    const float nn = gam * N[o] + S;
     N[o] = nn;
-    Mt[o] = from_f32<T>(nn / (gamma * Z[b] + 1.f));
+    Mt[o] = from_f32<T>(nn / (gam * (gvec ? Z[o] : Z[b]) + 1.f));
   }
 }
 
@@ -491,21 +496,21 @@ hipError_t dec_gate_finish(DType dt, const float* part, int ks, const void* Hc, 
 }
 
 hipError_t dec_mem_finish(const float* part, int ks, float* C, float* Z, int B, int D, float gamma,
-                          hipStream_t s) {
+                          const float* gvec, hipStream_t s) {
   hipLaunchKernelGGL(dec_mem_finish_kernel, dim3((D + 255) / 256, B), dim3(256), 0, s, part, ks,
-                     B, D, C, Z, gamma);
+                     B, D, C, Z, gamma, gvec);
   return hipGetLastError();
 }
 
 hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const float* Z, void* Mt,
-                    int B, int D, int L, float gamma, hipStream_t s) {
+                    int B, int D, int L, float gamma, const float* gvec, hipStream_t s) {
   const int np = dec_score_parts(D);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(dec_pool_kernel<bf16>, dim3(D / 64, B), dim3(256), 0, s, (const bf16*)Hc,
-                       spc, np, N, Z, (bf16*)Mt, D, L, gamma);
+                       spc, np, N, Z, (bf16*)Mt, D, L, gamma, gvec);
   else
     hipLaunchKernelGGL(dec_pool_kernel<float>, dim3(D / 64, B), dim3(256), 0, s, (const float*)Hc,
-                       spc, np, N, Z, (float*)Mt, D, L, gamma);
+                       spc, np, N, Z, (float*)Mt, D, L, gamma, gvec);
   return hipGetLastError();
 }
 

@@ -139,6 +139,10 @@ hipError_t attn_small_dkdv(DType dt, const void* qkv, const void* dout, const fl
 // (Nout, Zout; nullable).  Backward: the gradients arriving for that final
 // state (dNout, dZout; nullable) and the per-column gradient of Z at the
 // first block (e0 [B, D]; nullable).  All members null: a whole sequence.
+// With a per-channel decay (gvec [D], not null) every channel has its own
+// normaliser: Zin, Zout and dZout are then [B, D] (zcol), the scalar gamma
+// argument is unused, and the backward adds the decay gradient per channel
+// into dgamma [D] instead of into one scalar.
 struct Carry {
   const float* Nin = nullptr;
   const float* Zin = nullptr;
@@ -148,6 +152,8 @@ struct Carry {
   const float* dNout = nullptr;
   const float* dZout = nullptr;
   float* e0 = nullptr;
+  const float* gvec = nullptr;
+  bool zcol = false;
 };
 // Pooling, from the np partial scores per token written by gemm_score:
 // scores s [B*T], summaries S [B*nb, D] (float32, and St in the compute
@@ -159,8 +165,11 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
 // St = S in the compute type, [B*nb, D], and the decayed scans of S and Q);
 // for longer sequences a parallel scan gives M and a split-K product P,
 // using `part` (mem_part_bytes bytes; may be null when that is 0).
-bool mem_fused(int nb);
-size_t mem_part_bytes(int B, int nb, int D);
+// The single kernel scans the projected summaries, which equals projecting
+// the scan only for one decay shared by the channels: a per-channel decay
+// takes the scan + matrix-product path at any length.
+bool mem_fused(int nb, bool per_channel);
+size_t mem_part_bytes(int B, int nb, int D, bool per_channel);
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s);
@@ -188,13 +197,13 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, f
 // and adds the first block's decay term sum_cols dS_0 Nin + e0 Zin to
 // *dgamma (atomic); null outputs are skipped.
 hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, float* Zin,
-                      void* Mct, float* Pc, int B, int D, hipStream_t s);
+                      void* Mct, float* Pc, int B, int D, bool zcol, hipStream_t s);
 size_t carry_part_bytes(int B, int D);
 hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
                       bool transposed, int B, int D, hipStream_t s);
 hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
                         const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
-                        int D, float gamma, hipStream_t s);
+                        int D, float gamma, const float* gvec, bool zcol, hipStream_t s);
 // Pooling backward: per-token softmax weights a_t and score gradients ds_t,
 // and (when dwp_part is not null) partial sums of ds_t H[t] over chunks of
 // tokens, one row of D floats per chunk.
@@ -235,10 +244,11 @@ hipError_t dec_wo_finish(DType dt, const float* part, int ks, const void* wp, vo
 hipError_t dec_gate_finish(DType dt, const float* part, int ks, const void* Hc, const float* C,
                            const void* x, void* y, int B, int D, int L, int off, hipStream_t s);
 // After the block's last token: pooling, N = g N + S, Mt = N / (g Z + 1).
+// With a per-channel decay gvec [D], g and Z are per channel (Z [B, D]).
 hipError_t dec_pool(DType dt, const void* Hc, const float* spc, float* N, const float* Z, void* Mt,
-                    int B, int D, int L, float gamma, hipStream_t s);
+                    int B, int D, int L, float gamma, const float* gvec, hipStream_t s);
 // C = sum of the splits of Mt Wm, Z = g Z + 1.
 hipError_t dec_mem_finish(const float* part, int ks, float* C, float* Z, int B, int D, float gamma,
-                          hipStream_t s);
+                          const float* gvec, hipStream_t s);
 
 }  // namespace bcmt

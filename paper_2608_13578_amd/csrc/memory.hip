@@ -210,8 +210,10 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
   const int col = c0 + tid;
   const bool scol = tid < kMsCols && col < D;
   float N = 0.f, NP = 0.f, Z = 0.f, Qs = 0.f, E = 0.f, dg = 0.f;
-  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
-  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
+  // this thread's column: its decay and its incoming normaliser
+  const float gam = (scol && cr.gvec) ? cr.gvec[col] : gamma;
+  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (scol ? cr.Zin[(int64_t)b * D + col] : 0.f));
   if constexpr (FWD) {
     Z = zin;
     if (scol && cr.Nin) {
@@ -283,9 +285,9 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
         for (int w = 0; w < kMsWaves; ++w) g += part[w][ii][tid];
         const int64_t off = ((int64_t)b * nb + i) * D + col;
         if constexpr (FWD) {
-          N = gamma * N + S[off];
-          NP = gamma * NP + g;
-          Z = gamma * Z + 1.f;
+          N = gam * N + S[off];
+          NP = gam * NP + g;
+          Z = gam * Z + 1.f;
           const float rz = 1.f / Z;
           const float m = N * rz;
           M[off] = m;
@@ -293,20 +295,26 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
           P[off] = NP * rz;
           if (i == nb - 1) {
             if (cr.Nout) cr.Nout[(int64_t)b * D + col] = N;
-            if (cr.Zout && tid == 0 && blockIdx.x == 0) cr.Zout[b] = Z;
+            if (cr.Zout) {
+              if (cr.zcol) cr.Zout[(int64_t)b * D + col] = Z;
+              else if (tid == 0 && blockIdx.x == 0) cr.Zout[b] = Z;
+            }
           }
         } else {
-          const float z = zsum(i, gamma, lg2, zin);
+          const float z = zsum(i, gam, lg2, zin);
           const float m = Min[off];
-          Qs = g / z + gamma * Qs;
-          E = -g * m / z + gamma * E;
+          Qs = g / z + gam * Qs;
+          E = -g * m / z + gam * E;
           if (i == nb - 1) {
             if (cr.dNout) Qs += cr.dNout[(int64_t)b * D + col];
-            if (cr.dZout && col == 0) E += cr.dZout[b];
+            if (cr.dZout) {
+              if (cr.zcol) E += cr.dZout[(int64_t)b * D + col];
+              else if (col == 0) E += cr.dZout[b];
+            }
           }
           dS[off] = Qs;
           if (i >= 1) {
-            const float zp = zsum(i - 1, gamma, lg2, zin);
+            const float zp = zsum(i - 1, gam, lg2, zin);
             dg += Qs * (Min[off - D] * zp) + E * zp;
           } else if (cr.e0) {
             cr.e0[(int64_t)b * D + col] = E;
@@ -317,13 +325,17 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     __syncthreads();  // part[] is rewritten by the next row tile
   }
   if constexpr (!FWD) {
-    const float v = wave_sum(dg);
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    if (tid == 0 && dgamma) {
-      float t = 0.f;
-      for (int w = 0; w < kMsWaves; ++w) t += red[w];
-      unsafeAtomicAdd(dgamma, t);
+    if (cr.gvec) {  // per-channel decay gradient
+      if (scol && dgamma) unsafeAtomicAdd(dgamma + col, dg);
+    } else {
+      const float v = wave_sum(dg);
+      if (lane == 0) red[wave] = v;
+      __syncthreads();
+      if (tid == 0 && dgamma) {
+        float t = 0.f;
+        for (int w = 0; w < kMsWaves; ++w) t += red[w];
+        unsafeAtomicAdd(dgamma, t);
+      }
     }
   }
 }
@@ -362,9 +374,10 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
   const int b = blockIdx.y;
-  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
-  const float g16 = pow16(gamma);
-  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
+  const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
+  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+  const float g16 = pow16(gam);
+  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
   float carry = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;  // N just before this pass
   for (int p0 = 0; p0 < nb; p0 += kScChunks * kScRows) {
     const int a = p0 + k * kScRows;
@@ -377,7 +390,7 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
     float n = 0.f;
 #pragma unroll
     for (int r = 0; r < kScRows; ++r) {
-      n = gamma * n + v[r];
+      n = gam * n + v[r];
       v[r] = n;
     }
     agg[k][c] = n;
@@ -387,24 +400,30 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
       if (j == k) cin = cout;
       cout = g16 * cout + agg[j][c];
     }
-    float f = gamma;
+    float f = gam;
 #pragma unroll
     for (int r = 0; r < kScRows; ++r) {
       const int i = a + r;
       if (on && i < nb) {
         const float n = v[r] + f * cin;
-        const float m = n / zsum(i, gamma, lg2, zin);
+        const float m = n / zsum(i, gam, lg2, zin);
         const int64_t off = ((int64_t)b * nb + i) * D + col;
         M[off] = m;
         Mt[off] = from_f32<T>(m);
         if (i == nb - 1 && cr.Nout) cr.Nout[(int64_t)b * D + col] = n;
       }
-      f *= gamma;
+      f *= gam;
     }
     carry = cout;
     __syncthreads();  // agg[] is rewritten by the next pass
   }
-  if (cr.Zout && blockIdx.x == 0 && threadIdx.x == 0) cr.Zout[b] = zsum(nb - 1, gamma, lg2, zin);
+  if (cr.Zout) {
+    if (cr.zcol) {
+      if (on && k == 0) cr.Zout[(int64_t)b * D + col] = zsum(nb - 1, gam, lg2, zin);
+    } else if (blockIdx.x == 0 && threadIdx.x == 0) {
+      cr.Zout[b] = zsum(nb - 1, gam, lg2, zin);
+    }
+  }
 }
 
 // Reverse scans of the memory backward from dM (float32), M:
@@ -422,10 +441,11 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
   const int b = blockIdx.y;
-  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
-  const float g16 = pow16(gamma);
+  const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
+  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+  const float g16 = pow16(gam);
   constexpr int PASS = kScChunks * kScRows;
-  const float zin = cr.Zin ? cr.Zin[b] : 0.f;
+  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
   float cq = 0.f, ce = 0.f;  // Qs and E just after this pass
   float dg = 0.f;
   for (int p0 = (nb - 1) / PASS * PASS; p0 >= 0; p0 -= PASS) {
@@ -438,20 +458,23 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
       const int64_t off = ((int64_t)b * nb + i) * D + col;
       const float dm = ok ? dM[off] : 0.f;
       const float m = ok ? M[off] : 0.f;
-      const float z = zsum(i, gamma, lg2, zin);
+      const float z = zsum(i, gam, lg2, zin);
       x[r] = dm / z;
       y[r] = -dm * m / z;
       if (ok && i == nb - 1) {
         if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
-        if (cr.dZout && col == 0) y[r] += cr.dZout[b];
+        if (cr.dZout) {
+          if (cr.zcol) y[r] += cr.dZout[(int64_t)b * D + col];
+          else if (col == 0) y[r] += cr.dZout[b];
+        }
       }
       mprev[r] = ok && i >= 1 ? M[off - D] : 0.f;
     }
     float q = 0.f, e = 0.f;
 #pragma unroll
     for (int r = kScRows - 1; r >= 0; --r) {
-      q = x[r] + gamma * q;
-      e = y[r] + gamma * e;
+      q = x[r] + gam * q;
+      e = y[r] + gam * e;
       x[r] = q;
       y[r] = e;
     }
@@ -467,16 +490,16 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
       oq = aq[j][c] + g16 * oq;
       oe = ae[j][c] + g16 * oe;
     }
-    float f = gamma;
+    float f = gam;
 #pragma unroll
     for (int r = kScRows - 1; r >= 0; --r) {
       const int i = a + r;
       const float qs = x[r] + f * iq, es = y[r] + f * ie;
-      f *= gamma;
+      f *= gam;
       if (on && i < nb) {
         dS[((int64_t)b * nb + i) * D + col] = qs;
         if (i >= 1) {
-          const float zp = zsum(i - 1, gamma, lg2, zin);
+          const float zp = zsum(i - 1, gam, lg2, zin);
           dg += qs * (mprev[r] * zp) + es * zp;
         } else if (cr.e0) {
           cr.e0[(int64_t)b * D + col] = es;
@@ -486,6 +509,16 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
     cq = oq;
     ce = oe;
     __syncthreads();  // aq[] / ae[] are rewritten by the next pass
+  }
+  if (cr.gvec) {  // per-channel decay gradient: the column's chunks meet in LDS
+    aq[k][c] = dg;
+    __syncthreads();
+    if (k == 0 && on && dgamma) {
+      float t = 0.f;
+      for (int j = 0; j < kScChunks; ++j) t += aq[j][c];
+      unsafeAtomicAdd(dgamma + col, t);
+    }
+    return;
   }
   const float v = wave_sum(dg);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
@@ -589,24 +622,26 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
 // ------------------------------------------------------------------ chunk state
 // One workgroup per sequence.  carry_prep: copy of the incoming state and its
 // memory Nin / Zin in the compute type (the operand of the W_m product that
-// feeds the chunk's first block); zero when there is no incoming state.
+// feeds the chunk's first block); zero when there is no incoming state.  Z
+// is one value per sequence, or one per channel (zcol).
 template <typename T>
 __global__ __launch_bounds__(256) void carry_prep_kernel(const float* __restrict__ Nu,
                                                          const float* __restrict__ Zu,
                                                          float* __restrict__ Nin,
                                                          float* __restrict__ Zin,
                                                          T* __restrict__ Mct,
-                                                         float* __restrict__ Pc, int D) {
+                                                         float* __restrict__ Pc, int D, int zcol) {
   const int b = blockIdx.x;
-  const float z = Zu ? Zu[b] : 0.f;
   for (int c = threadIdx.x; c < D; c += blockDim.x) {
     const int64_t o = (int64_t)b * D + c;
     const float n = Nu ? Nu[o] : 0.f;
+    const float z = Zu ? (zcol ? Zu[o] : Zu[b]) : 0.f;
     Nin[o] = n;
+    if (zcol) Zin[o] = z;
     Mct[o] = from_f32<T>(z > 0.f ? n / z : 0.f);
     if (Pc) Pc[o] = 0.f;
   }
-  if (threadIdx.x == 0) Zin[b] = z;
+  if (!zcol && threadIdx.x == 0) Zin[b] = Zu ? Zu[b] : 0.f;
 }
 
 // carry_finish: gradients of the incoming state.  With M_in = Nin / Zin and
@@ -616,22 +651,36 @@ __global__ __launch_bounds__(256) void carry_prep_kernel(const float* __restrict
 //   dZin = sum_cols (g E_0 - dMc . M_in / Zin),
 //   dgamma += sum_cols (dS_0 Nin + E_0 Zin)
 // (the dMc terms vanish for an empty history, Zin = 0).
+// With a per-channel decay (gvec) and normalisers (zcol) the same terms are
+// kept per channel: dZin and the decay gradient are then [B, D] and [D].
 __global__ __launch_bounds__(256) void carry_finish_kernel(
     const float* __restrict__ Nin, const float* __restrict__ Zin, const float* __restrict__ dMc,
     const float* __restrict__ dS, const float* __restrict__ e0, float* __restrict__ dNin,
-    float* __restrict__ dZin, float* __restrict__ dgamma, int nb, int D, float gamma) {
+    float* __restrict__ dZin, float* __restrict__ dgamma, int nb, int D, float gamma,
+    const float* __restrict__ gvec, int zcol) {
   __shared__ float red[2][4];
   const int b = blockIdx.x, tid = threadIdx.x;
-  const float z = Zin[b];
   float ez = 0.f, dg = 0.f;
   for (int c = tid; c < D; c += blockDim.x) {
     const int64_t o = (int64_t)b * D + c;
+    const float z = zcol ? Zin[o] : Zin[b];
+    const float gam = gvec ? gvec[c] : gamma;
     const float n = Nin[o], dm = dMc[o], e = e0[o];
     const float q = dS[(int64_t)b * nb * D + c];
     const float dmz = z > 0.f ? dm / z : 0.f;
-    if (dNin) dNin[o] = dmz + gamma * q;
-    ez += gamma * e - (z > 0.f ? dmz * (n / z) : 0.f);
-    dg += q * n + e * z;
+    if (dNin) dNin[o] = dmz + gam * q;
+    const float ezc = gam * e - (z > 0.f ? dmz * (n / z) : 0.f);
+    const float dgc = q * n + e * z;
+    if (zcol) {
+      if (dZin) dZin[o] = ezc;
+    } else {
+      ez += ezc;
+    }
+    if (gvec) {
+      if (dgamma) unsafeAtomicAdd(dgamma + c, dgc);
+    } else {
+      dg += dgc;
+    }
   }
   ez = wave_sum(ez);
   dg = wave_sum(dg);
@@ -643,8 +692,8 @@ __global__ __launch_bounds__(256) void carry_finish_kernel(
   if (tid == 0) {
     const float tz = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
     const float tg = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-    if (dZin) dZin[b] = tz;
-    if (dgamma) unsafeAtomicAdd(dgamma, tg);
+    if (dZin && !zcol) dZin[b] = tz;
+    if (dgamma && !gvec) unsafeAtomicAdd(dgamma, tg);
   }
 }
 
@@ -900,16 +949,16 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
   return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
 }
 
-bool mem_fused(int nb) { return nb <= kMemFusedMaxBlocks; }
+bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !per_channel; }
 
-size_t mem_part_bytes(int B, int nb, int D) {
-  return mem_fused(nb) ? 0 : gemm_splitk_partial_bytes(B * nb, D, D, kMemMinK);
+size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
+  return mem_fused(nb, per_channel) ? 0 : gemm_splitk_partial_bytes(B * nb, D, D, kMemMinK);
 }
 
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s) {
-  if (!mem_fused(nb)) {
+  if (!mem_fused(nb, c.gvec != nullptr)) {
     // M from the scan, then P = M W_m as a matrix product.
     const dim3 grid((D + kScCols - 1) / kScCols, B);
     if (dt == DType::BF16)
@@ -950,7 +999,7 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
                    float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
                    const Carry& c, hipStream_t s) {
-  if (!mem_fused(nb)) {
+  if (!mem_fused(nb, c.gvec != nullptr)) {
     // dM = dP W_m^T as a matrix product, then the reverse scans.
     GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     hipError_t e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, false, kMemMinK, s);
@@ -977,13 +1026,13 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, f
 }
 
 hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, float* Zin,
-                      void* Mct, float* Pc, int B, int D, hipStream_t s) {
+                      void* Mct, float* Pc, int B, int D, bool zcol, hipStream_t s) {
   if (dt == DType::BF16)
     hipLaunchKernelGGL(carry_prep_kernel<bf16>, dim3(B), dim3(256), 0, s, Nu, Zu, Nin, Zin,
-                       (bf16*)Mct, Pc, D);
+                       (bf16*)Mct, Pc, D, zcol ? 1 : 0);
   else
     hipLaunchKernelGGL(carry_prep_kernel<float>, dim3(B), dim3(256), 0, s, Nu, Zu, Nin, Zin,
-                       (float*)Mct, Pc, D);
+                       (float*)Mct, Pc, D, zcol ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -998,10 +1047,10 @@ hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float
 
 hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
                         const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
-                        int D, float gamma, hipStream_t s) {
+                        int D, float gamma, const float* gvec, bool zcol, hipStream_t s) {
   if (!dNin && !dZin && !dgamma) return hipSuccess;
   hipLaunchKernelGGL(carry_finish_kernel, dim3(B), dim3(256), 0, s, Nin, Zin, dMc, dS, e0, dNin,
-                     dZin, dgamma, nb, D, gamma);
+                     dZin, dgamma, nb, D, gamma, gvec, zcol ? 1 : 0);
   return hipGetLastError();
 }
 

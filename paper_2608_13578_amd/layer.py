@@ -30,9 +30,16 @@ class LayerBuffers:
 
     def __init__(self, B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False,
                  accumulate=False, device="cuda"):
+        """gamma: the decay, or one decay per channel ([D] array: sets
+        BCMT_FLAG_CHANNEL_DECAY; its values go to the device as gamma_ch)."""
         self.dtype = dtype
         self.device = device
-        self.cfg = abi.make_config(B, T, D, H, L, gamma, dtype, residual, accumulate)
+        self.gamma_ch = None
+        if np.ndim(gamma) > 0:
+            self.gamma_ch = torch.tensor(np.asarray(gamma, dtype=np.float32), device=device)
+            gamma = 0.0
+        self.cfg = abi.make_config(B, T, D, H, L, gamma, dtype, residual, accumulate,
+                                   channel_decay=self.gamma_ch is not None)
         st = abi.bcmt_validate(self.cfg)
         if st != abi.BCMT_OK:
             raise abi.BcmtError(st, "bcmt_validate")
@@ -46,6 +53,8 @@ class LayerBuffers:
     def set_params(self, weights):
         """weights: dict of numpy float32 arrays (input-major [D, D], wp [D])."""
         self.params = {k: to_device(weights[k], self.dtype, self.device) for k in abi.PARAM_NAMES}
+        if self.gamma_ch is not None:
+            self.params["gamma_ch"] = self.gamma_ch
         return self.params
 
     def new_activation(self):
@@ -57,6 +66,8 @@ class LayerBuffers:
         g = {n: torch.zeros((D, D), **f) for n in ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg")}
         g["dwp"] = torch.zeros((D,), **f)
         g["dgamma"] = torch.zeros((4,), **f)  # 16 bytes, value in element 0
+        if self.gamma_ch is not None:
+            g["dgamma_ch"] = torch.zeros((D,), **f)
         return g
 
     def forward(self, X, Y, stream=None):
@@ -67,10 +78,12 @@ class LayerBuffers:
                                 stream=stream)
 
     def new_carry(self):
-        """A zeroed memory state (N [B, D], Z [B], float32): an empty history."""
+        """A zeroed memory state (N [B, D], Z [B] or [B, D] with a per-channel
+        decay, float32): an empty history."""
         B, _, D = self.shape
         f = dict(dtype=torch.float32, device=self.device)
-        return torch.zeros((B, D), **f), torch.zeros((B,), **f)
+        zshape = (B, D) if self.gamma_ch is not None else (B,)
+        return torch.zeros((B, D), **f), torch.zeros(zshape, **f)
 
     def forward_chunk(self, X, Y, carry_in, carry_out, stream=None):
         abi.bcmt_layer_forward_chunk(self.cfg, X, self.params, carry_in, Y, carry_out, self.saved,
@@ -87,7 +100,12 @@ class DecodeBuffers:
     def __init__(self, B, D, H, L, gamma=0.8, dtype="bf16", residual=False, device="cuda"):
         self.dtype = dtype
         self.device = device
-        self.cfg = abi.make_config(B, 1, D, H, L, gamma, dtype, residual)
+        self.gamma_ch = None
+        if np.ndim(gamma) > 0:
+            self.gamma_ch = torch.tensor(np.asarray(gamma, dtype=np.float32), device=device)
+            gamma = 0.0
+        self.cfg = abi.make_config(B, 1, D, H, L, gamma, dtype, residual,
+                                   channel_decay=self.gamma_ch is not None)
         u8 = dict(dtype=torch.uint8, device=device)
         n = abi.bcmt_decode_state_bytes(self.cfg)
         if n == 0:
@@ -99,6 +117,8 @@ class DecodeBuffers:
 
     def set_params(self, weights):
         self.params = {k: to_device(weights[k], self.dtype, self.device) for k in abi.PARAM_NAMES}
+        if self.gamma_ch is not None:
+            self.params["gamma_ch"] = self.gamma_ch
         return self.params
 
     def reset(self, carry_in=None, stream=None):

@@ -241,3 +241,19 @@ def test_decode_sizes_and_argument_errors(lib):
                                  None) == abi.BCMT_ERR_INVALID
     assert lib.bcmt_decode_reset(ctypes.byref(c), ctypes.byref(p), None, st, ws, wb - 1,
                                  None) == abi.BCMT_ERR_WORKSPACE
+
+
+def test_channel_decay_arguments(lib):
+    """With BCMT_FLAG_CHANNEL_DECAY the per-channel decay must be given."""
+    c = good()
+    c.flags |= abi.BCMT_FLAG_CHANNEL_DECAY
+    assert abi.bcmt_validate(c) == abi.BCMT_OK
+    assert abi.bcmt_saved_bytes(c) == abi.bcmt_saved_bytes(good())
+    bad = good()
+    bad.flags |= 8
+    assert abi.bcmt_validate(bad) == abi.BCMT_ERR_INVALID        # unknown flag
+    assert _fwd(c) == abi.BCMT_ERR_INVALID                        # gamma_ch missing
+    p = _params()
+    p.gamma_ch = A + 0x7000002                                    # misaligned
+    assert _fwd(c, params=p) == abi.BCMT_ERR_INVALID
+    assert _bwd(c) == abi.BCMT_ERR_INVALID

@@ -65,6 +65,8 @@ def gpu_chunks(torch, B, cuts, D, H, L, dtype, X, W, dY, gamma=0.8, residual=Fal
     for k in GRADS:
         out[k] = _host(grads[k])
     out["dgamma"] = float(grads["dgamma"][0].item())
+    if "dgamma_ch" in grads:
+        out["dgamma_ch"] = _host(grads["dgamma_ch"])
     out["dcarries"] = dins[::-1]
     return out
 
