@@ -276,6 +276,34 @@ def paper_shape(make_step, torch, abi, steps=30, warmup=5):
     return out
 
 
+def decay_variants(make_step, torch, steps=30, warmup=5):
+    """The measured layer with the decays the paper's sensitivity remark
+    spans (0.7, 0.8, 0.9) and with one decay per channel (drawn in
+    [0.7, 0.9]): tokens/s fwd+bwd for each."""
+    import numpy as np
+    w = WORKLOAD
+    B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} bf16"}
+    per_ch = np.random.default_rng(5).uniform(0.7, 0.9, D).astype(np.float32)
+    for name, gamma in (("gamma=0.7", 0.7), ("gamma=0.8", 0.8), ("gamma=0.9", 0.9),
+                        ("per-channel", per_ch)):
+        step, keep = make_step(B, T, D, H, L, gamma)
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out[name] = {"us_per_step": round(ms * 1e3, 1), "tokens_per_s": round(B * T / (ms / 1e3), 1)}
+        print(f"decay {name:12s}: {ms * 1e3:7.1f} us per step", file=sys.stderr)
+        del step, keep
+    return out
+
+
 DECODE = [{"B": 8, "D": 768, "H": 12, "L": 128, "gamma": 0.8},
           {"B": 2, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}]
 
@@ -339,6 +367,8 @@ def main():
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the long-context pass (bandwidth kernels at T=65536)")
     ap.add_argument("--no-decode", action="store_true", help="skip the incremental decoding pass")
+    ap.add_argument("--no-decay-variants", action="store_true",
+                    help="skip the pass over decay values and the per-channel decay")
     ap.add_argument("--no-paper-shape", action="store_true",
                     help="skip the pass at the paper's model width (D=128, 16-dim heads)")
     ap.add_argument("--profile-run", action="store_true",
@@ -499,6 +529,8 @@ def main():
         out["decode"] = [decode_bench(torch, abi, dt, g) for g in DECODE]
     if not args.no_paper_shape:
         out["paper_shape"] = paper_shape(make_step, torch, abi)
+    if not args.no_decay_variants:
+        out["decay_variants"] = decay_variants(make_step, torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)
