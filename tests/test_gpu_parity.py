@@ -126,6 +126,11 @@ CASES = [
     ("f32-dh16-one-block-T300", 1, 300, 64, 4, 512, "f32", 1.0, 0.05, 0.8, False),
     ("bf16-dh16-L128", 2, 512, 128, 8, 128, "bf16", 1.0, 0.02, 0.8, False),
     ("bf16-dh32-L1000", 1, 1000, 128, 4, 1000, "bf16", 1.0, 0.02, 0.8, False),
+    # the bf16 matrix-core kernels' three launch shapes (blocks of at most
+    # 32, at most 64, and longer), each with ragged blocks
+    ("bf16-dh16-ragged-L20", 2, 150, 128, 8, 20, "bf16", 1.0, 0.02, 0.8, False),
+    ("bf16-dh32-ragged-L48", 2, 200, 128, 4, 48, "bf16", 1.0, 0.02, 0.8, True),
+    ("bf16-dh16-stress-L200", 1, 450, 64, 4, 200, "bf16", 1.0, 2 / np.sqrt(64), 0.8, False),
 ]
 
 
