@@ -429,6 +429,10 @@ __device__ __forceinline__ int toff(int r, int c) {
 __device__ __forceinline__ bf16x8 trow8(const bf16* t, int r, int c0) {
   return *reinterpret_cast<const bf16x8*>(t + toff(r, c0));
 }
+// The same through inline assembly (see lds_read_tr()).
+__device__ __forceinline__ bf16x8 trow8a(const bf16* t, int r, int c0) {
+  return lds_read_b128(t + toff(r, c0));
+}
 __device__ __forceinline__ bf16x4 tcol4(const bf16* t, int k0, int c0, int lane) {
   const int i = lane & 15;
   return lds_read_tr(t + toff(k0 + (i >> 2), c0 + ((i & 3) << 2)));
@@ -569,13 +573,13 @@ __global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* _
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mnew = fmaxf(m[nq], mx);
-      const float alpha = exp2f(m[nq] - mnew);
+      const float alpha = exp2_fast(m[nq] - mnew);
       float ps = 0.f;
 #pragma unroll
       for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float pv = exp2f(s[nq][ku][r] - mnew);
+          const float pv = exp2_fast(s[nq][ku][r] - mnew);
           s[nq][ku][r] = pv;
           ps += pv;
         }
@@ -733,7 +737,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_bf16_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int u = kt + ku * 16 + lg * 4 + r;
-          const float pv = u <= t_eff ? exp2f(s[ku][r] * sl2 - ls[nq]) : 0.f;
+          const float pv = u <= t_eff ? exp2_fast(s[ku][r] * sl2 - ls[nq]) : 0.f;
           s[ku][r] = pv * (dp[ku][r] - dl[nq]);
         }
 #pragma unroll
@@ -858,7 +862,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
           const int ti = ts * 16 + lg * 4 + r;
           const int t = tt + ti;
           const bool ok = t >= u && t < be && u < be;
-          const float pv = ok ? exp2f(s[r] * sl2 - lsv[ts][r]) : 0.f;
+          const float pv = ok ? exp2_fast(s[r] * sl2 - lsv[ts][r]) : 0.f;
           p[ts][r] = pv;
           z[ts][r] = pv * (dp[r] - dlv[ts][r]);
         }
@@ -907,13 +911,290 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_bf16_kernel(
   }
 }
 
+// The two phases of the fused backward of one block, with the block's Q, K,
+// V and dO in LDS as tiles of 64 rows (tile t of matrix m at
+// blk + (m * NT + t) * 4096, m = Q, K, V, dO) and the lse and delta of its
+// queries in ls / dl (block-relative).  `dst` is dqkv at the sequence's first
+// row and the head's first column.
+
+// dK, dV for keys bs + w0 .. +31: scores held transposed, as in
+// attn_bwd_dkdv_bf16_kernel; key rows past the block end are masked to zero
+// probability.  Query tiles are taken in halves of 32 rows: both 16-key
+// groups share every fragment read of a half.  MASK = false serves the tiles
+// whose every query follows every key of the wave, inside the block.
+template <int NT, bool MASK>
+__device__ __forceinline__ void blk_dkdv_tile(const bf16* Qt, const bf16* Dt, const float* lst,
+                                              const float* dlt, const bf16x8 (&kf)[2][2],
+                                              const bf16x8 (&vf)[2][2], f32x4 (&dk)[2][4],
+                                              f32x4 (&dv)[2][4], int tt, int u0, int be,
+                                              float sl2, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    bf16x8 qr[2][2], dr[2][2], dtf[4], qtf[4];
+    f32x4 lsv[2], dlv[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int ts = 2 * tq + hh;
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        qr[hh][ds] = trow8a(Qt, ts * 16 + lr, ds * 32 + lg * 8);
+        dr[hh][ds] = trow8a(Dt, ts * 16 + lr, ds * 32 + lg * 8);
+      }
+      lsv[hh] = lds_read_f32x4(lst + ts * 16 + lg * 4);
+      dlv[hh] = lds_read_f32x4(dlt + ts * 16 + lg * 4);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dtf[j] = tcol8p(Dt, tq * 32, j, lane);
+      qtf[j] = tcol8p(Qt, tq * 32, j, lane);
+    }
+    lds_tr_wait();
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        lds_tr_bind(qr[hh][ds]);
+        lds_tr_bind(dr[hh][ds]);
+      }
+      lds_tr_bind(lsv[hh]);
+      lds_tr_bind(dlv[hh]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      lds_tr_bind(dtf[j]);
+      lds_tr_bind(qtf[j]);
+    }
+    f32x4 p[2][2], z[2][2];  // [key group][query row group of the half]
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int ts = 2 * tq + hh;
+#pragma unroll
+      for (int ku = 0; ku < 2; ++ku) {
+        f32x4 sc = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ds = 0; ds < 2; ++ds) {
+          sc = mma16(qr[hh][ds], kf[ku][ds], sc);
+          dp = mma16(dr[hh][ds], vf[ku][ds], dp);
+        }
+        const int u = u0 + ku * 16 + lr;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float pv = exp2_fast(sc[r] * sl2 - lsv[hh][r]);
+          if (MASK) {
+            const int t = tt + ts * 16 + lg * 4 + r;
+            pv = (t >= u && t < be && u < be) ? pv : 0.f;
+          }
+          p[ku][hh][r] = pv;
+          z[ku][hh][r] = pv * (dp[r] - dlv[hh][r]);
+        }
+      }
+    }
+#pragma unroll
+    for (int ku = 0; ku < 2; ++ku) {
+      const bf16x8 pf = frag_from<bf16>(p[ku][0], p[ku][1]);
+      const bf16x8 zf = frag_from<bf16>(z[ku][0], z[ku][1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        dv[ku][j] = mma16(dtf[j], pf, dv[ku][j]);
+        dk[ku][j] = mma16(qtf[j], zf, dk[ku][j]);
+      }
+    }
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void blk_dkdv(const bf16* blk, const float* ls, const float* dl,
+                                         bf16* dst, int64_t rs, int D, int bs, int be, int w0,
+                                         int ntile, float sl2, float scale, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+  const int kt0 = w0 / 64, kr0 = w0 % 64;
+  const bf16* Kb = blk + (1 * NT + kt0) * 4096;
+  const bf16* Vb = blk + (2 * NT + kt0) * 4096;
+  bf16x8 kf[2][2], vf[2][2];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      kf[ku][ds] = trow8a(Kb, kr0 + ku * 16 + lr, ds * 32 + lg * 8);
+      vf[ku][ds] = trow8a(Vb, kr0 + ku * 16 + lr, ds * 32 + lg * 8);
+    }
+  lds_tr_wait();
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      lds_tr_bind(kf[ku][ds]);
+      lds_tr_bind(vf[ku][ds]);
+    }
+  f32x4 dk[2][4], dv[2][4];
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dk[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dv[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  const int u0 = bs + w0;
+  for (int it = kt0; it < ntile; ++it) {
+    const int tt = bs + it * 64;
+    const bf16* Qt = blk + (0 * NT + it) * 4096;
+    const bf16* Dt = blk + (3 * NT + it) * 4096;
+    const bool full = tt >= u0 + 31 && tt + 63 < be && u0 + 31 < be;  // wave-uniform
+    if (full)
+      blk_dkdv_tile<NT, false>(Qt, Dt, ls + it * 64, dl + it * 64, kf, vf, dk, dv, tt, u0, be,
+                               sl2, lane);
+    else
+      blk_dkdv_tile<NT, true>(Qt, Dt, ls + it * 64, dl + it * 64, kf, vf, dk, dv, tt, u0, be,
+                              sl2, lane);
+  }
+#pragma unroll
+  for (int ku = 0; ku < 2; ++ku) {
+    const int u = u0 + ku * 16 + lr;
+    if (u < be) {
+      bf16* pp = dst + (int64_t)u * rs + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        store4(pp + D + j * 16, dk[ku][j][0] * scale, dk[ku][j][1] * scale, dk[ku][j][2] * scale,
+               dk[ku][j][3] * scale);
+        store4(pp + 2 * D + j * 16, dv[ku][j][0], dv[ku][j][1], dv[ku][j][2], dv[ku][j][3]);
+      }
+    }
+  }
+}
+
+// dQ contribution of one key tile (keys kt ..) to 16 queries tq .. of this
+// wave (as in attn_bwd_dq_bf16_kernel), recomputing the probabilities from
+// lse.  MASK = false serves a tile whose every key precedes every query.
+template <bool MASK>
+__device__ __forceinline__ void blk_dq_group(const bf16x8 (&kf)[4][2], const bf16x8 (&vf)[4][2],
+                                             const bf16x8 (&ktf)[4][2], const bf16x8 (&qf)[2],
+                                             const bf16x8 (&df)[2], float ls, float dl,
+                                             f32x4 (&dq)[4], int kt, int tq, int be, float sl2,
+                                             int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+  f32x4 sc[4], dp[4];
+#pragma unroll
+  for (int ku = 0; ku < 4; ++ku) {
+    sc[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dp[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      sc[ku] = mma16(kf[ku][ds], qf[ds], sc[ku]);
+      dp[ku] = mma16(vf[ku][ds], df[ds], dp[ku]);
+    }
+  }
+  const int t_eff = min(tq + lr, be - 1);
+#pragma unroll
+  for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float pv = exp2_fast(sc[ku][r] * sl2 - ls);
+      if (MASK) pv = kt + ku * 16 + lg * 4 + r <= t_eff ? pv : 0.f;
+      sc[ku][r] = pv * (dp[ku][r] - dl);
+    }
+#pragma unroll
+  for (int us = 0; us < 2; ++us) {
+    const bf16x8 zf = frag_from<bf16>(sc[2 * us], sc[2 * us + 1]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dq[j] = mma16(ktf[j][us], zf, dq[j]);
+  }
+}
+
+// dQ for queries bs + w0 .. +31.
+template <int NT>
+__device__ __forceinline__ void blk_dq(const bf16* blk, const float* ls_s, const float* dl_s,
+                                       bf16* dst, int64_t rs, int bs, int be, int w0, float sl2,
+                                       float scale, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+  const int qt0 = w0 / 64, qr0 = w0 % 64;
+  bf16x8 qf[2][2], df[2][2];
+  float dl[2], ls[2];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      qf[nq][ds] = trow8a(blk + (0 * NT + qt0) * 4096, qr0 + nq * 16 + lr, ds * 32 + lg * 8);
+      df[nq][ds] = trow8a(blk + (3 * NT + qt0) * 4096, qr0 + nq * 16 + lr, ds * 32 + lg * 8);
+    }
+    dl[nq] = lds_read_f32(dl_s + w0 + nq * 16 + lr);
+    ls[nq] = lds_read_f32(ls_s + w0 + nq * 16 + lr);
+  }
+  lds_tr_wait();
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      lds_tr_bind(qf[nq][ds]);
+      lds_tr_bind(df[nq][ds]);
+    }
+    lds_tr_bind(dl[nq]);
+    lds_tr_bind(ls[nq]);
+  }
+  f32x4 dq[2][4];
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dq[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int tw0 = bs + w0;
+  for (int it = 0; it <= qt0; ++it) {
+    const int kt = bs + it * 64;
+    const bf16* Kt = blk + (1 * NT + it) * 4096;
+    const bf16* Vt = blk + (2 * NT + it) * 4096;
+    bf16x8 kf[4][2], vf[4][2], ktf[4][2];
+#pragma unroll
+    for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        kf[ku][ds] = trow8a(Kt, ku * 16 + lr, ds * 32 + lg * 8);
+        vf[ku][ds] = trow8a(Vt, ku * 16 + lr, ds * 32 + lg * 8);
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) ktf[j][us] = tcol8p(Kt, us * 32, j, lane);
+    lds_tr_wait();
+#pragma unroll
+    for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+      for (int ds = 0; ds < 2; ++ds) {
+        lds_tr_bind(kf[ku][ds]);
+        lds_tr_bind(vf[ku][ds]);
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int us = 0; us < 2; ++us) lds_tr_bind(ktf[j][us]);
+#pragma unroll
+    for (int nq = 0; nq < 2; ++nq) {
+      const int tq = tw0 + nq * 16;
+      if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
+      if (kt + 63 <= tq && tq + 15 < be)        // every key precedes every query
+        blk_dq_group<false>(kf, vf, ktf, qf[nq], df[nq], ls[nq], dl[nq], dq[nq], kt, tq, be, sl2,
+                            lane);
+      else
+        blk_dq_group<true>(kf, vf, ktf, qf[nq], df[nq], ls[nq], dl[nq], dq[nq], kt, tq, be, sl2,
+                           lane);
+    }
+  }
+#pragma unroll
+  for (int nq = 0; nq < 2; ++nq) {
+    const int t = tw0 + nq * 16 + lr;
+    if (t < be) {
+      bf16* pp = dst + (int64_t)t * rs + lg * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        store4(pp + j * 16, dq[nq][j][0] * scale, dq[nq][j][1] * scale, dq[nq][j][2] * scale,
+               dq[nq][j][3] * scale);
+    }
+  }
+}
+
 // Fused backward of one block for blocks of at most NW * 32 tokens:
 // workgroup = (block, batch * head).  Q, K, V and dO of the whole block are
 // loaded into LDS once (direct loads); each wave first forms delta_t =
-// dO_t . O_t for its 32 queries, then owns 32 keys for dK and dV (scores
-// held transposed, as in attn_bwd_dkdv_bf16_kernel) and finally its 32
-// queries for dQ (as in attn_bwd_dq_bf16_kernel), recomputing the
-// probabilities from lse instead of keeping them.
+// dO_t . O_t for its 32 queries, then owns 32 keys for dK and dV and finally
+// its 32 queries for dQ.
 template <int NW>
 __global__ __launch_bounds__(NW * 64, NW >= 8 ? 1 : 2) void attn_bwd_block_bf16_kernel(
     const bf16* __restrict__ qkv, const bf16* __restrict__ o, const bf16* __restrict__ dout,
@@ -921,7 +1202,7 @@ __global__ __launch_bounds__(NW * 64, NW >= 8 ? 1 : 2) void attn_bwd_block_bf16_
     float sl2, float scale) {
   constexpr int NT = (NW * 32 + 63) / 64;  // 64-row tiles per matrix
   __shared__ __attribute__((aligned(1024))) bf16 lds[4][NT][64 * 64];  // Q, K, V, dO
-  __shared__ float ls_s[NT * 64], dl_s[NT * 64];
+  __shared__ __attribute__((aligned(16))) float ls_s[NT * 64], dl_s[NT * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int b = blockIdx.z / H, h = blockIdx.z % H;
@@ -966,188 +1247,12 @@ __global__ __launch_bounds__(NW * 64, NW >= 8 ? 1 : 2) void attn_bwd_block_bf16_
   vm_wait<0>();
   __syncthreads();
 
-  // ---- dK, dV for keys bs + w0 .. +31
-  if (bs + w0 < be) {
-    const int kt0 = w0 / 64, kr0 = w0 % 64;
-    bf16x8 kf[2][2], vf[2][2];
-#pragma unroll
-    for (int ku = 0; ku < 2; ++ku)
-#pragma unroll
-      for (int ds = 0; ds < 2; ++ds) {
-        kf[ku][ds] = trow8(lds[1][kt0], kr0 + ku * 16 + lr, ds * 32 + lg * 8);
-        vf[ku][ds] = trow8(lds[2][kt0], kr0 + ku * 16 + lr, ds * 32 + lg * 8);
-      }
-    f32x4 dk[2][4], dv[2][4];
-#pragma unroll
-    for (int ku = 0; ku < 2; ++ku)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        dk[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        dv[ku][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-    // Both 16-key groups share every fragment read of the query tile; key
-    // rows past the block end are masked to zero probability.
-    for (int it = kt0; it < ntile; ++it) {
-      const int tt = bs + it * 64;
-      const bf16* Qt = lds[0][it];
-      const bf16* Dt = lds[3][it];
-      f32x4 p[2][4], z[2][4];
-#pragma unroll
-      for (int ts = 0; ts < 4; ++ts) {
-        bf16x8 qr[2], dr[2];
-#pragma unroll
-        for (int ds = 0; ds < 2; ++ds) {
-          qr[ds] = trow8(Qt, ts * 16 + lr, ds * 32 + lg * 8);
-          dr[ds] = trow8(Dt, ts * 16 + lr, ds * 32 + lg * 8);
-        }
-#pragma unroll
-        for (int ku = 0; ku < 2; ++ku) {
-          const int u = bs + w0 + ku * 16 + lr;
-          f32x4 sc = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ds = 0; ds < 2; ++ds) {
-            sc = mma16(qr[ds], kf[ku][ds], sc);
-            dp = mma16(dr[ds], vf[ku][ds], dp);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int ti = ts * 16 + lg * 4 + r;
-            const int t = tt + ti;
-            const bool ok = t >= u && t < be && u < be;
-            const float pv = ok ? exp2f(sc[r] * sl2 - ls_s[it * 64 + ti]) : 0.f;
-            p[ku][ts][r] = pv;
-            z[ku][ts][r] = pv * (dp[r] - dl_s[it * 64 + ti]);
-          }
-        }
-      }
-#pragma unroll
-      for (int tq = 0; tq < 2; ++tq) {
-        bf16x8 dtf[4], qtf[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          dtf[j] = tcol8p(Dt, tq * 32, j, lane);
-          qtf[j] = tcol8p(Qt, tq * 32, j, lane);
-        }
-        lds_tr_wait();
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          lds_tr_bind(dtf[j]);
-          lds_tr_bind(qtf[j]);
-        }
-#pragma unroll
-        for (int ku = 0; ku < 2; ++ku) {
-          const bf16x8 pf = frag_from<bf16>(p[ku][2 * tq], p[ku][2 * tq + 1]);
-          const bf16x8 zf = frag_from<bf16>(z[ku][2 * tq], z[ku][2 * tq + 1]);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            dv[ku][j] = mma16(dtf[j], pf, dv[ku][j]);
-            dk[ku][j] = mma16(qtf[j], zf, dk[ku][j]);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int ku = 0; ku < 2; ++ku) {
-      const int u = bs + w0 + ku * 16 + lr;
-      if (u < be) {
-        bf16* pp = dqkv + ((int64_t)b * Tn + u) * rs + h * kDh + lg * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          store4(pp + D + j * 16, dk[ku][j][0] * scale, dk[ku][j][1] * scale,
-                 dk[ku][j][2] * scale, dk[ku][j][3] * scale);
-          store4(pp + 2 * D + j * 16, dv[ku][j][0], dv[ku][j][1], dv[ku][j][2], dv[ku][j][3]);
-        }
-      }
-    }
-  }
-
-  // ---- dQ for queries bs + w0 .. +31
-  if (bs + w0 < be) {
-    const int qt0 = w0 / 64, qr0 = w0 % 64;
-    bf16x8 qf[2][2], df[2][2];
-    float dl[2], ls[2];
-#pragma unroll
-    for (int nq = 0; nq < 2; ++nq) {
-#pragma unroll
-      for (int ds = 0; ds < 2; ++ds) {
-        qf[nq][ds] = trow8(lds[0][qt0], qr0 + nq * 16 + lr, ds * 32 + lg * 8);
-        df[nq][ds] = trow8(lds[3][qt0], qr0 + nq * 16 + lr, ds * 32 + lg * 8);
-      }
-      dl[nq] = dl_s[w0 + nq * 16 + lr];
-      ls[nq] = ls_s[w0 + nq * 16 + lr];
-    }
-    f32x4 dq[2][4];
-#pragma unroll
-    for (int nq = 0; nq < 2; ++nq)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) dq[nq][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int tw0 = bs + w0;
-    for (int it = 0; it <= qt0; ++it) {
-      const int kt = bs + it * 64;
-      const bf16* Kt = lds[1][it];
-      const bf16* Vt = lds[2][it];
-      bf16x8 kf[4][2], vf[4][2], ktf[4][2];
-#pragma unroll
-      for (int ku = 0; ku < 4; ++ku)
-#pragma unroll
-        for (int ds = 0; ds < 2; ++ds) {
-          kf[ku][ds] = trow8(Kt, ku * 16 + lr, ds * 32 + lg * 8);
-          vf[ku][ds] = trow8(Vt, ku * 16 + lr, ds * 32 + lg * 8);
-        }
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int us = 0; us < 2; ++us) ktf[j][us] = tcol8p(Kt, us * 32, j, lane);
-      lds_tr_wait();
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int us = 0; us < 2; ++us) lds_tr_bind(ktf[j][us]);
-#pragma unroll
-      for (int nq = 0; nq < 2; ++nq) {
-        const int tq = tw0 + nq * 16;
-        if (tq >= be || tq + 15 < kt) continue;  // wave-uniform
-        f32x4 sc[4], dp[4];
-#pragma unroll
-        for (int ku = 0; ku < 4; ++ku) {
-          sc[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
-          dp[ku] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ds = 0; ds < 2; ++ds) {
-            sc[ku] = mma16(kf[ku][ds], qf[nq][ds], sc[ku]);
-            dp[ku] = mma16(vf[ku][ds], df[nq][ds], dp[ku]);
-          }
-        }
-        const int t_eff = min(tq + lr, be - 1);
-#pragma unroll
-        for (int ku = 0; ku < 4; ++ku)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int u = kt + ku * 16 + lg * 4 + r;
-            const float pv = u <= t_eff ? exp2f(sc[ku][r] * sl2 - ls[nq]) : 0.f;
-            sc[ku][r] = pv * (dp[ku][r] - dl[nq]);
-          }
-#pragma unroll
-        for (int us = 0; us < 2; ++us) {
-          const bf16x8 zf = frag_from<bf16>(sc[2 * us], sc[2 * us + 1]);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) dq[nq][j] = mma16(ktf[j][us], zf, dq[nq][j]);
-        }
-      }
-    }
-#pragma unroll
-    for (int nq = 0; nq < 2; ++nq) {
-      const int t = tw0 + nq * 16 + lr;
-      if (t < be) {
-        bf16* pp = dqkv + ((int64_t)b * Tn + t) * rs + h * kDh + lg * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          store4(pp + j * 16, dq[nq][j][0] * scale, dq[nq][j][1] * scale, dq[nq][j][2] * scale,
-                 dq[nq][j][3] * scale);
-      }
-    }
-  }
+  bf16* dst = dqkv + (int64_t)b * Tn * rs + h * kDh;
+  if (bs + w0 < be)
+    blk_dkdv<NT>(&lds[0][0][0], ls_s, dl_s, dst, rs, D, bs, be, w0, ntile, sl2, scale, lane);
+  if (bs + w0 < be) blk_dq<NT>(&lds[0][0][0], ls_s, dl_s, dst, rs, bs, be, w0, sl2, scale, lane);
 }
+
 
 // Waves per attention workgroup (1, 2 or 4), each owning 32 queries or keys.
 int attn_waves(int L, int T) {
@@ -1246,10 +1351,11 @@ hipError_t attn_bwd_block(DType dt, const void* qkv, const void* out, const void
                           hipStream_t s) {
   if (!attn_bwd_fused(dt, T, D, H, L)) return hipErrorInvalidValue;
   const int lb = L < T ? L : T;
-  const int nw = lb <= 128 ? attn_waves(L, T) : 8;  // one wave per 32 tokens of the block
-  dim3 grid(1, (T + L - 1) / L, B * H);
+  const int nblk = (T + L - 1) / L;
   const float scale = 1.0f / sqrtf((float)kDh);
   const float sl2 = 1.4426950408889634f * scale;
+  const int nw = lb <= 128 ? attn_waves(L, T) : 8;  // one wave per 32 tokens of the block
+  dim3 grid(1, nblk, B * H);
 #define BLK(NW) hipLaunchKernelGGL(attn_bwd_block_bf16_kernel<NW>, grid, dim3(NW * 64), 0, s, (const bf16*)qkv, (const bf16*)out, (const bf16*)dout, lse, (bf16*)dqkv, T, D, H, L, sl2, scale)
   if (nw == 1) BLK(1); else if (nw == 2) BLK(2); else if (nw == 4) BLK(4); else BLK(8);
 #undef BLK

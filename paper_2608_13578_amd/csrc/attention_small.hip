@@ -1,16 +1,19 @@
 // Block-local causal attention (Sec. 3.3, 3.6) for heads of 16 or 32
 // dimensions, the head width of the paper's own model (d_model = 128, 8
-// heads, Sec. 4).  At such widths a head's score is a 16- or 32-term dot
-// product and the layer's cost sits in its D x D projections, so these
-// kernels use plain float32 vector arithmetic: one thread per query (per key
-// in the dK / dV pass), the other operand's rows staged through LDS in
-// chunks of kSmChunk tokens and read by broadcast, softmax in base 2 with a
-// running maximum.  The interface is that of the 64-dim two-pass path:
+// heads, Sec. 4).  Two implementations with one interface (that of the
+// 64-dim two-pass path):
 //   forward  out [B, T, D] at columns h*dh..; lse [B, H, T] (base 2, of the
 //            scores scaled by log2(e) / sqrt(dh));
 //   dq pass  dq into dqkv, delta [B, H, T] = dO . O per query;
 //   dkdv     dk, dv into dqkv.
 // qkv and dqkv are [B, T, 3D] with Q | K | V, head h at columns h*dh.
+//  - float32: plain vector arithmetic, one thread per query (per key in the
+//    dK / dV pass), the other operand's rows staged through LDS in chunks
+//    of kSmChunk tokens and read by broadcast, softmax in base 2 with a
+//    running maximum;
+//  - bf16: the matrix cores, with the tiling of the 64-dim kernels (32
+//    queries or keys per wave, tiles of 64 tokens; a 16-wide head fills
+//    half of the instruction's 32-deep step).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -392,13 +395,13 @@ __global__ __launch_bounds__(NW * 64) void attn_small_fwd_mfma_kernel(
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mnew = fmaxf(m[nq], mx);
-      const float alpha = exp2f(m[nq] - mnew);
+      const float alpha = exp2_fast(m[nq] - mnew);
       float ps = 0.f;
 #pragma unroll
       for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float pv = exp2f(s[nq][ku][r] - mnew);
+          const float pv = exp2_fast(s[nq][ku][r] - mnew);
           s[nq][ku][r] = pv;
           ps += pv;
         }
@@ -548,7 +551,7 @@ __global__ __launch_bounds__(NW * 64) void attn_small_dq_mfma_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int u = kt + ku * 16 + lg * 4 + r;
-          const float pv = u <= t_eff ? exp2f(sv[r] * sl2 - ls[nq]) : 0.f;
+          const float pv = u <= t_eff ? exp2_fast(sv[r] * sl2 - ls[nq]) : 0.f;
           sc[ku][r] = pv * (dp[r] - dl[nq]);
         }
       }
@@ -671,7 +674,7 @@ __global__ __launch_bounds__(NW * 64) void attn_small_dkdv_mfma_kernel(
         for (int r = 0; r < 4; ++r) {
           const int t = tt + ts * 16 + lg * 4 + r;
           const bool ok = t >= u && t < be && u < be;
-          const float pv = ok ? exp2f(sv[r] * sl2 - lsv[ts][r]) : 0.f;
+          const float pv = ok ? exp2_fast(sv[r] * sl2 - lsv[ts][r]) : 0.f;
           p[ts][r] = pv;
           z[ts][r] = pv * (dp[r] - dlv[ts][r]);
         }

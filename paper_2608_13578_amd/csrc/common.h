@@ -158,6 +158,11 @@ template <> __device__ __forceinline__ f32x8 frag_from<float>(const f32x4& a, co
   return r;
 }
 
+// 2^x with one v_exp_f32: results below the smallest normal float flush to
+// zero (exp2f adds a range reduction for them), which a softmax weight
+// can afford.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // ------------------------------------------------------------------ LDS helpers
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -168,9 +173,9 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 // direct global->LDS load in flight and drains all of them first
 // (s_waitcnt vmcnt(0)), which would also wait for the tiles being
 // prefetched.  Callers order these reads after their own vmcnt wait and
-// barrier for the tile they read, and pass every result through
-// lds_tr_fence() before using it: the compiler does not count these reads
-// in its LDS wait bookkeeping.
+// barrier for the tile they read, wait for them with lds_tr_wait() (or
+// lds_wait<N>()) and pass every result through lds_tr_bind() before using
+// it: the compiler does not count these reads in its LDS wait bookkeeping.
 __device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
   s16x4 v;
   const unsigned a = (unsigned)(uintptr_t)((lds_s16x4_t*)(p));
@@ -183,6 +188,13 @@ __device__ __forceinline__ f32x4 lds_read_f32x4(const float* p) {
   f32x4 v;
   const unsigned a = (unsigned)(uintptr_t)((__attribute__((address_space(3))) float*)(p));
   asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+// 4-byte LDS read in inline assembly; same contract as lds_read_tr().
+__device__ __forceinline__ float lds_read_f32(const float* p) {
+  float v;
+  const unsigned a = (unsigned)(uintptr_t)((__attribute__((address_space(3))) float*)(p));
+  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a));
   return v;
 }
 // 16-byte bf16 LDS read in inline assembly; same contract as lds_read_tr().
