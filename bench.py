@@ -239,7 +239,7 @@ PAPER_SHAPE = {"B": 16, "T": 1024, "D": 128, "H": 8, "Ls": [64, 128, 256, 512, 1
                "gamma": 0.8}
 
 
-def paper_shape(make_step, torch, abi, steps=30, warmup=5):
+def paper_shape(make_step, torch, abi, steps=100, warmup=100):
     """The layer at the paper's model width (d_model 128, 8 heads of 16
     dimensions) over the block sizes it sweeps; L = T is the dense limit
     (one block: plain causal attention, no memory).  Reports fwd+bwd
@@ -276,7 +276,7 @@ def paper_shape(make_step, torch, abi, steps=30, warmup=5):
     return out
 
 
-def decay_variants(make_step, torch, steps=30, warmup=5):
+def decay_variants(make_step, torch, steps=100, warmup=100):
     """The measured layer with the decays the paper's sensitivity remark
     spans (0.7, 0.8, 0.9) and with one decay per channel (drawn in
     [0.7, 0.9]): tokens/s fwd+bwd for each."""
@@ -361,8 +361,10 @@ def decode_bench(torch, abi, dt, g, blocks=2, warmup_blocks=1):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    # The GPU's clocks take some tens of milliseconds of load to settle: 200
+    # warm-up steps (about 70 ms here) reach the steady state that 10 do not.
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the long-context pass (bandwidth kernels at T=65536)")

@@ -638,7 +638,13 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
               (const float*)(W + p.dS), prm->wp, p.T, p.L, p.nb, D};
     LAUNCH(ST_HBAR, gemm_hbar(dt, g, e, s));
   }
-  // Output projection backward: dWo on the side stream, dHcat here.
+  // Output projection backward: dHcat here, then dWo on the side stream,
+  // where it overlaps the attention backward (a latency-bound kernel) rather
+  // than competing with the dHcat product for the matrix cores.
+  {
+    GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+    LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
+  }
   if (gr.dWo) {
     SIDE_BEGIN();
     {
@@ -647,10 +653,6 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
                     accum, 512);
     }
     SIDE_END();
-  }
-  {
-    GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
-    LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
   }
   // Block-local attention backward: one fused kernel when a block fits one
   // workgroup, else dQ (with delta) and then dK / dV.
