@@ -347,6 +347,13 @@ hipError_t order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
       LAUNCH(stage_red, gemm_splitk_reduce(part, sp_, (g).M, (g).N, C0, C1, C2, ldc, seg, acc, s)); \
   } while (0)
 
+// Minimum K per split of the D x D weight-gradient products on the side
+// stream (36 output tiles at D = 768): 2048 deals them as 4 splits, 144
+// workgroups, which leaves CUs to the critical path beside them.  At the
+// measured layer the step took 322 us against 326 us with 13 splits (512)
+// and 329 us with 8 (1024); 2 splits (4096) took 351 us.
+constexpr int kSideMinK = 2048;
+
 #define LAUNCH(stage, expr)                            \
   do {                                                 \
     TraceScope ts_(stage, s);                          \
@@ -579,7 +586,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
       if (gr.dWg) {
         GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
         LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
-                      accum, 512);
+                      accum, kSideMinK);
       }
       if (gr.dWm) {
         GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
@@ -650,7 +657,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     {
       GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
       LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
-                    accum, 512);
+                    accum, kSideMinK);
     }
     SIDE_END();
   }
