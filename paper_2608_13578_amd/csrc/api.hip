@@ -469,6 +469,15 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
   }
   // 2. Block-local causal attention (Sec. 3.3, 3.6).
   LAUNCH(ST_ATTN_FWD, attn_fwd(dt, SV + p.qkv, SV + p.o, (float*)(SV + p.lse), p.B, p.T, D, p.H, p.L, s));
+  // One block and no earlier state: the memory is empty, so C = 0 and
+  // Y = H (+X) exactly (Sec. 3.5, 3.8); the pooling, the scan and the gate
+  // product would only compute terms that vanish.
+  if (p.nb == 1 && !chunk) {
+    GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    LAUNCH(ST_WO, gemm_store(dt, g, Y, D, false, (cfg->flags & BCMT_FLAG_RESIDUAL) ? X : nullptr,
+                             D, s));
+    return BCMT_OK;
+  }
   // 3. Output projection (Sec. 3.3), also writing partial pooling scores.
   {
     GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -570,92 +579,108 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     s = side_s;                                                                        \
   } while (0)
 #define SIDE_END() (s = main_s)
-  // Gate and injection: dU, and the block sums of dY * G shifted back by one.
-  // dgamma is reduced with atomics later in the pass; this kernel clears it
-  // first unless the gradients accumulate.  The weight matrices and dwp are
-  // written (or accumulated) by fixed-order reductions.
-  LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                               (accum || !gvec) ? nullptr : dgam, gvec ? D : 0,
-                               (accum || gvec) ? nullptr : dgam, p.B, p.T, D, p.L,
-                               chunk ? (const float*)(SV + p.cP) : nullptr,
-                               chunk ? W + p.cpbar : nullptr, s));
-  // dWg = H^T dU and dWm = M^T dP on the side stream.
-  if (gr.dWg || gr.dWm) {
-    SIDE_BEGIN();
-    {
-      if (gr.dWg) {
-        GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-        LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
-                      accum, kSideMinK);
-      }
-      if (gr.dWm) {
-        GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
-                   0, 1};
-        LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
-                      accum, 512);
-        if (chunk) {
-          // The earlier blocks' memory fed the first block: dWm += Mc^T dPc.
-          GemmDesc gc{D, D, p.B, SV + p.cMt, D, true, {W + p.cpbar, nullptr, nullptr}, D, true,
-                      kSegNone, 0, 1};
-          LAUNCH_SPLITK(ST_CARRY_WGRAD, ST_CARRY_WGRAD, dt, gc, wpart, gr.dWm, nullptr, nullptr,
-                        D, D, true, 512);
+  const bool single = p.nb == 1 && !chunk;
+  if (single) {
+    // One block, no earlier state: Y = H (+X), so dH = dY, and dW_g, dW_m,
+    // dw_p and the decay gradient are zero (written unless accumulating).
+    if (!accum && (gr.dWg || gr.dWm || gr.dwp || dgam)) {
+      SIDE_BEGIN();
+      LAUNCH(ST_GATE_BWD, fill_f32(gr.dWg, gr.dWg ? (int64_t)D * D : 0, 0.f, s));
+      LAUNCH(ST_GATE_BWD, fill_f32(gr.dWm, gr.dWm ? (int64_t)D * D : 0, 0.f, s));
+      LAUNCH(ST_GATE_BWD, fill_f32(gr.dwp, gr.dwp ? D : 0, 0.f, s));
+      LAUNCH(ST_GATE_BWD, fill_f32(dgam, dgam ? (gvec ? D : 1) : 0, 0.f, s));
+      SIDE_END();
+    }
+  }
+  const void* dH = single ? dY : (const void*)(W + p.dh);
+  if (!single) {
+    // Gate and injection: dU, and the block sums of dY * G shifted back by one.
+    // dgamma is reduced with atomics later in the pass; this kernel clears it
+    // first unless the gradients accumulate.  The weight matrices and dwp are
+    // written (or accumulated) by fixed-order reductions.
+    LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
+                                 (accum || !gvec) ? nullptr : dgam, gvec ? D : 0,
+                                 (accum || gvec) ? nullptr : dgam, p.B, p.T, D, p.L,
+                                 chunk ? (const float*)(SV + p.cP) : nullptr,
+                                 chunk ? W + p.cpbar : nullptr, s));
+    // dWg = H^T dU and dWm = M^T dP on the side stream.
+    if (gr.dWg || gr.dWm) {
+      SIDE_BEGIN();
+      {
+        if (gr.dWg) {
+          GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+          LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
+                        accum, kSideMinK);
+        }
+        if (gr.dWm) {
+          GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
+                     0, 1};
+          LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
+                        accum, 512);
+          if (chunk) {
+            // The earlier blocks' memory fed the first block: dWm += Mc^T dPc.
+            GemmDesc gc{D, D, p.B, SV + p.cMt, D, true, {W + p.cpbar, nullptr, nullptr}, D, true,
+                        kSegNone, 0, 1};
+            LAUNCH_SPLITK(ST_CARRY_WGRAD, ST_CARRY_WGRAD, dt, gc, wpart, gr.dWm, nullptr, nullptr,
+                          D, D, true, 512);
+          }
         }
       }
+      SIDE_END();
     }
-    SIDE_END();
-  }
-  // Memory projection and decayed reverse scan: dM = dP Wm^T, dS and the
-  // decay gradient, in one kernel.  A chunk also feeds in the gradient of
-  // the state it passed on and forms the gradient of the state it took.
-  Carry cr;
-  cr.gvec = gvec;
-  cr.zcol = gvec != nullptr;
-  if (chunk) {
-    LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar, prm->Wm, (float*)(W + p.cdm),
-                                      (float*)(W + p.cpart_b), true, p.B, D, s));
-    cr.Zin = (const float*)(SV + p.cZ);
-    cr.dNout = dcout ? dcout->N : nullptr;
-    cr.dZout = dcout ? dcout->Z : nullptr;
-    cr.e0 = (float*)(W + p.ce0);
-  }
-  LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
-                             dgam, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
-                             cfg->gamma, cr, s));
-  if (chunk)
-    LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
-                                      (const float*)(W + p.cdm), (const float*)(W + p.dS),
-                                      (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
-                                      dcin ? dcin->Z : nullptr, dgam, p.B, p.nb, D,
-                                      cfg->gamma, gvec, gvec != nullptr, s));
-  // Pooling backward: per-token a_t and ds_t, and partial sums of
-  // ds_t H[t]; dwp = their sum on the side stream.
-  LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
-                               (const float*)(SV + p.S), (const float*)(W + p.dS),
-                               (float*)(W + p.a), (float*)(W + p.ds),
-                               gr.dwp ? (float*)(W + p.dwpp) : nullptr, p.B, p.T, D, p.L, s));
-  if (gr.dwp) {
-    SIDE_BEGIN();
-    LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
-    SIDE_END();
-  }
-  // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.
-  {
-    GemmDesc g{BT, D, D, W + p.du, D, false, {prm->Wg, nullptr, nullptr}, D, false, kSegNone, 0, 1};
-    HbarEpi e{W + p.dh, dY, (const float*)(W + p.a), (const float*)(W + p.ds),
-              (const float*)(W + p.dS), prm->wp, p.T, p.L, p.nb, D};
-    LAUNCH(ST_HBAR, gemm_hbar(dt, g, e, s));
-  }
+    // Memory projection and decayed reverse scan: dM = dP Wm^T, dS and the
+    // decay gradient, in one kernel.  A chunk also feeds in the gradient of
+    // the state it passed on and forms the gradient of the state it took.
+    Carry cr;
+    cr.gvec = gvec;
+    cr.zcol = gvec != nullptr;
+    if (chunk) {
+      LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar, prm->Wm, (float*)(W + p.cdm),
+                                        (float*)(W + p.cpart_b), true, p.B, D, s));
+      cr.Zin = (const float*)(SV + p.cZ);
+      cr.dNout = dcout ? dcout->N : nullptr;
+      cr.dZout = dcout ? dcout->Z : nullptr;
+      cr.e0 = (float*)(W + p.ce0);
+    }
+    LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
+                               dgam, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
+                               cfg->gamma, cr, s));
+    if (chunk)
+      LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
+                                        (const float*)(W + p.cdm), (const float*)(W + p.dS),
+                                        (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
+                                        dcin ? dcin->Z : nullptr, dgam, p.B, p.nb, D,
+                                        cfg->gamma, gvec, gvec != nullptr, s));
+    // Pooling backward: per-token a_t and ds_t, and partial sums of
+    // ds_t H[t]; dwp = their sum on the side stream.
+    LAUNCH(ST_POOL_BWD, pool_bwd(dt, SV + p.h, (const float*)(SV + p.s), (const float*)(SV + p.stats),
+                                 (const float*)(SV + p.S), (const float*)(W + p.dS),
+                                 (float*)(W + p.a), (float*)(W + p.ds),
+                                 gr.dwp ? (float*)(W + p.dwpp) : nullptr, p.B, p.T, D, p.L, s));
+    if (gr.dwp) {
+      SIDE_BEGIN();
+      LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
+      SIDE_END();
+    }
+    // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.
+    {
+      GemmDesc g{BT, D, D, W + p.du, D, false, {prm->Wg, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+      HbarEpi e{W + p.dh, dY, (const float*)(W + p.a), (const float*)(W + p.ds),
+                (const float*)(W + p.dS), prm->wp, p.T, p.L, p.nb, D};
+      LAUNCH(ST_HBAR, gemm_hbar(dt, g, e, s));
+    }
+  }  // the memory path's backward
   // Output projection backward: dHcat here, then dWo on the side stream,
   // where it overlaps the attention backward (a latency-bound kernel) rather
   // than competing with the dHcat product for the matrix cores.
   {
-    GemmDesc g{BT, D, D, W + p.dh, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+    GemmDesc g{BT, D, D, dH, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
   }
   if (gr.dWo) {
     SIDE_BEGIN();
     {
-      GemmDesc g{D, D, BT, SV + p.o, D, true, {W + p.dh, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+      GemmDesc g{D, D, BT, SV + p.o, D, true, {dH, nullptr, nullptr}, D, true, kSegNone, 0, 1};
       LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
                     accum, kSideMinK);
     }

@@ -207,6 +207,32 @@ def test_empty_history_is_the_plain_layer(torch_cuda, dtype, T, D, H, L):
     assert abs(plain["dgamma"] - ch["dgamma"]) <= 1e-5 * abs(plain["dgamma"])
 
 
+@pytest.mark.parametrize("dtype,T,D,H,L,res", [("bf16", 200, 256, 4, 256, False),
+                                               ("f32", 128, 128, 2, 128, False),
+                                               ("bf16", 256, 256, 4, 512, True)])
+def test_single_block_shortcut(torch_cuda, dtype, T, D, H, L, res):
+    """One block and no earlier state: the plain entry points skip the
+    memory path (Y = H, dH = dY); a chunk with no incoming state still runs
+    it, where every memory term is an exact zero.  Without the residual the
+    two agree bit for bit; with it, the shortcut adds X to the unrounded H,
+    so Y and dX agree to bf16 rounding.  dW_g, dW_m, dw_p and dgamma are 0."""
+    torch = torch_cuda
+    from test_gpu_parity import run_gpu
+    B = 2
+    X, W, dY = inputs(B, T, D, dtype, w_std=0.05)
+    plain = run_gpu(torch, B, T, D, H, L, dtype, X, W, dY, residual=res)
+    ch = gpu_chunks(torch, B, [0, T], D, H, L, dtype, X, W, dY, residual=res)
+    for k in ("dWg", "dWm", "dwp"):
+        assert not plain[k].any(), k
+    assert plain["dgamma"] == 0.0
+    keys = ("Y", "dX") + tuple(k for k in GRADS if k != "dgamma")
+    if not res:
+        for k in keys:
+            assert np.array_equal(plain[k], ch[k]), k
+    else:
+        compare({k: plain[k] for k in keys}, {k: ch[k] for k in keys}, dtype, "single-block")
+
+
 def test_long_context_chunks_match_whole_sequence(torch_cuda):
     """B=2, T=16384, D=1024, H=16, L=256 (64 blocks) as four chunks of 4096
     tokens against the whole sequence in one call, both on the GPU: the two
