@@ -255,6 +255,72 @@ const char* bcmt_strerror(int status);
 /* Library version, major * 10000 + minor * 100 + patch. */
 int bcmt_version(void);
 
+/* ---------------------------------------------------------------- language model
+ * A decoder-only language model built from BCMT layers: the architecture of
+ * the paper's experiments (Sec. 4.1 fixes d_model, layers, heads and batch;
+ * the other parts are read as a pre-LN decoder of the period):
+ *   x = E[tok] + Pe[t];  per layer x += mix(LN1(x)); x += gelu(LN2(x) W1) W2
+ *   (hidden 4d, GELU in tanh form, no biases); logits = LNf(x) E^T (head tied
+ *   to the embedding); loss = mean cross-entropy over all B T positions.
+ * mix is the BCMT layer above (bf16, no residual flag, decay fixed); with
+ * L >= T it is plain causal attention, the paper's Dense baseline.
+ * LayerNorm has gain and bias, eps 1e-5.  bf16 only.
+ *
+ * Parameters live in one flat vector (float32 master copy `params`, its
+ * bf16 working copy `params_bf16`, float32 `grads`, AdamW moments), arrays
+ * back to back in this order (every length is a multiple of 64 elements):
+ *   0  E  [Vp, d]  (Vp = V rounded up to a multiple of 128; rows V..Vp-1 are
+ *                   never read as tokens and their logits are masked)
+ *   1  Pe [T, d]
+ *   2 + 13 l + k, layer l:  k = 0 ln1_g, 1 ln1_b [d]; 2..7 Wq, Wk, Wv, Wo,
+ *                   Wm, Wg [d, d]; 8 wp [d]; 9 ln2_g, 10 ln2_b [d];
+ *                   11 W1 [d, 4d]; 12 W2 [4d, d]   (input-major: y = x W)
+ *   2 + 13 n_layer, +1:  lnf_g, lnf_b [d]
+ * Weights are input-major as in the layer.  Gradients of every array are
+ * written (not accumulated); E's gradient adds the tied head's and the
+ * lookups' parts, the latter with float32 atomics (rows sharing a token add
+ * in any order, so E's gradient may differ between runs by rounding). */
+typedef struct {
+  int32_t V;       /* vocabulary size, >= 2 */
+  int32_t d;       /* model width: a multiple of 64, at most 1024 */
+  int32_t H;       /* heads of each BCMT layer (d / H in {16, 32, 64}) */
+  int32_t n_layer; /* >= 1 */
+  int32_t B, T;    /* sequences per step and tokens per sequence */
+  int32_t L;       /* block size of the layers (L >= T: the Dense model) */
+  float gamma;     /* memory decay of the layers (fixed, not trained) */
+} bcmt_model_config;
+
+/* AdamW: p *= 1 - lr wd; m = b1 m + (1 - b1) g; v = b2 v + (1 - b2) g^2;
+ * p -= lr (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps). */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+  int32_t step; /* 1 for the first update */
+} bcmt_adamw;
+
+/* Floats in the flat parameter vector; 0 for an invalid config. */
+size_t bcmt_model_param_count(const bcmt_model_config* cfg);
+/* Offset and length (in elements) of array `index` of the flat vector. */
+int bcmt_model_param_array(const bcmt_model_config* cfg, int index, size_t* offset,
+                           size_t* count);
+/* Bytes of scratch workspace bcmt_model_train_step needs; 0 if invalid. */
+size_t bcmt_model_workspace_bytes(const bcmt_model_config* cfg);
+/* params_bf16 = bf16(params), the whole vector (enqueued on `stream`). */
+int bcmt_model_cast(const bcmt_model_config* cfg, const float* params, void* params_bf16,
+                    void* stream);
+/* One training step on `stream`: forward over tokens [B, T] (int32, ids in
+ * [0, V); others are clamped) with next-token targets [B, T], the mean
+ * cross-entropy into *loss (device float), the backward into grads, and
+ * with `opt` an AdamW update of params, adam_m, adam_v (all float32,
+ * param_count long) that also rewrites params_bf16.  Without `opt` only
+ * the gradients are computed (adam_m, adam_v may be NULL).  The forward
+ * reads params_bf16 (weights) and params (LayerNorm gains and biases).
+ * All pointers are device memory, 16-byte aligned; ws holds at least
+ * bcmt_model_workspace_bytes(cfg).  Errors as for the layer. */
+int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
+                          const int32_t* targets, float* params, void* params_bf16,
+                          float* grads, float* adam_m, float* adam_v, const bcmt_adamw* opt,
+                          float* loss, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Stage tracing (profiling aid) -------------------------------------
  * While tracing is on, every kernel launch of bcmt_layer_forward and
  * bcmt_layer_backward is bracketed by two HIP events recorded on the call's

@@ -36,7 +36,8 @@ EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_l
             "bcmt_layer_backward", "bcmt_layer_forward_chunk", "bcmt_layer_backward_chunk",
             "bcmt_decode_state_bytes", "bcmt_decode_workspace_bytes", "bcmt_decode_reset",
             "bcmt_decode_step", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
-            "bcmt_trace_read")
+            "bcmt_trace_read", "bcmt_model_param_count", "bcmt_model_param_array",
+            "bcmt_model_workspace_bytes", "bcmt_model_cast", "bcmt_model_train_step")
 
 PARAM_NAMES = ("Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp")
 GRAD_NAMES = ("dWq", "dWk", "dWv", "dWo", "dWm", "dWg", "dwp", "dgamma")
@@ -68,6 +69,18 @@ class bcmt_grads(ctypes.Structure):
 class bcmt_carry(ctypes.Structure):
     """Memory state between chunks: N [B, D] and Z [B], float32 device pointers."""
     _fields_ = [("N", ctypes.c_void_p), ("Z", ctypes.c_void_p)]
+
+
+class bcmt_model_config(ctypes.Structure):
+    _fields_ = [("V", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("n_layer", ctypes.c_int32), ("B", ctypes.c_int32), ("T", ctypes.c_int32),
+                ("L", ctypes.c_int32), ("gamma", ctypes.c_float)]
+
+
+class bcmt_adamw(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("step", ctypes.c_int32)]
 
 
 class bcmt_trace_entry(ctypes.Structure):
@@ -126,6 +139,20 @@ def lib():
         L.bcmt_trace_enable.restype = ctypes.c_int
         L.bcmt_trace_read.argtypes = [ctypes.POINTER(bcmt_trace_entry), ctypes.c_int]
         L.bcmt_trace_read.restype = ctypes.c_int
+        mcp = ctypes.POINTER(bcmt_model_config)
+        L.bcmt_model_param_count.argtypes = [mcp]
+        L.bcmt_model_param_count.restype = ctypes.c_size_t
+        L.bcmt_model_param_array.argtypes = [mcp, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t),
+                                             ctypes.POINTER(ctypes.c_size_t)]
+        L.bcmt_model_param_array.restype = ctypes.c_int
+        L.bcmt_model_workspace_bytes.argtypes = [mcp]
+        L.bcmt_model_workspace_bytes.restype = ctypes.c_size_t
+        L.bcmt_model_cast.argtypes = [mcp, vp, vp, vp]
+        L.bcmt_model_cast.restype = ctypes.c_int
+        L.bcmt_model_train_step.argtypes = [mcp, vp, vp, vp, vp, vp, vp, vp,
+                                            ctypes.POINTER(bcmt_adamw), vp, vp, ctypes.c_size_t,
+                                            vp]
+        L.bcmt_model_train_step.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -293,3 +320,48 @@ def bcmt_trace_read(max_entries=64):
     if n < 0:
         raise BcmtError(n, "bcmt_trace_read")
     return [(buf[i].name.decode(), buf[i].calls, buf[i].total_ms) for i in range(min(n, max_entries))]
+
+
+# ---- language model built from BCMT layers
+
+
+def make_model_config(V, d, H, n_layer, B, T, L, gamma=0.8):
+    return bcmt_model_config(int(V), int(d), int(H), int(n_layer), int(B), int(T), int(L),
+                             float(gamma))
+
+
+def bcmt_model_param_count(cfg):
+    return lib().bcmt_model_param_count(ctypes.byref(cfg))
+
+
+def bcmt_model_param_array(cfg, index):
+    """(offset, count) in elements of array `index` of the flat vector."""
+    off, cnt = ctypes.c_size_t(), ctypes.c_size_t()
+    st = lib().bcmt_model_param_array(ctypes.byref(cfg), int(index), ctypes.byref(off),
+                                      ctypes.byref(cnt))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_model_param_array")
+    return off.value, cnt.value
+
+
+def bcmt_model_workspace_bytes(cfg):
+    return lib().bcmt_model_workspace_bytes(ctypes.byref(cfg))
+
+
+def bcmt_model_cast(cfg, params, params_bf16, stream=None):
+    st = lib().bcmt_model_cast(ctypes.byref(cfg), _ptr(params), _ptr(params_bf16),
+                               _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_model_cast")
+
+
+def bcmt_model_train_step(cfg, tokens, targets, params, params_bf16, grads, adam_m, adam_v, opt,
+                          loss, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else _nbytes(ws)
+    st = lib().bcmt_model_train_step(ctypes.byref(cfg), _ptr(tokens), _ptr(targets),
+                                     _ptr(params), _ptr(params_bf16), _ptr(grads), _ptr(adam_m),
+                                     _ptr(adam_v), _ref(opt), _ptr(loss), _ptr(ws),
+                                     int(ws_bytes), _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_model_train_step")

@@ -231,30 +231,6 @@ __device__ __forceinline__ void run_epilogue(const Epi& epi, const f32x4 (&acc)[
 }
 
 // 8 consecutive elements to / from float (16 bytes of bf16, 32 of float).
-__device__ __forceinline__ void ld8(const bf16* p, float (&o)[8]) {
-  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = (float)v[e];
-}
-__device__ __forceinline__ void ld8(const float* p, float (&o)[8]) {
-  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    o[e] = a[e];
-    o[4 + e] = b[e];
-  }
-}
-__device__ __forceinline__ void st8(bf16* p, const float (&v)[8]) {
-  bf16x8 o;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
-  *reinterpret_cast<bf16x8*>(p) = o;
-}
-__device__ __forceinline__ void st8(float* p, const float (&v)[8]) {
-  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
-  *reinterpret_cast<f32x4*>(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
-}
-
 // Staged epilogue of the pipelined kernel.  The accumulator tile goes to
 // LDS (float32, rows of BN, 16-byte chunks XOR-swizzled by row so that the
 // 16 rows a fragment spans fall on distinct banks), then every thread hands
@@ -318,6 +294,73 @@ struct EpiStore {
       for (int e = 0; e < 8; ++e) o[e] += a[e];
     }
     st8(C + (int64_t)m * ldc + n, o);
+  }
+};
+
+// GELU, tanh form, and its derivative (the MLP of the language model).
+__device__ __forceinline__ float gelu_f(float u) {
+  const float c = 0.7978845608028654f;  // sqrt(2 / pi)
+  return 0.5f * u * (1.f + tanhf(c * (u + 0.044715f * u * u * u)));
+}
+__device__ __forceinline__ float gelu_grad_f(float u) {
+  const float c = 0.7978845608028654f;
+  const float t = tanhf(c * (u + 0.044715f * u * u * u));
+  return 0.5f * (1.f + t) + 0.5f * u * (1.f - t * t) * c * (1.f + 3.f * 0.044715f * u * u);
+}
+
+// MLP input product: stores U = acc (rounded to T, kept for the backward)
+// and A = gelu(U) of the rounded U.
+template <typename T>
+struct EpiGelu {
+  T* U;
+  T* A;
+  int64_t ld;
+  __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
+    const int64_t off = (int64_t)m * ld + n;
+    f32x4 a;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      v[r] = (float)(T)v[r];
+      a[r] = gelu_f(v[r]);
+    }
+    store4(U + off, v[0], v[1], v[2], v[3]);
+    store4(A + off, a[0], a[1], a[2], a[3]);
+  }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    const int64_t off = (int64_t)m * ld + n;
+    float u[8], a[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      u[k] = (float)(T)v[k];
+      a[k] = gelu_f(u[k]);
+    }
+    st8(U + off, u);
+    st8(A + off, a);
+  }
+};
+
+// Backward through the GELU: dU = acc * gelu'(U), U the stored forward value.
+template <typename T>
+struct EpiGeluBwd {
+  const T* U;
+  T* dU;
+  int64_t ld;
+  __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
+    const int64_t off = (int64_t)m * ld + n;
+    const f32x4 u = load4f(U + off);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(u[r]);
+    store4(dU + off, v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    const int64_t off = (int64_t)m * ld + n;
+    float u[8], d[8];
+    ld8(U + off, u);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) d[k] = v[k] * gelu_grad_f(u[k]);
+    st8(dU + off, d);
   }
 };
 
@@ -1094,6 +1137,23 @@ hipError_t gemm_gate(DType dt, const GemmDesc& g, const GateEpi& e, hipStream_t 
   if (!(!g.a_mcontig && g.b_ncontig && g.seg == kSegNone)) return hipErrorInvalidValue;
   if (dt == DType::BF16) return launch_any<bf16, false, true, kSegNone>(g, EpiGate<bf16>{e}, s);
   return launch<float, false, true, kSegNone>(g, EpiGate<float>{e}, s);
+}
+
+hipError_t gemm_gelu(DType dt, const GemmDesc& g, void* U, void* A, int64_t ld, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (dt != DType::BF16 || g.a_mcontig || g.seg != kSegNone) return hipErrorInvalidValue;
+  const EpiGelu<bf16> e{(bf16*)U, (bf16*)A, ld};
+  if (g.b_ncontig) return launch_any<bf16, false, true, kSegNone>(g, e, s);
+  return launch_any<bf16, false, false, kSegNone>(g, e, s);
+}
+
+hipError_t gemm_gelu_bwd(DType dt, const GemmDesc& g, const void* U, void* dU, int64_t ld,
+                         hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (dt != DType::BF16 || g.a_mcontig || g.seg != kSegNone) return hipErrorInvalidValue;
+  const EpiGeluBwd<bf16> e{(const bf16*)U, (bf16*)dU, ld};
+  if (g.b_ncontig) return launch_any<bf16, false, true, kSegNone>(g, e, s);
+  return launch_any<bf16, false, false, kSegNone>(g, e, s);
 }
 
 hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t s) {

@@ -99,6 +99,13 @@ struct HbarEpi {
 };
 hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t s);
 
+// Language-model MLP (bf16 only; A K-contiguous): U = acc and A = gelu(U)
+// (tanh form, of the rounded U), both [M, N] with row stride ld; and the
+// backward dU = acc * gelu'(U) with U as stored by gemm_gelu.
+hipError_t gemm_gelu(DType dt, const GemmDesc& g, void* U, void* A, int64_t ld, hipStream_t s);
+hipError_t gemm_gelu_bwd(DType dt, const GemmDesc& g, const void* U, void* dU, int64_t ld,
+                         hipStream_t s);
+
 // ------------------------------------------------------------------ attention
 // qkv: [B, T, 3D] (Q | K | V), head h at columns h*64 .. h*64+63 of each.
 hipError_t attn_fwd(DType dt, const void* qkv, void* out, float* lse, int B, int T, int D,

@@ -68,3 +68,48 @@ def make_upstream_grad(B, T, D, seed=1, std=1.0, bf16=False):
 def to_f64(layer):
     """Float64 copy of a weight dict (for the oracle)."""
     return {k: np.asarray(v, dtype=np.float64) for k, v in layer.items()}
+
+
+# ---- language model (flat parameter order of the model entry points)
+
+MODEL_LAYER_ARRAYS = ("ln1_g", "ln1_b", "Wq", "Wk", "Wv", "Wo", "Wm", "Wg", "wp", "ln2_g",
+                      "ln2_b", "W1", "W2")
+
+
+def model_array_names(n_layer):
+    """Names of the flat parameter vector's arrays, in order."""
+    names = ["E", "Pe"]
+    for l in range(n_layer):
+        names += [f"{l}.{k}" for k in MODEL_LAYER_ARRAYS]
+    return names + ["lnf_g", "lnf_b"]
+
+
+def make_model_inputs(V, d, T, n_layer, B, seed=0, w_std=0.1, ln_std=0.2):
+    """A seeded model parameter set and a token batch.
+
+    Returns (arrays, tokens, targets): float32 arrays in model_array_names
+    order with the matrices (E, Pe, W*) rounded to bfloat16 values and the
+    LayerNorm gains 1 + N(0, ln_std^2), biases and wp N(0, ...); tokens
+    uniform in [0, V) as int32 [B, T] and targets the tokens shifted by one
+    (the last position takes a fresh draw)."""
+    rng = np.random.default_rng(seed)
+    out = [bf16_round(_draw(rng, (V, d), w_std))[0], bf16_round(_draw(rng, (T, d), w_std))[0]]
+    for _ in range(n_layer):
+        for k in MODEL_LAYER_ARRAYS:
+            if k.endswith("_g"):
+                out.append((1 + _draw(rng, (d,), ln_std)).astype(np.float32))
+            elif k.endswith("_b"):
+                out.append(_draw(rng, (d,), ln_std))
+            elif k == "wp":
+                out.append(bf16_round(_draw(rng, (d,), w_std))[0])
+            elif k == "W1":
+                out.append(bf16_round(_draw(rng, (d, 4 * d), w_std))[0])
+            elif k == "W2":
+                out.append(bf16_round(_draw(rng, (4 * d, d), w_std))[0])
+            else:
+                out.append(bf16_round(_draw(rng, (d, d), w_std))[0])
+    out.append((1 + _draw(rng, (d,), ln_std)).astype(np.float32))
+    out.append(_draw(rng, (d,), ln_std))
+    tokens = rng.integers(0, V, (B, T)).astype(np.int32)
+    targets = np.concatenate([tokens[:, 1:], rng.integers(0, V, (B, 1)).astype(np.int32)], axis=1)
+    return out, tokens, targets

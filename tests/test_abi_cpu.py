@@ -257,3 +257,36 @@ def test_channel_decay_arguments(lib):
     p.gamma_ch = A + 0x7000002                                    # misaligned
     assert _fwd(c, params=p) == abi.BCMT_ERR_INVALID
     assert _bwd(c) == abi.BCMT_ERR_INVALID
+
+
+def test_model_layout_and_argument_errors(lib):
+    """The flat parameter vector holds the arrays of model_array_names back
+    to back, in order; E has V rounded up to a multiple of 128 rows.
+    Invalid configurations size to 0 and the step rejects null pointers
+    before touching the GPU."""
+    from paper_2608_13578_amd.inputs import make_model_inputs, model_array_names
+    V, d, H, nl, B, T, L = 97, 64, 4, 2, 2, 96, 32
+    c = abi.make_model_config(V, d, H, nl, B, T, L)
+    arrs, _, _ = make_model_inputs(V, d, T, nl, B)
+    names = model_array_names(nl)
+    off = 0
+    for i, (name, a) in enumerate(zip(names, arrs)):
+        o, n = abi.bcmt_model_param_array(c, i)
+        want = 128 * d if name == "E" else a.size
+        assert (o, n) == (off, want), name
+        off += n
+    assert abi.bcmt_model_param_count(c) == off
+    assert abi.bcmt_model_workspace_bytes(c) > 0
+    for bad in (dict(V=1), dict(d=96), dict(d=2048), dict(H=3), dict(n_layer=0), dict(L=0)):
+        kw = dict(V=V, d=d, H=H, n_layer=nl, B=B, T=T, L=L)
+        kw.update(bad)
+        cb = abi.make_model_config(**kw)
+        assert abi.bcmt_model_param_count(cb) == 0 and abi.bcmt_model_workspace_bytes(cb) == 0, bad
+    with pytest.raises(abi.BcmtError) as e:
+        abi.bcmt_model_param_array(c, len(names))
+    assert e.value.status == abi.BCMT_ERR_INVALID
+    for i in range(2):  # null tokens / workspace: rejected on the host
+        st = lib.bcmt_model_train_step(ctypes.byref(c), None if i == 0 else 16, 16, 16, 16, 16,
+                                       None, None, None, 16, None if i == 1 else 16, 1 << 40,
+                                       None)
+        assert st == abi.BCMT_ERR_INVALID
