@@ -304,6 +304,83 @@ def decay_variants(make_step, torch, steps=100, warmup=100):
     return out
 
 
+# The language model of the paper's experiments (Sec. 4.1: d_model 128, 6
+# layers, 8 heads, batch 16) with a GPT-2-sized vocabulary; Phase I compares
+# the Dense model with BCMT-128 over context lengths, Phase II the block
+# sizes at T = 1024 (the paper's two throughput tables).
+MODEL = {"V": 50257, "d": 128, "H": 8, "layers": 6, "B": 16, "gamma": 0.8,
+         "phase1": {"Ts": [128, 256, 512, 1024], "L": 128},
+         "phase2": {"T": 1024, "Ls": [64, 128, 256, 512]}}
+
+
+def model_bench(torch, abi, steps=20, warmup=20):
+    """Training step (forward, backward, AdamW) of the language model on
+    synthetic token ids: tokens/s, device bytes (workspace plus the float32
+    parameter, gradient and moment vectors and the bf16 copy) and the ratio
+    to the Dense model (L = T) at the same context length."""
+    import numpy as np
+    from paper_2608_13578_amd.model import ModelBuffers
+    m = MODEL
+    rng = np.random.default_rng(0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cache = {}
+
+    def run(T, L):
+        if (T, L) in cache:
+            return cache[(T, L)]
+        mb = ModelBuffers(m["V"], m["d"], m["H"], m["layers"], m["B"], T, L, m["gamma"])
+        p = torch.randn(mb.n, device="cuda") * 0.02
+        for name, (off, cnt) in zip(mb.names, mb.layout):
+            if name.endswith("_g"):
+                p[off:off + cnt] = 1.0
+            elif name.endswith("_b"):
+                p[off:off + cnt] = 0.0
+        mb.params.copy_(p)
+        abi.bcmt_model_cast(mb.cfg, mb.params, mb.params_bf16)
+        tok = torch.from_numpy(rng.integers(0, m["V"], (m["B"], T)).astype(np.int32)).cuda()
+        tgt = torch.roll(tok, -1, 1).contiguous()
+        opt = {"lr": 1e-4}
+        for _ in range(warmup):
+            mb.step(tok, tgt, opt)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            mb.step(tok, tgt, opt)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        mem = mb.ws_bytes + mb.n * (4 * 4 + 2)
+        r = {"ms_per_step": round(ms, 3), "tokens_per_s": round(m["B"] * T / (ms / 1e3), 1),
+             "device_bytes": int(mem)}
+        del mb, p, tok, tgt
+        torch.cuda.empty_cache()
+        cache[(T, L)] = r
+        return r
+
+    out = {"workload": f"bcmt-lm train step (fwd+bwd+AdamW) V={m['V']} d={m['d']} "
+                       f"layers={m['layers']} H={m['H']}x{m['d'] // m['H']} B={m['B']} bf16",
+           "phase1": {}, "phase2": {}}
+    L1 = m["phase1"]["L"]
+    for T in m["phase1"]["Ts"]:
+        dense, bc = run(T, T), run(T, L1)
+        out["phase1"][str(T)] = {"dense": dense, f"bcmt-{L1}": bc,
+                                 "speedup": round(bc["tokens_per_s"] / dense["tokens_per_s"], 3),
+                                 "memory_ratio": round(bc["device_bytes"] / dense["device_bytes"], 3)}
+    T2 = m["phase2"]["T"]
+    dense = run(T2, T2)
+    out["phase2"]["dense"] = dense
+    for L in m["phase2"]["Ls"]:
+        r = dict(run(T2, L))
+        r["speedup"] = round(r["tokens_per_s"] / dense["tokens_per_s"], 3)
+        r["memory_ratio"] = round(r["device_bytes"] / dense["device_bytes"], 3)
+        out["phase2"][f"bcmt-{L}"] = r
+    for T, r in out["phase1"].items():
+        print(f"model T={T:>5s}: dense {r['dense']['tokens_per_s'] / 1e6:6.2f} M tok/s, "
+              f"bcmt-{L1} {r[f'bcmt-{L1}']['tokens_per_s'] / 1e6:6.2f} M tok/s "
+              f"(x{r['speedup']:.2f}, memory x{r['memory_ratio']:.2f})", file=sys.stderr)
+    return out
+
+
 DECODE = [{"B": 8, "D": 768, "H": 12, "L": 128, "gamma": 0.8},
           {"B": 2, "D": 1024, "H": 16, "L": 256, "gamma": 0.8}]
 
@@ -371,6 +448,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the incremental decoding pass")
     ap.add_argument("--no-decay-variants", action="store_true",
                     help="skip the pass over decay values and the per-channel decay")
+    ap.add_argument("--no-model", action="store_true",
+                    help="skip the language-model pass (paper-shape training step)")
     ap.add_argument("--no-paper-shape", action="store_true",
                     help="skip the pass at the paper's model width (D=128, 16-dim heads)")
     ap.add_argument("--profile-run", action="store_true",
@@ -531,6 +610,8 @@ def main():
         out["decode"] = [decode_bench(torch, abi, dt, g) for g in DECODE]
     if not args.no_paper_shape:
         out["paper_shape"] = paper_shape(make_step, torch, abi)
+    if not args.no_model:
+        out["model"] = model_bench(torch, abi)
     if not args.no_decay_variants:
         out["decay_variants"] = decay_variants(make_step, torch)
     if not args.no_cpu_baseline:

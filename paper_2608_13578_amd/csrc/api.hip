@@ -42,6 +42,21 @@ constexpr int kMaxD = 2048;
 
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Minimum K per split of the D x D weight-gradient products on the side
+// stream: about 144 workgroups in all, which leaves CUs to the critical
+// path beside them (at D = 768, 36 output tiles: 2048-deep splits, 4 of
+// them; the step took 322 us against 326 us with 13 splits and 329 us with
+// 8; 2 splits took 351 us), and at least 128 deep (D = 128: one tile, 128
+// splits).
+int dd_min_k(int D, int K) {
+  const int64_t tiles = (int64_t)((D + 127) / 128) * ((D + 127) / 128);
+  const int mk = (int)((K * tiles / 144 + 63) / 64 * 64);
+  return mk < 128 ? 128 : mk;
+}
+// The same for dW_{q,k,v}: splits at least 128 deep (4 at D = 768, where
+// 2 were slower; up to 128 at small D).
+constexpr int kQkvMinK = 128;
+
 struct Plan {
   int B, T, D, H, L, nb;
   size_t es;
@@ -114,8 +129,8 @@ struct Plan {
     dqkv = take(3 * BTD * es);
     {
       const int BTi = B * T, BNi = B * nb;
-      size_t w = gemm_wgrad_partial_bytes(D, 3 * D, BTi);
-      w = std::max(w, gemm_wgrad_partial_bytes(D, D, BTi));
+      size_t w = gemm_splitk_partial_bytes(D, 3 * D, BTi, kQkvMinK);
+      w = std::max(w, gemm_splitk_partial_bytes(D, D, BTi, dd_min_k(D, BTi)));
       w = std::max(w, gemm_wgrad_partial_bytes(D, D, BNi));
       wpart = take(w);  // weight gradients (side stream, one after another)
     }
@@ -347,12 +362,6 @@ hipError_t order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
       LAUNCH(stage_red, gemm_splitk_reduce(part, sp_, (g).M, (g).N, C0, C1, C2, ldc, seg, acc, s)); \
   } while (0)
 
-// Minimum K per split of the D x D weight-gradient products on the side
-// stream (36 output tiles at D = 768): 2048 deals them as 4 splits, 144
-// workgroups, which leaves CUs to the critical path beside them.  At the
-// measured layer the step took 322 us against 326 us with 13 splits (512)
-// and 329 us with 8 (1024); 2 splits (4096) took 351 us.
-constexpr int kSideMinK = 2048;
 
 #define LAUNCH(stage, expr)                            \
   do {                                                 \
@@ -610,7 +619,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
         if (gr.dWg) {
           GemmDesc g{D, D, BT, SV + p.h, D, true, {W + p.du, nullptr, nullptr}, D, true, kSegNone, 0, 1};
           LAUNCH_SPLITK(ST_WG_WGRAD, ST_WG_WGRAD_RED, dt, g, wpart, gr.dWg, nullptr, nullptr, D, D,
-                        accum, kSideMinK);
+                        accum, dd_min_k(D, BT));
         }
         if (gr.dWm) {
           GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
@@ -682,7 +691,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     {
       GemmDesc g{D, D, BT, SV + p.o, D, true, {dH, nullptr, nullptr}, D, true, kSegNone, 0, 1};
       LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
-                    accum, kSideMinK);
+                    accum, dd_min_k(D, BT));
     }
     SIDE_END();
   }
@@ -707,7 +716,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
       GemmDesc g{D, 3 * D, BT, X, D, true, {W + p.dqkv, nullptr, nullptr}, 3 * D, true, kSegNone,
                  0, 1};
       LAUNCH_SPLITK(ST_QKV_WGRAD, ST_QKV_WGRAD_RED, dt, g, wpart, gr.dWq, gr.dWk, gr.dWv, D, D,
-                    accum, 512);
+                    accum, kQkvMinK);
     }
     SIDE_END();
   }

@@ -424,27 +424,34 @@ struct EpiPartial {
 };
 __device__ __forceinline__ void bind_split(EpiPartial& e, int z) { e.P += z * e.split_stride; }
 
-// Sums the split-K partials (4 consecutive columns per thread) and writes or
-// accumulates into the output segment that holds column n.
+// Sums the split-K partials and writes or accumulates into the output
+// segment that holds each column.  Workgroup = 64 consecutive groups of 4
+// columns; its four waves take the splits z = w, w + 4, ... of their group
+// (each in increasing z), and the four sums are added in a fixed order.
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, int splits,
                                                            int M, int N, float* C0, float* C1,
                                                            float* C2, int64_t ldc, int seg,
                                                            int accumulate) {
+  __shared__ f32x4 red[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t total = (int64_t)M * N / 4;
   const int64_t stride = (int64_t)M * N;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    f32x4 acc = *reinterpret_cast<const f32x4*>(P + i * 4);
-    for (int z = 1; z < splits; ++z) acc += *reinterpret_cast<const f32x4*>(P + z * stride + i * 4);
-    const int64_t e = i * 4;
-    const int m = (int)(e / N), n = (int)(e - (int64_t)m * N);
-    const int sg = n / seg;
-    float* base = sg == 0 ? C0 : sg == 1 ? C1 : C2;
-    if (!base) continue;
-    f32x4* dst = reinterpret_cast<f32x4*>(base + (int64_t)m * ldc + (n - sg * seg));
-    if (accumulate) acc += *dst;
-    *dst = acc;
-  }
+  const int64_t i = (int64_t)blockIdx.x * 64 + lane;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (i < total)
+    for (int z = wave; z < splits; z += 4) acc += *reinterpret_cast<const f32x4*>(P + z * stride + i * 4);
+  red[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0 || i >= total) return;
+  acc = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+  const int64_t e = i * 4;
+  const int m = (int)(e / N), n = (int)(e - (int64_t)m * N);
+  const int sg = n / seg;
+  float* base = sg == 0 ? C0 : sg == 1 ? C1 : C2;
+  if (!base) return;
+  f32x4* dst = reinterpret_cast<f32x4*>(base + (int64_t)m * ldc + (n - sg * seg));
+  if (accumulate) acc += *dst;
+  *dst = acc;
 }
 
 template <typename T>
@@ -1096,9 +1103,7 @@ hipError_t gemm_splitk_reduce(const float* partial, int splits, int M, int N, fl
                               hipStream_t s) {
   if (splits <= 1 || M <= 0 || N <= 0) return hipSuccess;
   const int64_t total = (int64_t)M * N / 4;
-  int64_t blocks = (total + 255) / 256;
-  if (blocks > 2048) blocks = 2048;
-  if (blocks < 1) blocks = 1;
+  const int64_t blocks = (total + 63) / 64;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, partial, splits,
                      M, N, C0, C1, C2, ldc, seg_len_n, accumulate ? 1 : 0);
   return hipGetLastError();

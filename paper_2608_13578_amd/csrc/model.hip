@@ -14,6 +14,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "../../include/bcmt.h"
 #include "common.h"
 #include "kernels.h"
@@ -22,7 +24,10 @@ namespace bcmt {
 namespace {
 
 constexpr float kLnEps = 1e-5f;
-constexpr int kLnRowsPerGroup = 64;  // rows per workgroup of the LayerNorm backward
+constexpr int kLnRowsPerGroup = 64;   // rows per workgroup of the LayerNorm backward
+constexpr int kLnWaves = 16;          // waves per workgroup of the LayerNorm backward
+constexpr int kWgradMinK = 128;     // split depth of the model's weight gradients
+constexpr int kDfMinK = 512;        // split depth of the head's input gradient (K = vocabulary)
 
 // ------------------------------------------------------------------ kernels
 
@@ -98,134 +103,180 @@ __global__ __launch_bounds__(256) void add_ln_fwd_kernel(const bf16* __restrict_
 // LayerNorm backward: dx = dres + rstd (dxh - mean(dxh) - xh mean(dxh xh))
 // with dxh = dy g (dres nullable; dx may alias dres), and this workgroup's
 // partial sums of dy xh (gain) and dy (bias) over its rows into
-// part[blockIdx.x][2][d].
-__global__ __launch_bounds__(256) void ln_bwd_kernel(
-    const bf16* __restrict__ dy, const bf16* __restrict__ xs, const float* __restrict__ mean,
+// part[blockIdx.x][2][d].  Each of the 16 waves takes 4 consecutive rows,
+// RB at a time with all their loads issued first; a lane holds up to NJ
+// elements of a row (d <= 64 NJ).  Dynamic LDS: 16 * 2 * d floats.
+template <typename TY, int NJ, int RB>
+__global__ __launch_bounds__(1024) void ln_bwd_kernel(
+    const TY* __restrict__ dy, const bf16* __restrict__ xs, const float* __restrict__ mean,
     const float* __restrict__ rstd, const float* __restrict__ g, const bf16* dres, bf16* dx,
     float* __restrict__ part, int rows, int d) {
-  __shared__ float red[4][2][1024];
+  constexpr int RW = kLnRowsPerGroup / kLnWaves;  // rows per wave
+  static_assert(RW % RB == 0, "row batches");
+  extern __shared__ float red[];                  // [kLnWaves][2][d]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = d >> 6;
-  float pg[16], pb[16];
+  float pg[NJ], pb[NJ], gg[NJ];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) pg[j] = pb[j] = 0.f;
-  const int r0 = blockIdx.x * kLnRowsPerGroup;
-  const int r1 = min(r0 + kLnRowsPerGroup, rows);
-  for (int r = r0 + wave; r < r1; r += 4) {
-    const int64_t base = (int64_t)r * d + lane;
-    const float mu = mean[r], rs = rstd[r];
-    float xh[16], gy[16];
-    float s1 = 0.f, s2 = 0.f;
+  for (int j = 0; j < NJ; ++j) {
+    pg[j] = pb[j] = 0.f;
+    gg[j] = j < n ? g[lane + 64 * j] : 0.f;
+  }
+  const int rw0 = blockIdx.x * kLnRowsPerGroup + wave * RW;
+  for (int q0 = 0; q0 < RW; q0 += RB) {
+    if (rw0 + q0 >= rows) break;  // wave-uniform
+    float dv[RB][NJ], xh[RB][NJ], mu[RB], rs[RB];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j < n) {
-        const float dv = (float)dy[base + 64 * j];
-        xh[j] = ((float)xs[base + 64 * j] - mu) * rs;
-        gy[j] = dv * g[lane + 64 * j];
-        s1 += gy[j];
-        s2 += gy[j] * xh[j];
-        pg[j] += dv * xh[j];
-        pb[j] += dv;
-      }
+    for (int q = 0; q < RB; ++q) {
+      const int r = min(rw0 + q0 + q, rows - 1);  // a short tail repeats the last row
+      const int64_t base = (int64_t)r * d + lane;
+      mu[q] = mean[r];
+      rs[q] = rstd[r];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (j < n) {
+          dv[q][j] = (float)dy[base + 64 * j];
+          xh[q][j] = (float)xs[base + 64 * j];
+        }
     }
-    const float m1 = wave_sum(s1) / (float)d, m2 = wave_sum(s2) / (float)d;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j < n) {
-        float o = rs * (gy[j] - m1 - xh[j] * m2);
-        if (dres) o += (float)dres[base + 64 * j];
-        dx[base + 64 * j] = (bf16)o;
+    for (int q = 0; q < RB; ++q) {
+      const int r = rw0 + q0 + q;
+      if (r >= rows) break;  // wave-uniform
+      const int64_t base = (int64_t)r * d + lane;
+      float gy[NJ];
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (j < n) {
+          xh[q][j] = (xh[q][j] - mu[q]) * rs[q];
+          gy[j] = dv[q][j] * gg[j];
+          s1 += gy[j];
+          s2 += gy[j] * xh[q][j];
+          pg[j] += dv[q][j] * xh[q][j];
+          pb[j] += dv[q][j];
+        }
+      }
+      const float m1 = wave_sum(s1) / (float)d, m2 = wave_sum(s2) / (float)d;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (j < n) {
+          float o = rs[q] * (gy[j] - m1 - xh[q][j] * m2);
+          if (dres) o += (float)dres[base + 64 * j];
+          dx[base + 64 * j] = (bf16)o;
+        }
       }
     }
   }
 #pragma unroll
-  for (int j = 0; j < 16; ++j)
+  for (int j = 0; j < NJ; ++j)
     if (j < n) {
-      red[wave][0][lane + 64 * j] = pg[j];
-      red[wave][1][lane + 64 * j] = pb[j];
+      red[(wave * 2 + 0) * d + lane + 64 * j] = pg[j];
+      red[(wave * 2 + 1) * d + lane + 64 * j] = pb[j];
     }
   __syncthreads();
   for (int c = threadIdx.x; c < d; c += blockDim.x) {
     float a = 0.f, bb = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      a += red[w][0][c];
-      bb += red[w][1][c];
+    for (int w = 0; w < kLnWaves; ++w) {
+      a += red[(w * 2 + 0) * d + c];
+      bb += red[(w * 2 + 1) * d + c];
     }
     part[((int64_t)blockIdx.x * 2 + 0) * d + c] = a;
     part[((int64_t)blockIdx.x * 2 + 1) * d + c] = bb;
   }
 }
 
-// dg[c] = sum_w part[w][0][c], db[c] = sum_w part[w][1][c], fixed order.
-__global__ __launch_bounds__(256) void ln_param_grad_kernel(const float* __restrict__ part,
-                                                            int nparts, int d,
-                                                            float* __restrict__ dg,
-                                                            float* __restrict__ db) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= 2 * d) return;
-  const int which = c / d, col = c % d;
-  float s = 0.f;
-  for (int w = 0; w < nparts; ++w) s += part[((int64_t)w * 2 + which) * d + col];
-  (which == 0 ? dg : db)[col] = s;
+// dg[c] = sum_w part[w][0][c], db[c] = sum_w part[w][1][c] in a fixed
+// order: workgroup = 64 columns of one of the two, wave k of 16 sums the
+// parts k, k + 16, ... (four accumulators in turn), then the waves add up.
+__global__ __launch_bounds__(1024) void ln_param_grad_kernel(const float* __restrict__ part,
+                                                             int nparts, int d,
+                                                             float* __restrict__ dg,
+                                                             float* __restrict__ db) {
+  __shared__ float red[16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c0 = blockIdx.x * 64;  // over the 2 d columns of [dg | db]
+  const int which = c0 / d, col = c0 % d + lane;
+  const float* src = part + (int64_t)which * d + col;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (int w = wave; w < nparts; w += 16, ++k) acc[k & 3] += src[(int64_t)w * 2 * d];
+  red[wave][lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (wave == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) t += red[w][lane];
+    (which == 0 ? dg : db)[col] = t;
+  }
 }
 
-// Cross-entropy of one row of logits per workgroup: row_loss[r] =
-// logsumexp(z[0..V)) - z[target]; the row is then overwritten with the
-// gradient (softmax - onehot) * inv_n, zero in the padding columns V..Vp.
-__global__ __launch_bounds__(256) void cross_entropy_kernel(bf16* __restrict__ logits,
-                                                            const int32_t* __restrict__ tgt,
-                                                            float* __restrict__ row_loss,
-                                                            int V, int Vp, float inv_n) {
-  __shared__ float sm[4], ss[4];
+// Cross-entropy of one row of logits per workgroup of 1024 threads, the
+// row held in registers (8 columns per thread per step, NC steps; Vp <=
+// 8192 NC): row_loss[r] = logsumexp(z[0..V)) - z[target], and the row is
+// overwritten with the gradient (softmax - onehot) * inv_n, zero in the
+// padding columns V..Vp.
+template <int NC>
+__global__ __launch_bounds__(1024) void cross_entropy_kernel(bf16* __restrict__ logits,
+                                                             const int32_t* __restrict__ tgt,
+                                                             float* __restrict__ row_loss,
+                                                             int V, int Vp, float inv_n) {
+  __shared__ float sm[16], ss[16];
   __shared__ float zt;
   const int r = blockIdx.x;
   bf16* z = logits + (int64_t)r * Vp;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tk = min(max(tgt[r], 0), V - 1);
-  // pass 1: running maximum and sum of exp, 8 columns per step
-  float m = -INFINITY, s = 0.f;
-  for (int c0 = threadIdx.x * 8; c0 < V; c0 += blockDim.x * 8) {
-    float v[8];
-    ld8(z + c0, v);
+  bf16x8 v[NC];  // kept as bf16: 4 registers per step
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      if (c0 + k < V) {
-        const float nm = fmaxf(m, v[k]);
-        s = s * __expf(m - nm) + __expf(v[k] - nm);
-        m = nm;
-      }
-    }
+  for (int q = 0; q < NC; ++q) {
+    const int c0 = (q * 1024 + threadIdx.x) * 8;
+    if (c0 < Vp) v[q] = *reinterpret_cast<const bf16x8*>(z + c0);
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c0 = (q * 1024 + threadIdx.x) * 8;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (c0 + k < V) m = fmaxf(m, (float)v[q][k]);
   }
   const float wm = wave_max(m);
-  s = s * (m == -INFINITY ? 0.f : __expf(m - wm));
-  const float ws = wave_sum(s);
-  if (lane == 0) {
-    sm[wave] = wm;
-    ss[wave] = ws;
-  }
+  if (lane == 0) sm[wave] = wm;
   if (threadIdx.x == 0) zt = (float)z[tk];
   __syncthreads();
   float M = sm[0];
 #pragma unroll
-  for (int w = 1; w < 4; ++w) M = fmaxf(M, sm[w]);
+  for (int w = 1; w < 16; ++w) M = fmaxf(M, sm[w]);
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c0 = (q * 1024 + threadIdx.x) * 8;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (c0 + k < V) s += __expf((float)v[q][k] - M);
+  }
+  const float ws = wave_sum(s);
+  if (lane == 0) ss[wave] = ws;
+  __syncthreads();
   float S = 0.f;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) S += ss[w] * __expf(sm[w] - M);
+  for (int w = 0; w < 16; ++w) S += ss[w];
   const float lse = M + __logf(S);
   if (threadIdx.x == 0) row_loss[r] = lse - zt;
-  // pass 2: the gradient, in place
-  for (int c0 = threadIdx.x * 8; c0 < Vp; c0 += blockDim.x * 8) {
-    float v[8];
-    ld8(z + c0, v);
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c0 = (q * 1024 + threadIdx.x) * 8;
+    if (c0 >= Vp) continue;
+    float o[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int c = c0 + k;
-      float p = c < V ? __expf(v[k] - lse) : 0.f;
+      float p = c < V ? __expf((float)v[q][k] - lse) : 0.f;
       if (c == tk) p -= 1.f;
-      v[k] = p * inv_n;
+      o[k] = p * inv_n;
     }
-    st8(z + c0, v);
+    st8(z + c0, o);
   }
 }
 
@@ -345,7 +396,7 @@ struct ModelPlan {
   size_t layer_saved, layer_ws, wpart_bytes, nparts;
   // offsets into the workspace
   size_t r, a, st1, saved, y, bn, st2, U, A, f, stf, logits, row_loss;
-  size_t dr, dt, dU, dxm, lnpart, wpart, lws, total;
+  size_t dr, dt, df32, dU, dxm, lnpart, wpart, lws, total;
 
   explicit ModelPlan(const bcmt_model_config& c) {
     BT = c.B * c.T;
@@ -357,11 +408,12 @@ struct ModelPlan {
     const size_t wb = bcmt_workspace_bytes(&lc, BCMT_PASS_BACKWARD);
     layer_ws = upb(wf > wb ? wf : wb);
     nparts = (BT + kLnRowsPerGroup - 1) / kLnRowsPerGroup;
-    size_t w = gemm_wgrad_partial_bytes(4 * d, d, BT);
-    const size_t w1 = gemm_wgrad_partial_bytes(d, 4 * d, BT);
-    const size_t w2 = gemm_wgrad_partial_bytes(Vp, d, BT);
-    if (w1 > w) w = w1;
-    if (w2 > w) w = w2;
+    size_t w = gemm_splitk_partial_bytes(4 * d, d, BT, kWgradMinK);
+    const size_t sizes[3] = {gemm_splitk_partial_bytes(d, 4 * d, BT, kWgradMinK),
+                             gemm_splitk_partial_bytes(Vp, d, BT, kWgradMinK),
+                             gemm_splitk_partial_bytes(BT, d, Vp, kDfMinK)};
+    for (size_t x : sizes)
+      if (x > w) w = x;
     wpart_bytes = upb(w);
     const size_t act = upb((size_t)BT * d * 2), act4 = upb((size_t)BT * 4 * d * 2);
     const size_t rowf = upb((size_t)BT * 4);
@@ -387,6 +439,7 @@ struct ModelPlan {
     row_loss = take(rowf);
     dr = take(act);               // gradient of the residual stream
     dt = take(act);
+    df32 = take((size_t)BT * d * 4);  // the head's input gradient (float32)
     dU = take(act4);
     dxm = take(act);
     lnpart = take(nparts * 2 * d * 4);
@@ -400,7 +453,7 @@ int check_model(const bcmt_model_config* c) {
   if (!c) return BCMT_ERR_INVALID;
   if (c->V < 2 || c->d < 64 || c->n_layer < 1 || c->B < 1 || c->T < 1 || c->L < 1 || c->H < 1)
     return BCMT_ERR_INVALID;
-  if (c->d % 64 != 0 || c->d > 1024) return BCMT_ERR_UNSUPPORTED;
+  if (c->d % 64 != 0 || c->d > 1024 || c->V > 65536) return BCMT_ERR_UNSUPPORTED;
   bcmt_config lc{c->B, c->T, c->d, c->H, c->L, c->gamma, BCMT_BF16, 0};
   return bcmt_validate(&lc);
 }
@@ -529,9 +582,21 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
     GemmDesc g{BT, p.Vp, d, W + p.f, d, false, {pw(0), nullptr, nullptr}, d, false, kSegNone, 0, 1};
     CHK(gemm_store(DType::BF16, g, logits, p.Vp, false, nullptr, 0, s));
   }
-  hipLaunchKernelGGL(cross_entropy_kernel, dim3(BT), dim3(256), 0, s, logits, targets,
-                     (float*)(W + p.row_loss), c.V, p.Vp, 1.f / (float)BT);
-  KCHK();
+  {
+    const int nc = (p.Vp + 8191) / 8192;  // 8-column steps per thread (Vp <= 65536)
+    float* rl = (float*)(W + p.row_loss);
+    const float inv = 1.f / (float)BT;
+#define CE(NC)                                                                              \
+  hipLaunchKernelGGL(cross_entropy_kernel<NC>, dim3(BT), dim3(1024), 0, s, logits, targets, rl, \
+                     c.V, p.Vp, inv)
+    if (nc <= 1) CE(1);
+    else if (nc <= 2) CE(2);
+    else if (nc <= 4) CE(4);
+    else if (nc <= 7) CE(7);
+    else CE(8);
+#undef CE
+    KCHK();
+  }
   hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(256), 0, s, (const float*)(W + p.row_loss), BT,
                      loss);
   KCHK();
@@ -541,27 +606,36 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
   float* lnpart = (float*)(W + p.lnpart);
   bf16* dr = (bf16*)(W + p.dr);
   bf16* dt = (bf16*)(W + p.dt);
-  auto ln_bwd = [&](const bf16* dy, const bf16* xs, const float* stats, int gi, const bf16* dres,
+  auto ln_bwd = [&](auto dy, const bf16* xs, const float* stats, int gi, const bf16* dres,
                     bf16* dx) -> hipError_t {
-    hipLaunchKernelGGL(ln_bwd_kernel, dim3((unsigned)p.nparts), dim3(256), 0, s, dy, xs, stats,
-                       stats + rowf / 4, pf(gi), dres, dx, lnpart, BT, d);
+    using TY = typename std::remove_cv<typename std::remove_pointer<decltype(dy)>::type>::type;
+    const size_t lds = (size_t)kLnWaves * 2 * d * sizeof(float);
+    if (d <= 256)
+      hipLaunchKernelGGL((ln_bwd_kernel<TY, 4, 4>), dim3((unsigned)p.nparts), dim3(64 * kLnWaves),
+                         lds, s, dy, xs, stats, stats + rowf / 4, pf(gi), dres, dx, lnpart, BT, d);
+    else
+      hipLaunchKernelGGL((ln_bwd_kernel<TY, 16, 1>), dim3((unsigned)p.nparts),
+                         dim3(64 * kLnWaves), lds, s, dy, xs, stats, stats + rowf / 4, pf(gi),
+                         dres, dx, lnpart, BT, d);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(ln_param_grad_kernel, dim3((2 * d + 255) / 256), dim3(256), 0, s, lnpart,
+    hipLaunchKernelGGL(ln_param_grad_kernel, dim3(2 * d / 64), dim3(1024), 0, s, lnpart,
                        (int)p.nparts, d, gw(gi), gw(gi + 1));
     return hipGetLastError();
   };
   {
     // dE = dlogits^T f (the tied head's part; the lookups add below)
     GemmDesc g{p.Vp, d, BT, logits, p.Vp, true, {W + p.f, nullptr, nullptr}, d, true, kSegNone, 0, 1};
-    CHK(gemm_wgrad(DType::BF16, g, wpart, gw(0), nullptr, nullptr, d, d, false, s));
+    CHK(gemm_splitk(DType::BF16, g, wpart, gw(0), nullptr, nullptr, d, d, false, kWgradMinK, s));
   }
   {
-    // df = dlogits E: B[v][k] = E[v][k], N-contiguous
+    // df = dlogits E: B[v][k] = E[v][k], N-contiguous; K = Vp is long and
+    // N = d narrow, so the product is split along K (float32 result)
     GemmDesc g{BT, d, p.Vp, logits, p.Vp, false, {pw(0), nullptr, nullptr}, d, true, kSegNone, 0, 1};
-    CHK(gemm_store(DType::BF16, g, dt, d, false, nullptr, 0, s));
+    CHK(gemm_splitk(DType::BF16, g, wpart, (float*)(W + p.df32), nullptr, nullptr, d, d, false,
+                    kDfMinK, s));
   }
-  CHK(ln_bwd(dt, R(2 * n), stf, lf, nullptr, dr));
+  CHK(ln_bwd((const float*)(W + p.df32), R(2 * n), stf, lf, nullptr, dr));
   for (int l = n - 1; l >= 0; --l) {
     const bf16* U = (const bf16*)(W + p.U + act4 * l);
     const bf16* A = (const bf16*)(W + p.A + act4 * l);
@@ -575,12 +649,13 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
     }
     {
       GemmDesc g{4 * d, d, BT, A, 4 * d, true, {dr, nullptr, nullptr}, d, true, kSegNone, 0, 1};
-      CHK(gemm_wgrad(DType::BF16, g, wpart, gw(lidx(l, 12)), nullptr, nullptr, d, d, false, s));
+      CHK(gemm_splitk(DType::BF16, g, wpart, gw(lidx(l, 12)), nullptr, nullptr, d, d, false,
+                      kWgradMinK, s));
     }
     {
       GemmDesc g{d, 4 * d, BT, bn, d, true, {dU, nullptr, nullptr}, 4 * d, true, kSegNone, 0, 1};
-      CHK(gemm_wgrad(DType::BF16, g, wpart, gw(lidx(l, 11)), nullptr, nullptr, 4 * d, 4 * d,
-                     false, s));
+      CHK(gemm_splitk(DType::BF16, g, wpart, gw(lidx(l, 11)), nullptr, nullptr, 4 * d, 4 * d,
+                      false, kWgradMinK, s));
     }
     {
       // d(LN2 out) = dU W1^T: B[k][n] = W1[n][k], K-contiguous
