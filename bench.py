@@ -278,16 +278,19 @@ def paper_shape(make_step, torch, abi, steps=100, warmup=100):
 
 def decay_variants(make_step, torch, steps=100, warmup=100):
     """The measured layer with the decays the paper's sensitivity remark
-    spans (0.7, 0.8, 0.9) and with one decay per channel (drawn in
-    [0.7, 0.9]): tokens/s fwd+bwd for each."""
+    spans (0.7, 0.8, 0.9), with one decay per channel (drawn in [0.7, 0.9])
+    and with a multi-scale memory (four channel groups decaying at 0.5, 0.8,
+    0.95, 0.99): tokens/s fwd+bwd for each."""
     import numpy as np
     w = WORKLOAD
     B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     out = {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} bf16"}
     per_ch = np.random.default_rng(5).uniform(0.7, 0.9, D).astype(np.float32)
+    # a multi-scale memory: four channel groups, each with its own decay
+    multi = np.repeat(np.array([0.5, 0.8, 0.95, 0.99], np.float32), D // 4)
     for name, gamma in (("gamma=0.7", 0.7), ("gamma=0.8", 0.8), ("gamma=0.9", 0.9),
-                        ("per-channel", per_ch)):
+                        ("per-channel", per_ch), ("multi-scale", multi)):
         step, keep = make_step(B, T, D, H, L, gamma)
         for _ in range(warmup):
             step()

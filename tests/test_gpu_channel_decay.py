@@ -120,3 +120,15 @@ def test_channel_decay_decode(torch_cuda):
     from paper_2608_13578_amd.inputs import to_f64
     ref, _ = orc.forward(X.astype(np.float64), to_f64(W), L, H, np.asarray(g, np.float64))
     compare({"Y": gpu}, {"Y": ref}, "bf16", "channel-decay-decode")
+
+
+def test_multi_scale_memory(torch_cuda):
+    """A multi-scale memory: four groups of channels, each with its own
+    decay (0.5, 0.8, 0.95, 0.99) and so its own memory over its channels,
+    as one per-channel decay vector; against the oracle."""
+    B, T, D, H, L = 2, 1024, 256, 4, 64
+    X, W, dY = inputs(B, T, D, "bf16", w_std=0.02)
+    g = np.repeat(np.array([0.5, 0.8, 0.95, 0.99], np.float32), D // 4)
+    gpu = run_gpu(torch_cuda, B, T, D, H, L, "bf16", X, W, dY, g)
+    ref = run_oracle(L, H, X, W, dY, g)
+    compare({k: gpu[k] for k in ref}, ref, "bf16", "multi-scale")

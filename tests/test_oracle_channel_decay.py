@@ -155,3 +155,21 @@ def test_channel_decay_gradients_finite_differences(with_state):
         ana = float((gr["dN_in"] * vn).sum())
         fd = directional(lambda e: outputs(N_=carry[0] + e * vn), 1e-3)
         assert abs(fd - ana) <= 1e-6 * np.linalg.norm(gr["dN_in"]) * np.linalg.norm(vn)
+
+
+def test_multi_scale_groups_are_separate_memories():
+    """Channel groups with their own decays are separate memories: the
+    memory of group k equals the single-decay memory (decay of group k) of
+    that group's summaries, and the normalisers follow each group's closed
+    form."""
+    X, W, _ = _setup(96)
+    g = np.repeat([0.3, 0.6, 0.9, 0.97], D // 4)
+    _, c = orc.forward(X, W, L, h, g)
+    S = c["S"]
+    for k in range(4):
+        cols = slice(k * D // 4, (k + 1) * D // 4)
+        M_k = orc.exp_memory(S[:, :, cols], float(g[k * D // 4]))
+        assert _rel(c["M"][:, :, cols], M_k) < 1e-13, k
+    N, Z = c["carry_out"]
+    n = 96 // L
+    assert np.allclose(Z, (1 - g ** n) / (1 - g), rtol=1e-13)
