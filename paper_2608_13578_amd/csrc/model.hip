@@ -215,68 +215,92 @@ __global__ __launch_bounds__(1024) void ln_param_grad_kernel(const float* __rest
 // row held in registers (8 columns per thread per step, NC steps; Vp <=
 // 8192 NC): row_loss[r] = logsumexp(z[0..V)) - z[target], and the row is
 // overwritten with the gradient (softmax - onehot) * inv_n, zero in the
-// padding columns V..Vp.
+// padding columns V..Vp.  The row stays packed (two bf16 per register) and
+// every pass unpacks it again, a shift or a mask per value: kept as floats
+// it would not fit in the registers.  The masks are selects, not branches.
+__device__ __forceinline__ float bf16_half(uint32_t w, int k) {
+  return __uint_as_float(k & 1 ? (w & 0xffff0000u) : (w << 16));
+}
+template <int NC>
+__device__ __forceinline__ void hide_row(uint32_t (&v)[NC][4]) {
+  // the compiler may not carry unpacked values from one pass to the next
+#pragma unroll
+  for (int q = 0; q < NC; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(v[q][j]));
+}
 template <int NC>
 __global__ __launch_bounds__(1024) void cross_entropy_kernel(bf16* __restrict__ logits,
                                                              const int32_t* __restrict__ tgt,
                                                              float* __restrict__ row_loss,
                                                              int V, int Vp, float inv_n) {
+  constexpr float kL2e = 1.4426950408889634f;
   __shared__ float sm[16], ss[16];
-  __shared__ float zt;
   const int r = blockIdx.x;
   bf16* z = logits + (int64_t)r * Vp;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tk = min(max(tgt[r], 0), V - 1);
-  bf16x8 v[NC];  // kept as bf16: 4 registers per step
+  uint32_t v[NC][4];
 #pragma unroll
   for (int q = 0; q < NC; ++q) {
+    // steps past the row end read its last 8 columns again (masked below)
     const int c0 = (q * 1024 + threadIdx.x) * 8;
-    if (c0 < Vp) v[q] = *reinterpret_cast<const bf16x8*>(z + c0);
+    const uint4 x = *reinterpret_cast<const uint4*>(z + min(c0, Vp - 8));
+    v[q][0] = x.x;
+    v[q][1] = x.y;
+    v[q][2] = x.z;
+    v[q][3] = x.w;
   }
   float m = -INFINITY;
 #pragma unroll
   for (int q = 0; q < NC; ++q) {
     const int c0 = (q * 1024 + threadIdx.x) * 8;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (c0 + k < V) m = fmaxf(m, (float)v[q][k]);
+    for (int k = 0; k < 8; ++k) m = fmaxf(m, c0 + k < V ? bf16_half(v[q][k >> 1], k) : -INFINITY);
   }
-  const float wm = wave_max(m);
-  if (lane == 0) sm[wave] = wm;
-  if (threadIdx.x == 0) zt = (float)z[tk];
+  m = wave_max(m);
+  if (lane == 0) sm[wave] = m;
   __syncthreads();
   float M = sm[0];
 #pragma unroll
   for (int w = 1; w < 16; ++w) M = fmaxf(M, sm[w]);
+  const float ml = M * kL2e;
+  hide_row<NC>(v);
   float s = 0.f;
 #pragma unroll
   for (int q = 0; q < NC; ++q) {
     const int c0 = (q * 1024 + threadIdx.x) * 8;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (c0 + k < V) s += __expf((float)v[q][k] - M);
+    for (int k = 0; k < 8; ++k) {
+      const float e = exp2_fast(fmaf(bf16_half(v[q][k >> 1], k), kL2e, -ml));
+      s += c0 + k < V ? e : 0.f;
+    }
   }
-  const float ws = wave_sum(s);
-  if (lane == 0) ss[wave] = ws;
+  s = wave_sum(s);
+  if (lane == 0) ss[wave] = s;
   __syncthreads();
   float S = 0.f;
 #pragma unroll
   for (int w = 0; w < 16; ++w) S += ss[w];
   const float lse = M + __logf(S);
-  if (threadIdx.x == 0) row_loss[r] = lse - zt;
+  const float ll = lse * kL2e;
+  hide_row<NC>(v);
 #pragma unroll
   for (int q = 0; q < NC; ++q) {
     const int c0 = (q * 1024 + threadIdx.x) * 8;
-    if (c0 >= Vp) continue;
     float o[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int c = c0 + k;
-      float p = c < V ? __expf((float)v[q][k] - lse) : 0.f;
-      if (c == tk) p -= 1.f;
+      const float x = bf16_half(v[q][k >> 1], k);
+      float p = c < V ? exp2_fast(fmaf(x, kL2e, -ll)) : 0.f;
+      if (c == tk) {
+        row_loss[r] = lse - x;
+        p -= 1.f;
+      }
       o[k] = p * inv_n;
     }
-    st8(z + c0, o);
+    if (c0 < Vp) st8(z + c0, o);
   }
 }
 

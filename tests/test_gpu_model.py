@@ -50,6 +50,9 @@ CASES = [
     ("bcmt-L32", 97, 64, 4, 2, 2, 96, 32),
     ("dense", 97, 64, 4, 2, 2, 96, 96),
     ("bcmt-dh32-ragged", 300, 128, 4, 1, 2, 100, 48),
+    # the paper's vocabulary: rows of 50304 padded logits, 7 register steps
+    # per thread in the loss kernel, 47 masked padding columns
+    ("bcmt-vocab50257", 50257, 64, 2, 1, 1, 40, 16),
 ]
 
 
