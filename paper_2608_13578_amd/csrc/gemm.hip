@@ -863,6 +863,75 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_pipe_kernel(int M, int N, 
                                                       n0, wm, wn, M, N, tid);
 }
 
+// The tied head of the language model, logits z = f E^T, consumed tile by
+// tile and never stored.  EpiHeadStats leaves, for every row of a 128-column
+// tile, (max, sum of exp(z - max)) over the columns below V at
+// part[2 (m ntile + tile)]; the staged epilogue hands a row's 128 columns to
+// 16 consecutive threads (one DPP row), which reduce them together.
+// EpiHeadGrad stores the loss gradient (softmax - onehot) * inv_n, zero in
+// the padding columns, given each row's log-sum-exp.
+constexpr float kLog2e = 1.4426950408889634f;
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));
+  v = fmaxf(v, dpp_mov<0x4E>(v));
+  v = fmaxf(v, dpp_mov<0x141>(v));
+  return fmaxf(v, dpp_mov<0x140>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  return v + dpp_mov<0x140>(v);
+}
+struct EpiHeadStats {
+  float* part;
+  int ntile;
+  int V;
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    // every thread takes part (the DPP steps read neighbours); only the
+    // row's first thread stores
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) mx = fmaxf(mx, n + e < V ? v[e] : -INFINITY);
+    mx = row16_max(mx);
+    const float ml = mx == -INFINITY ? 0.f : mx * kLog2e;
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = exp2_fast(fmaf(v[e], kLog2e, -ml));
+      sum += n + e < V ? x : 0.f;
+    }
+    sum = row16_sum(sum);
+    if (ok && (n & 127) == 0) {
+      float* q = part + 2 * ((int64_t)m * ntile + (n >> 7));
+      q[0] = mx;
+      q[1] = sum;
+    }
+  }
+};
+struct EpiHeadGrad {
+  bf16* G;
+  int64_t ld;
+  const float* lse;
+  const int32_t* tgt;
+  int V;
+  float inv_n;
+  __device__ __forceinline__ void apply8(int m, int n, const float (&v)[8], bool ok) const {
+    if (!ok) return;
+    const float ll = lse[m] * kLog2e;
+    const int tk = min(max(tgt[m], 0), V - 1);
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int c = n + e;
+      float p = c < V ? exp2_fast(fmaf(v[e], kLog2e, -ll)) : 0.f;
+      if (c == tk) p -= 1.f;
+      o[e] = p * inv_n;
+    }
+    st8(G + (int64_t)m * ld + n, o);
+  }
+};
+
 // ------------------------------------------------------------------ launch
 
 // Tile rows plus tile columns (counted per split, whose K ranges differ)
@@ -1159,6 +1228,26 @@ hipError_t gemm_gelu_bwd(DType dt, const GemmDesc& g, const void* U, void* dU, i
   const EpiGeluBwd<bf16> e{(const bf16*)U, (bf16*)dU, ld};
   if (g.b_ncontig) return launch_any<bf16, false, true, kSegNone>(g, e, s);
   return launch_any<bf16, false, false, kSegNone>(g, e, s);
+}
+
+// Both head products need the pipelined kernel (its epilogue layout) and
+// whole 128-column tiles.
+static bool head_shape_ok(const GemmDesc& g) {
+  return !g.a_mcontig && !g.b_ncontig && g.seg == kSegNone && g.splits <= 1 && g.K % 64 == 0 &&
+         g.M >= 8 && g.N % 128 == 0;
+}
+
+hipError_t gemm_head_stats(const GemmDesc& g, float* part, int V, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (!head_shape_ok(g) || V < 1 || V > g.N) return hipErrorInvalidValue;
+  return launch_pipe<false, false, kSegNone>(g, EpiHeadStats{part, g.N / 128, V}, s);
+}
+
+hipError_t gemm_head_grad(const GemmDesc& g, void* G, int64_t ld, const float* lse,
+                          const int32_t* tgt, int V, float inv_n, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (!head_shape_ok(g) || V < 1 || V > g.N) return hipErrorInvalidValue;
+  return launch_pipe<false, false, kSegNone>(g, EpiHeadGrad{(bf16*)G, ld, lse, tgt, V, inv_n}, s);
 }
 
 hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t s) {

@@ -105,6 +105,15 @@ hipError_t gemm_hbar(DType dt, const GemmDesc& g, const HbarEpi& e, hipStream_t 
 hipError_t gemm_gelu(DType dt, const GemmDesc& g, void* U, void* A, int64_t ld, hipStream_t s);
 hipError_t gemm_gelu_bwd(DType dt, const GemmDesc& g, const void* U, void* dU, int64_t ld,
                          hipStream_t s);
+// The tied head (bf16, A = f K-contiguous, B = E with B[k][v] = E[v][k],
+// M >= 8, K a multiple of 64, N = the vocabulary padded to a multiple of
+// 128): gemm_head_stats writes per row and 128-column tile (max, sum of
+// exp(z - max)) over the columns below V to part (float pairs, row-major
+// [M][N / 128]); gemm_head_grad writes G[m][n] = (softmax(z)[n] - [n ==
+// tgt[m]]) * inv_n as bf16, zero for n >= V, given lse[m].
+hipError_t gemm_head_stats(const GemmDesc& g, float* part, int V, hipStream_t s);
+hipError_t gemm_head_grad(const GemmDesc& g, void* G, int64_t ld, const float* lse,
+                          const int32_t* tgt, int V, float inv_n, hipStream_t s);
 
 // ------------------------------------------------------------------ attention
 // qkv: [B, T, 3D] (Q | K | V), head h at columns h*64 .. h*64+63 of each.

@@ -211,109 +211,60 @@ __global__ __launch_bounds__(1024) void ln_param_grad_kernel(const float* __rest
   }
 }
 
-// Cross-entropy of one row of logits per workgroup of 1024 threads, the
-// row held in registers (8 columns per thread per step, NC steps; Vp <=
-// 8192 NC): row_loss[r] = logsumexp(z[0..V)) - z[target], and the row is
-// overwritten with the gradient (softmax - onehot) * inv_n, zero in the
-// padding columns V..Vp.  The row stays packed (two bf16 per register) and
-// every pass unpacks it again, a shift or a mask per value: kept as floats
-// it would not fit in the registers.  The masks are selects, not branches.
-__device__ __forceinline__ float bf16_half(uint32_t w, int k) {
-  return __uint_as_float(k & 1 ? (w & 0xffff0000u) : (w << 16));
-}
-template <int NC>
-__device__ __forceinline__ void hide_row(uint32_t (&v)[NC][4]) {
-  // the compiler may not carry unpacked values from one pass to the next
-#pragma unroll
-  for (int q = 0; q < NC; ++q)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(v[q][j]));
-}
-template <int NC>
-__global__ __launch_bounds__(1024) void cross_entropy_kernel(bf16* __restrict__ logits,
-                                                             const int32_t* __restrict__ tgt,
-                                                             float* __restrict__ row_loss,
-                                                             int V, int Vp, float inv_n) {
+// Log-sum-exp of each row of logits from the head product's per-tile
+// partials (max, sum of exp(z - max)), one wave per row:
+// lse[r] = M + log sum_j s_j exp(m_j - M) with M the largest m_j, and
+// row_loss[r] = lse[r] - z[r][target], the target's logit taken again as
+// the float32 dot product f[r] . E[target].
+__global__ __launch_bounds__(256) void head_lse_kernel(const float* __restrict__ part, int ntile,
+                                                       const bf16* __restrict__ f,
+                                                       const bf16* __restrict__ E,
+                                                       const int32_t* __restrict__ tgt, int rows,
+                                                       int d, int V, float* __restrict__ lse,
+                                                       float* __restrict__ row_loss) {
   constexpr float kL2e = 1.4426950408889634f;
-  __shared__ float sm[16], ss[16];
-  const int r = blockIdx.x;
-  bf16* z = logits + (int64_t)r * Vp;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= rows) return;  // whole waves
+  float mx = -INFINITY, sm = 0.f;
+  for (int j = lane; j < ntile; j += 64) {
+    const float2 q = *reinterpret_cast<const float2*>(part + 2 * ((int64_t)r * ntile + j));
+    if (q.x > mx) {
+      sm = sm * exp2f((mx - q.x) * kL2e) + q.y;  // exp2f(-inf) = 0 on the first tile
+      mx = q.x;
+    } else {
+      sm += q.y * exp2f((q.x - mx) * kL2e);
+    }
+  }
+  const float M = wave_max(mx);
+  const float S = wave_sum(mx == -INFINITY ? 0.f : sm * exp2f((mx - M) * kL2e));
+  const float l = M + logf(S);
   const int tk = min(max(tgt[r], 0), V - 1);
-  uint32_t v[NC][4];
-#pragma unroll
-  for (int q = 0; q < NC; ++q) {
-    // steps past the row end read its last 8 columns again (masked below)
-    const int c0 = (q * 1024 + threadIdx.x) * 8;
-    const uint4 x = *reinterpret_cast<const uint4*>(z + min(c0, Vp - 8));
-    v[q][0] = x.x;
-    v[q][1] = x.y;
-    v[q][2] = x.z;
-    v[q][3] = x.w;
-  }
-  float m = -INFINITY;
-#pragma unroll
-  for (int q = 0; q < NC; ++q) {
-    const int c0 = (q * 1024 + threadIdx.x) * 8;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) m = fmaxf(m, c0 + k < V ? bf16_half(v[q][k >> 1], k) : -INFINITY);
-  }
-  m = wave_max(m);
-  if (lane == 0) sm[wave] = m;
-  __syncthreads();
-  float M = sm[0];
-#pragma unroll
-  for (int w = 1; w < 16; ++w) M = fmaxf(M, sm[w]);
-  const float ml = M * kL2e;
-  hide_row<NC>(v);
-  float s = 0.f;
-#pragma unroll
-  for (int q = 0; q < NC; ++q) {
-    const int c0 = (q * 1024 + threadIdx.x) * 8;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float e = exp2_fast(fmaf(bf16_half(v[q][k >> 1], k), kL2e, -ml));
-      s += c0 + k < V ? e : 0.f;
-    }
-  }
-  s = wave_sum(s);
-  if (lane == 0) ss[wave] = s;
-  __syncthreads();
-  float S = 0.f;
-#pragma unroll
-  for (int w = 0; w < 16; ++w) S += ss[w];
-  const float lse = M + __logf(S);
-  const float ll = lse * kL2e;
-  hide_row<NC>(v);
-#pragma unroll
-  for (int q = 0; q < NC; ++q) {
-    const int c0 = (q * 1024 + threadIdx.x) * 8;
-    float o[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int c = c0 + k;
-      const float x = bf16_half(v[q][k >> 1], k);
-      float p = c < V ? exp2_fast(fmaf(x, kL2e, -ll)) : 0.f;
-      if (c == tk) {
-        row_loss[r] = lse - x;
-        p -= 1.f;
-      }
-      o[k] = p * inv_n;
-    }
-    if (c0 < Vp) st8(z + c0, o);
+  float z = 0.f;
+  for (int k = lane; k < d; k += 64)
+    z += (float)f[(int64_t)r * d + k] * (float)E[(int64_t)tk * d + k];
+  z = wave_sum(z);
+  if (lane == 0) {
+    lse[r] = l;
+    row_loss[r] = l - z;
   }
 }
 
 // loss = sum(row_loss) / n, one workgroup, fixed order.
-__global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ row_loss,
-                                                       int n, float* __restrict__ loss) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(1024) void loss_sum_kernel(const float* __restrict__ row_loss,
+                                                        int n, float* __restrict__ loss) {
+  __shared__ float red[16];
   float s = 0.f;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) s += row_loss[i];
+#pragma unroll 4
+  for (int i = threadIdx.x; i < n; i += 1024) s += row_loss[i];
   s = wave_sum(s);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
-  if (threadIdx.x == 0) loss[0] = ((red[0] + red[1]) + (red[2] + red[3])) / (float)n;
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) t += red[w];
+    loss[0] = t / (float)n;
+  }
 }
 
 // dE[tok[r]] += dx[r] (float32 atomics: rows sharing a token add in any
@@ -419,7 +370,7 @@ struct ModelPlan {
   bcmt_config lc;  // the BCMT layer's config
   size_t layer_saved, layer_ws, wpart_bytes, nparts;
   // offsets into the workspace
-  size_t r, a, st1, saved, y, bn, st2, U, A, f, stf, logits, row_loss;
+  size_t r, a, st1, saved, y, bn, st2, U, A, f, stf, logits, hpart, lse, row_loss;
   size_t dr, dt, df32, dU, dxm, lnpart, wpart, lws, total;
 
   explicit ModelPlan(const bcmt_model_config& c) {
@@ -459,7 +410,9 @@ struct ModelPlan {
     A = take(act4 * n);           // MLP activations
     f = take(act);                // final LayerNorm output
     stf = take(rowf * 2);
-    logits = take((size_t)BT * Vp * 2);
+    logits = take((size_t)BT * Vp * 2);  // the loss gradient w.r.t. the logits
+    hpart = take((size_t)BT * (Vp / 128) * 8);
+    lse = take(rowf);
     row_loss = take(rowf);
     dr = take(act);               // gradient of the residual stream
     dt = take(act);
@@ -478,6 +431,7 @@ int check_model(const bcmt_model_config* c) {
   if (c->V < 2 || c->d < 64 || c->n_layer < 1 || c->B < 1 || c->T < 1 || c->L < 1 || c->H < 1)
     return BCMT_ERR_INVALID;
   if (c->d % 64 != 0 || c->d > 1024 || c->V > 65536) return BCMT_ERR_UNSUPPORTED;
+  if ((int64_t)c->B * c->T < 8) return BCMT_ERR_UNSUPPORTED;  // the head product needs 8 rows
   bcmt_config lc{c->B, c->T, c->d, c->H, c->L, c->gamma, BCMT_BF16, 0};
   return bcmt_validate(&lc);
 }
@@ -601,28 +555,19 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
                      pf(lf), pf(lf + 1), (bf16*)(W + p.f), stf, stf + rowf / 4, BT, d);
   KCHK();
   bf16* logits = (bf16*)(W + p.logits);
-  {
-    // logits = f E^T: B[k][v] = E[v][k], K-contiguous
-    GemmDesc g{BT, p.Vp, d, W + p.f, d, false, {pw(0), nullptr, nullptr}, d, false, kSegNone, 0, 1};
-    CHK(gemm_store(DType::BF16, g, logits, p.Vp, false, nullptr, 0, s));
-  }
-  {
-    const int nc = (p.Vp + 8191) / 8192;  // 8-column steps per thread (Vp <= 65536)
-    float* rl = (float*)(W + p.row_loss);
-    const float inv = 1.f / (float)BT;
-#define CE(NC)                                                                              \
-  hipLaunchKernelGGL(cross_entropy_kernel<NC>, dim3(BT), dim3(1024), 0, s, logits, targets, rl, \
-                     c.V, p.Vp, inv)
-    if (nc <= 1) CE(1);
-    else if (nc <= 2) CE(2);
-    else if (nc <= 4) CE(4);
-    else if (nc <= 7) CE(7);
-    else CE(8);
-#undef CE
-    KCHK();
-  }
-  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(256), 0, s, (const float*)(W + p.row_loss), BT,
-                     loss);
+  float* lse = (float*)(W + p.lse);
+  // logits = f E^T: B[k][v] = E[v][k], K-contiguous.  The product is taken
+  // twice and never stored: here for each row's log-sum-exp, at the start of
+  // the backward for the gradient.
+  const GemmDesc head{BT, p.Vp, d, W + p.f, d, false, {pw(0), nullptr, nullptr}, d, false,
+                      kSegNone, 0, 1};
+  CHK(gemm_head_stats(head, (float*)(W + p.hpart), c.V, s));
+  hipLaunchKernelGGL(head_lse_kernel, dim3((BT + 3) / 4), dim3(256), 0, s,
+                     (const float*)(W + p.hpart), p.Vp / 128, (const bf16*)(W + p.f), pw(0),
+                     targets, BT, d, c.V, lse, (float*)(W + p.row_loss));
+  KCHK();
+  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(1024), 0, s, (const float*)(W + p.row_loss),
+                     BT, loss);
   KCHK();
 
   // ---- backward
@@ -647,6 +592,8 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
                        (int)p.nparts, d, gw(gi), gw(gi + 1));
     return hipGetLastError();
   };
+  // dlogits = (softmax - onehot) / (B T), over the logits buffer
+  CHK(gemm_head_grad(head, logits, p.Vp, lse, targets, c.V, 1.f / (float)BT, s));
   {
     // dE = dlogits^T f (the tied head's part; the lookups add below)
     GemmDesc g{p.Vp, d, BT, logits, p.Vp, true, {W + p.f, nullptr, nullptr}, d, true, kSegNone, 0, 1};
