@@ -279,13 +279,15 @@ int bcmt_version(void);
  * Weights are input-major as in the layer.  Gradients of every array are
  * written (not accumulated); E's gradient adds the tied head's and the
  * lookups' parts, the latter with float32 atomics (rows sharing a token add
- * in any order, so E's gradient may differ between runs by rounding). */
+ * in any order, so E's gradient may differ between runs by rounding).
+ * Values below the stated minimums give BCMT_ERR_INVALID; d, V or B T
+ * beyond the GPU path's limits give BCMT_ERR_UNSUPPORTED. */
 typedef struct {
-  int32_t V;       /* vocabulary size, >= 2 */
+  int32_t V;       /* vocabulary size, 2 ..= 65536 */
   int32_t d;       /* model width: a multiple of 64, at most 1024 */
   int32_t H;       /* heads of each BCMT layer (d / H in {16, 32, 64}) */
   int32_t n_layer; /* >= 1 */
-  int32_t B, T;    /* sequences per step and tokens per sequence */
+  int32_t B, T;    /* sequences per step and tokens per sequence; B T >= 8 */
   int32_t L;       /* block size of the layers (L >= T: the Dense model) */
   float gamma;     /* memory decay of the layers (fixed, not trained) */
 } bcmt_model_config;

@@ -277,7 +277,8 @@ def test_model_layout_and_argument_errors(lib):
         off += n
     assert abi.bcmt_model_param_count(c) == off
     assert abi.bcmt_model_workspace_bytes(c) > 0
-    for bad in (dict(V=1), dict(d=96), dict(d=2048), dict(H=3), dict(n_layer=0), dict(L=0)):
+    for bad in (dict(V=1), dict(d=96), dict(d=2048), dict(H=3), dict(n_layer=0), dict(L=0),
+                dict(V=65537), dict(B=1, T=7)):
         kw = dict(V=V, d=d, H=H, n_layer=nl, B=B, T=T, L=L)
         kw.update(bad)
         cb = abi.make_model_config(**kw)
