@@ -316,7 +316,7 @@ MODEL = {"V": 50257, "d": 128, "H": 8, "layers": 6, "B": 16, "gamma": 0.8,
          "phase2": {"T": 1024, "Ls": [64, 128, 256, 512]}}
 
 
-def model_bench(torch, abi, steps=20, warmup=20):
+def model_bench(torch, abi, steps=20, warmup=20, only=None):
     """Training step (forward, backward, AdamW) of the language model on
     synthetic token ids: tokens/s, device bytes (workspace plus the float32
     parameter, gradient and moment vectors and the bf16 copy) and the ratio
@@ -359,6 +359,9 @@ def model_bench(torch, abi, steps=20, warmup=20):
         torch.cuda.empty_cache()
         cache[(T, L)] = r
         return r
+
+    if only is not None:  # one (T, L) configuration, for the profiler
+        return run(*only)
 
     out = {"workload": f"bcmt-lm train step (fwd+bwd+AdamW) V={m['V']} d={m['d']} "
                        f"layers={m['layers']} H={m['H']}x{m['d'] // m['H']} B={m['B']} bf16",
@@ -455,6 +458,9 @@ def main():
                     help="skip the language-model pass (paper-shape training step)")
     ap.add_argument("--no-paper-shape", action="store_true",
                     help="skip the pass at the paper's model width (D=128, 16-dim heads)")
+    ap.add_argument("--profile-model", action="store_true",
+                    help="for rocprofv3: only the language-model training step at T=1024, "
+                         "L=128 (--warmup untimed steps, then --steps)")
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
                          "library's stage tracing on (every stage serialised on one stream, "
@@ -478,6 +484,11 @@ def main():
     B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
     dt = w["dtype"]
     torch.cuda.set_device(0)
+    if args.profile_model:
+        r = model_bench(torch, abi, steps=args.steps, warmup=args.warmup,
+                        only=(1024, MODEL["phase1"]["L"]))
+        print(json.dumps({"profile_model": True, "T": 1024, "L": MODEL["phase1"]["L"], **r}))
+        return
 
     def make_step(B, T, D, H, L, gamma):
         X, [W] = make_layer_inputs(B, T, D, seed=0, bf16=True)
