@@ -467,7 +467,7 @@ def main():
                          "as in the per-stage pass of the normal run)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the benchmark runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the layer's multi-GPU sharding is a design, not an implementation)", file=sys.stderr)
         sys.exit(2)
 
