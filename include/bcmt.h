@@ -24,10 +24,8 @@
  *
  * Conventions
  *   - All tensors are row-major and live in device memory owned by the
- *     caller; the library allocates no tensor memory.  The only state it
- *     keeps is one non-blocking stream (default priority) and a few events
- *     per device, created by the first backward call on that device and
- *     kept until the process ends.
+ *     caller.  The layer entry points allocate nothing and create no streams
+ *     or events; they keep no state between calls.
  *   - Activations X, Y, dY, dX are [B, T, D]; weights Wq, Wk, Wv, Wo, Wm, Wg
  *     are [D, D] input-major (y = x W; a torch Linear weight is the
  *     transpose), wp is [D].  They all have the element type cfg->dtype.
@@ -35,12 +33,8 @@
  *   - Every pointer must be 16-byte aligned.
  *   - Work is enqueued on `stream` (a hipStream_t of the calling thread's
  *     current device; NULL means the default stream); nothing synchronises
- *     the host.  The backward pass runs its weight-gradient products on the
- *     library's stream, ordered after their inputs on `stream` with events,
- *     and makes `stream` wait for them before it returns: work enqueued on
- *     `stream` afterwards sees every output, exactly as if all of it had run
- *     on `stream`.  Calls on one device from several host threads are
- *     serialised while they enqueue.
+ *     the host.  The backward passes may also take a caller-owned second
+ *     stream (bcmt_side, below) for their weight-gradient products.
  *   - The GPU path needs a head width D / H of 64, 32 or 16 (the paper's
  *     model uses 16), D a multiple of 64 and D <= 2048.
  *
@@ -116,6 +110,24 @@ typedef struct {
   float* dgamma_ch;                         /* [D], with BCMT_FLAG_CHANNEL_DECAY */
 } bcmt_grads;
 
+/* Optional second stream of the backward passes.  The weight-gradient
+ * products (dWg, dWm, dwp, dWo, dWq, dWk, dWv), which no later step of the
+ * pass reads, then run on side->stream beside the critical path: each is
+ * ordered after its inputs on `stream` by recording side->fork on `stream`
+ * and making side->stream wait for it, and before returning the pass records
+ * side->join on side->stream and makes `stream` wait for it.  Work enqueued on
+ * `stream` after the call therefore sees every output, exactly as if all of
+ * it had run on `stream`.  The caller creates and owns the stream (same
+ * device as `stream`, default priority) and the two events (timing may be
+ * disabled), and must not use one bcmt_side in two calls that enqueue at the
+ * same time.  Passing NULL runs everything on `stream`.  While stage tracing
+ * is on, the second stream is not used. */
+typedef struct {
+  void* stream; /* hipStream_t */
+  void* fork;   /* hipEvent_t, recorded on `stream` before each branch */
+  void* join;   /* hipEvent_t, recorded on side->stream at the end */
+} bcmt_side;
+
 /* Host-only check of a configuration; returns BCMT_OK or a negative status.
  * Makes no HIP call. */
 int bcmt_validate(const bcmt_config* cfg);
@@ -149,12 +161,14 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
  *   grads  float32 weight/decay gradients (overwritten, or accumulated
  *          with BCMT_FLAG_ACCUM_WGRAD); NULL, or NULL members, skip them.
  *   ws     at least bcmt_workspace_bytes(cfg, BCMT_PASS_BACKWARD) bytes.
+ *   side   a second stream for the weight-gradient products, or NULL
+ *          (BCMT_ERR_INVALID if given without both events).
  * The weight-matrix gradients and dwp are reduced in a fixed order
  * (deterministic); dgamma is summed with float32 atomics, so it may differ
  * run to run in the last bits. */
 int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* params,
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
-                        void* ws, size_t ws_bytes, void* stream);
+                        void* ws, size_t ws_bytes, void* stream, const bcmt_side* side);
 
 /* ---- Chunked execution ---------------------------------------------------
  * Only the memory of Sec. 3.5 crosses block boundaries, through the decayed
@@ -206,7 +220,7 @@ int bcmt_layer_forward_chunk(const bcmt_config* cfg, const void* X, const bcmt_p
 int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* params,
                               const void* saved, const void* dY, const bcmt_carry* dcarry_out,
                               void* dX, const bcmt_carry* dcarry_in, const bcmt_grads* grads,
-                              void* ws, size_t ws_bytes, void* stream);
+                              void* ws, size_t ws_bytes, void* stream, const bcmt_side* side);
 
 /* ---- Incremental decoding ------------------------------------------------
  * The layer is causal (Sec. 3.6): the output of token t of block i depends
@@ -252,7 +266,8 @@ int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* params, int64_t 
 /* Static description of a status code. */
 const char* bcmt_strerror(int status);
 
-/* Library version, major * 10000 + minor * 100 + patch. */
+/* Library version, major * 10000 + minor * 100 + patch (2.0.0: the backward
+ * passes take a caller-owned second stream). */
 int bcmt_version(void);
 
 /* ---------------------------------------------------------------- language model
@@ -317,20 +332,23 @@ int bcmt_model_cast(const bcmt_model_config* cfg, const float* params, void* par
  * the gradients are computed (adam_m, adam_v may be NULL).  The forward
  * reads params_bf16 (weights) and params (LayerNorm gains and biases).
  * All pointers are device memory, 16-byte aligned; ws holds at least
- * bcmt_model_workspace_bytes(cfg).  Errors as for the layer. */
+ * bcmt_model_workspace_bytes(cfg).  `side` is passed to each layer's
+ * backward pass (NULL: everything on `stream`).  Errors as for the layer. */
 int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
                           const int32_t* targets, float* params, void* params_bf16,
                           float* grads, float* adam_m, float* adam_v, const bcmt_adamw* opt,
-                          float* loss, void* ws, size_t ws_bytes, void* stream);
+                          float* loss, void* ws, size_t ws_bytes, void* stream,
+                          const bcmt_side* side);
 
 /* ---- Stage tracing (profiling aid) -------------------------------------
  * While tracing is on, every kernel launch of bcmt_layer_forward and
  * bcmt_layer_backward is bracketed by two HIP events recorded on the call's
  * stream, so each stage's GPU time is measured in place.  While tracing is
  * on, the backward pass also keeps its weight-gradient products on the
- * call's stream instead of the library's stream, so that every stage is
- * timed alone.  The timing events are created by the library on first use
- * and reused.  Stage names are static strings such as "fwd.qkv_gemm" or
+ * call's stream instead of a second stream, so that every stage is timed
+ * alone.  The timing events (a fixed pool of 16384) are created by
+ * bcmt_trace_enable on the current device and reused; a launch that finds
+ * the pool exhausted (too many launches between two reads) is not timed.  Stage names are static strings such as "fwd.qkv_gemm" or
  * "bwd.attention_dkdv". */
 typedef struct {
   const char* name; /* static string */

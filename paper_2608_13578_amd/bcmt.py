@@ -71,6 +71,11 @@ class bcmt_carry(ctypes.Structure):
     _fields_ = [("N", ctypes.c_void_p), ("Z", ctypes.c_void_p)]
 
 
+class bcmt_side(ctypes.Structure):
+    """A second stream and its fork / join events (hipStream_t, hipEvent_t)."""
+    _fields_ = [("stream", ctypes.c_void_p), ("fork", ctypes.c_void_p), ("join", ctypes.c_void_p)]
+
+
 class bcmt_model_config(ctypes.Structure):
     _fields_ = [("V", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("n_layer", ctypes.c_int32), ("B", ctypes.c_int32), ("T", ctypes.c_int32),
@@ -110,8 +115,10 @@ def lib():
         L.bcmt_layer_forward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
                                          ctypes.c_size_t, vp]
         L.bcmt_layer_forward.restype = ctypes.c_int
+        sidep = ctypes.POINTER(bcmt_side)
         L.bcmt_layer_backward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
-                                          ctypes.POINTER(bcmt_grads), vp, ctypes.c_size_t, vp]
+                                          ctypes.POINTER(bcmt_grads), vp, ctypes.c_size_t, vp,
+                                          sidep]
         L.bcmt_layer_backward.restype = ctypes.c_int
         carryp = ctypes.POINTER(bcmt_carry)
         L.bcmt_layer_forward_chunk.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), carryp, vp,
@@ -119,7 +126,7 @@ def lib():
         L.bcmt_layer_forward_chunk.restype = ctypes.c_int
         L.bcmt_layer_backward_chunk.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp,
                                                 carryp, vp, carryp, ctypes.POINTER(bcmt_grads),
-                                                vp, ctypes.c_size_t, vp]
+                                                vp, ctypes.c_size_t, vp, sidep]
         L.bcmt_layer_backward_chunk.restype = ctypes.c_int
         L.bcmt_decode_state_bytes.argtypes = [cfgp]
         L.bcmt_decode_state_bytes.restype = ctypes.c_size_t
@@ -151,7 +158,7 @@ def lib():
         L.bcmt_model_cast.restype = ctypes.c_int
         L.bcmt_model_train_step.argtypes = [mcp, vp, vp, vp, vp, vp, vp, vp,
                                             ctypes.POINTER(bcmt_adamw), vp, vp, ctypes.c_size_t,
-                                            vp]
+                                            vp, sidep]
         L.bcmt_model_train_step.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,6 +216,18 @@ def _carry(c):
     return bcmt_carry(_ptr(c[0]), _ptr(c[1]))
 
 
+def _side(side):
+    """None, a bcmt_side, or an object with .stream, .fork and .join (torch
+    stream and events, or raw handles)."""
+    if side is None or isinstance(side, bcmt_side):
+        return side
+
+    def h(x, attr):
+        return x if isinstance(x, int) else getattr(x, attr)
+    return bcmt_side(h(side.stream, "cuda_stream"), h(side.fork, "cuda_event"),
+                     h(side.join, "cuda_event"))
+
+
 def _ref(x):
     return ctypes.byref(x) if x is not None else None
 
@@ -246,14 +265,15 @@ def bcmt_layer_forward(cfg, X, params, Y, saved, ws, ws_bytes=None, stream=None)
         raise BcmtError(st, "bcmt_layer_forward")
 
 
-def bcmt_layer_backward(cfg, X, params, saved, dY, dX, grads, ws, ws_bytes=None, stream=None):
+def bcmt_layer_backward(cfg, X, params, saved, dY, dX, grads, ws, ws_bytes=None, stream=None,
+                        side=None):
     if ws_bytes is None:
         ws_bytes = 0 if ws is None else _nbytes(ws)
     g = _grads(grads)
     st = lib().bcmt_layer_backward(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
                                    _ptr(saved), _ptr(dY), _ptr(dX),
                                    ctypes.byref(g) if g is not None else None, _ptr(ws),
-                                   int(ws_bytes), _stream(stream))
+                                   int(ws_bytes), _stream(stream), _ref(_side(side)))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_layer_backward")
 
@@ -270,14 +290,14 @@ def bcmt_layer_forward_chunk(cfg, X, params, carry_in, Y, carry_out, saved, ws, 
 
 
 def bcmt_layer_backward_chunk(cfg, X, params, saved, dY, dcarry_out, dX, dcarry_in, grads, ws,
-                              ws_bytes=None, stream=None):
+                              ws_bytes=None, stream=None, side=None):
     if ws_bytes is None:
         ws_bytes = 0 if ws is None else _nbytes(ws)
     g = _grads(grads)
     st = lib().bcmt_layer_backward_chunk(ctypes.byref(cfg), _ptr(X), ctypes.byref(_params(params)),
                                          _ptr(saved), _ptr(dY), _ref(_carry(dcarry_out)), _ptr(dX),
                                          _ref(_carry(dcarry_in)), _ref(g), _ptr(ws), int(ws_bytes),
-                                         _stream(stream))
+                                         _stream(stream), _ref(_side(side)))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_layer_backward_chunk")
 
@@ -356,12 +376,12 @@ def bcmt_model_cast(cfg, params, params_bf16, stream=None):
 
 
 def bcmt_model_train_step(cfg, tokens, targets, params, params_bf16, grads, adam_m, adam_v, opt,
-                          loss, ws, ws_bytes=None, stream=None):
+                          loss, ws, ws_bytes=None, stream=None, side=None):
     if ws_bytes is None:
         ws_bytes = 0 if ws is None else _nbytes(ws)
     st = lib().bcmt_model_train_step(ctypes.byref(cfg), _ptr(tokens), _ptr(targets),
                                      _ptr(params), _ptr(params_bf16), _ptr(grads), _ptr(adam_m),
                                      _ptr(adam_v), _ref(opt), _ptr(loss), _ptr(ws),
-                                     int(ws_bytes), _stream(stream))
+                                     int(ws_bytes), _stream(stream), _ref(_side(side)))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_model_train_step")

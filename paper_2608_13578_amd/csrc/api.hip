@@ -17,8 +17,9 @@
 // Backward runs the chain rule through the same steps in reverse.  Its
 // critical path (gate -> memory -> pooling -> dH -> attention -> dX) stays on
 // the caller's stream; the weight-gradient products, which nothing later in
-// the pass reads, run on a library-owned side stream that forks from the
-// caller's stream after their inputs exist and joins it before the pass ends.
+// the pass reads, run on a second stream that the caller may supply: it forks
+// from the caller's stream after their inputs exist and joins it before the
+// pass ends.  Without one, everything runs on the caller's stream.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -26,7 +27,6 @@
 #include <cstdint>
 #include <cstring>
 #include <algorithm>
-#include <map>
 #include <mutex>
 #include <vector>
 
@@ -68,8 +68,8 @@ struct Plan {
   // forward scratch
   size_t sp, St, mpart, cpart, fwd_bytes;
   // backward scratch
-  size_t du, pbar, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart;
-  size_t cpbar, cdm, ce0, cpart_b;  // chunk state gradients
+  size_t du, pbar, pbar_lo, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart;
+  size_t cpbar, cpbar_lo, cdm, ce0, cpart_b;  // chunk state gradients
   size_t bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
@@ -117,6 +117,8 @@ struct Plan {
     off = 0;
     du = take(BTD * es);
     pbar = take(BND * es);
+    // bf16: the low part of each shifted context-gradient value (hi + lo)
+    pbar_lo = take(dt == DType::BF16 ? BND * es : 0);
     dS = take(BND * 4);
     dM = take(mem_fused(nb, pc) ? 0 : BND * 4);
     mpart_b = take(mem_part_bytes(B, nb, D, pc));
@@ -135,6 +137,7 @@ struct Plan {
       wpart = take(w);  // weight gradients (side stream, one after another)
     }
     cpbar = take(BD * es);
+    cpbar_lo = take(dt == DType::BF16 ? BD * es : 0);
     cdm = take(BD * 4);
     ce0 = take(BD * 4);
     cpart_b = take(carry_part_bytes(B, D));
@@ -267,22 +270,28 @@ struct Tracer {
     hipEvent_t a, b;
   };
   std::vector<Rec> pending;
+  // Events are created by bcmt_trace_enable only, never by a layer call; a
+  // launch that finds the pool empty is not timed (and counted as dropped).
   std::vector<hipEvent_t> pool;
+  int created = 0;
+  int64_t dropped = 0;
   double total[ST_COUNT] = {};
   int calls[ST_COUNT] = {};
 
   hipEvent_t take() {
-    if (!pool.empty()) {
-      hipEvent_t e = pool.back();
-      pool.pop_back();
-      return e;
+    if (pool.empty()) {
+      ++dropped;
+      return nullptr;
     }
-    hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    hipEvent_t e = pool.back();
+    pool.pop_back();
     return e;
   }
 };
 Tracer g_trace;
+// Events the tracer holds: two per traced launch, enough for a few hundred
+// passes between two reads.
+constexpr int kTraceEvents = 16384;
 
 // Brackets one launch with two events on the launch stream when tracing is on.
 struct TraceScope {
@@ -292,6 +301,10 @@ struct TraceScope {
   TraceScope(int st, hipStream_t str) : stage(st), s(str) {
     if (!g_trace.on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_trace.mu);
+    if (g_trace.pool.size() < 2) {
+      ++g_trace.dropped;
+      return;
+    }
     a = g_trace.take();
     if (a && hipEventRecord(a, s) != hipSuccess) {
       g_trace.pool.push_back(a);
@@ -311,40 +324,6 @@ struct TraceScope {
     a = nullptr;
   }
 };
-
-// ------------------------------------------------------------------ side stream
-// One non-blocking side stream per device (default priority) and the events
-// that order it against the caller's stream.  Created on first use and kept
-// until the process ends; a pass holds its device's lock while it enqueues,
-// so that two host threads never interleave their uses of the events.
-struct SideDev {
-  std::mutex mu;
-  hipStream_t side = nullptr;
-  hipEvent_t ev[8] = {};
-  bool ready = false;
-};
-std::mutex g_side_mu;
-std::map<int, SideDev*> g_side;
-
-SideDev* side_for_current_device() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  SideDev* d;
-  {
-    std::lock_guard<std::mutex> lk(g_side_mu);
-    auto it = g_side.find(dev);
-    if (it == g_side.end()) it = g_side.emplace(dev, new SideDev).first;
-    d = it->second;
-  }
-  std::lock_guard<std::mutex> lk(d->mu);
-  if (!d->ready) {
-    if (hipStreamCreateWithFlags(&d->side, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    for (auto& e : d->ev)
-      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
-    d->ready = true;
-  }
-  return d;
-}
 
 // Makes `to` wait for everything enqueued so far on `from`.
 hipError_t order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
@@ -406,9 +385,21 @@ const char* bcmt_strerror(int status) {
   }
 }
 
-int bcmt_version(void) { return 100; }
+int bcmt_version(void) { return 20000; }
 
-int bcmt_trace_enable(int on) { return g_trace.on.exchange(on != 0) ? 1 : 0; }
+int bcmt_trace_enable(int on) {
+  if (on) {
+    // The timing events are created here, on the current device, once.
+    std::lock_guard<std::mutex> lk(g_trace.mu);
+    while (g_trace.created < kTraceEvents) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreate(&e) != hipSuccess) break;
+      g_trace.pool.push_back(e);
+      ++g_trace.created;
+    }
+  }
+  return g_trace.on.exchange(on != 0) ? 1 : 0;
+}
 
 int bcmt_trace_read(bcmt_trace_entry* out, int max_entries) {
   if (max_entries < 0 || (max_entries > 0 && !out)) return BCMT_ERR_INVALID;
@@ -511,7 +502,7 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
                                    cin ? nullptr : (float*)(SV + p.cP), p.B, D, cr.zcol, s));
     if (cin)
       LAUNCH(ST_CARRY_PROJ, carry_proj(dt, SV + p.cMt, prm->Wm, (float*)(SV + p.cP),
-                                       (float*)(W + p.cpart), false, p.B, D, s));
+                                       (float*)(W + p.cpart), false, false, p.B, D, s));
     cr.Nin = (const float*)(SV + p.cN);
     cr.Zin = (const float*)(SV + p.cZ);
     cr.Pc = (const float*)(SV + p.cP);
@@ -534,11 +525,12 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
 
 static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
                           const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
-                          void* ws, size_t ws_bytes, void* stream, bool chunk,
-                          const bcmt_carry* dcout, const bcmt_carry* dcin) {
+                          void* ws, size_t ws_bytes, void* stream, const bcmt_side* side,
+                          bool chunk, const bcmt_carry* dcout, const bcmt_carry* dcin) {
   int st = check_config(cfg);
   if (st != BCMT_OK) return st;
   if (!X || !prm || !saved || !dY) return BCMT_ERR_INVALID;
+  if (side && (!side->fork || !side->join)) return BCMT_ERR_INVALID;
   if (!carry_ok(dcout) || !carry_ok(dcin) || !decay_ok(cfg, prm)) return BCMT_ERR_INVALID;
   const void* w[7] = {prm->Wq, prm->Wk, prm->Wv, prm->Wo, prm->Wm, prm->Wg, prm->wp};
   for (const void* p : w)
@@ -563,13 +555,14 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   if (!ws) return BCMT_ERR_INVALID;
   if (ws_bytes < p.bwd_bytes) return BCMT_ERR_WORKSPACE;
 
-  SideDev* sd = side_for_current_device();
-  if (!sd) return BCMT_ERR_HIP;
-  std::lock_guard<std::mutex> side_lock(sd->mu);
-  // With per-stage tracing on, everything runs on the caller's stream so
-  // that each stage is timed alone.
-  const bool fork = !g_trace.on.load(std::memory_order_relaxed);
-  const hipStream_t main_s = (hipStream_t)stream, side_s = fork ? sd->side : main_s;
+  // The weight-gradient products go to the caller's second stream when one
+  // is given.  With per-stage tracing on, everything runs on the caller's
+  // stream so that each stage is timed alone.
+  const bool fork = side && !g_trace.on.load(std::memory_order_relaxed);
+  const hipStream_t main_s = (hipStream_t)stream;
+  const hipStream_t side_s = fork ? (hipStream_t)side->stream : main_s;
+  const hipEvent_t ev_fork = fork ? (hipEvent_t)side->fork : nullptr;
+  const hipEvent_t ev_join = fork ? (hipEvent_t)side->join : nullptr;
   hipStream_t s = main_s;  // the stream LAUNCH enqueues on
   const char* SV = (const char*)saved;
   char* W = (char*)ws;
@@ -579,12 +572,14 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
 
   const bool accum = cfg->flags & BCMT_FLAG_ACCUM_WGRAD;
   float* wpart = (float*)(W + p.wpart);
-  int nev = 0;
-  // Work between SIDE_BEGIN and SIDE_END runs on the side stream, after
-  // everything enqueued so far on the caller's stream.
+  int nfork = 0;
+  // Work between SIDE_BEGIN and SIDE_END runs on the second stream, after
+  // everything enqueued so far on the caller's stream.  One fork event serves
+  // every fork: each wait takes the record made just before it.
 #define SIDE_BEGIN()                                                                   \
   do {                                                                                 \
-    if (fork && order_after(side_s, main_s, sd->ev[nev++]) != hipSuccess) return BCMT_ERR_HIP; \
+    if (fork && order_after(side_s, main_s, ev_fork) != hipSuccess) return BCMT_ERR_HIP; \
+    nfork += fork;                                                                     \
     s = side_s;                                                                        \
   } while (0)
 #define SIDE_END() (s = main_s)
@@ -607,11 +602,14 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     // dgamma is reduced with atomics later in the pass; this kernel clears it
     // first unless the gradients accumulate.  The weight matrices and dwp are
     // written (or accumulated) by fixed-order reductions.
+    const bool lo = dt == DType::BF16;  // context gradients kept as hi + lo
     LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
+                                 lo ? W + p.pbar_lo : nullptr,
                                  (accum || !gvec) ? nullptr : dgam, gvec ? D : 0,
                                  (accum || gvec) ? nullptr : dgam, p.B, p.T, D, p.L,
                                  chunk ? (const float*)(SV + p.cP) : nullptr,
-                                 chunk ? W + p.cpbar : nullptr, s));
+                                 chunk ? W + p.cpbar : nullptr,
+                                 (chunk && lo) ? W + p.cpbar_lo : nullptr, s));
     // dWg = H^T dU and dWm = M^T dP on the side stream.
     if (gr.dWg || gr.dWm) {
       SIDE_BEGIN();
@@ -645,14 +643,18 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     cr.zcol = gvec != nullptr;
     if (chunk) {
       LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar, prm->Wm, (float*)(W + p.cdm),
-                                        (float*)(W + p.cpart_b), true, p.B, D, s));
+                                        (float*)(W + p.cpart_b), true, false, p.B, D, s));
+      if (lo)
+        LAUNCH(ST_CARRY_DGRAD, carry_proj(dt, W + p.cpbar_lo, prm->Wm, (float*)(W + p.cdm),
+                                          (float*)(W + p.cpart_b), true, true, p.B, D, s));
       cr.Zin = (const float*)(SV + p.cZ);
       cr.dNout = dcout ? dcout->N : nullptr;
       cr.dZout = dcout ? dcout->Z : nullptr;
       cr.e0 = (float*)(W + p.ce0);
     }
-    LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, prm->Wm, (const float*)(SV + p.M), (float*)(W + p.dS),
-                               dgam, (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
+    LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, lo ? W + p.pbar_lo : nullptr, prm->Wm,
+                               (const float*)(SV + p.M), (float*)(W + p.dS), dgam,
+                               (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
                                cfg->gamma, cr, s));
     if (chunk)
       LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
@@ -726,7 +728,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     LAUNCH(ST_DX, gemm_store(dt, g, dX, D, false, residual ? dY : nullptr, D, s));
   }
   // Join: later work on the caller's stream sees every side-stream result.
-  if (nev > 0 && order_after(main_s, side_s, sd->ev[nev++]) != hipSuccess) return BCMT_ERR_HIP;
+  if (nfork > 0 && order_after(main_s, side_s, ev_join) != hipSuccess) return BCMT_ERR_HIP;
 #undef SIDE_BEGIN
 #undef SIDE_END
   return BCMT_OK;
@@ -741,9 +743,9 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
 
 int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
-                        void* ws, size_t ws_bytes, void* stream) {
-  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, false, nullptr,
-                        nullptr);
+                        void* ws, size_t ws_bytes, void* stream, const bcmt_side* side) {
+  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, side, false,
+                        nullptr, nullptr);
 }
 
 int bcmt_layer_forward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
@@ -755,9 +757,10 @@ int bcmt_layer_forward_chunk(const bcmt_config* cfg, const void* X, const bcmt_p
 int bcmt_layer_backward_chunk(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
                               const void* saved, const void* dY, const bcmt_carry* dcarry_out,
                               void* dX, const bcmt_carry* dcarry_in, const bcmt_grads* grads,
-                              void* ws, size_t ws_bytes, void* stream) {
-  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, true, dcarry_out,
-                        dcarry_in);
+                              void* ws, size_t ws_bytes, void* stream,
+                              const bcmt_side* side) {
+  return layer_backward(cfg, X, prm, saved, dY, dX, grads, ws, ws_bytes, stream, side, true,
+                        dcarry_out, dcarry_in);
 }
 
 size_t bcmt_decode_state_bytes(const bcmt_config* cfg) {
@@ -790,7 +793,7 @@ int bcmt_decode_reset(const bcmt_config* cfg, const bcmt_params* prm, const bcmt
                                   channel_decay(cfg, prm) != nullptr, s));
   if (carry_in)
     LAUNCH(ST_DEC_RESET, carry_proj(p.dt, W + p.Mt, prm->Wm, (float*)(S + p.C),
-                                    (float*)(W + p.cpart), false, p.B, p.D, s));
+                                    (float*)(W + p.cpart), false, false, p.B, p.D, s));
   return BCMT_OK;
 }
 

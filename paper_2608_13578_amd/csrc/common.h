@@ -86,6 +86,21 @@ __device__ __forceinline__ f32x4 load4f(const bf16* p) {
   return r;
 }
 
+// The gate G = sigmoid(U), kept for the backward pass, is stored as fp16
+// when the layer runs in bf16: the same two bytes, eight times finer
+// steps on (0, 1).  Its block sums of dY * G feed the memory's and the
+// decay's gradients, which cancel heavily.
+typedef _Float16 f16;
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+template <typename T> struct GateT { typedef T type; };
+template <> struct GateT<bf16> { typedef f16 type; };
+__device__ __forceinline__ float to_f32(f16 x) { return (float)x; }
+__device__ __forceinline__ void store4(f16* p, float a, float b, float c, float d) {
+  f16x4 v = {(f16)a, (f16)b, (f16)c, (f16)d};
+  *reinterpret_cast<f16x4*>(p) = v;
+}
+
 // Wave-wide reductions over all 64 lanes.
 // Wave-wide sum / max, returned to every lane; the whole wave must be
 // active.  Within each row of 16 lanes, DPP moves (xor 1 and xor 2 inside
@@ -177,6 +192,12 @@ __device__ __forceinline__ void st8(bf16* p, const float (&v)[8]) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
   *reinterpret_cast<bf16x8*>(p) = o;
+}
+__device__ __forceinline__ void st8(f16* p, const float (&v)[8]) {
+  f16x8 o;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o[k] = (f16)v[k];
+  *reinterpret_cast<f16x8*>(p) = o;
 }
 __device__ __forceinline__ void st8(float* p, const float (&v)[8]) {
   *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};

@@ -475,7 +475,7 @@ struct EpiGate {
       y[r] = h[r] + g[r] * c[r] + x[r];
     }
     store4(reinterpret_cast<T*>(e.Y) + off, y[0], y[1], y[2], y[3]);
-    store4(reinterpret_cast<T*>(e.G) + off, g[0], g[1], g[2], g[3]);
+    store4(reinterpret_cast<typename GateT<T>::type*>(e.G) + off, g[0], g[1], g[2], g[3]);
   }
   __device__ __forceinline__ void apply8(int m, int n, const float (&u)[8], bool ok) const {
     if (!ok) return;
@@ -505,7 +505,7 @@ struct EpiGate {
       y[k] = h[k] + g[k] * c[k];
     }
     st8(reinterpret_cast<T*>(e.Y) + off, y);
-    st8(reinterpret_cast<T*>(e.G) + off, g);
+    st8(reinterpret_cast<typename GateT<T>::type*>(e.G) + off, g);
   }
 };
 

@@ -191,22 +191,26 @@ hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, flo
                    hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 // With Pc (a chunk after earlier blocks) block 0 uses Mc = Pc[b] and its
-// sum of dY * G goes to Pbar_c [B, D] (compute type).
+// sum of dY * G goes to Pbar_c [B, D] (compute type).  In bf16 each block sum
+// v is written as hi = bf16(v) to Pbar and lo = bf16(v - hi) to Pbar_lo (and
+// Pbar_c_lo), when those are not null; float32 ignores them.
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
-                    void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                    const float* Pc, void* Pbar_c, hipStream_t s);
-// Memory backward: dM = Pbar Wm^T, then the reverse decayed scan: dS and
-// the decay gradient (atomically added to *dgamma when given).  For long
-// sequences (see mem_fwd) dM goes through `dM` ([B*nb, D] float32) and a
-// split-K product using `part`; both may be null for short ones.
-hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
-                   float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
-                   const Carry& c, hipStream_t s);
+                    void* Pbar, void* Pbar_lo, float* zero_a, int na, float* zero_b, int B, int T,
+                    int D, int L, const float* Pc, void* Pbar_c, void* Pbar_c_lo, hipStream_t s);
+// Memory backward: dM = (Pbar + Pbar_lo) Wm^T (Pbar_lo may be null; float32
+// ignores it), then the reverse decayed scan: dS and the decay gradient
+// (atomically added to *dgamma when given).  For long sequences (see
+// mem_fwd) dM goes through `dM` ([B*nb, D] float32) and a split-K product
+// using `part`; both may be null for short ones.
+hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
+                   const float* M, float* dS, float* dgamma, float* dM, float* part, int B, int nb,
+                   int D, float gamma, const Carry& c, hipStream_t s);
 // Chunked execution.  carry_prep copies the incoming state (Nu [B, D],
 // Zu [B]; both null: empty history) to Nin / Zin and writes its memory
 // Mct = Nin / Zin (0 where Zin = 0) in the compute type; with no incoming
 // state it also zeroes Pc.  carry_proj: Pc = Mct Wm, or with `transposed`
-// dMc = Pbar_c Wm^T, both [B, D] float32, using `part`
+// dMc = Pbar_c Wm^T, both [B, D] float32 (added into `out` with
+// `accumulate`), using `part`
 // (carry_part_bytes bytes).  carry_finish forms the incoming state's
 // gradients from dMc, dS of block 0 and e0:
 //   dNin = dMc / Zin + g dS_0,  dZin = sum_cols (g e0 - dMc . M_in / Zin),
@@ -216,7 +220,7 @@ hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, fl
                       void* Mct, float* Pc, int B, int D, bool zcol, hipStream_t s);
 size_t carry_part_bytes(int B, int D);
 hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
-                      bool transposed, int B, int D, hipStream_t s);
+                      bool transposed, bool accumulate, int B, int D, hipStream_t s);
 hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
                         const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
                         int D, float gamma, const float* gvec, bool zcol, hipStream_t s);

@@ -194,7 +194,8 @@ constexpr int kMsCols = 32, kMsRows = 16, kMsWaves = 8, kMsGroup = 4;
 // fragments before multiplying them, so that the loads overlap.
 template <typename T, bool FWD>
 __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
-    const T* __restrict__ A, const T* __restrict__ Wm, const float* __restrict__ S,
+    const T* __restrict__ A, const T* __restrict__ Alo, const T* __restrict__ Wm,
+    const float* __restrict__ S,
     float* __restrict__ M, T* __restrict__ Mt, float* __restrict__ P, const float* __restrict__ Min,
     float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, int kcr,
     Carry cr) {
@@ -226,7 +227,8 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     const int rt = FWD ? q : nt - 1 - q;
     const int i0 = rt * kMsRows;
     const int arow = i0 + lr;
-    const T* ap = A + ((int64_t)b * nb + (arow < nb ? arow : 0)) * D;
+    const int64_t arow_off = ((int64_t)b * nb + (arow < nb ? arow : 0)) * D;
+    const T* ap = A + arow_off;
     f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     for (int kc = 0; kc < D; kc += (FWD ? kcr : D)) {
       const int kn = FWD ? min(kcr, D - kc) : D;
@@ -267,6 +269,21 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
         for (int u = 0; u < kMsGroup; ++u)
 #pragma unroll
           for (int ntl = 0; ntl < 2; ++ntl) acc[ntl] = mma16(bfr[u][ntl], af[u], acc[ntl]);
+        if constexpr (!FWD) {
+          // the low part of a hi + lo operand pair, against the same W_m fragments
+          if (Alo) {
+#pragma unroll
+            for (int u = 0; u < kMsGroup; ++u) {
+              const int ks = g0 + u * kMsWaves;
+              af[u] = (ks < nks && arow < nb) ? load_frag(Alo + arow_off + kc + ks * 32 + lg * 8)
+                                              : F{};
+            }
+#pragma unroll
+            for (int u = 0; u < kMsGroup; ++u)
+#pragma unroll
+              for (int ntl = 0; ntl < 2; ++ntl) acc[ntl] = mma16(bfr[u][ntl], af[u], acc[ntl]);
+          }
+        }
       }
     }
     // lane holds row i0 + lr, columns 16 ntl + 4 lg + r of this wave's sum
@@ -542,16 +559,20 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
 // Pbar_c[b].
 template <typename T>
 __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
-                                                       const T* __restrict__ G,
+                                                       const typename GateT<T>::type* __restrict__ G,
                                                        const float* __restrict__ P,
                                                        T* __restrict__ dU, T* __restrict__ Pbar,
                                                        float* __restrict__ zero_a, int na,
                                                        float* __restrict__ zero_b, int Tn, int D,
                                                        int L, int nb,
                                                        const float* __restrict__ Pc,
-                                                       T* __restrict__ Pbar_c) {
+                                                       T* __restrict__ Pbar_c,
+                                                       T* __restrict__ Pbar_lo,
+                                                       T* __restrict__ Pbar_c_lo) {
   constexpr int VE = Vec16<T>::N;
   typedef typename Vec16<T>::type vec;
+  typedef typename GateT<T>::type GT;  // fp16 with bf16 activations
+  typedef GT gvec __attribute__((ext_vector_type(VE)));
   __shared__ float racc[kTg][kVec * VE];
   if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
     for (int k = threadIdx.x; k < na; k += blockDim.x)
@@ -584,13 +605,14 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
   if (act) {
     constexpr int U = 2;
     for (int t0 = bs + tg; t0 < be; t0 += U * kTg) {
-      vec dy[U], g[U];
+      vec dy[U];
+      gvec g[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = t0 + u * kTg;
         const int64_t off = ((int64_t)b * Tn + t) * D + col;
         dy[u] = t < be ? load16(dY + off) : vec{};
-        g[u] = t < be ? load16(G + off) : vec{};
+        g[u] = t < be ? *reinterpret_cast<const gvec*>(G + off) : gvec{};
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -614,8 +636,17 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     float sum = 0.f;
     for (int k = 0; k < kTg; ++k) sum += racc[k][cc];
     const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * D + c0 + cc;
-    Pbar[dst] = from_f32<T>(i > 0 ? sum : 0.f);
-    if (i == 0 && Pbar_c) Pbar_c[(int64_t)b * D + c0 + cc] = from_f32<T>(sum);
+    // The sum as a pair hi + lo of the compute type (lo only for bf16): the
+    // memory gradient takes both, the W_m weight gradient hi alone.
+    const float v = i > 0 ? sum : 0.f;
+    const T hi = from_f32<T>(v);
+    Pbar[dst] = hi;
+    if (Pbar_lo) Pbar_lo[dst] = from_f32<T>(v - to_f32(hi));
+    if (i == 0 && Pbar_c) {
+      const T hc = from_f32<T>(sum);
+      Pbar_c[(int64_t)b * D + c0 + cc] = hc;
+      if (Pbar_c_lo) Pbar_c_lo[(int64_t)b * D + c0 + cc] = from_f32<T>(sum - to_f32(hc));
+    }
   }
 }
 
@@ -931,13 +962,14 @@ hipError_t pool_bwd_t(const void* H, const float* s_in, const float* stats, cons
 
 template <typename E>
 hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, void* Pbar,
-                      float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                      const float* Pc, void* Pbar_c, hipStream_t s) {
+                      void* Pbar_lo, float* zero_a, int na, float* zero_b, int B, int T, int D,
+                      int L, const float* Pc, void* Pbar_c, void* Pbar_c_lo, hipStream_t s) {
   const int nb = (T + L - 1) / L;
   const int cw = kVec * Vec16<E>::N;
   hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
-                     (const E*)dY, (const E*)G, P, (E*)dU, (E*)Pbar, zero_a, na, zero_b, T, D, L,
-                     nb, Pc, (E*)Pbar_c);
+                     (const E*)dY, (const typename GateT<E>::type*)G, P, (E*)dU, (E*)Pbar, zero_a,
+                     na, zero_b, T, D, L,
+                     nb, Pc, (E*)Pbar_c, (E*)Pbar_lo, (E*)Pbar_c_lo);
   return hipGetLastError();
 }
 
@@ -979,31 +1011,40 @@ hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, flo
   const size_t lds = (size_t)kcr * kMsCols * es;
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, true>), grid, dim3(kMsWaves * 64), lds, s,
-                       (const bf16*)St, (const bf16*)Wm, S, M, (bf16*)Mt, P, nullptr, nullptr,
-                       nullptr, nb, D, gamma, kcr, c);
+                       (const bf16*)St, (const bf16*)nullptr, (const bf16*)Wm, S, M, (bf16*)Mt, P,
+                       nullptr, nullptr, nullptr, nb, D, gamma, kcr, c);
   else
     hipLaunchKernelGGL((memscan_kernel<float, true>), grid, dim3(kMsWaves * 64), lds, s,
-                       (const float*)St, (const float*)Wm, S, M, (float*)Mt, P, nullptr, nullptr,
-                       nullptr, nb, D, gamma, kcr, c);
+                       (const float*)St, (const float*)nullptr, (const float*)Wm, S, M,
+                       (float*)Mt, P, nullptr, nullptr, nullptr, nb, D, gamma, kcr, c);
   return hipGetLastError();
 }
 
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
-                    void* Pbar, float* zero_a, int na, float* zero_b, int B, int T, int D, int L,
-                    const float* Pc, void* Pbar_c, hipStream_t s) {
+                    void* Pbar, void* Pbar_lo, float* zero_a, int na, float* zero_b, int B, int T,
+                    int D, int L, const float* Pc, void* Pbar_c, void* Pbar_c_lo, hipStream_t s) {
   if (dt == DType::BF16)
-    return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, Pc, Pbar_c, s);
-  return gate_bwd_t<float>(dY, G, P, dU, Pbar, zero_a, na, zero_b, B, T, D, L, Pc, Pbar_c, s);
+    return gate_bwd_t<bf16>(dY, G, P, dU, Pbar, Pbar_lo, zero_a, na, zero_b, B, T, D, L, Pc,
+                            Pbar_c, Pbar_c_lo, s);
+  return gate_bwd_t<float>(dY, G, P, dU, Pbar, nullptr, zero_a, na, zero_b, B, T, D, L, Pc,
+                           Pbar_c, nullptr, s);
 }
 
-hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, float* dS,
-                   float* dgamma, float* dM, float* part, int B, int nb, int D, float gamma,
-                   const Carry& c, hipStream_t s) {
+hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
+                   const float* M, float* dS, float* dgamma, float* dM, float* part, int B, int nb,
+                   int D, float gamma, const Carry& c, hipStream_t s) {
+  if (dt != DType::BF16) Pbar_lo = nullptr;
   if (!mem_fused(nb, c.gvec != nullptr)) {
-    // dM = dP W_m^T as a matrix product, then the reverse scans.
+    // dM = dP W_m^T as a matrix product (dP = hi + lo: two products), then
+    // the reverse scans.
     GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     hipError_t e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, false, kMemMinK, s);
     if (e != hipSuccess) return e;
+    if (Pbar_lo) {
+      g.A = Pbar_lo;
+      e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, true, kMemMinK, s);
+      if (e != hipSuccess) return e;
+    }
     const dim3 grid((D + kScCols - 1) / kScCols, B);
     if (dt == DType::BF16)
       hipLaunchKernelGGL(scan_bwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, dM, M, dS,
@@ -1016,12 +1057,12 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Wm, const float* M, f
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
-                       (const bf16*)Pbar, (const bf16*)Wm, nullptr, nullptr, nullptr, nullptr, M,
-                       dS, dgamma, nb, D, gamma, 0, c);
+                       (const bf16*)Pbar, (const bf16*)Pbar_lo, (const bf16*)Wm, nullptr, nullptr,
+                       nullptr, nullptr, M, dS, dgamma, nb, D, gamma, 0, c);
   else
     hipLaunchKernelGGL((memscan_kernel<float, false>), grid, dim3(kMsWaves * 64), 0, s,
-                       (const float*)Pbar, (const float*)Wm, nullptr, nullptr, nullptr, nullptr, M,
-                       dS, dgamma, nb, D, gamma, 0, c);
+                       (const float*)Pbar, (const float*)nullptr, (const float*)Wm, nullptr,
+                       nullptr, nullptr, nullptr, M, dS, dgamma, nb, D, gamma, 0, c);
   return hipGetLastError();
 }
 
@@ -1039,10 +1080,10 @@ hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, fl
 size_t carry_part_bytes(int B, int D) { return gemm_splitk_partial_bytes(B, D, D, kMemMinK); }
 
 hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
-                      bool transposed, int B, int D, hipStream_t s) {
+                      bool transposed, bool accumulate, int B, int D, hipStream_t s) {
   // B(k, n) = Wm[k, n] (Pc = Mct Wm) or Wm[n, k] (dMc = Pbar_c Wm^T).
   GemmDesc g{B, D, D, A, D, false, {Wm, nullptr, nullptr}, D, !transposed, kSegNone, 0, 1};
-  return gemm_splitk(dt, g, part, out, nullptr, nullptr, D, D, false, kMemMinK, s);
+  return gemm_splitk(dt, g, part, out, nullptr, nullptr, D, D, accumulate, kMemMinK, s);
 }
 
 hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,

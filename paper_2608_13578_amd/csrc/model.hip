@@ -479,9 +479,11 @@ int bcmt_model_cast(const bcmt_model_config* cfg, const float* params, void* par
 int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
                           const int32_t* targets, float* params, void* params_bf16,
                           float* grads, float* adam_m, float* adam_v, const bcmt_adamw* opt,
-                          float* loss, void* ws, size_t ws_bytes, void* stream) {
+                          float* loss, void* ws, size_t ws_bytes, void* stream,
+                          const bcmt_side* side) {
   const int st = check_model(cfg);
   if (st != BCMT_OK) return st;
+  if (side && (!side->fork || !side->join)) return BCMT_ERR_INVALID;
   if (!tokens || !targets || !params || !params_bf16 || !grads || !loss || !ws)
     return BCMT_ERR_INVALID;
   if (opt && (!adam_m || !adam_v || opt->step < 1)) return BCMT_ERR_INVALID;
@@ -647,7 +649,7 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
     lg.dWg = gw(lidx(l, 7));
     lg.dwp = gw(lidx(l, 8));
     int e = bcmt_layer_backward(&p.lc, W + p.a + act * l, &lp, W + p.saved + p.layer_saved * l,
-                                dr, W + p.dxm, &lg, W + p.lws, p.layer_ws, s);
+                                dr, W + p.dxm, &lg, W + p.lws, p.layer_ws, s, side);
     if (e != BCMT_OK) return e;
     CHK(ln_bwd((const bf16*)(W + p.dxm), R(2 * l), st1m(l), lidx(l, 0), dr, dr));
   }

@@ -25,14 +25,31 @@ def to_host64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+class SideStream:
+    """A caller-owned second stream (default priority) and the two events the
+    backward passes use to fork work onto it and join it back (bcmt_side)."""
+
+    def __init__(self, device="cuda"):
+        self.stream = torch.cuda.Stream(device=device)
+        self.fork = torch.cuda.Event()
+        self.join = torch.cuda.Event()
+        # torch creates an event's HIP handle on its first record
+        for e in (self.fork, self.join):
+            e.record(self.stream)
+        self.stream.synchronize()
+
+
 class LayerBuffers:
     """Holds a config, device weights and the scratch buffers of one layer."""
 
     def __init__(self, B, T, D, H, L, gamma=0.8, dtype="bf16", residual=False,
-                 accumulate=False, device="cuda"):
+                 accumulate=False, device="cuda", side=True):
         """gamma: the decay, or one decay per channel ([D] array: sets
-        BCMT_FLAG_CHANNEL_DECAY; its values go to the device as gamma_ch)."""
+        BCMT_FLAG_CHANNEL_DECAY; its values go to the device as gamma_ch).
+        side: run the backward's weight-gradient products on a second stream
+        (True: one made here; a SideStream; or None for one stream)."""
         self.dtype = dtype
+        self.side = SideStream(device) if side is True else side
         self.device = device
         self.gamma_ch = None
         if np.ndim(gamma) > 0:
@@ -75,7 +92,7 @@ class LayerBuffers:
 
     def backward(self, X, dY, dX, grads, stream=None):
         abi.bcmt_layer_backward(self.cfg, X, self.params, self.saved, dY, dX, grads, self.ws_bwd,
-                                stream=stream)
+                                stream=stream, side=self.side)
 
     def new_carry(self):
         """A zeroed memory state (N [B, D], Z [B] or [B, D] with a per-channel
@@ -91,7 +108,8 @@ class LayerBuffers:
 
     def backward_chunk(self, X, dY, dcarry_out, dX, dcarry_in, grads, stream=None):
         abi.bcmt_layer_backward_chunk(self.cfg, X, self.params, self.saved, dY, dcarry_out, dX,
-                                      dcarry_in, grads, self.ws_bwd, stream=stream)
+                                      dcarry_in, grads, self.ws_bwd, stream=stream,
+                                      side=self.side)
 
 
 class DecodeBuffers:

@@ -15,7 +15,9 @@ class ModelBuffers:
     """Flat float32 master parameters, their bf16 copy, gradients, AdamW
     moments, the loss and the workspace for one model configuration."""
 
-    def __init__(self, V, d, H, n_layer, B, T, L, gamma=0.8, device="cuda"):
+    def __init__(self, V, d, H, n_layer, B, T, L, gamma=0.8, device="cuda", side=True):
+        from .layer import SideStream
+        self.side = SideStream(device) if side is True else side
         self.cfg = abi.make_model_config(V, d, H, n_layer, B, T, L, gamma)
         self.n = abi.bcmt_model_param_count(self.cfg)
         if self.n == 0:
@@ -65,4 +67,5 @@ class ModelBuffers:
                                opt.get("eps", 1e-8), opt.get("weight_decay", 0.01),
                                self.step_count)
         abi.bcmt_model_train_step(self.cfg, tokens, targets, self.params, self.params_bf16,
-                                  self.grads, self.m, self.v, o, self.loss, self.ws, self.ws_bytes)
+                                  self.grads, self.m, self.v, o, self.loss, self.ws, self.ws_bytes,
+                                  side=self.side)

@@ -142,13 +142,13 @@ def test_forward_argument_errors(lib):
 
 
 def _bwd(cfg, X=A, saved=A + 0x20000000, dY=A + 0x30000000, dX=A + 0x38000000, grads=None,
-         ws=A + 0x40000000, ws_bytes=None, params=None):
+         ws=A + 0x40000000, ws_bytes=None, params=None, side=None):
     if ws_bytes is None:
         ws_bytes = abi.bcmt_workspace_bytes(cfg, abi.BCMT_PASS_BACKWARD)
     g = grads
     return abi.lib().bcmt_layer_backward(ctypes.byref(cfg), X, ctypes.byref(params or _params()),
                                          saved, dY, dX, ctypes.byref(g) if g else None, ws,
-                                         ws_bytes, None)
+                                         ws_bytes, None, ctypes.byref(side) if side else None)
 
 
 def test_backward_argument_errors(lib):
@@ -166,6 +166,26 @@ def test_backward_argument_errors(lib):
     assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dgamma misaligned
     g = abi.bcmt_grads(*([A + 0x50000008] + [None] * 7))
     assert _bwd(c, grads=g) == abi.BCMT_ERR_INVALID                        # dWq misaligned
+
+
+def test_backward_second_stream_arguments(lib):
+    """Without a second stream (NULL) the backward's argument checks are those
+    of the one-stream pass; a second stream needs both of its events."""
+    c = good()
+    need = abi.bcmt_workspace_bytes(c, abi.BCMT_PASS_BACKWARD)
+    for side in (None, abi.bcmt_side(0x1000, 0x2000, 0x3000)):
+        assert _bwd(c, saved=None, side=side) == abi.BCMT_ERR_INVALID
+        assert _bwd(c, ws=None, side=side) == abi.BCMT_ERR_INVALID
+        assert _bwd(c, ws_bytes=need - 256, side=side) == abi.BCMT_ERR_WORKSPACE
+        assert _bwd(good(D=96, H=1), side=side) == abi.BCMT_ERR_UNSUPPORTED
+    for side in (abi.bcmt_side(0x1000, None, 0x3000), abi.bcmt_side(0x1000, 0x2000, None),
+                 abi.bcmt_side(None, None, None)):
+        assert _bwd(c, side=side) == abi.BCMT_ERR_INVALID
+    # the model step passes the same structure to its layers
+    mc = abi.make_model_config(V=1000, d=128, H=8, n_layer=1, B=2, T=64, L=32)
+    st = lib.bcmt_model_train_step(ctypes.byref(mc), 16, 16, 16, 16, 16, None, None, None, 16, 16,
+                                   1 << 40, None, ctypes.byref(abi.bcmt_side(16, None, 16)))
+    assert st == abi.BCMT_ERR_INVALID
 
 
 def _carry(N, Z):
@@ -190,7 +210,7 @@ def test_chunk_argument_errors(lib):
         return lib.bcmt_layer_backward_chunk(
             ctypes.byref(c), A, ctypes.byref(p), saved, A + 0x30000000,
             ctypes.byref(dout) if dout else None, A + 0x38000000,
-            ctypes.byref(din) if din else None, None, A + 0x40000000, ws_b, None)
+            ctypes.byref(din) if din else None, None, A + 0x40000000, ws_b, None, None)
 
     for bad in (_carry(None, A + 0x71000000), _carry(A + 0x70000000, None),
                 _carry(A + 0x70000008, A + 0x71000000), _carry(A + 0x70000000, A + 0x71000002)):
@@ -289,5 +309,5 @@ def test_model_layout_and_argument_errors(lib):
     for i in range(2):  # null tokens / workspace: rejected on the host
         st = lib.bcmt_model_train_step(ctypes.byref(c), None if i == 0 else 16, 16, 16, 16, 16,
                                        None, None, None, 16, None if i == 1 else 16, 1 << 40,
-                                       None)
+                                       None, None)
         assert st == abi.BCMT_ERR_INVALID

@@ -14,7 +14,7 @@ float32.
 import numpy as np
 import pytest
 
-from test_gpu_parity import GRADS, TOL, compare, inputs, say, torch_cuda  # noqa: F401
+from test_gpu_parity import GRADS, compare, inputs, say, torch_cuda  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
@@ -103,7 +103,7 @@ def oracle_chunks(B, cuts, D, H, L, X, W, dY, gamma=0.8, residual=False, carry0=
     return out
 
 
-def compare_chunks(gpu, ref, dtype, label, tol=None):
+def compare_chunks(gpu, ref, dtype, label):
     """Tensors, plus each chunk's outgoing state and incoming-state gradient."""
     flat_g = {k: v for k, v in gpu.items() if k not in ("carries", "dcarries")}
     flat_r = {k: v for k, v in ref.items() if k not in ("carries", "dcarries")}
@@ -113,7 +113,7 @@ def compare_chunks(gpu, ref, dtype, label, tol=None):
     for n, (cg, cr) in enumerate(zip(gpu.get("dcarries", []), ref.get("dcarries", []))):
         flat_g[f"dN_in{n}"], flat_g[f"dZ_in{n}"] = cg
         flat_r[f"dN_in{n}"], flat_r[f"dZ_in{n}"] = cr
-    compare(flat_g, flat_r, dtype, label, tol)
+    compare(flat_g, flat_r, dtype, label)
 
 
 def _state(rng, B, D, Z):

@@ -11,7 +11,7 @@ oracle's Y, max|gpu - ref| / max|ref| <= 2e-2 (bf16) or 1e-4 (float32).
 import numpy as np
 import pytest
 
-from test_gpu_parity import TOL, TOL_STRESS_BF16, compare, inputs, say, torch_cuda  # noqa: F401
+from test_gpu_parity import compare, inputs, say, torch_cuda  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
@@ -75,8 +75,7 @@ def test_decode_matches_layer(torch_cuda, case):
     X, W, _ = inputs(B, T, D, dtype, w_std=ws)
     gpu = gpu_decode(torch_cuda, B, T, D, H, L, dtype, X, W, gamma, res, prefill=pre)
     ref = oracle_y(B, T, D, H, L, X, W, gamma, res)
-    tol = TOL_STRESS_BF16 if (ws > 0.1 and dtype == "bf16") else None
-    compare({"Y": gpu}, {"Y": ref}, dtype, name, tol)
+    compare({"Y": gpu}, {"Y": ref}, dtype, f"decode-{name}")
 
 
 def test_decode_measured_shape(torch_cuda):

@@ -3,21 +3,22 @@
 The GPU model keeps activations in bf16 (the residual stream included) with
 float32 accumulation; the oracle runs in float64 on the same bf16-valued
 weights and float32 LayerNorm parameters.  Bounds: the loss to 2e-3
-absolute (about 5e-4 of log V), every gradient array to 3e-2 of its largest
-element (the layer's bf16 bound, 2e-2, widened for the bf16 residual stream
-and LayerNorm outputs that the layer tests do not have), and the AdamW
+absolute (about 5e-4 of log V), every gradient array to 2e-2 of its largest
+element (the layer's bf16 bound; for the benchmarked model, the arrays listed
+in tolerances.LM have bounds derived from the rounding model), and the AdamW
 update, which is float32 arithmetic on the same inputs, to 1e-6.
 """
 
 import numpy as np
 import pytest
 
+import tolerances as tl
 from test_gpu_parity import say, torch_cuda  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
 LOSS_TOL = 2e-3
-GRAD_TOL = 3e-2
+GRAD_TOL = 2e-2
 
 
 def oracle_params(arrs, n_layer):
@@ -53,6 +54,9 @@ CASES = [
     # the paper's vocabulary: rows of 50304 padded logits, 7 register steps
     # per thread in the loss kernel, 47 masked padding columns
     ("bcmt-vocab50257", 50257, 64, 2, 1, 1, 40, 16),
+    # the benchmarked model (d = 128, 6 layers of 8 heads of 16, L = 128,
+    # the GPT-2 vocabulary) on one sequence of 1024 tokens
+    ("bcmt-bench-shape", 50257, 128, 8, 6, 1, 1024, 128),
 ]
 
 
@@ -67,16 +71,21 @@ def test_model_parity(torch_cuda, case):
                                  oracle_params(arrs, nl), L, H, gamma)
     G = mo.flatten(mo.backward(cache))
     loss = float(mb.loss.item())
+    bounds = tl.LM["bounds"] if name == tl.LM["case"] else {}
+    if bounds:
+        s = tl.LM
+        assert (V, d, H, nl, B, T, L) == (s["V"], s["d"], s["H"], s["layers"], s["B"], s["T"],
+                                          s["L"])
     worst = []
     for nm, g, r in zip(mb.names, mb.arrays(mb.grads), G):
         g, r = np.asarray(g).reshape(-1), np.asarray(r).reshape(-1)
         err = float(np.abs(g - r).max() / max(np.abs(r).max(), 1e-30))
-        worst.append((err, nm))
+        worst.append((err / bounds.get(nm, GRAD_TOL), err, nm))
     worst.sort(reverse=True)
     say(f"[{name}] loss {loss:.6f} vs {loss_ref:.6f}; worst grads "
-        + " ".join(f"{n}={e:.2e}" for e, n in worst[:4]))
+        + " ".join(f"{n}={e:.2e}" for _, e, n in worst[:4]))
     assert abs(loss - loss_ref) <= LOSS_TOL
-    assert worst[0][0] <= GRAD_TOL, worst[:3]
+    assert worst[0][0] <= 1.0, worst[:3]
 
 
 def test_model_adamw_update(torch_cuda):
