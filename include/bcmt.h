@@ -170,6 +170,26 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
                         void* ws, size_t ws_bytes, void* stream, const bcmt_side* side);
 
+/* ---- Forward pass without allocation -------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid it.  The same forward
+ * pass as bcmt_layer_forward, with its workspace taken from a device array
+ * inside the library (BCMT_NOALLOC_SCRATCH_BYTES on each GPU, held from when
+ * the library is loaded until the process ends) instead of a caller buffer.
+ *   saved  required (bcmt_saved_bytes() bytes, caller-owned), as for a
+ *          forward that a backward pass follows; inference uses it too.
+ * Returns BCMT_ERR_WORKSPACE when the pass needs more scratch than the array
+ * holds (bcmt_workspace_bytes(cfg, BCMT_PASS_FORWARD) above
+ * BCMT_NOALLOC_SCRATCH_BYTES; the forward of B = 2, T = 65536, D = 1024 at
+ * L = 256 needs 17 MiB), and BCMT_ERR_HIP if the array's address cannot be
+ * obtained; other errors as for bcmt_layer_forward.  The call allocates
+ * nothing and creates nothing.  Every call on one GPU uses that GPU's one
+ * array: calls whose work overlaps on the GPU (several streams, or several
+ * host threads) race on it and must be ordered by the caller. */
+#define BCMT_NOALLOC_SCRATCH_BYTES (32u << 20)
+int bcmt_layer_forward_noalloc(const bcmt_config* cfg, const void* X, const bcmt_params* params,
+                               void* Y, void* saved, void* stream);
+
 /* ---- Chunked execution ---------------------------------------------------
  * Only the memory of Sec. 3.5 crosses block boundaries, through the decayed
  * recurrence over blocks; attention, pooling and the gate stay inside a

@@ -33,6 +33,7 @@ BCMT_PASS_INFERENCE = 1
 BCMT_PASS_BACKWARD = 2
 
 EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_layer_forward",
+            "bcmt_layer_forward_noalloc",
             "bcmt_layer_backward", "bcmt_layer_forward_chunk", "bcmt_layer_backward_chunk",
             "bcmt_decode_state_bytes", "bcmt_decode_workspace_bytes", "bcmt_decode_reset",
             "bcmt_decode_step", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
@@ -115,6 +116,8 @@ def lib():
         L.bcmt_layer_forward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
                                          ctypes.c_size_t, vp]
         L.bcmt_layer_forward.restype = ctypes.c_int
+        L.bcmt_layer_forward_noalloc.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp]
+        L.bcmt_layer_forward_noalloc.restype = ctypes.c_int
         sidep = ctypes.POINTER(bcmt_side)
         L.bcmt_layer_backward.argtypes = [cfgp, vp, ctypes.POINTER(bcmt_params), vp, vp, vp,
                                           ctypes.POINTER(bcmt_grads), vp, ctypes.c_size_t, vp,
@@ -263,6 +266,18 @@ def bcmt_layer_forward(cfg, X, params, Y, saved, ws, ws_bytes=None, stream=None)
                                   _ptr(Y), _ptr(saved), _ptr(ws), int(ws_bytes), _stream(stream))
     if st != BCMT_OK:
         raise BcmtError(st, "bcmt_layer_forward")
+
+
+# bytes of the library's own forward scratch (bcmt_layer_forward_noalloc)
+BCMT_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def bcmt_layer_forward_noalloc(cfg, X, params, Y, saved, stream=None):
+    st = lib().bcmt_layer_forward_noalloc(ctypes.byref(cfg), _ptr(X),
+                                          ctypes.byref(_params(params)), _ptr(Y), _ptr(saved),
+                                          _stream(stream))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_layer_forward_noalloc")
 
 
 def bcmt_layer_backward(cfg, X, params, saved, dY, dX, grads, ws, ws_bytes=None, stream=None,

@@ -734,11 +734,51 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   return BCMT_OK;
 }
 
+// ------------------------------------------------------------------ allocation-free forward
+// The forward pass's workspace for bcmt_layer_forward_noalloc: one array per
+// GPU, part of the loaded code object (each device holds its own copy until
+// the process ends).  Host code never uses this name as an address: the
+// device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[BCMT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, or null if it cannot be found.
+void* scratch_for_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch[dev] = ptr;
+  }
+  return g_scratch[dev];
+}
+}  // namespace
+
 extern "C" {
 
 int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params* prm, void* Y,
                        void* saved, void* ws, size_t ws_bytes, void* stream) {
   return layer_forward(cfg, X, prm, Y, saved, ws, ws_bytes, stream, false, nullptr, nullptr);
+}
+
+int bcmt_layer_forward_noalloc(const bcmt_config* cfg, const void* X, const bcmt_params* prm,
+                               void* Y, void* saved, void* stream) {
+  // Every check that needs no device comes first, so that a size beyond the
+  // scratch array is rejected before any HIP call.
+  const int st = check_config(cfg);
+  if (st != BCMT_OK) return st;
+  if (!saved) return BCMT_ERR_INVALID;
+  if (Plan(*cfg).fwd_bytes > (size_t)BCMT_NOALLOC_SCRATCH_BYTES) return BCMT_ERR_WORKSPACE;
+  void* ws = scratch_for_current_device();
+  if (!ws) return BCMT_ERR_HIP;
+  return layer_forward(cfg, X, prm, Y, saved, ws, (size_t)BCMT_NOALLOC_SCRATCH_BYTES, stream,
+                       false, nullptr, nullptr);
 }
 
 int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* prm,

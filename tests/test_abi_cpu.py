@@ -141,6 +141,23 @@ def test_forward_argument_errors(lib):
                                   A + 0x40000000, 1 << 30, None) == abi.BCMT_ERR_INVALID
 
 
+def test_noalloc_forward_argument_errors(lib):
+    """The allocation-free forward rejects a pass whose workspace exceeds its
+    scratch array, and a missing `saved`, before any HIP call."""
+    small = good()
+    assert abi.bcmt_workspace_bytes(small, abi.BCMT_PASS_FORWARD) <= abi.BCMT_NOALLOC_SCRATCH_BYTES
+    big = good(B=16, T=65536, D=1024, H=16, L=32)
+    assert abi.bcmt_workspace_bytes(big, abi.BCMT_PASS_FORWARD) > abi.BCMT_NOALLOC_SCRATCH_BYTES
+    p = ctypes.byref(_params())
+    f = lib.bcmt_layer_forward_noalloc
+    assert f(ctypes.byref(big), A, p, A + 0x10000000, A + 0x20000000, None) == \
+        abi.BCMT_ERR_WORKSPACE
+    assert f(ctypes.byref(small), A, p, A + 0x10000000, None, None) == abi.BCMT_ERR_INVALID
+    assert f(ctypes.byref(good(T=0)), A, p, A + 0x10000000, A + 0x20000000, None) == \
+        abi.BCMT_ERR_INVALID
+    assert f(None, A, p, A + 0x10000000, A + 0x20000000, None) == abi.BCMT_ERR_INVALID
+
+
 def _bwd(cfg, X=A, saved=A + 0x20000000, dY=A + 0x30000000, dX=A + 0x38000000, grads=None,
          ws=A + 0x40000000, ws_bytes=None, params=None, side=None):
     if ws_bytes is None:
