@@ -120,7 +120,7 @@ struct Plan {
     // bf16: the low part of each shifted context-gradient value (hi + lo)
     pbar_lo = take(dt == DType::BF16 ? BND * es : 0);
     dS = take(BND * 4);
-    dM = take(mem_fused(nb, pc) ? 0 : BND * 4);
+    dM = take(0);  // (the long path's dM stays in split-K partials)
     mpart_b = take(mem_part_bytes(B, nb, D, pc));
     a = take(BT * 4);
     ds = take(BT * 4);

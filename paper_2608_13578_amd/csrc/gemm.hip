@@ -1138,6 +1138,11 @@ hipError_t dispatch_any(const GemmDesc& g, const Epi& epi, hipStream_t s) {
 
 }  // namespace
 
+int gemm_splitk_splits(int M, int N, int K, int min_k) {
+  int kc;
+  return splitk_plan(M, N, K, min_k, &kc);
+}
+
 size_t gemm_splitk_partial_bytes(int M, int N, int K, int min_k) {
   int kc;
   const int sp = splitk_plan(M, N, K, min_k, &kc);

@@ -50,6 +50,8 @@ size_t gemm_wgrad_partial_bytes(int M, int N, int K);
 // segments), every split at least min_k deep; with a single split the
 // outputs are written directly and `partial` is unused.
 size_t gemm_splitk_partial_bytes(int M, int N, int K, int min_k);
+// The number of splits gemm_splitk chooses for that product.
+int gemm_splitk_splits(int M, int N, int K, int min_k);
 hipError_t gemm_splitk(DType dt, const GemmDesc& g, float* partial, float* C0, float* C1,
                        float* C2, int64_t ldc, int seg_len_n, bool accumulate, int min_k,
                        hipStream_t s);
@@ -179,8 +181,9 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
 // Memory forward: M (float32), Mt (compute type) and P = M Wm from S.  Up
 // to a few dozen blocks per sequence one kernel does it all (Q = St Wm with
 // St = S in the compute type, [B*nb, D], and the decayed scans of S and Q);
-// for longer sequences a parallel scan gives M and a split-K product P,
-// using `part` (mem_part_bytes bytes; may be null when that is 0).
+// for longer sequences Q is a split-K product whose partials a parallel
+// scan of S and Q adds up, using `part` (mem_part_bytes bytes; may be null
+// when that is 0).
 // The single kernel scans the projected summaries, which equals projecting
 // the scan only for one decay shared by the channels: a per-channel decay
 // takes the scan + matrix-product path at any length.

@@ -155,6 +155,116 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
   }
 }
 
+// Whole-row pooling: one workgroup per (block, batch element) over all D
+// columns, used when there are enough such pairs to fill the chip.  Thread
+// = (16-byte vector v of the row, token group tg); the block's scores are
+// formed once per workgroup (the column-chunk layout forms them once per
+// chunk) and staged in LDS with their exponentials, 1024 tokens at a time
+// with the running maximum rescaling the partial sums.  Chunks of VR
+// vectors per row and TG token groups: NT = VR * TG threads, a multiple of
+// 64 (pool_row_groups).
+constexpr int kRowTile = 1024;
+// Whole-row pooling needs at least this many (block, batch element) pairs;
+// fewer take the column-chunk layout, which deals each pair to several
+// workgroups.
+constexpr int64_t kPoolRowMinGroups = 192;
+
+template <typename T>
+__global__ __launch_bounds__(512) void pool_row_kernel(const T* __restrict__ H,
+                                                       const float* __restrict__ sp, int np,
+                                                       float* __restrict__ s_out,
+                                                       float* __restrict__ S, T* __restrict__ St,
+                                                       float* __restrict__ stats, int Tn, int D,
+                                                       int L, int nb, int TG) {
+  constexpr int VE = Vec16<T>::N;
+  constexpr int U = 8;
+  typedef typename Vec16<T>::type vec;
+  extern __shared__ float pdyn[];  // racc [TG][D], then sc [kRowTile]
+  __shared__ float red[8];
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6;
+  const int VR = D / VE;
+  const int v = tid % VR, tg = tid / VR;
+  const int i = blockIdx.x, b = blockIdx.y;
+  const int bs = i * L, be = min(bs + L, Tn);
+  float* racc = pdyn;
+  float* sc = pdyn + TG * D;
+  const T* hb = H + ((int64_t)b * Tn) * D + v * VE;
+  float m = -INFINITY, l = 0.f, acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  for (int t0 = bs; t0 < be; t0 += kRowTile) {
+    const int n = min(kRowTile, be - t0);
+    // the tile's scores (the output projection left np partial sums each)
+    float mx = -INFINITY;
+    for (int t = tid; t < n; t += nt) {
+      const int64_t row = (int64_t)b * Tn + t0 + t;
+      const float* q = sp + row * np;
+      float x = 0.f;
+      for (int k = 0; k < np; ++k) x += q[k];
+      sc[t] = x;
+      s_out[row] = x;
+      mx = fmaxf(mx, x);
+    }
+    mx = wave_max(mx);
+    if ((tid & 63) == 0) red[tid >> 6] = mx;
+    __syncthreads();
+    float mn = m;
+    for (int w = 0; w < nw; ++w) mn = fmaxf(mn, red[w]);
+    __syncthreads();
+    float ls = 0.f;
+    for (int t = tid; t < n; t += nt) {
+      const float e = __expf(sc[t] - mn);
+      sc[t] = e;
+      ls += e;
+    }
+    ls = wave_sum(ls);
+    if ((tid & 63) == 0) red[tid >> 6] = ls;
+    __syncthreads();
+    float lt = 0.f;
+    for (int w = 0; w < nw; ++w) lt += red[w];
+    const float f = __expf(m - mn);
+    l = l * f + lt;
+    m = mn;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) acc[e] *= f;
+    if (tg < TG) {
+      for (int k0 = tg; k0 < n; k0 += U * TG) {
+        vec h[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = k0 + u * TG;
+          h[u] = k < n ? load16(hb + (int64_t)(t0 + k) * D) : vec{};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = k0 + u * TG;
+          const float w = k < n ? sc[k] : 0.f;
+#pragma unroll
+          for (int e = 0; e < VE; ++e) acc[e] += w * to_f32(h[u][e]);
+        }
+      }
+    }
+    __syncthreads();  // sc[] and red[] are rewritten by the next tile
+  }
+  if (tg < TG) {
+#pragma unroll
+    for (int e = 0; e < VE; ++e) racc[tg * D + v * VE + e] = acc[e];
+  }
+  __syncthreads();
+  const float inv = 1.0f / l;
+  const int64_t brow = (int64_t)(b * nb + i);
+  for (int c = tid; c < D; c += nt) {
+    float sum = 0.f;
+    for (int k = 0; k < TG; ++k) sum += racc[k * D + c];
+    S[brow * D + c] = sum * inv;
+    St[brow * D + c] = from_f32<T>(sum * inv);
+  }
+  if (tid == 0) {
+    stats[brow * 2] = m;
+    stats[brow * 2 + 1] = l;
+  }
+}
+
 // ------------------------------------------------------------------ memory projection + scan
 // Each workgroup owns 32 columns of one sequence and walks its N_b blocks in
 // row tiles of 16: a small matrix product gives the tile's 16 x 32 outputs
@@ -358,20 +468,23 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
 }
 
 // ------------------------------------------------------------------ long scans
-// For many blocks the memory path runs as two pieces: the decayed scans
-// below (parallel over blocks) and the W_m products as ordinary matrix
-// products (memscan_kernel walks all blocks of a sequence inside one
+// For many blocks the memory path runs as two pieces: the W_m products as
+// ordinary split-K matrix products, and the decayed scans below, parallel
+// over blocks (memscan_kernel walks all blocks of a sequence inside one
 // workgroup, which serialises a long sequence).
 //
-// Workgroup = (16 columns, sequence), thread = (column, chunk of 16
-// blocks), 16 chunks per pass of 256 blocks.  Each thread scans its chunk
-// with a zero carry, the chunk ends meet in LDS, each thread folds the
-// chunks before (after, for the reverse scan) into its carry, and applies
-// it: with the recurrence x_i = g x_{i-1} + y_i, the true value is the local
-// one plus g^(distance) times the carry.  A pass hands its end carry to the
-// next one; the first pass starts from the state of the earlier blocks
+// A scan runs as two launches over the same grid: workgroup = (64
+// columns, sequence, chunk of kScChunkRows blocks), four waves of 16 blocks
+// each, one column per lane (256-byte rows of float32).  The first launch
+// (LOCAL) scans each chunk from a zero carry and writes the chunk's
+// aggregate per column; the second (APPLY) folds the aggregates of the
+// chunks before it (after it, for the reverse scan) into its carry, scans
+// its chunk again from that carry and writes the results.  Within a chunk
+// the four waves meet in LDS the same way.  With the recurrence
+// x_i = g x_{i-1} + y_i, a value is its local one plus g^(distance) times
+// the carry.  The first chunk starts from the state of the earlier blocks
 // (zero for a whole sequence).
-constexpr int kScCols = 16, kScChunks = 16, kScRows = 16;
+constexpr int kScCols = 64, kScWaves = 4, kScRows = 16, kScChunkRows = kScWaves * kScRows;
 // Up to this many blocks per sequence the fused kernel runs; beyond it, the
 // scans above plus split-K matrix products (each split at least kMemMinK deep).
 constexpr int kMemFusedMaxBlocks = 32, kMemMinK = 256;
@@ -381,132 +494,245 @@ __device__ __forceinline__ float pow16(float g) {
   return g8 * g8;
 }
 
-// M = N / Z with N_i = g N_{i-1} + S_i (float32 and compute type).
-template <typename T>
-__global__ __launch_bounds__(kScCols * kScChunks) void scan_fwd_kernel(
+int scan_chunks(int nb) { return (nb + kScChunkRows - 1) / kScChunkRows; }
+
+// Forward: M = N / Z with N_i = g N_{i-1} + S_i (float32 and compute type).
+// With Qp (one decay for all channels) also the projected summaries
+// Q = S W_m, given as nq split-K partial products (stride qstride, added in
+// order): NP_i = g NP_{i-1} + Q_i and P = NP / Z = M W_m.  aggN / aggP hold
+// the chunk aggregates, [B, nch, D].
+template <typename T, bool APPLY>
+__global__ __launch_bounds__(kScCols * kScWaves) void scan_fwd_kernel(
     const float* __restrict__ S, float* __restrict__ M, T* __restrict__ Mt, int nb, int D,
-    float gamma, Carry cr) {
-  __shared__ float agg[kScChunks][kScCols];
-  const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
+    float gamma, Carry cr, const float* __restrict__ Qp, int nq, int64_t qstride,
+    float* __restrict__ P, float* __restrict__ aggN, float* __restrict__ aggP) {
+  __shared__ float wn[kScWaves][kScCols], wp[kScWaves][kScCols];
+  const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
-  const int b = blockIdx.y;
+  const int b = blockIdx.y, ch = blockIdx.z, nch = gridDim.z;
   const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
-  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
   const float g16 = pow16(gam);
-  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
-  float carry = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;  // N just before this pass
-  for (int p0 = 0; p0 < nb; p0 += kScChunks * kScRows) {
-    const int a = p0 + k * kScRows;
-    float v[kScRows];
+  const int a = ch * kScChunkRows + w * kScRows;  // this wave's first block
+  float v[kScRows], q[kScRows];
+  const int64_t off0 = ((int64_t)b * nb + a) * D + col;
 #pragma unroll
-    for (int r = 0; r < kScRows; ++r) {
-      const int i = a + r;
-      v[r] = on && i < nb ? S[((int64_t)b * nb + i) * D + col] : 0.f;
-    }
-    float n = 0.f;
+  for (int r = 0; r < kScRows; ++r) {
+    v[r] = on && a + r < nb ? S[off0 + (int64_t)r * D] : 0.f;
+    q[r] = 0.f;
+  }
+  // the partial products one slice at a time, every row's load in flight
+  for (int z = 0; Qp && z < nq; ++z) {
+    float t[kScRows];
 #pragma unroll
-    for (int r = 0; r < kScRows; ++r) {
-      n = gam * n + v[r];
-      v[r] = n;
+    for (int r = 0; r < kScRows; ++r)
+      t[r] = on && a + r < nb ? Qp[z * qstride + off0 + (int64_t)r * D] : 0.f;
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) q[r] += t[r];
+  }
+  if constexpr (!APPLY) {
+    // the summed products replace the first slice: the second pass reads one
+    if (Qp && nq > 1) {
+#pragma unroll
+      for (int r = 0; r < kScRows; ++r)
+        if (on && a + r < nb) const_cast<float*>(Qp)[off0 + (int64_t)r * D] = q[r];
     }
-    agg[k][c] = n;
-    __syncthreads();
-    float cin = carry, cout = carry;
-    for (int j = 0; j < kScChunks; ++j) {
-      if (j == k) cin = cout;
-      cout = g16 * cout + agg[j][c];
+  }
+  float n = 0.f, np = 0.f;
+#pragma unroll
+  for (int r = 0; r < kScRows; ++r) {
+    n = gam * n + v[r];
+    np = gam * np + q[r];
+    v[r] = n;
+    q[r] = np;
+  }
+  wn[w][c] = n;
+  wp[w][c] = np;
+  __syncthreads();
+  const int64_t arow = ((int64_t)b * nch + ch) * D + col;
+  if constexpr (!APPLY) {
+    if (w == 0 && on) {
+      float an = 0.f, ap = 0.f;
+      for (int j = 0; j < kScWaves; ++j) {
+        an = g16 * an + wn[j][c];
+        ap = g16 * ap + wp[j][c];
+      }
+      aggN[arow] = an;
+      aggP[arow] = ap;
+    }
+    return;
+  } else {
+    const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+    const float zin = !cr.Zin ? 0.f
+                      : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
+    // the state before this chunk: the earlier blocks', then every chunk before
+    float cn = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;
+    float cp = on && Qp && cr.Nin ? cr.Pc[(int64_t)b * D + col] * zin : 0.f;
+    const float g64 = g16 * g16 * g16 * g16;
+    for (int j0 = 0; j0 < ch && on; j0 += 8) {  // eight chunks' loads at a time
+      float tn[8], tp[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t ar = ((int64_t)b * nch + j0 + u) * D + col;
+        tn[u] = j0 + u < ch ? aggN[ar] : 0.f;
+        tp[u] = j0 + u < ch ? aggP[ar] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (j0 + u < ch) {
+          cn = g64 * cn + tn[u];
+          cp = g64 * cp + tp[u];
+        }
+      }
+    }
+    for (int j = 0; j < w; ++j) {  // then the waves before this one
+      cn = g16 * cn + wn[j][c];
+      cp = g16 * cp + wp[j][c];
     }
     float f = gam;
 #pragma unroll
     for (int r = 0; r < kScRows; ++r) {
       const int i = a + r;
       if (on && i < nb) {
-        const float n = v[r] + f * cin;
-        const float m = n / zsum(i, gam, lg2, zin);
-        const int64_t off = ((int64_t)b * nb + i) * D + col;
+        const float nn = v[r] + f * cn;
+        const float rz = 1.f / zsum(i, gam, lg2, zin);
+        const float m = nn * rz;
+        const int64_t off = off0 + (int64_t)r * D;
         M[off] = m;
         Mt[off] = from_f32<T>(m);
-        if (i == nb - 1 && cr.Nout) cr.Nout[(int64_t)b * D + col] = n;
+        if (Qp) P[off] = (q[r] + f * cp) * rz;
+        if (i == nb - 1 && cr.Nout) cr.Nout[(int64_t)b * D + col] = nn;
       }
       f *= gam;
     }
-    carry = cout;
-    __syncthreads();  // agg[] is rewritten by the next pass
-  }
-  if (cr.Zout) {
-    if (cr.zcol) {
-      if (on && k == 0) cr.Zout[(int64_t)b * D + col] = zsum(nb - 1, gam, lg2, zin);
-    } else if (blockIdx.x == 0 && threadIdx.x == 0) {
-      cr.Zout[b] = zsum(nb - 1, gam, lg2, zin);
+    if (cr.Zout && ch == 0 && w == 0) {
+      if (cr.zcol) {
+        if (on) cr.Zout[(int64_t)b * D + col] = zsum(nb - 1, gam, lg2, zin);
+      } else if (blockIdx.x == 0 && c == 0) {
+        cr.Zout[b] = zsum(nb - 1, gam, lg2, zin);
+      }
     }
   }
 }
 
-// Reverse scans of the memory backward from dM (float32), M:
+// Reverse scans of the memory backward from dM (nq split-K partial products,
+// stride qstride, added in order) and M:
 //   Qs_i = dM_i / Z_i + g Qs_{i+1} (= dS_i),  E_i = -dM_i . M_i / Z_i + g E_{i+1},
 //   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one atomic add per workgroup).
 // The gradients of a chunk's final state enter at the last block; E of the
-// first block goes to cr.e0.
-template <typename T>
-__global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
-    const float* __restrict__ dM, const float* __restrict__ M, float* __restrict__ dS,
-    float* __restrict__ dgamma, int nb, int D, float gamma, Carry cr) {
-  __shared__ float aq[kScChunks][kScCols], ae[kScChunks][kScCols];
-  __shared__ float red[kScCols * kScChunks / 64];
-  const int c = threadIdx.x % kScCols, k = threadIdx.x / kScCols;
+// first block goes to cr.e0.  aggQ / aggE: the chunk aggregates (each
+// chunk's values at its first block, from a zero carry).
+template <typename T, bool APPLY>
+__global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
+    const float* __restrict__ dM, int nq, int64_t qstride, const float* __restrict__ M,
+    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, Carry cr,
+    float* __restrict__ aggQ, float* __restrict__ aggE) {
+  __shared__ float wq[kScWaves][kScCols], we[kScWaves][kScCols];
+  __shared__ float red[kScWaves];
+  const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
-  const int b = blockIdx.y;
+  const int b = blockIdx.y, ch = blockIdx.z, nch = gridDim.z;
   const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
   const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
   const float g16 = pow16(gam);
-  constexpr int PASS = kScChunks * kScRows;
-  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
-  float cq = 0.f, ce = 0.f;  // Qs and E just after this pass
-  float dg = 0.f;
-  for (int p0 = (nb - 1) / PASS * PASS; p0 >= 0; p0 -= PASS) {
-    const int a = p0 + k * kScRows;
-    float x[kScRows], y[kScRows], mprev[kScRows];
+  const float zin = !cr.Zin ? 0.f
+                    : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
+  const int a = ch * kScChunkRows + w * kScRows;
+  const int64_t off0 = ((int64_t)b * nb + a) * D + col;
+  float x[kScRows], y[kScRows];
 #pragma unroll
-    for (int r = 0; r < kScRows; ++r) {
-      const int i = a + r;
-      const bool ok = on && i < nb;
-      const int64_t off = ((int64_t)b * nb + i) * D + col;
-      const float dm = ok ? dM[off] : 0.f;
-      const float m = ok ? M[off] : 0.f;
-      const float z = zsum(i, gam, lg2, zin);
-      x[r] = dm / z;
-      y[r] = -dm * m / z;
-      if (ok && i == nb - 1) {
-        if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
-        if (cr.dZout) {
-          if (cr.zcol) y[r] += cr.dZout[(int64_t)b * D + col];
-          else if (col == 0) y[r] += cr.dZout[b];
+  for (int r = 0; r < kScRows; ++r) x[r] = 0.f;
+  for (int z = 0; z < nq; ++z) {
+    float t[kScRows];
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r)
+      t[r] = on && a + r < nb ? dM[z * qstride + off0 + (int64_t)r * D] : 0.f;
+#pragma unroll
+    for (int r = 0; r < kScRows; ++r) x[r] += t[r];
+  }
+  if constexpr (!APPLY) {
+    // the summed products replace the first slice: the second pass reads one
+    if (nq > 1) {
+#pragma unroll
+      for (int r = 0; r < kScRows; ++r)
+        if (on && a + r < nb) const_cast<float*>(dM)[off0 + (int64_t)r * D] = x[r];
+    }
+  }
+  float mm[kScRows];
+#pragma unroll
+  for (int r = 0; r < kScRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
+#pragma unroll
+  for (int r = 0; r < kScRows; ++r) {
+    const int i = a + r;
+    const bool ok = on && i < nb;
+    const float m = mm[r];
+    const float rz = 1.f / zsum(i, gam, lg2, zin);
+    const float dm = x[r];
+    x[r] = dm * rz;
+    y[r] = -dm * m * rz;
+    if (ok && i == nb - 1) {
+      if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
+      if (cr.dZout) {
+        if (cr.zcol) y[r] += cr.dZout[(int64_t)b * D + col];
+        else if (col == 0) y[r] += cr.dZout[b];
+      }
+    }
+  }
+  float qq = 0.f, e = 0.f;
+#pragma unroll
+  for (int r = kScRows - 1; r >= 0; --r) {
+    qq = x[r] + gam * qq;
+    e = y[r] + gam * e;
+    x[r] = qq;
+    y[r] = e;
+  }
+  wq[w][c] = qq;
+  we[w][c] = e;
+  __syncthreads();
+  const int64_t arow = ((int64_t)b * nch + ch) * D + col;
+  if constexpr (!APPLY) {
+    if (w == 0 && on) {
+      float aq = 0.f, ae = 0.f;
+      for (int j = kScWaves - 1; j >= 0; --j) {
+        aq = wq[j][c] + g16 * aq;
+        ae = we[j][c] + g16 * ae;
+      }
+      aggQ[arow] = aq;
+      aggE[arow] = ae;
+    }
+    return;
+  } else {
+    // the carry entering this wave's last block: every later chunk (the
+    // last one may be short), then the later waves of this chunk
+    float iq = 0.f, ie = 0.f;
+    const float g64 = g16 * g16 * g16 * g16;
+    for (int j0 = nch - 1; j0 > ch && on; j0 -= 8) {  // eight chunks' loads at a time
+      float tq[8], te[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 - u;
+        const int64_t ar = ((int64_t)b * nch + j) * D + col;
+        tq[u] = j > ch ? aggQ[ar] : 0.f;
+        te[u] = j > ch ? aggE[ar] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 - u;
+        if (j > ch) {
+          // the last chunk may be short: g^(its length)
+          const int len = min(kScChunkRows, nb - j * kScChunkRows);
+          const float gl = len == kScChunkRows ? g64 : powf(gam, (float)len);
+          iq = tq[u] + gl * iq;
+          ie = te[u] + gl * ie;
         }
       }
-      mprev[r] = ok && i >= 1 ? M[off - D] : 0.f;
     }
-    float q = 0.f, e = 0.f;
-#pragma unroll
-    for (int r = kScRows - 1; r >= 0; --r) {
-      q = x[r] + gam * q;
-      e = y[r] + gam * e;
-      x[r] = q;
-      y[r] = e;
+    for (int j = kScWaves - 1; j > w; --j) {
+      iq = wq[j][c] + g16 * iq;
+      ie = we[j][c] + g16 * ie;
     }
-    aq[k][c] = q;
-    ae[k][c] = e;
-    __syncthreads();
-    float iq = cq, ie = ce, oq = cq, oe = ce;
-    for (int j = kScChunks - 1; j >= 0; --j) {
-      if (j == k) {
-        iq = oq;
-        ie = oe;
-      }
-      oq = aq[j][c] + g16 * oq;
-      oe = ae[j][c] + g16 * oe;
-    }
+    float dg = 0.f;
     float f = gam;
 #pragma unroll
     for (int r = kScRows - 1; r >= 0; --r) {
@@ -514,36 +740,35 @@ __global__ __launch_bounds__(kScCols * kScChunks) void scan_bwd_kernel(
       const float qs = x[r] + f * iq, es = y[r] + f * ie;
       f *= gam;
       if (on && i < nb) {
-        dS[((int64_t)b * nb + i) * D + col] = qs;
+        dS[off0 + (int64_t)r * D] = qs;
         if (i >= 1) {
           const float zp = zsum(i - 1, gam, lg2, zin);
-          dg += qs * (mprev[r] * zp) + es * zp;
+          const float mp = r > 0 ? mm[r > 0 ? r - 1 : 0] : M[off0 - D];
+          dg += qs * (mp * zp) + es * zp;
         } else if (cr.e0) {
           cr.e0[(int64_t)b * D + col] = es;
         }
       }
     }
-    cq = oq;
-    ce = oe;
-    __syncthreads();  // aq[] / ae[] are rewritten by the next pass
-  }
-  if (cr.gvec) {  // per-channel decay gradient: the column's chunks meet in LDS
-    aq[k][c] = dg;
-    __syncthreads();
-    if (k == 0 && on && dgamma) {
-      float t = 0.f;
-      for (int j = 0; j < kScChunks; ++j) t += aq[j][c];
-      unsafeAtomicAdd(dgamma + col, t);
+    if (cr.gvec) {  // per-channel decay gradient: the column's waves meet in LDS
+      __syncthreads();
+      wq[w][c] = dg;
+      __syncthreads();
+      if (w == 0 && on && dgamma) {
+        float t = 0.f;
+        for (int j = 0; j < kScWaves; ++j) t += wq[j][c];
+        unsafeAtomicAdd(dgamma + col, t);
+      }
+      return;
     }
-    return;
-  }
-  const float v = wave_sum(dg);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  if (threadIdx.x == 0 && dgamma) {
-    float t = 0.f;
-    for (int w = 0; w < kScCols * kScChunks / 64; ++w) t += red[w];
-    unsafeAtomicAdd(dgamma, t);
+    const float v = wave_sum(dg);
+    if (c == 0) red[w] = v;
+    __syncthreads();
+    if (threadIdx.x == 0 && dgamma) {
+      float t = 0.f;
+      for (int j = 0; j < kScWaves; ++j) t += red[j];
+      unsafeAtomicAdd(dgamma, t);
+    }
   }
 }
 
@@ -921,6 +1146,17 @@ template <typename E>
 hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, float* S, void* St,
                       float* stats, int B, int T, int D, int L, hipStream_t s) {
   const int nb = (T + L - 1) / L;
+  if ((int64_t)B * nb >= kPoolRowMinGroups) {
+    // whole rows: VR vectors per row, TG token groups, VR * TG threads a
+    // multiple of 64 and at least 256 (or VR itself when larger)
+    const int VR = D / Vec16<E>::N;
+    int TG = VR >= 256 ? 1 : (256 + VR - 1) / VR;
+    while ((VR * TG) % 64) ++TG;
+    const size_t lds = ((size_t)TG * D + kRowTile) * sizeof(float);
+    hipLaunchKernelGGL(pool_row_kernel<E>, dim3(nb, B), dim3(VR * TG), lds, s, (const E*)H, sp, np,
+                       s_out, S, (E*)St, stats, T, D, L, nb, TG);
+    return hipGetLastError();
+  }
   const int cw = kVec * Vec16<E>::N;
   hipLaunchKernelGGL(pool_fwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
                      (const E*)H, sp, np, s_out, S, (E*)St, stats, T, D, L, nb);
@@ -983,23 +1219,72 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
 
 bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !per_channel; }
 
+// The long path's W_m products keep their split-K partial products (one
+// slice per split, a single slice when there is one split) for the scans,
+// which add them in a fixed order: the forward's Q = St W_m, and the
+// backward's dM = Pbar Wm^T and Pbar_lo Wm^T (twice the slices).
 size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
-  return mem_fused(nb, per_channel) ? 0 : gemm_splitk_partial_bytes(B * nb, D, D, kMemMinK);
+  if (mem_fused(nb, per_channel)) return 0;
+  const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
+  // the partial slices, then the scans' two aggregate arrays [B, nch, D]
+  return (2 * (size_t)sp * B * nb + 2 * (size_t)B * scan_chunks(nb)) * D * sizeof(float);
+}
+
+// The two passes of a long scan over grid (columns / 64, B, chunks).
+template <typename T>
+hipError_t scan_fwd_run(const float* S, float* M, T* Mt, int B, int nb, int D, float gamma,
+                        const Carry& c, const float* Qp, int nq, float* P, float* agg,
+                        hipStream_t s) {
+  const int nch = scan_chunks(nb);
+  const dim3 grid((D + kScCols - 1) / kScCols, B, nch);
+  const int64_t qs = (int64_t)B * nb * D, as = (int64_t)B * nch * D;
+  hipLaunchKernelGGL((scan_fwd_kernel<T, false>), grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt,
+                     nb, D, gamma, c, Qp, nq, qs, P, agg, agg + as);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((scan_fwd_kernel<T, true>), grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt,
+                     nb, D, gamma, c, Qp, nq > 1 ? 1 : nq, qs, P, agg, agg + as);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t scan_bwd_run(const float* dM, int nq, const float* M, float* dS, float* dgamma, int B,
+                        int nb, int D, float gamma, const Carry& c, float* agg, hipStream_t s) {
+  const int nch = scan_chunks(nb);
+  const dim3 grid((D + kScCols - 1) / kScCols, B, nch);
+  const int64_t qs = (int64_t)B * nb * D, as = (int64_t)B * nch * D;
+  hipLaunchKernelGGL((scan_bwd_kernel<T, false>), grid, dim3(kScCols * kScWaves), 0, s, dM, nq, qs,
+                     M, dS, dgamma, nb, D, gamma, c, agg, agg + as);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((scan_bwd_kernel<T, true>), grid, dim3(kScCols * kScWaves), 0, s, dM,
+                     nq > 1 ? 1 : nq, qs, M, dS, dgamma, nb, D, gamma, c, agg, agg + as);
+  return hipGetLastError();
 }
 
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s) {
   if (!mem_fused(nb, c.gvec != nullptr)) {
-    // M from the scan, then P = M W_m as a matrix product.
-    const dim3 grid((D + kScCols - 1) / kScCols, B);
-    if (dt == DType::BF16)
-      hipLaunchKernelGGL(scan_fwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
-                         (bf16*)Mt, nb, D, gamma, c);
-    else
-      hipLaunchKernelGGL(scan_fwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, S, M,
-                         (float*)Mt, nb, D, gamma, c);
-    hipError_t e = hipGetLastError();
+    const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
+    float* agg = part + 2 * (int64_t)sp * B * nb * D;
+    if (!c.gvec) {
+      // Q = St W_m as split-K partial products, then one scan of S and Q
+      // gives M and P = M W_m (the decayed sum is linear).
+      GemmDesc g{B * nb, D, D, St, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+      int nq = 0;
+      hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false,
+                                         kMemMinK, &nq, s);
+      if (e != hipSuccess) return e;
+      if (dt == DType::BF16)
+        return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, part, nq, P, agg, s);
+      return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, part, nq, P, agg, s);
+    }
+    // One decay per channel: W_m mixes channels, so the scan of S comes
+    // first and P = M W_m is a matrix product of the memory.
+    hipError_t e = dt == DType::BF16
+        ? scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, nullptr, 0, nullptr, agg, s)
+        : scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, nullptr, 0, nullptr, agg, s);
     if (e != hipSuccess) return e;
     GemmDesc g{B * nb, D, D, Mt, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
     return gemm_splitk(dt, g, part, P, nullptr, nullptr, D, D, false, kMemMinK, s);
@@ -1034,25 +1319,27 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* 
                    const float* M, float* dS, float* dgamma, float* dM, float* part, int B, int nb,
                    int D, float gamma, const Carry& c, hipStream_t s) {
   if (dt != DType::BF16) Pbar_lo = nullptr;
+  (void)dM;
   if (!mem_fused(nb, c.gvec != nullptr)) {
-    // dM = dP W_m^T as a matrix product (dP = hi + lo: two products), then
-    // the reverse scans.
+    // dM = dP W_m^T as split-K partial products (dP = hi + lo: two
+    // products, their slices one after the other), added up by the reverse
+    // scans.
+    const int64_t qs = (int64_t)B * nb * D;
     GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
-    hipError_t e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, false, kMemMinK, s);
+    int sp = 0, sp2 = 0;
+    hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK,
+                                       &sp, s);
     if (e != hipSuccess) return e;
     if (Pbar_lo) {
       g.A = Pbar_lo;
-      e = gemm_splitk(dt, g, part, dM, nullptr, nullptr, D, D, true, kMemMinK, s);
+      float* lo = part + sp * qs;
+      e = gemm_splitk_product(dt, g, lo, lo, nullptr, nullptr, D, D, false, kMemMinK, &sp2, s);
       if (e != hipSuccess) return e;
     }
-    const dim3 grid((D + kScCols - 1) / kScCols, B);
+    float* agg = part + 2 * (int64_t)gemm_splitk_splits(B * nb, D, D, kMemMinK) * qs;
     if (dt == DType::BF16)
-      hipLaunchKernelGGL(scan_bwd_kernel<bf16>, grid, dim3(kScCols * kScChunks), 0, s, dM, M, dS,
-                         dgamma, nb, D, gamma, c);
-    else
-      hipLaunchKernelGGL(scan_bwd_kernel<float>, grid, dim3(kScCols * kScChunks), 0, s, dM, M,
-                         dS, dgamma, nb, D, gamma, c);
-    return hipGetLastError();
+      return scan_bwd_run<bf16>(part, sp + sp2, M, dS, dgamma, B, nb, D, gamma, c, agg, s);
+    return scan_bwd_run<float>(part, sp + sp2, M, dS, dgamma, B, nb, D, gamma, c, agg, s);
   }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)

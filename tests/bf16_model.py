@@ -14,9 +14,9 @@ The points where a value is rounded (``POINTS``):
   o     the attention output, stored; its row sums with dO give delta;
   h     the output projection H (Sec. 3.3), stored; pooling reads it;
   st    the block summaries as the operand of the W_m product (the memory
-        path of at most 32 blocks projects S and scans the projections);
+        path projects S and scans the projections);
   mt    the memory M as the operand of the W_m weight gradient (and of the
-        W_m product on the longer-sequence path);
+        W_m product of an incoming state's memory);
   g     the gate, stored for the backward pass in fp16 (the output uses it
         unrounded);
   y     the layer output (Sec. 3.8), stored;
@@ -58,9 +58,6 @@ POINTS = ("qkv", "pfwd", "o", "h", "st", "mt", "g", "y", "du", "pb", "dh", "do",
 FP16_POINTS = ("g",)
 # with the language model around the layer (lm_bf16_model): its own tensors
 ALL_POINTS = POINTS + ("lm",)
-# The memory path projects the summaries and scans the projections when a
-# sequence has at most this many blocks, else it scans S and projects M.
-FUSED_MAX_BLOCKS = 32
 
 
 def rounder(points=ALL_POINTS, jitter=0.0, seed=0):
@@ -105,8 +102,8 @@ def forward(X, W, L, h, gamma, rnd, residual=False, carry=None):
     """The layer with bf16 rounding at the GPU path's points; (Y, cache).
 
     ``carry`` = (N_in, Z_in): X is a chunk after earlier blocks, as in the
-    oracle (only for more than FUSED_MAX_BLOCKS blocks, where the GPU
-    projects the rounded memory, the incoming one included)."""
+    oracle; the incoming memory N_in / Z_in is projected from its bf16
+    value, and the chunk's projections continue the decayed sum from it."""
     X = np.asarray(X, dtype=np.float64)
     B, T, D = X.shape
     nb = orc.n_blocks(T, L)
@@ -132,23 +129,21 @@ def forward(X, W, L, h, gamma, rnd, residual=False, carry=None):
         a[:, b0:b1] = orc.softmax_last(s[:, b0:b1])
         S[:, i] = np.einsum("bt,btd->bd", a[:, b0:b1], Hl[:, b0:b1])
     extra = {}
+    Qm = rnd("st", S) @ W["Wm"]  # the projected summaries, scanned like S
     if carry is not None:
-        if nb <= FUSED_MAX_BLOCKS:
-            raise NotImplementedError("a carried state on the short memory path")
         N_in, Z_in = (np.asarray(a, dtype=np.float64) for a in carry)
         M, Nacc, Zacc = orc.exp_memory_carry(S, gamma, N_in, Z_in)
         Mext = np.concatenate([orc.carry_memory(N_in, Z_in)[:, None], M], axis=1)
         Mt = rnd("mt", Mext)
-        C = (Mt @ W["Wm"])[:, :-1]
+        Pc = Mt[:, 0] @ W["Wm"]
+        P = orc.exp_memory_carry(Qm, gamma, Pc * Z_in[:, None], Z_in)[0]
+        C = np.concatenate([Pc[:, None], P[:, :-1]], axis=1)
         extra = dict(N_in=N_in, Z_in=Z_in, Mext=Mext, Nacc=Nacc, Zacc=Zacc)
     else:
         Aw = orc.memory_weights(nb, gamma)[0]
         M = np.einsum("ij,bjd->bid", Aw, S)
         Mt = rnd("mt", M)
-        if nb <= FUSED_MAX_BLOCKS:
-            P = np.einsum("ij,bjd->bid", Aw, rnd("st", S) @ W["Wm"])
-        else:
-            P = Mt @ W["Wm"]
+        P = np.einsum("ij,bjd->bid", Aw, Qm)
         C = np.zeros_like(P)
         C[:, 1:] = P[:, :-1]
     G = orc.sigmoid(Hl @ W["Wg"])

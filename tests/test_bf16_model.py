@@ -47,9 +47,8 @@ def _model(X, W, L, H, gamma, dY, rnd, residual=False):
 
 @pytest.mark.parametrize("L,residual", [(20, True), (16, False), (130, False)])
 def test_model_without_rounding_is_the_oracle(L, residual):
-    """No rounding point active: the oracle's outputs and gradients, on the
-    memory path of at most 32 blocks (L=20, 16 blocks), the longer one
-    (L=16: 40 blocks) and a single block (L=130)."""
+    """No rounding point active: the oracle's outputs and gradients, with 7
+    blocks (L=20), 40 blocks (L=16) and a single block (L=130)."""
     X, W, dY = _case(2, 130 if L != 16 else 640, 64, 0.3)
     H = 4
     ref = _exact(X, W, L, H, 0.8, dY, residual)
@@ -74,11 +73,6 @@ def test_each_rounding_point_reaches_its_outputs():
         want = fwd_only.get(p) or bwd.get(p)
         if want is not None:
             assert moved <= want | {"Y"} and (moved & want), (p, moved)
-    # the longer memory path projects the rounded memory, not the summaries
-    X, W, dY = _case(1, 640, 64, 0.3)
-    ref = _exact(X, W, 16, 4, 0.8, dY)
-    got = _model(X, W, 16, 4, 0.8, dY, bm.rounder(points=("st",)))
-    assert all(_err(got[k], ref[k]) < 1e-12 for k in ref)
 
 
 @pytest.mark.parametrize("case", list(tl.DERIVED))
@@ -227,3 +221,21 @@ def test_lm_bounds_follow_from_the_model():
         assert b >= tl.MARGIN * e, (k, e, b)
         if k in s["bounds"]:
             assert b <= 2 * tl.MARGIN * e, (k, e, b)
+
+
+def test_model_with_carry_without_rounding_is_the_oracle():
+    """The chunked form (an incoming memory state) of the model, with no
+    rounding, is the oracle's chunk."""
+    X, W, dY = _case(2, 640, 64, 0.3)
+    rng = np.random.default_rng(5)
+    Z = np.array([3.0, 1.5])
+    N = Z[:, None] * rng.standard_normal((2, 64)) * 0.5
+    Y, c = orc.forward(X, W, 16, 4, 0.8, carry=(N, Z))
+    ref = orc.backward(c, dY)
+    ref["Y"] = Y
+    none = bm.rounder(points=())
+    Ym, cm = bm.forward(X, W, 16, 4, 0.8, none, carry=(N, Z))
+    got = bm.backward(cm, dY, none)
+    got["Y"] = Ym
+    for k in ref:
+        assert _err(np.asarray(got[k]), np.asarray(ref[k])) < 1e-12, k

@@ -71,25 +71,21 @@ def test_channel_decay_parity(torch_cuda, case):
     compare({k: gpu[k] for k in ref}, ref, dtype, name)
 
 
-@pytest.mark.parametrize("dtype,T,L,exact", [("bf16", 1024, 128, False), ("f32", 1200, 16, True)])
-def test_equal_channels_are_the_single_decay(torch_cuda, dtype, T, L, exact):
-    """Every channel at 0.8 gives the scalar-decay layer.  With more than 32
-    blocks both take the parallel scans and the same arithmetic: outputs and
-    weight gradients agree bit for bit.  With fewer, the scalar decay takes
-    the single-kernel path (which scans the projected summaries) and the
-    per-channel decay the scan + product path, so they agree to rounding.
-    The per-channel decay gradients add up to the scalar one."""
+@pytest.mark.parametrize("dtype,T,L", [("bf16", 1024, 128), ("f32", 1200, 16)])
+def test_equal_channels_are_the_single_decay(torch_cuda, dtype, T, L):
+    """Every channel at 0.8 gives the scalar-decay layer.  The scalar decay
+    scans the projected summaries (S W_m); a per-channel decay scans S and
+    then projects the memory (W_m mixes channels, so only one decay lets the
+    two orders agree), so the two agree to rounding, on the single-kernel
+    path (8 blocks) and on the parallel scans (75 blocks).  The per-channel
+    decay gradients add up to the scalar one."""
     B, D, H = 2, 128, 2
     X, W, dY = inputs(B, T, D, dtype, w_std=0.05)
     a = run_gpu(torch_cuda, B, T, D, H, L, dtype, X, W, dY, 0.8)
     b = run_gpu(torch_cuda, B, T, D, H, L, dtype, X, W, dY, np.full(D, 0.8, np.float32))
     keys = ("Y", "dX") + tuple(k for k in GRADS if k != "dgamma")
-    if exact:
-        for k in keys:
-            assert np.array_equal(a[k], b[k]), k
-    else:
-        compare({k: b[k] for k in keys}, {k: a[k] for k in keys}, dtype, "equal-channels")
-    tol = 1e-4 if exact else 2e-2
+    compare({k: b[k] for k in keys}, {k: a[k] for k in keys}, dtype, "equal-channels")
+    tol = 1e-4 if dtype == "f32" else 2e-2
     assert abs(b["dgamma_ch"].sum() - a["dgamma"]) <= tol * abs(a["dgamma"])
 
 

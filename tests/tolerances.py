@@ -38,7 +38,7 @@ DERIVED = {
     "bf16-dh16-stress-L200": (1, 450, 64, 4, 200, 2 / 64 ** 0.5, 0.8, False, {
         "Y": 0.038, "dX": 0.073, "dWq": 0.082, "dWk": 0.094, "dWv": 0.064, "dWo": 0.079,
         "dWm": 0.067, "dWg": 0.051, "dwp": 0.063, "dgamma": 0.054}),
-    "bf16-many-blocks-L16-g0.9": (2, 2550, 256, 4, 16, 0.02, 0.9, False, {"dgamma": 0.049}),
+    "bf16-many-blocks-L16-g0.9": (2, 2550, 256, 4, 16, 0.02, 0.9, False, {"dgamma": 0.04}),
 }
 
 # Full-size launches checked on sampled sequences (test_gpu_full_size): the
