@@ -71,8 +71,8 @@ def stage_work(name, B, T, D, H, L, es):
         # write M (both types) and P
         "fwd.memory_scan": B * nb * D * (4 + es + 4 + es + 4) + D * D * es,
         "bwd.gate": 3 * act + B * nb * D * (4 + es),
-        # read dP (compute type), W_m and M, write dS
-        "bwd.memory_scan": B * nb * D * (es + 4 + 4) + D * D * es,
+        # read dP (bf16: a hi + lo pair), W_m and M, write dS
+        "bwd.memory_scan": B * nb * D * ((2 * es if es == 2 else es) + 4 + 4) + D * D * es,
         # read H, s, dS and S; write a, ds and the dw_p partial rows
         "bwd.pool": act + BT * 12 + B * nb * D * 8 + pool_rows * D * 4,
         "bwd.pool_dwp": pool_rows * D * 4,
@@ -151,7 +151,32 @@ def cpu_baseline(seconds_target=12.0):
     return {"value": round(reps * bs * w["T"] / t, 1), "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{reps} x {bs} of the {w['B']} sequences (T={w['T']}, D={w['D']}, "
-                      f"H={w['H']}, L={w['L']}), float64 forward+backward, {t:.1f} s"}
+                      f"H={w['H']}, L={w['L']}), float64 forward+backward, {t:.1f} s",
+            "host": host_info()}
+
+
+def host_info():
+    """The host the oracle ran on: logical CPUs, this process's affinity,
+    CPU model and the BLAS NumPy calls (vendor, version, threads)."""
+    info = {"cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            info["blas"] = {"vendor": blas[0].get("internal_api"),
+                            "version": blas[0].get("version"),
+                            "threads": blas[0].get("num_threads")}
+    except Exception:
+        pass
+    return info
 
 
 # Long-context shape for the bandwidth-bound kernels: at the measured layer
@@ -331,6 +356,10 @@ def model_bench(torch, abi, steps=20, warmup=20, only=None):
     def run(T, L):
         if (T, L) in cache:
             return cache[(T, L)]
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
         mb = ModelBuffers(m["V"], m["d"], m["H"], m["layers"], m["B"], T, L, m["gamma"])
         p = torch.randn(mb.n, device="cuda") * 0.02
         for name, (off, cnt) in zip(mb.names, mb.layout):
@@ -339,6 +368,7 @@ def model_bench(torch, abi, steps=20, warmup=20, only=None):
             elif name.endswith("_b"):
                 p[off:off + cnt] = 0.0
         mb.params.copy_(p)
+        del p
         abi.bcmt_model_cast(mb.cfg, mb.params, mb.params_bf16)
         tok = torch.from_numpy(rng.integers(0, m["V"], (m["B"], T)).astype(np.int32)).cuda()
         tgt = torch.roll(tok, -1, 1).contiguous()
@@ -346,16 +376,20 @@ def model_bench(torch, abi, steps=20, warmup=20, only=None):
         for _ in range(warmup):
             mb.step(tok, tgt, opt)
         torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
         e0.record()
         for _ in range(steps):
             mb.step(tok, tgt, opt)
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
-        mem = mb.ws_bytes + mb.n * (4 * 4 + 2)
+        # peak device memory of the step, measured: every buffer of the model
+        # (workspace, parameters, gradients, moments, tokens) is a torch
+        # allocation, and the step allocates nothing of its own
+        peak = torch.cuda.max_memory_allocated() - base
         r = {"ms_per_step": round(ms, 3), "tokens_per_s": round(m["B"] * T / (ms / 1e3), 1),
-             "device_bytes": int(mem)}
-        del mb, p, tok, tgt
+             "device_bytes": int(peak)}
+        del mb, tok, tgt
         torch.cuda.empty_cache()
         cache[(T, L)] = r
         return r
@@ -441,6 +475,150 @@ def decode_bench(torch, abi, dt, g, blocks=2, warmup_blocks=1):
             "weight_GB/s": round(wbytes / (us * 1e-6) / 1e9, 1), "stage_us": per}
 
 
+def timed(torch, step, steps, warmup):
+    """ms per call of step() over `steps` calls after `warmup` untimed ones."""
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+# The block-size sweep of the benchmark configurations (B = 16, T = 1024,
+# D = 768, 12 heads); L = T is one block, the dense causal baseline.
+SWEEP = {"B": 16, "T": 1024, "D": 768, "H": 12, "Ls": [32, 64, 128, 256, 1024], "gamma": 0.8}
+
+
+def block_size_sweep(make_step, torch, steps=50, warmup=50):
+    g = SWEEP
+    B, T, D, H = g["B"], g["T"], g["D"], g["H"]
+    out = {"workload": f"bcmt-layer fwd+bwd B={B} T={T} D={D} H={H}x64 bf16", "by_L": {}}
+    for L in g["Ls"]:
+        step, keep = make_step(B, T, D, H, L, g["gamma"])
+        ms = timed(torch, step, steps, warmup)
+        fl = 3 * layer_flops(B, T, D, H, L)
+        out["by_L"][str(L)] = {"us_per_step": round(ms * 1e3, 1),
+                               "tokens_per_s": round(B * T / (ms / 1e3), 1),
+                               "mfma_frac": round(fl / (ms / 1e3) / 1e12 / PEAK["mfma_bf16_tflops"], 4)}
+        print(f"block-size sweep L={L:5d}: {ms * 1e3:8.1f} us per step, "
+              f"{B * T / (ms / 1e3) / 1e6:6.2f} M tokens/s", file=sys.stderr)
+        del step, keep
+    dense = out["by_L"][str(T)]["tokens_per_s"]
+    for r in out["by_L"].values():
+        r["vs_dense"] = round(r["tokens_per_s"] / dense, 3)
+    return out
+
+
+def long_t_sweep(make_step, torch, Ts=(4096, 16384, 65536), steps=8, warmup=3):
+    """The long-context shape at growing T: time per step and tokens/s, and
+    the time per token relative to the shortest T (1.0 = linear in T)."""
+    g = LONG
+    B, D, H, L = g["B"], g["D"], g["H"], g["L"]
+    out = {"workload": f"bcmt-layer fwd+bwd B={B} D={D} H={H}x64 L={L} bf16", "by_T": {}}
+    base = None
+    for T in Ts:
+        step, keep = make_step(B, T, D, H, L, g["gamma"])
+        ms = timed(torch, step, steps, warmup)
+        per_tok = ms / (B * T)
+        base = base or per_tok
+        out["by_T"][str(T)] = {"ms_per_step": round(ms, 3),
+                               "tokens_per_s": round(B * T / (ms / 1e3), 1),
+                               "time_per_token_vs_T4096": round(per_tok / base, 3)}
+        print(f"long context T={T:6d}: {ms:7.3f} ms per step, "
+              f"{B * T / (ms / 1e3) / 1e6:6.2f} M tokens/s", file=sys.stderr)
+        del step, keep
+        torch.cuda.empty_cache()
+    return out
+
+
+def stack_bench(torch, steps=10, warmup=5, layers=12):
+    """Forward then backward through a stack of residual BCMT layers at the
+    measured shape: stack time and tokens/s per layer (layers * B * T / t)."""
+    from paper_2608_13578_amd.inputs import make_layer_inputs, make_upstream_grad
+    from paper_2608_13578_amd.layer import LayerBuffers, SideStream, to_device
+    w = WORKLOAD
+    B, T, D, H, L = w["B"], w["T"], w["D"], w["H"], w["L"]
+    X, Ws = make_layer_inputs(B, T, D, seed=0, bf16=True, n_layers=layers)
+    dY = make_upstream_grad(B, T, D, seed=1, bf16=True)
+    side = SideStream()
+    lbs = []
+    for W in Ws:
+        lb = LayerBuffers(B, T, D, H, L, gamma=w["gamma"], dtype="bf16", residual=True,
+                          side=side)
+        lb.set_params(W)
+        lbs.append(lb)
+    xs = [to_device(X, "bf16")] + [lbs[0].new_activation() for _ in range(layers)]
+    dys = [to_device(dY, "bf16")] + [lbs[0].new_activation() for _ in range(layers)]
+    grads = [lb.new_grads() for lb in lbs]
+
+    def step():
+        for i, lb in enumerate(lbs):
+            lb.forward(xs[i], xs[i + 1])
+        for i in reversed(range(layers)):
+            j = layers - 1 - i
+            lbs[i].backward(xs[i], dys[j], dys[j + 1], grads[i])
+    ms = timed(torch, step, steps, warmup)
+    print(f"{layers}-layer stack: {ms:.3f} ms per step, "
+          f"{layers * B * T / (ms / 1e3) / 1e6:.2f} M layer-tokens/s", file=sys.stderr)
+    return {"workload": f"{layers} residual bcmt-layers fwd+bwd B={B} T={T} D={D} H={H}x64 L={L} bf16",
+            "ms_per_step": round(ms, 3), "tokens_per_s_per_layer": round(layers * B * T / (ms / 1e3), 1),
+            "tokens_per_s": round(B * T / (ms / 1e3), 1)}
+
+
+# The memory path's stress shape: B = 16 sequences of 65536 tokens in
+# blocks of 32 (2048 blocks each), D = 1024 (the long-context width).
+STRESS = {"B": 16, "T": 65536, "D": 1024, "H": 16, "L": 32, "gamma": 0.8}
+
+
+def stress_shape(make_step, torch, abi, steps=2, warmup=1):
+    """Per-stage times of the bandwidth-bound memory stages at the stress
+    shape (every stage alone on one stream), with bytes moved per launch
+    against the HBM peak."""
+    g = STRESS
+    B, T, D, H, L = g["B"], g["T"], g["D"], g["H"], g["L"]
+    step, keep = make_step(B, T, D, H, L, g["gamma"])
+    timed(torch, step, 1, warmup)
+    abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    stages = abi.bcmt_trace_read()
+    abi.bcmt_trace_enable(False)
+    res = {}
+    for name, calls, total in stages:
+        if not any(k in name for k in ("pool", "memory_scan", "bwd.gate")):
+            continue
+        bound, amount, unit = stage_work(name, B, T, D, H, L, 2)
+        avg_s = total / calls / 1e3
+        gbs = amount / avg_s / 1e9
+        res[name] = {"us": round(avg_s * 1e6, 1), "bytes": amount, "GB/s": round(gbs, 1),
+                     "frac": round(gbs / PEAK["hbm_gbs"], 3)}
+        print(f"stress {name:22s} {avg_s * 1e6:9.1f} us {gbs:8.1f} GB/s", file=sys.stderr)
+    del step, keep
+    torch.cuda.empty_cache()
+    return {"workload": f"bcmt-layer memory stages B={B} T={T} D={D} L={L} ({T // L} blocks) bf16",
+            "hbm_stages": res}
+
+
+def event_overhead_ms(torch, n=200):
+    """Interval of an empty pair of timing events on one stream (what the
+    stage tracer adds to each launch it brackets)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for a, b in evs:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) for a, b in evs)
+    return t[len(t) // 2]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -458,6 +636,9 @@ def main():
                     help="skip the language-model pass (paper-shape training step)")
     ap.add_argument("--no-paper-shape", action="store_true",
                     help="skip the pass at the paper's model width (D=128, 16-dim heads)")
+    ap.add_argument("--no-sweeps", action="store_true",
+                    help="skip the block-size sweep (B=16), the long-context T sweep, the "
+                         "12-layer stack and the memory path's stress shape")
     ap.add_argument("--profile-model", action="store_true",
                     help="for rocprofv3: only the language-model training step at T=1024, "
                          "L=128 (--warmup untimed steps, then --steps)")
@@ -537,6 +718,13 @@ def main():
         return step, (runs, grads)
 
     step, keep = make_step(B, T, D, H, L, w["gamma"])
+    # The GPU's clocks settle after some tens of milliseconds of load: steps
+    # for 0.25 s of wall time first, then the requested warm-up steps.
+    t_end = time.time() + 0.25
+    while time.time() < t_end:
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -594,6 +782,11 @@ def main():
     dom = max(rows, key=lambda r: r[3])
     name, per, avg_ms, per_step, bound, amount, rate = dom
     traffic = stored_traffic(name)
+    # The tracer's two events bracket each launch; an empty pair of events
+    # takes `ovh` on its own, which the kernel's duration excludes.
+    ovh = event_overhead_ms(torch)
+    kern_ms = max(avg_ms - ovh, 1e-6)
+    rate = amount / (kern_ms / 1e3)
     if bound == "mfma":
         peak = PEAK["mfma_bf16_tflops"] if dt == "bf16" else PEAK["mfma_f32_tflops"]
         roof = {"bound": "mfma", "kernel": name, "achieved": round(rate / 1e12, 2), "peak": peak,
@@ -602,7 +795,9 @@ def main():
         roof = {"bound": "hbm", "kernel": name, "achieved": round(rate / 1e9, 1),
                 "peak": PEAK["hbm_gbs"], "unit": "GB/s",
                 "frac": round(rate / 1e9 / PEAK["hbm_gbs"], 4), "traffic": traffic}
-    roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
+    roof["avg_launch_us"] = round(kern_ms * 1e3, 2)
+    roof["timing"] = (f"per-launch HIP events on the launch stream, {avg_ms * 1e3:.2f} us, "
+                      f"minus the {ovh * 1e3:.2f} us of an empty event pair")
     roof["work_per_launch"] = amount
     fl = 3 * layer_flops(B, T, D, H, L)
 
@@ -616,10 +811,18 @@ def main():
         "layer_mfma_frac": round(fl / (ms / 1e3) / 1e12 / PEAK["mfma_bf16_tflops"], 4),
         "roofline": roof,
     }
-    if not args.no_long_context:
-        del keep, step
+    del keep, step
+    torch.cuda.empty_cache()
+    if not args.no_sweeps:
+        out["block_size_sweep"] = block_size_sweep(make_step, torch)
+        out["stack"] = stack_bench(torch)
         torch.cuda.empty_cache()
+    if not args.no_long_context:
         out["long_context"] = long_context(make_step, torch, abi, dt, make_chunked=make_chunked)
+        torch.cuda.empty_cache()
+    if not args.no_sweeps:
+        out["long_context_T"] = long_t_sweep(make_step, torch)
+        out["stress_shape"] = stress_shape(make_step, torch, abi)
     if not args.no_decode:
         out["decode"] = [decode_bench(torch, abi, dt, g) for g in DECODE]
     if not args.no_paper_shape:
