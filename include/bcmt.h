@@ -128,6 +128,22 @@ typedef struct {
   void* join;   /* hipEvent_t, recorded on side->stream at the end */
 } bcmt_side;
 
+/* Optional helper: creates side->fork and side->join (side->stream is not
+ * touched) on the calling thread's current device, with no timing and no
+ * system-scope fence on record.  The fork and join only order two streams
+ * of one device and the host never waits on them; an event recorded with
+ * the default system-scope release writes back and invalidates the GPU's
+ * caches between the kernels around it, which costs the critical path
+ * several microseconds per record.  The caller owns the events and frees
+ * them with bcmt_side_events_destroy.  Returns BCMT_OK, BCMT_ERR_INVALID
+ * (side NULL) or BCMT_ERR_HIP (then nothing stays allocated and both
+ * members are NULL). */
+int bcmt_side_events_create(bcmt_side* side);
+
+/* Destroys side->fork and side->join (NULL members are skipped) and sets
+ * them to NULL.  The events must no longer be in use by enqueued work. */
+int bcmt_side_events_destroy(bcmt_side* side);
+
 /* Host-only check of a configuration; returns BCMT_OK or a negative status.
  * Makes no HIP call. */
 int bcmt_validate(const bcmt_config* cfg);
@@ -286,8 +302,8 @@ int bcmt_decode_step(const bcmt_config* cfg, const bcmt_params* params, int64_t 
 /* Static description of a status code. */
 const char* bcmt_strerror(int status);
 
-/* Library version, major * 10000 + minor * 100 + patch (2.0.0: the backward
- * passes take a caller-owned second stream). */
+/* Library version, major * 10000 + minor * 100 + patch (2.1.0: helpers
+ * that create and destroy a bcmt_side's events). */
 int bcmt_version(void);
 
 /* ---------------------------------------------------------------- language model

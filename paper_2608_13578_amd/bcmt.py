@@ -36,7 +36,8 @@ EXPORTED = ("bcmt_validate", "bcmt_saved_bytes", "bcmt_workspace_bytes", "bcmt_l
             "bcmt_layer_forward_noalloc",
             "bcmt_layer_backward", "bcmt_layer_forward_chunk", "bcmt_layer_backward_chunk",
             "bcmt_decode_state_bytes", "bcmt_decode_workspace_bytes", "bcmt_decode_reset",
-            "bcmt_decode_step", "bcmt_strerror", "bcmt_version", "bcmt_trace_enable",
+            "bcmt_decode_step", "bcmt_strerror", "bcmt_version", "bcmt_side_events_create",
+            "bcmt_side_events_destroy", "bcmt_trace_enable",
             "bcmt_trace_read", "bcmt_model_param_count", "bcmt_model_param_array",
             "bcmt_model_workspace_bytes", "bcmt_model_cast", "bcmt_model_train_step")
 
@@ -145,6 +146,10 @@ def lib():
         L.bcmt_strerror.restype = ctypes.c_char_p
         L.bcmt_version.argtypes = []
         L.bcmt_version.restype = ctypes.c_int
+        L.bcmt_side_events_create.argtypes = [ctypes.POINTER(bcmt_side)]
+        L.bcmt_side_events_create.restype = ctypes.c_int
+        L.bcmt_side_events_destroy.argtypes = [ctypes.POINTER(bcmt_side)]
+        L.bcmt_side_events_destroy.restype = ctypes.c_int
         L.bcmt_trace_enable.argtypes = [ctypes.c_int]
         L.bcmt_trace_enable.restype = ctypes.c_int
         L.bcmt_trace_read.argtypes = [ctypes.POINTER(bcmt_trace_entry), ctypes.c_int]
@@ -245,6 +250,19 @@ def bcmt_strerror(status):
 
 def bcmt_version():
     return lib().bcmt_version()
+
+
+def bcmt_side_events_create(side):
+    """Fills side.fork and side.join (a bcmt_side) with new events."""
+    st = lib().bcmt_side_events_create(ctypes.byref(side))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_side_events_create")
+
+
+def bcmt_side_events_destroy(side):
+    st = lib().bcmt_side_events_destroy(ctypes.byref(side))
+    if st != BCMT_OK:
+        raise BcmtError(st, "bcmt_side_events_destroy")
 
 
 def bcmt_validate(cfg):

@@ -385,7 +385,32 @@ const char* bcmt_strerror(int status) {
   }
 }
 
-int bcmt_version(void) { return 20000; }
+int bcmt_version(void) { return 20100; }
+
+int bcmt_side_events_create(bcmt_side* side) {
+  if (!side) return BCMT_ERR_INVALID;
+  side->fork = side->join = nullptr;
+  const unsigned flags = hipEventDisableTiming | hipEventDisableSystemFence;
+  hipEvent_t f = nullptr, j = nullptr;
+  if (hipEventCreateWithFlags(&f, flags) != hipSuccess) return BCMT_ERR_HIP;
+  if (hipEventCreateWithFlags(&j, flags) != hipSuccess) {
+    (void)hipEventDestroy(f);
+    return BCMT_ERR_HIP;
+  }
+  side->fork = f;
+  side->join = j;
+  return BCMT_OK;
+}
+
+int bcmt_side_events_destroy(bcmt_side* side) {
+  if (!side) return BCMT_ERR_INVALID;
+  int st = BCMT_OK;
+  for (void** e : {&side->fork, &side->join}) {
+    if (*e && hipEventDestroy((hipEvent_t)*e) != hipSuccess) st = BCMT_ERR_HIP;
+    *e = nullptr;
+  }
+  return st;
+}
 
 int bcmt_trace_enable(int on) {
   if (on) {
@@ -668,11 +693,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
                                  (const float*)(SV + p.S), (const float*)(W + p.dS),
                                  (float*)(W + p.a), (float*)(W + p.ds),
                                  gr.dwp ? (float*)(W + p.dwpp) : nullptr, p.B, p.T, D, p.L, s));
-    if (gr.dwp) {
-      SIDE_BEGIN();
-      LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
-      SIDE_END();
-    }
+    // (dwp, the sum of those partials, goes to the side stream with dWo.)
     // dH = dY + dU Wg^T + a_t dS[blk] + ds_t wp.
     {
       GemmDesc g{BT, D, D, W + p.du, D, false, {prm->Wg, nullptr, nullptr}, D, false, kSegNone, 0, 1};
@@ -688,13 +709,18 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     GemmDesc g{BT, D, D, dH, D, false, {prm->Wo, nullptr, nullptr}, D, false, kSegNone, 0, 1};
     LAUNCH(ST_WO_DGRAD, gemm_store(dt, g, W + p.dout, D, false, nullptr, 0, s));
   }
-  if (gr.dWo) {
+  // dwp joins this branch rather than taking a fork of its own after the
+  // pooling backward: each fork costs the caller's stream an event record.
+  const bool dwp_side = gr.dwp && !single;
+  if (gr.dWo || dwp_side) {
     SIDE_BEGIN();
-    {
+    if (gr.dWo) {
       GemmDesc g{D, D, BT, SV + p.o, D, true, {dH, nullptr, nullptr}, D, true, kSegNone, 0, 1};
       LAUNCH_SPLITK(ST_WO_WGRAD, ST_WO_WGRAD_RED, dt, g, wpart, gr.dWo, nullptr, nullptr, D, D,
                     accum, dd_min_k(D, BT));
     }
+    if (dwp_side)
+      LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
     SIDE_END();
   }
   // Block-local attention backward: one fused kernel when a block fits one

@@ -5,6 +5,8 @@ allocator (plumbing only) and forwards to the C ABI in ``bcmt``.  The layer's
 arithmetic runs entirely in the library's HIP kernels.
 """
 
+import sys
+
 import numpy as np
 import torch
 
@@ -27,16 +29,28 @@ def to_host64(t):
 
 class SideStream:
     """A caller-owned second stream (default priority) and the two events the
-    backward passes use to fork work onto it and join it back (bcmt_side)."""
+    backward passes use to fork work onto it and join it back (bcmt_side).
+    The events come from bcmt_side_events_create: no timing and no
+    system-scope fence on record, since they only order two streams of the
+    device."""
 
     def __init__(self, device="cuda"):
         self.stream = torch.cuda.Stream(device=device)
-        self.fork = torch.cuda.Event()
-        self.join = torch.cuda.Event()
-        # torch creates an event's HIP handle on its first record
-        for e in (self.fork, self.join):
-            e.record(self.stream)
-        self.stream.synchronize()
+        self._ev = abi.bcmt_side()
+        with torch.cuda.device(self.stream.device):
+            abi.bcmt_side_events_create(self._ev)
+        self.fork, self.join = self._ev.fork, self._ev.join
+
+    def __del__(self):
+        ev = getattr(self, "_ev", None)
+        if sys.is_finalizing():
+            return  # the process is ending: the events go with it
+        if ev is not None and (ev.fork or ev.join):
+            try:
+                torch.cuda.synchronize(self.stream.device)
+                abi.bcmt_side_events_destroy(ev)
+            except Exception:
+                pass
 
 
 class LayerBuffers:

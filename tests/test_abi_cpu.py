@@ -205,6 +205,16 @@ def test_backward_second_stream_arguments(lib):
     assert st == abi.BCMT_ERR_INVALID
 
 
+def test_side_event_helpers_arguments(lib):
+    """The event helpers reject a NULL structure; destroying a structure
+    whose events are NULL makes no HIP call and succeeds."""
+    assert lib.bcmt_side_events_create(None) == abi.BCMT_ERR_INVALID
+    assert lib.bcmt_side_events_destroy(None) == abi.BCMT_ERR_INVALID
+    s = abi.bcmt_side(0x1000, None, None)
+    assert lib.bcmt_side_events_destroy(ctypes.byref(s)) == abi.BCMT_OK
+    assert s.stream == 0x1000 and not s.fork and not s.join
+
+
 def _carry(N, Z):
     return abi.bcmt_carry(N, Z)
 
