@@ -420,11 +420,20 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
 // element (i % 4) of the 4-element rows addressed by lanes 4j + i/4; with
 // lane q addressing row k0 + q/4 at column c0 + 4 (q % 4), lane i receives
 // rows k0..k0+3 of column c0 + i.  Tile element (r, c) lives at
-// r*64 + 8*((c/8) ^ ((r/2) % 8)) + c % 8: the XOR swizzle of 16-byte chunks
-// spreads a fragment's rows over distinct banks.
-
+// r*64 + 8*((c/8) ^ tswz(r)) + c % 8.  A row read (16 lanes, 16 consecutive
+// rows, one chunk) needs rows 2j and 2j+1 (the two halves of the 64 banks)
+// on distinct chunks for distinct j: tswz is a permutation of the bits of
+// r/2.  A transposing read (16 lanes, 4 consecutive rows from a multiple of
+// 4, two adjacent chunks) needs rows 4j and 4j+2 on disjoint chunk pairs,
+// so row bit 1 goes to chunk bit 1; the next lane group (row bit 2, or row
+// bit 3 in tcol8p's order) moves to the other pairs through chunk bit 2.
+// (The plain (r/2) % 8 put rows 4j and 4j+2 on the same chunks: a two-way
+// conflict on every transposing read.)
+__device__ __forceinline__ int tswz(int r) {
+  return ((r >> 3) & 1) | (r & 2) | (((r ^ (r >> 1)) & 4));
+}
 __device__ __forceinline__ int toff(int r, int c) {
-  return r * 64 + (((c >> 3) ^ ((r >> 1) & 7)) << 3) + (c & 7);
+  return r * 64 + (((c >> 3) ^ tswz(r)) << 3) + (c & 7);
 }
 __device__ __forceinline__ bf16x8 trow8(const bf16* t, int r, int c0) {
   return *reinterpret_cast<const bf16x8*>(t + toff(r, c0));
@@ -457,7 +466,7 @@ __device__ __forceinline__ void tile_issue(const bf16* src, int64_t rs, int r0, 
   for (int i = 0; i < 8 / NW; ++i) {
     const int gi = wave * (8 / NW) + i;
     const int row = gi * 8 + (lane >> 3);
-    const int cg = (lane & 7) ^ ((row >> 1) & 7);
+    const int cg = (lane & 7) ^ tswz(row);
     const int grow = min(r0 + row, rlast);
     __builtin_amdgcn_global_load_lds(src + (int64_t)grow * rs + cg * 8, (lds_void_t*)(t + gi * 512),
                                      16, 0, 0);

@@ -554,7 +554,7 @@ struct EpiHbar {
 //   K-contiguous operand: [rows][64] with the 16-byte chunk c of row r
 //     holding global chunk c ^ ((r / 2) % 8); a fragment is one 16-byte read.
 //   M/N-contiguous operand: [64][rows] with chunk c of k-row kr holding
-//     global chunk c ^ (kr % 16); a fragment is two ds_read_b64_tr_b16
+//     global chunk c ^ rswz(kr); a fragment is two ds_read_b64_tr_b16
 //     reads.  That instruction hands lane i of each 16-lane group element
 //     (i % 4) of the 4-element rows read by lanes 4j + i/4, j = 0..3; with
 //     lane q addressing k-row k0 + q/4 at column c0 + 4 (q % 4), lane i
@@ -578,6 +578,18 @@ struct PipeOperand {
   // fragment read over all banks (rows are 64 or 128 bytes apart).
   __device__ __forceinline__ static int kswz(int r) {
     return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+  }
+  // XOR swizzle of an M/N-contiguous k-row's chunks.  A transposing
+  // fragment read has each 16-lane group read two adjacent chunks of four
+  // consecutive k-rows (k-row bits 0-1; bit 2 is the second read of the
+  // pair, bits 3-4 the lane group): bits 0-1 go to chunk bits 1-2, so the
+  // group's eight (k-row, chunk) pairs land in eight distinct chunk slots,
+  // and bit 3 ^ bit 4 to chunk bit 3, so that two groups read in the same
+  // cycle use disjoint halves of the banks.  (XOR with k-row & 15 left the
+  // k-row pairs 4j, 4j+1 on the same slots: a two-way bank conflict on
+  // every transposing read.)
+  __device__ __forceinline__ static int rswz(int kr) {
+    return ((kr & 3) << 1) ^ ((kr ^ (kr >> 1)) & 8);
   }
 };
 
@@ -623,7 +635,7 @@ struct PipeLoad {
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
         const int kr = (wave * PER + i) * RPI + lane / CPR;
-        const int cg = (lane % CPR) ^ (kr & 15);
+        const int cg = (lane % CPR) ^ Op::rswz(kr);
         const int gc = min(row0 + cg * 8, rmax - 8);
         voff[i] = (uint32_t)(((int64_t)kr * ld + (gc - c0)) * 2);
       }
@@ -663,7 +675,7 @@ struct PipeLoad {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         const int kr = ks * 32 + lg * 8 + hh * 4 + (lr >> 2);
-        const int c = (col >> 3) ^ (kr & 15);
+        const int c = (col >> 3) ^ Op::rswz(kr);
         h[hh] = lds_read_tr(s + kr * R + c * 8 + (col & 7));
       }
       bf16x8 r = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
