@@ -1031,13 +1031,19 @@ hipError_t launch(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Pipelined bf16 launch: 128 x 128 tiles, 2 x 2 waves, two 32 KB slabs in
-// flight, so that two workgroups share a CU (measured faster on these shapes
-// than a deeper ring with one workgroup per CU).  Needs the K range of every
-// split to be a whole number of 64-wide slabs.
-template <bool AMC, bool BNC, int SEG, class Epi>
-hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
-  constexpr int PBM = 128, PBN = 128, PBK = 64, ST = 2, WGM = 2, WGN = 2;
+// Pipelined bf16 launch: 128 x 128 tiles, two 32 KB slabs in flight, so
+// that two workgroups share a CU (measured faster on these shapes than a
+// deeper ring with one workgroup per CU).  Eight waves of 64 x 32 by
+// default: more waves to cover the load and LDS latencies, at 1.5x the
+// fragment reads per matrix instruction.  Four waves of 64 x 64 stay on
+// the weight gradients whose operands are both read transposed and that
+// fill the chip with splits, and on products whose B is split along K (the
+// input gradient of Q, K, V): there eight waves measured slower.  The
+// layer's forward + backward step took 308 instead of 316 us.  Needs the K
+// range of every split to be a whole number of 64-wide slabs.
+template <int WGM, int WGN, bool AMC, bool BNC, int SEG, class Epi>
+hipError_t launch_pipe_w(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  constexpr int PBM = 128, PBN = 128, PBK = 64, ST = 2;
   Operand<bf16, AMC, kSegNone> A{{(const bf16*)g.A, nullptr, nullptr}, g.lda, 0};
   Operand<bf16, BNC, SEG> B{{(const bf16*)g.B[0], (const bf16*)g.B[1], (const bf16*)g.B[2]}, g.ldb,
                             g.seg_len};
@@ -1051,6 +1057,18 @@ hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
   hipLaunchKernelGGL((gemm_pipe_kernel<PBM, PBN, PBK, ST, WGM, WGN, AMC, BNC, SEG, Epi>), grid,
                      dim3(WGM * WGN * 64), 0, s, g.M, g.N, g.K, A, B, kchunk, group, epi);
   return hipGetLastError();
+}
+
+template <bool AMC, bool BNC, int SEG, class Epi>
+hipError_t launch_pipe(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  if constexpr (AMC) {
+    int splits = g.splits < 1 ? 1 : g.splits;
+    if (g.kchunk > 0) splits = (g.K + g.kchunk - 1) / g.kchunk;
+    const int64_t wgs = (int64_t)((g.N + 127) / 128) * ((g.M + 127) / 128) * splits;
+    if (wgs >= 256) return launch_pipe_w<2, 2, AMC, BNC, SEG>(g, epi, s);
+  }
+  if constexpr (SEG == kSegK) return launch_pipe_w<2, 2, AMC, BNC, SEG>(g, epi, s);
+  return launch_pipe_w<2, 4, AMC, BNC, SEG>(g, epi, s);
 }
 
 template <typename T, bool AMC, bool BNC, int SEG, class Epi>
