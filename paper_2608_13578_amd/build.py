@@ -12,7 +12,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = ["gemm.hip", "attention.hip", "attention_small.hip", "memory.hip", "decode.hip",
-           "api.hip", "model.hip"]
+           "api.hip", "model.hip", "head.hip"]
 LIB = os.path.join(HERE, "libbcmt.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 ARCH = "gfx950"

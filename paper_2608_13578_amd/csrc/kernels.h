@@ -116,6 +116,20 @@ hipError_t gemm_gelu_bwd(DType dt, const GemmDesc& g, const void* U, void* dU, i
 hipError_t gemm_head_stats(const GemmDesc& g, float* part, int V, hipStream_t s);
 hipError_t gemm_head_grad(const GemmDesc& g, void* G, int64_t ld, const float* lse,
                           const int32_t* tgt, int V, float inv_n, hipStream_t s);
+// The same two passes without a tiled product, for d = 128 (head.hip): each
+// workgroup streams a range of the vocabulary past 128 rows of f held in
+// registers.  head_stats writes *nrange (max, sum of exp(z - max)) pairs
+// per row to part (row-major [rows][*nrange], natural units), for the
+// log-sum-exp kernel; head_grad writes G as gemm_head_grad does and df =
+// G E (float32 [rows][128]), through dfpart (head_partial_bytes) when the
+// vocabulary is split into several ranges.
+bool head_fused_ok(int d, int Vp);
+size_t head_partial_bytes(int rows, int d, int Vp);
+hipError_t head_stats(const void* f, const void* E, int rows, int d, int V, int Vp, float* part,
+                      int* nrange, hipStream_t s);
+hipError_t head_grad(const void* f, const void* E, int rows, int d, int V, int Vp,
+                     const float* lse, const int32_t* tgt, float inv_n, void* G, int64_t ldg,
+                     float* dfpart, float* df, hipStream_t s);
 
 // ------------------------------------------------------------------ attention
 // qkv: [B, T, 3D] (Q | K | V), head h at columns h*64 .. h*64+63 of each.

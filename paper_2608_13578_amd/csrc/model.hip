@@ -389,6 +389,7 @@ struct ModelPlan {
                              gemm_splitk_partial_bytes(BT, d, Vp, kDfMinK)};
     for (size_t x : sizes)
       if (x > w) w = x;
+    if (head_partial_bytes(BT, d, Vp) > w) w = head_partial_bytes(BT, d, Vp);
     wpart_bytes = upb(w);
     const size_t act = upb((size_t)BT * d * 2), act4 = upb((size_t)BT * 4 * d * 2);
     const size_t rowf = upb((size_t)BT * 4);
@@ -563,9 +564,14 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
   // the backward for the gradient.
   const GemmDesc head{BT, p.Vp, d, W + p.f, d, false, {pw(0), nullptr, nullptr}, d, false,
                       kSegNone, 0, 1};
-  CHK(gemm_head_stats(head, (float*)(W + p.hpart), c.V, s));
+  const bool fused_head = head_fused_ok(d, p.Vp);
+  int hparts = p.Vp / 128;
+  if (fused_head)
+    CHK(head_stats(W + p.f, pw(0), BT, d, c.V, p.Vp, (float*)(W + p.hpart), &hparts, s));
+  else
+    CHK(gemm_head_stats(head, (float*)(W + p.hpart), c.V, s));
   hipLaunchKernelGGL(head_lse_kernel, dim3((BT + 3) / 4), dim3(256), 0, s,
-                     (const float*)(W + p.hpart), p.Vp / 128, (const bf16*)(W + p.f), pw(0),
+                     (const float*)(W + p.hpart), hparts, (const bf16*)(W + p.f), pw(0),
                      targets, BT, d, c.V, lse, (float*)(W + p.row_loss));
   KCHK();
   hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(1024), 0, s, (const float*)(W + p.row_loss),
@@ -595,13 +601,18 @@ int bcmt_model_train_step(const bcmt_model_config* cfg, const int32_t* tokens,
     return hipGetLastError();
   };
   // dlogits = (softmax - onehot) / (B T), over the logits buffer
-  CHK(gemm_head_grad(head, logits, p.Vp, lse, targets, c.V, 1.f / (float)BT, s));
+  // (with the fused head, df = dlogits E comes out of the same pass)
+  if (fused_head)
+    CHK(head_grad(W + p.f, pw(0), BT, d, c.V, p.Vp, lse, targets, 1.f / (float)BT, logits, p.Vp,
+                  wpart, (float*)(W + p.df32), s));
+  else
+    CHK(gemm_head_grad(head, logits, p.Vp, lse, targets, c.V, 1.f / (float)BT, s));
   {
     // dE = dlogits^T f (the tied head's part; the lookups add below)
     GemmDesc g{p.Vp, d, BT, logits, p.Vp, true, {W + p.f, nullptr, nullptr}, d, true, kSegNone, 0, 1};
     CHK(gemm_splitk(DType::BF16, g, wpart, gw(0), nullptr, nullptr, d, d, false, kWgradMinK, s));
   }
-  {
+  if (!fused_head) {
     // df = dlogits E: B[v][k] = E[v][k], N-contiguous; K = Vp is long and
     // N = d narrow, so the product is split along K (float32 result)
     GemmDesc g{BT, d, p.Vp, logits, p.Vp, false, {pw(0), nullptr, nullptr}, d, true, kSegNone, 0, 1};

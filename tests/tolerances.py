@@ -65,15 +65,21 @@ STACK_ENSEMBLE = 4
 # heads of 16, L = 128) on one sequence of 1024 tokens: its residual stream,
 # LayerNorm outputs and MLP activations are bf16 too, and its attention is
 # as peaked as a mild stress case.  Bounds per gradient array (named as in
-# the flat parameter vector) from lm_bf16_model; the ensemble is the model
-# without jitter and LM_ENSEMBLE - 1 jittered realisations.
+# the flat parameter vector) from lm_bf16_model by the MARGIN rule over
+# LM_DERIVE realizations (the model without jitter and LM_DERIVE - 1
+# jittered ones), as tests/lm_bounds.py prints them.  A handful of
+# realizations is not enough here: the w_p gradients are covariances that
+# cancel heavily, and 1.wp's error ranges from 0.009 to 0.032 over 24 of
+# them.  test_bf16_model checks the bounds against the first LM_ENSEMBLE.
 LM = dict(case="bcmt-bench-shape", V=50257, d=128, H=8, layers=6, B=1, T=1024, L=128,
           gamma=0.8, bounds={
-              "E": 0.022, "Pe": 0.021, "0.Wq": 0.021, "0.Wk": 0.021, "1.Wq": 0.021, "1.Wk": 0.022,
-              "1.wp": 0.023, "2.Wq": 0.029, "2.Wk": 0.028, "2.Wg": 0.023, "2.wp": 0.029,
-              "3.Wq": 0.024, "3.ln2_g": 0.021, "4.Wq": 0.027, "4.Wk": 0.022, "5.Wq": 0.038,
-              "5.Wk": 0.03, "5.wp": 0.025, "5.ln2_g": 0.022})
+              "E": 0.022, "Pe": 0.023, "0.Wk": 0.023, "0.Wq": 0.021, "1.Wk": 0.03, "1.Wq": 0.028,
+              "1.wp": 0.04, "2.Wg": 0.023, "2.Wk": 0.03, "2.Wq": 0.033, "2.wp": 0.03,
+              "3.Wk": 0.023, "3.Wq": 0.028, "4.Wk": 0.022, "4.Wq": 0.032, "5.Wk": 0.042,
+              "5.Wq": 0.04, "5.wp": 0.035, "0.ln1_g": 0.021, "0.ln2_g": 0.021,
+              "1.ln2_g": 0.023, "3.ln2_g": 0.021, "5.ln2_g": 0.025})
 LM_ENSEMBLE = 4
+LM_DERIVE = 24
 
 # Cases whose outputs are compared without a backward pass: incremental
 # decoding of the stress distribution (Y only).
