@@ -48,6 +48,10 @@ def stage_work(name, B, T, D, H, L, es):
         "bwd.wm_wgrad_gemm": 2 * B * nb * D * D, "bwd.wg_dgrad_gemm": 2 * BT * D * D,
         "bwd.wo_dgrad_gemm": 2 * BT * D * D, "bwd.wo_wgrad_gemm": 2 * BT * D * D,
         "bwd.qkv_dgrad_gemm": 6 * BT * D * D, "bwd.qkv_wgrad_gemm": 6 * BT * D * D,
+        # long sequences: the memory projections as products of their own
+        # (Q = S W_m; dM = dP W_m^T with dP as a bf16 hi + lo pair)
+        "fwd.wm_gemm": 2 * B * nb * D * D,
+        "bwd.wm_dgrad_gemm": (4 if es == 2 else 2) * B * nb * D * D,
         # QK^T and PV over causal pairs (forward); the backward recomputes
         # QK^T twice and forms dP twice, dV, dK and dQ.
         "fwd.attention": 4 * 64 * H * pairs,
@@ -65,14 +69,20 @@ def stage_work(name, B, T, D, H, L, es):
     # dw_p partial rows: one per 8 * (16 / nvj) tokens of each block
     nvj = next(n for n in (1, 2, 4, 8) if n * 64 >= D // (16 // es) or n == 8)
     pool_rows = B * nb * -(-min(L, T) // (8 * (16 // nvj)))
+    fused = nb <= 32  # the single-kernel memory path (projection + scan)
     hbm = {
         "fwd.pool": act + BT * 4 + B * nb * D * 4 + B * nb * 8,
-        # memory projection + scan: read S (float32 and compute type) and W_m,
-        # write M (both types) and P
-        "fwd.memory_scan": B * nb * D * (4 + es + 4 + es + 4) + D * D * es,
+        # single kernel: read S (float32 and compute type) and W_m, write M
+        # (both types) and P; long path, the scans alone: read S and Q = S W_m
+        # (float32), write M (both types) and P, each once (the two-pass scan
+        # reads S and Q twice)
+        "fwd.memory_scan": (B * nb * D * (4 + es + 4 + es + 4) + D * D * es) if fused
+                           else B * nb * D * (4 + 4 + 4 + es + 4),
         "bwd.gate": 3 * act + B * nb * D * (4 + es),
-        # read dP (bf16: a hi + lo pair), W_m and M, write dS
-        "bwd.memory_scan": B * nb * D * ((2 * es if es == 2 else es) + 4 + 4) + D * D * es,
+        # single kernel: read dP (bf16: a hi + lo pair), W_m and M, write dS;
+        # long path, the reverse scans alone: read dM and M, write dS
+        "bwd.memory_scan": (B * nb * D * ((2 * es if es == 2 else es) + 4 + 4) + D * D * es)
+                           if fused else B * nb * D * (4 + 4 + 4),
         # read H, s, dS and S; write a, ds and the dw_p partial rows
         "bwd.pool": act + BT * 12 + B * nb * D * 8 + pool_rows * D * 4,
         "bwd.pool_dwp": pool_rows * D * 4,

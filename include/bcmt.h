@@ -179,9 +179,8 @@ int bcmt_layer_forward(const bcmt_config* cfg, const void* X, const bcmt_params*
  *   ws     at least bcmt_workspace_bytes(cfg, BCMT_PASS_BACKWARD) bytes.
  *   side   a second stream for the weight-gradient products, or NULL
  *          (BCMT_ERR_INVALID if given without both events).
- * The weight-matrix gradients and dwp are reduced in a fixed order
- * (deterministic); dgamma is summed with float32 atomics, so it may differ
- * run to run in the last bits. */
+ * Every gradient is reduced in a fixed order, so repeated calls give the
+ * same bits (the decay gradient from per-workgroup partials). */
 int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params* params,
                         const void* saved, const void* dY, void* dX, const bcmt_grads* grads,
                         void* ws, size_t ws_bytes, void* stream, const bcmt_side* side);

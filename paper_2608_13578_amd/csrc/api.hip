@@ -70,6 +70,8 @@ struct Plan {
   // backward scratch
   size_t du, pbar, pbar_lo, dS, dM, mpart_b, a, ds, dwpp, dh, dout, delta, dqkv, wpart;
   size_t cpbar, cpbar_lo, cdm, ce0, cpart_b;  // chunk state gradients
+  size_t dgp;  // decay-gradient partials (dgp_rows + B rows)
+  int dgp_rows;
   size_t bwd_bytes;
 
   explicit Plan(const bcmt_config& c) {
@@ -141,6 +143,10 @@ struct Plan {
     cdm = take(BD * 4);
     ce0 = take(BD * 4);
     cpart_b = take(carry_part_bytes(B, D));
+    // decay-gradient partials: the memory backward's rows, then B rows of
+    // the chunked path's first-block terms
+    dgp_rows = dg_part_rows(B, nb, D, pc);
+    dgp = take((size_t)(dgp_rows + B) * (pc ? D : 1) * 4);
     bwd_bytes = off;
   }
 };
@@ -241,9 +247,12 @@ bool carry_ok(const bcmt_carry* c) {
 // ------------------------------------------------------------------ tracing
 // Named stages of the two passes; each is one kernel launch.
 enum Stage {
-  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_CARRY_IN, ST_CARRY_PROJ, ST_SCAN_FWD, ST_GATE,
+  ST_QKV, ST_ATTN_FWD, ST_WO, ST_POOL_FWD, ST_CARRY_IN, ST_CARRY_PROJ, ST_WM_FWD, ST_SCAN_FWD,
+  ST_GATE,
   ST_GATE_BWD, ST_WG_WGRAD, ST_WG_WGRAD_RED, ST_WM_WGRAD,
-  ST_WM_WGRAD_RED, ST_CARRY_WGRAD, ST_CARRY_DGRAD, ST_MEM_BWD, ST_CARRY_BWD, ST_POOL_BWD, ST_DWP,
+  ST_WM_WGRAD_RED, ST_CARRY_WGRAD, ST_CARRY_DGRAD, ST_WM_BWD, ST_MEM_BWD, ST_CARRY_BWD,
+  ST_POOL_BWD, ST_DWP,
+  ST_DGAMMA,
   ST_HBAR, ST_WO_DGRAD, ST_WO_WGRAD, ST_WO_WGRAD_RED,
   ST_ATTN_BWD_BLOCK, ST_ATTN_BWD_DQ, ST_ATTN_BWD_DKDV, ST_DX, ST_QKV_WGRAD, ST_QKV_WGRAD_RED,
   ST_DEC_RESET, ST_DEC_QKV, ST_DEC_ATTN, ST_DEC_WO, ST_DEC_WO_FIN, ST_DEC_GATE, ST_DEC_GATE_FIN,
@@ -252,10 +261,11 @@ enum Stage {
 };
 const char* const kStageNames[ST_COUNT] = {
     "fwd.qkv_gemm", "fwd.attention", "fwd.wo_gemm", "fwd.pool", "fwd.carry_in",
-    "fwd.carry_proj_gemm", "fwd.memory_scan",
+    "fwd.carry_proj_gemm", "fwd.wm_gemm", "fwd.memory_scan",
     "fwd.gate_gemm", "bwd.gate", "bwd.wg_wgrad_gemm", "bwd.wg_wgrad_reduce",
     "bwd.wm_wgrad_gemm", "bwd.wm_wgrad_reduce", "bwd.carry_wm_wgrad_gemm",
-    "bwd.carry_dgrad_gemm", "bwd.memory_scan", "bwd.carry_in", "bwd.pool", "bwd.pool_dwp",
+    "bwd.carry_dgrad_gemm", "bwd.wm_dgrad_gemm", "bwd.memory_scan", "bwd.carry_in", "bwd.pool", "bwd.pool_dwp",
+    "bwd.decay_grad",
     "bwd.wg_dgrad_gemm",
     "bwd.wo_dgrad_gemm", "bwd.wo_wgrad_gemm", "bwd.wo_wgrad_reduce", "bwd.attention_block", "bwd.attention_dq",
     "bwd.attention_dkdv", "bwd.qkv_dgrad_gemm", "bwd.qkv_wgrad_gemm", "bwd.qkv_wgrad_reduce",
@@ -534,9 +544,24 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
     cr.Nout = cout ? cout->N : nullptr;
     cr.Zout = cout ? cout->Z : nullptr;
   }
-  LAUNCH(ST_SCAN_FWD, mem_fwd(dt, W + p.St, prm->Wm, (const float*)(SV + p.S), (float*)(SV + p.M),
-                              SV + p.Mt, (float*)(SV + p.P), (float*)(W + p.mpart), p.B, p.nb, D,
-                              cfg->gamma, cr, s));
+  if (mem_fused(p.nb, cr.gvec != nullptr)) {
+    LAUNCH(ST_SCAN_FWD, mem_fwd(dt, W + p.St, prm->Wm, (const float*)(SV + p.S),
+                                (float*)(SV + p.M), SV + p.Mt, (float*)(SV + p.P),
+                                (float*)(W + p.mpart), p.B, p.nb, D, cfg->gamma, cr, s));
+  } else {
+    // the W_m product and the scans timed apart
+    const bool pc = cr.gvec != nullptr;
+    int nq = 0;
+    if (!pc)
+      LAUNCH(ST_WM_FWD, mem_fwd_proj(dt, W + p.St, prm->Wm, SV + p.Mt, (float*)(SV + p.P),
+                                     (float*)(W + p.mpart), p.B, p.nb, D, false, &nq, s));
+    LAUNCH(ST_SCAN_FWD, mem_fwd_scan(dt, (const float*)(SV + p.S), (float*)(SV + p.M), SV + p.Mt,
+                                     (float*)(SV + p.P), (float*)(W + p.mpart), nq, p.B, p.nb, D,
+                                     cfg->gamma, cr, s));
+    if (pc)
+      LAUNCH(ST_WM_FWD, mem_fwd_proj(dt, W + p.St, prm->Wm, SV + p.Mt, (float*)(SV + p.P),
+                                     (float*)(W + p.mpart), p.B, p.nb, D, true, &nq, s));
+  }
   // 7. Gate and injection (Sec. 3.7, 3.8).
   {
     GemmDesc g{BT, D, D, SV + p.h, D, false, {prm->Wg, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -624,14 +649,11 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   const void* dH = single ? dY : (const void*)(W + p.dh);
   if (!single) {
     // Gate and injection: dU, and the block sums of dY * G shifted back by one.
-    // dgamma is reduced with atomics later in the pass; this kernel clears it
-    // first unless the gradients accumulate.  The weight matrices and dwp are
-    // written (or accumulated) by fixed-order reductions.
+    // The weight matrices, dwp and the decay gradient are written (or
+    // accumulated) by fixed-order reductions.
     const bool lo = dt == DType::BF16;  // context gradients kept as hi + lo
     LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                                 lo ? W + p.pbar_lo : nullptr,
-                                 (accum || !gvec) ? nullptr : dgam, gvec ? D : 0,
-                                 (accum || gvec) ? nullptr : dgam, p.B, p.T, D, p.L,
+                                 lo ? W + p.pbar_lo : nullptr, nullptr, 0, nullptr, p.B, p.T, D, p.L,
                                  chunk ? (const float*)(SV + p.cP) : nullptr,
                                  chunk ? W + p.cpbar : nullptr,
                                  (chunk && lo) ? W + p.cpbar_lo : nullptr, s));
@@ -677,15 +699,29 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
       cr.dZout = dcout ? dcout->Z : nullptr;
       cr.e0 = (float*)(W + p.ce0);
     }
-    LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, lo ? W + p.pbar_lo : nullptr, prm->Wm,
-                               (const float*)(SV + p.M), (float*)(W + p.dS), dgam,
-                               (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
-                               cfg->gamma, cr, s));
+    float* dgp = dgam ? (float*)(W + p.dgp) : nullptr;
+    if (mem_fused(p.nb, gvec != nullptr)) {
+      LAUNCH(ST_MEM_BWD, mem_bwd(dt, W + p.pbar, lo ? W + p.pbar_lo : nullptr, prm->Wm,
+                                 (const float*)(SV + p.M), (float*)(W + p.dS), dgp,
+                                 (float*)(W + p.dM), (float*)(W + p.mpart_b), p.B, p.nb, D,
+                                 cfg->gamma, cr, s));
+    } else {
+      int nq = 0;
+      LAUNCH(ST_WM_BWD, mem_bwd_proj(dt, W + p.pbar, lo ? W + p.pbar_lo : nullptr, prm->Wm,
+                                     (float*)(W + p.mpart_b), p.B, p.nb, D, &nq, s));
+      LAUNCH(ST_MEM_BWD, mem_bwd_scan(dt, (const float*)(SV + p.M), (float*)(W + p.dS), dgp,
+                                      (float*)(W + p.mpart_b), nq, p.B, p.nb, D, cfg->gamma, cr,
+                                      s));
+    }
     if (chunk)
       LAUNCH(ST_CARRY_BWD, carry_finish((const float*)(SV + p.cN), (const float*)(SV + p.cZ),
                                         (const float*)(W + p.cdm), (const float*)(W + p.dS),
                                         (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
-                                        dcin ? dcin->Z : nullptr, dgam, p.B, p.nb, D,
+                                        dcin ? dcin->Z : nullptr,
+                                        dgam ? (float*)(W + p.dgp) +
+                                                   (size_t)p.dgp_rows * (gvec ? D : 1)
+                                             : nullptr,
+                                        p.B, p.nb, D,
                                         cfg->gamma, gvec, gvec != nullptr, s));
     // Pooling backward: per-token a_t and ds_t, and partial sums of
     // ds_t H[t]; dwp = their sum on the side stream.
@@ -711,8 +747,10 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   }
   // dwp joins this branch rather than taking a fork of its own after the
   // pooling backward: each fork costs the caller's stream an event record.
+  // So does the decay gradient's fixed-order sum of its partials.
   const bool dwp_side = gr.dwp && !single;
-  if (gr.dWo || dwp_side) {
+  const bool dg_side = dgam && !single;
+  if (gr.dWo || dwp_side || dg_side) {
     SIDE_BEGIN();
     if (gr.dWo) {
       GemmDesc g{D, D, BT, SV + p.o, D, true, {dH, nullptr, nullptr}, D, true, kSegNone, 0, 1};
@@ -721,6 +759,9 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     }
     if (dwp_side)
       LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
+    if (dg_side)
+      LAUNCH(ST_DGAMMA, dgamma_reduce((const float*)(W + p.dgp), p.dgp_rows + (chunk ? p.B : 0),
+                                      gvec ? D : 1, dgam, accum, s));
     SIDE_END();
   }
   // Block-local attention backward: one fused kernel when a block fits one

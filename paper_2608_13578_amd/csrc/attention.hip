@@ -502,14 +502,17 @@ __global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* _
   if (q0 >= be) return;
   const int64_t rs = 3LL * D;
   const bf16* base = qkv + (int64_t)b * Tn * rs + h * kDh;
-  const int tw0 = q0 + wave * 32;
+  // The workgroup's 2 NW groups of 16 queries are dealt in pairs g, 2 NW - 1 - g,
+  // one pair per wave: a causal group's work grows with its position, so
+  // every wave gets about the same number of (query group, key tile) pairs.
+  const int tq[2] = {q0 + 16 * wave, q0 + 16 * (2 * NW - 1 - wave)};
   const int kend = min(be, q0 + QT);
   const int nt = (kend - bs + 63) / 64;
 
   bf16x8 qf[2][2];
 #pragma unroll
   for (int nq = 0; nq < 2; ++nq) {
-    const int t = tw0 + nq * 16 + lr;
+    const int t = tq[nq] + lr;
 #pragma unroll
     for (int ds = 0; ds < 2; ++ds)
       qf[nq][ds] = t < be ? *reinterpret_cast<const bf16x8*>(base + (int64_t)t * rs + ds * 32 + lg * 8)
@@ -545,8 +548,7 @@ __global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* _
     bool live[2];
 #pragma unroll
     for (int nq = 0; nq < 2; ++nq) {
-      const int tq = tw0 + nq * 16;
-      live[nq] = !(tq >= be || tq + 15 < kt);  // wave-uniform
+      live[nq] = !(tq[nq] >= be || tq[nq] + 15 < kt);  // wave-uniform
     }
     f32x4 s[2][4];
     if (live[0] || live[1]) {
@@ -567,8 +569,7 @@ __global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* _
 #pragma unroll
     for (int nq = 0; nq < 2; ++nq) {
       if (!live[nq]) continue;
-      const int tq = tw0 + nq * 16;
-      const int t_eff = min(tq + lr, be - 1);
+      const int t_eff = min(tq[nq] + lr, be - 1);
       float mx = -INFINITY;
 #pragma unroll
       for (int ku = 0; ku < 4; ++ku)
@@ -631,7 +632,7 @@ __global__ __launch_bounds__(NW * 64, 3) void attn_fwd_bf16_kernel(const bf16* _
     float lt = l[nq];
     lt += __shfl_xor(lt, 16, 64);
     lt += __shfl_xor(lt, 32, 64);
-    const int t = tw0 + nq * 16 + lr;
+    const int t = tq[nq] + lr;
     if (t < be) {
       const float inv = 1.0f / lt;
       bf16* op = out + ((int64_t)b * Tn + t) * D + h * kDh + lg * 4;

@@ -438,8 +438,22 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
   const int64_t stride = (int64_t)M * N;
   const int64_t i = (int64_t)blockIdx.x * 64 + lane;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (i < total)
-    for (int z = wave; z < splits; z += 4) acc += *reinterpret_cast<const f32x4*>(P + z * stride + i * 4);
+  if (i < total) {
+    // four of this wave's splits in flight at a time, added in increasing z
+    const float* p = P + i * 4;
+    int z = wave;
+    for (; z + 12 < splits; z += 16) {
+      const f32x4 a0 = *reinterpret_cast<const f32x4*>(p + z * stride);
+      const f32x4 a1 = *reinterpret_cast<const f32x4*>(p + (z + 4) * stride);
+      const f32x4 a2 = *reinterpret_cast<const f32x4*>(p + (z + 8) * stride);
+      const f32x4 a3 = *reinterpret_cast<const f32x4*>(p + (z + 12) * stride);
+      acc += a0;
+      acc += a1;
+      acc += a2;
+      acc += a3;
+    }
+    for (; z < splits; z += 4) acc += *reinterpret_cast<const f32x4*>(p + z * stride);
+  }
   red[wave][lane] = acc;
   __syncthreads();
   if (wave != 0 || i >= total) return;

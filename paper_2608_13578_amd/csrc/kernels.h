@@ -206,6 +206,21 @@ size_t mem_part_bytes(int B, int nb, int D, bool per_channel);
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s);
+// The long path's steps (what mem_fwd / mem_bwd run when mem_fused is
+// false), for callers that time them apart: mem_fwd_proj is the W_m
+// product (one decay: Q = St Wm as *nq split-K slices, before the scan; per
+// channel: P = Mt Wm, after it), mem_fwd_scan the two scan passes;
+// mem_bwd_proj the products dM = (Pbar + Pbar_lo) Wm^T (*nq slices),
+// mem_bwd_scan the reverse scans.
+hipError_t mem_fwd_proj(DType dt, const void* St, const void* Wm, const void* Mt, float* P,
+                        float* part, int B, int nb, int D, bool per_channel, int* nq,
+                        hipStream_t s);
+hipError_t mem_fwd_scan(DType dt, const float* S, float* M, void* Mt, float* P, float* part, int nq,
+                        int B, int nb, int D, float gamma, const Carry& c, hipStream_t s);
+hipError_t mem_bwd_proj(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
+                        float* part, int B, int nb, int D, int* nq, hipStream_t s);
+hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, float* part, int nq,
+                        int B, int nb, int D, float gamma, const Carry& c, hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 // With Pc (a chunk after earlier blocks) block 0 uses Mc = Pc[b] and its
 // sum of dY * G goes to Pbar_c [B, D] (compute type).  In bf16 each block sum
@@ -215,13 +230,19 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
                     void* Pbar, void* Pbar_lo, float* zero_a, int na, float* zero_b, int B, int T,
                     int D, int L, const float* Pc, void* Pbar_c, void* Pbar_c_lo, hipStream_t s);
 // Memory backward: dM = (Pbar + Pbar_lo) Wm^T (Pbar_lo may be null; float32
-// ignores it), then the reverse decayed scan: dS and the decay gradient
-// (atomically added to *dgamma when given).  For long sequences (see
-// mem_fwd) dM goes through `dM` ([B*nb, D] float32) and a split-K product
-// using `part`; both may be null for short ones.
+// ignores it), then the reverse decayed scan: dS and the decay gradient as
+// partials (when dgpart is given): dg_part_rows(B, nb, D, per channel) rows
+// of 1 float (one decay) or D floats (one per channel), every row written.
+// For long sequences (see mem_fwd) dM goes through a split-K product using
+// `part`; both may be null for short ones.
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
-                   const float* M, float* dS, float* dgamma, float* dM, float* part, int B, int nb,
+                   const float* M, float* dS, float* dgpart, float* dM, float* part, int B, int nb,
                    int D, float gamma, const Carry& c, hipStream_t s);
+int dg_part_rows(int B, int nb, int D, bool per_channel);
+// out[0 .. Dp) = (out if accumulate, else 0) + the sum of part[rows][Dp]
+// over its rows, in a fixed order (deterministic).
+hipError_t dgamma_reduce(const float* part, int rows, int Dp, float* out, bool accumulate,
+                         hipStream_t s);
 // Chunked execution.  carry_prep copies the incoming state (Nu [B, D],
 // Zu [B]; both null: empty history) to Nin / Zin and writes its memory
 // Mct = Nin / Zin (0 where Zin = 0) in the compute type; with no incoming
@@ -231,15 +252,16 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* 
 // (carry_part_bytes bytes).  carry_finish forms the incoming state's
 // gradients from dMc, dS of block 0 and e0:
 //   dNin = dMc / Zin + g dS_0,  dZin = sum_cols (g e0 - dMc . M_in / Zin),
-// and adds the first block's decay term sum_cols dS_0 Nin + e0 Zin to
-// *dgamma (atomic); null outputs are skipped.
+// and writes the first block's decay term sum_cols dS_0 Nin + e0 Zin as
+// B more partial rows at dgpart (1 or D floats each, as mem_bwd's); null
+// outputs are skipped.
 hipError_t carry_prep(DType dt, const float* Nu, const float* Zu, float* Nin, float* Zin,
                       void* Mct, float* Pc, int B, int D, bool zcol, hipStream_t s);
 size_t carry_part_bytes(int B, int D);
 hipError_t carry_proj(DType dt, const void* A, const void* Wm, float* out, float* part,
                       bool transposed, bool accumulate, int B, int D, hipStream_t s);
 hipError_t carry_finish(const float* Nin, const float* Zin, const float* dMc, const float* dS,
-                        const float* e0, float* dNin, float* dZin, float* dgamma, int B, int nb,
+                        const float* e0, float* dNin, float* dZin, float* dgpart, int B, int nb,
                         int D, float gamma, const float* gvec, bool zcol, hipStream_t s);
 // Pooling backward: per-token softmax weights a_t and score gradients ds_t,
 // and (when dwp_part is not null) partial sums of ds_t H[t] over chunks of

@@ -452,8 +452,11 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     __syncthreads();  // part[] is rewritten by the next row tile
   }
   if constexpr (!FWD) {
-    if (cr.gvec) {  // per-channel decay gradient
-      if (scol && dgamma) unsafeAtomicAdd(dgamma + col, dg);
+    // this workgroup's share of the decay gradient, as one partial
+    // (dg_part_rows): per channel, row b, its columns; else one value at
+    // row b * gridDim.x + blockIdx.x
+    if (cr.gvec) {
+      if (scol && dgamma) dgamma[(int64_t)b * D + col] = dg;
     } else {
       const float v = wave_sum(dg);
       if (lane == 0) red[wave] = v;
@@ -461,7 +464,7 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
       if (tid == 0 && dgamma) {
         float t = 0.f;
         for (int w = 0; w < kMsWaves; ++w) t += red[w];
-        unsafeAtomicAdd(dgamma, t);
+        dgamma[(int64_t)b * gridDim.x + blockIdx.x] = t;
       }
     }
   }
@@ -618,7 +621,7 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_fwd_kernel(
 // Reverse scans of the memory backward from dM (nq split-K partial products,
 // stride qstride, added in order) and M:
 //   Qs_i = dM_i / Z_i + g Qs_{i+1} (= dS_i),  E_i = -dM_i . M_i / Z_i + g E_{i+1},
-//   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one atomic add per workgroup).
+//   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one partial per workgroup).
 // The gradients of a chunk's final state enter at the last block; E of the
 // first block goes to cr.e0.  aggQ / aggE: the chunk aggregates (each
 // chunk's values at its first block, from a zero carry).
@@ -662,6 +665,8 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
   float mm[kScRows];
 #pragma unroll
   for (int r = 0; r < kScRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
+  // the memory of the block before this wave's first (its decay term)
+  const float mprev = APPLY && on && a >= 1 && a < nb ? M[off0 - D] : 0.f;
 #pragma unroll
   for (int r = 0; r < kScRows; ++r) {
     const int i = a + r;
@@ -743,21 +748,24 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
         dS[off0 + (int64_t)r * D] = qs;
         if (i >= 1) {
           const float zp = zsum(i - 1, gam, lg2, zin);
-          const float mp = r > 0 ? mm[r > 0 ? r - 1 : 0] : M[off0 - D];
+          const float mp = r > 0 ? mm[r > 0 ? r - 1 : 0] : mprev;
           dg += qs * (mp * zp) + es * zp;
         } else if (cr.e0) {
           cr.e0[(int64_t)b * D + col] = es;
         }
       }
     }
-    if (cr.gvec) {  // per-channel decay gradient: the column's waves meet in LDS
+    // the decay gradient as partials (dg_part_rows): per channel, row
+    // ch * B + b, this workgroup's columns; else one value per workgroup
+    const int64_t prow = (int64_t)ch * gridDim.y + b;
+    if (cr.gvec) {  // the column's waves meet in LDS
       __syncthreads();
       wq[w][c] = dg;
       __syncthreads();
       if (w == 0 && on && dgamma) {
         float t = 0.f;
         for (int j = 0; j < kScWaves; ++j) t += wq[j][c];
-        unsafeAtomicAdd(dgamma + col, t);
+        dgamma[prow * D + col] = t;
       }
       return;
     }
@@ -767,7 +775,7 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
     if (threadIdx.x == 0 && dgamma) {
       float t = 0.f;
       for (int j = 0; j < kScWaves; ++j) t += red[j];
-      unsafeAtomicAdd(dgamma, t);
+      dgamma[prow * gridDim.x + blockIdx.x] = t;
     }
   }
 }
@@ -778,8 +786,7 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
 // sums are written already shifted back by one block (row i-1 holds block
 // i's sum; the last row of each batch element is zero), in the compute type,
 // as the left operand of the W_m backward products.  The first workgroup
-// also clears dwp and dgamma (when given), which later kernels of the pass
-// accumulate into with atomics.  In a chunk that follows earlier blocks
+// also clears zero_a / zero_b when given.  In a chunk that follows earlier blocks
 // (Pc not null) block 0 was injected with Pc[b], and its sum goes to
 // Pbar_c[b].
 template <typename T>
@@ -933,7 +940,7 @@ __global__ __launch_bounds__(256) void carry_finish_kernel(
       ez += ezc;
     }
     if (gvec) {
-      if (dgamma) unsafeAtomicAdd(dgamma + c, dgc);
+      if (dgamma) dgamma[o] = dgc;  // partial row b
     } else {
       dg += dgc;
     }
@@ -949,7 +956,7 @@ __global__ __launch_bounds__(256) void carry_finish_kernel(
     const float tz = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
     const float tg = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
     if (dZin && !zcol) dZin[b] = tz;
-    if (dgamma && !gvec) unsafeAtomicAdd(dgamma, tg);
+    if (dgamma && !gvec) dgamma[b] = tg;  // partial row b
   }
 }
 
@@ -1120,6 +1127,43 @@ __global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ P
   }
 }
 
+// The decay gradient from its partials part[rows][Dp] (Dp = 1, or D with
+// one decay per channel): out[c] (+)= sum over rows, in a fixed order.
+// Dp = 1: one workgroup; thread t adds rows t, t + 256, ... in order, then
+// the waves' sums and the four wave results in a fixed order.  Dp > 1:
+// workgroup = 64 columns, wave w adds rows w, w + 4, ... in order, the four
+// sums meet in LDS.
+__global__ __launch_bounds__(256) void dgamma_reduce_kernel(const float* __restrict__ part,
+                                                            int rows, int Dp,
+                                                            float* __restrict__ out,
+                                                            int accumulate) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (Dp == 1) {
+    float t = 0.f;
+#pragma unroll 8
+    for (int r = threadIdx.x; r < rows; r += 256) t += part[r];
+    t = wave_sum(t);
+    if (lane == 0) red[wave][0] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const float v = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
+      out[0] = accumulate ? out[0] + v : v;
+    }
+    return;
+  }
+  const int c = blockIdx.x * 64 + lane;
+  float t = 0.f;
+  if (c < Dp)
+    for (int r = wave; r < rows; r += 4) t += part[(int64_t)r * Dp + c];
+  red[wave][lane] = t;
+  __syncthreads();
+  if (wave == 0 && c < Dp) {
+    const float v = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+    out[c] = accumulate ? out[c] + v : v;
+  }
+}
+
 __global__ void zero_two_kernel(float* a, int64_t na, float* b, int64_t nb) {
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < na + nb;
        k += (int64_t)gridDim.x * blockDim.x) {
@@ -1262,32 +1306,49 @@ hipError_t scan_bwd_run(const float* dM, int nq, const float* M, float* dS, floa
   return hipGetLastError();
 }
 
+// The long path in its steps (mem_fused false), each one launch sequence:
+// mem_fwd_proj the W_m product before the scans (one decay: Q = St W_m as
+// split-K partials, *nq slices) or after them (one decay per channel:
+// P = M W_m), mem_fwd_scan the two scan passes.
+hipError_t mem_fwd_proj(DType dt, const void* St, const void* Wm, const void* Mt, float* P,
+                        float* part, int B, int nb, int D, bool per_channel, int* nq,
+                        hipStream_t s) {
+  *nq = 0;
+  if (!per_channel) {
+    GemmDesc g{B * nb, D, D, St, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+    return gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK, nq, s);
+  }
+  GemmDesc g{B * nb, D, D, Mt, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
+  return gemm_splitk(dt, g, part, P, nullptr, nullptr, D, D, false, kMemMinK, s);
+}
+
+hipError_t mem_fwd_scan(DType dt, const float* S, float* M, void* Mt, float* P, float* part, int nq,
+                        int B, int nb, int D, float gamma, const Carry& c, hipStream_t s) {
+  const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
+  float* agg = part + 2 * (int64_t)sp * B * nb * D;
+  const float* Qp = c.gvec ? nullptr : part;
+  float* Pout = c.gvec ? nullptr : P;
+  if (dt == DType::BF16)
+    return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, agg,
+                              s);
+  return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, agg,
+                             s);
+}
+
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s) {
   if (!mem_fused(nb, c.gvec != nullptr)) {
-    const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
-    float* agg = part + 2 * (int64_t)sp * B * nb * D;
-    if (!c.gvec) {
-      // Q = St W_m as split-K partial products, then one scan of S and Q
-      // gives M and P = M W_m (the decayed sum is linear).
-      GemmDesc g{B * nb, D, D, St, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-      int nq = 0;
-      hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false,
-                                         kMemMinK, &nq, s);
-      if (e != hipSuccess) return e;
-      if (dt == DType::BF16)
-        return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, part, nq, P, agg, s);
-      return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, part, nq, P, agg, s);
-    }
-    // One decay per channel: W_m mixes channels, so the scan of S comes
-    // first and P = M W_m is a matrix product of the memory.
-    hipError_t e = dt == DType::BF16
-        ? scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, nullptr, 0, nullptr, agg, s)
-        : scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, nullptr, 0, nullptr, agg, s);
-    if (e != hipSuccess) return e;
-    GemmDesc g{B * nb, D, D, Mt, D, false, {Wm, nullptr, nullptr}, D, true, kSegNone, 0, 1};
-    return gemm_splitk(dt, g, part, P, nullptr, nullptr, D, D, false, kMemMinK, s);
+    // One decay: Q = St W_m, then one scan of S and Q gives M and P = M W_m
+    // (the decayed sum is linear).  One decay per channel: W_m mixes
+    // channels, so the scan of S comes first and P = M W_m is a product.
+    int nq = 0;
+    const bool pc = c.gvec != nullptr;
+    hipError_t e = hipSuccess;
+    if (!pc) e = mem_fwd_proj(dt, St, Wm, Mt, P, part, B, nb, D, false, &nq, s);
+    if (e == hipSuccess) e = mem_fwd_scan(dt, S, M, Mt, P, part, nq, B, nb, D, gamma, c, s);
+    if (e == hipSuccess && pc) e = mem_fwd_proj(dt, St, Wm, Mt, P, part, B, nb, D, true, &nq, s);
+    return e;
   }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   const int es = dt == DType::BF16 ? 2 : 4;
@@ -1315,41 +1376,58 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
                            Pbar_c, nullptr, s);
 }
 
+// The long path's backward steps: mem_bwd_proj dM = dP W_m^T as split-K
+// partials (dP = hi + lo: two products, their slices one after the other;
+// *nq slices in all), mem_bwd_scan the reverse scans, which add them up.
+hipError_t mem_bwd_proj(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
+                        float* part, int B, int nb, int D, int* nq, hipStream_t s) {
+  if (dt != DType::BF16) Pbar_lo = nullptr;
+  const int64_t qs = (int64_t)B * nb * D;
+  GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+  int sp = 0, sp2 = 0;
+  *nq = 0;
+  hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK,
+                                     &sp, s);
+  if (e != hipSuccess) return e;
+  if (Pbar_lo) {
+    g.A = Pbar_lo;
+    float* lo = part + sp * qs;
+    e = gemm_splitk_product(dt, g, lo, lo, nullptr, nullptr, D, D, false, kMemMinK, &sp2, s);
+    if (e != hipSuccess) return e;
+  }
+  *nq = sp + sp2;
+  return hipSuccess;
+}
+
+hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, float* part, int nq,
+                        int B, int nb, int D, float gamma, const Carry& c, hipStream_t s) {
+  const int64_t qs = (int64_t)B * nb * D;
+  float* agg = part + 2 * (int64_t)gemm_splitk_splits(B * nb, D, D, kMemMinK) * qs;
+  if (dt == DType::BF16)
+    return scan_bwd_run<bf16>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, agg, s);
+  return scan_bwd_run<float>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, agg, s);
+}
+
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
-                   const float* M, float* dS, float* dgamma, float* dM, float* part, int B, int nb,
+                   const float* M, float* dS, float* dgpart, float* dM, float* part, int B, int nb,
                    int D, float gamma, const Carry& c, hipStream_t s) {
   if (dt != DType::BF16) Pbar_lo = nullptr;
   (void)dM;
   if (!mem_fused(nb, c.gvec != nullptr)) {
-    // dM = dP W_m^T as split-K partial products (dP = hi + lo: two
-    // products, their slices one after the other), added up by the reverse
-    // scans.
-    const int64_t qs = (int64_t)B * nb * D;
-    GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
-    int sp = 0, sp2 = 0;
-    hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK,
-                                       &sp, s);
+    int nq = 0;
+    hipError_t e = mem_bwd_proj(dt, Pbar, Pbar_lo, Wm, part, B, nb, D, &nq, s);
     if (e != hipSuccess) return e;
-    if (Pbar_lo) {
-      g.A = Pbar_lo;
-      float* lo = part + sp * qs;
-      e = gemm_splitk_product(dt, g, lo, lo, nullptr, nullptr, D, D, false, kMemMinK, &sp2, s);
-      if (e != hipSuccess) return e;
-    }
-    float* agg = part + 2 * (int64_t)gemm_splitk_splits(B * nb, D, D, kMemMinK) * qs;
-    if (dt == DType::BF16)
-      return scan_bwd_run<bf16>(part, sp + sp2, M, dS, dgamma, B, nb, D, gamma, c, agg, s);
-    return scan_bwd_run<float>(part, sp + sp2, M, dS, dgamma, B, nb, D, gamma, c, agg, s);
+    return mem_bwd_scan(dt, M, dS, dgpart, part, nq, B, nb, D, gamma, c, s);
   }
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
                        (const bf16*)Pbar, (const bf16*)Pbar_lo, (const bf16*)Wm, nullptr, nullptr,
-                       nullptr, nullptr, M, dS, dgamma, nb, D, gamma, 0, c);
+                       nullptr, nullptr, M, dS, dgpart, nb, D, gamma, 0, c);
   else
     hipLaunchKernelGGL((memscan_kernel<float, false>), grid, dim3(kMsWaves * 64), 0, s,
                        (const float*)Pbar, (const float*)nullptr, (const float*)Wm, nullptr,
-                       nullptr, nullptr, nullptr, M, dS, dgamma, nb, D, gamma, 0, c);
+                       nullptr, nullptr, nullptr, M, dS, dgpart, nb, D, gamma, 0, c);
   return hipGetLastError();
 }
 
@@ -1433,6 +1511,21 @@ hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;
   hipLaunchKernelGGL(zero_two_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, na, b, nb);
+  return hipGetLastError();
+}
+
+int dg_part_rows(int B, int nb, int D, bool per_channel) {
+  if (mem_fused(nb, per_channel))
+    return per_channel ? B : ((D + kMsCols - 1) / kMsCols) * B;
+  const int nch = scan_chunks(nb);
+  return per_channel ? B * nch : ((D + kScCols - 1) / kScCols) * B * nch;
+}
+
+hipError_t dgamma_reduce(const float* part, int rows, int Dp, float* out, bool accumulate,
+                         hipStream_t s) {
+  if (!out) return hipSuccess;
+  hipLaunchKernelGGL(dgamma_reduce_kernel, dim3(Dp == 1 ? 1 : (Dp + 63) / 64), dim3(256), 0, s,
+                     part, rows, Dp, out, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 
