@@ -88,7 +88,7 @@ __device__ __forceinline__ bf16x8 ecol8(const bf16* t, int us, int j, int lane) 
 
 // GRAD false: part[2 (row nrange + range)] = (max z, sum exp(z - max)) over
 // the range's columns below V (natural units; a range without such columns
-// gives (-1e30 / ln 2, 0)).  GRAD true: G[row][v] for the range's columns
+// gives (-1e30, 0)).  GRAD true: G[row][v] for the range's columns
 // (zero for v >= V) and dfp[range][row][0..127] = sum over the range of
 // g[row][v] E[v][:].  Rows at or beyond `rows` are computed on zeros and
 // never stored.
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(kHThreads, 2) void head_kernel(
                       : bf16x8{};
     if constexpr (GRAD) {
       const int rc = ok ? row : 0;
-      lse2[nq] = lse[rc] * kHL2e;
+      lse2[nq] = lse[rc] * kHL2e - log2f(inv_n);  // exp2(z log2 e - lse2) = e^(z - lse) / n
       tk[nq] = min(max(tgt[rc], 0), V - 1);
     }
   }
@@ -181,56 +181,74 @@ __global__ __launch_bounds__(kHThreads, 2) void head_kernel(
             s[nq][k0 + u] = mma16(kf[u][ds], qf[nq][ds], s[nq][k0 + u]);
     }
     const int vb = v0 + 16 * lg;
+    // Only the last tile of the vocabulary has columns at or beyond V: the
+    // others skip the mask (wave-uniform).
+    const bool masked = v0 + kHVt > V;
+    if (masked) {
+#pragma unroll
+      for (int nq = 0; nq < 2; ++nq)
+#pragma unroll
+        for (int ku = 0; ku < 4; ++ku)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (vb + 4 * ku + r >= V) s[nq][ku][r] = -INFINITY;
+    }
 
     if constexpr (!GRAD) {
+      // m: running max of the raw logits; l: sum of exp(z - m), taken as
+      // exp2(z log2 e - m log2 e) with the scaling folded into one fma
 #pragma unroll
       for (int nq = 0; nq < 2; ++nq) {
         float mx = m[nq];
 #pragma unroll
         for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float z = vb + 4 * ku + r < V ? s[nq][ku][r] * kHL2e : -INFINITY;
-            s[nq][ku][r] = z;
-            mx = fmaxf(mx, z);
-          }
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nq][ku][r]);
+        const float c = mx * kHL2e;
         float ps = 0.f;
 #pragma unroll
         for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) ps += exp2_fast(s[nq][ku][r] - mx);
-        l[nq] = l[nq] * exp2_fast(m[nq] - mx) + ps;
+          for (int r = 0; r < 4; ++r) ps += exp2_fast(fmaf(s[nq][ku][r], kHL2e, -c));
+        // (the difference first: m may be the -1e30 start value, whose
+        // product with log2 e would not cancel exactly against c)
+        l[nq] = fmaf(l[nq], exp2_fast((m[nq] - mx) * kHL2e), ps);
         m[nq] = mx;
       }
     } else {
+      // g = exp(z - lse) / n - [v == target] / n, with 1/n folded into the
+      // exponent; the target's correction only where a row's target falls
+      // in this lane's 16 columns.  The bf16 values serve as G and as the
+      // df instruction's B operand (K step us = columns 16 lg + 8 us + 0..7).
+      bf16x8 pf[2][2];
 #pragma unroll
       for (int nq = 0; nq < 2; ++nq) {
-        const int row = r0 + nq * 16 + lr;
         float g[16];
 #pragma unroll
         for (int ku = 0; ku < 4; ++ku)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int v = vb + 4 * ku + r;
-            float p = v < V ? exp2_fast(fmaf(s[nq][ku][r], kHL2e, -lse2[nq])) : 0.f;
-            if (v == tk[nq]) p -= 1.f;
-            p *= inv_n;
-            s[nq][ku][r] = p;
-            g[4 * ku + r] = p;
-          }
+          for (int r = 0; r < 4; ++r)
+            g[4 * ku + r] = exp2_fast(fmaf(s[nq][ku][r], kHL2e, -lse2[nq]));
+        const int e = tk[nq] - vb;
+        if (e >= 0 && e < 16) {
+#pragma unroll
+          for (int k = 0; k < 16; ++k)
+            if (k == e) g[k] -= inv_n;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          pf[nq][0][k] = (bf16)g[k];
+          pf[nq][1][k] = (bf16)g[8 + k];
+        }
+        const int row = r0 + nq * 16 + lr;
         if (row < rows) {
           bf16* gp = G + (int64_t)row * ldg + vb;
-          st8(gp, *reinterpret_cast<const float(*)[8]>(g));
-          st8(gp + 8, *reinterpret_cast<const float(*)[8]>(g + 8));
+          *reinterpret_cast<bf16x8*>(gp) = pf[nq][0];
+          *reinterpret_cast<bf16x8*>(gp + 8) = pf[nq][1];
         }
       }
       // df += g E: A = E^T (feature rows, vocabulary in the logits' order),
-      // B = g rounded to bf16, as stored; E^T fragments four at a time
-      bf16x8 pf[2][2];
-#pragma unroll
-      for (int nq = 0; nq < 2; ++nq)
-#pragma unroll
-        for (int us = 0; us < 2; ++us) pf[nq][us] = frag_from<bf16>(s[nq][2 * us], s[nq][2 * us + 1]);
+      // B = g as stored; E^T fragments four at a time
 #pragma unroll
       for (int us = 0; us < 2; ++us)
 #pragma unroll
@@ -255,13 +273,13 @@ __global__ __launch_bounds__(kHThreads, 2) void head_kernel(
     for (int nq = 0; nq < 2; ++nq) {
       float mt = fmaxf(m[nq], __shfl_xor(m[nq], 16, 64));
       mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      float lt = l[nq] * exp2_fast(m[nq] - mt);
+      float lt = l[nq] * exp2_fast((m[nq] - mt) * kHL2e);
       lt += __shfl_xor(lt, 16, 64);
       lt += __shfl_xor(lt, 32, 64);
       const int row = r0 + nq * 16 + lr;
       if (lg == 0 && row < rows) {
         float* q = part + 2 * ((int64_t)row * nrange + range);
-        q[0] = mt / kHL2e;
+        q[0] = mt;
         q[1] = lt;
       }
     }
