@@ -656,6 +656,10 @@ def main():
                     help="for rocprofv3: a 256 MiB calibration copy, then steps with the "
                          "library's stage tracing on (every stage serialised on one stream, "
                          "as in the per-stage pass of the normal run)")
+    ap.add_argument("--shape", default=None,
+                    help="with --profile-run: B,T,D,H,L of the layer to profile instead of the "
+                         "measured workload (e.g. 16,65536,1024,16,32 for the memory path's "
+                         "stress shape)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -727,6 +731,11 @@ def main():
                 dcout = dcin
         return step, (runs, grads)
 
+    if args.shape:
+        if not args.profile_run:
+            print("bench.py: --shape needs --profile-run", file=sys.stderr)
+            sys.exit(2)
+        B, T, D, H, L = (int(v) for v in args.shape.split(","))
     step, keep = make_step(B, T, D, H, L, w["gamma"])
     # The GPU's clocks settle after some tens of milliseconds of load: steps
     # for 0.25 s of wall time first, then the requested warm-up steps.
@@ -752,7 +761,8 @@ def main():
         torch.cuda.synchronize()
         abi.bcmt_trace_read()
         abi.bcmt_trace_enable(False)
-        print(json.dumps({"profile_run": True, "steps": args.steps, "calibration_copy_bytes": 256 << 20}))
+        print(json.dumps({"profile_run": True, "steps": args.steps, "shape": [B, T, D, H, L],
+                          "calibration_copy_bytes": 256 << 20}))
         return
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()

@@ -43,14 +43,14 @@ constexpr int kMaxD = 2048;
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Minimum K per split of the D x D weight-gradient products on the side
-// stream: about 144 workgroups in all, which leaves CUs to the critical
-// path beside them (at D = 768, 36 output tiles: 2048-deep splits, 4 of
-// them; the step took 322 us against 326 us with 13 splits and 329 us with
-// 8; 2 splits took 351 us), and at least 128 deep (D = 128: one tile, 128
-// splits).
+// stream: about 288 workgroups in all, and at least 128 deep (D = 128: one
+// tile, 128 splits).  Same-box A/B against 144 workgroups: B = 2, T = 65536,
+// D = 1024 (64 tiles, 4 splits instead of 2) took dW_o and dW_g from 830 to
+// 430 us each and the step from 6.29 to 6.12-6.24 ms; B = 8, T = 1024,
+// D = 768 (8 splits instead of 4) 299.3 -> 298.4-298.9 us.
 int dd_min_k(int D, int K) {
   const int64_t tiles = (int64_t)((D + 127) / 128) * ((D + 127) / 128);
-  const int mk = (int)((K * tiles / 144 + 63) / 64 * 64);
+  const int mk = (int)((K * tiles / 288 + 63) / 64 * 64);
   return mk < 128 ? 128 : mk;
 }
 // The same for dW_{q,k,v}: splits at least 128 deep (4 at D = 768, where
