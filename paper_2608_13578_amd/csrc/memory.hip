@@ -472,133 +472,107 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
 
 // ------------------------------------------------------------------ long scans
 // For many blocks the memory path runs as two pieces: the W_m products as
-// ordinary split-K matrix products, and the decayed scans below, parallel
-// over blocks (memscan_kernel walks all blocks of a sequence inside one
-// workgroup, which serialises a long sequence).
+// ordinary split-K matrix products, and the decayed scans below
+// (memscan_kernel walks all blocks of a sequence through one matrix-core
+// pass per 16 blocks, which serialises a long sequence).
 //
-// A scan runs as two launches over the same grid: workgroup = (64
-// columns, sequence, chunk of kScChunkRows blocks), four waves of 16 blocks
-// each, one column per lane (256-byte rows of float32).  The first launch
-// (LOCAL) scans each chunk from a zero carry and writes the chunk's
-// aggregate per column; the second (APPLY) folds the aggregates of the
-// chunks before it (after it, for the reverse scan) into its carry, scans
-// its chunk again from that carry and writes the results.  Within a chunk
-// the four waves meet in LDS the same way.  With the recurrence
-// x_i = g x_{i-1} + y_i, a value is its local one plus g^(distance) times
-// the carry.  The first chunk starts from the state of the earlier blocks
-// (zero for a whole sequence).
-constexpr int kScCols = 64, kScWaves = 4, kScRows = 16, kScChunkRows = kScWaves * kScRows;
+// A scan is one launch over (64 columns, sequence): the workgroup owns its
+// columns of the whole sequence, so no other workgroup's result is ever
+// waited for, and every input is read once.  It walks the sequence in
+// super-chunks of 128 blocks: each of its 8 waves scans 16 consecutive
+// blocks of the super-chunk from a zero state (one lane per column, 256
+// bytes per row of float32), the waves' aggregates meet in LDS, and each
+// wave adds to its blocks the state entering its first block, decayed:
+// with x_i = g x_{i-1} + y_i, a value is its local one plus g^(distance)
+// times the carry.  The state leaving the super-chunk (the same sum, formed
+// by every wave in the same order) enters the next one.  The first
+// super-chunk starts from the state of the earlier blocks (zero for a
+// whole sequence).
+constexpr int kScCols = 64, kScWaves = 8, kScRows = 16, kScSuper = kScWaves * kScRows;
+// The reverse scan: 16 waves of 8 blocks (more loads in flight per
+// workgroup; its registers allow it, the forward's stores do not).
+constexpr int kSbWaves = 16, kSbRows = 8, kSbSuper = kSbWaves * kSbRows;
 // Up to this many blocks per sequence the fused kernel runs; beyond it, the
 // scans above plus split-K matrix products (each split at least kMemMinK deep).
 constexpr int kMemFusedMaxBlocks = 32, kMemMinK = 256;
 
-__device__ __forceinline__ float pow16(float g) {
-  float g2 = g * g, g4 = g2 * g2, g8 = g4 * g4;
-  return g8 * g8;
+// g^K for K a power of two: the decay across one wave's K blocks.
+template <int K>
+__device__ __forceinline__ float pow2k(float g) {
+  static_assert(K >= 1 && (K & (K - 1)) == 0, "power of two");
+#pragma unroll
+  for (int k = 1; k < K; k *= 2) g *= g;
+  return g;
 }
-
-int scan_chunks(int nb) { return (nb + kScChunkRows - 1) / kScChunkRows; }
 
 // Forward: M = N / Z with N_i = g N_{i-1} + S_i (float32 and compute type).
 // With Qp (one decay for all channels) also the projected summaries
 // Q = S W_m, given as nq split-K partial products (stride qstride, added in
-// order): NP_i = g NP_{i-1} + Q_i and P = NP / Z = M W_m.  aggN / aggP hold
-// the chunk aggregates, [B, nch, D].
-template <typename T, bool APPLY>
+// order): NP_i = g NP_{i-1} + Q_i and P = NP / Z = M W_m.
+template <typename T>
 __global__ __launch_bounds__(kScCols * kScWaves) void scan_fwd_kernel(
     const float* __restrict__ S, float* __restrict__ M, T* __restrict__ Mt, int nb, int D,
     float gamma, Carry cr, const float* __restrict__ Qp, int nq, int64_t qstride,
-    float* __restrict__ P, float* __restrict__ aggN, float* __restrict__ aggP) {
+    float* __restrict__ P) {
   __shared__ float wn[kScWaves][kScCols], wp[kScWaves][kScCols];
   const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
-  const int b = blockIdx.y, ch = blockIdx.z, nch = gridDim.z;
+  const int b = blockIdx.y;
   const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
-  const float g16 = pow16(gam);
-  const int a = ch * kScChunkRows + w * kScRows;  // this wave's first block
-  float v[kScRows], q[kScRows];
-  const int64_t off0 = ((int64_t)b * nb + a) * D + col;
+  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+  const float gw = pow2k<kScRows>(gam);  // across one wave's blocks
+  const float zin = !cr.Zin ? 0.f
+                    : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
+  // the state entering the current super-chunk
+  float sn = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;
+  float sp = on && Qp && cr.Nin ? cr.Pc[(int64_t)b * D + col] * zin : 0.f;
+  const int64_t cbase = (int64_t)b * nb * D + col;
+  for (int s0 = 0; s0 < nb; s0 += kScSuper) {
+    const int a = s0 + w * kScRows;  // this wave's first block
+    const int64_t off0 = cbase + (int64_t)a * D;
+    float v[kScRows], q[kScRows];
 #pragma unroll
-  for (int r = 0; r < kScRows; ++r) {
-    v[r] = on && a + r < nb ? S[off0 + (int64_t)r * D] : 0.f;
-    q[r] = 0.f;
-  }
-  // the partial products one slice at a time, every row's load in flight
-  for (int z = 0; Qp && z < nq; ++z) {
-    float t[kScRows];
-#pragma unroll
-    for (int r = 0; r < kScRows; ++r)
-      t[r] = on && a + r < nb ? Qp[z * qstride + off0 + (int64_t)r * D] : 0.f;
-#pragma unroll
-    for (int r = 0; r < kScRows; ++r) q[r] += t[r];
-  }
-  if constexpr (!APPLY) {
-    // the summed products replace the first slice: the second pass reads one
-    if (Qp && nq > 1) {
+    for (int r = 0; r < kScRows; ++r) {
+      v[r] = on && a + r < nb ? S[off0 + (int64_t)r * D] : 0.f;
+      q[r] = 0.f;
+    }
+    // the partial products one slice at a time, every row's load in flight
+    for (int z = 0; Qp && z < nq; ++z) {
+      float t[kScRows];
 #pragma unroll
       for (int r = 0; r < kScRows; ++r)
-        if (on && a + r < nb) const_cast<float*>(Qp)[off0 + (int64_t)r * D] = q[r];
-    }
-  }
-  float n = 0.f, np = 0.f;
+        t[r] = on && a + r < nb ? Qp[z * qstride + off0 + (int64_t)r * D] : 0.f;
 #pragma unroll
-  for (int r = 0; r < kScRows; ++r) {
-    n = gam * n + v[r];
-    np = gam * np + q[r];
-    v[r] = n;
-    q[r] = np;
-  }
-  wn[w][c] = n;
-  wp[w][c] = np;
-  __syncthreads();
-  const int64_t arow = ((int64_t)b * nch + ch) * D + col;
-  if constexpr (!APPLY) {
-    if (w == 0 && on) {
-      float an = 0.f, ap = 0.f;
-      for (int j = 0; j < kScWaves; ++j) {
-        an = g16 * an + wn[j][c];
-        ap = g16 * ap + wp[j][c];
-      }
-      aggN[arow] = an;
-      aggP[arow] = ap;
+      for (int r = 0; r < kScRows; ++r) q[r] += t[r];
     }
-    return;
-  } else {
-    const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
-    const float zin = !cr.Zin ? 0.f
-                      : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
-    // the state before this chunk: the earlier blocks', then every chunk before
-    float cn = on && cr.Nin ? cr.Nin[(int64_t)b * D + col] : 0.f;
-    float cp = on && Qp && cr.Nin ? cr.Pc[(int64_t)b * D + col] * zin : 0.f;
-    const float g64 = g16 * g16 * g16 * g16;
-    for (int j0 = 0; j0 < ch && on; j0 += 8) {  // eight chunks' loads at a time
-      float tn[8], tp[8];
+    float n = 0.f, np = 0.f;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int64_t ar = ((int64_t)b * nch + j0 + u) * D + col;
-        tn[u] = j0 + u < ch ? aggN[ar] : 0.f;
-        tp[u] = j0 + u < ch ? aggP[ar] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (j0 + u < ch) {
-          cn = g64 * cn + tn[u];
-          cp = g64 * cp + tp[u];
-        }
-      }
+    for (int r = 0; r < kScRows; ++r) {
+      n = gam * n + v[r];
+      np = gam * np + q[r];
+      v[r] = n;
+      q[r] = np;
     }
-    for (int j = 0; j < w; ++j) {  // then the waves before this one
-      cn = g16 * cn + wn[j][c];
-      cp = g16 * cp + wp[j][c];
+    wn[w][c] = n;
+    wp[w][c] = np;
+    __syncthreads();
+    // the state entering this wave's first block: the super-chunk's, then
+    // the waves before this one
+    float cn = sn, cp = sp;
+    for (int j = 0; j < w; ++j) {
+      cn = gw * cn + wn[j][c];
+      cp = gw * cp + wp[j][c];
     }
     float f = gam;
+    float zz = zsum(a, gam, lg2, zin);  // the normaliser, then its recurrence
 #pragma unroll
     for (int r = 0; r < kScRows; ++r) {
       const int i = a + r;
+      const float rz = 1.f / zz;
+      zz = gam * zz + 1.f;
       if (on && i < nb) {
         const float nn = v[r] + f * cn;
-        const float rz = 1.f / zsum(i, gam, lg2, zin);
         const float m = nn * rz;
         const int64_t off = off0 + (int64_t)r * D;
         M[off] = m;
@@ -608,12 +582,19 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_fwd_kernel(
       }
       f *= gam;
     }
-    if (cr.Zout && ch == 0 && w == 0) {
-      if (cr.zcol) {
-        if (on) cr.Zout[(int64_t)b * D + col] = zsum(nb - 1, gam, lg2, zin);
-      } else if (blockIdx.x == 0 && c == 0) {
-        cr.Zout[b] = zsum(nb - 1, gam, lg2, zin);
-      }
+    // the state leaving the super-chunk (only read when another follows,
+    // which is then a whole one): every wave forms it in the same order
+    for (int j = 0; j < kScWaves; ++j) {
+      sn = gw * sn + wn[j][c];
+      sp = gw * sp + wp[j][c];
+    }
+    __syncthreads();  // wn / wp are rewritten by the next super-chunk
+  }
+  if (cr.Zout && w == 0) {
+    if (cr.zcol) {
+      if (on) cr.Zout[(int64_t)b * D + col] = zsum(nb - 1, gam, lg2, zin);
+    } else if (blockIdx.x == 0 && c == 0) {
+      cr.Zout[b] = zsum(nb - 1, gam, lg2, zin);
     }
   }
 }
@@ -621,126 +602,91 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_fwd_kernel(
 // Reverse scans of the memory backward from dM (nq split-K partial products,
 // stride qstride, added in order) and M:
 //   Qs_i = dM_i / Z_i + g Qs_{i+1} (= dS_i),  E_i = -dM_i . M_i / Z_i + g E_{i+1},
-//   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one partial per workgroup).
-// The gradients of a chunk's final state enter at the last block; E of the
-// first block goes to cr.e0.  aggQ / aggE: the chunk aggregates (each
-// chunk's values at its first block, from a zero carry).
-template <typename T, bool APPLY>
-__global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
+//   dg = sum_{i>=1} Qs_i M_{i-1} Z_{i-1} + E_i Z_{i-1}   (one partial per workgroup;
+//   per column with one decay per channel).
+// Super-chunks from the last to the first; within one, the state entering a
+// wave's last block comes from the later waves.  The gradients of a chunk's
+// final state enter at the last block; E of the first block goes to cr.e0.
+template <typename T>
+__global__ __launch_bounds__(kScCols * kSbWaves) void scan_bwd_kernel(
     const float* __restrict__ dM, int nq, int64_t qstride, const float* __restrict__ M,
-    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, Carry cr,
-    float* __restrict__ aggQ, float* __restrict__ aggE) {
-  __shared__ float wq[kScWaves][kScCols], we[kScWaves][kScCols];
-  __shared__ float red[kScWaves];
+    float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, Carry cr) {
+  __shared__ float wq[kSbWaves][kScCols], we[kSbWaves][kScCols];
+  __shared__ float red[kSbWaves];
   const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
   const int col = blockIdx.x * kScCols + c;
   const bool on = col < D;
-  const int b = blockIdx.y, ch = blockIdx.z, nch = gridDim.z;
+  const int b = blockIdx.y;
   const float gam = (on && cr.gvec) ? cr.gvec[col] : gamma;  // this column's decay
   const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
-  const float g16 = pow16(gam);
+  const float gw = pow2k<kSbRows>(gam);  // across one wave's blocks
   const float zin = !cr.Zin ? 0.f
                     : (!cr.zcol ? cr.Zin[b] : (on ? cr.Zin[(int64_t)b * D + col] : 0.f));
-  const int a = ch * kScChunkRows + w * kScRows;
-  const int64_t off0 = ((int64_t)b * nb + a) * D + col;
-  float x[kScRows], y[kScRows];
+  const int64_t cbase = (int64_t)b * nb * D + col;
+  float sq = 0.f, se = 0.f;  // the state entering the current super-chunk from later blocks
+  float dg = 0.f;
+  for (int s0 = ((nb - 1) / kSbSuper) * kSbSuper; s0 >= 0; s0 -= kSbSuper) {
+    const int a = s0 + w * kSbRows;
+    const int64_t off0 = cbase + (int64_t)a * D;
+    float x[kSbRows], y[kSbRows];
 #pragma unroll
-  for (int r = 0; r < kScRows; ++r) x[r] = 0.f;
-  for (int z = 0; z < nq; ++z) {
-    float t[kScRows];
+    for (int r = 0; r < kSbRows; ++r) x[r] = 0.f;
+    for (int z = 0; z < nq; z += 2) {  // two slices' loads in flight at a time
+      float t[kSbRows], u[kSbRows];
+      const bool two = z + 1 < nq;
 #pragma unroll
-    for (int r = 0; r < kScRows; ++r)
-      t[r] = on && a + r < nb ? dM[z * qstride + off0 + (int64_t)r * D] : 0.f;
-#pragma unroll
-    for (int r = 0; r < kScRows; ++r) x[r] += t[r];
-  }
-  if constexpr (!APPLY) {
-    // the summed products replace the first slice: the second pass reads one
-    if (nq > 1) {
-#pragma unroll
-      for (int r = 0; r < kScRows; ++r)
-        if (on && a + r < nb) const_cast<float*>(dM)[off0 + (int64_t)r * D] = x[r];
-    }
-  }
-  float mm[kScRows];
-#pragma unroll
-  for (int r = 0; r < kScRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
-  // the memory of the block before this wave's first (its decay term)
-  const float mprev = APPLY && on && a >= 1 && a < nb ? M[off0 - D] : 0.f;
-#pragma unroll
-  for (int r = 0; r < kScRows; ++r) {
-    const int i = a + r;
-    const bool ok = on && i < nb;
-    const float m = mm[r];
-    const float rz = 1.f / zsum(i, gam, lg2, zin);
-    const float dm = x[r];
-    x[r] = dm * rz;
-    y[r] = -dm * m * rz;
-    if (ok && i == nb - 1) {
-      if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
-      if (cr.dZout) {
-        if (cr.zcol) y[r] += cr.dZout[(int64_t)b * D + col];
-        else if (col == 0) y[r] += cr.dZout[b];
-      }
-    }
-  }
-  float qq = 0.f, e = 0.f;
-#pragma unroll
-  for (int r = kScRows - 1; r >= 0; --r) {
-    qq = x[r] + gam * qq;
-    e = y[r] + gam * e;
-    x[r] = qq;
-    y[r] = e;
-  }
-  wq[w][c] = qq;
-  we[w][c] = e;
-  __syncthreads();
-  const int64_t arow = ((int64_t)b * nch + ch) * D + col;
-  if constexpr (!APPLY) {
-    if (w == 0 && on) {
-      float aq = 0.f, ae = 0.f;
-      for (int j = kScWaves - 1; j >= 0; --j) {
-        aq = wq[j][c] + g16 * aq;
-        ae = we[j][c] + g16 * ae;
-      }
-      aggQ[arow] = aq;
-      aggE[arow] = ae;
-    }
-    return;
-  } else {
-    // the carry entering this wave's last block: every later chunk (the
-    // last one may be short), then the later waves of this chunk
-    float iq = 0.f, ie = 0.f;
-    const float g64 = g16 * g16 * g16 * g16;
-    for (int j0 = nch - 1; j0 > ch && on; j0 -= 8) {  // eight chunks' loads at a time
-      float tq[8], te[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 - u;
-        const int64_t ar = ((int64_t)b * nch + j) * D + col;
-        tq[u] = j > ch ? aggQ[ar] : 0.f;
-        te[u] = j > ch ? aggE[ar] : 0.f;
+      for (int r = 0; r < kSbRows; ++r) {
+        t[r] = on && a + r < nb ? dM[z * qstride + off0 + (int64_t)r * D] : 0.f;
+        u[r] = two && on && a + r < nb ? dM[(z + 1) * qstride + off0 + (int64_t)r * D] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 - u;
-        if (j > ch) {
-          // the last chunk may be short: g^(its length)
-          const int len = min(kScChunkRows, nb - j * kScChunkRows);
-          const float gl = len == kScChunkRows ? g64 : powf(gam, (float)len);
-          iq = tq[u] + gl * iq;
-          ie = te[u] + gl * ie;
+      for (int r = 0; r < kSbRows; ++r) {
+        x[r] += t[r];
+        x[r] += u[r];
+      }
+    }
+    float mm[kSbRows];
+#pragma unroll
+    for (int r = 0; r < kSbRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
+    // the memory of the block before this wave's first (its decay term)
+    const float mprev = on && a >= 1 && a < nb ? M[off0 - D] : 0.f;
+#pragma unroll
+    for (int r = 0; r < kSbRows; ++r) {
+      const int i = a + r;
+      const bool ok = on && i < nb;
+      const float rz = 1.f / zsum(i, gam, lg2, zin);
+      const float dm = x[r];
+      x[r] = dm * rz;
+      y[r] = -dm * mm[r] * rz;
+      if (ok && i == nb - 1) {
+        if (cr.dNout) x[r] += cr.dNout[(int64_t)b * D + col];
+        if (cr.dZout) {
+          if (cr.zcol) y[r] += cr.dZout[(int64_t)b * D + col];
+          else if (col == 0) y[r] += cr.dZout[b];
         }
       }
     }
-    for (int j = kScWaves - 1; j > w; --j) {
-      iq = wq[j][c] + g16 * iq;
-      ie = we[j][c] + g16 * ie;
+    float qq = 0.f, e = 0.f;
+#pragma unroll
+    for (int r = kSbRows - 1; r >= 0; --r) {
+      qq = x[r] + gam * qq;
+      e = y[r] + gam * e;
+      x[r] = qq;
+      y[r] = e;
     }
-    float dg = 0.f;
+    wq[w][c] = qq;
+    we[w][c] = e;
+    __syncthreads();
+    // the state entering this wave's last block: the super-chunk's, then
+    // the later waves of this super-chunk
+    float iq = sq, ie = se;
+    for (int j = kSbWaves - 1; j > w; --j) {
+      iq = wq[j][c] + gw * iq;
+      ie = we[j][c] + gw * ie;
+    }
     float f = gam;
 #pragma unroll
-    for (int r = kScRows - 1; r >= 0; --r) {
+    for (int r = kSbRows - 1; r >= 0; --r) {
       const int i = a + r;
       const float qs = x[r] + f * iq, es = y[r] + f * ie;
       f *= gam;
@@ -755,28 +701,32 @@ __global__ __launch_bounds__(kScCols * kScWaves) void scan_bwd_kernel(
         }
       }
     }
-    // the decay gradient as partials (dg_part_rows): per channel, row
-    // ch * B + b, this workgroup's columns; else one value per workgroup
-    const int64_t prow = (int64_t)ch * gridDim.y + b;
-    if (cr.gvec) {  // the column's waves meet in LDS
-      __syncthreads();
-      wq[w][c] = dg;
-      __syncthreads();
-      if (w == 0 && on && dgamma) {
-        float t = 0.f;
-        for (int j = 0; j < kScWaves; ++j) t += wq[j][c];
-        dgamma[prow * D + col] = t;
-      }
-      return;
+    // the state entering the previous super-chunk, the same in every wave
+    for (int j = kSbWaves - 1; j >= 0; --j) {
+      sq = wq[j][c] + gw * sq;
+      se = we[j][c] + gw * se;
     }
-    const float v = wave_sum(dg);
-    if (c == 0) red[w] = v;
+    __syncthreads();  // wq / we are rewritten by the next super-chunk
+  }
+  // the decay gradient as partials (dg_part_rows): per channel, row b, this
+  // workgroup's columns; else one value per workgroup
+  if (cr.gvec) {  // the column's waves meet in LDS, in a fixed order
+    wq[w][c] = dg;
     __syncthreads();
-    if (threadIdx.x == 0 && dgamma) {
+    if (w == 0 && on && dgamma) {
       float t = 0.f;
-      for (int j = 0; j < kScWaves; ++j) t += red[j];
-      dgamma[prow * gridDim.x + blockIdx.x] = t;
+      for (int j = 0; j < kSbWaves; ++j) t += wq[j][c];
+      dgamma[(int64_t)b * D + col] = t;
     }
+    return;
+  }
+  const float v = wave_sum(dg);
+  if (c == 0) red[w] = v;
+  __syncthreads();
+  if (threadIdx.x == 0 && dgamma) {
+    float t = 0.f;
+    for (int j = 0; j < kSbWaves; ++j) t += red[j];
+    dgamma[(int64_t)b * gridDim.x + blockIdx.x] = t;
   }
 }
 
@@ -1270,39 +1220,25 @@ bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !p
 size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
   if (mem_fused(nb, per_channel)) return 0;
   const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
-  // the partial slices, then the scans' two aggregate arrays [B, nch, D]
-  return (2 * (size_t)sp * B * nb + 2 * (size_t)B * scan_chunks(nb)) * D * sizeof(float);
+  return 2 * (size_t)sp * B * nb * D * sizeof(float);
 }
 
-// The two passes of a long scan over grid (columns / 64, B, chunks).
+// One scan launch over grid (columns / 64, B).
 template <typename T>
 hipError_t scan_fwd_run(const float* S, float* M, T* Mt, int B, int nb, int D, float gamma,
-                        const Carry& c, const float* Qp, int nq, float* P, float* agg,
-                        hipStream_t s) {
-  const int nch = scan_chunks(nb);
-  const dim3 grid((D + kScCols - 1) / kScCols, B, nch);
-  const int64_t qs = (int64_t)B * nb * D, as = (int64_t)B * nch * D;
-  hipLaunchKernelGGL((scan_fwd_kernel<T, false>), grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt,
-                     nb, D, gamma, c, Qp, nq, qs, P, agg, agg + as);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((scan_fwd_kernel<T, true>), grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt,
-                     nb, D, gamma, c, Qp, nq > 1 ? 1 : nq, qs, P, agg, agg + as);
+                        const Carry& c, const float* Qp, int nq, float* P, hipStream_t s) {
+  const dim3 grid((D + kScCols - 1) / kScCols, B);
+  hipLaunchKernelGGL(scan_fwd_kernel<T>, grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt, nb, D,
+                     gamma, c, Qp, nq, (int64_t)B * nb * D, P);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t scan_bwd_run(const float* dM, int nq, const float* M, float* dS, float* dgamma, int B,
-                        int nb, int D, float gamma, const Carry& c, float* agg, hipStream_t s) {
-  const int nch = scan_chunks(nb);
-  const dim3 grid((D + kScCols - 1) / kScCols, B, nch);
-  const int64_t qs = (int64_t)B * nb * D, as = (int64_t)B * nch * D;
-  hipLaunchKernelGGL((scan_bwd_kernel<T, false>), grid, dim3(kScCols * kScWaves), 0, s, dM, nq, qs,
-                     M, dS, dgamma, nb, D, gamma, c, agg, agg + as);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((scan_bwd_kernel<T, true>), grid, dim3(kScCols * kScWaves), 0, s, dM,
-                     nq > 1 ? 1 : nq, qs, M, dS, dgamma, nb, D, gamma, c, agg, agg + as);
+                        int nb, int D, float gamma, const Carry& c, hipStream_t s) {
+  const dim3 grid((D + kScCols - 1) / kScCols, B);
+  hipLaunchKernelGGL(scan_bwd_kernel<T>, grid, dim3(kScCols * kSbWaves), 0, s, dM, nq,
+                     (int64_t)B * nb * D, M, dS, dgamma, nb, D, gamma, c);
   return hipGetLastError();
 }
 
@@ -1324,15 +1260,11 @@ hipError_t mem_fwd_proj(DType dt, const void* St, const void* Wm, const void* Mt
 
 hipError_t mem_fwd_scan(DType dt, const float* S, float* M, void* Mt, float* P, float* part, int nq,
                         int B, int nb, int D, float gamma, const Carry& c, hipStream_t s) {
-  const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
-  float* agg = part + 2 * (int64_t)sp * B * nb * D;
   const float* Qp = c.gvec ? nullptr : part;
   float* Pout = c.gvec ? nullptr : P;
   if (dt == DType::BF16)
-    return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, agg,
-                              s);
-  return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, agg,
-                             s);
+    return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, s);
+  return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, s);
 }
 
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
@@ -1401,11 +1333,8 @@ hipError_t mem_bwd_proj(DType dt, const void* Pbar, const void* Pbar_lo, const v
 
 hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, float* part, int nq,
                         int B, int nb, int D, float gamma, const Carry& c, hipStream_t s) {
-  const int64_t qs = (int64_t)B * nb * D;
-  float* agg = part + 2 * (int64_t)gemm_splitk_splits(B * nb, D, D, kMemMinK) * qs;
-  if (dt == DType::BF16)
-    return scan_bwd_run<bf16>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, agg, s);
-  return scan_bwd_run<float>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, agg, s);
+  if (dt == DType::BF16) return scan_bwd_run<bf16>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, s);
+  return scan_bwd_run<float>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, s);
 }
 
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
@@ -1517,8 +1446,7 @@ hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {
 int dg_part_rows(int B, int nb, int D, bool per_channel) {
   if (mem_fused(nb, per_channel))
     return per_channel ? B : ((D + kMsCols - 1) / kMsCols) * B;
-  const int nch = scan_chunks(nb);
-  return per_channel ? B * nch : ((D + kScCols - 1) / kScCols) * B * nch;
+  return per_channel ? B : ((D + kScCols - 1) / kScCols) * B;
 }
 
 hipError_t dgamma_reduce(const float* part, int rows, int Dp, float* out, bool accumulate,
