@@ -118,9 +118,10 @@ struct Plan {
 
     off = 0;
     du = take(BTD * es);
-    pbar = take(BND * es);
-    // bf16: the low part of each shifted context-gradient value (hi + lo)
-    pbar_lo = take(dt == DType::BF16 ? BND * es : 0);
+    // the shifted context gradient; bf16 keeps each value as hi + lo, a row
+    // [hi (D) | lo (D)] (so that one product over 2D takes both)
+    pbar = take(BND * es * (dt == DType::BF16 ? 2 : 1));
+    pbar_lo = pbar + (dt == DType::BF16 ? (size_t)D * es : 0);
     dS = take(BND * 4);
     dM = take(0);  // (the long path's dM stays in split-K partials)
     mpart_b = take(mem_part_bytes(B, nb, D, pc));
@@ -667,8 +668,8 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
                         accum, dd_min_k(D, BT));
         }
         if (gr.dWm) {
-          GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr}, D, true, kSegNone,
-                     0, 1};
+          GemmDesc g{D, D, BN, SV + p.Mt, D, true, {W + p.pbar, nullptr, nullptr},
+                     lo ? 2 * D : D, true, kSegNone, 0, 1};
           LAUNCH_SPLITK(ST_WM_WGRAD, ST_WM_WGRAD_RED, dt, g, wpart, gr.dWm, nullptr, nullptr, D, D,
                         accum, 512);
           if (chunk) {

@@ -1174,6 +1174,12 @@ struct EpiSegOut {
 
 template <typename T, class Epi>
 hipError_t dispatch_any(const GemmDesc& g, const Epi& epi, hipStream_t s) {
+  if (g.seg == kSegK) {  // B split along K (K-contiguous B only): bf16 products
+    if constexpr (sizeof(T) == 2) {
+      if (!g.a_mcontig && !g.b_ncontig) return launch_any<T, false, false, kSegK>(g, epi, s);
+    }
+    return hipErrorInvalidValue;
+  }
   if (g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch_any<T, true, true, kSegNone>(g, epi, s);
   if (!g.a_mcontig && g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, true, kSegNone>(g, epi, s);
   if (!g.a_mcontig && !g.b_ncontig && g.seg == kSegNone) return launch_any<T, false, false, kSegNone>(g, epi, s);
@@ -1202,7 +1208,9 @@ hipError_t gemm_splitk_product(DType dt, const GemmDesc& g0, float* partial, flo
                                int* splits, hipStream_t s) {
   *splits = 0;
   if (g0.M <= 0 || g0.N <= 0) return hipSuccess;
-  if (g0.N % 8 != 0 || seg_len_n % 8 != 0 || g0.seg != kSegNone) return hipErrorInvalidValue;
+  if (g0.N % 8 != 0 || seg_len_n % 8 != 0) return hipErrorInvalidValue;
+  if (g0.seg == kSegN || (g0.seg == kSegK && (g0.b_ncontig || g0.a_mcontig)))
+    return hipErrorInvalidValue;
   GemmDesc g = g0;
   int kc;
   g.splits = splitk_plan(g.M, g.N, g.K, min_k, &kc);

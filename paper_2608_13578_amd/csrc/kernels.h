@@ -210,7 +210,7 @@ hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, flo
 // false), for callers that time them apart: mem_fwd_proj is the W_m
 // product (one decay: Q = St Wm as *nq split-K slices, before the scan; per
 // channel: P = Mt Wm, after it), mem_fwd_scan the two scan passes;
-// mem_bwd_proj the products dM = (Pbar + Pbar_lo) Wm^T (*nq slices),
+// mem_bwd_proj the product dM = [hi | lo] [Wm^T; Wm^T] (*nq slices),
 // mem_bwd_scan the reverse scans.
 hipError_t mem_fwd_proj(DType dt, const void* St, const void* Wm, const void* Mt, float* P,
                         float* part, int B, int nb, int D, bool per_channel, int* nq,
@@ -223,13 +223,16 @@ hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, floa
                         int B, int nb, int D, float gamma, const Carry& c, hipStream_t s);
 // Gate backward; also zeroes zero_a[0..na) and *zero_b (either may be null).
 // With Pc (a chunk after earlier blocks) block 0 uses Mc = Pc[b] and its
-// sum of dY * G goes to Pbar_c [B, D] (compute type).  In bf16 each block sum
-// v is written as hi = bf16(v) to Pbar and lo = bf16(v - hi) to Pbar_lo (and
-// Pbar_c_lo), when those are not null; float32 ignores them.
+// sum of dY * G goes to Pbar_c [B, D] (compute type).  In bf16, with
+// Pbar_lo not null, each block sum v is kept as hi = bf16(v) and lo =
+// bf16(v - hi) in one row [hi (D) | lo (D)] of Pbar (rows 2D apart; Pbar_lo
+// marks that layout and is Pbar + D), and Pbar_c_lo holds the lo part of
+// Pbar_c; float32 ignores them.
 hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, void* dU,
                     void* Pbar, void* Pbar_lo, float* zero_a, int na, float* zero_b, int B, int T,
                     int D, int L, const float* Pc, void* Pbar_c, void* Pbar_c_lo, hipStream_t s);
-// Memory backward: dM = (Pbar + Pbar_lo) Wm^T (Pbar_lo may be null; float32
+// Memory backward: dM = (hi + lo) Wm^T over the rows of Pbar (the layout
+// gate_bwd writes; Pbar_lo null: rows of D values, hi alone; float32
 // ignores it), then the reverse decayed scan: dS and the decay gradient as
 // partials (when dgpart is given): dg_part_rows(B, nb, D, per channel) rows
 // of 1 float (one decay) or D floats (one per channel), every row written.

@@ -11,6 +11,8 @@
 //   N_i = g N_{i-1} + S_i,  Z_i = g Z_{i-1} + 1.
 // One workgroup owns 32 feature columns of one batch element over all
 // blocks, so no workgroup ever waits on another.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -308,7 +310,7 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     const float* __restrict__ S,
     float* __restrict__ M, T* __restrict__ Mt, float* __restrict__ P, const float* __restrict__ Min,
     float* __restrict__ dS, float* __restrict__ dgamma, int nb, int D, float gamma, int kcr,
-    Carry cr) {
+    Carry cr, int lda) {
   typedef typename Frag<T>::type F;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
   T* Bs = reinterpret_cast<T*>(dyn);  // [kcr][kMsCols] (forward only)
@@ -337,7 +339,7 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     const int rt = FWD ? q : nt - 1 - q;
     const int i0 = rt * kMsRows;
     const int arow = i0 + lr;
-    const int64_t arow_off = ((int64_t)b * nb + (arow < nb ? arow : 0)) * D;
+    const int64_t arow_off = ((int64_t)b * nb + (arow < nb ? arow : 0)) * lda;
     const T* ap = A + arow_off;
     f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     for (int kc = 0; kc < D; kc += (FWD ? kcr : D)) {
@@ -650,11 +652,18 @@ __global__ __launch_bounds__(kScCols * kSbWaves) void scan_bwd_kernel(
     for (int r = 0; r < kSbRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
     // the memory of the block before this wave's first (its decay term)
     const float mprev = on && a >= 1 && a < nb ? M[off0 - D] : 0.f;
+    // the normalisers of this wave's blocks: the closed form once, then the
+    // recurrence; and the one before its first block (its decay term)
+    float zs[kSbRows];
+    float zz = zsum(a, gam, lg2, zin);
+    const float zprev = a >= 1 ? zsum(a - 1, gam, lg2, zin) : 0.f;
 #pragma unroll
     for (int r = 0; r < kSbRows; ++r) {
       const int i = a + r;
       const bool ok = on && i < nb;
-      const float rz = 1.f / zsum(i, gam, lg2, zin);
+      zs[r] = zz;
+      const float rz = 1.f / zz;
+      zz = gam * zz + 1.f;
       const float dm = x[r];
       x[r] = dm * rz;
       y[r] = -dm * mm[r] * rz;
@@ -693,7 +702,7 @@ __global__ __launch_bounds__(kScCols * kSbWaves) void scan_bwd_kernel(
       if (on && i < nb) {
         dS[off0 + (int64_t)r * D] = qs;
         if (i >= 1) {
-          const float zp = zsum(i - 1, gam, lg2, zin);
+          const float zp = r > 0 ? zs[r > 0 ? r - 1 : 0] : zprev;
           const float mp = r > 0 ? mm[r > 0 ? r - 1 : 0] : mprev;
           dg += qs * (mp * zp) + es * zp;
         } else if (cr.e0) {
@@ -750,7 +759,7 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
                                                        const float* __restrict__ Pc,
                                                        T* __restrict__ Pbar_c,
                                                        T* __restrict__ Pbar_lo,
-                                                       T* __restrict__ Pbar_c_lo) {
+                                                       T* __restrict__ Pbar_c_lo, int ldp) {
   constexpr int VE = Vec16<T>::N;
   typedef typename Vec16<T>::type vec;
   typedef typename GateT<T>::type GT;  // fp16 with bf16 activations
@@ -817,7 +826,7 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
     const int cc = threadIdx.x;
     float sum = 0.f;
     for (int k = 0; k < kTg; ++k) sum += racc[k][cc];
-    const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * D + c0 + cc;
+    const int64_t dst = (int64_t)(b * nb + (i > 0 ? i - 1 : nb - 1)) * ldp + c0 + cc;
     // The sum as a pair hi + lo of the compute type (lo only for bf16): the
     // memory gradient takes both, the W_m weight gradient hi alone.
     const float v = i > 0 ? sum : 0.f;
@@ -1199,7 +1208,8 @@ hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, v
   hipLaunchKernelGGL(gate_bwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
                      (const E*)dY, (const typename GateT<E>::type*)G, P, (E*)dU, (E*)Pbar, zero_a,
                      na, zero_b, T, D, L,
-                     nb, Pc, (E*)Pbar_c, (E*)Pbar_lo, (E*)Pbar_c_lo);
+                     nb, Pc, (E*)Pbar_c, Pbar_lo ? (E*)Pbar + D : (E*)nullptr, (E*)Pbar_c_lo,
+                     Pbar_lo ? 2 * D : D);
   return hipGetLastError();
 }
 
@@ -1216,11 +1226,12 @@ bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !p
 // The long path's W_m products keep their split-K partial products (one
 // slice per split, a single slice when there is one split) for the scans,
 // which add them in a fixed order: the forward's Q = St W_m, and the
-// backward's dM = Pbar Wm^T and Pbar_lo Wm^T (twice the slices).
+// backward's dM = [Pbar | Pbar_lo] [Wm^T; Wm^T] (one product over 2D).
 size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
   if (mem_fused(nb, per_channel)) return 0;
-  const int sp = gemm_splitk_splits(B * nb, D, D, kMemMinK);
-  return 2 * (size_t)sp * B * nb * D * sizeof(float);
+  const int sp = std::max(gemm_splitk_splits(B * nb, D, D, kMemMinK),
+                          gemm_splitk_splits(B * nb, D, 2 * D, kMemMinK));
+  return (size_t)sp * B * nb * D * sizeof(float);
 }
 
 // One scan launch over grid (columns / 64, B).
@@ -1290,11 +1301,11 @@ hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, flo
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, true>), grid, dim3(kMsWaves * 64), lds, s,
                        (const bf16*)St, (const bf16*)nullptr, (const bf16*)Wm, S, M, (bf16*)Mt, P,
-                       nullptr, nullptr, nullptr, nb, D, gamma, kcr, c);
+                       nullptr, nullptr, nullptr, nb, D, gamma, kcr, c, D);
   else
     hipLaunchKernelGGL((memscan_kernel<float, true>), grid, dim3(kMsWaves * 64), lds, s,
                        (const float*)St, (const float*)nullptr, (const float*)Wm, S, M,
-                       (float*)Mt, P, nullptr, nullptr, nullptr, nb, D, gamma, kcr, c);
+                       (float*)Mt, P, nullptr, nullptr, nullptr, nb, D, gamma, kcr, c, D);
   return hipGetLastError();
 }
 
@@ -1313,22 +1324,15 @@ hipError_t gate_bwd(DType dt, const void* dY, const void* G, const float* P, voi
 // *nq slices in all), mem_bwd_scan the reverse scans, which add them up.
 hipError_t mem_bwd_proj(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
                         float* part, int B, int nb, int D, int* nq, hipStream_t s) {
-  if (dt != DType::BF16) Pbar_lo = nullptr;
-  const int64_t qs = (int64_t)B * nb * D;
-  GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
-  int sp = 0, sp2 = 0;
   *nq = 0;
-  hipError_t e = gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK,
-                                     &sp, s);
-  if (e != hipSuccess) return e;
-  if (Pbar_lo) {
-    g.A = Pbar_lo;
-    float* lo = part + sp * qs;
-    e = gemm_splitk_product(dt, g, lo, lo, nullptr, nullptr, D, D, false, kMemMinK, &sp2, s);
-    if (e != hipSuccess) return e;
+  if (dt == DType::BF16 && Pbar_lo) {
+    // rows [hi | lo] (2D wide) against [W_m^T; W_m^T]: one product over
+    // K = 2D whose B is the same matrix for both halves of K
+    GemmDesc g{B * nb, D, 2 * D, Pbar, 2 * D, false, {Wm, Wm, nullptr}, D, false, kSegK, D, 1};
+    return gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK, nq, s);
   }
-  *nq = sp + sp2;
-  return hipSuccess;
+  GemmDesc g{B * nb, D, D, Pbar, D, false, {Wm, nullptr, nullptr}, D, false, kSegNone, 0, 1};
+  return gemm_splitk_product(dt, g, part, part, nullptr, nullptr, D, D, false, kMemMinK, nq, s);
 }
 
 hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, float* part, int nq,
@@ -1351,12 +1355,13 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* 
   dim3 grid((D + kMsCols - 1) / kMsCols, B);
   if (dt == DType::BF16)
     hipLaunchKernelGGL((memscan_kernel<bf16, false>), grid, dim3(kMsWaves * 64), 0, s,
-                       (const bf16*)Pbar, (const bf16*)Pbar_lo, (const bf16*)Wm, nullptr, nullptr,
-                       nullptr, nullptr, M, dS, dgpart, nb, D, gamma, 0, c);
+                       (const bf16*)Pbar, Pbar_lo ? (const bf16*)Pbar + D : (const bf16*)nullptr,
+                       (const bf16*)Wm, nullptr, nullptr, nullptr, nullptr, M, dS, dgpart, nb, D,
+                       gamma, 0, c, Pbar_lo ? 2 * D : D);
   else
     hipLaunchKernelGGL((memscan_kernel<float, false>), grid, dim3(kMsWaves * 64), 0, s,
                        (const float*)Pbar, (const float*)nullptr, (const float*)Wm, nullptr,
-                       nullptr, nullptr, nullptr, M, dS, dgpart, nb, D, gamma, 0, c);
+                       nullptr, nullptr, nullptr, M, dS, dgpart, nb, D, gamma, 0, c, D);
   return hipGetLastError();
 }
 
