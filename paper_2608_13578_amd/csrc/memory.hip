@@ -54,7 +54,7 @@ constexpr int kVec = 16, kTg = 16;
 // S_i = sum_t a_t H[t].  The block's tokens are taken 256 at a time: their
 // scores go to LDS (one token per thread) with the tile's max and
 // exponential sum, then every thread adds its tokens' weighted rows with the
-// loads of four tokens in flight; the running max is the same for the whole
+// loads of eight tokens in flight; the running max is the same for the whole
 // workgroup, so only the token groups' sums remain to be added at the end.
 // Chunk 0 of each block also writes s (for the backward) and the block's
 // softmax statistics (max, normaliser); S_i is written in float32 and in
@@ -78,6 +78,20 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return r;
 }
 
+// A token's score from its np partial sums, added in order; the loads are
+// issued sixteen at a time, so that their latencies overlap.
+__device__ __forceinline__ float score_sum(const float* __restrict__ q, int np) {
+  float x = 0.f;
+  for (int k0 = 0; k0 < np; k0 += 16) {
+    float t[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) t[u] = k0 + u < np ? q[k0 + u] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) x += t[u];
+  }
+  return x;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
                                                        const float* __restrict__ sp, int np,
@@ -86,7 +100,7 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
                                                        float* __restrict__ stats, int Tn, int D,
                                                        int L, int nb) {
   constexpr int VE = Vec16<T>::N;
-  constexpr int U = 4;
+  constexpr int U = 8;
   typedef typename Vec16<T>::type vec;
   __shared__ float racc[kTg][kVec * VE];
   __shared__ float sc[256];
@@ -110,8 +124,7 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
     float x = -INFINITY;
     if (tid < n) {
       const int64_t row = (int64_t)b * Tn + t0 + tid;
-      x = 0.f;
-      for (int q = 0; q < np; ++q) x += sp[row * np + q];
+      x = score_sum(sp + row * np, np);
       if (first) s_out[row] = x;
     }
     sc[tid] = x;
@@ -200,9 +213,7 @@ __global__ __launch_bounds__(512) void pool_row_kernel(const T* __restrict__ H,
     float mx = -INFINITY;
     for (int t = tid; t < n; t += nt) {
       const int64_t row = (int64_t)b * Tn + t0 + t;
-      const float* q = sp + row * np;
-      float x = 0.f;
-      for (int k = 0; k < np; ++k) x += q[k];
+      const float x = score_sum(sp + row * np, np);
       sc[t] = x;
       s_out[row] = x;
       mx = fmaxf(mx, x);
@@ -324,9 +335,9 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
   const bool scol = tid < kMsCols && col < D;
   float N = 0.f, NP = 0.f, Z = 0.f, Qs = 0.f, E = 0.f, dg = 0.f;
   // this thread's column: its decay and its incoming normaliser
-  const float gam = (scol && cr.gvec) ? cr.gvec[col] : gamma;
-  const float lg2 = gam > 0.f ? log2f(gam) : 0.f;
-  const float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (scol ? cr.Zin[(int64_t)b * D + col] : 0.f));
+  float gam = (scol && cr.gvec) ? cr.gvec[col] : gamma;
+  float lg2 = gam > 0.f ? log2f(gam) : 0.f;
+  float zin = !cr.Zin ? 0.f : (!cr.zcol ? cr.Zin[b] : (scol ? cr.Zin[(int64_t)b * D + col] : 0.f));
   if constexpr (FWD) {
     Z = zin;
     if (scol && cr.Nin) {
@@ -334,6 +345,21 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
       NP = cr.Pc[(int64_t)b * D + col] * zin;
     }
   }
+  // the gradients of the state after the last block (backward)
+  float dn_last = 0.f, dz_last = 0.f;
+  if constexpr (!FWD) {
+    if (scol && cr.dNout) dn_last = cr.dNout[(int64_t)b * D + col];
+    if (cr.dZout) {
+      if (cr.zcol) dz_last = scol ? cr.dZout[(int64_t)b * D + col] : 0.f;
+      else if (col == 0) dz_last = cr.dZout[b];
+    }
+  }
+  // Loaded values pass through an empty asm before the row scans, so that
+  // the compiler waits for their loads there, once: a wait inside a row
+  // would also wait for the stores of the rows before it (vector memory
+  // operations complete in order).
+  asm volatile("" : "+v"(N), "+v"(NP), "+v"(Z), "+v"(gam), "+v"(lg2), "+v"(zin));
+  asm volatile("" : "+v"(dn_last), "+v"(dz_last));
 
   for (int q = 0; q < nt; ++q) {
     const int rt = FWD ? q : nt - 1 - q;
@@ -341,18 +367,41 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
     const int arow = i0 + lr;
     const int64_t arow_off = ((int64_t)b * nb + (arow < nb ? arow : 0)) * lda;
     const T* ap = A + arow_off;
+    // The tile's rows of S (forward) or M (backward, with the row before the
+    // tile), loaded ahead of the product so that their latency overlaps it
+    // and the recurrence below waits on no load.
+    float rv[kMsRows], rprev = 0.f;
+    if (scol) {
+      const float* src = FWD ? S : Min;
+#pragma unroll
+      for (int k = 0; k < kMsRows; ++k)
+        rv[k] = i0 + k < nb ? src[((int64_t)b * nb + i0 + k) * D + col] : 0.f;
+      if (!FWD && i0 >= 1) rprev = Min[((int64_t)b * nb + i0 - 1) * D + col];
+    }
     f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     for (int kc = 0; kc < D; kc += (FWD ? kcr : D)) {
       const int kn = FWD ? min(kcr, D - kc) : D;
       if constexpr (FWD) {
         __syncthreads();
+        // all of a batch's loads are issued before its LDS stores
         constexpr int VE = Vec16<T>::N;
         constexpr int VPR = kMsCols / VE;  // 16-byte vectors per staged row
-        for (int e = tid; e < kn * VPR; e += blockDim.x) {
-          const int kr = e / VPR, cv = (e % VPR) * VE;
-          const bool ok = c0 + cv < D;
-          store16(Bs + kr * kMsCols + cv,
-                  ok ? load16(Wm + (int64_t)(kc + kr) * D + c0 + cv) : typename Vec16<T>::type{});
+        constexpr int UB = 8;
+        typedef typename Vec16<T>::type V16;
+        for (int e0 = tid; e0 < kn * VPR; e0 += UB * blockDim.x) {
+          V16 v[UB];
+#pragma unroll
+          for (int u = 0; u < UB; ++u) {
+            const int e = e0 + u * blockDim.x;
+            const int kr = e / VPR, cv = (e % VPR) * VE;
+            v[u] = (e < kn * VPR && c0 + cv < D) ? load16(Wm + (int64_t)(kc + kr) * D + c0 + cv)
+                                                 : V16{};
+          }
+#pragma unroll
+          for (int u = 0; u < UB; ++u) {
+            const int e = e0 + u * blockDim.x;
+            if (e < kn * VPR) store16(Bs + (e / VPR) * kMsCols + (e % VPR) * VE, v[u]);
+          }
         }
         __syncthreads();
       }
@@ -404,7 +453,11 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) part[wave][lr][ntl * 16 + lg * 4 + r] = acc[ntl][r];
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kMsRows; ++k) asm volatile("" : "+v"(rv[k]));
+    asm volatile("" : "+v"(rprev));
     if (scol) {
+#pragma unroll
       for (int k = 0; k < kMsRows; ++k) {
         const int ii = FWD ? k : kMsRows - 1 - k;
         const int i = i0 + ii;
@@ -414,7 +467,7 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
         for (int w = 0; w < kMsWaves; ++w) g += part[w][ii][tid];
         const int64_t off = ((int64_t)b * nb + i) * D + col;
         if constexpr (FWD) {
-          N = gam * N + S[off];
+          N = gam * N + rv[ii];
           NP = gam * NP + g;
           Z = gam * Z + 1.f;
           const float rz = 1.f / Z;
@@ -422,29 +475,20 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
           M[off] = m;
           Mt[off] = from_f32<T>(m);
           P[off] = NP * rz;
-          if (i == nb - 1) {
-            if (cr.Nout) cr.Nout[(int64_t)b * D + col] = N;
-            if (cr.Zout) {
-              if (cr.zcol) cr.Zout[(int64_t)b * D + col] = Z;
-              else if (tid == 0 && blockIdx.x == 0) cr.Zout[b] = Z;
-            }
-          }
         } else {
           const float z = zsum(i, gam, lg2, zin);
-          const float m = Min[off];
+          const float m = rv[ii];
           Qs = g / z + gam * Qs;
           E = -g * m / z + gam * E;
           if (i == nb - 1) {
-            if (cr.dNout) Qs += cr.dNout[(int64_t)b * D + col];
-            if (cr.dZout) {
-              if (cr.zcol) E += cr.dZout[(int64_t)b * D + col];
-              else if (col == 0) E += cr.dZout[b];
-            }
+            Qs += dn_last;
+            E += dz_last;
           }
           dS[off] = Qs;
           if (i >= 1) {
             const float zp = zsum(i - 1, gam, lg2, zin);
-            dg += Qs * (Min[off - D] * zp) + E * zp;
+            const float mp = ii >= 1 ? rv[ii - 1] : rprev;
+            dg += Qs * (mp * zp) + E * zp;
           } else if (cr.e0) {
             cr.e0[(int64_t)b * D + col] = E;
           }
@@ -452,6 +496,14 @@ __global__ __launch_bounds__(kMsWaves * 64) void memscan_kernel(
       }
     }
     __syncthreads();  // part[] is rewritten by the next row tile
+  }
+  if constexpr (FWD) {
+    // the state after the last block
+    if (scol && cr.Nout) cr.Nout[(int64_t)b * D + col] = N;
+    if (scol && cr.Zout) {
+      if (cr.zcol) cr.Zout[(int64_t)b * D + col] = Z;
+      else if (tid == 0 && blockIdx.x == 0) cr.Zout[b] = Z;
+    }
   }
   if constexpr (!FWD) {
     // this workgroup's share of the decay gradient, as one partial
