@@ -43,13 +43,19 @@ constexpr int kMaxD = 2048;
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Minimum K per split of the D x D weight-gradient products on the side
-// stream: about 288 workgroups in all, and at least 128 deep (D = 128: one
-// tile, 128 splits).  Same-box A/B against 144 workgroups: B = 2, T = 65536,
-// D = 1024 (64 tiles, 4 splits instead of 2) took dW_o and dW_g from 830 to
-// 430 us each and the step from 6.29 to 6.12-6.24 ms; B = 8, T = 1024,
-// D = 768 (8 splits instead of 4) 299.3 -> 298.4-298.9 us.
+// stream.  Long inputs (splits of a 512-workgroup plan at least 8192 deep):
+// 128, i.e. the plan's two workgroups on every CU.  B = 2, T = 65536,
+// D = 1024: 512 instead of 320 workgroups took dW_o and dW_g from 457 to
+// 310 us each and the step from 6.49 to 6.23 ms; one workgroup per CU (256)
+// took them to 590 us.  Shorter inputs: about 288 workgroups, at least 128
+// deep (D = 128: one tile, 128 splits).  At B = 8, T = 1024, D = 768, 468
+// workgroups made the products 3.5 us faster but their reductions 1.7 us
+// slower and the step 10 us slower (the side stream then crowds out the
+// critical path); against 144 workgroups, 288 took the step from 299.3 to
+// 298.4-298.9 us.
 int dd_min_k(int D, int K) {
   const int64_t tiles = (int64_t)((D + 127) / 128) * ((D + 127) / 128);
+  if ((int64_t)K * tiles / 512 >= 8192) return 128;
   const int mk = (int)((K * tiles / 288 + 63) / 64 * 64);
   return mk < 128 ? 128 : mk;
 }

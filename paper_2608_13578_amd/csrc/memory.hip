@@ -974,97 +974,138 @@ __global__ __launch_bounds__(256) void carry_finish_kernel(
 // ------------------------------------------------------------------ pooling backward
 // With a_t the block softmax weights and dS_i the summary gradient:
 //   ds_t = a_t (dS_i . H[t] - dS_i . S_i),  dw_p = sum_t ds_t H[t].
-// Workgroup = (chunk of 8 * TB tokens of block i, batch element), 8 waves;
-// each wave requests its TB rows (NVJ 16-byte vectors per lane) at once,
-// forms their dot products with dS_i, writes a_t and ds_t (they feed the dH
-// epilogue of the W_g backward product) and keeps sum ds_t H[t] over its
-// rows in registers.  The waves' sums meet in LDS in a fixed order and the
-// chunk's sum becomes one row of dwp_part; colsum_kernel adds the rows, so
-// dw_p needs no atomics and comes out the same on every run.
-template <int NVJ> struct PoolRows { static constexpr int TB = 16 / NVJ; };
+// Each wave owns a segment of R consecutive rows of one block (the blocks'
+// segments are numbered batch element, block, segment; a workgroup takes
+// eight consecutive ones), so a launch has about B T / (8 R) workgroups
+// whatever the block size, and a wave reads dS_i and S_i once for its R rows.
+// The wave streams its rows TB at a time with the next TB rows' loads in
+// flight while it forms the current rows' dot products with dS_i, writes a_t
+// and ds_t (they feed the dH epilogue of the W_g backward product) and adds
+// ds_t H[t] into registers.  The waves' sums meet in LDS in a fixed order and
+// the workgroup's sum becomes one row of dwp_part; colsum_kernel adds the
+// rows, so dw_p needs no atomics and comes out the same on every run.
+// Rows a wave has in flight per load batch, by 16-byte vectors per lane and row.
+constexpr int pool_tb(int nvj) { return nvj >= 4 ? 1 : 4 / nvj; }
+template <int NVJ> struct PoolRows { static constexpr int TB = pool_tb(NVJ); };
 constexpr int kPoolWaves = 8;
 
 template <typename T, int NVJ>
 __global__ __launch_bounds__(kPoolWaves * 64) void pool_bwd_kernel(
     const T* __restrict__ H, const float* __restrict__ s_in, const float* __restrict__ stats,
     const float* __restrict__ S, const float* __restrict__ dS, float* __restrict__ a_out,
-    float* __restrict__ ds_out, float* __restrict__ dwp_part, int Tn, int D, int L, int nb,
-    int nch) {
+    float* __restrict__ ds_out, float* __restrict__ dwp_part, int Bn, int Tn, int D, int L, int nb,
+    int R, int nseg) {
   constexpr int VE = Vec16<T>::N;
   constexpr int TB = PoolRows<NVJ>::TB;
   constexpr int ROW = NVJ * 64 * VE;  // columns one wave covers
   typedef typename Vec16<T>::type vec;
   __shared__ float red[kPoolWaves / 2][ROW];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = blockIdx.x / nch, ch = blockIdx.x % nch, b = blockIdx.y;
-  const int bend = min(i * L + L, Tn);
-  const int t0 = i * L + ch * (kPoolWaves * TB) + wave * TB;  // this wave's first row
   const int Dv = D / VE;
-  const int64_t brow = (int64_t)(b * nb + i) * D;
-
-  // This wave's rows first: nothing else decides their addresses.
-  vec x[TB][NVJ];
-  float sv[TB];
-#pragma unroll
-  for (int k = 0; k < TB; ++k) {
-    const bool tok = t0 + k < bend;
-#pragma unroll
-    for (int j = 0; j < NVJ; ++j) {
-      const int v = lane + 64 * j;
-      x[k][j] = tok && v < Dv ? load16(H + ((int64_t)b * Tn + t0 + k) * D + v * VE) : vec{};
-    }
-    sv[k] = tok ? s_in[(int64_t)b * Tn + t0 + k] : 0.f;
-  }
-  float g[NVJ][VE];
-  float ss = 0.f;
-#pragma unroll
-  for (int j = 0; j < NVJ; ++j) {
-    const int v = lane + 64 * j;
-    if (v < Dv) {
-#pragma unroll
-      for (int q = 0; q < VE / 4; ++q) {
-        const f32x4 dv = *reinterpret_cast<const f32x4*>(dS + brow + v * VE + q * 4);
-        const f32x4 sw = *reinterpret_cast<const f32x4*>(S + brow + v * VE + q * 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          g[j][q * 4 + r] = dv[r];
-          ss += dv[r] * sw[r];
-        }
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < VE; ++e) g[j][e] = 0.f;
-    }
-  }
-  ss = wave_sum(ss);
-  const float mi = stats[(int64_t)(b * nb + i) * 2];
-  const float li = stats[(int64_t)(b * nb + i) * 2 + 1];
-
+  const int64_t seg = (int64_t)blockIdx.x * kPoolWaves + wave;
+  const int64_t nall = (int64_t)Bn * nb * nseg;
   float pw[NVJ][VE];
 #pragma unroll
   for (int j = 0; j < NVJ; ++j)
 #pragma unroll
     for (int e = 0; e < VE; ++e) pw[j][e] = 0.f;
+
+  if (seg < nall) {  // (uniform over the wave)
+    const int b = (int)(seg / ((int64_t)nb * nseg));
+    const int rem = (int)(seg - (int64_t)b * nb * nseg);
+    const int i = rem / nseg, sg = rem % nseg;
+    const int t0 = i * L + sg * R;
+    const int t1 = min(min(t0 + R, i * L + L), Tn);
+    const int64_t brow = (int64_t)(b * nb + i) * D;
+    const T* hrow = H + (int64_t)b * Tn * D;
+
+    float g[NVJ][VE];
+    float ss = 0.f;
 #pragma unroll
-  for (int k = 0; k < TB; ++k) {
-    float d = 0.f;
+    for (int j = 0; j < NVJ; ++j) {
+      const int v = lane + 64 * j;
+      if (v < Dv) {
 #pragma unroll
-    for (int j = 0; j < NVJ; ++j)
+        for (int q = 0; q < VE / 4; ++q) {
+          const f32x4 dv = *reinterpret_cast<const f32x4*>(dS + brow + v * VE + q * 4);
+          const f32x4 sw = *reinterpret_cast<const f32x4*>(S + brow + v * VE + q * 4);
 #pragma unroll
-      for (int e = 0; e < VE; ++e) d += g[j][e] * to_f32(x[k][j][e]);
-    d = wave_sum(d);
-    const int t = t0 + k;
-    const float a = __expf(sv[k] - mi) / li;
-    const float ds = t < bend ? a * (d - ss) : 0.f;
-    if (t < bend && lane == 0) {
-      const int64_t ti = (int64_t)b * Tn + t;
-      a_out[ti] = a;
-      ds_out[ti] = ds;
+          for (int r = 0; r < 4; ++r) {
+            g[j][q * 4 + r] = dv[r];
+            ss += dv[r] * sw[r];
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) g[j][e] = 0.f;
+      }
     }
+    const float mi = stats[(int64_t)(b * nb + i) * 2];
+    const float li = stats[(int64_t)(b * nb + i) * 2 + 1];
+
+    // rows t .. t+TB-1 (those below t1) into x and their scores into sv
+    auto fetch = [&](vec(&x)[TB][NVJ], float(&sv)[TB], int t) {
 #pragma unroll
-    for (int j = 0; j < NVJ; ++j)
+      for (int k = 0; k < TB; ++k) {
+        const bool tok = t + k < t1;
 #pragma unroll
-      for (int e = 0; e < VE; ++e) pw[j][e] += ds * to_f32(x[k][j][e]);
+        for (int j = 0; j < NVJ; ++j) {
+          const int v = lane + 64 * j;
+          x[k][j] = tok && v < Dv ? load16(hrow + (int64_t)(t + k) * D + v * VE) : vec{};
+        }
+        sv[k] = tok ? s_in[(int64_t)b * Tn + t + k] : 0.f;
+      }
+    };
+    float ssum = 0.f;  // wave_sum of ss, formed once the first rows are in flight
+    auto consume = [&](vec(&x)[TB][NVJ], const float(&sv)[TB], int t) {
+      float d[TB];
+#pragma unroll
+      for (int k = 0; k < TB; ++k) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+          for (int e = 0; e < VE; ++e) acc += g[j][e] * to_f32(x[k][j][e]);
+        d[k] = wave_sum(acc);
+      }
+      // The rows stay packed until the second pass converts them again
+      // (keeping both conversions would double the registers the rows take).
+#pragma unroll
+      for (int k = 0; k < TB; ++k)
+#pragma unroll
+        for (int j = 0; j < NVJ; ++j) asm volatile("" : "+v"(x[k][j]));
+      float dsv = 0.f, av = 0.f;
+#pragma unroll
+      for (int k = 0; k < TB; ++k) {
+        const bool tok = t + k < t1;
+        const float a = __expf(sv[k] - mi) / li;
+        const float ds = tok ? a * (d[k] - ssum) : 0.f;
+        if (lane == k) {
+          dsv = ds;
+          av = a;
+        }
+#pragma unroll
+        for (int j = 0; j < NVJ; ++j)
+#pragma unroll
+          for (int e = 0; e < VE; ++e) pw[j][e] += ds * to_f32(x[k][j][e]);
+      }
+      if (lane < TB && t + lane < t1) {
+        const int64_t ti = (int64_t)b * Tn + t + lane;
+        a_out[ti] = av;
+        ds_out[ti] = dsv;
+      }
+    };
+    vec xa[TB][NVJ], xb[TB][NVJ];
+    float sa[TB], sb[TB];
+    fetch(xa, sa, t0);
+    ssum = wave_sum(ss);
+    for (int t = t0; t < t1; t += 2 * TB) {
+      if (t + TB < t1) fetch(xb, sb, t + TB);
+      consume(xa, sa, t);
+      if (t + TB >= t1) break;
+      if (t + 2 * TB < t1) fetch(xa, sa, t + 2 * TB);
+      consume(xb, sb, t + TB);
+    }
   }
   if (!dwp_part) return;  // (uniform over the workgroup)
 
@@ -1087,7 +1128,7 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_bwd_kernel(
     __syncthreads();
   }
   if (wave == 0) {
-    float* row = dwp_part + ((int64_t)(b * nb + i) * nch + ch) * D;
+    float* row = dwp_part + (int64_t)blockIdx.x * D;
 #pragma unroll
     for (int j = 0; j < NVJ; ++j) {
       const int v = lane + 64 * j;
@@ -1102,19 +1143,22 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_bwd_kernel(
 }
 
 // out[c] = sum over rows r < R of P[r][c] for 64 columns per workgroup and
-// up to kColRows rows per workgroup (blockIdx.y): thread (vector v, row
-// group rg) adds rows rg, rg + 16, ... of its four columns, and the 16 row
-// groups meet in LDS in a fixed order.  With more than one row range
-// (gridDim.y > 1) each range writes its own row of `out` (stride N), which a
-// second pass adds up.
+// `per` rows per workgroup (blockIdx.y): thread (vector v, row group rg)
+// adds rows rg, rg + 16, ... of its four columns, and the 16 row groups meet
+// in LDS in a fixed order.  With more than one row range (gridDim.y > 1)
+// each range writes its own row of `out` (stride N), which a second pass
+// adds up.  One pass takes up to kColOnePass rows; longer inputs are first
+// folded kColRows rows at a time.
 constexpr int kColRows = 256;
+constexpr int kColOnePass = 1024;
 __global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ P, int64_t R, int N,
-                                                     float* __restrict__ out, int accumulate) {
+                                                     int64_t per, float* __restrict__ out,
+                                                     int accumulate) {
   __shared__ f32x4 red[16][16];
   const int v = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int c = blockIdx.x * 64 + v * 4;
-  const int64_t r0 = (int64_t)blockIdx.y * kColRows;
-  const int64_t r1 = r0 + kColRows < R ? r0 + kColRows : R;
+  const int64_t r0 = (int64_t)blockIdx.y * per;
+  const int64_t r1 = r0 + per < R ? r0 + per : R;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   if (c < N) {
     int64_t r = r0 + rg;
@@ -1218,13 +1262,32 @@ hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, floa
   return hipGetLastError();
 }
 
-// Tokens per pooling-backward workgroup and workgroups per block.
+// Rows per wave (R), segments per block and workgroups of the pooling
+// backward: R is a multiple of the rows a wave has in flight, chosen for
+// about 1024 workgroups, but at least 8 rows (at most 64, at most a block).
+// Short inputs thus leave CUs free for the weight-gradient products that run
+// beside this kernel on the second stream: at B = 8, T = 1024, D = 768, 512
+// workgroups of 2 rows per wave made this kernel 0.8 us faster and the step
+// 9.5 us slower than 128 workgroups.
+struct PoolBwdShape {
+  int R, nseg;
+  int64_t nwg;
+};
 template <typename E>
-void pool_bwd_shape(int D, int L, int T, int* tc, int* nch) {
-  const int nv = nvj_for(D / Vec16<E>::N);
-  *tc = kPoolWaves * (16 / nv);
+PoolBwdShape pool_bwd_shape(int B, int D, int L, int T) {
+  const int tb = pool_tb(nvj_for(D / Vec16<E>::N));
+  const int nb = (T + L - 1) / L;
   const int lb = L < T ? L : T;
-  *nch = (lb + *tc - 1) / *tc;
+  const int64_t want = (int64_t)B * T / (kPoolWaves * 1024);
+  int64_t r = (want + tb - 1) / tb * tb;
+  r = r < 8 ? 8 : r > 64 ? 64 : r;
+  const int64_t lr = (lb + tb - 1) / tb * tb;
+  if (r > lr) r = lr;
+  PoolBwdShape p;
+  p.R = (int)r;
+  p.nseg = (lb + p.R - 1) / p.R;
+  p.nwg = ((int64_t)B * nb * p.nseg + kPoolWaves - 1) / kPoolWaves;
+  return p;
 }
 
 template <typename E, int NV>
@@ -1232,10 +1295,11 @@ hipError_t pool_bwd_nv(const void* H, const float* s_in, const float* stats, con
                        const float* dS, float* a_out, float* ds_out, float* dwp_part, int B,
                        int T, int D, int L, hipStream_t s) {
   const int nb = (T + L - 1) / L;
-  int tc, nch;
-  pool_bwd_shape<E>(D, L, T, &tc, &nch);
-  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3(nb * nch, B), dim3(kPoolWaves * 64), 0, s,
-                     (const E*)H, s_in, stats, S, dS, a_out, ds_out, dwp_part, T, D, L, nb, nch);
+  const PoolBwdShape p = pool_bwd_shape<E>(B, D, L, T);
+  if (p.nwg > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((pool_bwd_kernel<E, NV>), dim3((unsigned)p.nwg), dim3(kPoolWaves * 64), 0,
+                     s, (const E*)H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, nb,
+                     p.R, p.nseg);
   return hipGetLastError();
 }
 
@@ -1454,17 +1518,15 @@ hipError_t pool_bwd(DType dt, const void* H, const float* s_in, const float* sta
   return pool_bwd_t<float>(H, s_in, stats, S, dS, a_out, ds_out, dwp_part, B, T, D, L, s);
 }
 
-// Rows of dw_p partial sums the pooling backward writes.
+// Rows of dw_p partial sums the pooling backward writes (one per workgroup).
 int64_t pool_rows(DType dt, int B, int T, int D, int L) {
-  int tc, nch;
-  if (dt == DType::BF16) pool_bwd_shape<bf16>(D, L, T, &tc, &nch);
-  else pool_bwd_shape<float>(D, L, T, &tc, &nch);
-  return (int64_t)B * ((T + L - 1) / L) * nch;
+  return dt == DType::BF16 ? pool_bwd_shape<bf16>(B, D, L, T).nwg
+                           : pool_bwd_shape<float>(B, D, L, T).nwg;
 }
 
 int64_t pool_bwd_partial_rows(DType dt, int B, int T, int D, int L) {
   int64_t r = pool_rows(dt, B, T, D, L), all = r;
-  while (r > 1) {  // the reduction's intermediate rows
+  while (r > kColOnePass) {  // the reduction's intermediate rows
     r = (r + kColRows - 1) / kColRows;
     all += r;
   }
@@ -1476,18 +1538,19 @@ hipError_t pool_dwp(float* dwp_part, DType dt, int B, int T, int D, int L, float
   if (!dwp) return hipSuccess;
   int64_t R = pool_rows(dt, B, T, D, L);
   float* in = dwp_part;
-  // Each pass folds kColRows rows into one, in a fixed order.
-  while (R > kColRows) {
+  // Each pass folds kColRows rows into one, in a fixed order, until one
+  // pass can take the rest.
+  while (R > kColOnePass) {
     const int64_t ranges = (R + kColRows - 1) / kColRows;
     if (ranges > 65535) return hipErrorInvalidValue;
     float* out = in + R * D;
     hipLaunchKernelGGL(colsum_kernel, dim3((D + 63) / 64, (unsigned)ranges), dim3(256), 0, s,
-                       (const float*)in, R, D, out, 0);
+                       (const float*)in, R, D, (int64_t)kColRows, out, 0);
     in = out;
     R = ranges;
   }
   hipLaunchKernelGGL(colsum_kernel, dim3((D + 63) / 64, 1), dim3(256), 0, s, (const float*)in, R,
-                     D, dwp, accumulate ? 1 : 0);
+                     D, R, dwp, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 
