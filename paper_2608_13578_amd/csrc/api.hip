@@ -525,10 +525,14 @@ static int layer_forward(const bcmt_config* cfg, const void* X, const bcmt_param
     GemmDesc g{BT, D, D, SV + p.o, D, false, {prm->Wo, nullptr, nullptr}, D, true, kSegNone, 0, 1};
     LAUNCH(ST_WO, gemm_score(dt, g, SV + p.h, prm->wp, (float*)(W + p.sp), s));
   }
-  // 4. Adaptive summaries (Sec. 3.4).
+  // 4. Adaptive summaries (Sec. 3.4); the launch also clears the records of
+  // the look-back scan that follows (long sequences, few of them).
+  int64_t nflag = 0;
+  float* flags = mem_lb_flags((float*)(W + p.mpart), p.B, p.nb, D,
+                              channel_decay(cfg, prm) != nullptr, chunk, &nflag);
   LAUNCH(ST_POOL_FWD, pool_fwd(dt, SV + p.h, (const float*)(W + p.sp), D / kDh,
                                (float*)(SV + p.s), (float*)(SV + p.S), W + p.St,
-                               (float*)(SV + p.stats), p.B, p.T, D, p.L, s));
+                               (float*)(SV + p.stats), p.B, p.T, D, p.L, flags, nflag, s));
   // 5-6. Exponential memory and its projection (Sec. 3.5): one kernel
   // projects the summaries (Q = S Wm, over only B * N_b rows) and scans S
   // and Q, which yields M and P = M Wm (the decayed sum is linear); the
@@ -607,6 +611,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
   // the decay gradient: one scalar, or one value per channel
   float* dgam = gvec ? gr.dgamma_ch : gr.dgamma;
   Plan p(*cfg);
+  const int dgr = dg_part_rows_used(p.B, p.nb, p.D, gvec != nullptr, chunk);  // rows this call writes
   const size_t act = (size_t)p.B * p.T * p.D * p.es;
   if (dX && (overlaps(dX, dY, act) || overlaps(dX, X, act))) return BCMT_ERR_INVALID;
   if (!ws) return BCMT_ERR_INVALID;
@@ -659,8 +664,15 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     // The weight matrices, dwp and the decay gradient are written (or
     // accumulated) by fixed-order reductions.
     const bool lo = dt == DType::BF16;  // context gradients kept as hi + lo
+    // (also clearing the records of the look-back scan of the memory
+    // backward: fewer than 128 sequence x column slices, at most 64 segments
+    // of 128 words each, so the count fits an int)
+    int64_t nflag = 0;
+    float* flags = mem_lb_flags((float*)(W + p.mpart_b), p.B, p.nb, D, gvec != nullptr, chunk,
+                                &nflag);
     LAUNCH(ST_GATE_BWD, gate_bwd(dt, dY, SV + p.g, (const float*)(SV + p.P), W + p.du, W + p.pbar,
-                                 lo ? W + p.pbar_lo : nullptr, nullptr, 0, nullptr, p.B, p.T, D, p.L,
+                                 lo ? W + p.pbar_lo : nullptr, flags, (int)nflag, nullptr, p.B,
+                                 p.T, D, p.L,
                                  chunk ? (const float*)(SV + p.cP) : nullptr,
                                  chunk ? W + p.cpbar : nullptr,
                                  (chunk && lo) ? W + p.cpbar_lo : nullptr, s));
@@ -726,7 +738,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
                                         (const float*)(W + p.ce0), dcin ? dcin->N : nullptr,
                                         dcin ? dcin->Z : nullptr,
                                         dgam ? (float*)(W + p.dgp) +
-                                                   (size_t)p.dgp_rows * (gvec ? D : 1)
+                                                   (size_t)dgr * (gvec ? D : 1)
                                              : nullptr,
                                         p.B, p.nb, D,
                                         cfg->gamma, gvec, gvec != nullptr, s));
@@ -767,7 +779,7 @@ static int layer_backward(const bcmt_config* cfg, const void* X, const bcmt_para
     if (dwp_side)
       LAUNCH(ST_DWP, pool_dwp((float*)(W + p.dwpp), dt, p.B, p.T, D, p.L, gr.dwp, accum, s));
     if (dg_side)
-      LAUNCH(ST_DGAMMA, dgamma_reduce((const float*)(W + p.dgp), p.dgp_rows + (chunk ? p.B : 0),
+      LAUNCH(ST_DGAMMA, dgamma_reduce((const float*)(W + p.dgp), dgr + (chunk ? p.B : 0),
                                       gvec ? D : 1, dgam, accum, s));
     SIDE_END();
   }

@@ -190,8 +190,10 @@ struct Carry {
 // Pooling, from the np partial scores per token written by gemm_score:
 // scores s [B*T], summaries S [B*nb, D] (float32, and St in the compute
 // type) and per-block softmax statistics (max, normaliser) [B*nb, 2].
+// Also clears zero[0 .. nzero) (may be null), shared among its workgroups.
 hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
-                    void* St, float* stats, int B, int T, int D, int L, hipStream_t s);
+                    void* St, float* stats, int B, int T, int D, int L, float* zero,
+                    int64_t nzero, hipStream_t s);
 // Memory forward: M (float32), Mt (compute type) and P = M Wm from S.  Up
 // to a few dozen blocks per sequence one kernel does it all (Q = St Wm with
 // St = S in the compute type, [B*nb, D], and the decayed scans of S and Q);
@@ -203,6 +205,12 @@ hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_o
 // takes the scan + matrix-product path at any length.
 bool mem_fused(int nb, bool per_channel);
 size_t mem_part_bytes(int B, int nb, int D, bool per_channel);
+// The look-back scans' records inside `part` (null and *nfloat = 0 where a
+// call with these sizes does not use them): a kernel earlier on the stream
+// must clear these *nfloat floats (pool_fwd's `zero` before the forward,
+// gate_bwd's zero_a before the backward).
+float* mem_lb_flags(float* part, int B, int nb, int D, bool per_channel, bool carry,
+                    int64_t* nfloat);
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
                    float* P, float* part, int B, int nb, int D, float gamma, const Carry& c,
                    hipStream_t s);
@@ -242,6 +250,10 @@ hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* 
                    const float* M, float* dS, float* dgpart, float* dM, float* part, int B, int nb,
                    int D, float gamma, const Carry& c, hipStream_t s);
 int dg_part_rows(int B, int nb, int D, bool per_channel);
+// The rows one call writes: without carried state (carry false) and few
+// sequences, the long path's look-back scans write one row per (sequence,
+// column slice, segment); dg_part_rows is the most over both kinds of call.
+int dg_part_rows_used(int B, int nb, int D, bool per_channel, bool carry);
 // out[0 .. Dp) = (out if accumulate, else 0) + the sum of part[rows][Dp]
 // over its rows, in a fixed order (deterministic).
 hipError_t dgamma_reduce(const float* part, int rows, int Dp, float* out, bool accumulate,

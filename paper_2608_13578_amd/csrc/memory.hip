@@ -92,16 +92,29 @@ __device__ __forceinline__ float score_sum(const float* __restrict__ q, int np) 
   return x;
 }
 
+// Clears zero[0 .. n) as a side task shared by every workgroup of a launch
+// (the records of a later kernel on the same stream).
+__device__ __forceinline__ void clear_share(float* zero, int64_t n) {
+  if (!zero) return;
+  const int64_t G = (int64_t)gridDim.x * gridDim.y * gridDim.z;
+  const int64_t g = ((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t per = (n + G - 1) / G;
+  const int64_t e = min(n, (g + 1) * per);
+  for (int64_t k = g * per + threadIdx.x; k < e; k += blockDim.x) zero[k] = 0.f;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void pool_fwd_kernel(const T* __restrict__ H,
                                                        const float* __restrict__ sp, int np,
                                                        float* __restrict__ s_out,
                                                        float* __restrict__ S, T* __restrict__ St,
                                                        float* __restrict__ stats, int Tn, int D,
-                                                       int L, int nb) {
+                                                       int L, int nb, float* __restrict__ zero,
+                                                       int64_t nzero) {
   constexpr int VE = Vec16<T>::N;
   constexpr int U = 8;
   typedef typename Vec16<T>::type vec;
+  clear_share(zero, nzero);
   __shared__ float racc[kTg][kVec * VE];
   __shared__ float sc[256];
   __shared__ float red[4];
@@ -190,10 +203,12 @@ __global__ __launch_bounds__(512) void pool_row_kernel(const T* __restrict__ H,
                                                        float* __restrict__ s_out,
                                                        float* __restrict__ S, T* __restrict__ St,
                                                        float* __restrict__ stats, int Tn, int D,
-                                                       int L, int nb, int TG) {
+                                                       int L, int nb, int TG,
+                                                       float* __restrict__ zero, int64_t nzero) {
   constexpr int VE = Vec16<T>::N;
   constexpr int U = 8;
   typedef typename Vec16<T>::type vec;
+  clear_share(zero, nzero);
   extern __shared__ float pdyn[];  // racc [TG][D], then sc [kRowTile]
   __shared__ float red[8];
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6;
@@ -791,6 +806,240 @@ __global__ __launch_bounds__(kScCols * kSbWaves) void scan_bwd_kernel(
   }
 }
 
+// ------------------------------------------------------------------ look-back scans
+// The long path's scans for few sequences (fewer than kLbMaxPairs sequence x
+// 64-column slices, which the scans above would give one workgroup each):
+// each sequence is cut into segments of kLbSeg blocks and every (segment,
+// sequence, column slice) gets a workgroup, so the launch fills the chip.
+// A workgroup scans its segment from a zero state, publishes the segment's
+// aggregate (the state at its last block; the reverse scan's, at its first)
+// for each of its columns, and reads the aggregates of the segments before
+// it (after it, in reverse), which it folds in a fixed order (Horner over
+// the segments, factor g^kLbSeg) into the state entering its segment; then
+// it finishes its outputs as the scans above do with a super-chunk's carry.
+// Reading every earlier aggregate (at most kLbMaxSeg - 1) rather than a
+// running prefix keeps the result independent of timing: the same on every
+// run.  Published words are 64 bits, the value's bits with a status word of
+// 1 above them, written and read with device-scope atomics so that a
+// workgroup on another XCD sees them; the launcher clears the words first.
+// Workgroups are numbered segment first (the reverse scan from the last
+// segment), so every segment a workgroup waits for belongs to a workgroup
+// launched before it, which publishes before it waits itself; a grid of a
+// few hundred small workgroups is resident at once in any case.  A wait
+// that exceeds kLbSpin polls gives up with NaN instead of hanging.  The
+// records are cleared by the kernel before the scan on the same stream
+// (pooling for the forward, the gate backward for the backward).
+// Scalar decay and whole sequences only (no carried state).
+constexpr int kLbWaves = 4, kLbRows = 4, kLbSeg = kLbWaves * kLbRows;
+constexpr int kLbMaxPairs = 128, kLbMinSeg = 4, kLbMaxSeg = 64;
+constexpr int kLbSpin = 1 << 18;
+
+// Words of one segment's record: [quantity 0 | quantity 1] x 64 columns.
+constexpr int kLbRec = 2 * kScCols;
+
+__device__ __forceinline__ void lb_publish(uint64_t* p, float v) {
+  const uint64_t w = (1ull << 32) | (uint64_t)__builtin_bit_cast(uint32_t, v);
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t lb_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// The value of a published word, polling until it is published.
+__device__ __forceinline__ float lb_value(const uint64_t* p, uint64_t w) {
+  for (int n = 0; (w >> 32) == 0; ++n) {
+    if (n >= kLbSpin) return __builtin_nanf("");
+    __builtin_amdgcn_s_sleep(2);
+    w = lb_load(p);
+  }
+  return __builtin_bit_cast(float, (uint32_t)w);
+}
+// Fold of the published aggregates of segments j = j0, j0 + dj, ... (cnt of
+// them) for one column and quantity: e = g * e + A_j in that order, sixteen
+// loads in flight at a time.
+__device__ __forceinline__ float lb_fold(const uint64_t* rec0, int j0, int dj, int cnt, float g) {
+  float e = 0.f;
+  for (int u0 = 0; u0 < cnt; u0 += 16) {
+    uint64_t w[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      w[u] = u0 + u < cnt ? lb_load(rec0 + (int64_t)(j0 + (u0 + u) * dj) * kLbRec) : 0ull;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (u0 + u < cnt)
+        e = fmaf(g, e, lb_value(rec0 + (int64_t)(j0 + (u0 + u) * dj) * kLbRec, w[u]));
+  }
+  return e;
+}
+
+// Forward (as scan_fwd_kernel without carried state): M = N / Z, and with Qp
+// the projected summaries' scan P = NP / Z.  flags: B * ncs * nseg records,
+// zero at launch.
+template <typename T>
+__global__ __launch_bounds__(kScCols * kLbWaves) void scan_fwd_lb_kernel(
+    const float* __restrict__ S, float* __restrict__ M, T* __restrict__ Mt, int B, int nb, int D,
+    float gamma, const float* __restrict__ Qp, int nq, int64_t qstride, float* __restrict__ P,
+    uint64_t* __restrict__ flags, int nseg) {
+  __shared__ float wn[kLbWaves][kScCols], wp[kLbWaves][kScCols], en[2][kScCols];
+  const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
+  const int ncs = (D + kScCols - 1) / kScCols;
+  const int id = blockIdx.x;
+  const int k = id / (B * ncs), b = (id / ncs) % B, x = id % ncs;
+  const int col = x * kScCols + c;
+  const bool on = col < D;
+  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+  const float gw = pow2k<kLbRows>(gamma), gs = pow2k<kLbSeg>(gamma);
+  const int a = k * kLbSeg + w * kLbRows;  // this wave's first block
+  const int64_t off0 = (int64_t)b * nb * D + (int64_t)a * D + col;
+  float v[kLbRows], q[kLbRows];
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) {
+    v[r] = on && a + r < nb ? S[off0 + (int64_t)r * D] : 0.f;
+    q[r] = 0.f;
+  }
+  for (int z = 0; Qp && z < nq; ++z) {
+#pragma unroll
+    for (int r = 0; r < kLbRows; ++r)
+      q[r] += on && a + r < nb ? Qp[z * qstride + off0 + (int64_t)r * D] : 0.f;
+  }
+  float n = 0.f, np = 0.f;
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) {
+    n = gamma * n + v[r];
+    np = gamma * np + q[r];
+    v[r] = n;
+    q[r] = np;
+  }
+  wn[w][c] = n;
+  wp[w][c] = np;
+  __syncthreads();
+  // wave 0: the aggregate of N, wave 1: of NP; publish it, then fold the
+  // earlier segments' into the state entering this one
+  uint64_t* rec0 = flags + ((int64_t)b * ncs + x) * nseg * kLbRec;
+  if (w < (Qp ? 2 : 1)) {
+    float agg = 0.f;
+    for (int j = 0; j < kLbWaves; ++j) agg = gw * agg + (w == 0 ? wn[j][c] : wp[j][c]);
+    if (k + 1 < nseg) lb_publish(rec0 + (int64_t)k * kLbRec + w * kScCols + c, agg);
+    en[w][c] = k > 0 ? lb_fold(rec0 + w * kScCols + c, 0, 1, k, gs) : 0.f;
+  }
+  __syncthreads();
+  float cn = en[0][c], cp = Qp ? en[1][c] : 0.f;
+  for (int j = 0; j < w; ++j) {
+    cn = gw * cn + wn[j][c];
+    cp = gw * cp + wp[j][c];
+  }
+  float f = gamma;
+  float zz = zsum(a, gamma, lg2, 0.f);
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) {
+    const int i = a + r;
+    const float rz = 1.f / zz;
+    zz = gamma * zz + 1.f;
+    if (on && i < nb) {
+      const float m = (v[r] + f * cn) * rz;
+      const int64_t off = off0 + (int64_t)r * D;
+      M[off] = m;
+      Mt[off] = from_f32<T>(m);
+      if (Qp) P[off] = (q[r] + f * cp) * rz;
+    }
+    f *= gamma;
+  }
+}
+
+// Backward (as scan_bwd_kernel without carried state): dS from the nq
+// partial slices of dM, and one decay-gradient partial per workgroup at
+// dgamma[(b * ncs + x) * nseg + segment].  Segments are taken from the last.
+template <typename T>
+__global__ __launch_bounds__(kScCols * kLbWaves) void scan_bwd_lb_kernel(
+    const float* __restrict__ dM, int nq, int64_t qstride, const float* __restrict__ M,
+    float* __restrict__ dS, float* __restrict__ dgamma, int B, int nb, int D, float gamma,
+    uint64_t* __restrict__ flags, int nseg) {
+  __shared__ float wq[kLbWaves][kScCols], we[kLbWaves][kScCols], en[2][kScCols];
+  __shared__ float red[kLbWaves];
+  const int c = threadIdx.x % kScCols, w = threadIdx.x / kScCols;
+  const int ncs = (D + kScCols - 1) / kScCols;
+  const int id = blockIdx.x;
+  const int k = nseg - 1 - id / (B * ncs), b = (id / ncs) % B, x = id % ncs;
+  const int col = x * kScCols + c;
+  const bool on = col < D;
+  const float lg2 = gamma > 0.f ? log2f(gamma) : 0.f;
+  const float gw = pow2k<kLbRows>(gamma), gs = pow2k<kLbSeg>(gamma);
+  const int a = k * kLbSeg + w * kLbRows;
+  const int64_t off0 = (int64_t)b * nb * D + (int64_t)a * D + col;
+  float xr[kLbRows], yr[kLbRows], mm[kLbRows], zs[kLbRows];
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) xr[r] = 0.f;
+  for (int z = 0; z < nq; ++z) {
+#pragma unroll
+    for (int r = 0; r < kLbRows; ++r)
+      xr[r] += on && a + r < nb ? dM[z * qstride + off0 + (int64_t)r * D] : 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) mm[r] = on && a + r < nb ? M[off0 + (int64_t)r * D] : 0.f;
+  const float mprev = on && a >= 1 && a < nb ? M[off0 - D] : 0.f;
+  float zz = zsum(a, gamma, lg2, 0.f);
+  const float zprev = a >= 1 ? zsum(a - 1, gamma, lg2, 0.f) : 0.f;
+#pragma unroll
+  for (int r = 0; r < kLbRows; ++r) {
+    zs[r] = zz;
+    const float rz = 1.f / zz;
+    zz = gamma * zz + 1.f;
+    const float dm = xr[r];
+    xr[r] = dm * rz;
+    yr[r] = -dm * mm[r] * rz;
+  }
+  float qq = 0.f, e = 0.f;
+#pragma unroll
+  for (int r = kLbRows - 1; r >= 0; --r) {
+    qq = xr[r] + gamma * qq;
+    e = yr[r] + gamma * e;
+    xr[r] = qq;
+    yr[r] = e;
+  }
+  wq[w][c] = qq;
+  we[w][c] = e;
+  __syncthreads();
+  // wave 0: the aggregate of Qs, wave 1: of E (the state at the segment's
+  // first block); publish it, then fold the later segments' (from the last)
+  // into the state entering this segment's last block
+  uint64_t* rec0 = flags + ((int64_t)b * ncs + x) * nseg * kLbRec;
+  if (w < 2) {
+    float agg = 0.f;
+    for (int j = kLbWaves - 1; j >= 0; --j) agg = (w == 0 ? wq[j][c] : we[j][c]) + gw * agg;
+    if (k > 0) lb_publish(rec0 + (int64_t)k * kLbRec + w * kScCols + c, agg);
+    en[w][c] = k + 1 < nseg ? lb_fold(rec0 + w * kScCols + c, nseg - 1, -1, nseg - 1 - k, gs)
+                            : 0.f;
+  }
+  __syncthreads();
+  float iq = en[0][c], ie = en[1][c];
+  for (int j = kLbWaves - 1; j > w; --j) {
+    iq = wq[j][c] + gw * iq;
+    ie = we[j][c] + gw * ie;
+  }
+  float f = gamma, dg = 0.f;
+#pragma unroll
+  for (int r = kLbRows - 1; r >= 0; --r) {
+    const int i = a + r;
+    const float qs = xr[r] + f * iq, es = yr[r] + f * ie;
+    f *= gamma;
+    if (on && i < nb) {
+      dS[off0 + (int64_t)r * D] = qs;
+      if (i >= 1) {
+        const float zp = r > 0 ? zs[r > 0 ? r - 1 : 0] : zprev;
+        const float mp = r > 0 ? mm[r > 0 ? r - 1 : 0] : mprev;
+        dg += qs * (mp * zp) + es * zp;
+      }
+    }
+  }
+  const float vsum = wave_sum(dg);
+  if (c == 0) red[w] = vsum;
+  __syncthreads();
+  if (threadIdx.x == 0 && dgamma) {
+    float t = 0.f;
+    for (int j = 0; j < kLbWaves; ++j) t += red[j];
+    dgamma[((int64_t)b * ncs + x) * nseg + k] = t;
+  }
+}
+
 // ------------------------------------------------------------------ gate backward
 // dU = dY * Mc * G (1 - G) per element, and the block sum of dY * G, which is
 // the gradient of the shifted memory, in the column-chunk layout.  The block
@@ -817,11 +1066,9 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const T* __restrict__ dY,
   typedef typename GateT<T>::type GT;  // fp16 with bf16 activations
   typedef GT gvec __attribute__((ext_vector_type(VE)));
   __shared__ float racc[kTg][kVec * VE];
-  if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
-    for (int k = threadIdx.x; k < na; k += blockDim.x)
-      if (zero_a) zero_a[k] = 0.f;
-    if (threadIdx.x == 0 && zero_b) *zero_b = 0.f;
-  }
+  clear_share(zero_a, na);
+  if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0 && zero_b)
+    *zero_b = 0.f;
   const int v = threadIdx.x % kVec, tg = threadIdx.x / kVec;
   const int i = blockIdx.x, b = blockIdx.y;
   const int c0 = blockIdx.z * kVec * VE;
@@ -1243,7 +1490,8 @@ int nvj_for(int Dv) {
 
 template <typename E>
 hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, float* S, void* St,
-                      float* stats, int B, int T, int D, int L, hipStream_t s) {
+                      float* stats, int B, int T, int D, int L, float* zero, int64_t nzero,
+                      hipStream_t s) {
   const int nb = (T + L - 1) / L;
   if ((int64_t)B * nb >= kPoolRowMinGroups) {
     // whole rows: VR vectors per row, TG token groups, VR * TG threads a
@@ -1253,12 +1501,12 @@ hipError_t pool_fwd_t(const void* H, const float* sp, int np, float* s_out, floa
     while ((VR * TG) % 64) ++TG;
     const size_t lds = ((size_t)TG * D + kRowTile) * sizeof(float);
     hipLaunchKernelGGL(pool_row_kernel<E>, dim3(nb, B), dim3(VR * TG), lds, s, (const E*)H, sp, np,
-                       s_out, S, (E*)St, stats, T, D, L, nb, TG);
+                       s_out, S, (E*)St, stats, T, D, L, nb, TG, zero, nzero);
     return hipGetLastError();
   }
   const int cw = kVec * Vec16<E>::N;
   hipLaunchKernelGGL(pool_fwd_kernel<E>, dim3(nb, B, (D + cw - 1) / cw), dim3(kVec * kTg), 0, s,
-                     (const E*)H, sp, np, s_out, S, (E*)St, stats, T, D, L, nb);
+                     (const E*)H, sp, np, s_out, S, (E*)St, stats, T, D, L, nb, zero, nzero);
   return hipGetLastError();
 }
 
@@ -1332,9 +1580,11 @@ hipError_t gate_bwd_t(const void* dY, const void* G, const float* P, void* dU, v
 }  // namespace
 
 hipError_t pool_fwd(DType dt, const void* H, const float* sp, int np, float* s_out, float* S,
-                    void* St, float* stats, int B, int T, int D, int L, hipStream_t s) {
-  if (dt == DType::BF16) return pool_fwd_t<bf16>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
-  return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, s);
+                    void* St, float* stats, int B, int T, int D, int L, float* zero,
+                    int64_t nzero, hipStream_t s) {
+  if (dt == DType::BF16)
+    return pool_fwd_t<bf16>(H, sp, np, s_out, S, St, stats, B, T, D, L, zero, nzero, s);
+  return pool_fwd_t<float>(H, sp, np, s_out, S, St, stats, B, T, D, L, zero, nzero, s);
 }
 
 bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !per_channel; }
@@ -1343,17 +1593,62 @@ bool mem_fused(int nb, bool per_channel) { return nb <= kMemFusedMaxBlocks && !p
 // slice per split, a single slice when there is one split) for the scans,
 // which add them in a fixed order: the forward's Q = St W_m, and the
 // backward's dM = [Pbar | Pbar_lo] [Wm^T; Wm^T] (one product over 2D).
-size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
-  if (mem_fused(nb, per_channel)) return 0;
+// Bytes of the W_m products' split-K slices.
+size_t mem_slice_bytes(int B, int nb, int D) {
   const int sp = std::max(gemm_splitk_splits(B * nb, D, D, kMemMinK),
                           gemm_splitk_splits(B * nb, D, 2 * D, kMemMinK));
-  return (size_t)sp * B * nb * D * sizeof(float);
+  return ((size_t)sp * B * nb * D * sizeof(float) + 255) / 256 * 256;
 }
 
-// One scan launch over grid (columns / 64, B).
+bool has_carry(const Carry& c) {
+  return c.Nin || c.Zin || c.Pc || c.Nout || c.Zout || c.dNout || c.dZout || c.e0;
+}
+
+// Segments of the look-back scans, or 0 where the scans above serve.
+int lb_nseg(int B, int nb, int D, bool per_channel, bool carry) {
+  if (per_channel || carry || mem_fused(nb, per_channel)) return 0;
+  const int ncs = (D + kScCols - 1) / kScCols;
+  if ((int64_t)B * ncs >= kLbMaxPairs) return 0;
+  const int ns = (nb + kLbSeg - 1) / kLbSeg;
+  return ns >= kLbMinSeg && ns <= kLbMaxSeg ? ns : 0;
+}
+
+// Words of the look-back records.
+int64_t lb_words(int B, int D, int nseg) {
+  return (int64_t)B * ((D + kScCols - 1) / kScCols) * nseg * kLbRec;
+}
+
+float* mem_lb_flags(float* part, int B, int nb, int D, bool per_channel, bool carry,
+                    int64_t* nfloat) {
+  const int ns = lb_nseg(B, nb, D, per_channel, carry);
+  *nfloat = ns ? 2 * lb_words(B, D, ns) : 0;
+  return ns ? reinterpret_cast<float*>(reinterpret_cast<char*>(part) + mem_slice_bytes(B, nb, D))
+            : nullptr;
+}
+
+size_t mem_part_bytes(int B, int nb, int D, bool per_channel) {
+  if (mem_fused(nb, per_channel)) return 0;
+  const int ns = lb_nseg(B, nb, D, per_channel, false);
+  return mem_slice_bytes(B, nb, D) + (ns ? (size_t)lb_words(B, D, ns) * 8 : 0);
+}
+
+// One scan launch over grid (columns / 64, B), or the look-back scan over
+// every (segment, sequence, column slice) for few sequences, whose records
+// (after the split-K slices in `part`, mem_lb_flags) an earlier kernel on
+// the stream has cleared.
 template <typename T>
 hipError_t scan_fwd_run(const float* S, float* M, T* Mt, int B, int nb, int D, float gamma,
-                        const Carry& c, const float* Qp, int nq, float* P, hipStream_t s) {
+                        const Carry& c, const float* Qp, int nq, float* P, float* part,
+                        hipStream_t s) {
+  const int ns = lb_nseg(B, nb, D, c.gvec != nullptr, has_carry(c));
+  if (ns) {
+    uint64_t* fl = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(part) +
+                                                mem_slice_bytes(B, nb, D));
+    const int nwg = B * ((D + kScCols - 1) / kScCols) * ns;
+    hipLaunchKernelGGL(scan_fwd_lb_kernel<T>, dim3(nwg), dim3(kScCols * kLbWaves), 0, s, S, M,
+                       Mt, B, nb, D, gamma, Qp, nq, (int64_t)B * nb * D, P, fl, ns);
+    return hipGetLastError();
+  }
   const dim3 grid((D + kScCols - 1) / kScCols, B);
   hipLaunchKernelGGL(scan_fwd_kernel<T>, grid, dim3(kScCols * kScWaves), 0, s, S, M, Mt, nb, D,
                      gamma, c, Qp, nq, (int64_t)B * nb * D, P);
@@ -1362,7 +1657,16 @@ hipError_t scan_fwd_run(const float* S, float* M, T* Mt, int B, int nb, int D, f
 
 template <typename T>
 hipError_t scan_bwd_run(const float* dM, int nq, const float* M, float* dS, float* dgamma, int B,
-                        int nb, int D, float gamma, const Carry& c, hipStream_t s) {
+                        int nb, int D, float gamma, const Carry& c, float* part, hipStream_t s) {
+  const int ns = lb_nseg(B, nb, D, c.gvec != nullptr, has_carry(c));
+  if (ns) {
+    uint64_t* fl = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(part) +
+                                                mem_slice_bytes(B, nb, D));
+    const int nwg = B * ((D + kScCols - 1) / kScCols) * ns;
+    hipLaunchKernelGGL(scan_bwd_lb_kernel<T>, dim3(nwg), dim3(kScCols * kLbWaves), 0, s, dM, nq,
+                       (int64_t)B * nb * D, M, dS, dgamma, B, nb, D, gamma, fl, ns);
+    return hipGetLastError();
+  }
   const dim3 grid((D + kScCols - 1) / kScCols, B);
   hipLaunchKernelGGL(scan_bwd_kernel<T>, grid, dim3(kScCols * kSbWaves), 0, s, dM, nq,
                      (int64_t)B * nb * D, M, dS, dgamma, nb, D, gamma, c);
@@ -1390,8 +1694,10 @@ hipError_t mem_fwd_scan(DType dt, const float* S, float* M, void* Mt, float* P, 
   const float* Qp = c.gvec ? nullptr : part;
   float* Pout = c.gvec ? nullptr : P;
   if (dt == DType::BF16)
-    return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, s);
-  return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout, s);
+    return scan_fwd_run<bf16>(S, M, (bf16*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout,
+                              part, s);
+  return scan_fwd_run<float>(S, M, (float*)Mt, B, nb, D, gamma, c, Qp, c.gvec ? 0 : nq, Pout,
+                             part, s);
 }
 
 hipError_t mem_fwd(DType dt, const void* St, const void* Wm, const float* S, float* M, void* Mt,
@@ -1453,8 +1759,9 @@ hipError_t mem_bwd_proj(DType dt, const void* Pbar, const void* Pbar_lo, const v
 
 hipError_t mem_bwd_scan(DType dt, const float* M, float* dS, float* dgpart, float* part, int nq,
                         int B, int nb, int D, float gamma, const Carry& c, hipStream_t s) {
-  if (dt == DType::BF16) return scan_bwd_run<bf16>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, s);
-  return scan_bwd_run<float>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, s);
+  if (dt == DType::BF16)
+    return scan_bwd_run<bf16>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, part, s);
+  return scan_bwd_run<float>(part, nq, M, dS, dgpart, B, nb, D, gamma, c, part, s);
 }
 
 hipError_t mem_bwd(DType dt, const void* Pbar, const void* Pbar_lo, const void* Wm,
@@ -1563,10 +1870,19 @@ hipError_t zero_two(float* a, int64_t na, float* b, int64_t nb, hipStream_t s) {
   return hipGetLastError();
 }
 
-int dg_part_rows(int B, int nb, int D, bool per_channel) {
+// Decay-gradient partial rows the memory backward writes in a call (with or
+// without carried state), and the most any call writes.
+int dg_part_rows_used(int B, int nb, int D, bool per_channel, bool carry) {
   if (mem_fused(nb, per_channel))
     return per_channel ? B : ((D + kMsCols - 1) / kMsCols) * B;
+  const int ns = lb_nseg(B, nb, D, per_channel, carry);
+  if (ns) return B * ((D + kScCols - 1) / kScCols) * ns;
   return per_channel ? B : ((D + kScCols - 1) / kScCols) * B;
+}
+
+int dg_part_rows(int B, int nb, int D, bool per_channel) {
+  return std::max(dg_part_rows_used(B, nb, D, per_channel, false),
+                  dg_part_rows_used(B, nb, D, per_channel, true));
 }
 
 hipError_t dgamma_reduce(const float* part, int rows, int Dp, float* out, bool accumulate,

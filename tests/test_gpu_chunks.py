@@ -191,20 +191,29 @@ def test_state_buffers_in_place(torch_cuda):
     assert abs(a["dgamma"] - b["dgamma"]) <= 1e-5 * abs(a["dgamma"])
 
 
-@pytest.mark.parametrize("dtype,T,D,H,L", [("bf16", 512, 256, 4, 64), ("f32", 2048, 128, 2, 32)])
-def test_empty_history_is_the_plain_layer(torch_cuda, dtype, T, D, H, L):
+@pytest.mark.parametrize("dtype,T,D,H,L,exact", [("bf16", 512, 256, 4, 64, True),
+                                                 ("f32", 2048, 128, 2, 32, False)])
+def test_empty_history_is_the_plain_layer(torch_cuda, dtype, T, D, H, L, exact):
     """A chunk with no incoming state computes what the plain entry points
-    compute: identical outputs and gradients (dgamma to its atomics'
-    rounding)."""
+    compute.  With 8 blocks both take the single memory kernel: identical
+    outputs and gradients (dgamma to its partials' rounding).  With 64
+    blocks of two sequences the plain call scans through segments of 16
+    blocks (the look-back scans for few sequences), the chunk through the
+    scans that carry a state, which add the same terms in another order:
+    equal to float32 rounding."""
     torch = torch_cuda
-    from test_gpu_parity import run_gpu
+    from test_gpu_parity import run_gpu, compare
     B = 2
     X, W, dY = inputs(B, T, D, dtype, w_std=0.05)
     plain = run_gpu(torch, B, T, D, H, L, dtype, X, W, dY)
     ch = gpu_chunks(torch, B, [0, T], D, H, L, dtype, X, W, dY)
-    for k in ("Y", "dX") + GRADS:
-        assert np.array_equal(plain[k], ch[k]), k
-    assert abs(plain["dgamma"] - ch["dgamma"]) <= 1e-5 * abs(plain["dgamma"])
+    if exact:
+        for k in ("Y", "dX") + GRADS:
+            assert np.array_equal(plain[k], ch[k]), k
+        assert abs(plain["dgamma"] - ch["dgamma"]) <= 1e-5 * abs(plain["dgamma"])
+    else:
+        keys = ("Y", "dX", "dgamma") + GRADS
+        compare({k: ch[k] for k in keys}, {k: plain[k] for k in keys}, dtype, "empty-history")
 
 
 @pytest.mark.parametrize("dtype,T,D,H,L,res", [("bf16", 200, 256, 4, 256, False),
