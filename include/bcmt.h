@@ -196,7 +196,7 @@ int bcmt_layer_backward(const bcmt_config* cfg, const void* X, const bcmt_params
  * Returns BCMT_ERR_WORKSPACE when the pass needs more scratch than the array
  * holds (bcmt_workspace_bytes(cfg, BCMT_PASS_FORWARD) above
  * BCMT_NOALLOC_SCRATCH_BYTES; the forward of B = 2, T = 65536, D = 1024 at
- * L = 256 needs 17 MiB), and BCMT_ERR_HIP if the array's address cannot be
+ * L = 256 needs 26 MiB), and BCMT_ERR_HIP if the array's address cannot be
  * obtained; other errors as for bcmt_layer_forward.  The call allocates
  * nothing and creates nothing.  Every call on one GPU uses that GPU's one
  * array: calls whose work overlaps on the GPU (several streams, or several
