@@ -66,9 +66,14 @@ def stage_work(name, B, T, D, H, L, es):
     if name.endswith("_reduce"):
         return "hbm", 0, "byte"  # split-K reductions: size depends on the split plan
     act = BT * D * es
-    # dw_p partial rows: one per 8 * (16 / nvj) tokens of each block
+    # dw_p partial rows: one per pooling-backward workgroup of 8 row
+    # segments of R rows (R a multiple of the rows in flight, for about 1024
+    # workgroups, 8 to 64 rows, at most a block)
     nvj = next(n for n in (1, 2, 4, 8) if n * 64 >= D // (16 // es) or n == 8)
-    pool_rows = B * nb * -(-min(L, T) // (8 * (16 // nvj)))
+    tb = 1 if nvj >= 4 else 4 // nvj
+    lb = min(L, T)
+    rseg = min(max(-(-(BT // 8192) // tb) * tb, 8), 64, -(-lb // tb) * tb)
+    pool_rows = -(-(B * nb * -(-lb // rseg)) // 8)
     fused = nb <= 32  # the single-kernel memory path (projection + scan)
     hbm = {
         "fwd.pool": act + BT * 4 + B * nb * D * 4 + B * nb * 8,
