@@ -106,13 +106,16 @@ CASES = [
     ("bf16-ragged-T1000", 1, 1000, 256, 4, 128, "bf16", 1.0, 2 / np.sqrt(256), 0.8, False),
     ("bf16-L1024-dense", 1, 1024, 256, 4, 1024, "bf16", 1.0, 0.02, 0.8, False),
     ("bf16-L256", 2, 1024, 256, 4, 256, "bf16", 1.0, 0.02, 0.8, True),
-    # 1024 blocks: the w_p gradient's partial rows take two reduction passes,
-    # and the memory scans run in chunks over two passes of 256 blocks
+    # 512 blocks per sequence: the W_m products and the look-back scans
+    # across workgroups (32 segments of 16 blocks per sequence)
     ("f32-many-blocks-L8", 2, 4096, 128, 2, 8, "f32", 1.0, 0.05, 0.8, False),
-    # 160 blocks per sequence (the chunked scans and the W_m products), ragged,
-    # at the paper's decay and at 0.9 (there the decay gradient is a small
-    # sum of large terms of both signs: its bound comes from the rounding
-    # model).
+    # the look-back scans with a ragged last segment (126 blocks: 7 segments
+    # of 16 and one of 14) and a ragged last block (3 tokens)
+    ("f32-look-back-ragged", 1, 1003, 128, 2, 8, "f32", 1.0, 0.05, 0.8, False),
+    # 160 blocks per sequence (the look-back scans and the W_m products),
+    # ragged, at the paper's decay and at 0.9 (there the decay gradient is a
+    # small sum of large terms of both signs: its bound comes from the
+    # rounding model).
     ("bf16-many-blocks-L16", 2, 2550, 256, 4, 16, "bf16", 1.0, 0.02, 0.8, False),
     ("bf16-many-blocks-L16-g0.9", 2, 2550, 256, 4, 16, "bf16", 1.0, 0.02, 0.9, False),
     # heads of 16 and 32 dimensions (the paper's model uses 16): ragged
@@ -184,14 +187,38 @@ def test_forward_is_deterministic_and_causal(torch_cuda):
         assert not torch.equal(Y1[:, t + 1:], Y3[:, t + 1:]), t
 
 
+def test_forward_is_deterministic_on_the_look_back_scans(torch_cuda):
+    """Two sequences of 160 blocks take the look-back scans, whose
+    workgroups wait for one another's published aggregates: the forward is
+    still bit-identical from run to run."""
+    torch = torch_cuda
+    from paper_2608_13578_amd.layer import LayerBuffers, to_device
+    B, T, D, H, L = 2, 2560, 256, 4, 16
+    say(f"case look-back forward determinism: B={B} T={T} D={D} L={L} bf16")
+    X, W, _ = inputs(B, T, D, "bf16")
+    lb = LayerBuffers(B, T, D, H, L, dtype="bf16")
+    lb.set_params(W)
+    Xd = to_device(X, "bf16")
+    Ys = []
+    for _ in range(3):
+        Y = lb.new_activation()
+        lb.forward(Xd, Y)
+        torch.cuda.synchronize()
+        Ys.append(Y)
+    for Y in Ys[1:]:
+        assert torch.equal(Ys[0], Y)
+
+
 @pytest.mark.parametrize("T,L,per_channel", [(1024, 128, False), (2560, 16, False),
                                               (2560, 16, True)],
                          ids=["fused-memory", "long-scan", "long-scan-per-channel"])
 def test_backward_is_deterministic(torch_cuda, T, L, per_channel):
     """Every gradient, the decay gradient included, is reduced in a fixed
     order (per-workgroup partials, no atomics): repeated backward passes
-    give the same bits, on the single-kernel memory path (8 blocks) and the
-    parallel scans (160 blocks), with one decay or one per channel."""
+    give the same bits, on the single-kernel memory path (8 blocks), the
+    look-back scans across workgroups (160 blocks of two sequences, one
+    decay: every segment folds the aggregates before it in a fixed order)
+    and the per-channel scans."""
     torch = torch_cuda
     from paper_2608_13578_amd.layer import LayerBuffers, to_device
     B, D, H = 2, 256, 4
