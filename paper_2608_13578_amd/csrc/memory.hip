@@ -824,14 +824,15 @@ __global__ __launch_bounds__(kScCols * kSbWaves) void scan_bwd_kernel(
 // workgroup on another XCD sees them; the launcher clears the words first.
 // Workgroups are numbered segment first (the reverse scan from the last
 // segment), so every segment a workgroup waits for belongs to a workgroup
-// launched before it, which publishes before it waits itself; a grid of a
-// few hundred small workgroups is resident at once in any case.  A wait
-// that exceeds kLbSpin polls gives up with NaN instead of hanging.  The
+// launched before it, which publishes before it waits itself; and the grid
+// is kept to kLbMaxGroups small workgroups (256 threads, about 50
+// registers, 2.5 KB of LDS), four per CU, which the chip holds at once.  A
+// wait that exceeds kLbSpin polls gives up with NaN instead of hanging.  The
 // records are cleared by the kernel before the scan on the same stream
 // (pooling for the forward, the gate backward for the backward).
 // Scalar decay and whole sequences only (no carried state).
 constexpr int kLbWaves = 4, kLbRows = 4, kLbSeg = kLbWaves * kLbRows;
-constexpr int kLbMaxPairs = 128, kLbMinSeg = 4, kLbMaxSeg = 64;
+constexpr int kLbMaxPairs = 128, kLbMinSeg = 4, kLbMaxSeg = 64, kLbMaxGroups = 1024;
 constexpr int kLbSpin = 1 << 18;
 
 // Words of one segment's record: [quantity 0 | quantity 1] x 64 columns.
@@ -1610,6 +1611,7 @@ int lb_nseg(int B, int nb, int D, bool per_channel, bool carry) {
   const int ncs = (D + kScCols - 1) / kScCols;
   if ((int64_t)B * ncs >= kLbMaxPairs) return 0;
   const int ns = (nb + kLbSeg - 1) / kLbSeg;
+  if ((int64_t)B * ncs * ns > kLbMaxGroups) return 0;
   return ns >= kLbMinSeg && ns <= kLbMaxSeg ? ns : 0;
 }
 
