@@ -130,6 +130,14 @@ CASES = [
     ("bf16-dh16-ragged-L20", 2, 150, 128, 8, 20, "bf16", 1.0, 0.02, 0.8, False),
     ("bf16-dh32-ragged-L48", 2, 200, 128, 4, 48, "bf16", 1.0, 0.02, 0.8, True),
     ("bf16-dh16-stress-L200", 1, 450, 64, 4, 200, "bf16", 1.0, 2 / np.sqrt(64), 0.8, False),
+    # degenerate blocks: every token a block of its own (attention returns
+    # V and pooling returns H, so the exact dW_q, dW_k and dw_p are zero and
+    # the metric takes the absolute error; the memory is a decayed average
+    # of earlier tokens), blocks of two tokens with a one-token last block,
+    # and sequences of one token
+    ("f32-L1", 1, 40, 128, 2, 1, "f32", 1.0, 0.05, 0.8, False),
+    ("bf16-L2-ragged", 2, 67, 128, 2, 2, "bf16", 1.0, 0.02, 0.8, False),
+    ("f32-T1", 2, 1, 128, 2, 64, "f32", 1.0, 0.05, 0.8, False),
 ]
 
 
