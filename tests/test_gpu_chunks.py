@@ -132,6 +132,9 @@ CHAINS = [
     # 50 blocks per chunk: the parallel scans and the W_m matrix products
     ("f32-long-scans", 2, [0, 800, 1600], 128, 2, 16, "f32", 0.05, 0.9, False),
     ("f32-fused-residual-gamma0", 1, [0, 96, 160, 320], 192, 3, 32, "f32", 0.05, 0.0, True),
+    # blocks of two tokens: a chunk of one block, then three, then three
+    # and a half
+    ("f32-L2-short-chunks", 1, [0, 2, 8, 15], 128, 2, 2, "f32", 0.05, 0.8, False),
 ]
 
 

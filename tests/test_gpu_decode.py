@@ -65,6 +65,10 @@ CASES = [
     # decoding after a prefill of whole blocks
     ("bf16-prefill", 2, 200, 256, 4, 32, "bf16", 0.02, 0.8, False, 96),
     ("f32-prefill", 2, 90, 128, 2, 16, "f32", 0.05, 0.8, True, 48),
+    # every token completes a block (one-token blocks), and two-token
+    # blocks after a prefill of five
+    ("f32-L1", 2, 20, 128, 2, 1, "f32", 0.05, 0.8, False, 0),
+    ("bf16-L2-prefill", 2, 30, 128, 2, 2, "bf16", 0.02, 0.8, False, 10),
 ]
 
 
