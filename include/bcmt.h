@@ -44,6 +44,12 @@
  *   BCMT_ERR_UNSUPPORTED and BCMT_ERR_WORKSPACE mean that nothing ran.
  *   BCMT_ERR_HIP reports a failed kernel launch; kernels enqueued before it
  *   may have run.
+ *   On long sequences with few sequence x column slices the decayed scans
+ *   of Sec. 3.5 pass partial sums between workgroups of one launch, all of
+ *   which are resident at once.  Each wait for an earlier workgroup is
+ *   bounded: one that runs out (only possible while other work holds the
+ *   GPU that long) writes NaN into the outputs that depend on it instead
+ *   of hanging, so a NaN there is the error report.
  */
 #ifndef BCMT_H_
 #define BCMT_H_
